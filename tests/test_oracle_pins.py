@@ -1,0 +1,377 @@
+"""Pins for the CPU oracle: checks against values fixed by the paper's
+definitions and by mathematics, not against the oracle itself.
+
+  * hand-derived worked examples (tests/golden/*.json, each citing its equation)
+  * library routines for the number formats (torch's E4M3FN and bf16 casts)
+  * closed forms (one head, one dimension: the top-k are the largest scalar keys)
+  * identities stated by the paper or implied by Algorithm 1 (g = 1 is dense;
+    c >= L with the guardrail is dense; Reuse shares one set per group;
+    causality; identical members; Refine with a full candidate set)
+  * invariances (positive scaling of gates / query scales, head permutation)
+  * exact integer arithmetic for fp8 inner products
+  * brute force on tiny inputs (Python sorting)
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from workload.gen import encode_bf16, make_prefill
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def gold(name):
+    with open(os.path.join(GOLD, name)) as f:
+        return json.load(f)
+
+
+def bf16_bits(x):
+    return encode_bf16(np.asarray(x, dtype=np.float32))
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _built(oracle_lib):
+    return oracle_lib
+
+
+# ------------------------------------------------------------------ codecs
+def test_e4m3_decode_matches_torch_for_all_codes():
+    codes = torch.arange(256, dtype=torch.int32).to(torch.uint8)
+    ref = codes.view(torch.float8_e4m3fn).to(torch.float64).numpy()
+    ours = np.array([oracle.e4m3_decode(c) for c in range(256)])
+    nan = np.isnan(ref)
+    assert list(np.nonzero(nan)[0]) == [0x7F, 0xFF]
+    assert np.array_equal(np.isnan(ours), nan)
+    assert np.array_equal(ours[~nan], ref[~nan])
+    assert ours[0x7E] == 448.0 and ours[0x01] == 2.0 ** -9
+
+
+def test_e4m3_encode_matches_torch_rne():
+    vals = np.array([oracle.e4m3_decode(c) for c in range(0x7F)])       # non-negative finite
+    mids = (vals[:-1] + vals[1:]) / 2                                     # exact ties
+    rng = np.random.default_rng(7)
+    rand = rng.uniform(-448, 448, 20000)
+    small = rng.uniform(-0.05, 0.05, 20000)
+    xs = np.concatenate([vals, -vals, mids, -mids, rand, small]).astype(np.float32)
+    ref = torch.from_numpy(xs).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    ours = np.array([oracle.e4m3_encode(float(x)) for x in xs], dtype=np.uint8)
+    # +-0: torch keeps the sign of zero, as the oracle does
+    assert np.array_equal(ours, ref)
+
+
+def test_e4m3_encode_saturates():
+    assert oracle.e4m3_encode(449.0) == 0x7E
+    assert oracle.e4m3_encode(1e30) == 0x7E
+    assert oracle.e4m3_encode(-500.0) == 0xFE
+
+
+def test_bf16_codec_matches_torch():
+    rng = np.random.default_rng(3)
+    xs = np.concatenate([rng.standard_normal(20000) * 10.0 ** rng.integers(-8, 8, 20000),
+                         [0.0, -0.0, 1.0, 1.00390625, 1.01171875]]).astype(np.float32)
+    ref = bf16_bits(xs)
+    ours = np.array([oracle.bf16_encode(float(x)) for x in xs], dtype=np.uint16)
+    assert np.array_equal(ours, ref)
+    back = np.array([oracle.bf16_decode(int(b)) for b in ref])
+    assert np.array_equal(back, torch.from_numpy(ref.view(np.int16)).view(torch.bfloat16).double().numpy())
+
+
+# ------------------------------------------------------------------ golden
+def test_golden_scores_bf16():
+    G = gold("scores_bf16_h2_d3.json")
+    k = bf16_bits(G["keys"])
+    for case in G["queries"]:
+        q = bf16_bits(case["q"])
+        w = np.array(case["w"], dtype=np.float32)
+        t = case["t"]
+        f = oracle.scores("bf16", q, 1.0, w, k, None, t)
+        assert list(f) == case["scores"], case["derivation"]
+        for m, expect in case["topk"].items():
+            qq = q[None]
+            ww = w[None]
+            out = oracle.index("bf16", qq, None, ww, t, k, None, len(G["keys"]),
+                               mode=oracle.DENSE, topk=int(m))["idx"][0]
+            assert list(out) == expect, (t, m)
+
+
+def test_golden_scores_fp8_scaled():
+    G = gold("scores_fp8_scaled.json")
+    kc = np.array(G["key_codes"], dtype=np.uint8)
+    for code, v in zip(kc.ravel(), np.array(G["key_values"]).ravel()):
+        assert oracle.e4m3_decode(int(code)) == v
+    ks = np.array(G["key_scale"], dtype=np.float32)
+    for case in G["queries"]:
+        qc = np.array(case["q_codes"], dtype=np.uint8)
+        w = np.array(case["w"], dtype=np.float32)
+        f = oracle.scores("fp8", qc, case["q_scale"], w, kc, ks, case["t"])
+        assert list(f) == case["scores"], case["derivation"]
+        for m, expect in case["topk"].items():
+            out = oracle.index("fp8", qc[None], np.array([case["q_scale"]], np.float32), w[None],
+                               case["t"], kc, ks, len(kc), mode=oracle.DENSE, topk=int(m))["idx"][0]
+            assert list(out) == expect
+
+
+def test_golden_proxy_fp8():
+    G = gold("proxy_fp8_h1_d4.json")
+    q = np.array([m["q_codes"] for m in G["members"]], dtype=np.uint8)
+    for code, v in zip(q.ravel(), np.array([m["q_values"] for m in G["members"]]).ravel()):
+        assert oracle.e4m3_decode(int(code)) == v
+    qs = np.array([m["q_scale"] for m in G["members"]], dtype=np.float32)
+    w = np.array([m["w"] for m in G["members"]], dtype=np.float32)
+    pq, psc, pw = oracle.proxy("fp8", q, qs, w)
+    assert pq.tolist() == G["proxy_codes"], G["derivation"]
+    assert psc == G["proxy_scale"]
+    assert pw.tolist() == G["proxy_w"]
+
+
+def test_golden_proxy_bf16():
+    G = gold("proxy_bf16_h1_d2.json")
+    q = bf16_bits([m["q_values"] for m in G["members"]])
+    w = np.array([m["w"] for m in G["members"]], dtype=np.float32)
+    pq, psc, pw = oracle.proxy("bf16", q, None, w)
+    assert pq.tolist() == bf16_bits(G["proxy_values"]).tolist(), G["derivation"]
+    assert psc == 1.0 and pw.tolist() == G["proxy_w"]
+
+
+def test_golden_group_reuse_refine():
+    G = gold("group_reuse_refine_h1_d2.json")
+    k = bf16_bits(G["keys"])
+    q = bf16_bits([m["q"] for m in G["queries"]])
+    w = np.array([m["w"] for m in G["queries"]], dtype=np.float32)
+    p0, g, c, m = G["p0"], G["g"], G["c"], G["k"]
+    n_k = len(G["keys"])
+    r = oracle.index("bf16", q, None, w, p0, k, None, n_k, mode=oracle.REUSE, g=g, c=c, topk=m,
+                     want_proxy=True)
+    assert [sorted(x) for x in r["idx"].tolist()] == [sorted(x) for x in G["reuse"]]
+    f = oracle.scores("bf16", r["pq"][0], 1.0, r["pw"][0], k, None, p0)
+    assert list(f) == G["proxy_scores"], G["derivation"]
+    r = oracle.index("bf16", q, None, w, p0, k, None, n_k, mode=oracle.REFINE, g=g, c=c, topk=m,
+                     want_cand=True)
+    assert sorted(r["cand"][0].tolist()) == sorted(G["refine_cand"])
+    assert [sorted(x) for x in r["idx"].tolist()] == [sorted(x) for x in G["refine"]]
+    r = oracle.index("bf16", q, None, w, p0, k, None, n_k, mode=oracle.DENSE, topk=m)
+    assert [sorted(x) for x in r["idx"].tolist()] == [sorted(x) for x in G["dense"]]
+
+
+# ------------------------------------------------------------------ closed form / brute force
+@pytest.mark.parametrize("fmt", ["bf16", "fp8"])
+def test_closed_form_one_head_one_dim(fmt):
+    """H = d = 1, w > 0, q > 0: I(s) = w q ks k_s for k_s > 0 and 0 otherwise, so the
+    top-k over [0, t] is the k largest scalar keys (ties: lower position)."""
+    rng = np.random.default_rng(11)
+    L, m = 200, 17
+    kv = rng.choice([-2.0, -1.0, -0.5, 0.0, 0.25, 0.5, 1.0, 1.5, 2.0, 3.0], size=L)
+    if fmt == "fp8":
+        kc = np.array([oracle.e4m3_encode(x) for x in kv], np.uint8)[:, None]
+        ks = rng.choice([0.5, 1.0, 2.0], size=L).astype(np.float32)
+        qc = np.array([[[oracle.e4m3_encode(1.5)]]], np.uint8)
+        qs = np.array([0.25], np.float32)
+        key_val = np.array([oracle.e4m3_decode(int(c)) for c in kc[:, 0]]) * ks
+    else:
+        kc = bf16_bits(kv[:, None])
+        ks, qs = None, None
+        qc = bf16_bits([[[1.5]]])
+        key_val = kv
+    w = np.array([[0.75]], np.float32)
+    for t in [0, 5, 16, 17, 120, L - 1]:
+        out = oracle.index(fmt, qc, qs, w, t, kc, ks, L, mode=oracle.DENSE, topk=m)["idx"][0]
+        vals = [max(0.0, key_val[s]) for s in range(t + 1)]
+        order = sorted(range(t + 1), key=lambda s: (-vals[s], s))[:m]
+        expect = order + [-1] * (m - len(order))
+        assert out.tolist() == expect, t
+
+
+def test_topk_bruteforce_with_ties():
+    rng = np.random.default_rng(5)
+    for trial in range(200):
+        n = int(rng.integers(0, 60))
+        f = rng.integers(-3, 4, size=n).astype(np.float64)
+        f[rng.random(n) < 0.1] = -0.0
+        pos = rng.permutation(1000)[:n].astype(np.int32)
+        m = int(rng.integers(1, 70))
+        out = oracle.topk(f, pos, m)
+        order = sorted(range(n), key=lambda i: (-f[i], pos[i]))[:m]
+        expect = [int(pos[i]) for i in order] + [-1] * max(0, m - n)
+        assert out.tolist() == expect
+
+
+def test_fp8_inner_products_are_exact():
+    """Values of E4M3FN codes times 2^9 are integers, so with one head, unit gate
+    and unit scales the score equals the integer dot product / 2^18 exactly."""
+    rng = np.random.default_rng(2)
+    d, L = 128, 64
+    finite = [c for c in range(256) if c not in (0x7F, 0xFF)]
+    ints = {c: int(round(oracle.e4m3_decode(c) * 512)) for c in finite}
+    assert all(abs(oracle.e4m3_decode(c) * 512 - ints[c]) == 0 for c in finite)
+    kc = rng.choice(finite, size=(L, d)).astype(np.uint8)
+    qc = rng.choice(finite, size=(1, d)).astype(np.uint8)
+    f = oracle.scores("fp8", qc, 1.0, np.ones(1, np.float32), kc, np.ones(L, np.float32), L - 1)
+    for s in range(L):
+        dot = sum(ints[int(a)] * ints[int(b)] for a, b in zip(qc[0], kc[s]))
+        assert f[s] == max(0, dot) / 2.0 ** 18
+
+
+# ------------------------------------------------------------------ identities of Algorithm 1
+def small(fmt, L=96, seed=21, H=4, d=8, rho=0.95):
+    return make_prefill(L, fmt, seed=seed, rho=rho, H=H, d=d, threads=1)
+
+
+def run(x, mode, **kw):
+    L = x.q.shape[0]
+    p0 = kw.pop("p0", 0)
+    n_q = kw.pop("n_q", L - p0)
+    return oracle.index(x.dtype, x.q[p0:p0 + n_q], None if x.q_scale is None else x.q_scale[p0:p0 + n_q],
+                        x.w[p0:p0 + n_q], p0, x.k, x.k_scale, L, mode=mode, **kw)
+
+
+def as_sets(idx):
+    return [frozenset(int(v) for v in row) for row in idx]
+
+
+@pytest.mark.parametrize("fmt", ["bf16", "fp8"])
+def test_group_of_one_is_dense(fmt):
+    """App. A: a group size of one recovers the per-query indexer exactly."""
+    x = small(fmt)
+    dense = run(x, oracle.DENSE, topk=10)["idx"]
+    for mode in (oracle.REUSE, oracle.REFINE):
+        for db in (0, 16):
+            r = run(x, mode, g=1, c=20, topk=10, dense_below=db)["idx"]
+            assert np.array_equal(np.sort(r, 1), np.sort(dense, 1)), (mode, db)
+
+
+@pytest.mark.parametrize("fmt", ["bf16", "fp8"])
+def test_budget_covering_the_sequence_is_dense(fmt):
+    """c >= L: every group starts before c, so Algorithm 1's guardrail sends
+    all of them to the dense path."""
+    x = small(fmt, L=64)
+    dense = run(x, oracle.DENSE, topk=8)["idx"]
+    for mode in (oracle.REUSE, oracle.REFINE):
+        r = run(x, mode, g=4, c=64, topk=8)["idx"]
+        assert np.array_equal(r, dense)
+
+
+@pytest.mark.parametrize("fmt", ["bf16", "fp8"])
+@pytest.mark.parametrize("g", [2, 3, 4])
+def test_reuse_shares_one_set_and_is_causal(fmt, g):
+    x = small(fmt, L=90)
+    c, m = 24, 8
+    r = run(x, oracle.REUSE, g=g, c=c, topk=m)["idx"]
+    L = x.q.shape[0]
+    for start in range(0, L, g):
+        rows = r[start:min(start + g, L)]
+        if start >= c:                                  # proxy group
+            assert all(np.array_equal(rows[0], row) for row in rows)
+            assert rows.max() <= start                  # Eq. 5 cutoff at t0
+        for i, row in enumerate(rows):
+            valid = row[row >= 0]
+            assert valid.max() <= start + i and len(set(valid)) == len(valid)
+
+
+@pytest.mark.parametrize("fmt", ["bf16", "fp8"])
+@pytest.mark.parametrize("g", [2, 4])
+def test_refine_with_full_candidates_is_truncated_dense(fmt, g):
+    """Guardrail off and c > t0: C is the whole prefix [0, t0], so each member's
+    set is the top-k of its own scores over [0, t0] (brute-force sort)."""
+    x = small(fmt, L=40)
+    m = 6
+    r = run(x, oracle.REFINE, g=g, c=64, topk=m, dense_below=0)["idx"]
+    for t in range(40):
+        t0 = (t // g) * g
+        f = oracle.scores(x.dtype, x.q[t], 1.0 if x.q_scale is None else x.q_scale[t], x.w[t],
+                          x.k, x.k_scale, t0)
+        order = sorted(range(t0 + 1), key=lambda s: (-f[s], s))[:m]
+        assert sorted(r[t][r[t] >= 0].tolist()) == sorted(order), t
+
+
+@pytest.mark.parametrize("fmt", ["bf16", "fp8"])
+def test_identical_members_proxy_is_the_member(fmt):
+    """Equal members (g a power of two): the mean equals the member, so Reuse,
+    Refine and the dense set truncated at t0 coincide."""
+    x = small(fmt, L=48)
+    g = 4
+    for a in (x.q, x.w) + ((x.q_scale,) if x.q_scale is not None else ()):
+        for t in range(48):
+            a[t] = a[(t // g) * g]
+    m = 6
+    reuse = run(x, oracle.REUSE, g=g, c=64, topk=m, dense_below=0, want_proxy=True)
+    refine = run(x, oracle.REFINE, g=g, c=64, topk=m, dense_below=0)["idx"]
+    for t in range(48):
+        t0 = (t // g) * g
+        if x.dtype == "bf16":
+            assert np.array_equal(reuse["pq"][t // g], x.q[t0])
+        f = oracle.scores(x.dtype, x.q[t0], 1.0 if x.q_scale is None else x.q_scale[t0], x.w[t0],
+                          x.k, x.k_scale, t0)
+        order = sorted(range(t0 + 1), key=lambda s: (-f[s], s))[:m]
+        order += [-1] * (m - len(order))
+        assert sorted(reuse["idx"][t].tolist()) == sorted(order)
+        assert sorted(refine[t].tolist()) == sorted(order)
+
+
+def test_fp8_proxy_requantisation_matches_torch_cast():
+    """The fp8 proxy: fp32 mean of the dequantised members, scale amax/448,
+    codes by RNE; the codes must equal torch's cast of the same fp32 values."""
+    x = small("fp8", L=16, H=4, d=8)
+    for g in (2, 3, 4):
+        q, qs, w = x.q[:g], x.q_scale[:g], x.w[:g]
+        pq, psc, pw = oracle.proxy("fp8", q, qs, w)
+        deq = torch.from_numpy(q).view(torch.float8_e4m3fn).float() * torch.from_numpy(qs)[:, None, None]
+        acc = deq[0].clone()
+        for i in range(1, g):
+            acc = acc + deq[i]
+        mean = acc / float(g)
+        sigma = (mean.abs().max() / 448.0).item()
+        assert psc == np.float32(sigma)
+        ref = (mean / torch.tensor(sigma, dtype=torch.float32)).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+        assert np.array_equal(pq, ref)
+        wr = torch.from_numpy(w[0]).clone()
+        for i in range(1, g):
+            wr = wr + torch.from_numpy(w[i])
+        assert np.array_equal(pw, (wr / float(g)).numpy())
+
+
+@pytest.mark.parametrize("fmt", ["bf16", "fp8"])
+def test_positive_scalings_and_head_permutation(fmt):
+    x = small(fmt, L=64)
+    m = 9
+    base = run(x, oracle.DENSE, topk=m)["idx"]
+    y = small(fmt, L=64)
+    y.w *= np.float32(4.0)
+    assert np.array_equal(run(y, oracle.DENSE, topk=m)["idx"], base)
+    if fmt == "fp8":
+        y = small(fmt, L=64)
+        y.q_scale *= np.float32(0.5)
+        assert np.array_equal(run(y, oracle.DENSE, topk=m)["idx"], base)
+    perm = np.random.default_rng(0).permutation(x.q.shape[1])
+    for t in (0, 31, 63):
+        f0 = oracle.scores(fmt, x.q[t], 1.0 if x.q_scale is None else x.q_scale[t], x.w[t], x.k, x.k_scale, t)
+        f1 = oracle.scores(fmt, x.q[t][perm], 1.0 if x.q_scale is None else x.q_scale[t], x.w[t][perm],
+                           x.k, x.k_scale, t)
+        assert np.allclose(f0, f1, rtol=1e-12, atol=0)
+
+
+def test_negating_gates_reverses_order_of_active_keys():
+    """One head: negating the gate negates every score, so the dense top-k over
+    keys with a positive dot becomes the bottom of the order."""
+    x = small("bf16", L=50, H=1, d=8)
+    t = 49
+    f = oracle.scores("bf16", x.q[t], 1.0, x.w[t], x.k, None, t)
+    g = oracle.scores("bf16", x.q[t], 1.0, -x.w[t], x.k, None, t)
+    assert np.array_equal(g, -f)
+
+
+def test_group_count_and_ragged_tail():
+    """Eq. 2: groups are runs of g from the call's first query; a short last
+    group of one row is its own proxy, which gives the dense set truncated at
+    its own position, i.e. the dense set."""
+    x = small("fp8", L=45)
+    dense = run(x, oracle.DENSE, topk=5)["idx"]
+    r = run(x, oracle.REUSE, g=4, c=8, topk=5)["idx"]        # 45 = 11*4 + 1
+    assert sorted(r[44].tolist()) == sorted(dense[44].tolist())
+    chunked = np.concatenate([run(x, oracle.REUSE, g=4, c=8, topk=5, p0=p, n_q=min(16, 45 - p))["idx"]
+                              for p in range(0, 45, 16)])
+    assert np.array_equal(chunked, r)                         # chunks of a multiple of g
