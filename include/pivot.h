@@ -1,0 +1,188 @@
+/*
+ * pivot.h - C ABI of the MI355X (gfx950) PIVOT indexer library (libpivot.so).
+ *
+ * The library computes the DeepSeek-Sparse-Attention lightning indexer and the
+ * PIVOT grouped replacement for it (PIVOT: Efficient Query-Group Indexing for
+ * Token-Level Sparse Attention):
+ *
+ *   score   I[t,s] = sum_j w[t,j] * ReLU(q[t,j] . k[s])          Sec. 3.1 Eq. (1)
+ *           fp8 form: kscale[s] * sum_j (w[t,j] * qscale[t])
+ *                              * ReLU(q8[t,j] . k8[s])             App. A
+ *   dense   T_t = TopK({I[t,s] : s <= t}, k)                      Sec. 3.1
+ *   PIVOT   Algorithm 1 (App. E): groups of g queries (Eqs. 2-3), a proxy per
+ *           group (per-head mean, Eq. 4), one proxy scan over s <= t0 (Eq. 5),
+ *           then Reuse (proxy top-k shared, Eq. 6) or Refine (proxy top-c
+ *           candidates, Eq. 7, re-scored per member, Eqs. 8-9); groups whose
+ *           first position t0 is below the guardrail threshold are indexed
+ *           densely.
+ *
+ * Conventions for every entry point:
+ *   - positions are 0-based; a query at position t may select any s <= t;
+ *   - an index set is k int32 positions in unspecified order; when fewer than
+ *     k positions are valid, all of them are returned followed by -1;
+ *   - TopK ranks by score, then by lower position among equal scores;
+ *   - "dev" pointers are device memory on the current HIP device, "host"
+ *     pointers are host memory read during the call;
+ *   - the caller owns every buffer; the library never allocates device memory
+ *     and never synchronises the stream; work is enqueued on `stream`
+ *     (a hipStream_t, NULL for the null stream);
+ *   - every argument is validated before the first launch; a failed call
+ *     returns a status and launches nothing; no call aborts or throws;
+ *   - v1 supports H = 64 indexer heads of dimension d = 128 (UNSUPPORTED
+ *     otherwise); fp8 means OCP E4M3FN (largest finite 448) with fp32
+ *     per-token scales; gates w are fp32.
+ */
+#ifndef PIVOT_H
+#define PIVOT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  PIVOT_OK = 0,
+  PIVOT_ERR_INVALID_ARG = 1,  /* null pointer, inconsistent size or parameter */
+  PIVOT_ERR_UNSUPPORTED = 2,  /* shape or dtype this build does not specialise */
+  PIVOT_ERR_WORKSPACE = 3,    /* workspace_bytes below pivot_workspace_size() */
+  PIVOT_ERR_HIP = 4           /* a HIP launch failed; see pivot_last_error() */
+} pivot_status;
+
+typedef enum { PIVOT_DT_BF16 = 0, PIVOT_DT_FP8_E4M3 = 1 } pivot_dtype;
+
+typedef enum { PIVOT_REUSE = 0, PIVOT_REFINE = 1 } pivot_mode;
+
+/* Passed as `mode` to pivot_workspace_size() for a dense call. */
+#define PIVOT_DENSE (-1)
+
+/*
+ * One indexer call over B sequences.
+ *
+ * Layouts (row-major, contiguous):
+ *   q        dev  [B, n_q, H, d]  bf16 bits or E4M3FN codes
+ *   q_scale  dev  [B, n_q]        fp32, fp8 only (NULL for bf16)
+ *   w        dev  [B, n_q, H]     fp32 gates
+ *   k        dev  [B, k_seq_stride, d]  keys of each sequence, position-major
+ *   k_scale  dev  [B, k_seq_stride]     fp32, fp8 only (NULL for bf16)
+ *   out_idx  dev  [B, n_q, topk]  int32 result
+ *
+ * Sequence b holds n_q queries at positions q_pos0[b] .. q_pos0[b]+n_q-1 and
+ * keys at positions 0 .. n_k[b]-1, with q_pos0[b] + n_q <= n_k[b] <=
+ * k_seq_stride.  Prefill passes B = 1, q_pos0 = the chunk start and
+ * n_k = q_pos0 + n_q; chunks whose start is a multiple of g give groups aligned
+ * to absolute positions.  Decode passes n_q = g (the current query and its MTP
+ * drafts, Eq. 3) and q_pos0[b] = n_k[b] - g.
+ */
+typedef struct {
+  int32_t dtype;            /* pivot_dtype */
+  int32_t heads;            /* H, must be 64 */
+  int32_t dim;              /* d, must be 128 */
+  int32_t batch;            /* B >= 1 */
+  int32_t n_q;              /* queries per sequence in this call, >= 0 */
+  const int32_t* q_pos0;    /* host [B] */
+  const int32_t* n_k;       /* host [B] */
+  const void* q;
+  const float* q_scale;
+  const float* w;
+  const void* k;
+  const float* k_scale;
+  int64_t k_seq_stride;     /* key rows between consecutive sequences */
+  int32_t topk;             /* k >= 1 */
+  int32_t* out_idx;
+  void* workspace;          /* dev scratch, >= pivot_workspace_size() bytes, 256-B aligned */
+  size_t workspace_bytes;
+  void* stream;             /* hipStream_t */
+} pivot_args;
+
+/*
+ * Workspace bytes needed by pivot_dense_index (mode = PIVOT_DENSE) or by
+ * pivot_group_index (mode = PIVOT_REUSE / PIVOT_REFINE with g, c and the
+ * guardrail at c) for the shapes in `a`; only the host arrays q_pos0 / n_k are
+ * read.  Returns 0 if the shapes are invalid.  The fp32 score rows are tiled so
+ * that this size stays near 1 GiB for long prefixes.  Any workspace of at
+ * least this size works; smaller ones down to one score tile also work (more
+ * tiles), and below that the entry points return PIVOT_ERR_WORKSPACE.
+ */
+size_t pivot_workspace_size(const pivot_args* a, int32_t mode, int32_t g, int32_t c);
+
+/*
+ * Dense lightning indexer (Sec. 3.1 Eq. 1 with the fp8 form of App. A):
+ * out_idx[b, i, :] = TopK over s in [0, q_pos0[b] + i] of the score of query
+ * (b, i) against key s, k = a->topk.
+ */
+pivot_status pivot_dense_index(const pivot_args* a);
+
+/*
+ * PIVOT (Algorithm 1, App. E).  Groups are runs of g consecutive queries from
+ * each sequence's first query in the call (Eq. 2; a decode call with n_q = g is
+ * one MTP group, Eq. 3); the last run may be shorter.  For a group with first
+ * position t0:
+ *   - t0 < dense_below: each member gets its dense index set (the guardrail of
+ *     Algorithm 1; pass dense_below = c to follow Algorithm 1, 0 to disable,
+ *     a negative value means c);
+ *   - otherwise the proxy is the per-head mean of the members' dequantised
+ *     queries and of their gates (Eq. 4), stored as a query row (fp8: scale
+ *     amax/448 and round-to-nearest-even codes; bf16: round-to-nearest-even);
+ *     a group of one is its own proxy.  The proxy scores positions [0, t0]
+ *     (Eq. 5).  PIVOT_REUSE gives every member the proxy top-k (Eq. 6);
+ *     PIVOT_REFINE keeps the proxy top-c set C (Eq. 7) and gives each member
+ *     the top-k of its own scores over C (Eqs. 8-9).
+ * Requirements: g >= 1; Refine needs topk <= c <= 8192.
+ * out_cand (optional, Refine only): dev int32 [B, ceil(n_q/g), c] receives each
+ * group's candidate set (unordered, -1 padded; all -1 for guardrail groups).
+ */
+pivot_status pivot_group_index(const pivot_args* a, int32_t mode, int32_t g, int32_t c,
+                               int32_t dense_below, int32_t* out_cand);
+
+/*
+ * Stage: proxy rows of Eq. 4 for one sequence's queries q [n_q, H, d] /
+ * q_scale [n_q] / w [n_q, H] split into runs of g (last may be shorter).
+ * Writes out_q [ceil(n_q/g), H, d] (same format as q), out_scale
+ * [ceil(n_q/g)] (1.0 for bf16) and out_w [ceil(n_q/g), H].  Dev pointers.
+ */
+pivot_status pivot_proxy_rows(int32_t dtype, int32_t heads, int32_t dim, int32_t n_q, int32_t g,
+                              const void* q, const float* q_scale, const float* w,
+                              void* out_q, float* out_scale, float* out_w, void* stream);
+
+/*
+ * Stage: score rows (Eq. 1 / App. A).  Row r (r < n_rows) of q [n_rows, H, d],
+ * q_scale [n_rows] (fp8) and w [n_rows, H] is scored against keys
+ * s = 0 .. lim0 + r * lim_step of k / k_scale (which must hold at least that
+ * many keys); out[r * ld + s] receives the fp32 score.  Entries past a row's
+ * limit are not written.  Requires ld >= lim0 + (n_rows-1)*lim_step + 1.
+ */
+pivot_status pivot_score_rows(int32_t dtype, int32_t heads, int32_t dim, int32_t n_rows,
+                              const void* q, const float* q_scale, const float* w,
+                              const void* k, const float* k_scale, int64_t lim0, int32_t lim_step,
+                              float* out, int64_t ld, void* stream);
+
+/*
+ * Stage: TopK of fp32 rows.  Row r of scores [n_rows, ld] has its first
+ * n0 + r * n_step entries valid; out [n_rows, m] receives their top-m
+ * positions (score descending, then position ascending; -0 == +0; -1 padded).
+ */
+pivot_status pivot_topk_rows(int32_t n_rows, const float* scores, int64_t ld, int64_t n0,
+                             int32_t n_step, int32_t m, int32_t* out, void* stream);
+
+/*
+ * Utility: x [n] fp32 -> E4M3FN codes out [n] with the same conversion the
+ * proxy kernel uses (round to nearest even).  Dev pointers.
+ */
+pivot_status pivot_encode_e4m3(const float* x, uint8_t* out, int64_t n, void* stream);
+
+/* Static description of a status code. */
+const char* pivot_status_string(int32_t status);
+
+/* Detail of the last failure on the calling thread (empty if none). */
+const char* pivot_last_error(void);
+
+/* Library version string. */
+const char* pivot_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PIVOT_H */

@@ -1,0 +1,246 @@
+"""MI355X (gfx950) PIVOT indexer: thin Python binding of libpivot.so.
+
+Every function marshals torch tensors (device memory) and the current HIP
+stream into the C ABI declared in include/pivot.h and calls it; all arithmetic
+runs in the library's HIP kernels.  The binding allocates the workspace the
+library asks for (the library itself never allocates).  Importing works without
+a GPU; calling needs the built library and a gfx950 device, and fails loudly
+otherwise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libpivot.so")
+
+PIVOT_OK, PIVOT_ERR_INVALID_ARG, PIVOT_ERR_UNSUPPORTED, PIVOT_ERR_WORKSPACE, PIVOT_ERR_HIP = range(5)
+PIVOT_DT_BF16, PIVOT_DT_FP8_E4M3 = 0, 1
+PIVOT_REUSE, PIVOT_REFINE = 0, 1
+PIVOT_DENSE = -1
+H, D = 64, 128
+
+EXPORTED = ["pivot_workspace_size", "pivot_dense_index", "pivot_group_index", "pivot_proxy_rows",
+            "pivot_score_rows", "pivot_topk_rows", "pivot_encode_e4m3", "pivot_status_string",
+            "pivot_last_error", "pivot_version"]
+
+
+class PivotError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {status_string(status)} ({last_error()})")
+
+
+class pivot_args(ctypes.Structure):
+    _fields_ = [
+        ("dtype", ctypes.c_int32), ("heads", ctypes.c_int32), ("dim", ctypes.c_int32),
+        ("batch", ctypes.c_int32), ("n_q", ctypes.c_int32),
+        ("q_pos0", ctypes.POINTER(ctypes.c_int32)), ("n_k", ctypes.POINTER(ctypes.c_int32)),
+        ("q", ctypes.c_void_p), ("q_scale", ctypes.c_void_p), ("w", ctypes.c_void_p),
+        ("k", ctypes.c_void_p), ("k_scale", ctypes.c_void_p), ("k_seq_stride", ctypes.c_int64),
+        ("topk", ctypes.c_int32), ("out_idx", ctypes.c_void_p),
+        ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t),
+        ("stream", ctypes.c_void_p),
+    ]
+
+
+_lib = None
+
+
+def lib():
+    """Load libpivot.so (built by __graft_entry__.build() / paper_2607_24593_amd.build)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"HIP library missing: {LIB_PATH}; build it with paper_2607_24593_amd.build")
+        L = ctypes.CDLL(LIB_PATH)
+        A = ctypes.POINTER(pivot_args)
+        I32, I64, P = ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p
+        L.pivot_workspace_size.restype = ctypes.c_size_t
+        L.pivot_workspace_size.argtypes = [A, I32, I32, I32]
+        L.pivot_dense_index.restype = I32
+        L.pivot_dense_index.argtypes = [A]
+        L.pivot_group_index.restype = I32
+        L.pivot_group_index.argtypes = [A, I32, I32, I32, I32, P]
+        L.pivot_proxy_rows.restype = I32
+        L.pivot_proxy_rows.argtypes = [I32, I32, I32, I32, I32, P, P, P, P, P, P, P]
+        L.pivot_score_rows.restype = I32
+        L.pivot_score_rows.argtypes = [I32, I32, I32, I32, P, P, P, P, P, I64, I32, P, I64, P]
+        L.pivot_topk_rows.restype = I32
+        L.pivot_topk_rows.argtypes = [I32, P, I64, I64, I32, I32, P, P]
+        L.pivot_encode_e4m3.restype = I32
+        L.pivot_encode_e4m3.argtypes = [P, P, I64, P]
+        L.pivot_status_string.restype = ctypes.c_char_p
+        L.pivot_status_string.argtypes = [I32]
+        L.pivot_last_error.restype = ctypes.c_char_p
+        L.pivot_last_error.argtypes = []
+        L.pivot_version.restype = ctypes.c_char_p
+        L.pivot_version.argtypes = []
+        _lib = L
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().pivot_status_string(int(status)).decode()
+
+
+def last_error() -> str:
+    return lib().pivot_last_error().decode()
+
+
+def version() -> str:
+    return lib().pivot_version().decode()
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, torch.cuda.Stream):
+        return ctypes.c_void_p(stream.cuda_stream)
+    return ctypes.c_void_p(int(stream))
+
+
+def _dtype_code(q) -> int:
+    if q.element_size() == 1:
+        return PIVOT_DT_FP8_E4M3
+    if q.element_size() == 2:
+        return PIVOT_DT_BF16
+    raise ValueError("q must hold fp8 codes (1 byte) or bf16 (2 bytes)")
+
+
+def _check(status: int, where: str):
+    if status != PIVOT_OK:
+        raise PivotError(status, where)
+
+
+_WS = {}
+
+
+def workspace(nbytes: int, device) -> torch.Tensor:
+    """A cached device buffer of at least nbytes (256-byte aligned by torch)."""
+    dev = torch.device(device)
+    key = (dev.type, dev.index)
+    buf = _WS.get(key)
+    if buf is None or buf.numel() < nbytes:
+        _WS.pop(key, None)
+        buf = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=dev)
+        _WS[key] = buf
+    return buf
+
+
+def make_args(q, q_scale, w, k, k_scale, q_pos0, n_k, topk, out_idx, k_seq_stride=None, stream=None):
+    """pivot_args for q [B, n_q, H, d] (or [n_q, H, d]), w [B, n_q, H], k [B, S, d]
+    (or [S, d]); q_pos0 / n_k are ints or per-sequence lists."""
+    if q.dim() == 3:
+        q = q.unsqueeze(0)
+        w = w.unsqueeze(0)
+        q_scale = None if q_scale is None else q_scale.unsqueeze(0)
+    if k.dim() == 2:
+        k = k.unsqueeze(0)
+        k_scale = None if k_scale is None else k_scale.unsqueeze(0)
+    B, n_q = q.shape[0], q.shape[1]
+    pos = [int(q_pos0)] * B if isinstance(q_pos0, int) else [int(v) for v in q_pos0]
+    nk = [int(n_k)] * B if isinstance(n_k, int) else [int(v) for v in n_k]
+    for t in (q, w, k, out_idx) + tuple(x for x in (q_scale, k_scale) if x is not None):
+        if not t.is_contiguous():
+            raise ValueError("tensors must be contiguous")
+    a = pivot_args()
+    a.dtype = _dtype_code(q)
+    a.heads, a.dim = q.shape[2], q.shape[3]
+    a.batch, a.n_q = B, n_q
+    a._pos = (ctypes.c_int32 * B)(*pos)
+    a._nk = (ctypes.c_int32 * B)(*nk)
+    a.q_pos0 = ctypes.cast(a._pos, ctypes.POINTER(ctypes.c_int32))
+    a.n_k = ctypes.cast(a._nk, ctypes.POINTER(ctypes.c_int32))
+    a.q, a.q_scale, a.w = _ptr(q), _ptr(q_scale), _ptr(w)
+    a.k, a.k_scale = _ptr(k), _ptr(k_scale)
+    a.k_seq_stride = k.shape[1] if k_seq_stride is None else int(k_seq_stride)
+    a.topk = int(topk)
+    a.out_idx = _ptr(out_idx)
+    a.stream = _stream(stream)
+    a._keep = (q, q_scale, w, k, k_scale, out_idx)
+    return a
+
+
+def pivot_workspace_size(a: pivot_args, mode: int = PIVOT_DENSE, g: int = 1, c: int = 0) -> int:
+    return int(lib().pivot_workspace_size(ctypes.byref(a), int(mode), int(g), int(c)))
+
+
+def _attach_workspace(a, mode, g, c, ws, device):
+    need = pivot_workspace_size(a, mode, g, c)
+    if need == 0 and a.n_q > 0:
+        return  # invalid shapes: the entry point reports the reason
+    buf = ws if ws is not None else workspace(need, device)
+    a.workspace = _ptr(buf)
+    a.workspace_bytes = buf.numel() * buf.element_size()
+    a._ws = buf
+
+
+def pivot_dense_index(q, q_scale, w, k, k_scale, q_pos0, n_k, topk, out=None, ws=None, stream=None):
+    """Dense lightning indexer: returns int32 [B, n_q, topk] (or [n_q, topk])."""
+    squeeze = q.dim() == 3
+    shape = (q.shape[0], topk) if squeeze else (q.shape[0], q.shape[1], topk)
+    out = torch.empty(shape, dtype=torch.int32, device=q.device) if out is None else out
+    a = make_args(q, q_scale, w, k, k_scale, q_pos0, n_k, topk, out, stream=stream)
+    _attach_workspace(a, PIVOT_DENSE, 1, 0, ws, q.device)
+    _check(lib().pivot_dense_index(ctypes.byref(a)), "pivot_dense_index")
+    return out
+
+
+def pivot_group_index(q, q_scale, w, k, k_scale, q_pos0, n_k, topk, mode, g, c, dense_below=-1,
+                      out=None, out_cand=None, ws=None, stream=None):
+    """PIVOT Reuse / Refine (Algorithm 1): returns int32 [B, n_q, topk] (or [n_q, topk])."""
+    squeeze = q.dim() == 3
+    shape = (q.shape[0], topk) if squeeze else (q.shape[0], q.shape[1], topk)
+    out = torch.empty(shape, dtype=torch.int32, device=q.device) if out is None else out
+    a = make_args(q, q_scale, w, k, k_scale, q_pos0, n_k, topk, out, stream=stream)
+    _attach_workspace(a, mode, g, c, ws, q.device)
+    _check(lib().pivot_group_index(ctypes.byref(a), int(mode), int(g), int(c), int(dense_below),
+                                   _ptr(out_cand)), "pivot_group_index")
+    return out
+
+
+def pivot_proxy_rows(q, q_scale, w, g, stream=None):
+    """Eq. 4 proxies of runs of g rows of one sequence: (q_proxy, scale, w_proxy)."""
+    n_q = q.shape[0]
+    ng = (n_q + g - 1) // g
+    pq = torch.empty((ng,) + tuple(q.shape[1:]), dtype=q.dtype, device=q.device)
+    ps = torch.empty(ng, dtype=torch.float32, device=q.device)
+    pw = torch.empty((ng, w.shape[1]), dtype=torch.float32, device=q.device)
+    _check(lib().pivot_proxy_rows(_dtype_code(q), q.shape[1], q.shape[2], n_q, int(g), _ptr(q), _ptr(q_scale),
+                                  _ptr(w), _ptr(pq), _ptr(ps), _ptr(pw), _stream(stream)), "pivot_proxy_rows")
+    return pq, ps, pw
+
+
+def pivot_score_rows(q, q_scale, w, k, k_scale, lim0, lim_step, ld=None, out=None, stream=None):
+    """Scores of rows q [n, H, d] over keys 0 .. lim0 + r * lim_step: fp32 [n, ld]."""
+    n = q.shape[0]
+    lim_max = lim0 + (n - 1) * lim_step
+    ld = lim_max + 1 if ld is None else ld
+    out = torch.full((n, ld), float("nan"), dtype=torch.float32, device=q.device) if out is None else out
+    _check(lib().pivot_score_rows(_dtype_code(q), q.shape[1], q.shape[2], n, _ptr(q), _ptr(q_scale), _ptr(w),
+                                  _ptr(k), _ptr(k_scale), int(lim0), int(lim_step), _ptr(out), int(ld),
+                                  _stream(stream)), "pivot_score_rows")
+    return out
+
+
+def pivot_topk_rows(scores, n0, n_step, m, out=None, stream=None):
+    """Top-m positions of rows of scores [n, ld] with n0 + r * n_step valid entries."""
+    n, ld = scores.shape
+    out = torch.empty((n, m), dtype=torch.int32, device=scores.device) if out is None else out
+    _check(lib().pivot_topk_rows(n, _ptr(scores), ld, int(n0), int(n_step), int(m), _ptr(out), _stream(stream)),
+           "pivot_topk_rows")
+    return out
+
+
+def pivot_encode_e4m3(x, out=None, stream=None):
+    out = torch.empty(x.shape, dtype=torch.uint8, device=x.device) if out is None else out
+    _check(lib().pivot_encode_e4m3(_ptr(x), _ptr(out), x.numel(), _stream(stream)), "pivot_encode_e4m3")
+    return out

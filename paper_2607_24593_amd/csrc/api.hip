@@ -1,0 +1,465 @@
+// C ABI of libpivot.so: argument validation, the group plan of Algorithm 1
+// (App. E), workspace carving and the launch sequence on the caller's stream.
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <vector>
+
+#include "launch.h"
+#include "pivot.h"
+
+using namespace pivot;
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+pivot_status fail(pivot_status s, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+pivot_status hip_check(hipError_t e, const char* what) {
+  if (e == hipSuccess) return PIVOT_OK;
+  return fail(PIVOT_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+constexpr size_t kAlign = 256;
+constexpr int64_t kDefaultScoreBytes = int64_t(1) << 30;  // score tiles target ~1 GiB
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+int64_t ld_for(int64_t n) { return (n + 63) / 64 * 64; }
+int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// The group plan: for each sequence, how many leading query rows take the dense
+// path (the guardrail of Algorithm 1) and from which group on the proxy path runs.
+struct Plan {
+  int mode = PIVOT_DENSE;  // PIVOT_DENSE, PIVOT_REUSE or PIVOT_REFINE
+  int g = 1, c = 0, dense_below = 0;
+  int n_groups = 0;
+  int B = 0, n_q = 0, topk = 0, dtype = 0, EB = 1;
+  size_t row_bytes = 0;
+  std::vector<int32_t> dense_rows, first_proxy, q_pos0, n_k;
+  int dense_hi = 0;     // max dense_rows over sequences
+  int proxy_lo = 0;     // min first_proxy over sequences
+  int64_t max_nk = 0;
+  // workspace layout
+  size_t off_pq = 0, off_psc = 0, off_pw = 0, off_cand = 0, off_scores = 0, fixed = 0;
+};
+
+pivot_status check_args(const pivot_args* a) {
+  if (!a) return fail(PIVOT_ERR_INVALID_ARG, "args is NULL");
+  if (a->dtype != PIVOT_DT_BF16 && a->dtype != PIVOT_DT_FP8_E4M3)
+    return fail(PIVOT_ERR_UNSUPPORTED, "dtype %d not supported", a->dtype);
+  if (a->heads != kH || a->dim != kD)
+    return fail(PIVOT_ERR_UNSUPPORTED, "heads=%d dim=%d: this build specialises H=64, d=128", a->heads, a->dim);
+  if (a->batch < 1) return fail(PIVOT_ERR_INVALID_ARG, "batch must be >= 1");
+  if (a->n_q < 0) return fail(PIVOT_ERR_INVALID_ARG, "n_q must be >= 0");
+  if (a->topk < 1) return fail(PIVOT_ERR_INVALID_ARG, "topk must be >= 1");
+  if (!a->q_pos0 || !a->n_k) return fail(PIVOT_ERR_INVALID_ARG, "q_pos0 and n_k (host arrays) are required");
+  for (int b = 0; b < a->batch; ++b) {
+    if (a->q_pos0[b] < 0) return fail(PIVOT_ERR_INVALID_ARG, "q_pos0[%d] < 0", b);
+    if ((int64_t)a->q_pos0[b] + a->n_q > a->n_k[b])
+      return fail(PIVOT_ERR_INVALID_ARG, "n_k[%d]=%d < q_pos0+n_q=%lld", b, a->n_k[b],
+                  (long long)a->q_pos0[b] + a->n_q);
+    if (a->n_k[b] > a->k_seq_stride)
+      return fail(PIVOT_ERR_INVALID_ARG, "n_k[%d]=%d exceeds k_seq_stride=%lld", b, a->n_k[b],
+                  (long long)a->k_seq_stride);
+  }
+  if (a->n_q > 0) {
+    if (!a->q || !a->w || !a->k || !a->out_idx)
+      return fail(PIVOT_ERR_INVALID_ARG, "q, w, k and out_idx are required");
+    if (a->dtype == PIVOT_DT_FP8_E4M3 && (!a->q_scale || !a->k_scale))
+      return fail(PIVOT_ERR_INVALID_ARG, "fp8 inputs need q_scale and k_scale");
+  }
+  return PIVOT_OK;
+}
+
+pivot_status make_plan(const pivot_args* a, int mode, int g, int c, int dense_below, Plan& p) {
+  pivot_status s = check_args(a);
+  if (s != PIVOT_OK) return s;
+  if (mode != PIVOT_DENSE && mode != PIVOT_REUSE && mode != PIVOT_REFINE)
+    return fail(PIVOT_ERR_INVALID_ARG, "mode %d", mode);
+  if (mode != PIVOT_DENSE) {
+    if (g < 1) return fail(PIVOT_ERR_INVALID_ARG, "g must be >= 1");
+    if (c < 0) return fail(PIVOT_ERR_INVALID_ARG, "c must be >= 0");
+    if (mode == PIVOT_REFINE && c < a->topk) return fail(PIVOT_ERR_INVALID_ARG, "Refine needs c >= topk");
+    if (mode == PIVOT_REFINE && c > 8192) return fail(PIVOT_ERR_UNSUPPORTED, "Refine supports c <= 8192");
+  } else {
+    g = 1;
+    c = 0;
+  }
+  p.mode = mode;
+  p.g = g;
+  p.c = c;
+  p.dense_below = (mode == PIVOT_DENSE) ? 0 : (dense_below < 0 ? c : dense_below);
+  p.B = a->batch;
+  p.n_q = a->n_q;
+  p.topk = a->topk;
+  p.dtype = a->dtype;
+  p.EB = a->dtype == PIVOT_DT_FP8_E4M3 ? 1 : 2;
+  p.row_bytes = (size_t)kH * kD * p.EB;
+  p.n_groups = (int)cdiv(p.n_q, g);
+  p.dense_rows.resize(p.B);
+  p.first_proxy.resize(p.B);
+  p.q_pos0.assign(a->q_pos0, a->q_pos0 + p.B);
+  p.n_k.assign(a->n_k, a->n_k + p.B);
+  p.dense_hi = 0;
+  p.proxy_lo = p.n_groups;
+  p.max_nk = 0;
+  for (int b = 0; b < p.B; ++b) {
+    int J;
+    if (mode == PIVOT_DENSE) {
+      J = p.n_groups;
+    } else {
+      const int64_t gap = (int64_t)p.dense_below - p.q_pos0[b];  // groups with t0 < dense_below
+      J = gap <= 0 ? 0 : (int)std::min<int64_t>(cdiv(gap, g), p.n_groups);
+    }
+    p.first_proxy[b] = J;
+    p.dense_rows[b] = (int)std::min<int64_t>((int64_t)J * g, p.n_q);
+    p.dense_hi = std::max(p.dense_hi, p.dense_rows[b]);
+    p.proxy_lo = std::min(p.proxy_lo, J);
+    p.max_nk = std::max<int64_t>(p.max_nk, p.n_k[b]);
+  }
+  // workspace layout
+  size_t off = 0;
+  const size_t ng = (size_t)p.B * p.n_groups;
+  if (mode != PIVOT_DENSE && p.proxy_lo < p.n_groups) {
+    p.off_pq = off;
+    off = align_up(off + ng * p.row_bytes);
+    p.off_psc = off;
+    off = align_up(off + ng * sizeof(float));
+    p.off_pw = off;
+    off = align_up(off + ng * kH * sizeof(float));
+    if (mode == PIVOT_REFINE) {
+      p.off_cand = off;
+      off = align_up(off + ng * (size_t)c * sizeof(int32_t));
+    }
+  }
+  p.off_scores = off;
+  p.fixed = off;
+  return PIVOT_OK;
+}
+
+// Bytes of scores for the whole call at once, and for the smallest tile.
+void score_need(const Plan& p, int64_t& full, int64_t& min_tile) {
+  full = 0;
+  min_tile = 0;
+  const int64_t ld = ld_for(p.max_nk);
+  if (p.dense_hi > 0) {
+    const int64_t rows = (p.B == 1) ? p.dense_hi : (int64_t)p.B * p.n_q;
+    full = std::max(full, rows * ld * 4);
+    min_tile = std::max(min_tile, ((p.B == 1) ? std::min<int64_t>(16, rows) : p.n_q) * ld * 4);
+  }
+  if (p.mode != PIVOT_DENSE && p.proxy_lo < p.n_groups) {
+    const int64_t rows = (p.B == 1) ? (p.n_groups - p.proxy_lo) : (int64_t)p.B * p.n_groups;
+    full = std::max(full, rows * ld * 4);
+    min_tile = std::max(min_tile, ((p.B == 1) ? std::min<int64_t>(16, rows) : p.n_groups) * ld * 4);
+  }
+}
+
+size_t recommended_bytes(const Plan& p) {
+  int64_t full, min_tile;
+  score_need(p, full, min_tile);
+  const int64_t scores = std::min(full, std::max(min_tile, kDefaultScoreBytes));
+  return p.fixed + (size_t)scores;
+}
+
+SeqTable table_for(const Plan& p, int b0, int nb) {
+  SeqTable st;
+  memset(&st, 0, sizeof st);
+  st.n = nb;
+  for (int u = 0; u < nb; ++u) {
+    st.q_pos0[u] = p.q_pos0[b0 + u];
+    st.dense_rows[u] = p.dense_rows[b0 + u];
+    st.first_proxy[u] = p.first_proxy[b0 + u];
+  }
+  return st;
+}
+
+// Largest limit of an active row of rs in any sequence of st.
+int64_t max_limit(const SeqTable& st, const RowSpace& rs) {
+  int64_t lim = -1;
+  for (int b = 0; b < st.n; ++b) {
+    int hi = rs.i1;
+    int lo = rs.i0;
+    if (rs.kind == kDenseRows) hi = std::min(hi, st.dense_rows[b]);
+    if (rs.kind == kProxyRows) lo = std::max(lo, st.first_proxy[b]);
+    if (hi > lo) lim = std::max(lim, (int64_t)st.q_pos0[b] + (int64_t)(hi - 1) * rs.step);
+  }
+  return lim;
+}
+
+struct RowData {
+  const void* q;
+  const float* qs;
+  const float* w;
+  int64_t seq_rows;  // rows per sequence in q
+};
+
+// Score and select rows [lo, hi) of each sequence, tiled to the score budget.
+pivot_status run_rows(const pivot_args* a, const Plan& p, int kind, int lo, int hi, int step, int per_seq,
+                      const RowData& rd_all, OutDesc od_all, float* scores, int64_t score_bytes,
+                      hipStream_t stream) {
+  if (hi <= lo) return PIVOT_OK;
+  const int64_t ld_max = ld_for(p.max_nk);
+  const int64_t row_bytes = ld_max * 4;
+  int seqs_per_tile, rows_per_tile;
+  if (p.B == 1) {
+    seqs_per_tile = 1;
+    int64_t r = score_bytes / row_bytes;
+    r = std::max<int64_t>(16, r / 16 * 16);
+    rows_per_tile = (int)std::min<int64_t>(r, hi - lo);
+  } else {
+    rows_per_tile = hi - lo;
+    int64_t s = score_bytes / (row_bytes * (hi - lo));
+    seqs_per_tile = (int)std::max<int64_t>(1, std::min<int64_t>(s, kMaxSeq));
+  }
+  if ((int64_t)seqs_per_tile * rows_per_tile * row_bytes > score_bytes)
+    return fail(PIVOT_ERR_WORKSPACE, "workspace too small for one score tile");
+  for (int b0 = 0; b0 < p.B; b0 += seqs_per_tile) {
+    const int nb = std::min(seqs_per_tile, p.B - b0);
+    SeqTable st = table_for(p, b0, nb);
+    RowData rd = rd_all;
+    rd.q = (const uint8_t*)rd_all.q + (size_t)b0 * rd_all.seq_rows * p.row_bytes;
+    rd.qs = rd_all.qs ? rd_all.qs + (size_t)b0 * rd_all.seq_rows : nullptr;
+    rd.w = rd_all.w + (size_t)b0 * rd_all.seq_rows * kH;
+    const uint8_t* kb = (const uint8_t*)a->k + (size_t)b0 * a->k_seq_stride * kD * p.EB;
+    const float* ksb = a->k_scale ? a->k_scale + (size_t)b0 * a->k_seq_stride : nullptr;
+    OutDesc od = od_all;
+    od.base = od_all.base + (size_t)b0 * od_all.per_seq * od_all.m;
+    for (int i0 = lo; i0 < hi; i0 += rows_per_tile) {
+      RowSpace rs{i0, std::min(hi, i0 + rows_per_tile), step, kind};
+      const int64_t lim = max_limit(st, rs);
+      if (lim < 0) continue;
+      const int64_t ld = ld_for(lim + 1);
+      pivot_status s = hip_check(launch_score(p.dtype, rd.q, rd.qs, rd.w, rd.seq_rows, kb, ksb, a->k_seq_stride,
+                                              st, rs, lim, scores, ld, stream),
+                                 "score kernel");
+      if (s != PIVOT_OK) return s;
+      s = hip_check(launch_topk(scores, ld, st, rs, od, stream), "top-k kernel");
+      if (s != PIVOT_OK) return s;
+    }
+  }
+  (void)per_seq;
+  return PIVOT_OK;
+}
+
+pivot_status check_workspace(const pivot_args* a, const Plan& p, int64_t& score_bytes) {
+  int64_t full, min_tile;
+  score_need(p, full, min_tile);
+  const size_t need_min = p.fixed + (size_t)min_tile;
+  if (need_min > 0) {
+    if (!a->workspace) return fail(PIVOT_ERR_WORKSPACE, "workspace is NULL (need >= %zu bytes)", need_min);
+    if (reinterpret_cast<uintptr_t>(a->workspace) % kAlign)
+      return fail(PIVOT_ERR_INVALID_ARG, "workspace must be %zu-byte aligned", kAlign);
+    if (a->workspace_bytes < need_min)
+      return fail(PIVOT_ERR_WORKSPACE, "workspace_bytes=%zu < minimum %zu", a->workspace_bytes, need_min);
+  }
+  score_bytes = (int64_t)(a->workspace_bytes - p.fixed);
+  return PIVOT_OK;
+}
+
+pivot_status dense_part(const pivot_args* a, const Plan& p, float* scores, int64_t score_bytes, hipStream_t stream) {
+  RowData rd{a->q, a->dtype == PIVOT_DT_FP8_E4M3 ? a->q_scale : nullptr, a->w, p.n_q};
+  OutDesc od{a->out_idx, p.topk, p.n_q, 0, p.n_q};
+  const int kind = p.mode == PIVOT_DENSE ? kAll : kDenseRows;
+  return run_rows(a, p, kind, 0, p.dense_hi, 1, p.n_q, rd, od, scores, score_bytes, stream);
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t pivot_workspace_size(const pivot_args* a, int32_t mode, int32_t g, int32_t c) {
+  if (!a) return 0;
+  pivot_args shape = *a;
+  // pointers are not read for sizing: give the validator non-null stand-ins
+  static const float dummy = 0.f;
+  shape.q = shape.k = &dummy;
+  shape.w = shape.q_scale = shape.k_scale = &dummy;
+  shape.out_idx = reinterpret_cast<int32_t*>(const_cast<float*>(&dummy));
+  Plan p;
+  if (make_plan(&shape, mode, g, c, c, p) != PIVOT_OK) return 0;
+  return recommended_bytes(p);
+}
+
+pivot_status pivot_dense_index(const pivot_args* a) {
+  Plan p;
+  pivot_status s = make_plan(a, PIVOT_DENSE, 1, 0, 0, p);
+  if (s != PIVOT_OK) return s;
+  if (p.n_q == 0) return PIVOT_OK;
+  int64_t score_bytes;
+  s = check_workspace(a, p, score_bytes);
+  if (s != PIVOT_OK) return s;
+  float* scores = reinterpret_cast<float*>((uint8_t*)a->workspace + p.off_scores);
+  return dense_part(a, p, scores, score_bytes, (hipStream_t)a->stream);
+}
+
+pivot_status pivot_group_index(const pivot_args* a, int32_t mode, int32_t g, int32_t c, int32_t dense_below,
+                               int32_t* out_cand) {
+  if (mode != PIVOT_REUSE && mode != PIVOT_REFINE) return fail(PIVOT_ERR_INVALID_ARG, "mode %d", mode);
+  Plan p;
+  pivot_status s = make_plan(a, mode, g, c, dense_below, p);
+  if (s != PIVOT_OK) return s;
+  if (p.n_q == 0) return PIVOT_OK;
+  hipStream_t stream = (hipStream_t)a->stream;
+  if (out_cand && mode == PIVOT_REFINE) {
+    // the caller's buffer replaces the workspace's candidate region
+    p.fixed = p.off_cand;
+    p.off_scores = p.off_cand;
+  }
+  int64_t score_bytes;
+  s = check_workspace(a, p, score_bytes);
+  if (s != PIVOT_OK) return s;
+  uint8_t* ws = (uint8_t*)a->workspace;
+  float* scores = reinterpret_cast<float*>(ws + p.off_scores);
+
+  s = dense_part(a, p, scores, score_bytes, stream);  // guardrail groups (Algorithm 1)
+  if (s != PIVOT_OK) return s;
+  if (p.proxy_lo >= p.n_groups) {
+    if (out_cand && mode == PIVOT_REFINE)
+      for (int b0 = 0; b0 < p.B; b0 += kMaxSeq) {
+        const int nb = std::min(kMaxSeq, p.B - b0);
+        SeqTable st = table_for(p, b0, nb);
+        s = hip_check(launch_fill_guardrail(out_cand + (size_t)b0 * p.n_groups * c, p.n_groups, c, st, 0,
+                                            p.n_groups, -1, stream),
+                      "fill kernel");
+        if (s != PIVOT_OK) return s;
+      }
+    return PIVOT_OK;
+  }
+
+  void* pq = ws + p.off_pq;
+  float* psc = reinterpret_cast<float*>(ws + p.off_psc);
+  float* pw = reinterpret_cast<float*>(ws + p.off_pw);
+  int32_t* cand = (mode == PIVOT_REFINE) ? (out_cand ? out_cand : reinterpret_cast<int32_t*>(ws + p.off_cand))
+                                         : nullptr;
+  const float* qs = p.dtype == PIVOT_DT_FP8_E4M3 ? a->q_scale : nullptr;
+
+  for (int b0 = 0; b0 < p.B; b0 += kMaxSeq) {  // Eq. 4 proxies
+    const int nb = std::min(kMaxSeq, p.B - b0);
+    SeqTable st = table_for(p, b0, nb);
+    const size_t qoff = (size_t)b0 * p.n_q;
+    const size_t poff = (size_t)b0 * p.n_groups;
+    s = hip_check(launch_proxy(p.dtype, (const uint8_t*)a->q + qoff * p.row_bytes, qs ? qs + qoff : nullptr,
+                               a->w + qoff * kH, p.n_q, p.g, p.n_groups, st, p.proxy_lo, p.n_groups, false,
+                               (uint8_t*)pq + poff * p.row_bytes, psc + poff, pw + poff * kH, stream),
+                  "proxy kernel");
+    if (s != PIVOT_OK) return s;
+  }
+
+  // Eq. 5 proxy scan, then Eq. 6 (Reuse: top-k shared by the members) or
+  // Eq. 7 (Refine: top-c candidates)
+  RowData rd{pq, psc, pw, p.n_groups};
+  OutDesc od = (mode == PIVOT_REUSE) ? OutDesc{a->out_idx, p.topk, p.n_q, p.g, p.n_q}
+                                     : OutDesc{cand, c, p.n_groups, 0, 0};
+  s = run_rows(a, p, kProxyRows, p.proxy_lo, p.n_groups, p.g, p.n_groups, rd, od, scores, score_bytes, stream);
+  if (s != PIVOT_OK) return s;
+  if (mode == PIVOT_REUSE) return PIVOT_OK;
+
+  for (int b0 = 0; b0 < p.B; b0 += kMaxSeq) {  // Eqs. 8-9
+    const int nb = std::min(kMaxSeq, p.B - b0);
+    SeqTable st = table_for(p, b0, nb);
+    const size_t qoff = (size_t)b0 * p.n_q;
+    int32_t* cb = cand + (size_t)b0 * p.n_groups * c;
+    if (out_cand) {
+      s = hip_check(launch_fill_guardrail(cb, p.n_groups, c, st, 0, p.n_groups, -1, stream), "fill kernel");
+      if (s != PIVOT_OK) return s;
+    }
+    s = hip_check(launch_refine(p.dtype, (const uint8_t*)a->q + qoff * p.row_bytes, qs ? qs + qoff : nullptr,
+                                a->w + qoff * kH, p.n_q, p.g, p.n_groups,
+                                (const uint8_t*)a->k + (size_t)b0 * a->k_seq_stride * kD * p.EB,
+                                a->k_scale ? a->k_scale + (size_t)b0 * a->k_seq_stride : nullptr, a->k_seq_stride,
+                                st, p.proxy_lo, p.n_groups, cb, c, p.topk, a->out_idx + qoff * p.topk, stream),
+                  "refine kernel");
+    if (s != PIVOT_OK) return s;
+  }
+  return PIVOT_OK;
+}
+
+pivot_status pivot_proxy_rows(int32_t dtype, int32_t heads, int32_t dim, int32_t n_q, int32_t g, const void* q,
+                              const float* q_scale, const float* w, void* out_q, float* out_scale, float* out_w,
+                              void* stream) {
+  if (dtype != PIVOT_DT_BF16 && dtype != PIVOT_DT_FP8_E4M3) return fail(PIVOT_ERR_UNSUPPORTED, "dtype %d", dtype);
+  if (heads != kH || dim != kD) return fail(PIVOT_ERR_UNSUPPORTED, "heads=%d dim=%d", heads, dim);
+  if (n_q < 0 || g < 1) return fail(PIVOT_ERR_INVALID_ARG, "n_q >= 0 and g >= 1 required");
+  if (n_q == 0) return PIVOT_OK;
+  if (!q || !w || !out_q || !out_scale || !out_w || (dtype == PIVOT_DT_FP8_E4M3 && !q_scale))
+    return fail(PIVOT_ERR_INVALID_ARG, "null pointer");
+  SeqTable st;
+  memset(&st, 0, sizeof st);
+  st.n = 1;
+  const int ng = (int)cdiv(n_q, g);
+  return hip_check(launch_proxy(dtype, q, dtype == PIVOT_DT_FP8_E4M3 ? q_scale : nullptr, w, n_q, g, ng, st, 0, ng,
+                                true, out_q, out_scale, out_w, (hipStream_t)stream),
+                   "proxy kernel");
+}
+
+pivot_status pivot_score_rows(int32_t dtype, int32_t heads, int32_t dim, int32_t n_rows, const void* q,
+                              const float* q_scale, const float* w, const void* k, const float* k_scale,
+                              int64_t lim0, int32_t lim_step, float* out, int64_t ld, void* stream) {
+  if (dtype != PIVOT_DT_BF16 && dtype != PIVOT_DT_FP8_E4M3) return fail(PIVOT_ERR_UNSUPPORTED, "dtype %d", dtype);
+  if (heads != kH || dim != kD) return fail(PIVOT_ERR_UNSUPPORTED, "heads=%d dim=%d", heads, dim);
+  if (n_rows < 0 || lim0 < 0 || lim_step < 0) return fail(PIVOT_ERR_INVALID_ARG, "negative size");
+  if (n_rows == 0) return PIVOT_OK;
+  if (!q || !w || !k || !out || (dtype == PIVOT_DT_FP8_E4M3 && (!q_scale || !k_scale)))
+    return fail(PIVOT_ERR_INVALID_ARG, "null pointer");
+  const int64_t lim_max = lim0 + (int64_t)(n_rows - 1) * lim_step;
+  if (lim_max > 0x7FFFFFFE) return fail(PIVOT_ERR_INVALID_ARG, "limits exceed int32 positions");
+  if (ld < lim_max + 1) return fail(PIVOT_ERR_INVALID_ARG, "ld=%lld < %lld", (long long)ld, (long long)lim_max + 1);
+  SeqTable st;
+  memset(&st, 0, sizeof st);
+  st.n = 1;
+  st.q_pos0[0] = (int32_t)lim0;
+  RowSpace rs{0, n_rows, lim_step, kAll};
+  const bool fp8 = dtype == PIVOT_DT_FP8_E4M3;
+  return hip_check(launch_score(dtype, q, fp8 ? q_scale : nullptr, w, n_rows, k, fp8 ? k_scale : nullptr, 0, st, rs,
+                                lim_max, out, ld, (hipStream_t)stream),
+                   "score kernel");
+}
+
+pivot_status pivot_topk_rows(int32_t n_rows, const float* scores, int64_t ld, int64_t n0, int32_t n_step, int32_t m,
+                             int32_t* out, void* stream) {
+  if (n_rows < 0 || n0 < 0 || n_step < 0 || m < 1) return fail(PIVOT_ERR_INVALID_ARG, "bad size");
+  if (n_rows == 0) return PIVOT_OK;
+  if (!scores || !out) return fail(PIVOT_ERR_INVALID_ARG, "null pointer");
+  const int64_t n_max = n0 + (int64_t)(n_rows - 1) * n_step;
+  if (n_max > ld) return fail(PIVOT_ERR_INVALID_ARG, "row length %lld exceeds ld", (long long)n_max);
+  if (n_max > 0x7FFFFFFE) return fail(PIVOT_ERR_INVALID_ARG, "rows exceed int32 positions");
+  SeqTable st;
+  memset(&st, 0, sizeof st);
+  st.n = 1;
+  st.q_pos0[0] = (int32_t)(n0 - 1);
+  RowSpace rs{0, n_rows, n_step, kAll};
+  OutDesc od{out, m, n_rows, 0, 0};
+  return hip_check(launch_topk(scores, ld, st, rs, od, (hipStream_t)stream), "top-k kernel");
+}
+
+pivot_status pivot_encode_e4m3(const float* x, uint8_t* out, int64_t n, void* stream) {
+  if (n < 0) return fail(PIVOT_ERR_INVALID_ARG, "n < 0");
+  if (n == 0) return PIVOT_OK;
+  if (!x || !out) return fail(PIVOT_ERR_INVALID_ARG, "null pointer");
+  return hip_check(launch_encode_e4m3(x, out, n, (hipStream_t)stream), "encode kernel");
+}
+
+const char* pivot_status_string(int32_t status) {
+  switch (status) {
+    case PIVOT_OK: return "ok";
+    case PIVOT_ERR_INVALID_ARG: return "invalid argument";
+    case PIVOT_ERR_UNSUPPORTED: return "unsupported shape or dtype";
+    case PIVOT_ERR_WORKSPACE: return "workspace too small";
+    case PIVOT_ERR_HIP: return "HIP launch failure";
+    default: return "unknown status";
+  }
+}
+
+const char* pivot_last_error(void) { return g_err; }
+
+const char* pivot_version(void) { return "pivot-gfx950 0.1"; }
+
+}  // extern "C"

@@ -1,0 +1,111 @@
+// Workgroup-wide exact top-m selection (radix select on order-preserving keys).
+//
+// Selects the `need` elements of a source that rank first by (key descending,
+// position ascending) and hands each selected position to `emit`.  The key is
+// resolved 8 bits at a time (4 histogram passes); if the m-th key is shared by
+// more elements than remain to be taken, 4 more passes over the positions of
+// the tied elements pick the lowest ones.  A final pass emits every element
+// above the threshold.  Positions must be distinct non-negative int32.
+//
+// Sources provide n() and get(e, key, pos) for e in [0, n()); they are
+// enumerated with a thread stride, so any memory (LDS or global) works.
+#pragma once
+
+#include "device_common.h"
+
+namespace pivot {
+
+struct SelectShared {
+  uint32_t hist[256];
+  uint32_t digit, before, equal;
+  int32_t emitted;
+};
+
+// One wave (the workgroup's first) finds the digit d where the running count
+// crosses `rem`, scanning digits downwards (desc) or upwards (!desc).  Writes
+// sh.digit, sh.before (count strictly before d in scan order), sh.equal (count at d).
+template <bool DESC>
+__device__ __forceinline__ void find_digit(SelectShared& sh, uint32_t rem) {
+  const int lane = threadIdx.x & 63;
+  if (threadIdx.x >= 64) return;
+  uint32_t v[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) v[i] = sh.hist[4 * lane + i];
+  const uint32_t tot = v[0] + v[1] + v[2] + v[3];
+  uint32_t s = tot;  // inclusive scan in scan order
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    uint32_t t = DESC ? __shfl_down(s, o, 64) : __shfl_up(s, o, 64);
+    bool ok = DESC ? (lane + o < 64) : (lane >= o);
+    if (ok) s += t;
+  }
+  uint32_t before = s - tot;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int i = DESC ? 3 - k : k;
+    if (before < rem && rem <= before + v[i]) {
+      sh.digit = 4 * lane + i;
+      sh.before = before;
+      sh.equal = v[i];
+    }
+    before += v[i];
+  }
+}
+
+template <int THREADS, class Src, class Emit>
+__device__ void block_select(const Src& src, uint32_t need, SelectShared& sh, Emit emit) {
+  const int tid = threadIdx.x;
+  const int n = src.n();
+  if (need == 0 || n <= 0) return;
+  uint32_t prefix = 0, mask = 0, rem = need, equal = 0;
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    for (int i = tid; i < 256; i += THREADS) sh.hist[i] = 0;
+    __syncthreads();
+    for (int e = tid; e < n; e += THREADS) {
+      uint32_t key;
+      int32_t pos;
+      src.get(e, key, pos);
+      if ((key & mask) == prefix) atomicAdd(&sh.hist[(key >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    find_digit<true>(sh, rem);
+    __syncthreads();
+    rem -= sh.before;
+    equal = sh.equal;
+    prefix |= sh.digit << shift;
+    mask |= 255u << shift;
+    __syncthreads();
+  }
+  const uint32_t T = prefix;
+  const bool all_ties = (rem == equal);
+  uint32_t ipref = 0, imask = 0;
+  if (!all_ties) {
+    for (int shift = 24; shift >= 0; shift -= 8) {
+      for (int i = tid; i < 256; i += THREADS) sh.hist[i] = 0;
+      __syncthreads();
+      for (int e = tid; e < n; e += THREADS) {
+        uint32_t key;
+        int32_t pos;
+        src.get(e, key, pos);
+        const uint32_t p = (uint32_t)pos;
+        if (key == T && (p & imask) == ipref) atomicAdd(&sh.hist[(p >> shift) & 255u], 1u);
+      }
+      __syncthreads();
+      find_digit<false>(sh, rem);
+      __syncthreads();
+      rem -= sh.before;
+      ipref |= sh.digit << shift;
+      imask |= 255u << shift;
+      __syncthreads();
+    }
+  }
+  for (int e = tid; e < n; e += THREADS) {
+    uint32_t key;
+    int32_t pos;
+    src.get(e, key, pos);
+    if (key > T || (key == T && (all_ties || (uint32_t)pos <= ipref))) emit(pos);
+  }
+  __syncthreads();
+}
+
+}  // namespace pivot

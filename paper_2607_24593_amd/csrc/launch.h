@@ -1,0 +1,51 @@
+// Host-side launchers of the gfx950 kernels (internal to libpivot.so).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "device_common.h"
+
+namespace pivot {
+
+// Where a row's top-m indices go: row (b, i) writes out rows
+//   fan_g == 0: b * per_seq + i
+//   fan_g  > 0: b * per_seq + i * fan_g + u, u < min(fan_g, fan_n - i * fan_g)
+// (the fan-out shares a proxy's top-k with the members of its group).
+struct OutDesc {
+  int32_t* base;
+  int32_t m;
+  int32_t per_seq;
+  int32_t fan_g;
+  int32_t fan_n;
+};
+
+// Proxy rows (Eq. 4) of groups [j0, j1) of each sequence; q rows are
+// [B, n_q, H, d], proxies [B, n_groups, H, d].  all_groups ignores first_proxy.
+hipError_t launch_proxy(int dtype, const void* q, const float* q_scale, const float* w, int n_q, int g,
+                        int n_groups, const SeqTable& st, int j0, int j1, bool all_groups, void* pq,
+                        float* psc, float* pw, hipStream_t stream);
+
+// Score rows rs (row data [B, q_seq_rows, H, d]) against each sequence's keys
+// 0 .. limit; out [B * (i1 - i0), ld].  lim_max: largest limit of any active row.
+hipError_t launch_score(int dtype, const void* q, const float* q_scale, const float* w, int64_t q_seq_rows,
+                        const void* k, const float* k_scale, int64_t k_seq_stride, const SeqTable& st,
+                        const RowSpace& rs, int64_t lim_max, float* out, int64_t ld, hipStream_t stream);
+
+// Top-m of score rows: row (b, i) has limit + 1 valid entries.
+hipError_t launch_topk(const float* scores, int64_t ld, const SeqTable& st, const RowSpace& rs,
+                       const OutDesc& od, hipStream_t stream);
+
+// Refine (Eqs. 8-9) for groups [j0, j1) with j >= first_proxy[b].
+hipError_t launch_refine(int dtype, const void* q, const float* q_scale, const float* w, int n_q, int g,
+                         int n_groups, const void* k, const float* k_scale, int64_t k_seq_stride,
+                         const SeqTable& st, int j0, int j1, const int32_t* cand, int c, int m,
+                         int32_t* out_idx, hipStream_t stream);
+
+// Fill rows (b, j) with j < first_proxy[b], j in [j0, j1), of a [B, per_seq, width] int32 array.
+hipError_t launch_fill_guardrail(int32_t* base, int per_seq, int width, const SeqTable& st, int j0, int j1,
+                                 int32_t value, hipStream_t stream);
+
+hipError_t launch_encode_e4m3(const float* x, uint8_t* out, int64_t n, hipStream_t stream);
+
+}  // namespace pivot

@@ -1,0 +1,110 @@
+// Register-resident query rows and one 16-key MFMA step of the lightning-indexer
+// score (Sec. 3.1 Eq. 1; fp8 form of App. A):
+//
+//   S(row, s) = kscale[s] * sum_j (w[row, j] * qscale[row]) * ReLU(q[row, j] . k[s])
+//
+// Layout.  The inner products of R query rows x 64 heads against 16 keys form
+// a (64 R) x 16 matrix computed as 4R MFMA tiles of 16 (row, head) pairs x 16
+// keys, with K = d = 128 (one v_mfma_f32_16x16x128_f8f6f4, or four
+// v_mfma_f32_16x16x32_bf16).  The accumulator of a 16x16 MFMA puts tile rows
+// 4q .. 4q+3 in lane group q (lanes 16q .. 16q+15), key n in lane 16q + n.
+// Tile rows are assigned so that every lane group belongs to ONE query row:
+// with G = 4/R lane groups per row, tile j row 4q + i is head
+// 4G j + 4 (q mod G) + i of query row q / G.  Each lane therefore folds ReLU
+// and its gate into a running fp32 sum over its own heads with no cross-lane
+// traffic; only G > 1 needs log2(G) shuffles per 16 keys at the end.
+//
+// K split.  Lane l supplies dims 32 (l / 16) .. 32 (l / 16) + 31 of its A row
+// and of its B column.  Any assignment of dims to (lane group, register slot)
+// gives the same product as long as A and B use the same one.
+#pragma once
+
+#include "device_common.h"
+
+namespace pivot {
+
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+
+template <int DT>
+struct KeyFrag;
+
+template <>
+struct KeyFrag<kFp8> {
+  v8i v;  // 32 E4M3 codes
+  __device__ __forceinline__ void load(const uint8_t* key_row, int kg) {
+    const v4i* p = reinterpret_cast<const v4i*>(key_row + 32 * kg);
+    v4i lo = p[0], hi = p[1];
+    v = v8i{lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+  }
+};
+
+template <>
+struct KeyFrag<kBf16> {
+  v4i v[4];  // 4 x 8 bf16
+  __device__ __forceinline__ void load(const uint8_t* key_row, int kg) {
+    const v4i* p = reinterpret_cast<const v4i*>(key_row + 64 * kg);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) v[s] = p[s];
+  }
+};
+
+template <int DT, int R>
+struct RowTile {
+  static_assert(R == 1 || R == 2 || R == 4, "rows per wave");
+  static constexpr int G = 4 / R;        // lane groups per query row
+  static constexpr int T = 4 * R;        // MFMA tiles (16 (row, head) pairs each)
+  static constexpr int EB = DT == kFp8 ? 1 : 2;
+  static constexpr int ROW_BYTES = kH * kD * EB;
+
+  KeyFrag<DT> a[T];   // A operand, same register format as a key fragment
+  float wv[T][4];     // gate * query scale of this lane's (row, head) pairs
+
+  // rows[r]: the R query rows' codes; wrow[r]: gates; qscale[r]: per-row scale.
+  __device__ __forceinline__ void load(const uint8_t* const* rows, const float* const* wrow,
+                                       const float* qscale, int lane) {
+    const int lr = lane & 15, kg = lane >> 4;
+    const int gq_a = lr >> 2, i_a = lr & 3;
+    const uint8_t* arow = rows[gq_a / G];
+#pragma unroll
+    for (int j = 0; j < T; ++j) {
+      const int head = 4 * G * j + 4 * (gq_a % G) + i_a;
+      a[j].load(arow + (size_t)head * kD * EB, kg);
+    }
+    const int gq = kg;
+    const int qr = gq / G;
+    const float* wr = wrow[qr];
+    const float sc = qscale[qr];
+#pragma unroll
+    for (int j = 0; j < T; ++j)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) wv[j][i] = wr[4 * G * j + 4 * (gq % G) + i] * sc;
+  }
+
+  // Gate-weighted ReLU sum over all heads of row (lane >> 4) / G for key
+  // (lane & 15) of the fragment b; identical in every lane group of the row.
+  __device__ __forceinline__ float score(const KeyFrag<DT>& b) const {
+    float acc = 0.f;
+#pragma unroll
+    for (int j = 0; j < T; ++j) {
+      v4f c = {0.f, 0.f, 0.f, 0.f};
+      if constexpr (DT == kFp8) {
+        c = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a[j].v, b.v, c, 0, 0, 0, 0, 0, 0);
+      } else {
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+          c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(v8bf, a[j].v[s]),
+                                                      __builtin_bit_cast(v8bf, b.v[s]), c, 0, 0, 0);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc = fmaf(wv[j][i], fmaxf(c[i], 0.f), acc);
+    }
+    if constexpr (G >= 2) acc += __shfl_xor(acc, 16, kWave);
+    if constexpr (G >= 4) acc += __shfl_xor(acc, 32, kWave);
+    return acc;
+  }
+};
+
+}  // namespace pivot

@@ -1,0 +1,172 @@
+// Proxy aggregation (Sec. 4.2 Eq. 4): the per-head mean of a group's
+// dequantised queries and of its gates, stored back in the query format.
+//
+// One workgroup per group, 256 threads x 32 consecutive elements of the
+// 64 x 128 row.  Every step is rounded once in fp32, in a fixed order
+// (member-ascending sums, then one correctly rounded divide by |G|), with FMA
+// contraction disabled, so the result is reproducible bit for bit:
+//   fp8 : mean of (qscale_t * q8_t); scale = amax / 448; codes = RNE(mean / scale)
+//   bf16: mean of q_t; RNE to bf16
+// A group of one is copied unchanged.
+#include "launch.h"
+
+namespace pivot {
+
+// Four fp32 -> E4M3FN codes packed little-endian, round to nearest even
+// (gfx950 OCP conversion).
+__device__ __forceinline__ uint32_t encode_e4m3_quad(float a, float b, float c, float d) {
+  int word = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false);
+  return (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(c, d, word, true);
+}
+
+__device__ __forceinline__ float decode_e4m3(uint32_t word, int byte) {
+  // byte is a compile-time constant after unrolling
+  switch (byte) {
+    case 0: return __builtin_amdgcn_cvt_f32_fp8((int)word, 0);
+    case 1: return __builtin_amdgcn_cvt_f32_fp8((int)word, 1);
+    case 2: return __builtin_amdgcn_cvt_f32_fp8((int)word, 2);
+    default: return __builtin_amdgcn_cvt_f32_fp8((int)word, 3);
+  }
+}
+
+__device__ __forceinline__ uint16_t bf16_rne(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+template <int DT>
+__global__ __launch_bounds__(256) void proxy_kernel(const uint8_t* __restrict__ q,
+                                                    const float* __restrict__ q_scale,
+                                                    const float* __restrict__ w, int n_q, int g, int n_groups,
+                                                    SeqTable st, int j0, int all_groups,
+                                                    uint8_t* __restrict__ pq, float* __restrict__ psc,
+                                                    float* __restrict__ pw) {
+#pragma clang fp contract(off)
+  constexpr int EB = DT == kFp8 ? 1 : 2;
+  constexpr int ROW_BYTES = kH * kD * EB;
+  constexpr int PER = 32;  // elements per thread
+  const int j = j0 + blockIdx.x, b = blockIdx.y;
+  if (b >= st.n || j >= n_groups) return;
+  if (!all_groups && j < st.first_proxy[b]) return;
+  const int gs = min(g, n_q - j * g);
+  const int64_t r0 = (int64_t)b * n_q + (int64_t)j * g;
+  const int64_t pr = (int64_t)b * n_groups + j;
+  const int tid = threadIdx.x;
+  const int e0 = tid * PER;
+
+  if (gs == 1) {
+    const uint4* src = reinterpret_cast<const uint4*>(q + r0 * ROW_BYTES + e0 * EB);
+    uint4* dst = reinterpret_cast<uint4*>(pq + pr * ROW_BYTES + e0 * EB);
+#pragma unroll
+    for (int v = 0; v < PER * EB / 16; ++v) dst[v] = src[v];
+    if (tid == 0) psc[pr] = (DT == kFp8) ? q_scale[r0] : 1.0f;
+    if (tid < kH) pw[pr * kH + tid] = w[r0 * kH + tid];
+    return;
+  }
+
+  float sum[PER];
+#pragma unroll
+  for (int e = 0; e < PER; ++e) sum[e] = 0.0f;
+  for (int u = 0; u < gs; ++u) {
+    const uint4* src = reinterpret_cast<const uint4*>(q + (r0 + u) * ROW_BYTES + e0 * EB);
+    if constexpr (DT == kFp8) {
+      const float sq = q_scale[r0 + u];
+      uint4 v0 = src[0], v1 = src[1];
+      uint32_t words[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+#pragma unroll
+      for (int e = 0; e < PER; ++e) {
+        float x = decode_e4m3(words[e >> 2], e & 3);
+        float deq = sq * x;
+        sum[e] = sum[e] + deq;
+      }
+    } else {
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        uint4 pkt = src[v];
+        uint32_t words[4] = {pkt.x, pkt.y, pkt.z, pkt.w};
+#pragma unroll
+        for (int h = 0; h < 4; ++h) {
+          sum[8 * v + 2 * h] = sum[8 * v + 2 * h] + __uint_as_float(words[h] << 16);
+          sum[8 * v + 2 * h + 1] = sum[8 * v + 2 * h + 1] + __uint_as_float(words[h] & 0xFFFF0000u);
+        }
+      }
+    }
+  }
+  const float count = (float)gs;
+  float amax = 0.0f;
+#pragma unroll
+  for (int e = 0; e < PER; ++e) {
+    sum[e] = sum[e] / count;  // correctly rounded fp32 divide
+    amax = fmaxf(amax, fabsf(sum[e]));
+  }
+
+  if (tid < kH) {
+    float s = 0.0f;
+    for (int u = 0; u < gs; ++u) s = s + w[(r0 + u) * kH + tid];
+    pw[pr * kH + tid] = s / count;
+  }
+
+  if constexpr (DT == kFp8) {
+    __shared__ float wmax[4];
+    amax = wave_max(amax);
+    if ((tid & 63) == 0) wmax[tid >> 6] = amax;
+    __syncthreads();
+    amax = fmaxf(fmaxf(wmax[0], wmax[1]), fmaxf(wmax[2], wmax[3]));
+    const float sigma = amax > 0.0f ? amax / 448.0f : 1.0f;
+    uint32_t out[8];
+#pragma unroll
+    for (int v = 0; v < 8; ++v) {
+      out[v] = encode_e4m3_quad(sum[4 * v] / sigma, sum[4 * v + 1] / sigma, sum[4 * v + 2] / sigma,
+                                sum[4 * v + 3] / sigma);
+    }
+    uint4* dst = reinterpret_cast<uint4*>(pq + pr * ROW_BYTES + e0);
+    dst[0] = uint4{out[0], out[1], out[2], out[3]};
+    dst[1] = uint4{out[4], out[5], out[6], out[7]};
+    if (tid == 0) psc[pr] = sigma;
+  } else {
+    uint32_t out[16];
+#pragma unroll
+    for (int v = 0; v < 16; ++v) out[v] = (uint32_t)bf16_rne(sum[2 * v]) | ((uint32_t)bf16_rne(sum[2 * v + 1]) << 16);
+    uint4* dst = reinterpret_cast<uint4*>(pq + pr * ROW_BYTES + e0 * 2);
+#pragma unroll
+    for (int v = 0; v < 4; ++v) dst[v] = uint4{out[4 * v], out[4 * v + 1], out[4 * v + 2], out[4 * v + 3]};
+    if (tid == 0) psc[pr] = 1.0f;
+  }
+}
+
+hipError_t launch_proxy(int dtype, const void* q, const float* q_scale, const float* w, int n_q, int g,
+                        int n_groups, const SeqTable& st, int j0, int j1, bool all_groups, void* pq,
+                        float* psc, float* pw, hipStream_t stream) {
+  if (j1 <= j0 || st.n <= 0) return hipSuccess;
+  dim3 grid((unsigned)(j1 - j0), (unsigned)st.n);
+  if (dtype == kFp8)
+    hipLaunchKernelGGL(proxy_kernel<kFp8>, grid, dim3(256), 0, stream, (const uint8_t*)q, q_scale, w, n_q, g,
+                       n_groups, st, j0, (int)all_groups, (uint8_t*)pq, psc, pw);
+  else
+    hipLaunchKernelGGL(proxy_kernel<kBf16>, grid, dim3(256), 0, stream, (const uint8_t*)q, q_scale, w, n_q, g,
+                       n_groups, st, j0, (int)all_groups, (uint8_t*)pq, psc, pw);
+  return hipGetLastError();
+}
+
+__global__ __launch_bounds__(256) void encode_e4m3_kernel(const float* __restrict__ x, uint8_t* __restrict__ out,
+                                                          int64_t n) {
+  int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (i >= n) return;
+  float v[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) v[e] = (i + e < n) ? x[i + e] : 0.0f;
+  uint32_t word = encode_e4m3_quad(v[0], v[1], v[2], v[3]);
+#pragma unroll
+  for (int e = 0; e < 4; ++e)
+    if (i + e < n) out[i + e] = (uint8_t)(word >> (8 * e));
+}
+
+hipError_t launch_encode_e4m3(const float* x, uint8_t* out, int64_t n, hipStream_t stream) {
+  if (n <= 0) return hipSuccess;
+  int64_t blocks = (n + 1023) / 1024;
+  hipLaunchKernelGGL(encode_e4m3_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, x, out, n);
+  return hipGetLastError();
+}
+
+}  // namespace pivot

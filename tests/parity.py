@@ -1,0 +1,111 @@
+"""Parity rule between a GPU index set and the oracle's.
+
+For one output row with oracle set O (top-m of the oracle scores f over a
+domain D) and GPU set G, both padded with -1:
+  * same number of -1 entries, no duplicates, G within D;
+  * with tau = the oracle score of O's m-th element (its minimum) and
+    tol = rtol * |tau|: every s in G \\ O has f(s) >= tau - tol and every s in
+    O \\ G has f(s) <= tau + tol.
+rtol is 2e-3 for bf16 inputs and 2e-2 for fp8 inputs (scores compared with the
+fp64 oracle).  Scores are only computed for rows whose sets differ.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+RTOL = {"bf16": 2e-3, "fp8": 2e-2}
+
+
+class ParityError(AssertionError):
+    pass
+
+
+def check_row(gpu, ora, f_of, rtol, in_domain, label=""):
+    """gpu, ora: int arrays (-1 padded); f_of(idx array) -> oracle fp64 scores;
+    in_domain(idx array) -> bool array.  Returns the number of boundary swaps."""
+    gpu = np.asarray(gpu)
+    ora = np.asarray(ora)
+    G = gpu[gpu >= 0]
+    O = ora[ora >= 0]
+    if (gpu < -1).any():
+        raise ParityError(f"{label}: invalid entries {gpu[gpu < -1][:5]}")
+    if len(np.unique(G)) != len(G):
+        raise ParityError(f"{label}: duplicate indices")
+    if (gpu == -1).sum() != (ora == -1).sum():
+        raise ParityError(f"{label}: {(gpu == -1).sum()} pads vs oracle {(ora == -1).sum()}")
+    if len(G) and not in_domain(G).all():
+        raise ParityError(f"{label}: indices outside the domain: {G[~in_domain(G)][:5]}")
+    sg, so = set(G.tolist()), set(O.tolist())
+    if sg == so:
+        return 0
+    extra = np.array(sorted(sg - so), dtype=np.int64)
+    missing = np.array(sorted(so - sg), dtype=np.int64)
+    tau = float(f_of(O).min())
+    tol = rtol * abs(tau)
+    fe = f_of(extra)
+    fm = f_of(missing)
+    if (fe < tau - tol).any() or (fm > tau + tol).any():
+        raise ParityError(f"{label}: tau={tau:.6g} tol={tol:.3g}; extra f={np.sort(fe)[:4]}, "
+                          f"missing f={np.sort(fm)[-4:]}")
+    return len(extra)
+
+
+def check_pivot(fmt, q, qs, w, p0, k, ks, n_k, *, mode, g, c, topk, dense_below, gpu_idx,
+                gpu_cand=None, groups=None, label=""):
+    """Check one sequence's GPU result against the oracle (Algorithm 1).
+
+    q / qs / w: the call's n_q query rows (numpy); k / ks: the sequence's keys.
+    mode: oracle.DENSE / REUSE / REFINE.  Refine needs gpu_cand ([n_groups, c])
+    for the two-stage check: (1) the candidate set against the oracle's proxy
+    top-c, (2) each member's set against the oracle's Refine run on the GPU's
+    own candidates.  Returns the number of boundary swaps accepted."""
+    import oracle
+
+    rtol = RTOL[fmt]
+    n_q = q.shape[0]
+    if mode == oracle.DENSE:
+        g, db = 1, n_k + 1
+    else:
+        db = c if dense_below < 0 else dense_below
+    res = oracle.index(fmt, q, qs, w, p0, k, ks, n_k, mode=mode, g=g, c=c, topk=topk,
+                       dense_below=(0 if mode == oracle.DENSE else db), groups=groups,
+                       want_cand=(mode == oracle.REFINE), want_proxy=(mode != oracle.DENSE))
+    n_groups = (n_q + g - 1) // g
+    sel = range(n_groups) if groups is None else groups
+    swaps = 0
+
+    def member_scores(r):
+        return lambda idx: oracle.scores_at(fmt, q[r], 1.0 if qs is None else qs[r], w[r], k, ks, idx)
+
+    for j in sel:
+        t0 = p0 + j * g
+        gs = min(g, n_q - j * g)
+        rows = list(range(j * g, j * g + gs))
+        if mode == oracle.DENSE or t0 < db:
+            for r in rows:
+                t = p0 + r
+                swaps += check_row(gpu_idx[r], res["idx"][r], member_scores(r), rtol,
+                                   lambda idx, t=t: (idx >= 0) & (idx <= t), f"{label} dense row {r}")
+            if mode == oracle.REFINE and gpu_cand is not None:
+                if not (gpu_cand[j] == -1).all():
+                    raise ParityError(f"{label}: guardrail group {j} has candidates")
+            continue
+        pq, psc, pw = res["pq"][j], res["psc"][j], res["pw"][j]
+
+        def fbar(idx, pq=pq, psc=psc, pw=pw):
+            return oracle.scores_at(fmt, pq, psc, pw, k, ks, idx)
+
+        def dom0(idx, t0=t0):
+            return (idx >= 0) & (idx <= t0)
+
+        if mode == oracle.REUSE:
+            for r in rows:
+                swaps += check_row(gpu_idx[r], res["idx"][r], fbar, rtol, dom0, f"{label} reuse row {r}")
+            continue
+        swaps += check_row(gpu_cand[j], res["cand"][j], fbar, rtol, dom0, f"{label} candidates of group {j}")
+        C = gpu_cand[j][gpu_cand[j] >= 0]
+        ref2 = oracle.refine_on(fmt, q[rows], None if qs is None else qs[rows], w[rows], k, ks, C, topk)
+        for u, r in enumerate(rows):
+            swaps += check_row(gpu_idx[r], ref2[u], member_scores(r), rtol,
+                               lambda idx, C=C: np.isin(idx, C), f"{label} refine row {r}")
+    return swaps

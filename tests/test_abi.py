@@ -1,0 +1,170 @@
+"""C ABI of libpivot.so on the CPU: the library loads, exports every function
+include/pivot.h declares, and rejects bad arguments with the documented status
+before launching anything (no call here reaches a kernel)."""
+import ctypes
+import os
+import re
+
+import pytest
+import torch
+
+import paper_2607_24593_amd as pv
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "pivot.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(pv.LIB_PATH), reason="libpivot.so not built")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^[A-Za-z_][\w\s\*]*?\b(pivot_\w+)\s*\(", text, flags=re.M)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert len(names) >= 10, names
+    L = pv.lib()
+    for n in names:
+        assert hasattr(L, n), n
+    assert sorted(names) == sorted(pv.EXPORTED)
+
+
+def test_status_strings_and_version():
+    assert pv.status_string(0) == "ok"
+    assert "workspace" in pv.status_string(3)
+    assert pv.status_string(99) == "unknown status"
+    assert pv.version().startswith("pivot-gfx950")
+
+
+FAKE = 1 << 40  # a non-null address the library must never dereference before launching
+
+
+def args(dtype=pv.PIVOT_DT_FP8_E4M3, B=1, n_q=64, q_pos0=0, n_k=None, topk=8, heads=64, dim=128,
+         scales=True, ws_bytes=0, ws_addr=FAKE):
+    a = pv.pivot_args()
+    a.dtype, a.heads, a.dim, a.batch, a.n_q = dtype, heads, dim, B, n_q
+    pos = [q_pos0] * max(B, 1)
+    nk = [q_pos0 + n_q if n_k is None else n_k] * max(B, 1)
+    a._pos = (ctypes.c_int32 * len(pos))(*pos)
+    a._nk = (ctypes.c_int32 * len(nk))(*nk)
+    a.q_pos0 = ctypes.cast(a._pos, ctypes.POINTER(ctypes.c_int32))
+    a.n_k = ctypes.cast(a._nk, ctypes.POINTER(ctypes.c_int32))
+    a.q = a.w = a.k = a.out_idx = FAKE
+    a.q_scale = a.k_scale = FAKE if scales else None
+    a.k_seq_stride = max(nk + [0])
+    a.topk = topk
+    a.workspace = ws_addr
+    a.workspace_bytes = ws_bytes
+    a.stream = None
+    return a
+
+
+def dense(a):
+    return pv.lib().pivot_dense_index(ctypes.byref(a))
+
+
+def group(a, mode=pv.PIVOT_REFINE, g=4, c=16, db=-1):
+    return pv.lib().pivot_group_index(ctypes.byref(a), mode, g, c, db, None)
+
+
+def test_null_args():
+    assert pv.lib().pivot_dense_index(None) == pv.PIVOT_ERR_INVALID_ARG
+    assert pv.lib().pivot_workspace_size(None, -1, 1, 0) == 0
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(heads=32), pv.PIVOT_ERR_UNSUPPORTED),
+    (dict(dim=64), pv.PIVOT_ERR_UNSUPPORTED),
+    (dict(dtype=5), pv.PIVOT_ERR_UNSUPPORTED),
+    (dict(topk=0), pv.PIVOT_ERR_INVALID_ARG),
+    (dict(n_q=-1), pv.PIVOT_ERR_INVALID_ARG),
+    (dict(B=0), pv.PIVOT_ERR_INVALID_ARG),
+    (dict(q_pos0=10, n_k=70), pv.PIVOT_ERR_INVALID_ARG),      # n_k < q_pos0 + n_q
+    (dict(q_pos0=-3), pv.PIVOT_ERR_INVALID_ARG),
+    (dict(scales=False), pv.PIVOT_ERR_INVALID_ARG),          # fp8 without scales
+])
+def test_dense_validation(kw, status):
+    a = args(**kw)
+    assert dense(a) == status
+    assert pv.last_error() != ""
+
+
+def test_missing_pointer():
+    a = args()
+    a.k = None
+    assert dense(a) == pv.PIVOT_ERR_INVALID_ARG
+
+
+def test_bf16_needs_no_scales():
+    a = args(dtype=pv.PIVOT_DT_BF16, scales=False, ws_bytes=0)
+    assert dense(a) == pv.PIVOT_ERR_WORKSPACE  # passes validation, stops at the workspace check
+
+
+@pytest.mark.parametrize("mode,g,c,status", [
+    (pv.PIVOT_REFINE, 0, 16, pv.PIVOT_ERR_INVALID_ARG),
+    (pv.PIVOT_REFINE, 4, 4, pv.PIVOT_ERR_INVALID_ARG),        # c < k
+    (pv.PIVOT_REFINE, 4, 16384, pv.PIVOT_ERR_UNSUPPORTED),    # c beyond the LDS budget
+    (7, 4, 16, pv.PIVOT_ERR_INVALID_ARG),
+    (pv.PIVOT_REUSE, 4, -1, pv.PIVOT_ERR_INVALID_ARG),
+])
+def test_group_validation(mode, g, c, status):
+    assert group(args(), mode, g, c) == status
+
+
+def test_workspace_checks():
+    a = args(ws_bytes=0)
+    assert dense(a) == pv.PIVOT_ERR_WORKSPACE
+    need = pv.pivot_workspace_size(a, pv.PIVOT_DENSE)
+    assert need > 0
+    a = args(ws_bytes=need, ws_addr=FAKE + 4)
+    assert dense(a) == pv.PIVOT_ERR_INVALID_ARG                # misaligned
+    a = args(ws_bytes=need // 8)
+    assert dense(a) == pv.PIVOT_ERR_WORKSPACE
+    a = args(ws_bytes=need, ws_addr=None)
+    assert dense(a) == pv.PIVOT_ERR_WORKSPACE
+
+
+def test_empty_call_is_ok_without_workspace():
+    a = args(n_q=0, q_pos0=5, n_k=5, ws_bytes=0, ws_addr=None)
+    assert dense(a) == pv.PIVOT_OK
+    assert group(a) == pv.PIVOT_OK
+
+
+def test_workspace_size_closed_form():
+    # dense, one sequence: 100 rows x ld(1000)=1024 fp32
+    a = args(n_q=100, q_pos0=900)
+    assert pv.pivot_workspace_size(a, pv.PIVOT_DENSE) == 100 * 1024 * 4
+    # Refine, g=4, c=16, guardrail at c: all 25 groups start at t0 >= 900 >= c
+    ng = 25
+    fixed = 0
+    for nbytes in (ng * 64 * 128, ng * 4, ng * 64 * 4, ng * 16 * 4):
+        fixed += (nbytes + 255) // 256 * 256
+    assert pv.pivot_workspace_size(a, pv.PIVOT_REFINE, 4, 16) == fixed + ng * 1024 * 4
+    # Reuse needs no candidate buffer
+    fixed_r = fixed - (ng * 16 * 4 + 255) // 256 * 256
+    assert pv.pivot_workspace_size(a, pv.PIVOT_REUSE, 4, 16) == fixed_r + ng * 1024 * 4
+    # long prefix: score tiles stay near 1 GiB
+    a = args(n_q=16384, q_pos0=262144 - 16384)
+    assert pv.pivot_workspace_size(a, pv.PIVOT_DENSE) == 1 << 30
+
+
+def test_stage_validation():
+    L = pv.lib()
+    assert L.pivot_score_rows(1, 64, 128, 4, FAKE, FAKE, FAKE, FAKE, FAKE, 10, 1, FAKE, 5, None) == \
+        pv.PIVOT_ERR_INVALID_ARG                               # ld < lim + 1
+    assert L.pivot_score_rows(1, 32, 128, 4, FAKE, FAKE, FAKE, FAKE, FAKE, 10, 1, FAKE, 64, None) == \
+        pv.PIVOT_ERR_UNSUPPORTED
+    assert L.pivot_topk_rows(2, FAKE, 10, 8, 4, 4, FAKE, None) == pv.PIVOT_ERR_INVALID_ARG  # 12 > ld
+    assert L.pivot_topk_rows(0, None, 0, 0, 0, 4, None, None) == pv.PIVOT_OK
+    assert L.pivot_proxy_rows(1, 64, 128, 8, 0, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == \
+        pv.PIVOT_ERR_INVALID_ARG
+    assert L.pivot_encode_e4m3(None, None, 0, None) == pv.PIVOT_OK
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(pv, "LIB_PATH", str(tmp_path / "missing.so"))
+    monkeypatch.setattr(pv, "_lib", None)
+    with pytest.raises(RuntimeError, match="HIP library missing"):
+        pv.lib()

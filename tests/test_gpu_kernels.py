@@ -1,0 +1,99 @@
+"""Per-kernel GPU tests through the C ABI stage entry points."""
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2607_24593_amd as pv
+from gpu_util import dev, host, say
+from workload.gen import make_prefill
+
+pytestmark = pytest.mark.gpu
+
+
+def test_encode_e4m3_matches_oracle_rne():
+    vals = np.array([oracle.e4m3_decode(c) for c in range(0x7F)])
+    mids = (vals[:-1] + vals[1:]) / 2
+    rng = np.random.default_rng(1)
+    x = np.concatenate([vals, -vals, mids, -mids, rng.uniform(-448, 448, 50000),
+                        rng.normal(0, 0.01, 50000), [0.0, -0.0]]).astype(np.float32)
+    say("encode_e4m3", x.size)
+    got = host(pv.pivot_encode_e4m3(dev(x)))
+    ref = np.array([oracle.e4m3_encode(float(v)) for v in x], dtype=np.uint8)
+    bad = np.nonzero(got != ref)[0]
+    assert bad.size == 0, [(float(x[i]), int(got[i]), int(ref[i])) for i in bad[:8]]
+
+
+@pytest.mark.parametrize("fmt", ["fp8", "bf16"])
+@pytest.mark.parametrize("g", [1, 2, 3, 4, 8])
+def test_proxy_rows_bit_exact(fmt, g):
+    x = make_prefill(37, fmt, seed=100 + g, threads=1)
+    say("proxy_rows", fmt, "g", g)
+    pq, ps, pw = pv.pivot_proxy_rows(dev(x.q), dev(x.q_scale), dev(x.w), g)
+    pq, ps, pw = host(pq), host(ps), host(pw)
+    if fmt == "bf16":
+        pq = pq.view(np.uint16)
+    for j in range((37 + g - 1) // g):
+        rows = slice(j * g, min(37, (j + 1) * g))
+        oq, osc, ow = oracle.proxy(fmt, x.q[rows], None if x.q_scale is None else x.q_scale[rows], x.w[rows])
+        assert np.array_equal(pq[j], oq), (j, np.nonzero(pq[j] != oq))
+        assert ps[j] == np.float32(osc), j
+        assert np.array_equal(pw[j], ow), j
+
+
+@pytest.mark.parametrize("fmt", ["fp8", "bf16"])
+@pytest.mark.parametrize("n_rows,lim0,step", [(1, 5000, 0), (2, 4999, 1), (3, 700, 7), (5, 33, 2),
+                                              (16, 4100, 1), (40, 8300, 3), (64, 0, 130)])
+def test_score_rows_match_oracle(fmt, n_rows, lim0, step):
+    lim_max = lim0 + (n_rows - 1) * step
+    L = lim_max + 1
+    x = make_prefill(max(L, n_rows), fmt, seed=7, threads=4)
+    q, qs, w = x.q[:n_rows], None if x.q_scale is None else x.q_scale[:n_rows], x.w[:n_rows]
+    ld = lim_max + 1 + 13
+    say("score_rows", fmt, n_rows, lim0, step)
+    got = host(pv.pivot_score_rows(dev(q), dev(qs), dev(w), dev(x.k), dev(x.k_scale), lim0, step, ld=ld))
+    for r in range(n_rows):
+        lim = lim0 + r * step
+        f = oracle.scores(fmt, q[r], 1.0 if qs is None else qs[r], w[r], x.k, x.k_scale, lim)
+        scale = np.abs(f).max() + 1e-30
+        err = np.abs(got[r, :lim + 1] - f).max() / scale
+        assert err < 1e-4, (r, err)
+        assert np.isnan(got[r, lim + 1:]).all(), r   # nothing written past the row's limit
+
+
+def _expect_topk(row, n, m):
+    return oracle.topk(row[:n].astype(np.float64), np.arange(n, dtype=np.int32), m)
+
+
+@pytest.mark.parametrize("case", ["normal", "ties", "signed_zeros", "short", "exact", "long2k", "long4k",
+                                  "ragged", "constant"])
+def test_topk_rows_exact(case):
+    rng = np.random.default_rng(zlib.crc32(case.encode()))
+    n0, step, m = 5000, 0, 100
+    if case == "normal":
+        rows = rng.standard_normal((6, 5000))
+    elif case == "ties":
+        rows = rng.integers(0, 10, (6, 5000)).astype(np.float64)
+    elif case == "signed_zeros":
+        rows = rng.choice([-0.0, 0.0, 1.0, -1.0, 2.0], size=(3, 40000)); n0 = 40000
+    elif case == "short":
+        rows = rng.standard_normal((4, 64)); n0, m = 50, 100
+    elif case == "exact":
+        rows = rng.standard_normal((3, 100)); n0, m = 100, 100
+    elif case == "long2k":
+        rows = rng.standard_normal((2, 262144)); n0, m = 262144, 2048
+    elif case == "long4k":
+        rows = np.exp(rng.standard_normal((2, 131072)) * 3); n0, m = 131072, 4096
+    elif case == "ragged":
+        rows = rng.standard_normal((40, 3000)); n0, step, m = 17, 70, 64
+    else:
+        rows = np.full((2, 20000), 3.5); n0, m = 20000, 700
+    rows = rows.astype(np.float32)
+    say("topk_rows", case, rows.shape, n0, step, m)
+    got = host(pv.pivot_topk_rows(dev(rows), n0, step, m))
+    for r in range(rows.shape[0]):
+        n = n0 + r * step
+        exp = _expect_topk(rows[r], n, m)
+        assert sorted(got[r].tolist()) == sorted(exp.tolist()), (case, r)

@@ -1,0 +1,151 @@
+"""End-to-end GPU parity of pivot_dense_index / pivot_group_index with the
+oracle (Algorithm 1), on inputs small enough for the oracle, spanning several
+score segments and top-k tiles, with ragged groups, chunked calls, the
+guardrail on and off, and batched decode groups."""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2607_24593_amd as pv
+from gpu_util import dev, host, say
+from parity import check_pivot
+from workload.gen import make_decode, make_prefill
+
+pytestmark = pytest.mark.gpu
+
+MODES = {"dense": oracle.DENSE, "reuse": oracle.REUSE, "refine": oracle.REFINE}
+PV_MODE = {"reuse": pv.PIVOT_REUSE, "refine": pv.PIVOT_REFINE}
+
+
+def run_gpu(x, mode, p0, n_q, topk, g=1, c=0, dense_below=-1):
+    q = x.q[p0:p0 + n_q]
+    qs = None if x.q_scale is None else x.q_scale[p0:p0 + n_q]
+    w = x.w[p0:p0 + n_q]
+    n_k = p0 + n_q
+    say(mode, x.dtype, "p0", p0, "n_q", n_q, "topk", topk, "g", g, "c", c, "db", dense_below)
+    args = (dev(q), dev(qs), dev(w), dev(x.k[:n_k]), dev(None if x.k_scale is None else x.k_scale[:n_k]), p0, n_k, topk)
+    cand = None
+    if mode == "dense":
+        idx = pv.pivot_dense_index(*args)
+    else:
+        ng = (n_q + g - 1) // g
+        cand_t = None
+        if mode == "refine":
+            import torch
+            cand_t = torch.full((1, ng, c), -7, dtype=torch.int32, device="cuda")
+        idx = pv.pivot_group_index(*args, mode=PV_MODE[mode], g=g, c=c, dense_below=dense_below, out_cand=cand_t)
+        cand = None if cand_t is None else host(cand_t)[0]
+    return host(idx), cand, (q, qs, w, n_k)
+
+
+def check(x, mode, p0, n_q, topk, g=1, c=0, dense_below=-1, groups=None, label=""):
+    idx, cand, (q, qs, w, n_k) = run_gpu(x, mode, p0, n_q, topk, g, c, dense_below)
+    if groups is not None:
+        keep = np.zeros(n_q, bool)
+        for j in groups:
+            keep[j * g:(j + 1) * g] = True
+    return check_pivot(x.dtype, q, qs, w, p0, x.k[:n_k], None if x.k_scale is None else x.k_scale[:n_k], n_k,
+                       mode=MODES[mode], g=g, c=c, topk=topk, dense_below=dense_below, gpu_idx=idx,
+                       gpu_cand=cand, groups=groups, label=label)
+
+
+@pytest.fixture(scope="module")
+def small_bf16():
+    return make_prefill(1100, "bf16", seed=31, threads=4)
+
+
+@pytest.fixture(scope="module")
+def long_fp8():
+    return make_prefill(9000, "fp8", seed=32, threads=8)
+
+
+@pytest.mark.parametrize("mode", ["dense", "reuse", "refine"])
+def test_bf16_every_query(small_bf16, mode):
+    """Every query of a 1100-position bf16 prefill (ragged last group, g=4)."""
+    check(small_bf16, mode, 0, 1099, 64, g=4, c=256, label=f"bf16 {mode}")
+
+
+def _sample_groups(n_q, g, p0, c, rng, extra=()):
+    ng = (n_q + g - 1) // g
+    pick = {0, 1, ng - 1, ng - 2} | set(int(v) for v in rng.integers(0, ng, 12))
+    for t in (c - g, c, c + g) + tuple(extra):      # around the guardrail and segment edges
+        j = (t - p0) // g
+        if 0 <= j < ng:
+            pick.add(j)
+    return sorted(pick)
+
+
+@pytest.mark.parametrize("mode", ["dense", "reuse", "refine"])
+@pytest.mark.parametrize("g", [2, 4, 8])
+def test_fp8_sampled_groups(long_fp8, mode, g):
+    """fp8, 8999 queries (segments of 4096 keys, ragged tail), sampled groups."""
+    rng = np.random.default_rng(g)
+    n_q = 8999
+    groups = _sample_groups(n_q, g if mode != "dense" else 1, 0, 1024, rng, extra=(4095, 4096, 8191, 8192))
+    check(long_fp8, mode, 0, n_q, 256, g=g if mode != "dense" else 1, c=1024, groups=groups,
+          label=f"fp8 {mode} g{g}")
+
+
+@pytest.mark.parametrize("mode", ["reuse", "refine"])
+def test_fp8_chunk_with_offset(long_fp8, mode):
+    """A later chunk of a prefill: queries 5120 .. 8999 against keys 0 .. 8999."""
+    rng = np.random.default_rng(5)
+    p0, n_q, g = 5120, 3880, 4
+    groups = _sample_groups(n_q, g, p0, 1024, rng)
+    check(long_fp8, mode, p0, n_q, 256, g=g, c=1024, groups=groups, label=f"chunk {mode}")
+
+
+@pytest.mark.parametrize("dense_below", [0, 3000])
+def test_guardrail_threshold(long_fp8, dense_below):
+    """Guardrail disabled (every group on the proxy path, also t0 < c, where the
+    candidate set is the whole prefix) and set above c."""
+    rng = np.random.default_rng(9)
+    n_q, g = 4000, 4
+    groups = _sample_groups(n_q, g, 0, 1024, rng, extra=(0, 4, 8, 300, 2996, 3000))
+    check(long_fp8, "refine", 0, n_q, 128, g=g, c=1024, dense_below=dense_below, groups=groups,
+          label=f"db {dense_below}")
+    check(long_fp8, "reuse", 0, n_q, 128, g=g, c=1024, dense_below=dense_below, groups=groups,
+          label=f"db {dense_below}")
+
+
+def test_group_of_one_equals_dense(long_fp8):
+    """App. A identity on the GPU: g = 1 Reuse and Refine give the dense sets."""
+    p0, n_q = 3000, 64
+    d, _, _ = run_gpu(long_fp8, "dense", p0, n_q, 100)
+    for mode in ("reuse", "refine"):
+        r, _, _ = run_gpu(long_fp8, mode, p0, n_q, 100, g=1, c=200, dense_below=0)
+        assert np.array_equal(np.sort(r, 1), np.sort(d, 1)), mode
+
+
+@pytest.mark.parametrize("g", [2, 4])
+@pytest.mark.parametrize("mode", ["dense", "reuse", "refine"])
+def test_decode_batch(mode, g):
+    """Decode: B sequences, each one MTP group of g queries at the end of its context."""
+    B, L = 6, 5000
+    x = make_decode(B, L, g, "fp8", seed=40 + g, threads=6)
+    import torch
+    say("decode", mode, "B", B, "L", L, "g", g)
+    q, qs, w = dev(x.q), dev(x.q_scale), dev(x.w)
+    k, ks = dev(x.k), dev(x.k_scale)
+    topk, c = 256, 1024
+    if mode == "dense":
+        idx = pv.pivot_dense_index(q, qs, w, k, ks, [L - g] * B, [L] * B, topk)
+        cand = None
+    else:
+        cand_t = torch.full((B, 1, c), -7, dtype=torch.int32, device="cuda") if mode == "refine" else None
+        idx = pv.pivot_group_index(q, qs, w, k, ks, [L - g] * B, [L] * B, topk, mode=PV_MODE[mode], g=g, c=c,
+                                   out_cand=cand_t)
+        cand = None if cand_t is None else host(cand_t)
+    idx = host(idx)
+    for b in range(B):
+        check_pivot("fp8", x.q[b], x.q_scale[b], x.w[b], L - g, x.k[b], x.k_scale[b], L, mode=MODES[mode], g=g,
+                    c=c, topk=topk, dense_below=-1, gpu_idx=idx[b], gpu_cand=None if cand is None else cand[b],
+                    label=f"decode b{b}")
+
+
+def test_repeatable(long_fp8):
+    """Same inputs, same indices (fixed tie-breaks, no order dependence)."""
+    a, ca, _ = run_gpu(long_fp8, "refine", 4000, 2000, 256, g=4, c=1024)
+    b, cb, _ = run_gpu(long_fp8, "refine", 4000, 2000, 256, g=4, c=1024)
+    assert np.array_equal(np.sort(a, 1), np.sort(b, 1))
+    assert np.array_equal(np.sort(ca, 1), np.sort(cb, 1))
