@@ -1,0 +1,302 @@
+#!/usr/bin/env python
+"""Benchmark of the PIVOT indexer hot path on one MI355X (gfx950).
+
+One step = one PIVOT-Refine pass (g=4, c=4096, k=2048) over a whole 131072-token
+fp8 prefill, issued as 16 calls of 8192 queries against their full causal
+prefix: grouping and guardrail planning, proxy aggregation, proxy scan, proxy
+top-c, and the per-member gather / re-score / top-k.  Inputs are synthetic
+(workload.gen, the 128K prefill recipe) and resident in HBM before timing.
+
+Reported besides the headline queries/s: the dense indexer and PIVOT-Reuse on
+the same prefill (speedup), a group-size sweep, MTP decode (32 x 131072 cached
+keys, g=2), per-kernel times from HIP events recorded around each launch
+inside the timed steps, the roofline fraction of the dominant kernel, and the
+CPU oracle timed on a sample of the same workload.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK = {"fp8": 5000.0, "bf16": 2500.0}  # dense MFMA TFLOP/s (MI355X)
+HBM_PEAK = 8000.0                        # GB/s
+FLOP_PER_PAIR = 2 * 64 * 128             # one (row, key) score: 64 heads x 128-dim dot
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+# ---------------------------------------------------------------- accounting
+def plan_chunk(p0, n_q, g, c, mode):
+    """Rows of one call as the library plans them (Algorithm 1 guardrail at c)."""
+    ng = (n_q + g - 1) // g
+    if mode == "dense":
+        return n_q, []
+    gap = c - p0
+    J = 0 if gap <= 0 else min(-(-gap // g), ng)
+    dense_rows = min(J * g, n_q)
+    proxies = [(p0 + j * g, min(g, n_q - j * g)) for j in range(J, ng)]
+    return dense_rows, proxies
+
+
+def units(chunks, mode, g, c, topk, eb_q=1, eb_k=1):
+    """Algorithmic work per pass: score pairs, select bytes, refine bytes and flops, proxy bytes."""
+    row_q = 64 * 128 * eb_q + 4 + 4 * 64
+    pairs = sel_bytes = ref_bytes = ref_flops = prox_bytes = 0
+    for p0, n_q in chunks:
+        dense_rows, proxies = plan_chunk(p0, n_q, g, c, mode)
+        dp = sum(p0 + i + 1 for i in range(dense_rows))
+        pairs += dp
+        sel_bytes += 4 * dp + 4 * topk * dense_rows
+        for t0, gs in proxies:
+            n = t0 + 1
+            pairs += n
+            m = topk if mode == "reuse" else c
+            fan = gs if mode == "reuse" else 1
+            sel_bytes += 4 * n + 4 * min(m, n) * fan
+            prox_bytes += (gs + 1) * row_q if gs > 1 else 0
+            if mode == "refine":
+                nc = min(c, n)
+                ref_bytes += nc * (128 * eb_k + 4) + 4 * nc + gs * row_q + 4 * gs * topk
+                ref_flops += gs * nc * FLOP_PER_PAIR
+    return dict(pairs=pairs, score_flops=pairs * FLOP_PER_PAIR, select_bytes=sel_bytes,
+                refine_bytes=ref_bytes, refine_flops=ref_flops, proxy_bytes=prox_bytes)
+
+
+# ---------------------------------------------------------------- runs
+class Prefill:
+    def __init__(self, wl, threads):
+        import torch
+        from workload.gen import make
+        t = time.time()
+        x = make(wl, threads=threads)
+        log(f"generated {wl.name} in {time.time() - t:.1f}s")
+        self.wl, self.x = wl, x
+        d = lambda a: None if a is None else torch.from_numpy(a.view("int16") if a.dtype.name == "uint16" else a).cuda()  # noqa
+        self.q, self.qs, self.w, self.k, self.ks = d(x.q), d(x.q_scale), d(x.w), d(x.k), d(x.k_scale)
+        L = wl.L
+        self.chunks = [(p0, min(wl.chunk, L - p0)) for p0 in range(0, L, wl.chunk)]
+        self.out = torch.empty((L, wl.topk), dtype=torch.int32, device="cuda")
+        import paper_2607_24593_amd as pv
+        self.pv = pv
+        p0, n = self.chunks[-1]
+        need = 0
+        for g in wl.g:
+            a = pv.make_args(self.q[p0:p0 + n], self.qs[p0:p0 + n] if self.qs is not None else None,
+                             self.w[p0:p0 + n], self.k[:p0 + n], None if self.ks is None else self.ks[:p0 + n],
+                             p0, p0 + n, wl.topk, self.out[p0:p0 + n])
+            for mode in (pv.PIVOT_DENSE, pv.PIVOT_REUSE, pv.PIVOT_REFINE):
+                need = max(need, pv.pivot_workspace_size(a, mode, g, wl.c))
+        self.ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+        log(f"workspace {need / 2**30:.2f} GiB")
+
+    def run(self, mode, g):
+        pv, wl = self.pv, self.wl
+        for p0, n in self.chunks:
+            sl = slice(p0, p0 + n)
+            args = (self.q[sl], None if self.qs is None else self.qs[sl], self.w[sl], self.k[:p0 + n],
+                    None if self.ks is None else self.ks[:p0 + n], p0, p0 + n, wl.topk)
+            if mode == "dense":
+                pv.pivot_dense_index(*args, out=self.out[sl], ws=self.ws)
+            else:
+                pv.pivot_group_index(*args, mode=pv.PIVOT_REUSE if mode == "reuse" else pv.PIVOT_REFINE,
+                                     g=g, c=wl.c, out=self.out[sl], ws=self.ws)
+
+
+def timed(fn, reps):
+    import torch
+    torch.cuda.synchronize()
+    t = time.perf_counter()
+    for _ in range(reps):
+        fn()
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t) / reps
+
+
+def decode_bench(reps):
+    import torch
+    import paper_2607_24593_amd as pv
+    from workload.gen import WORKLOADS, make
+    wl = WORKLOADS["decode-32x128k-fp8"]
+    t = time.time()
+    x = make(wl, threads=16)
+    log(f"generated {wl.name} in {time.time() - t:.1f}s")
+    B, L, g = wl.batch, wl.L, wl.g[0]
+    d = lambda a: torch.from_numpy(a).cuda()  # noqa: E731
+    q, qs, w, k, ks = d(x.q), d(x.q_scale), d(x.w), d(x.k), d(x.k_scale)
+    pos, nk = [L - g] * B, [L] * B
+    out = torch.empty((B, g, wl.topk), dtype=torch.int32, device="cuda")
+    res = {}
+    for mode in ("dense", "reuse", "refine"):
+        if mode == "dense":
+            fn = lambda: pv.pivot_dense_index(q, qs, w, k, ks, pos, nk, wl.topk, out=out)  # noqa: E731
+        else:
+            m = pv.PIVOT_REUSE if mode == "reuse" else pv.PIVOT_REFINE
+            fn = lambda m=m: pv.pivot_group_index(q, qs, w, k, ks, pos, nk, wl.topk, mode=m, g=g, c=wl.c,  # noqa
+                                                  out=out)
+        fn()
+        sec = timed(fn, reps)
+        res[mode] = {"us_per_step": sec * 1e6, "queries_per_s": B * g / sec}
+    for mode in ("reuse", "refine"):
+        res[mode]["speedup_vs_dense"] = res["dense"]["us_per_step"] / res[mode]["us_per_step"]
+    key_bytes = B * L * (128 + 4)
+    res["dense"]["key_stream_GBps"] = key_bytes / (res["dense"]["us_per_step"] * 1e-6) / 1e9
+    res["workload"] = wl.name
+    return res
+
+
+def cpu_baseline(pf, g, budget_s=12.0, max_groups=4096):
+    """The oracle (C, fp64, OpenMP) on a sample of PIVOT-Refine groups of the same
+    prefill: groups at uniformly random positions past the guardrail, drawn until
+    about budget_s seconds of CPU work."""
+    import numpy as np
+    import oracle
+    oracle.build(force=False)
+    wl, x = pf.wl, pf.x
+    rng = np.random.default_rng(0)
+    lo = wl.c  # first position past the guardrail
+    fp8 = wl.dtype == "fp8"
+    t0s = []
+    t = time.perf_counter()
+    while time.perf_counter() - t < budget_s and len(t0s) < max_groups:
+        t0 = int(rng.integers(lo, wl.L - g)) // g * g
+        oracle.index(wl.dtype, x.q[t0:t0 + g], x.q_scale[t0:t0 + g] if fp8 else None, x.w[t0:t0 + g], t0,
+                     x.k[:t0 + g], x.k_scale[:t0 + g] if fp8 else None, t0 + g, mode=oracle.REFINE, g=g, c=wl.c,
+                     topk=wl.topk)
+        t0s.append(t0)
+    sec = time.perf_counter() - t
+    t0s.sort()
+    pairs_sample = sum(t0 + 1 + g * wl.c for t0 in t0s)
+    full = units(pf.chunks, "refine", g, wl.c, wl.topk)
+    pairs_full = full["pairs"] + full["refine_flops"] // FLOP_PER_PAIR
+    return {"value": len(t0s) * g / sec, "unit": "queries/s", "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": f"{len(t0s)} PIVOT-Refine groups (g={g}, c={wl.c}, k={wl.topk}) at random positions "
+                      f"{t0s[0]}..{t0s[-1]} of {wl.name}, {sec:.1f}s",
+            "full_config_s_extrapolated": sec * pairs_full / pairs_sample}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="prefill-128k-fp8")
+    ap.add_argument("--g", type=int, default=4)
+    ap.add_argument("--reps", type=int, default=2, help="passes per mode for the comparison table")
+    ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for {max(args.gpus, world)})",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2607_24593_amd as pv
+    from workload.gen import WORKLOADS
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    pv.lib()
+    wl = WORKLOADS[args.workload]
+    g = args.g
+    pf = Prefill(wl, threads=16)
+
+    # ---- headline: PIVOT-Refine steps
+    for _ in range(args.warmup):
+        pf.run("refine", g)
+    torch.cuda.synchronize()
+    pv.pivot_profile_begin()
+    t = time.perf_counter()
+    for _ in range(args.steps):
+        pf.run("refine", g)
+    torch.cuda.synchronize()
+    step_s = (time.perf_counter() - t) / args.steps
+    prof = pv.pivot_profile_end()
+    log(f"refine g={g}: {step_s * 1e3:.2f} ms/step; kernels {prof}")
+    qps = wl.L / step_s
+
+    eb = 1 if wl.dtype == "fp8" else 2
+    u = units(pf.chunks, "refine", g, wl.c, wl.topk, eb, eb)
+    K = args.steps
+    kern = {}
+    for name, (n, ms) in prof.items():
+        if n == 0:
+            continue
+        e = {"launches_per_step": n / K, "ms_per_step": ms / K, "avg_launch_ms": ms / n}
+        if name == "score":
+            e.update(bound="mfma", achieved=u["score_flops"] * K / (ms * 1e-3) / 1e12, unit="TFLOP/s",
+                     peak=PEAK[wl.dtype])
+        elif name == "select":
+            e.update(bound="hbm", achieved=u["select_bytes"] * K / (ms * 1e-3) / 1e9, unit="GB/s", peak=HBM_PEAK)
+        elif name == "refine":
+            e.update(bound="hbm", achieved=u["refine_bytes"] * K / (ms * 1e-3) / 1e9, unit="GB/s", peak=HBM_PEAK,
+                     mfma_TFLOPs=u["refine_flops"] * K / (ms * 1e-3) / 1e12)
+        elif name == "proxy":
+            e.update(bound="hbm", achieved=u["proxy_bytes"] * K / (ms * 1e-3) / 1e9, unit="GB/s", peak=HBM_PEAK)
+        if "achieved" in e:
+            e["frac"] = e["achieved"] / e["peak"]
+        kern[name] = e
+    dom = max(kern, key=lambda n: kern[n]["ms_per_step"])
+    dk = kern[dom]
+    roofline = {"kernel": dom, "bound": dk.get("bound"), "achieved": dk.get("achieved"), "peak": dk.get("peak"),
+                "unit": dk.get("unit"), "frac": dk.get("frac"), "traffic": None,
+                "units_per_step": {"score_pairs": u["pairs"], "score_flops": u["score_flops"],
+                                   "select_bytes": u["select_bytes"], "refine_bytes": u["refine_bytes"]}}
+
+    # ---- comparison: dense, Reuse, g sweep
+    modes = {}
+    dense_s = timed(lambda: pf.run("dense", g), args.reps)
+    ud = units(pf.chunks, "dense", 1, wl.c, wl.topk, eb, eb)
+    modes["dense"] = {"ms_per_pass": dense_s * 1e3, "queries_per_s": wl.L / dense_s,
+                      "score_TFLOPs_incl_select": ud["score_flops"] / dense_s / 1e12}
+    log(f"dense: {dense_s * 1e3:.2f} ms")
+    sweep = wl.g if not args.no_sweep else (g,)
+    for gg in sweep:
+        for mode in ("reuse", "refine"):
+            s = step_s if (mode == "refine" and gg == g) else timed(lambda: pf.run(mode, gg), args.reps)
+            modes[f"{mode}_g{gg}"] = {"ms_per_pass": s * 1e3, "queries_per_s": wl.L / s,
+                                      "speedup_vs_dense": dense_s / s}
+            log(f"{mode} g={gg}: {s * 1e3:.2f} ms ({dense_s / s:.2f}x)")
+
+    dec = None if args.no_decode else decode_bench(reps=50)
+    cpu = None if args.no_cpu_baseline else cpu_baseline(pf, g)
+
+    line = {
+        "metric": "indexed queries/s and speedup vs dense indexer at 128K prefill; MFMA % of peak",
+        "value": qps,
+        "unit": "queries/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": step_s * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic",
+        "config": {"workload": wl.name, "L": wl.L, "H": wl.H, "d": wl.d, "topk": wl.topk, "c": wl.c, "g": g,
+                   "chunk": wl.chunk, "mode": "refine", "guardrail": "t0 < c -> dense"},
+        "speedup_vs_dense": dense_s / step_s,
+        "mfma_frac_score_kernel": kern.get("score", {}).get("frac"),
+        "roofline": roofline,
+        "kernels": kern,
+        "modes": modes,
+        "decode": dec,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -172,6 +172,31 @@ pivot_status pivot_topk_rows(int32_t n_rows, const float* scores, int64_t ld, in
  */
 pivot_status pivot_encode_e4m3(const float* x, uint8_t* out, int64_t n, void* stream);
 
+/*
+ * Kernel timing.  Between pivot_profile_begin() and pivot_profile_end() every
+ * kernel the library launches is bracketed by two HIP events recorded on the
+ * launch's stream.  pivot_profile_end() waits for those events and returns,
+ * per kernel kind, the number of launches and the summed event-to-event time;
+ * it then stops recording.  Event objects are host-side resources created on
+ * first use; no device memory is allocated.  One profile at a time per process.
+ */
+enum {
+  PIVOT_KERNEL_PROXY = 0,   /* proxy aggregation, Eq. 4 */
+  PIVOT_KERNEL_SCORE = 1,   /* MFMA scoring, Eq. 1 / Eq. 5 */
+  PIVOT_KERNEL_SELECT = 2,  /* row top-k / top-c selection */
+  PIVOT_KERNEL_REFINE = 3,  /* Refine gather, re-score and select, Eqs. 8-9 */
+  PIVOT_KERNEL_FILL = 4,    /* -1 fill of guardrail candidate rows */
+  PIVOT_KERNEL_KINDS = 5
+};
+
+typedef struct {
+  int64_t launches[PIVOT_KERNEL_KINDS];
+  double total_ms[PIVOT_KERNEL_KINDS];
+} pivot_profile;
+
+pivot_status pivot_profile_begin(void);
+pivot_status pivot_profile_end(pivot_profile* out);
+
 /* Static description of a status code. */
 const char* pivot_status_string(int32_t status);
 

@@ -24,14 +24,19 @@ PIVOT_DENSE = -1
 H, D = 64, 128
 
 EXPORTED = ["pivot_workspace_size", "pivot_dense_index", "pivot_group_index", "pivot_proxy_rows",
-            "pivot_score_rows", "pivot_topk_rows", "pivot_encode_e4m3", "pivot_status_string",
-            "pivot_last_error", "pivot_version"]
+            "pivot_score_rows", "pivot_topk_rows", "pivot_encode_e4m3", "pivot_profile_begin",
+            "pivot_profile_end", "pivot_status_string", "pivot_last_error", "pivot_version"]
+KERNELS = ["proxy", "score", "select", "refine", "fill"]
 
 
 class PivotError(RuntimeError):
     def __init__(self, status: int, where: str):
         self.status = status
         super().__init__(f"{where}: {status_string(status)} ({last_error()})")
+
+
+class pivot_profile(ctypes.Structure):
+    _fields_ = [("launches", ctypes.c_int64 * 5), ("total_ms", ctypes.c_double * 5)]
 
 
 class pivot_args(ctypes.Structure):
@@ -73,6 +78,10 @@ def lib():
         L.pivot_topk_rows.argtypes = [I32, P, I64, I64, I32, I32, P, P]
         L.pivot_encode_e4m3.restype = I32
         L.pivot_encode_e4m3.argtypes = [P, P, I64, P]
+        L.pivot_profile_begin.restype = I32
+        L.pivot_profile_begin.argtypes = []
+        L.pivot_profile_end.restype = I32
+        L.pivot_profile_end.argtypes = [ctypes.POINTER(pivot_profile)]
         L.pivot_status_string.restype = ctypes.c_char_p
         L.pivot_status_string.argtypes = [I32]
         L.pivot_last_error.restype = ctypes.c_char_p
@@ -238,6 +247,17 @@ def pivot_topk_rows(scores, n0, n_step, m, out=None, stream=None):
     _check(lib().pivot_topk_rows(n, _ptr(scores), ld, int(n0), int(n_step), int(m), _ptr(out), _stream(stream)),
            "pivot_topk_rows")
     return out
+
+
+def pivot_profile_begin():
+    _check(lib().pivot_profile_begin(), "pivot_profile_begin")
+
+
+def pivot_profile_end() -> dict:
+    """{kernel: (launches, total_ms)} since pivot_profile_begin()."""
+    p = pivot_profile()
+    _check(lib().pivot_profile_end(ctypes.byref(p)), "pivot_profile_end")
+    return {name: (int(p.launches[i]), float(p.total_ms[i])) for i, name in enumerate(KERNELS)}
 
 
 def pivot_encode_e4m3(x, out=None, stream=None):

@@ -4,6 +4,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <vector>
 
 #include "launch.h"
@@ -26,6 +27,44 @@ pivot_status fail(pivot_status s, const char* fmt, ...) {
 pivot_status hip_check(hipError_t e, const char* what) {
   if (e == hipSuccess) return PIVOT_OK;
   return fail(PIVOT_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// ---- optional per-kernel event timing (pivot_profile_begin / _end) ----
+struct ProfRecord {
+  int kind;
+  hipEvent_t start, stop;
+};
+std::mutex g_prof_mu;
+bool g_prof_on = false;
+std::vector<ProfRecord> g_prof_recs;
+std::vector<hipEvent_t> g_prof_pool;
+
+hipEvent_t prof_event() {
+  if (!g_prof_pool.empty()) {
+    hipEvent_t e = g_prof_pool.back();
+    g_prof_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+// Run one launcher; with profiling on, bracket it with events on `stream`.
+template <class F>
+hipError_t timed(int kind, hipStream_t stream, F launch) {
+  if (!g_prof_on) return launch();
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  ProfRecord r{kind, prof_event(), prof_event()};
+  if (!r.start || !r.stop) return hipErrorOutOfMemory;
+  hipError_t e = hipEventRecord(r.start, stream);
+  if (e != hipSuccess) return e;
+  e = launch();
+  if (e != hipSuccess) return e;
+  e = hipEventRecord(r.stop, stream);
+  if (e != hipSuccess) return e;
+  g_prof_recs.push_back(r);
+  return hipSuccess;
 }
 
 constexpr size_t kAlign = 256;
@@ -237,11 +276,14 @@ pivot_status run_rows(const pivot_args* a, const Plan& p, int kind, int lo, int 
       const int64_t lim = max_limit(st, rs);
       if (lim < 0) continue;
       const int64_t ld = ld_for(lim + 1);
-      pivot_status s = hip_check(launch_score(p.dtype, rd.q, rd.qs, rd.w, rd.seq_rows, kb, ksb, a->k_seq_stride,
-                                              st, rs, lim, scores, ld, stream),
+      pivot_status s = hip_check(timed(PIVOT_KERNEL_SCORE, stream, [&] {
+                                   return launch_score(p.dtype, rd.q, rd.qs, rd.w, rd.seq_rows, kb, ksb,
+                                                       a->k_seq_stride, st, rs, lim, scores, ld, stream);
+                                 }),
                                  "score kernel");
       if (s != PIVOT_OK) return s;
-      s = hip_check(launch_topk(scores, ld, st, rs, od, stream), "top-k kernel");
+      s = hip_check(timed(PIVOT_KERNEL_SELECT, stream, [&] { return launch_topk(scores, ld, st, rs, od, stream); }),
+                    "top-k kernel");
       if (s != PIVOT_OK) return s;
     }
   }
@@ -326,8 +368,10 @@ pivot_status pivot_group_index(const pivot_args* a, int32_t mode, int32_t g, int
       for (int b0 = 0; b0 < p.B; b0 += kMaxSeq) {
         const int nb = std::min(kMaxSeq, p.B - b0);
         SeqTable st = table_for(p, b0, nb);
-        s = hip_check(launch_fill_guardrail(out_cand + (size_t)b0 * p.n_groups * c, p.n_groups, c, st, 0,
-                                            p.n_groups, -1, stream),
+        s = hip_check(timed(PIVOT_KERNEL_FILL, stream, [&] {
+                        return launch_fill_guardrail(out_cand + (size_t)b0 * p.n_groups * c, p.n_groups, c, st,
+                                                     0, p.n_groups, -1, stream);
+                      }),
                       "fill kernel");
         if (s != PIVOT_OK) return s;
       }
@@ -346,9 +390,12 @@ pivot_status pivot_group_index(const pivot_args* a, int32_t mode, int32_t g, int
     SeqTable st = table_for(p, b0, nb);
     const size_t qoff = (size_t)b0 * p.n_q;
     const size_t poff = (size_t)b0 * p.n_groups;
-    s = hip_check(launch_proxy(p.dtype, (const uint8_t*)a->q + qoff * p.row_bytes, qs ? qs + qoff : nullptr,
-                               a->w + qoff * kH, p.n_q, p.g, p.n_groups, st, p.proxy_lo, p.n_groups, false,
-                               (uint8_t*)pq + poff * p.row_bytes, psc + poff, pw + poff * kH, stream),
+    s = hip_check(timed(PIVOT_KERNEL_PROXY, stream, [&] {
+                    return launch_proxy(p.dtype, (const uint8_t*)a->q + qoff * p.row_bytes,
+                                        qs ? qs + qoff : nullptr, a->w + qoff * kH, p.n_q, p.g, p.n_groups, st,
+                                        p.proxy_lo, p.n_groups, false, (uint8_t*)pq + poff * p.row_bytes,
+                                        psc + poff, pw + poff * kH, stream);
+                  }),
                   "proxy kernel");
     if (s != PIVOT_OK) return s;
   }
@@ -368,14 +415,19 @@ pivot_status pivot_group_index(const pivot_args* a, int32_t mode, int32_t g, int
     const size_t qoff = (size_t)b0 * p.n_q;
     int32_t* cb = cand + (size_t)b0 * p.n_groups * c;
     if (out_cand) {
-      s = hip_check(launch_fill_guardrail(cb, p.n_groups, c, st, 0, p.n_groups, -1, stream), "fill kernel");
+      s = hip_check(timed(PIVOT_KERNEL_FILL, stream,
+                          [&] { return launch_fill_guardrail(cb, p.n_groups, c, st, 0, p.n_groups, -1, stream); }),
+                    "fill kernel");
       if (s != PIVOT_OK) return s;
     }
-    s = hip_check(launch_refine(p.dtype, (const uint8_t*)a->q + qoff * p.row_bytes, qs ? qs + qoff : nullptr,
-                                a->w + qoff * kH, p.n_q, p.g, p.n_groups,
-                                (const uint8_t*)a->k + (size_t)b0 * a->k_seq_stride * kD * p.EB,
-                                a->k_scale ? a->k_scale + (size_t)b0 * a->k_seq_stride : nullptr, a->k_seq_stride,
-                                st, p.proxy_lo, p.n_groups, cb, c, p.topk, a->out_idx + qoff * p.topk, stream),
+    s = hip_check(timed(PIVOT_KERNEL_REFINE, stream, [&] {
+                    return launch_refine(p.dtype, (const uint8_t*)a->q + qoff * p.row_bytes,
+                                         qs ? qs + qoff : nullptr, a->w + qoff * kH, p.n_q, p.g, p.n_groups,
+                                         (const uint8_t*)a->k + (size_t)b0 * a->k_seq_stride * kD * p.EB,
+                                         a->k_scale ? a->k_scale + (size_t)b0 * a->k_seq_stride : nullptr,
+                                         a->k_seq_stride, st, p.proxy_lo, p.n_groups, cb, c, p.topk,
+                                         a->out_idx + qoff * p.topk, stream);
+                  }),
                   "refine kernel");
     if (s != PIVOT_OK) return s;
   }
@@ -445,6 +497,36 @@ pivot_status pivot_encode_e4m3(const float* x, uint8_t* out, int64_t n, void* st
   if (n == 0) return PIVOT_OK;
   if (!x || !out) return fail(PIVOT_ERR_INVALID_ARG, "null pointer");
   return hip_check(launch_encode_e4m3(x, out, n, (hipStream_t)stream), "encode kernel");
+}
+
+pivot_status pivot_profile_begin(void) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  if (g_prof_on) return fail(PIVOT_ERR_INVALID_ARG, "a profile is already running");
+  g_prof_recs.clear();
+  g_prof_on = true;
+  return PIVOT_OK;
+}
+
+pivot_status pivot_profile_end(pivot_profile* out) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  if (!g_prof_on) return fail(PIVOT_ERR_INVALID_ARG, "no profile is running");
+  g_prof_on = false;
+  pivot_profile acc;
+  memset(&acc, 0, sizeof acc);
+  pivot_status st = PIVOT_OK;
+  for (ProfRecord& r : g_prof_recs) {
+    float ms = 0.f;
+    hipError_t e = hipEventSynchronize(r.stop);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, r.start, r.stop);
+    if (e != hipSuccess && st == PIVOT_OK) st = hip_check(e, "profile events");
+    acc.launches[r.kind] += 1;
+    acc.total_ms[r.kind] += ms;
+    g_prof_pool.push_back(r.start);
+    g_prof_pool.push_back(r.stop);
+  }
+  g_prof_recs.clear();
+  if (out) *out = acc;
+  return st;
 }
 
 const char* pivot_status_string(int32_t status) {
