@@ -152,11 +152,16 @@ pivot_status pivot_proxy_rows(int32_t dtype, int32_t heads, int32_t dim, int32_t
  * s = 0 .. lim0 + r * lim_step of k / k_scale (which must hold at least that
  * many keys); out[r * ld + s] receives the fp32 score.  Entries past a row's
  * limit are not written.  Requires ld >= lim0 + (n_rows-1)*lim_step + 1.
+ * fp8 rows need a workspace of PIVOT_SCORE_ROWS_WORKSPACE(n_rows) bytes
+ * (256-B aligned) for the per-row linear term of the epilogue; bf16 needs none.
  */
+#define PIVOT_SCORE_ROWS_WORKSPACE(n_rows) \
+  ((((size_t)(n_rows) * 512 + 255) / 256) * 256 + (size_t)(n_rows) * 16)
 pivot_status pivot_score_rows(int32_t dtype, int32_t heads, int32_t dim, int32_t n_rows,
                               const void* q, const float* q_scale, const float* w,
                               const void* k, const float* k_scale, int64_t lim0, int32_t lim_step,
-                              float* out, int64_t ld, void* stream);
+                              float* out, int64_t ld, void* workspace, size_t workspace_bytes,
+                              void* stream);
 
 /*
  * Stage: TopK of fp32 rows.  Row r of scores [n_rows, ld] has its first
@@ -186,7 +191,8 @@ enum {
   PIVOT_KERNEL_SELECT = 2,  /* row top-k / top-c selection */
   PIVOT_KERNEL_REFINE = 3,  /* Refine gather, re-score and select, Eqs. 8-9 */
   PIVOT_KERNEL_FILL = 4,    /* -1 fill of guardrail candidate rows */
-  PIVOT_KERNEL_KINDS = 5
+  PIVOT_KERNEL_LIN = 5,     /* per-row linear term of the fp8 score epilogue */
+  PIVOT_KERNEL_KINDS = 6
 };
 
 typedef struct {

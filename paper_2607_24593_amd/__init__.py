@@ -26,7 +26,7 @@ H, D = 64, 128
 EXPORTED = ["pivot_workspace_size", "pivot_dense_index", "pivot_group_index", "pivot_proxy_rows",
             "pivot_score_rows", "pivot_topk_rows", "pivot_encode_e4m3", "pivot_profile_begin",
             "pivot_profile_end", "pivot_status_string", "pivot_last_error", "pivot_version"]
-KERNELS = ["proxy", "score", "select", "refine", "fill"]
+KERNELS = ["proxy", "score", "select", "refine", "fill", "lin"]
 
 
 class PivotError(RuntimeError):
@@ -36,7 +36,7 @@ class PivotError(RuntimeError):
 
 
 class pivot_profile(ctypes.Structure):
-    _fields_ = [("launches", ctypes.c_int64 * 5), ("total_ms", ctypes.c_double * 5)]
+    _fields_ = [("launches", ctypes.c_int64 * 6), ("total_ms", ctypes.c_double * 6)]
 
 
 class pivot_args(ctypes.Structure):
@@ -73,7 +73,7 @@ def lib():
         L.pivot_proxy_rows.restype = I32
         L.pivot_proxy_rows.argtypes = [I32, I32, I32, I32, I32, P, P, P, P, P, P, P]
         L.pivot_score_rows.restype = I32
-        L.pivot_score_rows.argtypes = [I32, I32, I32, I32, P, P, P, P, P, I64, I32, P, I64, P]
+        L.pivot_score_rows.argtypes = [I32, I32, I32, I32, P, P, P, P, P, I64, I32, P, I64, P, ctypes.c_size_t, P]
         L.pivot_topk_rows.restype = I32
         L.pivot_topk_rows.argtypes = [I32, P, I64, I64, I32, I32, P, P]
         L.pivot_encode_e4m3.restype = I32
@@ -228,15 +228,22 @@ def pivot_proxy_rows(q, q_scale, w, g, stream=None):
     return pq, ps, pw
 
 
+def score_rows_workspace(n_rows: int) -> int:
+    """PIVOT_SCORE_ROWS_WORKSPACE of include/pivot.h."""
+    return (n_rows * 512 + 255) // 256 * 256 + n_rows * 16
+
+
 def pivot_score_rows(q, q_scale, w, k, k_scale, lim0, lim_step, ld=None, out=None, stream=None):
     """Scores of rows q [n, H, d] over keys 0 .. lim0 + r * lim_step: fp32 [n, ld]."""
     n = q.shape[0]
     lim_max = lim0 + (n - 1) * lim_step
     ld = lim_max + 1 if ld is None else ld
     out = torch.full((n, ld), float("nan"), dtype=torch.float32, device=q.device) if out is None else out
+    nbytes = score_rows_workspace(n) if _dtype_code(q) == PIVOT_DT_FP8_E4M3 else 0
+    ws = workspace(nbytes, q.device) if nbytes else None
     _check(lib().pivot_score_rows(_dtype_code(q), q.shape[1], q.shape[2], n, _ptr(q), _ptr(q_scale), _ptr(w),
-                                  _ptr(k), _ptr(k_scale), int(lim0), int(lim_step), _ptr(out), int(ld),
-                                  _stream(stream)), "pivot_score_rows")
+                                  _ptr(k), _ptr(k_scale), int(lim0), int(lim_step), _ptr(out), int(ld), _ptr(ws),
+                                  nbytes, _stream(stream)), "pivot_score_rows")
     return out
 
 

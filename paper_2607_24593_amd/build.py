@@ -21,6 +21,8 @@ FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
     # no packed fp32 instructions (v_pk_fma_f32 / v_pk_mul_f32 / v_pk_add_f32)
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA results in VGPRs, so the epilogue reads them without v_accvgpr_read
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
     "-Wall", "-Wno-unused-result",
     f"-I{INCLUDE}", f"-I{CSRC}",
 ]

@@ -8,6 +8,7 @@
 #include <vector>
 
 #include "launch.h"
+#include "mfma_tile.h"
 #include "pivot.h"
 
 using namespace pivot;
@@ -88,6 +89,8 @@ struct Plan {
   int64_t max_nk = 0;
   // workspace layout
   size_t off_pq = 0, off_psc = 0, off_pw = 0, off_cand = 0, off_scores = 0, fixed = 0;
+  size_t off_qlin = 0, off_qlsc = 0, off_plin = 0, off_plsc = 0;  // fp8 epilogue's linear term
+  bool qlin = false, plin = false;
 };
 
 pivot_status check_args(const pivot_args* a) {
@@ -167,7 +170,25 @@ pivot_status make_plan(const pivot_args* a, int mode, int g, int c, int dense_be
   // workspace layout
   size_t off = 0;
   const size_t ng = (size_t)p.B * p.n_groups;
-  if (mode != PIVOT_DENSE && p.proxy_lo < p.n_groups) {
+  const bool fp8 = p.dtype == PIVOT_DT_FP8_E4M3;
+  const bool proxies = mode != PIVOT_DENSE && p.proxy_lo < p.n_groups;
+  // query rows need the linear term when scored densely or re-scored by Refine
+  p.qlin = fp8 && (p.dense_hi > 0 || (proxies && mode == PIVOT_REFINE));
+  p.plin = fp8 && proxies;
+  if (p.qlin) {
+    const size_t nq = (size_t)p.B * p.n_q;
+    p.off_qlin = off;
+    off = align_up(off + nq * kLinBytes);
+    p.off_qlsc = off;
+    off = align_up(off + nq * kLinLevels * sizeof(float));
+  }
+  if (p.plin) {
+    p.off_plin = off;
+    off = align_up(off + ng * kLinBytes);
+    p.off_plsc = off;
+    off = align_up(off + ng * kLinLevels * sizeof(float));
+  }
+  if (proxies) {
     p.off_pq = off;
     off = align_up(off + ng * p.row_bytes);
     p.off_psc = off;
@@ -237,6 +258,8 @@ struct RowData {
   const void* q;
   const float* qs;
   const float* w;
+  const uint8_t* lin;  // fp8 only
+  const float* lsc;
   int64_t seq_rows;  // rows per sequence in q
 };
 
@@ -267,6 +290,8 @@ pivot_status run_rows(const pivot_args* a, const Plan& p, int kind, int lo, int 
     rd.q = (const uint8_t*)rd_all.q + (size_t)b0 * rd_all.seq_rows * p.row_bytes;
     rd.qs = rd_all.qs ? rd_all.qs + (size_t)b0 * rd_all.seq_rows : nullptr;
     rd.w = rd_all.w + (size_t)b0 * rd_all.seq_rows * kH;
+    rd.lin = rd_all.lin ? rd_all.lin + (size_t)b0 * rd_all.seq_rows * kLinBytes : nullptr;
+    rd.lsc = rd_all.lsc ? rd_all.lsc + (size_t)b0 * rd_all.seq_rows * kLinLevels : nullptr;
     const uint8_t* kb = (const uint8_t*)a->k + (size_t)b0 * a->k_seq_stride * kD * p.EB;
     const float* ksb = a->k_scale ? a->k_scale + (size_t)b0 * a->k_seq_stride : nullptr;
     OutDesc od = od_all;
@@ -277,8 +302,8 @@ pivot_status run_rows(const pivot_args* a, const Plan& p, int kind, int lo, int 
       if (lim < 0) continue;
       const int64_t ld = ld_for(lim + 1);
       pivot_status s = hip_check(timed(PIVOT_KERNEL_SCORE, stream, [&] {
-                                   return launch_score(p.dtype, rd.q, rd.qs, rd.w, rd.seq_rows, kb, ksb,
-                                                       a->k_seq_stride, st, rs, lim, scores, ld, stream);
+                                   return launch_score(p.dtype, rd.q, rd.qs, rd.w, rd.lin, rd.lsc, rd.seq_rows, kb,
+                                                       ksb, a->k_seq_stride, st, rs, lim, scores, ld, stream);
                                  }),
                                  "score kernel");
       if (s != PIVOT_OK) return s;
@@ -306,8 +331,23 @@ pivot_status check_workspace(const pivot_args* a, const Plan& p, int64_t& score_
   return PIVOT_OK;
 }
 
+// Linear-term rows (mfma_tile.h) of the call's queries: all of them for a
+// batch or when Refine re-scores members, else the leading dense rows.
+pivot_status query_lin(const pivot_args* a, const Plan& p, uint8_t* ws, hipStream_t stream) {
+  if (!p.qlin) return PIVOT_OK;
+  const int64_t rows = (p.B == 1 && p.mode != PIVOT_REFINE) ? p.dense_hi : (int64_t)p.B * p.n_q;
+  return hip_check(timed(PIVOT_KERNEL_LIN, stream, [&] {
+                     return launch_lin(a->q, a->q_scale, a->w, 0, rows, ws + p.off_qlin,
+                                       reinterpret_cast<float*>(ws + p.off_qlsc), stream);
+                   }),
+                   "linear-term kernel");
+}
+
 pivot_status dense_part(const pivot_args* a, const Plan& p, float* scores, int64_t score_bytes, hipStream_t stream) {
-  RowData rd{a->q, a->dtype == PIVOT_DT_FP8_E4M3 ? a->q_scale : nullptr, a->w, p.n_q};
+  uint8_t* ws = (uint8_t*)a->workspace;
+  const bool fp8 = a->dtype == PIVOT_DT_FP8_E4M3;
+  RowData rd{a->q, fp8 ? a->q_scale : nullptr, a->w, fp8 ? ws + p.off_qlin : nullptr,
+             fp8 ? reinterpret_cast<const float*>(ws + p.off_qlsc) : nullptr, p.n_q};
   OutDesc od{a->out_idx, p.topk, p.n_q, 0, p.n_q};
   const int kind = p.mode == PIVOT_DENSE ? kAll : kDenseRows;
   return run_rows(a, p, kind, 0, p.dense_hi, 1, p.n_q, rd, od, scores, score_bytes, stream);
@@ -339,6 +379,8 @@ pivot_status pivot_dense_index(const pivot_args* a) {
   s = check_workspace(a, p, score_bytes);
   if (s != PIVOT_OK) return s;
   float* scores = reinterpret_cast<float*>((uint8_t*)a->workspace + p.off_scores);
+  s = query_lin(a, p, (uint8_t*)a->workspace, (hipStream_t)a->stream);
+  if (s != PIVOT_OK) return s;
   return dense_part(a, p, scores, score_bytes, (hipStream_t)a->stream);
 }
 
@@ -361,6 +403,8 @@ pivot_status pivot_group_index(const pivot_args* a, int32_t mode, int32_t g, int
   uint8_t* ws = (uint8_t*)a->workspace;
   float* scores = reinterpret_cast<float*>(ws + p.off_scores);
 
+  s = query_lin(a, p, ws, stream);
+  if (s != PIVOT_OK) return s;
   s = dense_part(a, p, scores, score_bytes, stream);  // guardrail groups (Algorithm 1)
   if (s != PIVOT_OK) return s;
   if (p.proxy_lo >= p.n_groups) {
@@ -400,9 +444,19 @@ pivot_status pivot_group_index(const pivot_args* a, int32_t mode, int32_t g, int
     if (s != PIVOT_OK) return s;
   }
 
+  uint8_t* plin = p.plin ? ws + p.off_plin : nullptr;
+  float* plsc = p.plin ? reinterpret_cast<float*>(ws + p.off_plsc) : nullptr;
+  if (p.plin) {
+    const int64_t r0 = p.B == 1 ? p.proxy_lo : 0, r1 = (int64_t)p.B * p.n_groups;
+    s = hip_check(timed(PIVOT_KERNEL_LIN, stream,
+                        [&] { return launch_lin(pq, psc, pw, r0, r1, plin, plsc, stream); }),
+                  "linear-term kernel");
+    if (s != PIVOT_OK) return s;
+  }
+
   // Eq. 5 proxy scan, then Eq. 6 (Reuse: top-k shared by the members) or
   // Eq. 7 (Refine: top-c candidates)
-  RowData rd{pq, psc, pw, p.n_groups};
+  RowData rd{pq, p.dtype == PIVOT_DT_FP8_E4M3 ? psc : nullptr, pw, plin, plsc, p.n_groups};
   OutDesc od = (mode == PIVOT_REUSE) ? OutDesc{a->out_idx, p.topk, p.n_q, p.g, p.n_q}
                                      : OutDesc{cand, c, p.n_groups, 0, 0};
   s = run_rows(a, p, kProxyRows, p.proxy_lo, p.n_groups, p.g, p.n_groups, rd, od, scores, score_bytes, stream);
@@ -422,7 +476,11 @@ pivot_status pivot_group_index(const pivot_args* a, int32_t mode, int32_t g, int
     }
     s = hip_check(timed(PIVOT_KERNEL_REFINE, stream, [&] {
                     return launch_refine(p.dtype, (const uint8_t*)a->q + qoff * p.row_bytes,
-                                         qs ? qs + qoff : nullptr, a->w + qoff * kH, p.n_q, p.g, p.n_groups,
+                                         qs ? qs + qoff : nullptr, a->w + qoff * kH,
+                                         p.qlin ? ws + p.off_qlin + qoff * kLinBytes : nullptr,
+                                         p.qlin ? reinterpret_cast<const float*>(ws + p.off_qlsc) + qoff * kLinLevels
+                                                : nullptr,
+                                         p.n_q, p.g, p.n_groups,
                                          (const uint8_t*)a->k + (size_t)b0 * a->k_seq_stride * kD * p.EB,
                                          a->k_scale ? a->k_scale + (size_t)b0 * a->k_seq_stride : nullptr,
                                          a->k_seq_stride, st, p.proxy_lo, p.n_groups, cb, c, p.topk,
@@ -454,7 +512,8 @@ pivot_status pivot_proxy_rows(int32_t dtype, int32_t heads, int32_t dim, int32_t
 
 pivot_status pivot_score_rows(int32_t dtype, int32_t heads, int32_t dim, int32_t n_rows, const void* q,
                               const float* q_scale, const float* w, const void* k, const float* k_scale,
-                              int64_t lim0, int32_t lim_step, float* out, int64_t ld, void* stream) {
+                              int64_t lim0, int32_t lim_step, float* out, int64_t ld, void* workspace,
+                              size_t workspace_bytes, void* stream) {
   if (dtype != PIVOT_DT_BF16 && dtype != PIVOT_DT_FP8_E4M3) return fail(PIVOT_ERR_UNSUPPORTED, "dtype %d", dtype);
   if (heads != kH || dim != kD) return fail(PIVOT_ERR_UNSUPPORTED, "heads=%d dim=%d", heads, dim);
   if (n_rows < 0 || lim0 < 0 || lim_step < 0) return fail(PIVOT_ERR_INVALID_ARG, "negative size");
@@ -464,14 +523,29 @@ pivot_status pivot_score_rows(int32_t dtype, int32_t heads, int32_t dim, int32_t
   const int64_t lim_max = lim0 + (int64_t)(n_rows - 1) * lim_step;
   if (lim_max > 0x7FFFFFFE) return fail(PIVOT_ERR_INVALID_ARG, "limits exceed int32 positions");
   if (ld < lim_max + 1) return fail(PIVOT_ERR_INVALID_ARG, "ld=%lld < %lld", (long long)ld, (long long)lim_max + 1);
+  const bool fp8 = dtype == PIVOT_DT_FP8_E4M3;
+  const size_t lin_off = align_up((size_t)n_rows * kLinBytes);
+  const size_t need = fp8 ? lin_off + (size_t)n_rows * kLinLevels * sizeof(float) : 0;
+  if (need > 0) {
+    if (!workspace || workspace_bytes < need)
+      return fail(PIVOT_ERR_WORKSPACE, "score rows need %zu workspace bytes", need);
+    if (reinterpret_cast<uintptr_t>(workspace) % kAlign)
+      return fail(PIVOT_ERR_INVALID_ARG, "workspace must be %zu-byte aligned", kAlign);
+  }
+  uint8_t* lin = fp8 ? (uint8_t*)workspace : nullptr;
+  float* lsc = fp8 ? reinterpret_cast<float*>((uint8_t*)workspace + lin_off) : nullptr;
   SeqTable st;
   memset(&st, 0, sizeof st);
   st.n = 1;
   st.q_pos0[0] = (int32_t)lim0;
   RowSpace rs{0, n_rows, lim_step, kAll};
-  const bool fp8 = dtype == PIVOT_DT_FP8_E4M3;
-  return hip_check(launch_score(dtype, q, fp8 ? q_scale : nullptr, w, n_rows, k, fp8 ? k_scale : nullptr, 0, st, rs,
-                                lim_max, out, ld, (hipStream_t)stream),
+  if (fp8) {
+    pivot_status s = hip_check(launch_lin(q, q_scale, w, 0, n_rows, lin, lsc, (hipStream_t)stream),
+                               "linear-term kernel");
+    if (s != PIVOT_OK) return s;
+  }
+  return hip_check(launch_score(dtype, q, fp8 ? q_scale : nullptr, w, lin, lsc, n_rows, k, fp8 ? k_scale : nullptr, 0,
+                                st, rs, lim_max, out, ld, (hipStream_t)stream),
                    "score kernel");
 }
 

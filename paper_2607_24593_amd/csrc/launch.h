@@ -26,19 +26,27 @@ hipError_t launch_proxy(int dtype, const void* q, const float* q_scale, const fl
                         int n_groups, const SeqTable& st, int j0, int j1, bool all_groups, void* pq,
                         float* psc, float* pw, hipStream_t stream);
 
-// Score rows rs (row data [B, q_seq_rows, H, d]) against each sequence's keys
-// 0 .. limit; out [B * (i1 - i0), ld].  lim_max: largest limit of any active row.
-hipError_t launch_score(int dtype, const void* q, const float* q_scale, const float* w, int64_t q_seq_rows,
-                        const void* k, const float* k_scale, int64_t k_seq_stride, const SeqTable& st,
-                        const RowSpace& rs, int64_t lim_max, float* out, int64_t ld, hipStream_t stream);
+// The fp8 epilogue's linear term (mfma_tile.h) for flat rows [r0, r1) of an
+// fp8 row array: lin [rows, 4 * 128] codes, lin_scale [rows, 4].
+hipError_t launch_lin(const void* q, const float* q_scale, const float* w, int64_t r0, int64_t r1, uint8_t* lin,
+                      float* lin_scale, hipStream_t stream);
+
+// Score rows rs (row data [B, q_seq_rows, H, d], with lin / lin_scale rows in
+// the same order for fp8) against each sequence's keys 0 .. limit;
+// out [B * (i1 - i0), ld].  lim_max: largest limit of any active row.
+hipError_t launch_score(int dtype, const void* q, const float* q_scale, const float* w, const uint8_t* lin,
+                        const float* lin_scale, int64_t q_seq_rows, const void* k, const float* k_scale,
+                        int64_t k_seq_stride, const SeqTable& st, const RowSpace& rs, int64_t lim_max, float* out,
+                        int64_t ld, hipStream_t stream);
 
 // Top-m of score rows: row (b, i) has limit + 1 valid entries.
 hipError_t launch_topk(const float* scores, int64_t ld, const SeqTable& st, const RowSpace& rs,
                        const OutDesc& od, hipStream_t stream);
 
 // Refine (Eqs. 8-9) for groups [j0, j1) with j >= first_proxy[b].
-hipError_t launch_refine(int dtype, const void* q, const float* q_scale, const float* w, int n_q, int g,
-                         int n_groups, const void* k, const float* k_scale, int64_t k_seq_stride,
+hipError_t launch_refine(int dtype, const void* q, const float* q_scale, const float* w, const uint8_t* lin,
+                         const float* lin_scale, int n_q, int g, int n_groups, const void* k,
+                         const float* k_scale, int64_t k_seq_stride,
                          const SeqTable& st, int j0, int j1, const int32_t* cand, int c, int m,
                          int32_t* out_idx, hipStream_t stream);
 

@@ -10,9 +10,19 @@
 // 4q .. 4q+3 in lane group q (lanes 16q .. 16q+15), key n in lane 16q + n.
 // Tile rows are assigned so that every lane group belongs to ONE query row:
 // with G = 4/R lane groups per row, tile j row 4q + i is head
-// 4G j + 4 (q mod G) + i of query row q / G.  Each lane therefore folds ReLU
-// and its gate into a running fp32 sum over its own heads with no cross-lane
-// traffic; only G > 1 needs log2(G) shuffles per 16 keys at the end.
+// 4G j + 4 (q mod G) + i of query row q / G.  Each lane therefore folds its
+// heads into a running fp32 sum with no cross-lane traffic; only G > 1 needs
+// log2(G) shuffles per 16 keys at the end.
+//
+// fp8 epilogue.  With x = q8 . k8 and w' = w * qscale,
+//   sum_j w'_j ReLU(x_j) = sum_j (w'_j / 2) |x_j|  +  u . k8,
+//   u = sum_j (w'_j / 2) q8_j   (a 128-vector per row),
+// because ReLU(x) = (x + |x|) / 2.  The first sum costs one FMA per element
+// (|x| is a free source modifier) instead of a max and an FMA.  The second is
+// linear in the key: u is stored as four fp8 levels u ~ sum_l sigma_l c_l
+// (each level quantises the residual of the previous ones, so the error is
+// ~2^-16 of max|u|), and one more MFMA tile per 16 keys computes c_l . k8 for
+// the R rows' levels.  bf16 rows use (w/2)|x| + (w/2)x directly (two FMAs).
 //
 // K split.  Lane l supplies dims 32 (l / 16) .. 32 (l / 16) + 31 of its A row
 // and of its B column.  Any assignment of dims to (lane group, register slot)
@@ -27,6 +37,9 @@ typedef int v8i __attribute__((ext_vector_type(8)));
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+
+constexpr int kLinLevels = 4;
+constexpr int kLinBytes = kLinLevels * kD;  // fp8 codes of the four levels of u, per row
 
 template <int DT>
 struct KeyFrag;
@@ -51,6 +64,11 @@ struct KeyFrag<kBf16> {
   }
 };
 
+__device__ __forceinline__ v4f mfma_fp8(const v8i& a, const v8i& b) {
+  const v4f z = {0.f, 0.f, 0.f, 0.f};
+  return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, z, 0, 0, 0, 0, 0, 0);
+}
+
 template <int DT, int R>
 struct RowTile {
   static_assert(R == 1 || R == 2 || R == 4, "rows per wave");
@@ -60,11 +78,15 @@ struct RowTile {
   static constexpr int ROW_BYTES = kH * kD * EB;
 
   KeyFrag<DT> a[T];   // A operand, same register format as a key fragment
-  float wv[T][4];     // gate * query scale of this lane's (row, head) pairs
+  float wv[T][4];     // w * qscale / 2 (bf16: qscale = 1)
+  KeyFrag<kFp8> al;   // fp8: the four levels of u of the wave's rows
+  float ls[4];        // fp8: level scales of this lane's row (0 in non-owning lane groups)
 
-  // rows[r]: the R query rows' codes; wrow[r]: gates; qscale[r]: per-row scale.
+  // rows[r]: the R query rows' codes; wrow[r]: gates; qscale[r]: per-row scale;
+  // lin[r] / lscale[r]: the rows' levels of u and their scales (fp8 only).
   __device__ __forceinline__ void load(const uint8_t* const* rows, const float* const* wrow,
-                                       const float* qscale, int lane) {
+                                       const float* qscale, const uint8_t* const* lin,
+                                       const float* const* lscale, int lane) {
     const int lr = lane & 15, kg = lane >> 4;
     const int gq_a = lr >> 2, i_a = lr & 3;
     const uint8_t* arow = rows[gq_a / G];
@@ -76,30 +98,56 @@ struct RowTile {
     const int gq = kg;
     const int qr = gq / G;
     const float* wr = wrow[qr];
-    const float sc = qscale[qr];
+    const float sc = (DT == kFp8) ? qscale[qr] * 0.5f : 0.5f;
 #pragma unroll
     for (int j = 0; j < T; ++j)
 #pragma unroll
       for (int i = 0; i < 4; ++i) wv[j][i] = wr[4 * G * j + 4 * (gq % G) + i] * sc;
+    if constexpr (DT == kFp8) {
+      al.load(lin[gq_a / G] + i_a * kD, kg);
+      const bool own = (gq % G) == 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) ls[i] = own ? lscale[qr][i] : 0.f;
+    }
   }
 
   // Gate-weighted ReLU sum over all heads of row (lane >> 4) / G for key
   // (lane & 15) of the fragment b; identical in every lane group of the row.
   __device__ __forceinline__ float score(const KeyFrag<DT>& b) const {
     float acc = 0.f;
+    if constexpr (DT == kFp8) {
+      // Software pipeline: the MFMA of tile j+1 is issued before the epilogue
+      // of tile j, so the matrix core and the VALU work side by side and only
+      // two accumulators are live.  The scheduling barriers keep the compiler
+      // from hoisting all MFMAs ahead (which would need 4 (T+1) accumulator
+      // registers and push operands into AGPRs).
+      v4f cl = mfma_fp8(al.v, b.v);
+      v4f c = mfma_fp8(a[0].v, b.v);
 #pragma unroll
-    for (int j = 0; j < T; ++j) {
-      v4f c = {0.f, 0.f, 0.f, 0.f};
-      if constexpr (DT == kFp8) {
-        c = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a[j].v, b.v, c, 0, 0, 0, 0, 0, 0);
-      } else {
+      for (int j = 1; j <= T; ++j) {
+        v4f nxt = c;
+        if (j < T) nxt = mfma_fp8(a[j].v, b.v);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc = fmaf(wv[j - 1][i], fabsf(c[i]), acc);
+        asm volatile("" : "+v"(acc));  // pins this epilogue between the barriers
+        __builtin_amdgcn_sched_barrier(0);
+        c = nxt;
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc = fmaf(ls[i], cl[i], acc);
+    } else {
+#pragma unroll
+      for (int j = 0; j < T; ++j) {
+        v4f c = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int s = 0; s < 4; ++s)
           c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(v8bf, a[j].v[s]),
                                                       __builtin_bit_cast(v8bf, b.v[s]), c, 0, 0, 0);
-      }
+        // w ReLU(x) = (w/2) |x| + (w/2) x: two FMAs, no max
 #pragma unroll
-      for (int i = 0; i < 4; ++i) acc = fmaf(wv[j][i], fmaxf(c[i], 0.f), acc);
+        for (int i = 0; i < 4; ++i) acc = fmaf(wv[j][i], c[i], fmaf(wv[j][i], fabsf(c[i]), acc));
+      }
     }
     if constexpr (G >= 2) acc += __shfl_xor(acc, 16, kWave);
     if constexpr (G >= 4) acc += __shfl_xor(acc, 32, kWave);

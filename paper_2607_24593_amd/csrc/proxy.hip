@@ -9,6 +9,7 @@
 //   bf16: mean of q_t; RNE to bf16
 // A group of one is copied unchanged.
 #include "launch.h"
+#include "mfma_tile.h"
 
 namespace pivot {
 
@@ -166,6 +167,53 @@ hipError_t launch_encode_e4m3(const float* x, uint8_t* out, int64_t n, hipStream
   if (n <= 0) return hipSuccess;
   int64_t blocks = (n + 1023) / 1024;
   hipLaunchKernelGGL(encode_e4m3_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, x, out, n);
+  return hipGetLastError();
+}
+
+}  // namespace pivot
+
+namespace pivot {
+
+// The linear part of the fp8 epilogue (mfma_tile.h): for each row,
+// u = sum_j (w_j * qscale / 2) * q8_j, a 128-vector, stored as four fp8 levels:
+// level l holds codes c_l = RNE((u - sum_{l'<l} sigma_l' c_l') / sigma_l) with
+// sigma_l = max|residual| / 448, so the remaining error shrinks ~16x per level.
+// One wave per row; lane l owns dims 2l and 2l+1.
+__global__ __launch_bounds__(256) void lin_kernel(const uint8_t* __restrict__ q, const float* __restrict__ q_scale,
+                                                  const float* __restrict__ w, int64_t r0, int64_t r1,
+                                                  uint8_t* __restrict__ lin, float* __restrict__ lin_scale) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = r0 + (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= r1) return;
+  const uint8_t* qr = q + row * (int64_t)(kH * kD);
+  const float* wr = w + row * kH;
+  const float half_scale = q_scale[row] * 0.5f;
+  float u0 = 0.f, u1 = 0.f;
+  for (int h = 0; h < kH; ++h) {
+    const float wh = wr[h] * half_scale;
+    const uint32_t pair = *reinterpret_cast<const uint16_t*>(qr + h * kD + 2 * lane);
+    u0 = fmaf(wh, __builtin_amdgcn_cvt_f32_fp8((int)pair, 0), u0);
+    u1 = fmaf(wh, __builtin_amdgcn_cvt_f32_fp8((int)pair, 1), u1);
+  }
+  uint8_t* out = lin + row * (int64_t)kLinBytes;
+#pragma unroll
+  for (int l = 0; l < kLinLevels; ++l) {
+    const float amax = wave_max(fmaxf(fabsf(u0), fabsf(u1)));
+    const float sigma = amax > 0.f ? amax / 448.0f : 1.0f;
+    const int word = __builtin_amdgcn_cvt_pk_fp8_f32(u0 / sigma, u1 / sigma, 0, false);
+    *reinterpret_cast<uint16_t*>(out + l * kD + 2 * lane) = (uint16_t)word;
+    u0 -= sigma * __builtin_amdgcn_cvt_f32_fp8(word, 0);
+    u1 -= sigma * __builtin_amdgcn_cvt_f32_fp8(word, 1);
+    if (lane == 0) lin_scale[row * kLinLevels + l] = sigma;
+  }
+}
+
+hipError_t launch_lin(const void* q, const float* q_scale, const float* w, int64_t r0, int64_t r1, uint8_t* lin,
+                      float* lin_scale, hipStream_t stream) {
+  if (r1 <= r0) return hipSuccess;
+  const int64_t blocks = (r1 - r0 + 3) / 4;
+  hipLaunchKernelGGL(lin_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, (const uint8_t*)q, q_scale, w, r0,
+                     r1, lin, lin_scale);
   return hipGetLastError();
 }
 

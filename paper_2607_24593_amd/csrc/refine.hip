@@ -28,8 +28,10 @@ struct CandSource {
 template <int DT>
 __global__ __launch_bounds__(256) void refine_kernel(const uint8_t* __restrict__ q,
                                                      const float* __restrict__ q_scale,
-                                                     const float* __restrict__ w, int n_q, int g, int n_groups,
-                                                     const uint8_t* __restrict__ k,
+                                                     const float* __restrict__ w,
+                                                     const uint8_t* __restrict__ lin,
+                                                     const float* __restrict__ lin_scale, int n_q, int g,
+                                                     int n_groups, const uint8_t* __restrict__ k,
                                                      const float* __restrict__ k_scale, int64_t k_seq_stride,
                                                      SeqTable st, int j0, const int32_t* __restrict__ cand, int c,
                                                      int m, int32_t* __restrict__ out_idx) {
@@ -53,6 +55,8 @@ __global__ __launch_bounds__(256) void refine_kernel(const uint8_t* __restrict__
     const int rows_here = min(4, gs - 4 * quad);
     const uint8_t* rows[4];
     const float* wrows[4];
+    const uint8_t* lrows[4];
+    const float* lsc[4];
     float qs[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
@@ -60,9 +64,11 @@ __global__ __launch_bounds__(256) void refine_kernel(const uint8_t* __restrict__
       rows[r] = q + row * Tile::ROW_BYTES;
       wrows[r] = w + row * kH;
       qs[r] = (DT == kFp8) ? q_scale[row] : 1.0f;
+      lrows[r] = (DT == kFp8) ? lin + row * kLinBytes : nullptr;
+      lsc[r] = (DT == kFp8) ? lin_scale + row * kLinLevels : nullptr;
     }
     Tile tile;
-    tile.load(rows, wrows, qs, lane);
+    tile.load(rows, wrows, qs, lrows, lsc, lane);
     const int nfrag = (nc + 15) >> 4;
     int f = wave;
     KeyFrag<DT> cur, nxt;
@@ -78,6 +84,7 @@ __global__ __launch_bounds__(256) void refine_kernel(const uint8_t* __restrict__
         nxt.load(kb + (int64_t)s_nxt * kD * EB, kg);
       }
       float acc = tile.score(cur);
+      asm volatile("" : "+v"(acc));  // keep the epilogue ahead of the store's branch
       const int slot = 16 * f + lr;
       if (slot < nc && kg < rows_here) {
         if constexpr (DT == kFp8) acc *= ksb[s_cur];
@@ -100,8 +107,9 @@ __global__ __launch_bounds__(256) void refine_kernel(const uint8_t* __restrict__
   }
 }
 
-hipError_t launch_refine(int dtype, const void* q, const float* q_scale, const float* w, int n_q, int g,
-                         int n_groups, const void* k, const float* k_scale, int64_t k_seq_stride,
+hipError_t launch_refine(int dtype, const void* q, const float* q_scale, const float* w, const uint8_t* lin,
+                         const float* lin_scale, int n_q, int g, int n_groups, const void* k,
+                         const float* k_scale, int64_t k_seq_stride,
                          const SeqTable& st, int j0, int j1, const int32_t* cand, int c, int m,
                          int32_t* out_idx, hipStream_t stream) {
   if (j1 <= j0 || st.n <= 0) return hipSuccess;
@@ -109,12 +117,12 @@ hipError_t launch_refine(int dtype, const void* q, const float* q_scale, const f
   dim3 grid((unsigned)(j1 - j0), (unsigned)st.n);
   if (dtype == kFp8) {
     (void)hipFuncSetAttribute((const void*)refine_kernel<kFp8>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    hipLaunchKernelGGL(refine_kernel<kFp8>, grid, dim3(256), lds, stream, (const uint8_t*)q, q_scale, w, n_q, g,
-                       n_groups, (const uint8_t*)k, k_scale, k_seq_stride, st, j0, cand, c, m, out_idx);
+    hipLaunchKernelGGL(refine_kernel<kFp8>, grid, dim3(256), lds, stream, (const uint8_t*)q, q_scale, w, lin, lin_scale,
+                       n_q, g, n_groups, (const uint8_t*)k, k_scale, k_seq_stride, st, j0, cand, c, m, out_idx);
   } else {
     (void)hipFuncSetAttribute((const void*)refine_kernel<kBf16>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    hipLaunchKernelGGL(refine_kernel<kBf16>, grid, dim3(256), lds, stream, (const uint8_t*)q, q_scale, w, n_q, g,
-                       n_groups, (const uint8_t*)k, k_scale, k_seq_stride, st, j0, cand, c, m, out_idx);
+    hipLaunchKernelGGL(refine_kernel<kBf16>, grid, dim3(256), lds, stream, (const uint8_t*)q, q_scale, w, lin, lin_scale,
+                       n_q, g, n_groups, (const uint8_t*)k, k_scale, k_seq_stride, st, j0, cand, c, m, out_idx);
   }
   return hipGetLastError();
 }

@@ -24,7 +24,9 @@ namespace pivot {
 template <int DT, int R, bool KSPLIT>
 __global__ __launch_bounds__(256) void score_kernel(const uint8_t* __restrict__ q,
                                                     const float* __restrict__ q_scale,
-                                                    const float* __restrict__ w, int64_t q_seq_rows,
+                                                    const float* __restrict__ w,
+                                                    const uint8_t* __restrict__ lin,
+                                                    const float* __restrict__ lin_scale, int64_t q_seq_rows,
                                                     const uint8_t* __restrict__ k,
                                                     const float* __restrict__ k_scale, int64_t k_seq_stride,
                                                     SeqTable st, RowSpace rs, float* __restrict__ out,
@@ -49,6 +51,8 @@ __global__ __launch_bounds__(256) void score_kernel(const uint8_t* __restrict__ 
 
   const uint8_t* rows[R];
   const float* wrows[R];
+  const uint8_t* lrows[R];
+  const float* lsc[R];
   float qs[R];
 #pragma unroll
   for (int r = 0; r < R; ++r) {
@@ -57,9 +61,11 @@ __global__ __launch_bounds__(256) void score_kernel(const uint8_t* __restrict__ 
     rows[r] = q + row * Tile::ROW_BYTES;
     wrows[r] = w + row * kH;
     qs[r] = (DT == kFp8) ? q_scale[row] : 1.0f;
+    lrows[r] = (DT == kFp8) ? lin + row * kLinBytes : nullptr;
+    lsc[r] = (DT == kFp8) ? lin_scale + row * kLinLevels : nullptr;
   }
   Tile tile;
-  tile.load(rows, wrows, qs, lane);
+  tile.load(rows, wrows, qs, lrows, lsc, lane);
 
   const uint8_t* kb = k + (int64_t)b * k_seq_stride * kD * EB;
   const float* ksb = (DT == kFp8) ? k_scale + (int64_t)b * k_seq_stride : nullptr;
@@ -70,62 +76,76 @@ __global__ __launch_bounds__(256) void score_kernel(const uint8_t* __restrict__ 
   const int64_t my_lim = row_limit(st, rs, b, my_i);
   float* orow = out + ((int64_t)b * nrows + (my_i - rs.i0)) * ld;
 
-  const int stride = KSPLIT ? 64 : 16;
+  // Two key fragments alternate: while one is scored the other is loading
+  // (the second wave on the SIMD covers the rest of the latency).  Loads past
+  // the segment are clamped to a valid key (their data is never used), so no
+  // load is conditional.
+  const int64_t S = KSPLIT ? 64 : 16;
   int64_t t = seg0 + (KSPLIT ? 16 * wave : 0);
-  KeyFrag<DT> cur, nxt;
-  if (t < seg1) cur.load(kb + min(t + lr, lim_max) * kD * EB, kg);
-  for (; t < seg1; t += stride) {
-    const int64_t tn = t + stride;
-    if (tn < seg1) nxt.load(kb + min(tn + lr, lim_max) * kD * EB, kg);
-    float acc = tile.score(cur);
-    const int64_t s = t + lr;
+  auto key_at = [&](int64_t base) { return kb + min(base + lr, lim_max) * kD * EB; };
+  auto emit = [&](float acc, int64_t base) {
+    // keep the epilogue ahead of the store's branch (no sinking into it)
+    asm volatile("" : "+v"(acc));
+    const int64_t s = base + lr;
     if (writer && s <= my_lim) {
       if constexpr (DT == kFp8) acc *= ksb[s];
       orow[s] = acc;
     }
-    cur = nxt;
+  };
+  KeyFrag<DT> f0, f1;
+  f0.load(key_at(t), kg);
+  f1.load(key_at(t + S), kg);
+  for (; t < seg1; t += 2 * S) {
+    emit(tile.score(f0), t);
+    f0.load(key_at(t + 2 * S), kg);
+    if (t + S >= seg1) break;
+    emit(tile.score(f1), t + S);
+    f1.load(key_at(t + 3 * S), kg);
   }
 }
 
 template <int DT, int R, bool KSPLIT>
-static hipError_t run_score(const void* q, const float* qs, const float* w, int64_t q_seq_rows, const void* k,
-                            const float* ks, int64_t kstride, const SeqTable& st, const RowSpace& rs,
-                            int64_t lim_max, float* out, int64_t ld, int seg, hipStream_t stream) {
+static hipError_t run_score(const void* q, const float* qs, const float* w, const uint8_t* lin, const float* lsc,
+                            int64_t q_seq_rows, const void* k, const float* ks, int64_t kstride, const SeqTable& st,
+                            const RowSpace& rs, int64_t lim_max, float* out, int64_t ld, int seg,
+                            hipStream_t stream) {
   constexpr int RB = KSPLIT ? R : 4 * R;
   const int nrows = rs.i1 - rs.i0;
   const int64_t nseg = ((lim_max + 1 + seg - 1) / seg + 7) / 8 * 8;
   const int64_t nblk = (int64_t)st.n * ((nrows + RB - 1) / RB);
   if (nseg > 0x7FFFFFFF || nblk > 65535) return hipErrorInvalidConfiguration;
   hipLaunchKernelGGL((score_kernel<DT, R, KSPLIT>), dim3((unsigned)nseg, (unsigned)nblk), dim3(256), 0, stream,
-                     (const uint8_t*)q, qs, w, q_seq_rows, (const uint8_t*)k, ks, kstride, st, rs, out, ld, seg);
+                     (const uint8_t*)q, qs, w, lin, lsc, q_seq_rows, (const uint8_t*)k, ks, kstride, st, rs, out,
+                     ld, seg);
   return hipGetLastError();
 }
 
-hipError_t launch_score(int dtype, const void* q, const float* q_scale, const float* w, int64_t q_seq_rows,
-                        const void* k, const float* k_scale, int64_t k_seq_stride, const SeqTable& st,
-                        const RowSpace& rs, int64_t lim_max, float* out, int64_t ld, hipStream_t stream) {
+hipError_t launch_score(int dtype, const void* q, const float* q_scale, const float* w, const uint8_t* lin,
+                        const float* lin_scale, int64_t q_seq_rows, const void* k, const float* k_scale,
+                        int64_t k_seq_stride, const SeqTable& st, const RowSpace& rs, int64_t lim_max, float* out,
+                        int64_t ld, hipStream_t stream) {
   const int nrows = rs.i1 - rs.i0;
   if (nrows <= 0 || lim_max < 0 || st.n <= 0) return hipSuccess;
   if (dtype == kFp8) {
     if (nrows >= 16)
-      return run_score<kFp8, 4, false>(q, q_scale, w, q_seq_rows, k, k_scale, k_seq_stride, st, rs, lim_max,
+      return run_score<kFp8, 4, false>(q, q_scale, w, lin, lin_scale, q_seq_rows, k, k_scale, k_seq_stride, st, rs, lim_max,
                                        out, ld, 4096, stream);
     if (nrows == 1)
-      return run_score<kFp8, 1, true>(q, q_scale, w, q_seq_rows, k, k_scale, k_seq_stride, st, rs, lim_max,
+      return run_score<kFp8, 1, true>(q, q_scale, w, lin, lin_scale, q_seq_rows, k, k_scale, k_seq_stride, st, rs, lim_max,
                                       out, ld, 2048, stream);
     if (nrows == 2)
-      return run_score<kFp8, 2, true>(q, q_scale, w, q_seq_rows, k, k_scale, k_seq_stride, st, rs, lim_max,
+      return run_score<kFp8, 2, true>(q, q_scale, w, lin, lin_scale, q_seq_rows, k, k_scale, k_seq_stride, st, rs, lim_max,
                                       out, ld, 2048, stream);
-    return run_score<kFp8, 4, true>(q, q_scale, w, q_seq_rows, k, k_scale, k_seq_stride, st, rs, lim_max, out,
+    return run_score<kFp8, 4, true>(q, q_scale, w, lin, lin_scale, q_seq_rows, k, k_scale, k_seq_stride, st, rs, lim_max, out,
                                     ld, 2048, stream);
   }
   if (nrows >= 16)
-    return run_score<kBf16, 2, false>(q, nullptr, w, q_seq_rows, k, nullptr, k_seq_stride, st, rs, lim_max,
+    return run_score<kBf16, 2, false>(q, nullptr, w, nullptr, nullptr, q_seq_rows, k, nullptr, k_seq_stride, st, rs, lim_max,
                                       out, ld, 2048, stream);
   if (nrows == 1)
-    return run_score<kBf16, 1, true>(q, nullptr, w, q_seq_rows, k, nullptr, k_seq_stride, st, rs, lim_max,
+    return run_score<kBf16, 1, true>(q, nullptr, w, nullptr, nullptr, q_seq_rows, k, nullptr, k_seq_stride, st, rs, lim_max,
                                      out, ld, 2048, stream);
-  return run_score<kBf16, 2, true>(q, nullptr, w, q_seq_rows, k, nullptr, k_seq_stride, st, rs, lim_max, out,
+  return run_score<kBf16, 2, true>(q, nullptr, w, nullptr, nullptr, q_seq_rows, k, nullptr, k_seq_stride, st, rs, lim_max, out,
                                    ld, 2048, stream);
 }
 

@@ -133,29 +133,35 @@ def test_empty_call_is_ok_without_workspace():
 
 
 def test_workspace_size_closed_form():
+    up = lambda n: (n + 255) // 256 * 256  # noqa: E731
+    lin = lambda rows: up(rows * 512) + up(rows * 16)  # noqa: E731  (fp8 epilogue's linear term)
     # dense, one sequence: 100 rows x ld(1000)=1024 fp32
     a = args(n_q=100, q_pos0=900)
-    assert pv.pivot_workspace_size(a, pv.PIVOT_DENSE) == 100 * 1024 * 4
-    # Refine, g=4, c=16, guardrail at c: all 25 groups start at t0 >= 900 >= c
+    assert pv.pivot_workspace_size(a, pv.PIVOT_DENSE) == lin(100) + 100 * 1024 * 4
+    b = args(n_q=100, q_pos0=900, dtype=pv.PIVOT_DT_BF16, scales=False)
+    assert pv.pivot_workspace_size(b, pv.PIVOT_DENSE) == 100 * 1024 * 4
+    # Refine, g=4, c=16, guardrail at c: all 25 groups start at t0 >= 900 >= c;
+    # members need the linear term (Refine re-scores them), and so do proxies
     ng = 25
-    fixed = 0
-    for nbytes in (ng * 64 * 128, ng * 4, ng * 64 * 4, ng * 16 * 4):
-        fixed += (nbytes + 255) // 256 * 256
-    assert pv.pivot_workspace_size(a, pv.PIVOT_REFINE, 4, 16) == fixed + ng * 1024 * 4
-    # Reuse needs no candidate buffer
-    fixed_r = fixed - (ng * 16 * 4 + 255) // 256 * 256
-    assert pv.pivot_workspace_size(a, pv.PIVOT_REUSE, 4, 16) == fixed_r + ng * 1024 * 4
+    proxies = up(ng * 64 * 128) + up(ng * 4) + up(ng * 64 * 4)
+    cand = up(ng * 16 * 4)
+    assert pv.pivot_workspace_size(a, pv.PIVOT_REFINE, 4, 16) == lin(100) + lin(ng) + proxies + cand + ng * 1024 * 4
+    # Reuse: no candidate buffer, no member rows to re-score
+    assert pv.pivot_workspace_size(a, pv.PIVOT_REUSE, 4, 16) == lin(ng) + proxies + ng * 1024 * 4
     # long prefix: score tiles stay near 1 GiB
     a = args(n_q=16384, q_pos0=262144 - 16384)
-    assert pv.pivot_workspace_size(a, pv.PIVOT_DENSE) == 1 << 30
+    assert pv.pivot_workspace_size(a, pv.PIVOT_DENSE) == lin(16384) + (1 << 30)
 
 
 def test_stage_validation():
     L = pv.lib()
-    assert L.pivot_score_rows(1, 64, 128, 4, FAKE, FAKE, FAKE, FAKE, FAKE, 10, 1, FAKE, 5, None) == \
+    assert L.pivot_score_rows(1, 64, 128, 4, FAKE, FAKE, FAKE, FAKE, FAKE, 10, 1, FAKE, 5, FAKE, 1 << 20, None) == \
         pv.PIVOT_ERR_INVALID_ARG                               # ld < lim + 1
-    assert L.pivot_score_rows(1, 32, 128, 4, FAKE, FAKE, FAKE, FAKE, FAKE, 10, 1, FAKE, 64, None) == \
+    assert L.pivot_score_rows(1, 32, 128, 4, FAKE, FAKE, FAKE, FAKE, FAKE, 10, 1, FAKE, 64, FAKE, 1 << 20, None) == \
         pv.PIVOT_ERR_UNSUPPORTED
+    need = pv.score_rows_workspace(4)
+    assert L.pivot_score_rows(1, 64, 128, 4, FAKE, FAKE, FAKE, FAKE, FAKE, 10, 1, FAKE, 64, FAKE, need - 1, None) == \
+        pv.PIVOT_ERR_WORKSPACE
     assert L.pivot_topk_rows(2, FAKE, 10, 8, 4, 4, FAKE, None) == pv.PIVOT_ERR_INVALID_ARG  # 12 > ld
     assert L.pivot_topk_rows(0, None, 0, 0, 0, 4, None, None) == pv.PIVOT_OK
     assert L.pivot_proxy_rows(1, 64, 128, 8, 0, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == \
