@@ -90,6 +90,7 @@ struct Plan {
   // workspace layout
   size_t off_pq = 0, off_psc = 0, off_pw = 0, off_cand = 0, off_scores = 0, fixed = 0;
   size_t off_qlin = 0, off_qlsc = 0, off_plin = 0, off_plsc = 0;  // fp8 epilogue's linear term
+  size_t off_rsc = 0;                                              // Refine member scores
   bool qlin = false, plin = false;
 };
 
@@ -131,6 +132,7 @@ pivot_status make_plan(const pivot_args* a, int mode, int g, int c, int dense_be
     if (c < 0) return fail(PIVOT_ERR_INVALID_ARG, "c must be >= 0");
     if (mode == PIVOT_REFINE && c < a->topk) return fail(PIVOT_ERR_INVALID_ARG, "Refine needs c >= topk");
     if (mode == PIVOT_REFINE && c > 8192) return fail(PIVOT_ERR_UNSUPPORTED, "Refine supports c <= 8192");
+    if (mode == PIVOT_REFINE && g > 65535) return fail(PIVOT_ERR_UNSUPPORTED, "Refine supports g <= 65535");
   } else {
     g = 1;
     c = 0;
@@ -196,6 +198,8 @@ pivot_status make_plan(const pivot_args* a, int mode, int g, int c, int dense_be
     p.off_pw = off;
     off = align_up(off + ng * kH * sizeof(float));
     if (mode == PIVOT_REFINE) {
+      p.off_rsc = off;
+      off = align_up(off + ng * (size_t)g * c * sizeof(float));
       p.off_cand = off;
       off = align_up(off + ng * (size_t)c * sizeof(int32_t));
     }
@@ -484,6 +488,8 @@ pivot_status pivot_group_index(const pivot_args* a, int32_t mode, int32_t g, int
                                          (const uint8_t*)a->k + (size_t)b0 * a->k_seq_stride * kD * p.EB,
                                          a->k_scale ? a->k_scale + (size_t)b0 * a->k_seq_stride : nullptr,
                                          a->k_seq_stride, st, p.proxy_lo, p.n_groups, cb, c, p.topk,
+                                         reinterpret_cast<float*>(ws + p.off_rsc) +
+                                             (size_t)b0 * p.n_groups * p.g * c,
                                          a->out_idx + qoff * p.topk, stream);
                   }),
                   "refine kernel");

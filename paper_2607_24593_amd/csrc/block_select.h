@@ -7,8 +7,9 @@
 // the tied elements pick the lowest ones.  A final pass emits every element
 // above the threshold.  Positions must be distinct non-negative int32.
 //
-// Sources provide n() and get(e, key, pos) for e in [0, n()); they are
-// enumerated with a thread stride, so any memory (LDS or global) works.
+// A source provides visit(f), calling f(key, pos) for each of the calling
+// thread's elements; every thread of the workgroup calls it.  Sources may keep
+// their elements in registers, LDS or global memory.
 #pragma once
 
 #include "device_common.h"
@@ -55,18 +56,14 @@ __device__ __forceinline__ void find_digit(SelectShared& sh, uint32_t rem) {
 template <int THREADS, class Src, class Emit>
 __device__ void block_select(const Src& src, uint32_t need, SelectShared& sh, Emit emit) {
   const int tid = threadIdx.x;
-  const int n = src.n();
-  if (need == 0 || n <= 0) return;
+  if (need == 0) return;
   uint32_t prefix = 0, mask = 0, rem = need, equal = 0;
   for (int shift = 24; shift >= 0; shift -= 8) {
     for (int i = tid; i < 256; i += THREADS) sh.hist[i] = 0;
     __syncthreads();
-    for (int e = tid; e < n; e += THREADS) {
-      uint32_t key;
-      int32_t pos;
-      src.get(e, key, pos);
+    src.visit([&](uint32_t key, int32_t) {
       if ((key & mask) == prefix) atomicAdd(&sh.hist[(key >> shift) & 255u], 1u);
-    }
+    });
     __syncthreads();
     find_digit<true>(sh, rem);
     __syncthreads();
@@ -83,13 +80,10 @@ __device__ void block_select(const Src& src, uint32_t need, SelectShared& sh, Em
     for (int shift = 24; shift >= 0; shift -= 8) {
       for (int i = tid; i < 256; i += THREADS) sh.hist[i] = 0;
       __syncthreads();
-      for (int e = tid; e < n; e += THREADS) {
-        uint32_t key;
-        int32_t pos;
-        src.get(e, key, pos);
+      src.visit([&](uint32_t key, int32_t pos) {
         const uint32_t p = (uint32_t)pos;
         if (key == T && (p & imask) == ipref) atomicAdd(&sh.hist[(p >> shift) & 255u], 1u);
-      }
+      });
       __syncthreads();
       find_digit<false>(sh, rem);
       __syncthreads();
@@ -99,13 +93,22 @@ __device__ void block_select(const Src& src, uint32_t need, SelectShared& sh, Em
       __syncthreads();
     }
   }
-  for (int e = tid; e < n; e += THREADS) {
-    uint32_t key;
-    int32_t pos;
-    src.get(e, key, pos);
+  src.visit([&](uint32_t key, int32_t pos) {
     if (key > T || (key == T && (all_ties || (uint32_t)pos <= ipref))) emit(pos);
-  }
+  });
   __syncthreads();
 }
+
+// Elements e = tid, tid + THREADS, ... < count of (key[], pos[]) arrays.
+template <int THREADS>
+struct ArraySource {
+  const uint32_t* key;
+  const int32_t* pos;
+  int count;
+  template <class F>
+  __device__ __forceinline__ void visit(F f) const {
+    for (int e = threadIdx.x; e < count; e += THREADS) f(key[e], pos[e]);
+  }
+};
 
 }  // namespace pivot

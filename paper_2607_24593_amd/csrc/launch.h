@@ -43,12 +43,13 @@ hipError_t launch_score(int dtype, const void* q, const float* q_scale, const fl
 hipError_t launch_topk(const float* scores, int64_t ld, const SeqTable& st, const RowSpace& rs,
                        const OutDesc& od, hipStream_t stream);
 
-// Refine (Eqs. 8-9) for groups [j0, j1) with j >= first_proxy[b].
+// Refine (Eqs. 8-9) for groups [j0, j1) with j >= first_proxy[b]: re-score
+// the candidates into rescore [B, n_groups, g, c] fp32, then select top-m.
 hipError_t launch_refine(int dtype, const void* q, const float* q_scale, const float* w, const uint8_t* lin,
                          const float* lin_scale, int n_q, int g, int n_groups, const void* k,
-                         const float* k_scale, int64_t k_seq_stride,
-                         const SeqTable& st, int j0, int j1, const int32_t* cand, int c, int m,
-                         int32_t* out_idx, hipStream_t stream);
+                         const float* k_scale, int64_t k_seq_stride, const SeqTable& st, int j0, int j1,
+                         const int32_t* cand, int c, int m, float* rescore, int32_t* out_idx,
+                         hipStream_t stream);
 
 // Fill rows (b, j) with j < first_proxy[b], j in [j0, j1), of a [B, per_seq, width] int32 array.
 hipError_t launch_fill_guardrail(int32_t* base, int per_seq, int width, const SeqTable& st, int j0, int j1,

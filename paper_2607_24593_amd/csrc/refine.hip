@@ -1,129 +1,174 @@
 // PIVOT-Refine fine step (Sec. 4.4 Eqs. 8-9): every member of a group
-// re-scores the group's candidate set C with its own query and gates and keeps
-// its own top-k.
+// re-scores the group's candidate set C with its own query and gates (Eq. 8)
+// and keeps its own top-k (Eq. 9).
 //
-// One workgroup (4 waves) per group.  Members are taken four at a time: the
-// four rows sit in every wave's registers as MFMA A operands (mfma_tile.h) and
-// the waves split C into 16-candidate fragments, each lane gathering 32 bytes
-// of one candidate key by index.  Scores are kept in LDS as order-preserving
-// keys (four rows of |C|), then block_select() takes each member's top-k with
-// ties broken by lower position.
+// rescore_kernel: one workgroup (4 waves) per group and block of R members
+// (R = 4 for fp8, 2 for bf16), held as the A operands of the MFMA row tile
+// (mfma_tile.h); the waves split C into 16-candidate fragments.  The candidate positions are staged in
+// LDS, so each lane reads its position there and gathers 32 bytes of that key
+// two fragments ahead of its use.  Scores before the key scale go to a
+// [group, member, |C|] fp32 buffer (it stays in the last-level cache for the
+// select that follows, which applies the key scale).
+//
+// topk_short_kernel: one workgroup per (group, member) row of |C| <= 8192
+// scores; each thread keeps its share of (key, position) pairs in registers
+// and block_select() takes the top-k, ties broken by lower position.
 #include "block_select.h"
 #include "launch.h"
 #include "mfma_tile.h"
 
 namespace pivot {
 
-struct CandSource {
-  const uint32_t* key;
-  const int32_t* pos;
-  int count;
-  __device__ int n() const { return count; }
-  __device__ void get(int e, uint32_t& k, int32_t& p) const {
-    k = key[e];
-    p = pos[e];
-  }
-};
+constexpr int kMaxCand = 8192;
 
-template <int DT>
-__global__ __launch_bounds__(256) void refine_kernel(const uint8_t* __restrict__ q,
-                                                     const float* __restrict__ q_scale,
-                                                     const float* __restrict__ w,
-                                                     const uint8_t* __restrict__ lin,
-                                                     const float* __restrict__ lin_scale, int n_q, int g,
-                                                     int n_groups, const uint8_t* __restrict__ k,
-                                                     const float* __restrict__ k_scale, int64_t k_seq_stride,
-                                                     SeqTable st, int j0, const int32_t* __restrict__ cand, int c,
-                                                     int m, int32_t* __restrict__ out_idx) {
-  using Tile = RowTile<DT, 4>;
+template <int DT, int R>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void rescore_kernel(
+    const uint8_t* __restrict__ q, const float* __restrict__ q_scale, const float* __restrict__ w,
+    const uint8_t* __restrict__ lin, const float* __restrict__ lin_scale, int n_q, int g, int n_groups,
+    const uint8_t* __restrict__ k, int64_t k_seq_stride, SeqTable st, int j0, const int32_t* __restrict__ cand,
+    int c, float* __restrict__ rsc) {
+  using Tile = RowTile<DT, R>;
   constexpr int EB = Tile::EB;
-  extern __shared__ uint32_t skeys[];  // [4][c]
-  __shared__ SelectShared sel;
-  const int j = j0 + blockIdx.x, b = blockIdx.y;
+  __shared__ int32_t spos[kMaxCand];
+  const int j = j0 + blockIdx.x, b = blockIdx.y, blk = blockIdx.z;  // members [R blk, R blk + R)
   if (b >= st.n || j >= n_groups || j < st.first_proxy[b]) return;
+  const int gs = min(g, n_q - j * g);
+  if (R * blk >= gs) return;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int64_t t0 = (int64_t)st.q_pos0[b] + (int64_t)j * g;
   const int nc = (int)min((int64_t)c, t0 + 1);
-  const int gs = min(g, n_q - j * g);
+  const int rows_here = min(R, gs - R * blk);
   const int32_t* crow = cand + ((int64_t)b * n_groups + j) * c;
-  const int64_t r0 = (int64_t)b * n_q + (int64_t)j * g;
+  const int64_t r0 = (int64_t)b * n_q + (int64_t)j * g + R * blk;
   const uint8_t* kb = k + (int64_t)b * k_seq_stride * kD * EB;
-  const float* ksb = (DT == kFp8) ? k_scale + (int64_t)b * k_seq_stride : nullptr;
   const int lr = lane & 15, kg = lane >> 4;
+  for (int e = tid; e < nc; e += 256) spos[e] = crow[e];
 
-  for (int quad = 0; quad * 4 < gs; ++quad) {
-    const int rows_here = min(4, gs - 4 * quad);
-    const uint8_t* rows[4];
-    const float* wrows[4];
-    const uint8_t* lrows[4];
-    const float* lsc[4];
-    float qs[4];
+  const uint8_t* rows[R];
+  const float* wrows[R];
+  const uint8_t* lrows[R];
+  const float* lsc[R];
+  float qs[R];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int64_t row = r0 + 4 * quad + min(r, rows_here - 1);
-      rows[r] = q + row * Tile::ROW_BYTES;
-      wrows[r] = w + row * kH;
-      qs[r] = (DT == kFp8) ? q_scale[row] : 1.0f;
-      lrows[r] = (DT == kFp8) ? lin + row * kLinBytes : nullptr;
-      lsc[r] = (DT == kFp8) ? lin_scale + row * kLinLevels : nullptr;
-    }
-    Tile tile;
-    tile.load(rows, wrows, qs, lrows, lsc, lane);
-    const int nfrag = (nc + 15) >> 4;
-    int f = wave;
-    KeyFrag<DT> cur, nxt;
-    int32_t s_cur = 0, s_nxt = 0;
-    if (f < nfrag) {
-      s_cur = crow[min(16 * f + lr, nc - 1)];
-      cur.load(kb + (int64_t)s_cur * kD * EB, kg);
-    }
-    for (; f < nfrag; f += 4) {
-      const int fn = f + 4;
-      if (fn < nfrag) {
-        s_nxt = crow[min(16 * fn + lr, nc - 1)];
-        nxt.load(kb + (int64_t)s_nxt * kD * EB, kg);
-      }
-      float acc = tile.score(cur);
-      asm volatile("" : "+v"(acc));  // keep the epilogue ahead of the store's branch
-      const int slot = 16 * f + lr;
-      if (slot < nc && kg < rows_here) {
-        if constexpr (DT == kFp8) acc *= ksb[s_cur];
-        skeys[kg * c + slot] = float_key(acc);
-      }
-      cur = nxt;
-      s_cur = s_nxt;
-    }
-    __syncthreads();
-    for (int r = 0; r < rows_here; ++r) {
-      int32_t* orow = out_idx + (r0 + 4 * quad + r) * m;
-      if (tid == 0) sel.emitted = 0;
-      __syncthreads();
-      const int need = min(m, nc);
-      CandSource src{skeys + r * c, crow, nc};
-      block_select<256>(src, (uint32_t)need, sel, [&](int32_t p) { orow[atomicAdd(&sel.emitted, 1)] = p; });
-      for (int p = need + tid; p < m; p += 256) orow[p] = -1;
-    }
-    __syncthreads();
+  for (int r = 0; r < R; ++r) {
+    const int64_t row = r0 + min(r, rows_here - 1);
+    rows[r] = q + row * Tile::ROW_BYTES;
+    wrows[r] = w + row * kH;
+    qs[r] = (DT == kFp8) ? q_scale[row] : 1.0f;
+    lrows[r] = (DT == kFp8) ? lin + row * kLinBytes : nullptr;
+    lsc[r] = (DT == kFp8) ? lin_scale + row * kLinLevels : nullptr;
   }
+  Tile tile;
+  tile.load(rows, wrows, qs, lrows, lsc, lane);
+  __syncthreads();  // candidate positions staged
+
+  const int qr = kg / Tile::G;
+  const bool writer = (kg % Tile::G) == 0 && qr < rows_here;
+  float* mrow = rsc + (((int64_t)b * n_groups + j) * g + R * blk + qr) * (int64_t)c;
+  const int nfrag = (nc + 15) >> 4;
+  constexpr int S = 4;  // fragment stride between the waves
+  auto pos_of = [&](int f) { return spos[min(16 * f + lr, nc - 1)]; };
+  auto emit = [&](float acc, int f) {
+    asm volatile("" : "+v"(acc));  // keep the epilogue ahead of the store's branch
+    const int slot = 16 * f + lr;
+    if (writer && slot < nc) mrow[slot] = acc;
+  };
+  // two fragments in flight per wave; loads past the end repeat the last
+  // candidate (never stored)
+  int f = wave;
+  KeyFrag<DT> k0, k1;
+  k0.load(kb + (int64_t)pos_of(f) * kD * EB, kg);
+  k1.load(kb + (int64_t)pos_of(f + S) * kD * EB, kg);
+  for (; f < nfrag; f += 2 * S) {
+    int pn = pos_of(f + 2 * S);
+    emit(tile.score(k0), f);
+    k0.load(kb + (int64_t)pn * kD * EB, kg);
+    if (f + S >= nfrag) break;
+    pn = pos_of(f + 3 * S);
+    emit(tile.score(k1), f + S);
+    k1.load(kb + (int64_t)pn * kD * EB, kg);
+  }
+}
+
+// (key, position) pairs e = tid + 256 v held in registers.
+template <int V>
+struct RegSource {
+  uint32_t key[V];
+  int32_t pos[V];
+  int count;
+  template <class F>
+  __device__ __forceinline__ void visit(F f) const {
+#pragma unroll
+    for (int v = 0; v < V; ++v)
+      if ((int)threadIdx.x + 256 * v < count) f(key[v], pos[v]);
+  }
+};
+
+template <int V>
+__global__ __launch_bounds__(256) void topk_short_kernel(const float* __restrict__ rsc,
+                                                         const int32_t* __restrict__ cand,
+                                                         const float* __restrict__ k_scale, int64_t k_seq_stride,
+                                                         int n_q, int g, int n_groups, SeqTable st, int j0, int c,
+                                                         int m, int32_t* __restrict__ out_idx) {
+  __shared__ SelectShared sel;
+  const int j = j0 + blockIdx.x, b = blockIdx.y, member = blockIdx.z;
+  if (b >= st.n || j >= n_groups || j < st.first_proxy[b]) return;
+  const int gs = min(g, n_q - j * g);
+  if (member >= gs) return;
+  const int tid = threadIdx.x;
+  const int64_t t0 = (int64_t)st.q_pos0[b] + (int64_t)j * g;
+  const int nc = (int)min((int64_t)c, t0 + 1);
+  const int64_t grp = (int64_t)b * n_groups + j;
+  const float* srow = rsc + (grp * g + member) * (int64_t)c;
+  const int32_t* crow = cand + grp * c;
+  int32_t* orow = out_idx + ((int64_t)b * n_q + (int64_t)j * g + member) * m;
+
+  const float* ksb = k_scale ? k_scale + (int64_t)b * k_seq_stride : nullptr;
+  RegSource<V> src;
+  src.count = nc;
+#pragma unroll
+  for (int v = 0; v < V; ++v) {
+    const int e = tid + 256 * v;
+    const bool ok = e < nc;
+    const int32_t p = ok ? crow[e] : 0;
+    const float f = ok ? srow[e] : 0.f;
+    src.key[v] = ok ? float_key(ksb ? f * ksb[p] : f) : 0u;
+    src.pos[v] = p;
+  }
+  if (tid == 0) sel.emitted = 0;
+  __syncthreads();
+  const int need = min(m, nc);
+  block_select<256>(src, (uint32_t)need, sel, [&](int32_t p) { orow[atomicAdd(&sel.emitted, 1)] = p; });
+  for (int p = need + tid; p < m; p += 256) orow[p] = -1;
 }
 
 hipError_t launch_refine(int dtype, const void* q, const float* q_scale, const float* w, const uint8_t* lin,
                          const float* lin_scale, int n_q, int g, int n_groups, const void* k,
-                         const float* k_scale, int64_t k_seq_stride,
-                         const SeqTable& st, int j0, int j1, const int32_t* cand, int c, int m,
-                         int32_t* out_idx, hipStream_t stream) {
+                         const float* k_scale, int64_t k_seq_stride, const SeqTable& st, int j0, int j1,
+                         const int32_t* cand, int c, int m, float* rescore, int32_t* out_idx,
+                         hipStream_t stream) {
   if (j1 <= j0 || st.n <= 0) return hipSuccess;
-  const size_t lds = (size_t)4 * c * sizeof(uint32_t);
-  dim3 grid((unsigned)(j1 - j0), (unsigned)st.n);
-  if (dtype == kFp8) {
-    (void)hipFuncSetAttribute((const void*)refine_kernel<kFp8>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    hipLaunchKernelGGL(refine_kernel<kFp8>, grid, dim3(256), lds, stream, (const uint8_t*)q, q_scale, w, lin, lin_scale,
-                       n_q, g, n_groups, (const uint8_t*)k, k_scale, k_seq_stride, st, j0, cand, c, m, out_idx);
-  } else {
-    (void)hipFuncSetAttribute((const void*)refine_kernel<kBf16>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    hipLaunchKernelGGL(refine_kernel<kBf16>, grid, dim3(256), lds, stream, (const uint8_t*)q, q_scale, w, lin, lin_scale,
-                       n_q, g, n_groups, (const uint8_t*)k, k_scale, k_seq_stride, st, j0, cand, c, m, out_idx);
-  }
+  if (c > kMaxCand) return hipErrorInvalidValue;
+  if (dtype == kFp8)
+    hipLaunchKernelGGL((rescore_kernel<kFp8, 4>), dim3((unsigned)(j1 - j0), (unsigned)st.n, (unsigned)((g + 3) / 4)),
+                       dim3(256), 0, stream, (const uint8_t*)q, q_scale, w, lin, lin_scale, n_q, g, n_groups,
+                       (const uint8_t*)k, k_seq_stride, st, j0, cand, c, rescore);
+  else
+    hipLaunchKernelGGL((rescore_kernel<kBf16, 2>), dim3((unsigned)(j1 - j0), (unsigned)st.n, (unsigned)((g + 1) / 2)),
+                       dim3(256), 0, stream, (const uint8_t*)q, q_scale, w, lin, lin_scale, n_q, g, n_groups,
+                       (const uint8_t*)k, k_seq_stride, st, j0, cand, c, rescore);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  dim3 sgrid((unsigned)(j1 - j0), (unsigned)st.n, (unsigned)g);
+  if (c <= 1024)
+    hipLaunchKernelGGL(topk_short_kernel<4>, sgrid, dim3(256), 0, stream, rescore, cand,
+                       dtype == kFp8 ? k_scale : nullptr, k_seq_stride, n_q, g, n_groups, st, j0, c, m, out_idx);
+  else if (c <= 4096)
+    hipLaunchKernelGGL(topk_short_kernel<16>, sgrid, dim3(256), 0, stream, rescore, cand,
+                       dtype == kFp8 ? k_scale : nullptr, k_seq_stride, n_q, g, n_groups, st, j0, c, m, out_idx);
+  else
+    hipLaunchKernelGGL(topk_short_kernel<32>, sgrid, dim3(256), 0, stream, rescore, cand,
+                       dtype == kFp8 ? k_scale : nullptr, k_seq_stride, n_q, g, n_groups, st, j0, c, m, out_idx);
   return hipGetLastError();
 }
 

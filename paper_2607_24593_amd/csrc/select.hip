@@ -17,7 +17,7 @@
 namespace pivot {
 
 constexpr int kSelThreads = 512;
-constexpr int kSelCap = 8192;
+constexpr int kSelCap = 6144;  // LDS: 16 KiB histogram + 48 KiB candidates -> two workgroups per CU
 
 struct TopkShared {
   uint32_t hist[4096];
@@ -28,24 +28,12 @@ struct TopkShared {
   int32_t ncand;
 };
 
-struct LdsSource {
-  const uint32_t* key;
-  const int32_t* pos;
-  int count;
-  __device__ int n() const { return count; }
-  __device__ void get(int e, uint32_t& k, int32_t& p) const {
-    k = key[e];
-    p = pos[e];
-  }
-};
-
 struct RowSource {
   const float* row;
   int count;
-  __device__ int n() const { return count; }
-  __device__ void get(int e, uint32_t& k, int32_t& p) const {
-    k = float_key(row[e]);
-    p = e;
+  template <class F>
+  __device__ __forceinline__ void visit(F f) const {
+    for (int e = threadIdx.x; e < count; e += kSelThreads) f(float_key(row[e]), e);
   }
 };
 
@@ -153,7 +141,7 @@ __global__ __launch_bounds__(kSelThreads) void topk_rows_kernel(const float* __r
       }
     });
     __syncthreads();
-    LdsSource src{sh.ckey, sh.cpos, sh.ncand};
+    ArraySource<kSelThreads> src{sh.ckey, sh.cpos, sh.ncand};
     block_select<kSelThreads>(src, (uint32_t)m - above, sh.sel, emit);
   } else {
     RowSource src{row, n};

@@ -144,7 +144,7 @@ def test_workspace_size_closed_form():
     # members need the linear term (Refine re-scores them), and so do proxies
     ng = 25
     proxies = up(ng * 64 * 128) + up(ng * 4) + up(ng * 64 * 4)
-    cand = up(ng * 16 * 4)
+    cand = up(ng * 16 * 4) + up(ng * 4 * 16 * 4)   # candidate sets + members' re-scores
     assert pv.pivot_workspace_size(a, pv.PIVOT_REFINE, 4, 16) == lin(100) + lin(ng) + proxies + cand + ng * 1024 * 4
     # Reuse: no candidate buffer, no member rows to re-score
     assert pv.pivot_workspace_size(a, pv.PIVOT_REUSE, 4, 16) == lin(ng) + proxies + ng * 1024 * 4
