@@ -44,12 +44,24 @@ constexpr int kLinBytes = kLinLevels * kD;  // fp8 codes of the four levels of u
 template <int DT>
 struct KeyFrag;
 
+// Buffer resource over [base, base + bytes): buffer loads through it are
+// range-checked by the hardware (reads past the end return zero).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
 template <>
 struct KeyFrag<kFp8> {
   v8i v;  // 32 E4M3 codes
   __device__ __forceinline__ void load(const uint8_t* key_row, int kg) {
     const v4i* p = reinterpret_cast<const v4i*>(key_row + 32 * kg);
     v4i lo = p[0], hi = p[1];
+    v = v8i{lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+  }
+  // key at byte offset `row_off` of the resource, this lane's 32 bytes
+  __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t r, uint32_t row_off, int kg) {
+    v4i lo = __builtin_amdgcn_raw_buffer_load_b128(r, row_off + 32 * kg, 0, 0);
+    v4i hi = __builtin_amdgcn_raw_buffer_load_b128(r, row_off + 32 * kg + 16, 0, 0);
     v = v8i{lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
   }
 };
@@ -61,6 +73,10 @@ struct KeyFrag<kBf16> {
     const v4i* p = reinterpret_cast<const v4i*>(key_row + 64 * kg);
 #pragma unroll
     for (int s = 0; s < 4; ++s) v[s] = p[s];
+  }
+  __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t r, uint32_t row_off, int kg) {
+#pragma unroll
+    for (int s = 0; s < 4; ++s) v[s] = __builtin_amdgcn_raw_buffer_load_b128(r, row_off + 64 * kg + 16 * s, 0, 0);
   }
 };
 

@@ -34,7 +34,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void r
   if (b >= st.n || j >= n_groups || j < st.first_proxy[b]) return;
   const int gs = min(g, n_q - j * g);
   if (R * blk >= gs) return;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
   const int64_t t0 = (int64_t)st.q_pos0[b] + (int64_t)j * g;
   const int nc = (int)min((int64_t)c, t0 + 1);
   const int rows_here = min(R, gs - R * blk);

@@ -13,9 +13,10 @@
 //              from L2 once and served to 4 waves from the vector L1;
 //   keys mode  (< 16 rows per sequence, decode): the 4 waves hold the same rows
 //              and split the keys.
-// Grid: x = key segment, y = row block.  Linear workgroup ids are dealt to the
-// 8 XCDs round robin, so with a segment count that is a multiple of 8 each XCD
-// always streams the same 1/8 of the keys and keeps it in its own L2.
+// Grid: x = key segment, y = row block, in linear order, so the causal
+// triangle's active (row block, segment) pairs spread evenly over the 8 XCDs
+// (pinning segments to XCDs would idle the XCDs that own the late segments of
+// short prefixes).  The segment length adapts to the launch size.
 #include "launch.h"
 #include "mfma_tile.h"
 
@@ -33,21 +34,37 @@ __global__ __launch_bounds__(256) void score_kernel(const uint8_t* __restrict__ 
                                                     int64_t ld, int seg_keys) {
   using Tile = RowTile<DT, R>;
   constexpr int EB = Tile::EB;
+  constexpr int KB = kD * EB;  // bytes per key
   constexpr int RB = KSPLIT ? R : 4 * R;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  __shared__ float sks[4096];  // the segment's key scales (fp8)
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
   const int nrows = rs.i1 - rs.i0;
   const int nbps = (nrows + RB - 1) / RB;
   const int b = blockIdx.y / nbps;
   if (b >= st.n) return;
-  const int i_w = rs.i0 + (blockIdx.y % nbps) * RB + (KSPLIT ? 0 : wave * R);
+  const int i_blk = rs.i0 + (blockIdx.y % nbps) * RB;
+  const int64_t seg0 = (int64_t)blockIdx.x * seg_keys;
 
+  // the workgroup's key range (uniform, so every wave reaches the barrier)
+  int64_t lim_blk = -1;
+  for (int r = 0; r < RB; ++r)
+    if (row_active(st, rs, b, i_blk + r)) lim_blk = max(lim_blk, row_limit(st, rs, b, i_blk + r));
+  if (lim_blk < seg0) return;
+  const int nseg_keys = (int)(min(seg0 + (int64_t)seg_keys, lim_blk + 1) - seg0);
+  const float* ksb = (DT == kFp8) ? k_scale + (int64_t)b * k_seq_stride + seg0 : nullptr;
+  if constexpr (DT == kFp8) {
+    for (int e = tid; e < nseg_keys; e += 256) sks[e] = ksb[e];
+    __syncthreads();
+  }
+
+  const int i_w = i_blk + (KSPLIT ? 0 : wave * R);
   int64_t lim_max = -1;
 #pragma unroll
   for (int r = 0; r < R; ++r)
     if (row_active(st, rs, b, i_w + r)) lim_max = max(lim_max, row_limit(st, rs, b, i_w + r));
-  const int64_t seg0 = (int64_t)blockIdx.x * seg_keys;
-  if (lim_max < seg0) return;  // waves are independent: no workgroup barrier follows
-  const int64_t seg1 = min(seg0 + (int64_t)seg_keys, lim_max + 1);
+  if (lim_max < seg0) return;  // no workgroup barrier follows
+  const int nkeys = (int)(min(seg0 + (int64_t)seg_keys, lim_max + 1) - seg0);  // this wave's keys
 
   const uint8_t* rows[R];
   const float* wrows[R];
@@ -67,52 +84,61 @@ __global__ __launch_bounds__(256) void score_kernel(const uint8_t* __restrict__ 
   Tile tile;
   tile.load(rows, wrows, qs, lrows, lsc, lane);
 
-  const uint8_t* kb = k + (int64_t)b * k_seq_stride * kD * EB;
-  const float* ksb = (DT == kFp8) ? k_scale + (int64_t)b * k_seq_stride : nullptr;
+  // keys of the segment through a range-checked buffer resource: offsets are
+  // 32-bit and fragments that run past the wave's last key read zeros
+  const __amdgpu_buffer_rsrc_t kr =
+      buffer_rsrc(k + ((int64_t)b * k_seq_stride + seg0) * KB, (uint32_t)nkeys * KB);
   const int lr = lane & 15, kg = lane >> 4;
   const int qr = kg / Tile::G;
   const int my_i = i_w + qr;
   const bool writer = (kg % Tile::G) == 0 && row_active(st, rs, b, my_i);
-  const int64_t my_lim = row_limit(st, rs, b, my_i);
-  float* orow = out + ((int64_t)b * nrows + (my_i - rs.i0)) * ld;
+  const int my_n = (int)min((int64_t)nkeys, row_limit(st, rs, b, my_i) + 1 - seg0);  // keys this row takes
+  float* orow = out + ((int64_t)b * nrows + (my_i - rs.i0)) * ld + seg0;
 
-  // Two key fragments alternate: while one is scored the other is loading
-  // (the second wave on the SIMD covers the rest of the latency).  Loads past
-  // the segment are clamped to a valid key (their data is never used), so no
-  // load is conditional.
-  const int64_t S = KSPLIT ? 64 : 16;
-  int64_t t = seg0 + (KSPLIT ? 16 * wave : 0);
-  auto key_at = [&](int64_t base) { return kb + min(base + lr, lim_max) * kD * EB; };
-  auto emit = [&](float acc, int64_t base) {
-    // keep the epilogue ahead of the store's branch (no sinking into it)
-    asm volatile("" : "+v"(acc));
-    const int64_t s = base + lr;
-    if (writer && s <= my_lim) {
-      if constexpr (DT == kFp8) acc *= ksb[s];
+  const int S = KSPLIT ? 64 : 16;
+  int t = KSPLIT ? 16 * wave : 0;  // key offset within the segment
+  auto emit = [&](float acc, int base) {
+    asm volatile("" : "+v"(acc));  // keep the epilogue ahead of the store's branch
+    const int s = base + lr;
+    if (writer && s < my_n) {
+      if constexpr (DT == kFp8) acc *= sks[s];
       orow[s] = acc;
     }
   };
-  KeyFrag<DT> f0, f1;
-  f0.load(key_at(t), kg);
-  f1.load(key_at(t + S), kg);
-  for (; t < seg1; t += 2 * S) {
+  // Three key fragments rotate: while one is scored the next two are loading.
+  KeyFrag<DT> f0, f1, f2;
+  f0.load(kr, (uint32_t)(t + lr) * KB, kg);
+  f1.load(kr, (uint32_t)(t + S + lr) * KB, kg);
+  f2.load(kr, (uint32_t)(t + 2 * S + lr) * KB, kg);
+  for (; t < nkeys; t += 3 * S) {
     emit(tile.score(f0), t);
-    f0.load(key_at(t + 2 * S), kg);
-    if (t + S >= seg1) break;
+    f0.load(kr, (uint32_t)(t + 3 * S + lr) * KB, kg);
+    if (t + S >= nkeys) break;
     emit(tile.score(f1), t + S);
-    f1.load(key_at(t + 3 * S), kg);
+    f1.load(kr, (uint32_t)(t + 4 * S + lr) * KB, kg);
+    if (t + 2 * S >= nkeys) break;
+    emit(tile.score(f2), t + 2 * S);
+    f2.load(kr, (uint32_t)(t + 5 * S + lr) * KB, kg);
   }
 }
+
+// Workgroups one launch should have for the machine to stay busy through the
+// causal tail: 256 CUs x 2 resident workgroups x 4 rounds.
+constexpr int64_t kTargetWorkgroups = 2048;
 
 template <int DT, int R, bool KSPLIT>
 static hipError_t run_score(const void* q, const float* qs, const float* w, const uint8_t* lin, const float* lsc,
                             int64_t q_seq_rows, const void* k, const float* ks, int64_t kstride, const SeqTable& st,
-                            const RowSpace& rs, int64_t lim_max, float* out, int64_t ld, int seg,
+                            const RowSpace& rs, int64_t lim_max, float* out, int64_t ld, int max_seg,
                             hipStream_t stream) {
   constexpr int RB = KSPLIT ? R : 4 * R;
   const int nrows = rs.i1 - rs.i0;
-  const int64_t nseg = ((lim_max + 1 + seg - 1) / seg + 7) / 8 * 8;
   const int64_t nblk = (int64_t)st.n * ((nrows + RB - 1) / RB);
+  // Longest key segment that still gives kTargetWorkgroups (down to 512 keys);
+  // longer segments amortise the row-tile load over more keys.
+  int seg = max_seg;  // <= 4096: the key scales of a segment are staged in LDS
+  while (seg > 512 && nblk * ((lim_max + seg) / seg) < kTargetWorkgroups) seg >>= 1;
+  const int64_t nseg = (lim_max + seg) / seg;
   if (nseg > 0x7FFFFFFF || nblk > 65535) return hipErrorInvalidConfiguration;
   hipLaunchKernelGGL((score_kernel<DT, R, KSPLIT>), dim3((unsigned)nseg, (unsigned)nblk), dim3(256), 0, stream,
                      (const uint8_t*)q, qs, w, lin, lsc, q_seq_rows, (const uint8_t*)k, ks, kstride, st, rs, out,
