@@ -185,6 +185,41 @@ def cpu_baseline(pf, g, budget_s=12.0, max_groups=4096):
             "full_config_s_extrapolated": sec * pairs_full / pairs_sample}
 
 
+def recorded_traffic(kernel):
+    """HBM bytes per launch of the score kernel from the committed counter
+    summary, or None when its sources changed since the counters were taken."""
+    import hashlib
+    if kernel != "score":
+        return None
+    path = os.path.join(ROOT, "profiles", "score_kernel_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    rec = {}
+    for line in open(path):
+        if line.strip() and not line.startswith("#"):
+            key, val = line.split()
+            rec[key] = val
+    csrc = os.path.join(ROOT, "paper_2607_24593_amd", "csrc")
+    src = b"".join(open(os.path.join(csrc, f), "rb").read()
+                   for f in ("score.hip", "mfma_tile.h", "device_common.h", "api.hip"))
+    if hashlib.sha256(src).hexdigest() != rec.get("sources_sha256"):
+        return None
+    return float(rec["read_bytes_per_launch"]) + float(rec["written_bytes_per_launch"])
+
+
+def calibrate_copy(nbytes=1 << 30, reps=3):
+    """A plain elementwise copy of nbytes (reads nbytes, writes nbytes): the
+    reference for scaling FETCH_SIZE / WRITE_SIZE counter readings."""
+    import torch
+    x = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    y = torch.empty_like(x)
+    for _ in range(reps):
+        torch.mul(x, 1.0, out=y)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibration": "elementwise copy", "bytes_read": nbytes, "bytes_written": nbytes,
+                      "dispatches": reps}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -196,7 +231,13 @@ def main():
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-compare", action="store_true", help="skip the dense / Reuse / sweep passes")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a plain 1 GiB device copy kernel (HBM counter calibration)")
     args = ap.parse_args()
+    if args.calibrate_copy:
+        calibrate_copy()
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for {max(args.gpus, world)})",
@@ -250,18 +291,20 @@ def main():
     dom = max(kern, key=lambda n: kern[n]["ms_per_step"])
     dk = kern[dom]
     roofline = {"kernel": dom, "bound": dk.get("bound"), "achieved": dk.get("achieved"), "peak": dk.get("peak"),
-                "unit": dk.get("unit"), "frac": dk.get("frac"), "traffic": None,
+                "unit": dk.get("unit"), "frac": dk.get("frac"), "traffic": recorded_traffic(dom),
+                "traffic_unit": "HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
                 "units_per_step": {"score_pairs": u["pairs"], "score_flops": u["score_flops"],
                                    "select_bytes": u["select_bytes"], "refine_bytes": u["refine_bytes"]}}
 
     # ---- comparison: dense, Reuse, g sweep
     modes = {}
-    dense_s = timed(lambda: pf.run("dense", g), args.reps)
+    dense_s = None if args.no_compare else timed(lambda: pf.run("dense", g), args.reps)
     ud = units(pf.chunks, "dense", 1, wl.c, wl.topk, eb, eb)
-    modes["dense"] = {"ms_per_pass": dense_s * 1e3, "queries_per_s": wl.L / dense_s,
-                      "score_TFLOPs_incl_select": ud["score_flops"] / dense_s / 1e12}
-    log(f"dense: {dense_s * 1e3:.2f} ms")
-    sweep = wl.g if not args.no_sweep else (g,)
+    if dense_s is not None:
+        modes["dense"] = {"ms_per_pass": dense_s * 1e3, "queries_per_s": wl.L / dense_s,
+                          "score_TFLOPs_incl_select": ud["score_flops"] / dense_s / 1e12}
+        log(f"dense: {dense_s * 1e3:.2f} ms")
+    sweep = () if args.no_compare else (wl.g if not args.no_sweep else (g,))
     for gg in sweep:
         for mode in ("reuse", "refine"):
             s = step_s if (mode == "refine" and gg == g) else timed(lambda: pf.run(mode, gg), args.reps)
@@ -287,7 +330,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "L": wl.L, "H": wl.H, "d": wl.d, "topk": wl.topk, "c": wl.c, "g": g,
                    "chunk": wl.chunk, "mode": "refine", "guardrail": "t0 < c -> dense"},
-        "speedup_vs_dense": dense_s / step_s,
+        "speedup_vs_dense": None if dense_s is None else dense_s / step_s,
         "mfma_frac_score_kernel": kern.get("score", {}).get("frac"),
         "roofline": roofline,
         "kernels": kern,
