@@ -75,7 +75,7 @@ def units(chunks, mode, g, c, topk, eb_q=1, eb_k=1):
 
 # ---------------------------------------------------------------- runs
 class Prefill:
-    def __init__(self, wl, threads):
+    def __init__(self, wl, threads, score_tile_mb=None):
         import torch
         from workload.gen import make
         t = time.time()
@@ -97,6 +97,10 @@ class Prefill:
                              p0, p0 + n, wl.topk, self.out[p0:p0 + n])
             for mode in (pv.PIVOT_DENSE, pv.PIVOT_REUSE, pv.PIVOT_REFINE):
                 need = max(need, pv.pivot_workspace_size(a, mode, g, wl.c))
+        if score_tile_mb is not None:
+            # the library tiles score rows to fit the workspace: replace the
+            # default ~1 GiB score tile by the requested size
+            need = need - (1 << 30) + int(score_tile_mb) * (1 << 20)
         self.ws = torch.empty(need, dtype=torch.uint8, device="cuda")
         log(f"workspace {need / 2**30:.2f} GiB")
 
@@ -232,6 +236,8 @@ def main():
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-compare", action="store_true", help="skip the dense / Reuse / sweep passes")
+    ap.add_argument("--score-tile-mb", type=int, default=None,
+                    help="score-tile budget in MiB (default: the library's recommended workspace)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy kernel (HBM counter calibration)")
     args = ap.parse_args()
@@ -251,7 +257,7 @@ def main():
     pv.lib()
     wl = WORKLOADS[args.workload]
     g = args.g
-    pf = Prefill(wl, threads=16)
+    pf = Prefill(wl, threads=16, score_tile_mb=args.score_tile_mb)
 
     # ---- headline: PIVOT-Refine steps
     for _ in range(args.warmup):
@@ -329,7 +335,8 @@ def main():
         "dtype": wl.dtype,
         "data": "synthetic",
         "config": {"workload": wl.name, "L": wl.L, "H": wl.H, "d": wl.d, "topk": wl.topk, "c": wl.c, "g": g,
-                   "chunk": wl.chunk, "mode": "refine", "guardrail": "t0 < c -> dense"},
+                   "chunk": wl.chunk, "mode": "refine", "guardrail": "t0 < c -> dense",
+                   "workspace_bytes": int(pf.ws.numel())},
         "speedup_vs_dense": None if dense_s is None else dense_s / step_s,
         "mfma_frac_score_kernel": kern.get("score", {}).get("frac"),
         "roofline": roofline,

@@ -111,4 +111,76 @@ struct ArraySource {
   }
 };
 
+// Two-level exact top-m of a source with n elements (n > m): a 4096-bin
+// histogram of the top 12 key bits finds the bin b1 holding the m-th key;
+// keys above b1 are emitted at once and b1's keys are compacted into LDS
+// (at most CAP), where block_select() resolves the rest.  If b1 holds more
+// than CAP keys, block_select() runs over the whole source instead.
+template <int CAP>
+struct TwoLevelShared {
+  uint32_t hist[4096];
+  uint32_t ckey[CAP];
+  int32_t cpos[CAP];
+  SelectShared sel;
+  uint32_t wsum[16];
+  uint32_t b1, above, in_b1;
+  int32_t ncand;
+};
+
+template <int THREADS, int CAP, class Src, class Emit>
+__device__ void two_level_select(const Src& src, uint32_t m, TwoLevelShared<CAP>& sh, Emit emit) {
+  const int tid = threadIdx.x;
+  for (int k = tid; k < 4096; k += THREADS) sh.hist[k] = 0;
+  if (tid == 0) sh.ncand = 0;
+  __syncthreads();
+  src.visit([&](uint32_t key, int32_t) { atomicAdd(&sh.hist[key >> 20], 1u); });
+  __syncthreads();
+  {  // bin where the count from the top crosses m: each thread owns 4096/THREADS bins
+    constexpr int PER = 4096 / THREADS;
+    const int lane = tid & 63, wv = tid >> 6;
+    uint32_t tot = 0;
+#pragma unroll
+    for (int k = 0; k < PER; ++k) tot += sh.hist[PER * tid + k];
+    uint32_t s = tot;  // inclusive suffix sum within the wave (lanes >= lane)
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      uint32_t t = __shfl_down(s, o, 64);
+      if (lane + o < 64) s += t;
+    }
+    if (lane == 0) sh.wsum[wv] = s;
+    __syncthreads();
+    uint32_t above = s - tot;
+    for (int w = wv + 1; w < THREADS / 64; ++w) above += sh.wsum[w];
+#pragma unroll
+    for (int k = PER - 1; k >= 0; --k) {
+      const uint32_t h = sh.hist[PER * tid + k];
+      if (above < m && m <= above + h) {
+        sh.b1 = PER * tid + k;
+        sh.above = above;
+        sh.in_b1 = h;
+      }
+      above += h;
+    }
+  }
+  __syncthreads();
+  const uint32_t b1 = sh.b1, above = sh.above, in_b1 = sh.in_b1;
+  if (in_b1 <= (uint32_t)CAP) {
+    src.visit([&](uint32_t key, int32_t pos) {
+      const uint32_t top = key >> 20;
+      if (top > b1) {
+        emit(pos);
+      } else if (top == b1) {
+        const int c = atomicAdd(&sh.ncand, 1);
+        sh.ckey[c] = key;
+        sh.cpos[c] = pos;
+      }
+    });
+    __syncthreads();
+    ArraySource<THREADS> cand{sh.ckey, sh.cpos, sh.ncand};
+    block_select<THREADS>(cand, m - above, sh.sel, emit);
+  } else {
+    block_select<THREADS>(src, m, sh.sel, emit);
+  }
+}
+
 }  // namespace pivot

@@ -136,11 +136,13 @@ __global__ __launch_bounds__(256) void topk_short_kernel(const float* __restrict
     src.key[v] = ok ? float_key(ksb ? f * ksb[p] : f) : 0u;
     src.pos[v] = p;
   }
+  if (nc <= m) {  // every candidate is selected
+    for (int p = tid; p < m; p += 256) orow[p] = p < nc ? crow[p] : -1;
+    return;
+  }
   if (tid == 0) sel.emitted = 0;
   __syncthreads();
-  const int need = min(m, nc);
-  block_select<256>(src, (uint32_t)need, sel, [&](int32_t p) { orow[atomicAdd(&sel.emitted, 1)] = p; });
-  for (int p = need + tid; p < m; p += 256) orow[p] = -1;
+  block_select<256>(src, (uint32_t)m, sel, [&](int32_t p) { orow[atomicAdd(&sel.emitted, 1)] = p; });
 }
 
 hipError_t launch_refine(int dtype, const void* q, const float* q_scale, const float* w, const uint8_t* lin,
