@@ -238,11 +238,17 @@ def main():
     ap.add_argument("--no-compare", action="store_true", help="skip the dense / Reuse / sweep passes")
     ap.add_argument("--score-tile-mb", type=int, default=None,
                     help="score-tile budget in MiB (default: the library's recommended workspace)")
+    ap.add_argument("--decode-only", action="store_true", help="only the decode measurement")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy kernel (HBM counter calibration)")
     args = ap.parse_args()
     if args.calibrate_copy:
         calibrate_copy()
+        return
+    if args.decode_only:
+        import paper_2607_24593_amd as pv
+        pv.lib()
+        print(json.dumps({"decode": decode_bench(reps=50)}), flush=True)
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:

@@ -91,6 +91,7 @@ struct Plan {
   size_t off_pq = 0, off_psc = 0, off_pw = 0, off_cand = 0, off_scores = 0, fixed = 0;
   size_t off_qlin = 0, off_qlsc = 0, off_plin = 0, off_plsc = 0;  // fp8 epilogue's linear term
   size_t off_rsc = 0;                                              // Refine member scores
+  size_t off_split = 0, split_bytes = 0;                           // split select (few long rows)
   bool qlin = false, plin = false;
 };
 
@@ -122,7 +123,9 @@ pivot_status check_args(const pivot_args* a) {
   return PIVOT_OK;
 }
 
-pivot_status make_plan(const pivot_args* a, int mode, int g, int c, int dense_below, Plan& p) {
+// ext_cand: Refine writes its candidate sets to the caller's buffer, so the
+// workspace reserves none.
+pivot_status make_plan(const pivot_args* a, int mode, int g, int c, int dense_below, bool ext_cand, Plan& p) {
   pivot_status s = check_args(a);
   if (s != PIVOT_OK) return s;
   if (mode != PIVOT_DENSE && mode != PIVOT_REUSE && mode != PIVOT_REFINE)
@@ -201,8 +204,16 @@ pivot_status make_plan(const pivot_args* a, int mode, int g, int c, int dense_be
       p.off_rsc = off;
       off = align_up(off + ng * (size_t)g * c * sizeof(float));
       p.off_cand = off;
-      off = align_up(off + ng * (size_t)c * sizeof(int32_t));
+      if (!ext_cand) off = align_up(off + ng * (size_t)c * sizeof(int32_t));
     }
+  }
+  // few long rows (decode): each row's selection is spread over several workgroups
+  const int64_t sel_rows = std::max<int64_t>(p.dense_hi > 0 ? (int64_t)p.B * p.n_q : 0,
+                                             proxies ? (int64_t)p.B * p.n_groups : 0);
+  if (sel_rows > 0 && sel_rows <= kSplitMaxRows && p.max_nk >= kSplitMinLen) {
+    p.off_split = off;
+    p.split_bytes = split_scratch_bytes(sel_rows, kSplitCap);
+    off = align_up(off + p.split_bytes);
   }
   p.off_scores = off;
   p.fixed = off;
@@ -311,7 +322,12 @@ pivot_status run_rows(const pivot_args* a, const Plan& p, int kind, int lo, int 
                                  }),
                                  "score kernel");
       if (s != PIVOT_OK) return s;
-      s = hip_check(timed(PIVOT_KERNEL_SELECT, stream, [&] { return launch_topk(scores, ld, st, rs, od, stream); }),
+      s = hip_check(timed(PIVOT_KERNEL_SELECT, stream,
+                          [&] {
+                            return launch_topk(scores, ld, st, rs, od,
+                                               p.split_bytes ? (uint8_t*)a->workspace + p.off_split : nullptr,
+                                               p.split_bytes, lim, stream);
+                          }),
                     "top-k kernel");
       if (s != PIVOT_OK) return s;
     }
@@ -370,13 +386,13 @@ size_t pivot_workspace_size(const pivot_args* a, int32_t mode, int32_t g, int32_
   shape.w = shape.q_scale = shape.k_scale = &dummy;
   shape.out_idx = reinterpret_cast<int32_t*>(const_cast<float*>(&dummy));
   Plan p;
-  if (make_plan(&shape, mode, g, c, c, p) != PIVOT_OK) return 0;
+  if (make_plan(&shape, mode, g, c, c, false, p) != PIVOT_OK) return 0;
   return recommended_bytes(p);
 }
 
 pivot_status pivot_dense_index(const pivot_args* a) {
   Plan p;
-  pivot_status s = make_plan(a, PIVOT_DENSE, 1, 0, 0, p);
+  pivot_status s = make_plan(a, PIVOT_DENSE, 1, 0, 0, false, p);
   if (s != PIVOT_OK) return s;
   if (p.n_q == 0) return PIVOT_OK;
   int64_t score_bytes;
@@ -392,15 +408,10 @@ pivot_status pivot_group_index(const pivot_args* a, int32_t mode, int32_t g, int
                                int32_t* out_cand) {
   if (mode != PIVOT_REUSE && mode != PIVOT_REFINE) return fail(PIVOT_ERR_INVALID_ARG, "mode %d", mode);
   Plan p;
-  pivot_status s = make_plan(a, mode, g, c, dense_below, p);
+  pivot_status s = make_plan(a, mode, g, c, dense_below, out_cand != nullptr && mode == PIVOT_REFINE, p);
   if (s != PIVOT_OK) return s;
   if (p.n_q == 0) return PIVOT_OK;
   hipStream_t stream = (hipStream_t)a->stream;
-  if (out_cand && mode == PIVOT_REFINE) {
-    // the caller's buffer replaces the workspace's candidate region
-    p.fixed = p.off_cand;
-    p.off_scores = p.off_cand;
-  }
   int64_t score_bytes;
   s = check_workspace(a, p, score_bytes);
   if (s != PIVOT_OK) return s;
@@ -569,7 +580,7 @@ pivot_status pivot_topk_rows(int32_t n_rows, const float* scores, int64_t ld, in
   st.q_pos0[0] = (int32_t)(n0 - 1);
   RowSpace rs{0, n_rows, n_step, kAll};
   OutDesc od{out, m, n_rows, 0, 0};
-  return hip_check(launch_topk(scores, ld, st, rs, od, (hipStream_t)stream), "top-k kernel");
+  return hip_check(launch_topk(scores, ld, st, rs, od, nullptr, 0, n_max - 1, (hipStream_t)stream), "top-k kernel");
 }
 
 pivot_status pivot_encode_e4m3(const float* x, uint8_t* out, int64_t n, void* stream) {

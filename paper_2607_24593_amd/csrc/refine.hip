@@ -13,6 +13,8 @@
 // topk_short_kernel: one workgroup per (group, member) row of |C| <= 8192
 // scores; each thread keeps its share of (key, position) pairs in registers
 // and block_select() takes the top-k, ties broken by lower position.
+#include <algorithm>
+
 #include "block_select.h"
 #include "launch.h"
 #include "mfma_tile.h"
@@ -26,11 +28,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void r
     const uint8_t* __restrict__ q, const float* __restrict__ q_scale, const float* __restrict__ w,
     const uint8_t* __restrict__ lin, const float* __restrict__ lin_scale, int n_q, int g, int n_groups,
     const uint8_t* __restrict__ k, int64_t k_seq_stride, SeqTable st, int j0, const int32_t* __restrict__ cand,
-    int c, float* __restrict__ rsc) {
+    int c, int parts, float* __restrict__ rsc) {
   using Tile = RowTile<DT, R>;
   constexpr int EB = Tile::EB;
   __shared__ int32_t spos[kMaxCand];
-  const int j = j0 + blockIdx.x, b = blockIdx.y, blk = blockIdx.z;  // members [R blk, R blk + R)
+  // members [R blk, R blk + R); candidate fragments of slice `part`
+  const int j = j0 + blockIdx.x, b = blockIdx.y, blk = blockIdx.z / parts, part = blockIdx.z % parts;
   if (b >= st.n || j >= n_groups || j < st.first_proxy[b]) return;
   const int gs = min(g, n_q - j * g);
   if (R * blk >= gs) return;
@@ -43,7 +46,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void r
   const int64_t r0 = (int64_t)b * n_q + (int64_t)j * g + R * blk;
   const uint8_t* kb = k + (int64_t)b * k_seq_stride * kD * EB;
   const int lr = lane & 15, kg = lane >> 4;
-  for (int e = tid; e < nc; e += 256) spos[e] = crow[e];
+  const int nfrag_all = (nc + 15) >> 4;
+  const int fpp = (nfrag_all + parts - 1) / parts;
+  const int fbeg = min(nfrag_all, part * fpp), fend = min(nfrag_all, fbeg + fpp);
+  if (fbeg >= fend) return;
+  const int cbeg = 16 * fbeg, ncs = min(nc, 16 * fend) - cbeg;  // this slice's candidates
+  for (int e = tid; e < ncs; e += 256) spos[e] = crow[cbeg + e];
 
   const uint8_t* rows[R];
   const float* wrows[R];
@@ -66,13 +74,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void r
   const int qr = kg / Tile::G;
   const bool writer = (kg % Tile::G) == 0 && qr < rows_here;
   float* mrow = rsc + (((int64_t)b * n_groups + j) * g + R * blk + qr) * (int64_t)c;
-  const int nfrag = (nc + 15) >> 4;
+  const int nfrag = fend - fbeg;
   constexpr int S = 4;  // fragment stride between the waves
-  auto pos_of = [&](int f) { return spos[min(16 * f + lr, nc - 1)]; };
+  auto pos_of = [&](int f) { return spos[min(16 * f + lr, ncs - 1)]; };
   auto emit = [&](float acc, int f) {
     asm volatile("" : "+v"(acc));  // keep the epilogue ahead of the store's branch
     const int slot = 16 * f + lr;
-    if (writer && slot < nc) mrow[slot] = acc;
+    if (writer && slot < ncs) mrow[cbeg + slot] = acc;
   };
   // two fragments in flight per wave; loads past the end repeat the last
   // candidate (never stored)
@@ -152,14 +160,18 @@ hipError_t launch_refine(int dtype, const void* q, const float* q_scale, const f
                          hipStream_t stream) {
   if (j1 <= j0 || st.n <= 0) return hipSuccess;
   if (c > kMaxCand) return hipErrorInvalidValue;
+  // few groups (decode): split the candidates so the launch still fills the GPU
+  const int R = dtype == kFp8 ? 4 : 2;
+  const int64_t wgs = (int64_t)(j1 - j0) * st.n * ((g + R - 1) / R);
+  const int nfrag = (c + 15) / 16;
+  const int parts = (int)std::max<int64_t>(1, std::min<int64_t>(std::max(1, nfrag / 8), (512 + wgs - 1) / wgs));
+  const dim3 grid((unsigned)(j1 - j0), (unsigned)st.n, (unsigned)(((g + R - 1) / R) * parts));
   if (dtype == kFp8)
-    hipLaunchKernelGGL((rescore_kernel<kFp8, 4>), dim3((unsigned)(j1 - j0), (unsigned)st.n, (unsigned)((g + 3) / 4)),
-                       dim3(256), 0, stream, (const uint8_t*)q, q_scale, w, lin, lin_scale, n_q, g, n_groups,
-                       (const uint8_t*)k, k_seq_stride, st, j0, cand, c, rescore);
+    hipLaunchKernelGGL((rescore_kernel<kFp8, 4>), grid, dim3(256), 0, stream, (const uint8_t*)q, q_scale, w, lin,
+                       lin_scale, n_q, g, n_groups, (const uint8_t*)k, k_seq_stride, st, j0, cand, c, parts, rescore);
   else
-    hipLaunchKernelGGL((rescore_kernel<kBf16, 2>), dim3((unsigned)(j1 - j0), (unsigned)st.n, (unsigned)((g + 1) / 2)),
-                       dim3(256), 0, stream, (const uint8_t*)q, q_scale, w, lin, lin_scale, n_q, g, n_groups,
-                       (const uint8_t*)k, k_seq_stride, st, j0, cand, c, rescore);
+    hipLaunchKernelGGL((rescore_kernel<kBf16, 2>), grid, dim3(256), 0, stream, (const uint8_t*)q, q_scale, w, lin,
+                       lin_scale, n_q, g, n_groups, (const uint8_t*)k, k_seq_stride, st, j0, cand, c, parts, rescore);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   dim3 sgrid((unsigned)(j1 - j0), (unsigned)st.n, (unsigned)g);

@@ -8,6 +8,8 @@
 // whose threshold bin overflows LDS (e.g. many equal scores) select directly
 // over the row.
 // A row with no more than m valid entries returns all of them, then -1.
+#include <algorithm>
+
 #include "block_select.h"
 #include "launch.h"
 
@@ -81,12 +83,251 @@ __global__ __launch_bounds__(kSelThreads) void topk_rows_kernel(const float* __r
   two_level_select<kSelThreads>(src, (uint32_t)m, sh, [&](int32_t p) { put(atomicAdd(&sh.sel.emitted, 1), p); });
 }
 
+// ---------------------------------------------------------------------------
+// Split select: rows too few to fill the GPU with one workgroup each (decode:
+// 32-64 rows of 131072 scores) are cut into P slices, each a workgroup.
+//   1 split_zero    clear each row's global histogram and counters;
+//   2 split_hist    per slice: 4096-bin LDS histogram of the top 12 key bits,
+//                   merged into the row's global histogram with atomics;
+//   3 split_emit    per slice: find the row's threshold bin b1 from the global
+//                   histogram; emit keys above b1 (global counter), append keys
+//                   in b1 to the row's candidate buffer;
+//   4 split_final   per row: block_select() over the candidates (or, if b1
+//                   overflowed the buffer, over the whole row).
+// Same result as the one-workgroup path: the set of the m largest keys, ties
+// to the lower position.
+struct SplitRowHeader {
+  int32_t emitted;
+  int32_t ncand;
+  int32_t pad[62];
+};
+
+struct SplitScratch {
+  uint32_t* hist;          // [rows, 4096]
+  SplitRowHeader* head;    // [rows]
+  uint32_t* ckey;          // [rows, cap]
+  int32_t* cpos;           // [rows, cap]
+  int32_t cap;
+};
+
+size_t split_scratch_bytes(int64_t rows, int cap) {
+  auto up = [](size_t x) { return (x + 255) / 256 * 256; };
+  return up(rows * 4096 * sizeof(uint32_t)) + up(rows * sizeof(SplitRowHeader)) +
+         2 * up(rows * (size_t)cap * sizeof(uint32_t));
+}
+
+static SplitScratch carve_split(void* base, int64_t rows, int cap) {
+  auto up = [](size_t x) { return (x + 255) / 256 * 256; };
+  uint8_t* p = (uint8_t*)base;
+  SplitScratch s;
+  s.hist = (uint32_t*)p;
+  p += up(rows * 4096 * sizeof(uint32_t));
+  s.head = (SplitRowHeader*)p;
+  p += up(rows * sizeof(SplitRowHeader));
+  s.ckey = (uint32_t*)p;
+  p += up(rows * (size_t)cap * sizeof(uint32_t));
+  s.cpos = (int32_t*)p;
+  s.cap = cap;
+  return s;
+}
+
+// Row r of a launch: sequence and local index, its length, its output rows.
+struct RowRef {
+  int b, i;
+  int n;
+  bool active;
+  __device__ RowRef(const SeqTable& st, const RowSpace& rs, int r) {
+    const int nrows = rs.i1 - rs.i0;
+    b = r / nrows;
+    i = rs.i0 + r % nrows;
+    active = row_active(st, rs, b, i);
+    n = active ? (int)max((int64_t)0, row_limit(st, rs, b, i) + 1) : 0;
+  }
+};
+
+__device__ __forceinline__ void put_index(const OutDesc& od, int b, int i, int p, int32_t v) {
+  int64_t dest0;
+  int ndest;
+  if (od.fan_g == 0) {
+    dest0 = (int64_t)b * od.per_seq + i;
+    ndest = 1;
+  } else {
+    dest0 = (int64_t)b * od.per_seq + (int64_t)i * od.fan_g;
+    ndest = min(od.fan_g, od.fan_n - i * od.fan_g);
+  }
+  for (int u = 0; u < ndest; ++u) od.base[(dest0 + u) * od.m + p] = v;
+}
+
+__global__ __launch_bounds__(256) void split_zero_kernel(SplitScratch sc, int rows) {
+  const int r = blockIdx.x;
+  if (r >= rows) return;
+  for (int k = threadIdx.x; k < 4096; k += 256) sc.hist[(int64_t)r * 4096 + k] = 0;
+  if (threadIdx.x == 0) {
+    sc.head[r].emitted = 0;
+    sc.head[r].ncand = 0;
+  }
+}
+
+__device__ __forceinline__ void slice_of(int n, int P, int part, int& lo, int& hi) {
+  const int per = ((n + P - 1) / P + 3) & ~3;  // multiple of 4: aligned vector loads
+  lo = min(n, part * per);
+  hi = min(n, lo + per);
+}
+
+__global__ __launch_bounds__(256) void split_hist_kernel(const float* __restrict__ scores, int64_t ld, SeqTable st,
+                                                         RowSpace rs, int m, int P, SplitScratch sc) {
+  __shared__ uint32_t hist[4096];
+  const int r = blockIdx.y, part = blockIdx.x;
+  RowRef rr(st, rs, r);
+  if (!rr.active || rr.n <= m) return;
+  int lo, hi;
+  slice_of(rr.n, P, part, lo, hi);
+  for (int k = threadIdx.x; k < 4096; k += 256) hist[k] = 0;
+  __syncthreads();
+  const float* row = scores + (int64_t)r * ld;
+  for (int e = lo + 4 * (int)threadIdx.x; e < hi; e += 1024) {
+    if (e + 4 <= hi) {
+      const float4 v = *reinterpret_cast<const float4*>(row + e);
+      atomicAdd(&hist[float_key(v.x) >> 20], 1u);
+      atomicAdd(&hist[float_key(v.y) >> 20], 1u);
+      atomicAdd(&hist[float_key(v.z) >> 20], 1u);
+      atomicAdd(&hist[float_key(v.w) >> 20], 1u);
+    } else {
+      for (int x = e; x < hi; ++x) atomicAdd(&hist[float_key(row[x]) >> 20], 1u);
+    }
+  }
+  __syncthreads();
+  uint32_t* g = sc.hist + (int64_t)r * 4096;
+  for (int k = threadIdx.x; k < 4096; k += 256)
+    if (hist[k]) atomicAdd(&g[k], hist[k]);
+}
+
+// Threshold bin of row r from its global histogram (every thread gets it).
+struct Threshold {
+  uint32_t b1, above, in_b1;
+};
+
+__device__ Threshold row_threshold(const uint32_t* g, uint32_t m, uint32_t* wsum, Threshold* out) {
+  constexpr int PER = 16;  // 4096 bins / 256 threads
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  uint32_t h[PER];
+  uint32_t tot = 0;
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    h[k] = g[PER * tid + k];
+    tot += h[k];
+  }
+  uint32_t s = tot;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    uint32_t t = __shfl_down(s, o, 64);
+    if (lane + o < 64) s += t;
+  }
+  if (lane == 0) wsum[wv] = s;
+  __syncthreads();
+  uint32_t above = s - tot;
+  for (int w = wv + 1; w < 4; ++w) above += wsum[w];
+#pragma unroll
+  for (int k = PER - 1; k >= 0; --k) {
+    if (above < m && m <= above + h[k]) *out = Threshold{(uint32_t)(PER * tid + k), above, h[k]};
+    above += h[k];
+  }
+  __syncthreads();
+  return *out;
+}
+
+__global__ __launch_bounds__(256) void split_emit_kernel(const float* __restrict__ scores, int64_t ld, SeqTable st,
+                                                         RowSpace rs, OutDesc od, int P, SplitScratch sc) {
+  __shared__ uint32_t wsum[4];
+  __shared__ Threshold th;
+  const int r = blockIdx.y, part = blockIdx.x;
+  RowRef rr(st, rs, r);
+  if (!rr.active || rr.n <= od.m) return;
+  const Threshold t = row_threshold(sc.hist + (int64_t)r * 4096, (uint32_t)od.m, wsum, &th);
+  if (t.in_b1 > (uint32_t)sc.cap) return;  // split_final selects over the whole row
+  int lo, hi;
+  slice_of(rr.n, P, part, lo, hi);
+  const float* row = scores + (int64_t)r * ld;
+  SplitRowHeader* head = sc.head + r;
+  uint32_t* ck = sc.ckey + (int64_t)r * sc.cap;
+  int32_t* cp = sc.cpos + (int64_t)r * sc.cap;
+  for (int e = lo + (int)threadIdx.x; e < hi; e += 256) {
+    const uint32_t key = float_key(row[e]);
+    const uint32_t top = key >> 20;
+    if (top > t.b1) {
+      put_index(od, rr.b, rr.i, atomicAdd(&head->emitted, 1), e);
+    } else if (top == t.b1) {
+      const int c = atomicAdd(&head->ncand, 1);
+      ck[c] = key;
+      cp[c] = e;
+    }
+  }
+}
+
+struct GlobalArraySource {
+  const uint32_t* key;
+  const int32_t* pos;
+  int count;
+  template <class F>
+  __device__ __forceinline__ void visit(F f) const {
+    for (int e = threadIdx.x; e < count; e += 256) f(key[e], pos[e]);
+  }
+};
+
+struct GlobalRowSource {
+  const float* row;
+  int count;
+  template <class F>
+  __device__ __forceinline__ void visit(F f) const {
+    for (int e = threadIdx.x; e < count; e += 256) f(float_key(row[e]), e);
+  }
+};
+
+__global__ __launch_bounds__(256) void split_final_kernel(const float* __restrict__ scores, int64_t ld, SeqTable st,
+                                                          RowSpace rs, OutDesc od, SplitScratch sc) {
+  __shared__ uint32_t wsum[4];
+  __shared__ Threshold th;
+  __shared__ SelectShared sel;
+  const int r = blockIdx.x;
+  RowRef rr(st, rs, r);
+  if (!rr.active) return;
+  const int m = od.m;
+  if (rr.n <= m) {
+    for (int p = threadIdx.x; p < m; p += 256) put_index(od, rr.b, rr.i, p, p < rr.n ? p : -1);
+    return;
+  }
+  const Threshold t = row_threshold(sc.hist + (int64_t)r * 4096, (uint32_t)m, wsum, &th);
+  SplitRowHeader* head = sc.head + r;
+  if (threadIdx.x == 0) sel.emitted = (t.in_b1 <= (uint32_t)sc.cap) ? head->emitted : 0;
+  __syncthreads();
+  auto emit = [&](int32_t p) { put_index(od, rr.b, rr.i, atomicAdd(&sel.emitted, 1), p); };
+  if (t.in_b1 <= (uint32_t)sc.cap) {
+    GlobalArraySource src{sc.ckey + (int64_t)r * sc.cap, sc.cpos + (int64_t)r * sc.cap, head->ncand};
+    block_select<256>(src, (uint32_t)m - t.above, sel, emit);
+  } else {
+    GlobalRowSource src{scores + (int64_t)r * ld, rr.n};
+    block_select<256>(src, (uint32_t)m, sel, emit);
+  }
+}
+
 hipError_t launch_topk(const float* scores, int64_t ld, const SeqTable& st, const RowSpace& rs,
-                       const OutDesc& od, hipStream_t stream) {
+                       const OutDesc& od, void* scratch, size_t scratch_bytes, int64_t lim_max,
+                       hipStream_t stream) {
   const int nrows = rs.i1 - rs.i0;
   if (nrows <= 0 || st.n <= 0) return hipSuccess;
   const int64_t blocks = (int64_t)st.n * nrows;
   if (blocks > 0x7FFFFFFF) return hipErrorInvalidConfiguration;
+  if (scratch && blocks <= kSplitMaxRows && lim_max + 1 >= kSplitMinLen &&
+      split_scratch_bytes(blocks, kSplitCap) <= scratch_bytes) {
+    const int rows = (int)blocks;
+    const int P = (int)std::max<int64_t>(1, std::min<int64_t>(64, 2048 / rows));
+    SplitScratch sc = carve_split(scratch, rows, kSplitCap);
+    hipLaunchKernelGGL(split_zero_kernel, dim3(rows), dim3(256), 0, stream, sc, rows);
+    hipLaunchKernelGGL(split_hist_kernel, dim3(P, rows), dim3(256), 0, stream, scores, ld, st, rs, od.m, P, sc);
+    hipLaunchKernelGGL(split_emit_kernel, dim3(P, rows), dim3(256), 0, stream, scores, ld, st, rs, od, P, sc);
+    hipLaunchKernelGGL(split_final_kernel, dim3(rows), dim3(256), 0, stream, scores, ld, st, rs, od, sc);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(topk_rows_kernel, dim3((unsigned)blocks), dim3(kSelThreads), 0, stream, scores, ld, st, rs,
                      od);
   return hipGetLastError();

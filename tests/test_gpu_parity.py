@@ -117,11 +117,12 @@ def test_group_of_one_equals_dense(long_fp8):
         assert np.array_equal(np.sort(r, 1), np.sort(d, 1)), mode
 
 
+@pytest.mark.parametrize("B,L", [(6, 5000), (5, 20000)])
 @pytest.mark.parametrize("g", [2, 4])
 @pytest.mark.parametrize("mode", ["dense", "reuse", "refine"])
-def test_decode_batch(mode, g):
-    """Decode: B sequences, each one MTP group of g queries at the end of its context."""
-    B, L = 6, 5000
+def test_decode_batch(mode, g, B, L):
+    """Decode: B sequences, each one MTP group of g queries at the end of its
+    context (20000-key contexts take the split select and split re-score)."""
     x = make_decode(B, L, g, "fp8", seed=40 + g, threads=6)
     import torch
     say("decode", mode, "B", B, "L", L, "g", g)
