@@ -2,9 +2,9 @@
 //
 // Selects the `need` elements of a source that rank first by (key descending,
 // position ascending) and hands each selected position to `emit`.  The key is
-// resolved 8 bits at a time (4 histogram passes); if the m-th key is shared by
-// more elements than remain to be taken, 4 more passes over the positions of
-// the tied elements pick the lowest ones.  A final pass emits every element
+// resolved in 4 histogram passes (12, 8, 8, 4 bits); if the m-th key is shared
+// by more elements than remain to be taken, 4 more passes over the positions
+// of the tied elements pick the lowest ones.  A final pass emits every element
 // above the threshold.  Positions must be distinct non-negative int32.
 //
 // A source provides visit(f), calling f(key, pos) for each of the calling
@@ -17,60 +17,76 @@
 namespace pivot {
 
 struct SelectShared {
-  uint32_t hist[256];
+  uint32_t hist[4096];
+  uint32_t wsum[16];
   uint32_t digit, before, equal;
   int32_t emitted;
 };
 
-// One wave (the workgroup's first) finds the digit d where the running count
-// crosses `rem`, scanning digits downwards (desc) or upwards (!desc).  Writes
-// sh.digit, sh.before (count strictly before d in scan order), sh.equal (count at d).
-template <bool DESC>
-__device__ __forceinline__ void find_digit(SelectShared& sh, uint32_t rem) {
-  const int lane = threadIdx.x & 63;
-  if (threadIdx.x >= 64) return;
-  uint32_t v[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) v[i] = sh.hist[4 * lane + i];
-  const uint32_t tot = v[0] + v[1] + v[2] + v[3];
-  uint32_t s = tot;  // inclusive scan in scan order
+// Find the digit d (of `bins`) where the running count crosses `rem`, scanning
+// digits downwards (desc) or upwards (!desc); every thread owns bins/THREADS
+// consecutive digits.  Writes sh.digit, sh.before (count strictly before d in
+// scan order) and sh.equal (count at d).  Contains workgroup barriers.
+template <int THREADS, bool DESC>
+__device__ __forceinline__ void find_digit(SelectShared& sh, uint32_t rem, int bins) {
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int per = bins / THREADS;  // bins is a multiple of THREADS, or smaller
+  const int lo = per > 0 ? per * tid : tid;
+  const int cnt = per > 0 ? per : (tid < bins ? 1 : 0);
+  uint32_t tot = 0;
+  for (int k = 0; k < cnt; ++k) tot += sh.hist[lo + k];
+  uint32_t s = tot;  // inclusive scan over lanes in scan order
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
     uint32_t t = DESC ? __shfl_down(s, o, 64) : __shfl_up(s, o, 64);
-    bool ok = DESC ? (lane + o < 64) : (lane >= o);
-    if (ok) s += t;
+    if (DESC ? (lane + o < 64) : (lane >= o)) s += t;
   }
+  if (DESC ? lane == 0 : lane == 63) sh.wsum[wv] = s;
+  __syncthreads();
   uint32_t before = s - tot;
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const int i = DESC ? 3 - k : k;
-    if (before < rem && rem <= before + v[i]) {
-      sh.digit = 4 * lane + i;
-      sh.before = before;
-      sh.equal = v[i];
-    }
-    before += v[i];
+  if (DESC) {
+    for (int w = wv + 1; w < THREADS / 64; ++w) before += sh.wsum[w];
+  } else {
+    for (int w = 0; w < wv; ++w) before += sh.wsum[w];
   }
+  for (int kk = 0; kk < cnt; ++kk) {
+    const int k = DESC ? cnt - 1 - kk : kk;
+    const uint32_t h = sh.hist[lo + k];
+    if (before < rem && rem <= before + h) {
+      sh.digit = lo + k;
+      sh.before = before;
+      sh.equal = h;
+    }
+    before += h;
+  }
+  __syncthreads();
 }
 
+// Key digits, most significant first: 12 bits (sign, exponent, 3 mantissa
+// bits: spreads typical scores over many bins, so the histogram atomics rarely
+// collide), then 8, 8, 4.  Positions use 8-bit digits.
 template <int THREADS, class Src, class Emit>
 __device__ void block_select(const Src& src, uint32_t need, SelectShared& sh, Emit emit) {
+  constexpr int kShift[4] = {20, 12, 4, 0};
+  constexpr int kBits[4] = {12, 8, 8, 4};
   const int tid = threadIdx.x;
   if (need == 0) return;
   uint32_t prefix = 0, mask = 0, rem = need, equal = 0;
-  for (int shift = 24; shift >= 0; shift -= 8) {
-    for (int i = tid; i < 256; i += THREADS) sh.hist[i] = 0;
+#pragma unroll
+  for (int pass = 0; pass < 4; ++pass) {
+    const int shift = kShift[pass], bins = 1 << kBits[pass];
+    const uint32_t dmask = (uint32_t)bins - 1;
+    for (int i = tid; i < bins; i += THREADS) sh.hist[i] = 0;
     __syncthreads();
     src.visit([&](uint32_t key, int32_t) {
-      if ((key & mask) == prefix) atomicAdd(&sh.hist[(key >> shift) & 255u], 1u);
+      if ((key & mask) == prefix) atomicAdd(&sh.hist[(key >> shift) & dmask], 1u);
     });
     __syncthreads();
-    find_digit<true>(sh, rem);
-    __syncthreads();
+    find_digit<THREADS, true>(sh, rem, bins);
     rem -= sh.before;
     equal = sh.equal;
     prefix |= sh.digit << shift;
-    mask |= 255u << shift;
+    mask |= dmask << shift;
     __syncthreads();
   }
   const uint32_t T = prefix;
@@ -85,8 +101,7 @@ __device__ void block_select(const Src& src, uint32_t need, SelectShared& sh, Em
         if (key == T && (p & imask) == ipref) atomicAdd(&sh.hist[(p >> shift) & 255u], 1u);
       });
       __syncthreads();
-      find_digit<false>(sh, rem);
-      __syncthreads();
+      find_digit<THREADS, false>(sh, rem, 256);
       rem -= sh.before;
       ipref |= sh.digit << shift;
       imask |= 255u << shift;
@@ -118,11 +133,9 @@ struct ArraySource {
 // than CAP keys, block_select() runs over the whole source instead.
 template <int CAP>
 struct TwoLevelShared {
-  uint32_t hist[4096];
   uint32_t ckey[CAP];
   int32_t cpos[CAP];
-  SelectShared sel;
-  uint32_t wsum[16];
+  SelectShared sel;  // its 4096-bin histogram also serves the first level
   uint32_t b1, above, in_b1;
   int32_t ncand;
 };
@@ -130,40 +143,15 @@ struct TwoLevelShared {
 template <int THREADS, int CAP, class Src, class Emit>
 __device__ void two_level_select(const Src& src, uint32_t m, TwoLevelShared<CAP>& sh, Emit emit) {
   const int tid = threadIdx.x;
-  for (int k = tid; k < 4096; k += THREADS) sh.hist[k] = 0;
+  uint32_t* hist = sh.sel.hist;
+  for (int k = tid; k < 4096; k += THREADS) hist[k] = 0;
   if (tid == 0) sh.ncand = 0;
   __syncthreads();
-  src.visit([&](uint32_t key, int32_t) { atomicAdd(&sh.hist[key >> 20], 1u); });
+  src.visit([&](uint32_t key, int32_t) { atomicAdd(&hist[key >> 20], 1u); });
   __syncthreads();
-  {  // bin where the count from the top crosses m: each thread owns 4096/THREADS bins
-    constexpr int PER = 4096 / THREADS;
-    const int lane = tid & 63, wv = tid >> 6;
-    uint32_t tot = 0;
-#pragma unroll
-    for (int k = 0; k < PER; ++k) tot += sh.hist[PER * tid + k];
-    uint32_t s = tot;  // inclusive suffix sum within the wave (lanes >= lane)
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      uint32_t t = __shfl_down(s, o, 64);
-      if (lane + o < 64) s += t;
-    }
-    if (lane == 0) sh.wsum[wv] = s;
-    __syncthreads();
-    uint32_t above = s - tot;
-    for (int w = wv + 1; w < THREADS / 64; ++w) above += sh.wsum[w];
-#pragma unroll
-    for (int k = PER - 1; k >= 0; --k) {
-      const uint32_t h = sh.hist[PER * tid + k];
-      if (above < m && m <= above + h) {
-        sh.b1 = PER * tid + k;
-        sh.above = above;
-        sh.in_b1 = h;
-      }
-      above += h;
-    }
-  }
+  find_digit<THREADS, true>(sh.sel, m, 4096);  // the bin holding the m-th key
+  const uint32_t b1 = sh.sel.digit, above = sh.sel.before, in_b1 = sh.sel.equal;
   __syncthreads();
-  const uint32_t b1 = sh.b1, above = sh.above, in_b1 = sh.in_b1;
   if (in_b1 <= (uint32_t)CAP) {
     src.visit([&](uint32_t key, int32_t pos) {
       const uint32_t top = key >> 20;

@@ -6,13 +6,14 @@
 // (R = 4 for fp8, 2 for bf16), held as the A operands of the MFMA row tile
 // (mfma_tile.h); the waves split C into 16-candidate fragments.  The candidate positions are staged in
 // LDS, so each lane reads its position there and gathers 32 bytes of that key
-// two fragments ahead of its use.  Scores before the key scale go to a
+// (and, for fp8, its scale) two fragments ahead of its use.  Scores go to a
 // [group, member, |C|] fp32 buffer (it stays in the last-level cache for the
-// select that follows, which applies the key scale).
+// select that follows).
 //
 // topk_short_kernel: one workgroup per (group, member) row of |C| <= 8192
 // scores; each thread keeps its share of (key, position) pairs in registers
-// and block_select() takes the top-k, ties broken by lower position.
+// (both read with coalesced loads) and block_select() takes the top-k, ties
+// broken by lower position.
 #include <algorithm>
 
 #include "block_select.h"
@@ -27,8 +28,8 @@ template <int DT, int R>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void rescore_kernel(
     const uint8_t* __restrict__ q, const float* __restrict__ q_scale, const float* __restrict__ w,
     const uint8_t* __restrict__ lin, const float* __restrict__ lin_scale, int n_q, int g, int n_groups,
-    const uint8_t* __restrict__ k, int64_t k_seq_stride, SeqTable st, int j0, const int32_t* __restrict__ cand,
-    int c, int parts, float* __restrict__ rsc) {
+    const uint8_t* __restrict__ k, const float* __restrict__ k_scale, int64_t k_seq_stride, SeqTable st, int j0,
+    const int32_t* __restrict__ cand, int c, int parts, float* __restrict__ rsc) {
   using Tile = RowTile<DT, R>;
   constexpr int EB = Tile::EB;
   __shared__ int32_t spos[kMaxCand];
@@ -45,6 +46,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void r
   const int32_t* crow = cand + ((int64_t)b * n_groups + j) * c;
   const int64_t r0 = (int64_t)b * n_q + (int64_t)j * g + R * blk;
   const uint8_t* kb = k + (int64_t)b * k_seq_stride * kD * EB;
+  const float* ksb = DT == kFp8 ? k_scale + (int64_t)b * k_seq_stride : nullptr;
   const int lr = lane & 15, kg = lane >> 4;
   const int nfrag_all = (nc + 15) >> 4;
   const int fpp = (nfrag_all + parts - 1) / parts;
@@ -77,24 +79,32 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void r
   const int nfrag = fend - fbeg;
   constexpr int S = 4;  // fragment stride between the waves
   auto pos_of = [&](int f) { return spos[min(16 * f + lr, ncs - 1)]; };
-  auto emit = [&](float acc, int f) {
+  auto emit = [&](float acc, float ks, int f) {
+    acc *= ks;
     asm volatile("" : "+v"(acc));  // keep the epilogue ahead of the store's branch
     const int slot = 16 * f + lr;
     if (writer && slot < ncs) mrow[cbeg + slot] = acc;
   };
+  auto scale_of = [&](int p) { return DT == kFp8 ? ksb[p] : 1.0f; };
   // two fragments in flight per wave; loads past the end repeat the last
   // candidate (never stored)
   int f = wave;
   KeyFrag<DT> k0, k1;
-  k0.load(kb + (int64_t)pos_of(f) * kD * EB, kg);
-  k1.load(kb + (int64_t)pos_of(f + S) * kD * EB, kg);
+  int pn = pos_of(f);
+  float s0 = scale_of(pn), s1;
+  k0.load(kb + (int64_t)pn * kD * EB, kg);
+  pn = pos_of(f + S);
+  s1 = scale_of(pn);
+  k1.load(kb + (int64_t)pn * kD * EB, kg);
   for (; f < nfrag; f += 2 * S) {
-    int pn = pos_of(f + 2 * S);
-    emit(tile.score(k0), f);
+    pn = pos_of(f + 2 * S);
+    emit(tile.score(k0), s0, f);
+    s0 = scale_of(pn);
     k0.load(kb + (int64_t)pn * kD * EB, kg);
     if (f + S >= nfrag) break;
     pn = pos_of(f + 3 * S);
-    emit(tile.score(k1), f + S);
+    emit(tile.score(k1), s1, f + S);
+    s1 = scale_of(pn);
     k1.load(kb + (int64_t)pn * kD * EB, kg);
   }
 }
@@ -115,10 +125,9 @@ struct RegSource {
 
 template <int V>
 __global__ __launch_bounds__(256) void topk_short_kernel(const float* __restrict__ rsc,
-                                                         const int32_t* __restrict__ cand,
-                                                         const float* __restrict__ k_scale, int64_t k_seq_stride,
-                                                         int n_q, int g, int n_groups, SeqTable st, int j0, int c,
-                                                         int m, int32_t* __restrict__ out_idx) {
+                                                         const int32_t* __restrict__ cand, int n_q, int g,
+                                                         int n_groups, SeqTable st, int j0, int c, int m,
+                                                         int32_t* __restrict__ out_idx) {
   __shared__ SelectShared sel;
   const int j = j0 + blockIdx.x, b = blockIdx.y, member = blockIdx.z;
   if (b >= st.n || j >= n_groups || j < st.first_proxy[b]) return;
@@ -132,17 +141,14 @@ __global__ __launch_bounds__(256) void topk_short_kernel(const float* __restrict
   const int32_t* crow = cand + grp * c;
   int32_t* orow = out_idx + ((int64_t)b * n_q + (int64_t)j * g + member) * m;
 
-  const float* ksb = k_scale ? k_scale + (int64_t)b * k_seq_stride : nullptr;
   RegSource<V> src;
   src.count = nc;
 #pragma unroll
   for (int v = 0; v < V; ++v) {
     const int e = tid + 256 * v;
     const bool ok = e < nc;
-    const int32_t p = ok ? crow[e] : 0;
-    const float f = ok ? srow[e] : 0.f;
-    src.key[v] = ok ? float_key(ksb ? f * ksb[p] : f) : 0u;
-    src.pos[v] = p;
+    src.key[v] = ok ? float_key(srow[e]) : 0u;
+    src.pos[v] = ok ? crow[e] : 0;
   }
   if (nc <= m) {  // every candidate is selected
     for (int p = tid; p < m; p += 256) orow[p] = p < nc ? crow[p] : -1;
@@ -168,22 +174,24 @@ hipError_t launch_refine(int dtype, const void* q, const float* q_scale, const f
   const dim3 grid((unsigned)(j1 - j0), (unsigned)st.n, (unsigned)(((g + R - 1) / R) * parts));
   if (dtype == kFp8)
     hipLaunchKernelGGL((rescore_kernel<kFp8, 4>), grid, dim3(256), 0, stream, (const uint8_t*)q, q_scale, w, lin,
-                       lin_scale, n_q, g, n_groups, (const uint8_t*)k, k_seq_stride, st, j0, cand, c, parts, rescore);
+                       lin_scale, n_q, g, n_groups, (const uint8_t*)k, k_scale, k_seq_stride, st, j0, cand, c, parts,
+                       rescore);
   else
     hipLaunchKernelGGL((rescore_kernel<kBf16, 2>), grid, dim3(256), 0, stream, (const uint8_t*)q, q_scale, w, lin,
-                       lin_scale, n_q, g, n_groups, (const uint8_t*)k, k_seq_stride, st, j0, cand, c, parts, rescore);
+                       lin_scale, n_q, g, n_groups, (const uint8_t*)k, nullptr, k_seq_stride, st, j0, cand, c, parts,
+                       rescore);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   dim3 sgrid((unsigned)(j1 - j0), (unsigned)st.n, (unsigned)g);
   if (c <= 1024)
-    hipLaunchKernelGGL(topk_short_kernel<4>, sgrid, dim3(256), 0, stream, rescore, cand,
-                       dtype == kFp8 ? k_scale : nullptr, k_seq_stride, n_q, g, n_groups, st, j0, c, m, out_idx);
+    hipLaunchKernelGGL(topk_short_kernel<4>, sgrid, dim3(256), 0, stream, rescore, cand, n_q, g, n_groups, st, j0, c,
+                       m, out_idx);
   else if (c <= 4096)
-    hipLaunchKernelGGL(topk_short_kernel<16>, sgrid, dim3(256), 0, stream, rescore, cand,
-                       dtype == kFp8 ? k_scale : nullptr, k_seq_stride, n_q, g, n_groups, st, j0, c, m, out_idx);
+    hipLaunchKernelGGL(topk_short_kernel<16>, sgrid, dim3(256), 0, stream, rescore, cand, n_q, g, n_groups, st, j0,
+                       c, m, out_idx);
   else
-    hipLaunchKernelGGL(topk_short_kernel<32>, sgrid, dim3(256), 0, stream, rescore, cand,
-                       dtype == kFp8 ? k_scale : nullptr, k_seq_stride, n_q, g, n_groups, st, j0, c, m, out_idx);
+    hipLaunchKernelGGL(topk_short_kernel<32>, sgrid, dim3(256), 0, stream, rescore, cand, n_q, g, n_groups, st, j0,
+                       c, m, out_idx);
   return hipGetLastError();
 }
 

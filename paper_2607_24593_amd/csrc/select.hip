@@ -1,12 +1,25 @@
 // Per-row top-m selection over fp32 score rows (the TopK of Sec. 3.1 and of
 // Eqs. 6-7): one 512-thread workgroup per row.
 //
-// two_level_select() (block_select.h) over the row in global memory, read with
-// 16-byte vector loads: pass 1 builds a 4096-bin histogram of the top 12 key
-// bits, pass 2 emits the keys above the threshold bin and compacts that bin
-// into LDS, where the remaining bits are resolved (ties: lower position).  Rows
-// whose threshold bin overflows LDS (e.g. many equal scores) select directly
-// over the row.
+// Long rows (n >= kSampleMinLen) are read once when the expected number of
+// compacted keys fits in LDS:
+//   1 sample   every stride-th 256-byte chunk of the row (at most 8192
+//              scores) is held in registers; two histogram passes over the
+//              sample (top 12, then next 8 key bits) find a 20-bit prefix
+//              `thr` such that at least ts sampled keys have prefix >= thr,
+//              where ts is the sample's expected share of m plus four
+//              standard deviations;
+//   2 compact  one pass over the row appends every key with prefix >= thr to
+//              LDS (at most CAP: 4096 for m <= 2048, else 8000);
+//   3 select   if the pass found at least m keys (and no more than CAP),
+//              they include every key >= the m-th largest of the row, ties
+//              included, so block_select() over them is exact; otherwise the
+//              row takes the two-pass path below.
+// Other rows: two_level_select() (block_select.h) over the row in global
+// memory: pass 1 builds a 4096-bin histogram of the top 12 key bits, pass 2
+// emits the keys above the threshold bin and compacts that bin into LDS, where
+// the remaining bits are resolved (ties: lower position); a threshold bin that
+// overflows LDS (e.g. many equal scores) selects directly over the row.
 // A row with no more than m valid entries returns all of them, then -1.
 #include <algorithm>
 
@@ -16,42 +29,85 @@
 namespace pivot {
 
 constexpr int kSelThreads = 512;
-constexpr int kSelCap = 6144;  // LDS: 16 KiB histogram + 48 KiB candidates -> two workgroups per CU
+// LDS candidates: 16 KiB histogram + 32 KiB -> three workgroups per CU, or
+// + 62.5 KiB -> two
+constexpr int kSelCapSmall = 4096;
+constexpr int kSelCapLarge = 8000;
+constexpr int kSampleMinLen = 16384;  // shorter rows take the two-pass path
+constexpr int kChunk4 = 16;           // float4 per sampled chunk (256 bytes)
+constexpr int kSampleChunks = 128;    // at most 8192 sampled scores, 16 per thread
+constexpr int kSampleV = kSampleChunks * kChunk4 / kSelThreads;
 
-// Elements of a score row, visited with 16-byte vector loads when aligned.
+// Elements of a score row, visited with 16-byte vector loads (four in flight
+// per thread) when aligned.
 struct RowSource {
   const float* row;
   int count;
   template <class F>
   __device__ __forceinline__ void visit(F f) const {
+    constexpr int T = kSelThreads;
     const int tid = threadIdx.x;
     if ((reinterpret_cast<uintptr_t>(row) & 15u) == 0) {
       const int n4 = count >> 2;
       const float4* r4 = reinterpret_cast<const float4*>(row);
+      auto each = [&](const float4& a, int i) {
+        f(float_key(a.x), 4 * i); f(float_key(a.y), 4 * i + 1);
+        f(float_key(a.z), 4 * i + 2); f(float_key(a.w), 4 * i + 3);
+      };
       int i = tid;
-      for (; i + kSelThreads < n4; i += 2 * kSelThreads) {
-        const float4 a = r4[i], b = r4[i + kSelThreads];
-        const int j = i + kSelThreads;
-        f(float_key(a.x), 4 * i); f(float_key(a.y), 4 * i + 1);
-        f(float_key(a.z), 4 * i + 2); f(float_key(a.w), 4 * i + 3);
-        f(float_key(b.x), 4 * j); f(float_key(b.y), 4 * j + 1);
-        f(float_key(b.z), 4 * j + 2); f(float_key(b.w), 4 * j + 3);
+      for (; i + 3 * T < n4; i += 4 * T) {
+        const float4 a = r4[i], b = r4[i + T], c = r4[i + 2 * T], d = r4[i + 3 * T];
+        each(a, i); each(b, i + T); each(c, i + 2 * T); each(d, i + 3 * T);
       }
-      for (; i < n4; i += kSelThreads) {
-        const float4 a = r4[i];
-        f(float_key(a.x), 4 * i); f(float_key(a.y), 4 * i + 1);
-        f(float_key(a.z), 4 * i + 2); f(float_key(a.w), 4 * i + 3);
-      }
-      for (int e = 4 * n4 + tid; e < count; e += kSelThreads) f(float_key(row[e]), e);
+      for (; i < n4; i += T) each(r4[i], i);
+      for (int e = 4 * n4 + tid; e < count; e += T) f(float_key(row[e]), e);
     } else {
-      for (int e = tid; e < count; e += kSelThreads) f(float_key(row[e]), e);
+      for (int e = tid; e < count; e += T) f(float_key(row[e]), e);
     }
   }
 };
 
+// The sampled keys (positions are not needed).
+struct SampleSource {
+  uint32_t key[4 * (kSampleV > 0 ? kSampleV : 1)];
+  bool ok[kSampleV];
+  template <class F>
+  __device__ __forceinline__ void visit(F f) const {
+#pragma unroll
+    for (int v = 0; v < kSampleV; ++v)
+      if (ok[v]) {
+        f(key[4 * v], 0); f(key[4 * v + 1], 0); f(key[4 * v + 2], 0); f(key[4 * v + 3], 0);
+      }
+  }
+};
+
+// 20-bit key prefix of the ts-th largest sampled key (ts <= sampled count).
+template <class Src>
+__device__ uint32_t sample_prefix(const Src& src, uint32_t ts, SelectShared& sh) {
+  const int tid = threadIdx.x;
+  for (int k = tid; k < 4096; k += kSelThreads) sh.hist[k] = 0;
+  __syncthreads();
+  src.visit([&](uint32_t key, int32_t) { atomicAdd(&sh.hist[key >> 20], 1u); });
+  __syncthreads();
+  find_digit<kSelThreads, true>(sh, ts, 4096);
+  const uint32_t d1 = sh.digit, rem = ts - sh.before;
+  __syncthreads();
+  for (int k = tid; k < 256; k += kSelThreads) sh.hist[k] = 0;
+  __syncthreads();
+  src.visit([&](uint32_t key, int32_t) {
+    if ((key >> 20) == d1) atomicAdd(&sh.hist[(key >> 12) & 255u], 1u);
+  });
+  __syncthreads();
+  find_digit<kSelThreads, true>(sh, rem, 256);
+  const uint32_t thr = (d1 << 8) | sh.digit;
+  __syncthreads();
+  return thr;
+}
+
+template <int CAP>
 __global__ __launch_bounds__(kSelThreads) void topk_rows_kernel(const float* __restrict__ scores, int64_t ld,
                                                                 SeqTable st, RowSpace rs, OutDesc od) {
-  __shared__ TwoLevelShared<kSelCap> sh;
+  __shared__ TwoLevelShared<CAP> sh;
   const int nrows = rs.i1 - rs.i0;
   const int b = blockIdx.x / nrows;
   const int i = rs.i0 + blockIdx.x % nrows;
@@ -79,8 +135,54 @@ __global__ __launch_bounds__(kSelThreads) void topk_rows_kernel(const float* __r
     return;
   }
   if (tid == 0) sh.sel.emitted = 0;
+  auto emit = [&](int32_t p) { put(atomicAdd(&sh.sel.emitted, 1), p); };
   RowSource src{row, n};
-  two_level_select<kSelThreads>(src, (uint32_t)m, sh, [&](int32_t p) { put(atomicAdd(&sh.sel.emitted, 1), p); });
+  const bool aligned = (reinterpret_cast<uintptr_t>(row) & 15u) == 0;
+  if (n >= kSampleMinLen && aligned) {
+    const int nch = n / (4 * kChunk4);
+    const int stride = max(16, (nch + kSampleChunks - 1) / kSampleChunks);
+    const int sch = (nch + stride - 1) / stride;  // chunks 0, stride, 2 stride, ... < nch
+    const float4* r4 = reinterpret_cast<const float4*>(row);
+    SampleSource smp;
+#pragma unroll
+    for (int v = 0; v < kSampleV; ++v) {
+      const int qi = tid + kSelThreads * v;
+      smp.ok[v] = qi < sch * kChunk4;
+      const float4 a = smp.ok[v] ? r4[(int64_t)(qi / kChunk4) * stride * kChunk4 + qi % kChunk4]
+                                 : make_float4(0.f, 0.f, 0.f, 0.f);
+      smp.key[4 * v] = float_key(a.x);
+      smp.key[4 * v + 1] = float_key(a.y);
+      smp.key[4 * v + 2] = float_key(a.z);
+      smp.key[4 * v + 3] = float_key(a.w);
+    }
+    const int s = sch * 4 * kChunk4;
+    const float rm = (float)s * (float)m / (float)n;
+    const uint32_t ts = (uint32_t)ceilf(rm + 4.0f * sqrtf(rm)) + 1u;
+    // expected compacted count ts n / s: leave room for its spread
+    if (ts < (uint32_t)s && (float)ts * (float)n <= 0.8f * (float)CAP * (float)s) {
+      const uint32_t thr = sample_prefix(smp, ts, sh.sel);
+      if (tid == 0) sh.ncand = 0;
+      __syncthreads();
+      src.visit([&](uint32_t key, int32_t pos) {
+        if ((key >> 12) >= thr) {
+          const int c = atomicAdd(&sh.ncand, 1);
+          if (c < CAP) {
+            sh.ckey[c] = key;
+            sh.cpos[c] = pos;
+          }
+        }
+      });
+      __syncthreads();
+      const int found = sh.ncand;
+      __syncthreads();  // every thread has read the count before it is reused
+      if (found >= m && found <= CAP) {
+        ArraySource<kSelThreads> cand{sh.ckey, sh.cpos, found};
+        block_select<kSelThreads>(cand, (uint32_t)m, sh.sel, emit);
+        return;
+      }
+    }
+  }
+  two_level_select<kSelThreads>(src, (uint32_t)m, sh, emit);
 }
 
 // ---------------------------------------------------------------------------
@@ -240,6 +342,7 @@ __global__ __launch_bounds__(256) void split_emit_kernel(const float* __restrict
                                                          RowSpace rs, OutDesc od, int P, SplitScratch sc) {
   __shared__ uint32_t wsum[4];
   __shared__ Threshold th;
+  __shared__ int32_t n_above, n_equal, base_above, base_equal;
   const int r = blockIdx.y, part = blockIdx.x;
   RowRef rr(st, rs, r);
   if (!rr.active || rr.n <= od.m) return;
@@ -251,13 +354,33 @@ __global__ __launch_bounds__(256) void split_emit_kernel(const float* __restrict
   SplitRowHeader* head = sc.head + r;
   uint32_t* ck = sc.ckey + (int64_t)r * sc.cap;
   int32_t* cp = sc.cpos + (int64_t)r * sc.cap;
+  // count this slice's keys above / in the threshold bin, reserve both ranges
+  // with one global atomic each, then write (a slice is a few thousand keys,
+  // so the second read hits the cache)
+  if (threadIdx.x == 0) n_above = n_equal = 0;
+  __syncthreads();
+  int my_above = 0, my_equal = 0;
+  for (int e = lo + (int)threadIdx.x; e < hi; e += 256) {
+    const uint32_t top = float_key(row[e]) >> 20;
+    my_above += top > t.b1;
+    my_equal += top == t.b1;
+  }
+  if (my_above) atomicAdd(&n_above, my_above);
+  if (my_equal) atomicAdd(&n_equal, my_equal);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    base_above = n_above ? atomicAdd(&head->emitted, n_above) : 0;
+    base_equal = n_equal ? atomicAdd(&head->ncand, n_equal) : 0;
+    n_above = n_equal = 0;
+  }
+  __syncthreads();
   for (int e = lo + (int)threadIdx.x; e < hi; e += 256) {
     const uint32_t key = float_key(row[e]);
     const uint32_t top = key >> 20;
     if (top > t.b1) {
-      put_index(od, rr.b, rr.i, atomicAdd(&head->emitted, 1), e);
+      put_index(od, rr.b, rr.i, base_above + atomicAdd(&n_above, 1), e);
     } else if (top == t.b1) {
-      const int c = atomicAdd(&head->ncand, 1);
+      const int c = base_equal + atomicAdd(&n_equal, 1);
       ck[c] = key;
       cp[c] = e;
     }
@@ -328,8 +451,12 @@ hipError_t launch_topk(const float* scores, int64_t ld, const SeqTable& st, cons
     hipLaunchKernelGGL(split_final_kernel, dim3(rows), dim3(256), 0, stream, scores, ld, st, rs, od, sc);
     return hipGetLastError();
   }
-  hipLaunchKernelGGL(topk_rows_kernel, dim3((unsigned)blocks), dim3(kSelThreads), 0, stream, scores, ld, st, rs,
-                     od);
+  if (od.m <= kSelCapSmall / 2)
+    hipLaunchKernelGGL(topk_rows_kernel<kSelCapSmall>, dim3((unsigned)blocks), dim3(kSelThreads), 0, stream, scores,
+                       ld, st, rs, od);
+  else
+    hipLaunchKernelGGL(topk_rows_kernel<kSelCapLarge>, dim3((unsigned)blocks), dim3(kSelThreads), 0, stream, scores,
+                       ld, st, rs, od);
   return hipGetLastError();
 }
 

@@ -68,8 +68,12 @@ def _expect_topk(row, n, m):
 
 
 @pytest.mark.parametrize("case", ["normal", "ties", "signed_zeros", "short", "exact", "long2k", "long4k",
-                                  "ragged", "constant"])
+                                  "ragged", "constant", "sample_miss", "sample_ragged", "heavy_tail", "small_m",
+                                  "unaligned", "m4k_normal"])
 def test_topk_rows_exact(case):
+    """Rows of 16384+ scores with m <= 2048 take the sampled one-pass path; the
+    sample_miss rows put the sample's largest keys where the rest of the row is
+    low, so the pass finds fewer than m keys and falls back to two passes."""
     rng = np.random.default_rng(zlib.crc32(case.encode()))
     n0, step, m = 5000, 0, 100
     if case == "normal":
@@ -88,6 +92,20 @@ def test_topk_rows_exact(case):
         rows = np.exp(rng.standard_normal((2, 131072)) * 3); n0, m = 131072, 4096
     elif case == "ragged":
         rows = rng.standard_normal((40, 3000)); n0, step, m = 17, 70, 64
+    elif case == "sample_miss":
+        rows = rng.standard_normal((2, 65536)) * 0.1
+        sampled = (np.arange(65536) // 64) % 16 == 0        # every 16th 256-byte chunk
+        rows[:, sampled] += 5.0; n0, m = 65536, 2048
+    elif case == "sample_ragged":
+        rows = rng.standard_normal((6, 70000)); n0, step, m = 16384, 10001, 2048
+    elif case == "heavy_tail":
+        rows = np.exp(rng.standard_normal((3, 131072)) * 3); n0, m = 131072, 2048
+    elif case == "small_m":
+        rows = rng.standard_normal((3, 100000)); n0, m = 100000, 16
+    elif case == "unaligned":
+        rows = rng.standard_normal((4, 40001)); n0, step, m = 39990, 3, 1000
+    elif case == "m4k_normal":
+        rows = rng.standard_normal((3, 70000)); n0, m = 70000, 4096
     else:
         rows = np.full((2, 20000), 3.5); n0, m = 20000, 700
     rows = rows.astype(np.float32)

@@ -150,3 +150,55 @@ def test_repeatable(long_fp8):
     b, cb, _ = run_gpu(long_fp8, "refine", 4000, 2000, 256, g=4, c=1024)
     assert np.array_equal(np.sort(a, 1), np.sort(b, 1))
     assert np.array_equal(np.sort(ca, 1), np.sort(cb, 1))
+
+
+def _tied(L, fmt, seed, pool):
+    """A prefill whose keys repeat `pool` distinct key vectors (position s holds
+    vector s % pool), so every score row has `pool` distinct values and the
+    top-k boundary falls inside a run of exact ties."""
+    x = make_prefill(L, fmt, seed=seed, threads=8)
+    src = np.arange(L) % pool
+    x.k = np.ascontiguousarray(x.k[src])
+    if x.k_scale is not None:
+        x.k_scale = np.ascontiguousarray(x.k_scale[src])
+    return x
+
+
+def _separated(f, rtol=4e-2):
+    v = np.unique(f)
+    return len(v) < 2 or (np.diff(v) > rtol * np.abs(v[1:])).all()
+
+
+@pytest.mark.parametrize("fmt,L,c,topk,pool", [("fp8", 3000, 1024, 256, 6), ("bf16", 3000, 1024, 256, 5),
+                                               ("fp8", 9000, 4096, 2048, 6)])
+@pytest.mark.parametrize("mode", ["dense", "reuse", "refine"])
+def test_tied_keys_exact(fmt, L, c, topk, pool, mode):
+    """Exact ties at the boundary go to the lower position: the GPU sets equal the
+    oracle's, entry for entry, in every row whose distinct scores are far apart
+    compared with the score error (candidate sets likewise)."""
+    x = _tied(L, fmt, 41 + L + pool, pool)
+    g = 4
+    n_q = L
+    groups = sorted({0, 255, 256, 300, (n_q - 1) // g} | set(range(c // g, n_q // g, 97)))
+    idx, cand, (q, qs, w, n_k) = run_gpu(x, mode, 0, n_q, topk, g=g, c=c)
+    rows = [r for j in groups for r in range(j * g, min(n_q, (j + 1) * g))]
+    res = oracle.index(fmt, q, qs, w, 0, x.k, x.k_scale, n_k, mode=MODES[mode], g=1 if mode == "dense" else g,
+                       c=c, topk=topk, groups=rows if mode == "dense" else groups,
+                       want_cand=(mode == "refine"), want_proxy=(mode != "dense"))
+    pool_pos = np.arange(pool, dtype=np.int32)
+    checked = 0
+    for r in rows:
+        f = oracle.scores_at(fmt, q[r], 1.0 if qs is None else qs[r], w[r], x.k, x.k_scale, pool_pos)
+        if not _separated(f):
+            continue
+        j = r // g
+        if mode != "dense" and j * g >= c:
+            fp = oracle.scores_at(fmt, res["pq"][j], res["psc"][j], res["pw"][j], x.k, x.k_scale, pool_pos)
+            if not _separated(fp):
+                continue
+            if mode == "refine":
+                assert sorted(cand[j].tolist()) == sorted(res["cand"][j].tolist()), ("cand", j)
+        assert sorted(idx[r].tolist()) == sorted(res["idx"][r].tolist()), (mode, r)
+        checked += 1
+    say("tied rows checked", checked, "of", len(rows))
+    assert checked >= len(rows) // 2
