@@ -56,6 +56,9 @@ typedef enum { PIVOT_REUSE = 0, PIVOT_REFINE = 1 } pivot_mode;
 
 /* Passed as `mode` to pivot_workspace_size() for a dense call. */
 #define PIVOT_DENSE (-1)
+/* Keys per sequence (and score row length) this build handles: 2^27.  The
+ * scoring kernel addresses four score rows through one 32-bit range. */
+#define PIVOT_MAX_KEYS (1 << 27)
 
 /*
  * One indexer call over B sequences.
@@ -70,7 +73,8 @@ typedef enum { PIVOT_REUSE = 0, PIVOT_REFINE = 1 } pivot_mode;
  *
  * Sequence b holds n_q queries at positions q_pos0[b] .. q_pos0[b]+n_q-1 and
  * keys at positions 0 .. n_k[b]-1, with q_pos0[b] + n_q <= n_k[b] <=
- * k_seq_stride.  Prefill passes B = 1, q_pos0 = the chunk start and
+ * k_seq_stride and n_k[b] <= PIVOT_MAX_KEYS (else PIVOT_ERR_UNSUPPORTED).
+ * Prefill passes B = 1, q_pos0 = the chunk start and
  * n_k = q_pos0 + n_q; chunks whose start is a multiple of g give groups aligned
  * to absolute positions.  Decode passes n_q = g (the current query and its MTP
  * drafts, Eq. 3) and q_pos0[b] = n_k[b] - g.
@@ -151,7 +155,8 @@ pivot_status pivot_proxy_rows(int32_t dtype, int32_t heads, int32_t dim, int32_t
  * q_scale [n_rows] (fp8) and w [n_rows, H] is scored against keys
  * s = 0 .. lim0 + r * lim_step of k / k_scale (which must hold at least that
  * many keys); out[r * ld + s] receives the fp32 score.  Entries past a row's
- * limit are not written.  Requires ld >= lim0 + (n_rows-1)*lim_step + 1.
+ * limit are not written.  Requires ld >= lim0 + (n_rows-1)*lim_step + 1 and
+ * ld <= PIVOT_MAX_KEYS (else PIVOT_ERR_UNSUPPORTED).
  * fp8 rows need a workspace of PIVOT_SCORE_ROWS_WORKSPACE(n_rows) bytes
  * (256-B aligned) for the per-row linear term of the epilogue; bf16 needs none.
  */

@@ -21,6 +21,7 @@ PIVOT_OK, PIVOT_ERR_INVALID_ARG, PIVOT_ERR_UNSUPPORTED, PIVOT_ERR_WORKSPACE, PIV
 PIVOT_DT_BF16, PIVOT_DT_FP8_E4M3 = 0, 1
 PIVOT_REUSE, PIVOT_REFINE = 0, 1
 PIVOT_DENSE = -1
+PIVOT_MAX_KEYS = 1 << 27
 H, D = 64, 128
 
 EXPORTED = ["pivot_workspace_size", "pivot_dense_index", "pivot_group_index", "pivot_proxy_rows",

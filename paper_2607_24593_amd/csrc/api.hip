@@ -113,6 +113,8 @@ pivot_status check_args(const pivot_args* a) {
     if (a->n_k[b] > a->k_seq_stride)
       return fail(PIVOT_ERR_INVALID_ARG, "n_k[%d]=%d exceeds k_seq_stride=%lld", b, a->n_k[b],
                   (long long)a->k_seq_stride);
+    if (a->n_k[b] > PIVOT_MAX_KEYS)
+      return fail(PIVOT_ERR_UNSUPPORTED, "n_k[%d]=%d exceeds PIVOT_MAX_KEYS=%d", b, a->n_k[b], PIVOT_MAX_KEYS);
   }
   if (a->n_q > 0) {
     if (!a->q || !a->w || !a->k || !a->out_idx)
@@ -540,6 +542,8 @@ pivot_status pivot_score_rows(int32_t dtype, int32_t heads, int32_t dim, int32_t
   const int64_t lim_max = lim0 + (int64_t)(n_rows - 1) * lim_step;
   if (lim_max > 0x7FFFFFFE) return fail(PIVOT_ERR_INVALID_ARG, "limits exceed int32 positions");
   if (ld < lim_max + 1) return fail(PIVOT_ERR_INVALID_ARG, "ld=%lld < %lld", (long long)ld, (long long)lim_max + 1);
+  if (ld > PIVOT_MAX_KEYS)
+    return fail(PIVOT_ERR_UNSUPPORTED, "ld=%lld exceeds PIVOT_MAX_KEYS=%d", (long long)ld, PIVOT_MAX_KEYS);
   const bool fp8 = dtype == PIVOT_DT_FP8_E4M3;
   const size_t lin_off = align_up((size_t)n_rows * kLinBytes);
   const size_t need = fp8 ? lin_off + (size_t)n_rows * kLinLevels * sizeof(float) : 0;

@@ -1,11 +1,23 @@
 // Workgroup-wide exact top-m selection (radix select on order-preserving keys).
 //
 // Selects the `need` elements of a source that rank first by (key descending,
-// position ascending) and hands each selected position to `emit`.  The key is
-// resolved in 4 histogram passes (12, 8, 8, 4 bits); if the m-th key is shared
-// by more elements than remain to be taken, 4 more passes over the positions
-// of the tied elements pick the lowest ones.  A final pass emits every element
-// above the threshold.  Positions must be distinct non-negative int32.
+// position ascending) and hands each selected position to put(slot, pos), with
+// consecutive slots counted from sh.emitted (set by the caller).
+//
+// With BUCKET (for sets whose scores straddle zero and crowd a few exponents,
+// where radix digits taken from the top key bits pile most elements into a
+// handful of bins and the histogram atomics on one LDS address serialise):
+//   1 the key range [kmin, kmax] (one reduction);
+//   2 a 256-bin histogram of the VALUE, linearly bucketed over that range
+//     (a monotone map, so buckets keep the order), finds the bucket b* that
+//     holds the need-th element.
+// Then (over b*, or over all elements without BUCKET):
+//   3 the key bits shared by every element are skipped (AND / OR reduction)
+//     and 8-bit radix passes over the rest find the threshold key;
+//   4 if the threshold key is shared by more elements than remain to be taken,
+//     4 passes over the positions of the tied elements pick the lowest ones;
+//   5 every element above the threshold (and the chosen ties) is emitted.
+// Positions must be distinct non-negative int32.
 //
 // A source provides visit(f), calling f(key, pos) for each of the calling
 // thread's elements; every thread of the workgroup calls it.  Sources may keep
@@ -16,9 +28,26 @@
 
 namespace pivot {
 
+// Appends the calling lanes whose `take` is set through ONE atomic on the LDS
+// counter per wave (not one per lane: lanes of a wave appending to the same
+// counter would serialise on it); f(slot) runs on the taking lanes.  Must be
+// reached by all lanes of the wave that may take.
+template <class F>
+__device__ __forceinline__ void wave_append(bool take, int32_t* counter, F f) {
+  const uint64_t bal = __ballot(take);
+  if (bal == 0) return;
+  const int leader = __ffsll((unsigned long long)bal) - 1;
+  int base = 0;
+  if ((int)(threadIdx.x & 63) == leader) base = atomicAdd(counter, (int)__popcll((unsigned long long)bal));
+  base = __shfl(base, leader, 64);
+  if (take)
+    f(base + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u)));
+}
+
 struct SelectShared {
-  uint32_t hist[4096];
+  uint32_t hist[256];
   uint32_t wsum[16];
+  uint32_t wand[16], wor[16];
   uint32_t digit, before, equal;
   int32_t emitted;
 };
@@ -28,13 +57,13 @@ struct SelectShared {
 // consecutive digits.  Writes sh.digit, sh.before (count strictly before d in
 // scan order) and sh.equal (count at d).  Contains workgroup barriers.
 template <int THREADS, bool DESC>
-__device__ __forceinline__ void find_digit(SelectShared& sh, uint32_t rem, int bins) {
+__device__ __forceinline__ void find_digit(const uint32_t* hist, SelectShared& sh, uint32_t rem, int bins) {
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int per = bins / THREADS;  // bins is a multiple of THREADS, or smaller
   const int lo = per > 0 ? per * tid : tid;
   const int cnt = per > 0 ? per : (tid < bins ? 1 : 0);
   uint32_t tot = 0;
-  for (int k = 0; k < cnt; ++k) tot += sh.hist[lo + k];
+  for (int k = 0; k < cnt; ++k) tot += hist[lo + k];
   uint32_t s = tot;  // inclusive scan over lanes in scan order
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
@@ -51,7 +80,7 @@ __device__ __forceinline__ void find_digit(SelectShared& sh, uint32_t rem, int b
   }
   for (int kk = 0; kk < cnt; ++kk) {
     const int k = DESC ? cnt - 1 - kk : kk;
-    const uint32_t h = sh.hist[lo + k];
+    const uint32_t h = hist[lo + k];
     if (before < rem && rem <= before + h) {
       sh.digit = lo + k;
       sh.before = before;
@@ -62,31 +91,92 @@ __device__ __forceinline__ void find_digit(SelectShared& sh, uint32_t rem, int b
   __syncthreads();
 }
 
-// Key digits, most significant first: 12 bits (sign, exponent, 3 mantissa
-// bits: spreads typical scores over many bins, so the histogram atomics rarely
-// collide), then 8, 8, 4.  Positions use 8-bit digits.
-template <int THREADS, class Src, class Emit>
-__device__ void block_select(const Src& src, uint32_t need, SelectShared& sh, Emit emit) {
-  constexpr int kShift[4] = {20, 12, 4, 0};
-  constexpr int kBits[4] = {12, 8, 8, 4};
+// Inverse of float_key (zero comes back as +0).
+__device__ __forceinline__ float key_float(uint32_t k) {
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
+}
+
+// Workgroup reduction of (min, max) or (and, or) pairs through sh.wand / sh.wor.
+template <int THREADS, bool MINMAX>
+__device__ __forceinline__ void block_pair_reduce(uint32_t& a, uint32_t& o, SelectShared& sh) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+#pragma unroll
+  for (int d = 32; d > 0; d >>= 1) {
+    const uint32_t x = __shfl_xor(a, d, 64), y = __shfl_xor(o, d, 64);
+    a = MINMAX ? min(a, x) : (a & x);
+    o = MINMAX ? max(o, y) : (o | y);
+  }
+  if (lane == 0) {
+    sh.wand[wv] = a;
+    sh.wor[wv] = o;
+  }
+  __syncthreads();
+  for (int w = 0; w < THREADS / 64; ++w) {
+    a = MINMAX ? min(a, sh.wand[w]) : (a & sh.wand[w]);
+    o = MINMAX ? max(o, sh.wor[w]) : (o | sh.wor[w]);
+  }
+  __syncthreads();
+}
+
+template <int THREADS, bool BUCKET, class Src, class Put>
+__device__ void block_select(const Src& src, uint32_t need, SelectShared& sh, Put put) {
   const int tid = threadIdx.x;
   if (need == 0) return;
-  uint32_t prefix = 0, mask = 0, rem = need, equal = 0;
-#pragma unroll
-  for (int pass = 0; pass < 4; ++pass) {
-    const int shift = kShift[pass], bins = 1 << kBits[pass];
-    const uint32_t dmask = (uint32_t)bins - 1;
-    for (int i = tid; i < bins; i += THREADS) sh.hist[i] = 0;
+  uint32_t kmin = ~0u, kmax = 0u;
+  if constexpr (BUCKET) {
+    src.visit([&](uint32_t key, int32_t) {
+      kmin = min(kmin, key);
+      kmax = max(kmax, key);
+    });
+    block_pair_reduce<THREADS, true>(kmin, kmax, sh);
+  }
+  // value buckets: bucket(key) is monotone in the key
+  const float fmin = key_float(kmin);
+  const float scale = 256.0f / (key_float(kmax) - fmin);
+  const bool bucketed = BUCKET && kmin != kmax && scale > 0.0f && scale < __builtin_inff();
+  auto bucket = [&](uint32_t key) { return min(255, (int)((key_float(key) - fmin) * scale)); };
+  uint32_t rem = need, equal = 0xFFFFFFFFu;  // equal: keys at the threshold (unknown: take the tie passes)
+  int bsel = 0;
+  if (bucketed) {
+    for (int i = tid; i < 256; i += THREADS) sh.hist[i] = 0;
+    __syncthreads();
+    src.visit([&](uint32_t key, int32_t) { atomicAdd(&sh.hist[bucket(key)], 1u); });
+    __syncthreads();
+    find_digit<THREADS, true>(sh.hist, sh, rem, 256);
+    bsel = (int)sh.digit;
+    rem -= sh.before;
+    equal = sh.equal;
+    __syncthreads();
+  }
+  auto member = [&](uint32_t key) { return !bucketed || bucket(key) == bsel; };
+  // bits shared by the members of the bucket
+  uint32_t a = ~0u, o = 0u;
+  src.visit([&](uint32_t key, int32_t) {
+    if (member(key)) {
+      a &= key;
+      o |= key;
+    }
+  });
+  block_pair_reduce<THREADS, false>(a, o, sh);
+  const uint32_t diff = a ^ o;
+  int low = diff ? 32 - __clz(diff) : 0;  // key bits [0, low) still to resolve
+  uint32_t fixed = low == 32 ? 0u : ~((1u << low) - 1u);
+  uint32_t prefix = a & fixed;
+  while (low > 0) {
+    const int w = low < 8 ? low : 8, shift = low - w;
+    const uint32_t dmask = (1u << w) - 1u;
+    for (int i = tid; i < 256; i += THREADS) sh.hist[i] = 0;
     __syncthreads();
     src.visit([&](uint32_t key, int32_t) {
-      if ((key & mask) == prefix) atomicAdd(&sh.hist[(key >> shift) & dmask], 1u);
+      if ((key & fixed) == prefix && member(key)) atomicAdd(&sh.hist[(key >> shift) & dmask], 1u);
     });
     __syncthreads();
-    find_digit<THREADS, true>(sh, rem, bins);
+    find_digit<THREADS, true>(sh.hist, sh, rem, 256);
     rem -= sh.before;
     equal = sh.equal;
     prefix |= sh.digit << shift;
-    mask |= dmask << shift;
+    fixed |= dmask << shift;
+    low = shift;
     __syncthreads();
   }
   const uint32_t T = prefix;
@@ -101,7 +191,7 @@ __device__ void block_select(const Src& src, uint32_t need, SelectShared& sh, Em
         if (key == T && (p & imask) == ipref) atomicAdd(&sh.hist[(p >> shift) & 255u], 1u);
       });
       __syncthreads();
-      find_digit<THREADS, false>(sh, rem, 256);
+      find_digit<THREADS, false>(sh.hist, sh, rem, 256);
       rem -= sh.before;
       ipref |= sh.digit << shift;
       imask |= 255u << shift;
@@ -109,7 +199,8 @@ __device__ void block_select(const Src& src, uint32_t need, SelectShared& sh, Em
     }
   }
   src.visit([&](uint32_t key, int32_t pos) {
-    if (key > T || (key == T && (all_ties || (uint32_t)pos <= ipref))) emit(pos);
+    const bool take = key > T || (key == T && (all_ties || (uint32_t)pos <= ipref));
+    wave_append(take, &sh.emitted, [&](int slot) { put(slot, pos); });
   });
   __syncthreads();
 }
@@ -133,31 +224,31 @@ struct ArraySource {
 // than CAP keys, block_select() runs over the whole source instead.
 template <int CAP>
 struct TwoLevelShared {
+  uint32_t hist[4096];
   uint32_t ckey[CAP];
   int32_t cpos[CAP];
-  SelectShared sel;  // its 4096-bin histogram also serves the first level
+  SelectShared sel;
   uint32_t b1, above, in_b1;
   int32_t ncand;
 };
 
-template <int THREADS, int CAP, class Src, class Emit>
-__device__ void two_level_select(const Src& src, uint32_t m, TwoLevelShared<CAP>& sh, Emit emit) {
+template <int THREADS, int CAP, class Src, class Put>
+__device__ void two_level_select(const Src& src, uint32_t m, TwoLevelShared<CAP>& sh, Put put) {
   const int tid = threadIdx.x;
-  uint32_t* hist = sh.sel.hist;
+  uint32_t* hist = sh.hist;
   for (int k = tid; k < 4096; k += THREADS) hist[k] = 0;
   if (tid == 0) sh.ncand = 0;
   __syncthreads();
   src.visit([&](uint32_t key, int32_t) { atomicAdd(&hist[key >> 20], 1u); });
   __syncthreads();
-  find_digit<THREADS, true>(sh.sel, m, 4096);  // the bin holding the m-th key
+  find_digit<THREADS, true>(hist, sh.sel, m, 4096);  // the bin holding the m-th key
   const uint32_t b1 = sh.sel.digit, above = sh.sel.before, in_b1 = sh.sel.equal;
   __syncthreads();
   if (in_b1 <= (uint32_t)CAP) {
     src.visit([&](uint32_t key, int32_t pos) {
       const uint32_t top = key >> 20;
-      if (top > b1) {
-        emit(pos);
-      } else if (top == b1) {
+      wave_append(top > b1, &sh.sel.emitted, [&](int slot) { put(slot, pos); });
+      if (top == b1) {  // rare: a plain LDS atomic
         const int c = atomicAdd(&sh.ncand, 1);
         sh.ckey[c] = key;
         sh.cpos[c] = pos;
@@ -165,9 +256,9 @@ __device__ void two_level_select(const Src& src, uint32_t m, TwoLevelShared<CAP>
     });
     __syncthreads();
     ArraySource<THREADS> cand{sh.ckey, sh.cpos, sh.ncand};
-    block_select<THREADS>(cand, m - above, sh.sel, emit);
+    block_select<THREADS, false>(cand, m - above, sh.sel, put);
   } else {
-    block_select<THREADS>(src, m, sh.sel, emit);
+    block_select<THREADS, false>(src, m, sh.sel, put);
   }
 }
 

@@ -6,7 +6,7 @@
 // (R = 4 for fp8, 2 for bf16), held as the A operands of the MFMA row tile
 // (mfma_tile.h); the waves split C into 16-candidate fragments.  The candidate positions are staged in
 // LDS, so each lane reads its position there and gathers 32 bytes of that key
-// (and, for fp8, its scale) two fragments ahead of its use.  Scores go to a
+// (and, for fp8, its scale) three fragments ahead of its use.  Scores go to a
 // [group, member, |C|] fp32 buffer (it stays in the last-level cache for the
 // select that follows).
 //
@@ -75,37 +75,41 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void r
 
   const int qr = kg / Tile::G;
   const bool writer = (kg % Tile::G) == 0 && qr < rows_here;
-  float* mrow = rsc + (((int64_t)b * n_groups + j) * g + R * blk + qr) * (int64_t)c;
+  // scores leave through a buffer resource over the block's R member rows;
+  // lanes with nothing to store give an offset past its end (dropped), so
+  // every lane issues the same memory operations and the waits stay exact
+  const __amdgpu_buffer_rsrc_t orr =
+      buffer_rsrc(rsc + (((int64_t)b * n_groups + j) * g + R * blk) * (int64_t)c, (uint32_t)(R * c * 4));
+  const uint32_t my_off = (uint32_t)(qr * c + cbeg) * 4u;
   const int nfrag = fend - fbeg;
   constexpr int S = 4;  // fragment stride between the waves
   auto pos_of = [&](int f) { return spos[min(16 * f + lr, ncs - 1)]; };
   auto emit = [&](float acc, float ks, int f) {
-    acc *= ks;
-    asm volatile("" : "+v"(acc));  // keep the epilogue ahead of the store's branch
     const int slot = 16 * f + lr;
-    if (writer && slot < ncs) mrow[cbeg + slot] = acc;
+    const uint32_t off = (writer && slot < ncs) ? my_off + 4u * (uint32_t)slot : 0xFFFFFFFFu;
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc * ks), orr, off, 0, 0);
   };
   auto scale_of = [&](int p) { return DT == kFp8 ? ksb[p] : 1.0f; };
-  // two fragments in flight per wave; loads past the end repeat the last
-  // candidate (never stored)
+  auto fetch = [&](KeyFrag<DT>& kf, float& sc, int ff) {
+    const int p = pos_of(ff);
+    sc = scale_of(p);
+    kf.load(kb + (int64_t)p * kD * EB, kg);
+  };
+  // three fragments in flight per wave, with no exits in the loop body:
+  // fragments past the end repeat the last candidate and are not stored
   int f = wave;
-  KeyFrag<DT> k0, k1;
-  int pn = pos_of(f);
-  float s0 = scale_of(pn), s1;
-  k0.load(kb + (int64_t)pn * kD * EB, kg);
-  pn = pos_of(f + S);
-  s1 = scale_of(pn);
-  k1.load(kb + (int64_t)pn * kD * EB, kg);
-  for (; f < nfrag; f += 2 * S) {
-    pn = pos_of(f + 2 * S);
+  KeyFrag<DT> k0, k1, k2;
+  float s0, s1, s2;
+  fetch(k0, s0, f);
+  fetch(k1, s1, f + S);
+  fetch(k2, s2, f + 2 * S);
+  for (; f < nfrag; f += 3 * S) {
     emit(tile.score(k0), s0, f);
-    s0 = scale_of(pn);
-    k0.load(kb + (int64_t)pn * kD * EB, kg);
-    if (f + S >= nfrag) break;
-    pn = pos_of(f + 3 * S);
+    fetch(k0, s0, f + 3 * S);
     emit(tile.score(k1), s1, f + S);
-    s1 = scale_of(pn);
-    k1.load(kb + (int64_t)pn * kD * EB, kg);
+    fetch(k1, s1, f + 4 * S);
+    emit(tile.score(k2), s2, f + 2 * S);
+    fetch(k2, s2, f + 5 * S);
   }
 }
 
@@ -156,7 +160,7 @@ __global__ __launch_bounds__(256) void topk_short_kernel(const float* __restrict
   }
   if (tid == 0) sel.emitted = 0;
   __syncthreads();
-  block_select<256>(src, (uint32_t)m, sel, [&](int32_t p) { orow[atomicAdd(&sel.emitted, 1)] = p; });
+  block_select<256, true>(src, (uint32_t)m, sel, [&](int slot, int32_t p) { orow[slot] = p; });
 }
 
 hipError_t launch_refine(int dtype, const void* q, const float* q_scale, const float* w, const uint8_t* lin,
@@ -170,7 +174,8 @@ hipError_t launch_refine(int dtype, const void* q, const float* q_scale, const f
   const int R = dtype == kFp8 ? 4 : 2;
   const int64_t wgs = (int64_t)(j1 - j0) * st.n * ((g + R - 1) / R);
   const int nfrag = (c + 15) / 16;
-  const int parts = (int)std::max<int64_t>(1, std::min<int64_t>(std::max(1, nfrag / 8), (512 + wgs - 1) / wgs));
+  // (at least 6 fragments per wave: the loop runs in steps of 3)
+  const int parts = (int)std::max<int64_t>(1, std::min<int64_t>(std::max(1, nfrag / 24), (512 + wgs - 1) / wgs));
   const dim3 grid((unsigned)(j1 - j0), (unsigned)st.n, (unsigned)(((g + R - 1) / R) * parts));
   if (dtype == kFp8)
     hipLaunchKernelGGL((rescore_kernel<kFp8, 4>), grid, dim3(256), 0, stream, (const uint8_t*)q, q_scale, w, lin,

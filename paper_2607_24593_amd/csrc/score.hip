@@ -93,19 +93,27 @@ __global__ __launch_bounds__(256) void score_kernel(const uint8_t* __restrict__ 
   const int my_i = i_w + qr;
   const bool writer = (kg % Tile::G) == 0 && row_active(st, rs, b, my_i);
   const int my_n = (int)min((int64_t)nkeys, row_limit(st, rs, b, my_i) + 1 - seg0);  // keys this row takes
-  float* orow = out + ((int64_t)b * nrows + (my_i - rs.i0)) * ld + seg0;
+  // Scores leave through a buffer resource over the wave's R output rows:
+  // lanes with nothing to store give an offset past its end, which the
+  // hardware drops.  Every lane issues the same stores, so the count of
+  // outstanding memory operations never depends on the data and the waits
+  // before each fragment stay exact.  (The host keeps R * ld * 4 < 2^31.)
+  const __amdgpu_buffer_rsrc_t orr = buffer_rsrc(out + ((int64_t)b * nrows + (i_w - rs.i0)) * ld + seg0,
+                                                 (uint32_t)(((int64_t)(R - 1) * ld + nkeys) * 4));
+  const uint32_t my_off = (uint32_t)((int64_t)qr * ld * 4);
 
   const int S = KSPLIT ? 64 : 16;
   int t = KSPLIT ? 16 * wave : 0;  // key offset within the segment
   auto emit = [&](float acc, int base) {
-    asm volatile("" : "+v"(acc));  // keep the epilogue ahead of the store's branch
     const int s = base + lr;
-    if (writer && s < my_n) {
-      if constexpr (DT == kFp8) acc *= sks[s];
-      orow[s] = acc;
-    }
+    if constexpr (DT == kFp8) acc *= sks[s & 4095];
+    const uint32_t off = (writer && s < my_n) ? my_off + 4u * (uint32_t)s : 0xFFFFFFFFu;
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc), orr, off, 0, 0);
   };
   // Three key fragments rotate: while one is scored the next two are loading.
+  // The loop body has no exits, so the compiler keeps each reload right after
+  // the fragment's last use; fragments past the wave's keys read zeros and
+  // their stores are dropped.
   KeyFrag<DT> f0, f1, f2;
   f0.load(kr, (uint32_t)(t + lr) * KB, kg);
   f1.load(kr, (uint32_t)(t + S + lr) * KB, kg);
@@ -113,10 +121,8 @@ __global__ __launch_bounds__(256) void score_kernel(const uint8_t* __restrict__ 
   for (; t < nkeys; t += 3 * S) {
     emit(tile.score(f0), t);
     f0.load(kr, (uint32_t)(t + 3 * S + lr) * KB, kg);
-    if (t + S >= nkeys) break;
     emit(tile.score(f1), t + S);
     f1.load(kr, (uint32_t)(t + 4 * S + lr) * KB, kg);
-    if (t + 2 * S >= nkeys) break;
     emit(tile.score(f2), t + 2 * S);
     f2.load(kr, (uint32_t)(t + 5 * S + lr) * KB, kg);
   }

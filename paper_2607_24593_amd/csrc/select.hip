@@ -81,24 +81,25 @@ struct SampleSource {
   }
 };
 
-// 20-bit key prefix of the ts-th largest sampled key (ts <= sampled count).
+// 20-bit key prefix of the ts-th largest sampled key (ts <= sampled count);
+// hist: 4096 bins of LDS.
 template <class Src>
-__device__ uint32_t sample_prefix(const Src& src, uint32_t ts, SelectShared& sh) {
+__device__ uint32_t sample_prefix(const Src& src, uint32_t ts, uint32_t* hist, SelectShared& sh) {
   const int tid = threadIdx.x;
-  for (int k = tid; k < 4096; k += kSelThreads) sh.hist[k] = 0;
+  for (int k = tid; k < 4096; k += kSelThreads) hist[k] = 0;
   __syncthreads();
-  src.visit([&](uint32_t key, int32_t) { atomicAdd(&sh.hist[key >> 20], 1u); });
+  src.visit([&](uint32_t key, int32_t) { atomicAdd(&hist[key >> 20], 1u); });
   __syncthreads();
-  find_digit<kSelThreads, true>(sh, ts, 4096);
+  find_digit<kSelThreads, true>(hist, sh, ts, 4096);
   const uint32_t d1 = sh.digit, rem = ts - sh.before;
   __syncthreads();
-  for (int k = tid; k < 256; k += kSelThreads) sh.hist[k] = 0;
+  for (int k = tid; k < 256; k += kSelThreads) hist[k] = 0;
   __syncthreads();
   src.visit([&](uint32_t key, int32_t) {
-    if ((key >> 20) == d1) atomicAdd(&sh.hist[(key >> 12) & 255u], 1u);
+    if ((key >> 20) == d1) atomicAdd(&hist[(key >> 12) & 255u], 1u);
   });
   __syncthreads();
-  find_digit<kSelThreads, true>(sh, rem, 256);
+  find_digit<kSelThreads, true>(hist, sh, rem, 256);
   const uint32_t thr = (d1 << 8) | sh.digit;
   __syncthreads();
   return thr;
@@ -135,7 +136,6 @@ __global__ __launch_bounds__(kSelThreads) void topk_rows_kernel(const float* __r
     return;
   }
   if (tid == 0) sh.sel.emitted = 0;
-  auto emit = [&](int32_t p) { put(atomicAdd(&sh.sel.emitted, 1), p); };
   RowSource src{row, n};
   const bool aligned = (reinterpret_cast<uintptr_t>(row) & 15u) == 0;
   if (n >= kSampleMinLen && aligned) {
@@ -160,11 +160,11 @@ __global__ __launch_bounds__(kSelThreads) void topk_rows_kernel(const float* __r
     const uint32_t ts = (uint32_t)ceilf(rm + 4.0f * sqrtf(rm)) + 1u;
     // expected compacted count ts n / s: leave room for its spread
     if (ts < (uint32_t)s && (float)ts * (float)n <= 0.8f * (float)CAP * (float)s) {
-      const uint32_t thr = sample_prefix(smp, ts, sh.sel);
+      const uint32_t thr = sample_prefix(smp, ts, sh.hist, sh.sel);
       if (tid == 0) sh.ncand = 0;
       __syncthreads();
       src.visit([&](uint32_t key, int32_t pos) {
-        if ((key >> 12) >= thr) {
+        if ((key >> 12) >= thr) {  // a few percent of the row: plain LDS atomics
           const int c = atomicAdd(&sh.ncand, 1);
           if (c < CAP) {
             sh.ckey[c] = key;
@@ -177,12 +177,12 @@ __global__ __launch_bounds__(kSelThreads) void topk_rows_kernel(const float* __r
       __syncthreads();  // every thread has read the count before it is reused
       if (found >= m && found <= CAP) {
         ArraySource<kSelThreads> cand{sh.ckey, sh.cpos, found};
-        block_select<kSelThreads>(cand, (uint32_t)m, sh.sel, emit);
+        block_select<kSelThreads, false>(cand, (uint32_t)m, sh.sel, put);
         return;
       }
     }
   }
-  two_level_select<kSelThreads>(src, (uint32_t)m, sh, emit);
+  two_level_select<kSelThreads>(src, (uint32_t)m, sh, put);
 }
 
 // ---------------------------------------------------------------------------
@@ -377,13 +377,11 @@ __global__ __launch_bounds__(256) void split_emit_kernel(const float* __restrict
   for (int e = lo + (int)threadIdx.x; e < hi; e += 256) {
     const uint32_t key = float_key(row[e]);
     const uint32_t top = key >> 20;
-    if (top > t.b1) {
-      put_index(od, rr.b, rr.i, base_above + atomicAdd(&n_above, 1), e);
-    } else if (top == t.b1) {
-      const int c = base_equal + atomicAdd(&n_equal, 1);
-      ck[c] = key;
-      cp[c] = e;
-    }
+    wave_append(top > t.b1, &n_above, [&](int slot) { put_index(od, rr.b, rr.i, base_above + slot, e); });
+    wave_append(top == t.b1, &n_equal, [&](int slot) {
+      ck[base_equal + slot] = key;
+      cp[base_equal + slot] = e;
+    });
   }
 }
 
@@ -423,13 +421,13 @@ __global__ __launch_bounds__(256) void split_final_kernel(const float* __restric
   SplitRowHeader* head = sc.head + r;
   if (threadIdx.x == 0) sel.emitted = (t.in_b1 <= (uint32_t)sc.cap) ? head->emitted : 0;
   __syncthreads();
-  auto emit = [&](int32_t p) { put_index(od, rr.b, rr.i, atomicAdd(&sel.emitted, 1), p); };
+  auto put = [&](int slot, int32_t p) { put_index(od, rr.b, rr.i, slot, p); };
   if (t.in_b1 <= (uint32_t)sc.cap) {
     GlobalArraySource src{sc.ckey + (int64_t)r * sc.cap, sc.cpos + (int64_t)r * sc.cap, head->ncand};
-    block_select<256>(src, (uint32_t)m - t.above, sel, emit);
+    block_select<256, false>(src, (uint32_t)m - t.above, sel, put);
   } else {
     GlobalRowSource src{scores + (int64_t)r * ld, rr.n};
-    block_select<256>(src, (uint32_t)m, sel, emit);
+    block_select<256, false>(src, (uint32_t)m, sel, put);
   }
 }
 

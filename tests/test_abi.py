@@ -84,6 +84,7 @@ def test_null_args():
     (dict(q_pos0=10, n_k=70), pv.PIVOT_ERR_INVALID_ARG),      # n_k < q_pos0 + n_q
     (dict(q_pos0=-3), pv.PIVOT_ERR_INVALID_ARG),
     (dict(scales=False), pv.PIVOT_ERR_INVALID_ARG),          # fp8 without scales
+    (dict(q_pos0=pv.PIVOT_MAX_KEYS - 63, n_q=64), pv.PIVOT_ERR_UNSUPPORTED),  # n_k past the key limit
 ])
 def test_dense_validation(kw, status):
     a = args(**kw)
@@ -159,6 +160,8 @@ def test_stage_validation():
         pv.PIVOT_ERR_INVALID_ARG                               # ld < lim + 1
     assert L.pivot_score_rows(1, 32, 128, 4, FAKE, FAKE, FAKE, FAKE, FAKE, 10, 1, FAKE, 64, FAKE, 1 << 20, None) == \
         pv.PIVOT_ERR_UNSUPPORTED
+    assert L.pivot_score_rows(1, 64, 128, 4, FAKE, FAKE, FAKE, FAKE, FAKE, 10, 1, FAKE, pv.PIVOT_MAX_KEYS + 64,
+                              FAKE, 1 << 20, None) == pv.PIVOT_ERR_UNSUPPORTED  # ld past the key limit
     need = pv.score_rows_workspace(4)
     assert L.pivot_score_rows(1, 64, 128, 4, FAKE, FAKE, FAKE, FAKE, FAKE, 10, 1, FAKE, 64, FAKE, need - 1, None) == \
         pv.PIVOT_ERR_WORKSPACE
