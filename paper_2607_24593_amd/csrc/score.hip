@@ -52,19 +52,14 @@ __global__ __launch_bounds__(256) void score_kernel(const uint8_t* __restrict__ 
     if (row_active(st, rs, b, i_blk + r)) lim_blk = max(lim_blk, row_limit(st, rs, b, i_blk + r));
   if (lim_blk < seg0) return;
   const int nseg_keys = (int)(min(seg0 + (int64_t)seg_keys, lim_blk + 1) - seg0);
-  const float* ksb = (DT == kFp8) ? k_scale + (int64_t)b * k_seq_stride + seg0 : nullptr;
-  if constexpr (DT == kFp8) {
-    for (int e = tid; e < nseg_keys; e += 256) sks[e] = ksb[e];
-    __syncthreads();
-  }
 
   const int i_w = i_blk + (KSPLIT ? 0 : wave * R);
   int64_t lim_max = -1;
 #pragma unroll
   for (int r = 0; r < R; ++r)
     if (row_active(st, rs, b, i_w + r)) lim_max = max(lim_max, row_limit(st, rs, b, i_w + r));
-  if (lim_max < seg0) return;  // no workgroup barrier follows
-  const int nkeys = (int)(min(seg0 + (int64_t)seg_keys, lim_max + 1) - seg0);  // this wave's keys
+  // this wave's keys (0: the wave only helps stage the key scales)
+  const int nkeys = lim_max < seg0 ? 0 : (int)(min(seg0 + (int64_t)seg_keys, lim_max + 1) - seg0);
 
   const uint8_t* rows[R];
   const float* wrows[R];
@@ -81,6 +76,18 @@ __global__ __launch_bounds__(256) void score_kernel(const uint8_t* __restrict__ 
     lrows[r] = (DT == kFp8) ? lin + row * kLinBytes : nullptr;
     lsc[r] = (DT == kFp8) ? lin_scale + row * kLinLevels : nullptr;
   }
+  // The segment's key scales, the row tile and the first key fragments are
+  // all requested before the one workgroup barrier, the scales first (all 16
+  // loads of a thread in flight at once, range-checked), so their latencies
+  // overlap and the scales can be written to LDS without waiting for the rest.
+  constexpr int KS_PER = 4096 / 256;
+  float ksv[KS_PER];
+  if constexpr (DT == kFp8) {
+    const __amdgpu_buffer_rsrc_t ksr = buffer_rsrc(k_scale + (int64_t)b * k_seq_stride + seg0, (uint32_t)nseg_keys * 4);
+#pragma unroll
+    for (int u = 0; u < KS_PER; ++u)
+      ksv[u] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(ksr, (uint32_t)(tid + 256 * u) * 4u, 0, 0));
+  }
   Tile tile;
   tile.load(rows, wrows, qs, lrows, lsc, lane);
 
@@ -88,6 +95,21 @@ __global__ __launch_bounds__(256) void score_kernel(const uint8_t* __restrict__ 
   // 32-bit and fragments that run past the wave's last key read zeros
   const __amdgpu_buffer_rsrc_t kr =
       buffer_rsrc(k + ((int64_t)b * k_seq_stride + seg0) * KB, (uint32_t)nkeys * KB);
+  const int S = KSPLIT ? 64 : 16;
+  int t = KSPLIT ? 16 * wave : 0;  // key offset within the segment
+  const int lr0 = lane & 15, kg0 = lane >> 4;
+  KeyFrag<DT> f0, f1, f2;
+  f0.load(kr, (uint32_t)(t + lr0) * KB, kg0);
+  f1.load(kr, (uint32_t)(t + S + lr0) * KB, kg0);
+  f2.load(kr, (uint32_t)(t + 2 * S + lr0) * KB, kg0);
+
+  if constexpr (DT == kFp8) {
+#pragma unroll
+    for (int u = 0; u < KS_PER; ++u) sks[tid + 256 * u] = ksv[u];  // zeros past the segment
+    __syncthreads();
+  }
+  if (nkeys == 0) return;  // no workgroup barrier follows
+
   const int lr = lane & 15, kg = lane >> 4;
   const int qr = kg / Tile::G;
   const int my_i = i_w + qr;
@@ -102,8 +124,6 @@ __global__ __launch_bounds__(256) void score_kernel(const uint8_t* __restrict__ 
                                                  (uint32_t)(((int64_t)(R - 1) * ld + nkeys) * 4));
   const uint32_t my_off = (uint32_t)((int64_t)qr * ld * 4);
 
-  const int S = KSPLIT ? 64 : 16;
-  int t = KSPLIT ? 16 * wave : 0;  // key offset within the segment
   auto emit = [&](float acc, int base) {
     const int s = base + lr;
     if constexpr (DT == kFp8) acc *= sks[s & 4095];
@@ -114,10 +134,6 @@ __global__ __launch_bounds__(256) void score_kernel(const uint8_t* __restrict__ 
   // The loop body has no exits, so the compiler keeps each reload right after
   // the fragment's last use; fragments past the wave's keys read zeros and
   // their stores are dropped.
-  KeyFrag<DT> f0, f1, f2;
-  f0.load(kr, (uint32_t)(t + lr) * KB, kg);
-  f1.load(kr, (uint32_t)(t + S + lr) * KB, kg);
-  f2.load(kr, (uint32_t)(t + 2 * S + lr) * KB, kg);
   for (; t < nkeys; t += 3 * S) {
     emit(tile.score(f0), t);
     f0.load(kr, (uint32_t)(t + 3 * S + lr) * KB, kg);
