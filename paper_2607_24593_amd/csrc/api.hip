@@ -91,7 +91,6 @@ struct Plan {
   size_t off_pq = 0, off_psc = 0, off_pw = 0, off_cand = 0, off_scores = 0, fixed = 0;
   size_t off_qlin = 0, off_qlsc = 0, off_plin = 0, off_plsc = 0;  // fp8 epilogue's linear term
   size_t off_rsc = 0;                                              // Refine member scores
-  size_t off_split = 0, split_bytes = 0;                           // split select (few long rows)
   bool qlin = false, plin = false;
 };
 
@@ -209,14 +208,6 @@ pivot_status make_plan(const pivot_args* a, int mode, int g, int c, int dense_be
       if (!ext_cand) off = align_up(off + ng * (size_t)c * sizeof(int32_t));
     }
   }
-  // few long rows (decode): each row's selection is spread over several workgroups
-  const int64_t sel_rows = std::max<int64_t>(p.dense_hi > 0 ? (int64_t)p.B * p.n_q : 0,
-                                             proxies ? (int64_t)p.B * p.n_groups : 0);
-  if (sel_rows > 0 && sel_rows <= kSplitMaxRows && p.max_nk >= kSplitMinLen) {
-    p.off_split = off;
-    p.split_bytes = split_scratch_bytes(sel_rows, kSplitCap);
-    off = align_up(off + p.split_bytes);
-  }
   p.off_scores = off;
   p.fixed = off;
   return PIVOT_OK;
@@ -326,9 +317,7 @@ pivot_status run_rows(const pivot_args* a, const Plan& p, int kind, int lo, int 
       if (s != PIVOT_OK) return s;
       s = hip_check(timed(PIVOT_KERNEL_SELECT, stream,
                           [&] {
-                            return launch_topk(scores, ld, st, rs, od,
-                                               p.split_bytes ? (uint8_t*)a->workspace + p.off_split : nullptr,
-                                               p.split_bytes, lim, stream);
+                            return launch_topk(scores, ld, st, rs, od, lim, stream);
                           }),
                     "top-k kernel");
       if (s != PIVOT_OK) return s;
@@ -584,7 +573,7 @@ pivot_status pivot_topk_rows(int32_t n_rows, const float* scores, int64_t ld, in
   st.q_pos0[0] = (int32_t)(n0 - 1);
   RowSpace rs{0, n_rows, n_step, kAll};
   OutDesc od{out, m, n_rows, 0, 0};
-  return hip_check(launch_topk(scores, ld, st, rs, od, nullptr, 0, n_max - 1, (hipStream_t)stream), "top-k kernel");
+  return hip_check(launch_topk(scores, ld, st, rs, od, n_max - 1, (hipStream_t)stream), "top-k kernel");
 }
 
 pivot_status pivot_encode_e4m3(const float* x, uint8_t* out, int64_t n, void* stream) {

@@ -39,17 +39,11 @@ hipError_t launch_score(int dtype, const void* q, const float* q_scale, const fl
                         int64_t k_seq_stride, const SeqTable& st, const RowSpace& rs, int64_t lim_max, float* out,
                         int64_t ld, hipStream_t stream);
 
-// Top-m of score rows: row (b, i) has limit + 1 valid entries.  Launches with
-// at most kSplitMaxRows rows of at least kSplitMinLen entries spread each row
-// over several workgroups when `scratch` holds split_scratch_bytes(rows,
-// kSplitCap) bytes; otherwise (or with scratch == nullptr) one workgroup per row.
-constexpr int kSplitMaxRows = 256;
-constexpr int kSplitMinLen = 16384;
-constexpr int kSplitCap = 16384;
-size_t split_scratch_bytes(int64_t rows, int cap);
+// Top-m of score rows: row (b, i) has limit + 1 valid entries; lim_max is
+// the largest limit.  Up to 256 long rows (decode) get one 1024-thread
+// workgroup each, more rows one 512-thread workgroup each.
 hipError_t launch_topk(const float* scores, int64_t ld, const SeqTable& st, const RowSpace& rs,
-                       const OutDesc& od, void* scratch, size_t scratch_bytes, int64_t lim_max,
-                       hipStream_t stream);
+                       const OutDesc& od, int64_t lim_max, hipStream_t stream);
 
 // Refine (Eqs. 8-9) for groups [j0, j1) with j >= first_proxy[b]: re-score
 // the candidates into rescore [B, n_groups, g, c] fp32, then select top-m.
