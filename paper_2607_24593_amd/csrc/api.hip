@@ -344,9 +344,15 @@ pivot_status check_workspace(const pivot_args* a, const Plan& p, int64_t& score_
 
 // Linear-term rows (mfma_tile.h) of the call's queries: all of them for a
 // batch or when Refine re-scores members, else the leading dense rows.
+// Query rows that need the fp8 linear term: the dense rows, or every row when
+// Refine re-scores the members.
+int64_t query_lin_rows(const Plan& p) {
+  return (p.B == 1 && p.mode != PIVOT_REFINE) ? p.dense_hi : (int64_t)p.B * p.n_q;
+}
+
 pivot_status query_lin(const pivot_args* a, const Plan& p, uint8_t* ws, hipStream_t stream) {
   if (!p.qlin) return PIVOT_OK;
-  const int64_t rows = (p.B == 1 && p.mode != PIVOT_REFINE) ? p.dense_hi : (int64_t)p.B * p.n_q;
+  const int64_t rows = query_lin_rows(p);
   return hip_check(timed(PIVOT_KERNEL_LIN, stream, [&] {
                      return launch_lin(a->q, a->q_scale, a->w, 0, rows, ws + p.off_qlin,
                                        reinterpret_cast<float*>(ws + p.off_qlsc), stream);
@@ -409,11 +415,51 @@ pivot_status pivot_group_index(const pivot_args* a, int32_t mode, int32_t g, int
   uint8_t* ws = (uint8_t*)a->workspace;
   float* scores = reinterpret_cast<float*>(ws + p.off_scores);
 
-  s = query_lin(a, p, ws, stream);
-  if (s != PIVOT_OK) return s;
+  void* pq = ws + p.off_pq;
+  float* psc = reinterpret_cast<float*>(ws + p.off_psc);
+  float* pw = reinterpret_cast<float*>(ws + p.off_pw);
+  int32_t* cand = (mode == PIVOT_REFINE) ? (out_cand ? out_cand : reinterpret_cast<int32_t*>(ws + p.off_cand))
+                                         : nullptr;
+  const float* qs = p.dtype == PIVOT_DT_FP8_E4M3 ? a->q_scale : nullptr;
+  const bool any_proxy = p.proxy_lo < p.n_groups;
+
+  if (any_proxy)
+    for (int b0 = 0; b0 < p.B; b0 += kMaxSeq) {  // Eq. 4 proxies
+      const int nb = std::min(kMaxSeq, p.B - b0);
+      SeqTable st = table_for(p, b0, nb);
+      const size_t qoff = (size_t)b0 * p.n_q;
+      const size_t poff = (size_t)b0 * p.n_groups;
+      s = hip_check(timed(PIVOT_KERNEL_PROXY, stream, [&] {
+                      return launch_proxy(p.dtype, (const uint8_t*)a->q + qoff * p.row_bytes,
+                                          qs ? qs + qoff : nullptr, a->w + qoff * kH, p.n_q, p.g, p.n_groups, st,
+                                          p.proxy_lo, p.n_groups, false, (uint8_t*)pq + poff * p.row_bytes,
+                                          psc + poff, pw + poff * kH, stream);
+                    }),
+                    "proxy kernel");
+      if (s != PIVOT_OK) return s;
+    }
+
+  // the fp8 linear terms of the query rows (dense rows, Refine members) and of
+  // the proxies, in one launch
+  uint8_t* plin = p.plin ? ws + p.off_plin : nullptr;
+  float* plsc = p.plin ? reinterpret_cast<float*>(ws + p.off_plsc) : nullptr;
+  {
+    LinRows qset, pset;
+    if (p.qlin)
+      qset = LinRows{(const uint8_t*)a->q, a->q_scale, a->w, 0, query_lin_rows(p), ws + p.off_qlin,
+                     reinterpret_cast<float*>(ws + p.off_qlsc)};
+    if (p.plin)
+      pset = LinRows{(const uint8_t*)pq, psc, pw, p.B == 1 ? p.proxy_lo : 0, (int64_t)p.B * p.n_groups, plin, plsc};
+    if (p.qlin || p.plin) {
+      s = hip_check(timed(PIVOT_KERNEL_LIN, stream, [&] { return launch_lin(qset, pset, stream); }),
+                    "linear-term kernel");
+      if (s != PIVOT_OK) return s;
+    }
+  }
+
   s = dense_part(a, p, scores, score_bytes, stream);  // guardrail groups (Algorithm 1)
   if (s != PIVOT_OK) return s;
-  if (p.proxy_lo >= p.n_groups) {
+  if (!any_proxy) {
     if (out_cand && mode == PIVOT_REFINE)
       for (int b0 = 0; b0 < p.B; b0 += kMaxSeq) {
         const int nb = std::min(kMaxSeq, p.B - b0);
@@ -426,38 +472,6 @@ pivot_status pivot_group_index(const pivot_args* a, int32_t mode, int32_t g, int
         if (s != PIVOT_OK) return s;
       }
     return PIVOT_OK;
-  }
-
-  void* pq = ws + p.off_pq;
-  float* psc = reinterpret_cast<float*>(ws + p.off_psc);
-  float* pw = reinterpret_cast<float*>(ws + p.off_pw);
-  int32_t* cand = (mode == PIVOT_REFINE) ? (out_cand ? out_cand : reinterpret_cast<int32_t*>(ws + p.off_cand))
-                                         : nullptr;
-  const float* qs = p.dtype == PIVOT_DT_FP8_E4M3 ? a->q_scale : nullptr;
-
-  for (int b0 = 0; b0 < p.B; b0 += kMaxSeq) {  // Eq. 4 proxies
-    const int nb = std::min(kMaxSeq, p.B - b0);
-    SeqTable st = table_for(p, b0, nb);
-    const size_t qoff = (size_t)b0 * p.n_q;
-    const size_t poff = (size_t)b0 * p.n_groups;
-    s = hip_check(timed(PIVOT_KERNEL_PROXY, stream, [&] {
-                    return launch_proxy(p.dtype, (const uint8_t*)a->q + qoff * p.row_bytes,
-                                        qs ? qs + qoff : nullptr, a->w + qoff * kH, p.n_q, p.g, p.n_groups, st,
-                                        p.proxy_lo, p.n_groups, false, (uint8_t*)pq + poff * p.row_bytes,
-                                        psc + poff, pw + poff * kH, stream);
-                  }),
-                  "proxy kernel");
-    if (s != PIVOT_OK) return s;
-  }
-
-  uint8_t* plin = p.plin ? ws + p.off_plin : nullptr;
-  float* plsc = p.plin ? reinterpret_cast<float*>(ws + p.off_plsc) : nullptr;
-  if (p.plin) {
-    const int64_t r0 = p.B == 1 ? p.proxy_lo : 0, r1 = (int64_t)p.B * p.n_groups;
-    s = hip_check(timed(PIVOT_KERNEL_LIN, stream,
-                        [&] { return launch_lin(pq, psc, pw, r0, r1, plin, plsc, stream); }),
-                  "linear-term kernel");
-    if (s != PIVOT_OK) return s;
   }
 
   // Eq. 5 proxy scan, then Eq. 6 (Reuse: top-k shared by the members) or

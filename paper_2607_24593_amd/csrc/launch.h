@@ -27,7 +27,17 @@ hipError_t launch_proxy(int dtype, const void* q, const float* q_scale, const fl
                         float* psc, float* pw, hipStream_t stream);
 
 // The fp8 epilogue's linear term (mfma_tile.h) for flat rows [r0, r1) of an
-// fp8 row array: lin [rows, 4 * 128] codes, lin_scale [rows, 4].
+// fp8 row array: lin [rows, 4 * 128] codes, lin_scale [rows, 4].  The two-set
+// form covers two row arrays (e.g. query rows and their proxies) in one launch.
+struct LinRows {
+  const uint8_t* q = nullptr;
+  const float* q_scale = nullptr;
+  const float* w = nullptr;
+  int64_t r0 = 0, r1 = 0;
+  uint8_t* lin = nullptr;
+  float* lin_scale = nullptr;
+};
+hipError_t launch_lin(const LinRows& set0, const LinRows& set1, hipStream_t stream);
 hipError_t launch_lin(const void* q, const float* q_scale, const float* w, int64_t r0, int64_t r1, uint8_t* lin,
                       float* lin_scale, hipStream_t stream);
 

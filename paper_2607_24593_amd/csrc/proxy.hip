@@ -179,23 +179,24 @@ namespace pivot {
 // level l holds codes c_l = RNE((u - sum_{l'<l} sigma_l' c_l') / sigma_l) with
 // sigma_l = max|residual| / 448, so the remaining error shrinks ~16x per level.
 // One wave per row; lane l owns dims 2l and 2l+1.
-__global__ __launch_bounds__(256) void lin_kernel(const uint8_t* __restrict__ q, const float* __restrict__ q_scale,
-                                                  const float* __restrict__ w, int64_t r0, int64_t r1,
-                                                  uint8_t* __restrict__ lin, float* __restrict__ lin_scale) {
+__global__ __launch_bounds__(256) void lin_kernel(LinRows set0, LinRows set1, int64_t blocks0) {
+  const bool first = blockIdx.x < blocks0;
+  const LinRows rs = first ? set0 : set1;
   const int lane = threadIdx.x & 63;
-  const int64_t row = r0 + (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (row >= r1) return;
-  const uint8_t* qr = q + row * (int64_t)(kH * kD);
-  const float* wr = w + row * kH;
-  const float half_scale = q_scale[row] * 0.5f;
+  const int64_t row = rs.r0 + ((int64_t)blockIdx.x - (first ? 0 : blocks0)) * 4 + (threadIdx.x >> 6);
+  if (row >= rs.r1) return;
+  const uint8_t* qr = rs.q + row * (int64_t)(kH * kD);
+  const float* wr = rs.w + row * kH;
+  const float half_scale = rs.q_scale[row] * 0.5f;
   float u0 = 0.f, u1 = 0.f;
+#pragma unroll 16
   for (int h = 0; h < kH; ++h) {
     const float wh = wr[h] * half_scale;
     const uint32_t pair = *reinterpret_cast<const uint16_t*>(qr + h * kD + 2 * lane);
     u0 = fmaf(wh, __builtin_amdgcn_cvt_f32_fp8((int)pair, 0), u0);
     u1 = fmaf(wh, __builtin_amdgcn_cvt_f32_fp8((int)pair, 1), u1);
   }
-  uint8_t* out = lin + row * (int64_t)kLinBytes;
+  uint8_t* out = rs.lin + row * (int64_t)kLinBytes;
 #pragma unroll
   for (int l = 0; l < kLinLevels; ++l) {
     const float amax = wave_max(fmaxf(fabsf(u0), fabsf(u1)));
@@ -204,17 +205,22 @@ __global__ __launch_bounds__(256) void lin_kernel(const uint8_t* __restrict__ q,
     *reinterpret_cast<uint16_t*>(out + l * kD + 2 * lane) = (uint16_t)word;
     u0 -= sigma * __builtin_amdgcn_cvt_f32_fp8(word, 0);
     u1 -= sigma * __builtin_amdgcn_cvt_f32_fp8(word, 1);
-    if (lane == 0) lin_scale[row * kLinLevels + l] = sigma;
+    if (lane == 0) rs.lin_scale[row * kLinLevels + l] = sigma;
   }
+}
+
+hipError_t launch_lin(const LinRows& set0, const LinRows& set1, hipStream_t stream) {
+  const int64_t b0 = set0.r1 > set0.r0 ? (set0.r1 - set0.r0 + 3) / 4 : 0;
+  const int64_t b1 = set1.r1 > set1.r0 ? (set1.r1 - set1.r0 + 3) / 4 : 0;
+  if (b0 + b1 == 0) return hipSuccess;
+  if (b0 + b1 > 0x7FFFFFFF) return hipErrorInvalidConfiguration;
+  hipLaunchKernelGGL(lin_kernel, dim3((unsigned)(b0 + b1)), dim3(256), 0, stream, set0, set1, b0);
+  return hipGetLastError();
 }
 
 hipError_t launch_lin(const void* q, const float* q_scale, const float* w, int64_t r0, int64_t r1, uint8_t* lin,
                       float* lin_scale, hipStream_t stream) {
-  if (r1 <= r0) return hipSuccess;
-  const int64_t blocks = (r1 - r0 + 3) / 4;
-  hipLaunchKernelGGL(lin_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, (const uint8_t*)q, q_scale, w, r0,
-                     r1, lin, lin_scale);
-  return hipGetLastError();
+  return launch_lin(LinRows{(const uint8_t*)q, q_scale, w, r0, r1, lin, lin_scale}, LinRows{}, stream);
 }
 
 }  // namespace pivot
