@@ -136,19 +136,22 @@ def test_empty_call_is_ok_without_workspace():
 def test_workspace_size_closed_form():
     up = lambda n: (n + 255) // 256 * 256  # noqa: E731
     lin = lambda rows: up(rows * 512) + up(rows * 16)  # noqa: E731  (fp8 epilogue's linear term)
-    # dense, one sequence: 100 rows x ld(1000)=1024 fp32
+    ld = lambda n: (((n + 63) // 64) | 1) * 64  # noqa: E731  (row stride: an odd multiple of 64 floats)
+    assert ld(1000) == 1088 and ld(1024) == 1088 and ld(1088) == 1088
+    # dense, one sequence: 100 rows x ld(1000)=1088 fp32
     a = args(n_q=100, q_pos0=900)
-    assert pv.pivot_workspace_size(a, pv.PIVOT_DENSE) == lin(100) + 100 * 1024 * 4
+    assert pv.pivot_workspace_size(a, pv.PIVOT_DENSE) == lin(100) + 100 * ld(1000) * 4
     b = args(n_q=100, q_pos0=900, dtype=pv.PIVOT_DT_BF16, scales=False)
-    assert pv.pivot_workspace_size(b, pv.PIVOT_DENSE) == 100 * 1024 * 4
+    assert pv.pivot_workspace_size(b, pv.PIVOT_DENSE) == 100 * ld(1000) * 4
     # Refine, g=4, c=16, guardrail at c: all 25 groups start at t0 >= 900 >= c;
     # members need the linear term (Refine re-scores them), and so do proxies
     ng = 25
     proxies = up(ng * 64 * 128) + up(ng * 4) + up(ng * 64 * 4)
     cand = up(ng * 16 * 4) + up(ng * 4 * 16 * 4)   # candidate sets + members' re-scores
-    assert pv.pivot_workspace_size(a, pv.PIVOT_REFINE, 4, 16) == lin(100) + lin(ng) + proxies + cand + ng * 1024 * 4
+    assert pv.pivot_workspace_size(a, pv.PIVOT_REFINE, 4, 16) == \
+        lin(100) + lin(ng) + proxies + cand + ng * ld(1000) * 4
     # Reuse: no candidate buffer, no member rows to re-score
-    assert pv.pivot_workspace_size(a, pv.PIVOT_REUSE, 4, 16) == lin(ng) + proxies + ng * 1024 * 4
+    assert pv.pivot_workspace_size(a, pv.PIVOT_REUSE, 4, 16) == lin(ng) + proxies + ng * ld(1000) * 4
     # long prefix: score tiles stay near 1 GiB
     a = args(n_q=16384, q_pos0=262144 - 16384)
     assert pv.pivot_workspace_size(a, pv.PIVOT_DENSE) == lin(16384) + (1 << 30)

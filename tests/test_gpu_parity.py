@@ -202,3 +202,21 @@ def test_tied_keys_exact(fmt, L, c, topk, pool, mode):
         checked += 1
     say("tied rows checked", checked, "of", len(rows))
     assert checked >= len(rows) // 2
+
+
+@pytest.fixture(scope="module")
+def long20k_fp8():
+    return make_prefill(20000, "fp8", seed=33, threads=8)
+
+
+@pytest.mark.parametrize("mode", ["dense", "reuse", "refine"])
+def test_many_long_rows(long20k_fp8, mode):
+    """More than 256 rows of 16384+ scores in one select launch: the one-pass
+    select with candidates in the workspace scratch (dense: 2048 rows; proxies:
+    512 rows of g=4)."""
+    x = long20k_fp8
+    p0, n_q = 20000 - 2048, 2048
+    g = 1 if mode == "dense" else 4
+    rng = np.random.default_rng(5)
+    groups = sorted({0, n_q // g - 1} | set(int(v) for v in rng.integers(0, n_q // g, 10)))
+    check(x, mode, p0, n_q, 2048, g=g, c=4096, groups=groups, label=f"20k {mode}")
