@@ -132,23 +132,25 @@ struct RowTile {
   __device__ __forceinline__ float score(const KeyFrag<DT>& b) const {
     float acc = 0.f;
     if constexpr (DT == kFp8) {
-      // Software pipeline: the MFMA of tile j+1 is issued before the epilogue
-      // of tile j, so the matrix core and the VALU work side by side and only
-      // two accumulators are live.  The scheduling barriers keep the compiler
+      // Software pipeline: the MFMA of tile j+2 is issued before the epilogue
+      // of tile j, so the matrix core and the VALU work side by side with
+      // three accumulators live.  The scheduling barriers keep the compiler
       // from hoisting all MFMAs ahead (which would need 4 (T+1) accumulator
       // registers and push operands into AGPRs).
       v4f cl = mfma_fp8(al.v, b.v);
-      v4f c = mfma_fp8(a[0].v, b.v);
+      v4f c0 = mfma_fp8(a[0].v, b.v);
+      v4f c1 = mfma_fp8(a[1].v, b.v);
 #pragma unroll
-      for (int j = 1; j <= T; ++j) {
-        v4f nxt = c;
+      for (int j = 2; j <= T + 1; ++j) {
+        v4f nxt = c1;
         if (j < T) nxt = mfma_fp8(a[j].v, b.v);
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) acc = fmaf(wv[j - 1][i], fabsf(c[i]), acc);
+        for (int i = 0; i < 4; ++i) acc = fmaf(wv[j - 2][i], fabsf(c0[i]), acc);
         asm volatile("" : "+v"(acc));  // pins this epilogue between the barriers
         __builtin_amdgcn_sched_barrier(0);
-        c = nxt;
+        c0 = c1;
+        c1 = nxt;
       }
 #pragma unroll
       for (int i = 0; i < 4; ++i) acc = fmaf(ls[i], cl[i], acc);
