@@ -205,6 +205,72 @@ __device__ void block_select(const Src& src, uint32_t need, SelectShared& sh, Pu
   __syncthreads();
 }
 
+// Fast exact top-`need` of a source whose keys spread over a range of values
+// (a candidate set): one reduction for the key range, one pass over a
+// 4096-bin histogram of the value bucketed linearly over that range (a
+// monotone map), and one pass that emits every element of the buckets above
+// the one holding the need-th element and lists that bucket's members in
+// LDS; each listed member then counts the members ranking above it (key
+// descending, position ascending).  Returns false, having emitted nothing,
+// when the keys are all equal or the bucket holds more than kBucketList
+// elements; the caller then uses block_select().
+// hist: 4096 LDS words; lkey / lpos: kBucketList LDS entries; lcount: an LDS word.
+constexpr int kBucketList = 256;
+
+template <int THREADS, class Src, class Put>
+__device__ bool bucket_select(const Src& src, uint32_t need, uint32_t* hist, uint32_t* lkey, int32_t* lpos,
+                              int32_t* lcount, SelectShared& sh, Put put) {
+  const int tid = threadIdx.x;
+  uint32_t kmin = ~0u, kmax = 0u;
+  src.visit([&](uint32_t key, int32_t) {
+    kmin = min(kmin, key);
+    kmax = max(kmax, key);
+  });
+  block_pair_reduce<THREADS, true>(kmin, kmax, sh);
+  const float fmin = key_float(kmin);
+  const float scale = 4096.0f / (key_float(kmax) - fmin);
+  if (kmin == kmax || !(scale > 0.0f && scale < __builtin_inff())) return false;
+  auto bucket = [&](uint32_t key) { return min(4095, (int)((key_float(key) - fmin) * scale)); };
+  for (int k = tid; k < 4096; k += THREADS) hist[k] = 0;
+  if (tid == 0) *lcount = 0;
+  __syncthreads();
+  src.visit([&](uint32_t key, int32_t) { atomicAdd(&hist[bucket(key)], 1u); });
+  __syncthreads();
+  find_digit<THREADS, true>(hist, sh, need, 4096);
+  const int bsel = (int)sh.digit;
+  const uint32_t rem = need - sh.before, in_b = sh.equal;
+  __syncthreads();
+  if (in_b > (uint32_t)kBucketList) return false;
+  src.visit([&](uint32_t key, int32_t pos) {
+    const int bk = bucket(key);
+    wave_append(bk > bsel, &sh.emitted, [&](int slot) { put(slot, pos); });
+    if (bk == bsel) {
+      const int c = atomicAdd(lcount, 1);
+      lkey[c] = key;
+      lpos[c] = pos;
+    }
+  });
+  __syncthreads();
+  for (int t0 = 0; t0 < (int)in_b; t0 += THREADS) {
+    const int t = t0 + tid;
+    bool take = false;
+    int32_t pos = 0;
+    if (t < (int)in_b) {
+      const uint32_t key = lkey[t];
+      pos = lpos[t];
+      uint32_t rank = 0;
+      for (int u = 0; u < (int)in_b; ++u) {
+        const uint32_t ku = lkey[u];
+        rank += (ku > key) || (ku == key && lpos[u] < pos);
+      }
+      take = rank < rem;
+    }
+    wave_append(take, &sh.emitted, [&](int slot) { put(slot, pos); });
+  }
+  __syncthreads();
+  return true;
+}
+
 // Elements e = tid, tid + THREADS, ... < count of (key[], pos[]) arrays.
 template <int THREADS>
 struct ArraySource {
@@ -229,7 +295,7 @@ struct TwoLevelShared {
   int32_t cpos[CAP];
   SelectShared sel;
   uint32_t b1, above, in_b1;
-  int32_t ncand;
+  int32_t ncand, lcount;
 };
 
 template <int THREADS, int CAP, class Src, class Put>
@@ -256,7 +322,10 @@ __device__ void two_level_select(const Src& src, uint32_t m, TwoLevelShared<CAP>
     });
     __syncthreads();
     ArraySource<THREADS> cand{sh.ckey, sh.cpos, sh.ncand};
-    block_select<THREADS, false>(cand, m - above, sh.sel, put);
+    // the histogram is free again: it serves the bucket pass and its list
+    if (!bucket_select<THREADS>(cand, m - above, hist, hist, reinterpret_cast<int32_t*>(hist + kBucketList),
+                                &sh.lcount, sh.sel, put))
+      block_select<THREADS, false>(cand, m - above, sh.sel, put);
   } else {
     block_select<THREADS, false>(src, m, sh.sel, put);
   }

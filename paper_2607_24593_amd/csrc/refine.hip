@@ -133,6 +133,8 @@ __global__ __launch_bounds__(256) void topk_short_kernel(const float* __restrict
                                                          int n_groups, SeqTable st, int j0, int c, int m,
                                                          int32_t* __restrict__ out_idx) {
   __shared__ SelectShared sel;
+  __shared__ uint32_t hist[4096];
+  __shared__ int32_t lcount;
   const int j = j0 + blockIdx.x, b = blockIdx.y, member = blockIdx.z;
   if (b >= st.n || j >= n_groups || j < st.first_proxy[b]) return;
   const int gs = min(g, n_q - j * g);
@@ -160,7 +162,10 @@ __global__ __launch_bounds__(256) void topk_short_kernel(const float* __restrict
   }
   if (tid == 0) sel.emitted = 0;
   __syncthreads();
-  block_select<256, true>(src, (uint32_t)m, sel, [&](int slot, int32_t p) { orow[slot] = p; });
+  auto put = [&](int slot, int32_t p) { orow[slot] = p; };
+  if (!bucket_select<256>(src, (uint32_t)m, hist, hist, reinterpret_cast<int32_t*>(hist + kBucketList), &lcount, sel,
+                          put))
+    block_select<256, true>(src, (uint32_t)m, sel, put);
 }
 
 hipError_t launch_refine(int dtype, const void* q, const float* q_scale, const float* w, const uint8_t* lin,

@@ -184,7 +184,10 @@ __global__ __launch_bounds__(T) void topk_rows_kernel(const float* __restrict__ 
       __syncthreads();  // every thread has read the count before it is reused
       if (found >= m && found <= CAP) {
         ArraySource<T> cand{sh.ckey, sh.cpos, found};
-        block_select<T, false>(cand, (uint32_t)m, sh.sel, put);
+        // the sample's histogram is free: it serves the bucket pass and its list
+        if (!bucket_select<T>(cand, (uint32_t)m, sh.hist, sh.hist, reinterpret_cast<int32_t*>(sh.hist + kBucketList),
+                              &sh.lcount, sh.sel, put))
+          block_select<T, false>(cand, (uint32_t)m, sh.sel, put);
         return;
       }
     }
