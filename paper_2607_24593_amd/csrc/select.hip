@@ -69,6 +69,26 @@ struct RowSource {
       for (int e = tid; e < count; e += T) f(float_key(row[e]), e);
     }
   }
+  // the same walk (aligned rows only) handing over the raw scores
+  template <class F>
+  __device__ __forceinline__ void visit_raw(F f) const {
+    const int tid = threadIdx.x;
+    const int n4 = count >> 2;
+    const float4* r4 = reinterpret_cast<const float4*>(row);
+    auto each = [&](const float4& a, int i) {
+      f(a.x, 4 * i); f(a.y, 4 * i + 1); f(a.z, 4 * i + 2); f(a.w, 4 * i + 3);
+    };
+    int i = tid;
+    for (; i + (U - 1) * T < n4; i += U * T) {
+      float4 a[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) a[u] = r4[i + u * T];
+#pragma unroll
+      for (int u = 0; u < U; ++u) each(a[u], i + u * T);
+    }
+    for (; i < n4; i += T) each(r4[i], i);
+    for (int e = 4 * n4 + tid; e < count; e += T) f(row[e], e);
+  }
 };
 
 // The sampled keys (positions are not needed): V float4 per thread.
@@ -170,11 +190,14 @@ __global__ __launch_bounds__(T) void topk_rows_kernel(const float* __restrict__ 
       const uint32_t thr = sample_prefix<T>(smp, ts, sh.hist, sh.sel);
       if (tid == 0) sh.ncand = 0;
       __syncthreads();
-      src.visit([&](uint32_t key, int32_t pos) {
-        if ((key >> 12) >= thr) {  // a few percent of the row: plain LDS atomics
+      // key >> 12 >= thr  <=>  score >= the smallest score with that prefix
+      // (the key map is monotone; -0 and +0 share a key and compare equal)
+      const float fthr = key_float(thr << 12);
+      src.visit_raw([&](float v, int32_t pos) {
+        if (v >= fthr) {  // a few percent of the row: plain LDS atomics
           const int c = atomicAdd(&sh.ncand, 1);
           if (c < CAP) {
-            sh.ckey[c] = key;
+            sh.ckey[c] = float_key(v);
             sh.cpos[c] = pos;
           }
         }
