@@ -21,6 +21,8 @@ _LIB = os.environ.get("PIVOT_ORACLE_LIB") or os.path.join(_HERE, "libpivot_oracl
 
 DENSE, REUSE, REFINE = 0, 1, 2
 FMT = {"bf16": 0, "fp8": 1}
+WINDOW_SHARED, WINDOW_PER_QUERY = 0, 1     # App. B: prefill and decode readings
+AGG_MEAN, AGG_FIRST, AGG_LAST = 0, 1, 2    # Eq. 4 mean, or one member's row
 
 
 def compile_source(src: str, out: str) -> str:
@@ -66,6 +68,8 @@ def lib():
         L.oracle_refine_on.argtypes = [I, I, I, P, P, P, I, P, P, P, I64, I, P]
         L.oracle_index.argtypes = [I, I, I, P, P, P, I, I64, P, P, I64,
                                    I, I, I, I, I, P, I, P, P, P, P, P]
+        L.oracle_index_ex.argtypes = [I, I, I, P, P, P, I, I64, P, P, I64,
+                                      I, I, I, I, I, I, I, I, P, I, P, P, P, P, P]
         L.oracle_num_threads.restype = I
         _lib = L
     return _lib
@@ -169,15 +173,23 @@ def refine_on(fmt: str, q, q_scale, w, k, k_scale, cand, m: int) -> np.ndarray:
     return out
 
 
+def cand_width(c: int, g: int, window: int = 0, window_kind: int = WINDOW_SHARED) -> int:
+    """Candidate slots per group: c, or c + W + g - 1 with the decode window."""
+    return c + window + g - 1 if (window > 0 and window_kind == WINDOW_PER_QUERY) else c
+
+
 def index(fmt: str, q, q_scale, w, p0: int, k, k_scale, n_k: int, *, mode: int, g: int = 1,
           c: int = 0, topk: int, dense_below: int | None = None, groups=None,
-          want_cand: bool = False, want_proxy: bool = False):
+          want_cand: bool = False, want_proxy: bool = False, window: int = 0,
+          window_kind: int = WINDOW_SHARED, agg: int = AGG_MEAN):
     """Algorithm 1 over one sequence's queries q [n_q,H,d] at positions p0.. .
 
     mode DENSE / REUSE / REFINE.  dense_below defaults to c (the guardrail of
-    Algorithm 1); 0 disables it.  groups: optional list of group indices to
-    compute (rows of other groups are returned as -2).  Returns a dict with
-    'idx' [n_q, topk] and, if asked, 'cand' [n_groups, c] and the proxies."""
+    Algorithm 1); 0 disables it.  window / window_kind: App. B's local window
+    (Refine only).  agg: proxy aggregation.  groups: optional list of group
+    indices to compute (rows of other groups are returned as -2).  Returns a
+    dict with 'idx' [n_q, topk] and, if asked, 'cand' [n_groups, width] and the
+    proxies."""
     q = _c(q, _code_dtype(fmt))
     n_q, H, d = q.shape
     qs = _c(q_scale, np.float32) if fmt == "fp8" else None
@@ -191,14 +203,15 @@ def index(fmt: str, q, q_scale, w, p0: int, k, k_scale, n_k: int, *, mode: int, 
     n_groups = (n_q + g - 1) // g
     sel = None if groups is None else np.ascontiguousarray(groups, dtype=np.int32)
     out = np.full((n_q, topk), -2, dtype=np.int32)
-    cand = np.full((n_groups, c), -2, dtype=np.int32) if (want_cand and mode == REFINE) else None
+    width = cand_width(c, g, window, window_kind)
+    cand = np.full((n_groups, width), -2, dtype=np.int32) if (want_cand and mode == REFINE) else None
     pq = np.zeros((n_groups, H, d), dtype=_code_dtype(fmt)) if want_proxy else None
     psc = np.zeros(n_groups, dtype=np.float32) if want_proxy else None
     pw = np.zeros((n_groups, H), dtype=np.float32) if want_proxy else None
-    rc = lib().oracle_index(FMT[fmt], H, d, _p(q), _p(qs), _p(w), n_q, int(p0), _p(k), _p(ks),
-                            int(n_k), mode, g, c, topk, dense_below,
-                            _p(sel), 0 if sel is None else len(sel),
-                            _p(out), _p(cand), _p(pq), _p(psc), _p(pw))
+    rc = lib().oracle_index_ex(FMT[fmt], H, d, _p(q), _p(qs), _p(w), n_q, int(p0), _p(k), _p(ks),
+                               int(n_k), mode, g, c, topk, dense_below, int(window), int(window_kind),
+                               int(agg), _p(sel), 0 if sel is None else len(sel),
+                               _p(out), _p(cand), _p(pq), _p(psc), _p(pw))
     if rc != 0:
         raise ValueError("oracle_index rejected its arguments")
     res = {"idx": out}

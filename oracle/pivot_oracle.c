@@ -18,6 +18,8 @@
  *     per-query selection:                Sec. 4.4 Eqs. (7), (8), (9)
  *   - short-group guardrail and the
  *     overall order of the steps:         App. E, Algorithm 1
+ *   - local window W (prefill / decode):  App. B
+ *   - first / last member as the proxy:   Sec. 5.4 (query aggregation ablation)
  *
  * Readings where the paper is silent (the same list is kept with the design
  * notes of the repository):
@@ -31,7 +33,19 @@
  *     format: bf16 by RNE, or fp8 E4M3FN with scale amax/448 and RNE codes
  *     saturated to +-448;
  *   - the guardrail of Algorithm 1 (t0 < c -> dense) applies to both variants;
- *     `dense_below` carries its threshold (callers pass c, or 0 to disable).
+ *     `dense_below` carries its threshold (callers pass c, or 0 to disable);
+ *   - local window (Refine only; W = 0 is the plain candidate set):
+ *       prefill ("shared"): the union of the members' windows is the w_g =
+ *         W + g - 1 positions t0-W+1 .. t0+g-1; the proxy fills the other
+ *         c - w_g slots with its top over [0, t0-W] (the positions before the
+ *         union); union positions below 0 or past the group's last member are
+ *         empty (-1);
+ *       decode ("per query"): the pool is the proxy's top-c over [0, t0]; the
+ *         union t0-W+1 .. t0+g-1 follows it (c + W + g - 1 slots), with
+ *         positions already in the pool emptied; W >= g;
+ *       member t re-scores the slots it may use: position <= t, and, for a
+ *         union slot of the per-query kind, position >= t - W + 1;
+ *   - first / last aggregation: the proxy is that member's row, unchanged.
  *
  * Floating point: every score is accumulated in double.  For fp8 inputs the
  * inner products are exact in double (codes are multiples of 2^-9 with
@@ -198,13 +212,16 @@ static void dense_row(const keyset* K, const void* q_row, double sq, const float
 
 /* Eq. (4): the group's proxy query.  Members are rows [0, gs) of q / w /
  * q_scale.  Writes the proxy codes (H*d), its scale and its H gates. */
-static void proxy_of(int fmt, int H, int d, const void* q, const float* q_scale,
-                     const float* w, int gs, void* pq, float* psc, float* pw) {
+enum { OR_AGG_MEAN = 0, OR_AGG_FIRST = 1, OR_AGG_LAST = 2 };
+
+static void proxy_of_agg(int fmt, int H, int d, const void* q, const float* q_scale,
+                         const float* w, int gs, int agg, void* pq, float* psc, float* pw) {
     size_t n = (size_t)H * d, b = fmt == OR_FP8 ? 1 : 2;
-    if (gs == 1) {                       /* a group of one is its own proxy */
-        memcpy(pq, q, n * b);
-        *psc = (fmt == OR_FP8) ? q_scale[0] : 1.0f;
-        memcpy(pw, w, sizeof(float) * (size_t)H);
+    if (gs == 1 || agg != OR_AGG_MEAN) { /* a group of one is its own proxy; first / last member */
+        int t = (agg == OR_AGG_LAST) ? gs - 1 : 0;
+        memcpy(pq, (const char*)q + (size_t)t * n * b, n * b);
+        *psc = (fmt == OR_FP8) ? q_scale[t] : 1.0f;
+        memcpy(pw, w + (size_t)t * H, sizeof(float) * (size_t)H);
         return;
     }
     float* mean = (float*)malloc(sizeof(float) * n);
@@ -235,6 +252,11 @@ static void proxy_of(int fmt, int H, int d, const void* q, const float* q_scale,
         *psc = sigma;
     }
     free(mean);
+}
+
+static void proxy_of(int fmt, int H, int d, const void* q, const float* q_scale,
+                     const float* w, int gs, void* pq, float* psc, float* pw) {
+    proxy_of_agg(fmt, H, d, q, q_scale, w, gs, OR_AGG_MEAN, pq, psc, pw);
 }
 
 int oracle_proxy(int fmt, int H, int d, const void* q, const float* q_scale, const float* w,
@@ -294,25 +316,38 @@ int oracle_refine_on(int fmt, int H, int d, const void* q, const float* q_scale,
  * keys are positions 0 .. n_k-1.  Groups are runs of g rows starting at the
  * first row (Eq. (2)); a decode call passes its g MTP queries as one run
  * (Eq. (3)).  mode: 0 dense (every row: TopK over [0, t]), 1 Reuse, 2 Refine.
+ * window / window_kind / agg: App. B's local window (0 = none; kind 0 the
+ * prefill reading, 1 the decode reading) and the proxy aggregation (0 mean,
+ * 1 first member, 2 last member), as read in the header.
  *
  * sel / n_sel: optional list of group indices to compute (others are left
  * untouched); NULL computes every group.  out_idx [n_q, topk]; out_cand
- * [n_groups, c] (Refine only, optional; -1 for guardrail groups);
- * out_pq / out_psc / out_pw: optional proxies [n_groups, H*d] / [n_groups] /
- * [n_groups, H] (left untouched for guardrail groups).
+ * [n_groups, width] (Refine only, optional; -1 for guardrail groups), width =
+ * c, or c + W + g - 1 for the decode window; out_pq / out_psc / out_pw:
+ * optional proxies [n_groups, H*d] / [n_groups] / [n_groups, H] (left
+ * untouched for guardrail groups).
  */
-int oracle_index(int fmt, int H, int d,
-                 const void* q, const float* q_scale, const float* w, int n_q, int64_t p0,
-                 const void* k, const float* k_scale, int64_t n_k,
-                 int mode, int g, int c, int m, int dense_below,
-                 const int32_t* sel, int n_sel,
-                 int32_t* out_idx, int32_t* out_cand,
-                 void* out_pq, float* out_psc, float* out_pw) {
+int oracle_index_ex(int fmt, int H, int d,
+                    const void* q, const float* q_scale, const float* w, int n_q, int64_t p0,
+                    const void* k, const float* k_scale, int64_t n_k,
+                    int mode, int g, int c, int m, int dense_below,
+                    int window, int window_kind, int agg,
+                    const int32_t* sel, int n_sel,
+                    int32_t* out_idx, int32_t* out_cand,
+                    void* out_pq, float* out_psc, float* out_pw) {
     build_codecs();
     if (H < 1 || d < 1 || n_q < 0 || m < 1 || g < 1) return 1;
     if (p0 < 0 || p0 + n_q > n_k) return 1;
-    if (mode == OR_REFINE && c < m) return 1;
     if (fmt == OR_FP8 && (!q_scale || !k_scale)) return 1;
+    if (window < 0 || (window > 0 && mode != OR_REFINE)) return 1;
+    if (window_kind != 0 && window_kind != 1) return 1;
+    if (agg < OR_AGG_MEAN || agg > OR_AGG_LAST) return 1;
+    const int W = window;
+    const int wg = W > 0 ? W + g - 1 : 0;                   /* the union's slots */
+    if (W > 0 && window_kind == 0 && c < wg) return 1;
+    if (W > 0 && window_kind == 1 && W < g) return 1;
+    const int width = (W > 0 && window_kind == 1) ? c + wg : c;   /* candidate slots */
+    if (mode == OR_REFINE && width < m) return 1;
     keyset K = {fmt, H, d, k, fmt == OR_FP8 ? k_scale : NULL};
     size_t b = fmt == OR_FP8 ? 1 : 2;
     size_t rowb = (size_t)H * d * b;
@@ -329,27 +364,29 @@ int oracle_index(int fmt, int H, int d,
         int64_t t0 = p0 + r0;
         const char* qg = (const char*)q + (size_t)r0 * rowb;
         const float* sg = fmt == OR_FP8 ? q_scale + r0 : NULL;
-        const float* wg = w + (size_t)r0 * H;
+        const float* wg_ = w + (size_t)r0 * H;
         int32_t* og = out_idx + (size_t)r0 * m;
 
         if (mode == OR_DENSE || t0 < dense_below) {          /* dense, or guardrail */
             for (int t = 0; t < gs; ++t)
-                dense_row(&K, qg + (size_t)t * rowb, sg ? (double)sg[t] : 1.0, wg + (size_t)t * H,
+                dense_row(&K, qg + (size_t)t * rowb, sg ? (double)sg[t] : 1.0, wg_ + (size_t)t * H,
                           t0 + t, m, og + (size_t)t * m);
             if (mode == OR_REFINE && out_cand)
-                for (int i = 0; i < c; ++i) out_cand[(size_t)grp * c + i] = -1;
+                for (int i = 0; i < width; ++i) out_cand[(size_t)grp * width + i] = -1;
             continue;
         }
 
         float psc;                                                   /* Eq. (4) */
-        proxy_of(fmt, H, d, qg, sg, wg, gs, pq, &psc, pw);
+        proxy_of_agg(fmt, H, d, qg, sg, wg_, gs, agg, pq, &psc, pw);
         if (out_pq) memcpy((char*)out_pq + (size_t)grp * rowb, pq, rowb);
         if (out_psc) out_psc[grp] = psc;
         if (out_pw) memcpy(out_pw + (size_t)grp * H, pw, sizeof(float) * (size_t)H);
 
-        int64_t n = t0 + 1;                                          /* Eq. (5) */
-        int32_t* pos = (int32_t*)malloc(sizeof(int32_t) * (size_t)n);
-        double* f = (double*)malloc(sizeof(double) * (size_t)n);
+        /* Eq. (5), over [0, t0] (or [0, t0-W] before a prefill window) */
+        int64_t lim = (W > 0 && window_kind == 0) ? t0 - W : t0;
+        int64_t n = lim + 1 > 0 ? lim + 1 : 0;
+        int32_t* pos = (int32_t*)malloc(sizeof(int32_t) * (size_t)(n > 0 ? n : 1));
+        double* f = (double*)malloc(sizeof(double) * (size_t)(n > 0 ? n : 1));
         for (int64_t s = 0; s < n; ++s) pos[s] = (int32_t)s;
         score_positions(&K, pq, fmt == OR_FP8 ? (double)psc : 1.0, pw, pos, n, f);
 
@@ -357,16 +394,35 @@ int oracle_index(int fmt, int H, int d,
             topk(f, pos, n, m, og);
             for (int t = 1; t < gs; ++t) memcpy(og + (size_t)t * m, og, sizeof(int32_t) * (size_t)m);
         } else {                                                     /* Eqs. (7)-(9) */
-            int32_t* cand = (int32_t*)malloc(sizeof(int32_t) * (size_t)c);
-            int nc = topk(f, pos, n, c, cand);
-            if (out_cand) memcpy(out_cand + (size_t)grp * c, cand, sizeof(int32_t) * (size_t)c);
-            double* fc = (double*)malloc(sizeof(double) * (size_t)(nc > 0 ? nc : 1));
+            int32_t* cand = (int32_t*)malloc(sizeof(int32_t) * (size_t)width);
+            int proxy_slots = (W > 0 && window_kind == 0) ? c - wg : c;
+            if (proxy_slots > 0) topk(f, pos, n, proxy_slots, cand);
+            for (int u = 0; u < wg; ++u) {                           /* App. B window union */
+                int64_t p = t0 - W + 1 + u;
+                int ok = p >= 0 && p <= t0 + gs - 1;
+                if (ok && window_kind == 1)                          /* decode: not twice */
+                    for (int i = 0; i < c; ++i)
+                        if (cand[i] == (int32_t)p) { ok = 0; break; }
+                cand[proxy_slots + u] = ok ? (int32_t)p : -1;
+            }
+            if (out_cand) memcpy(out_cand + (size_t)grp * width, cand, sizeof(int32_t) * (size_t)width);
+            int32_t* use = (int32_t*)malloc(sizeof(int32_t) * (size_t)width);
+            double* fc = (double*)malloc(sizeof(double) * (size_t)width);
             for (int t = 0; t < gs; ++t) {
+                int64_t tt = t0 + t;
+                int nu = 0;
+                for (int i = 0; i < width; ++i) {
+                    int32_t p = cand[i];
+                    if (p < 0 || p > tt) continue;
+                    if (W > 0 && window_kind == 1 && i >= c && p < tt - W + 1) continue;
+                    use[nu++] = p;
+                }
                 score_positions(&K, qg + (size_t)t * rowb, sg ? (double)sg[t] : 1.0,
-                                wg + (size_t)t * H, cand, nc, fc);
-                topk(fc, cand, nc, m, og + (size_t)t * m);
+                                wg_ + (size_t)t * H, use, nu, fc);
+                topk(fc, use, nu, m, og + (size_t)t * m);
             }
             free(fc);
+            free(use);
             free(cand);
         }
         free(pos);
@@ -375,6 +431,17 @@ int oracle_index(int fmt, int H, int d,
     free(pq);
     free(pw);
     return 0;
+}
+
+int oracle_index(int fmt, int H, int d,
+                 const void* q, const float* q_scale, const float* w, int n_q, int64_t p0,
+                 const void* k, const float* k_scale, int64_t n_k,
+                 int mode, int g, int c, int m, int dense_below,
+                 const int32_t* sel, int n_sel,
+                 int32_t* out_idx, int32_t* out_cand,
+                 void* out_pq, float* out_psc, float* out_pw) {
+    return oracle_index_ex(fmt, H, d, q, q_scale, w, n_q, p0, k, k_scale, n_k, mode, g, c, m, dense_below,
+                           0, 0, OR_AGG_MEAN, sel, n_sel, out_idx, out_cand, out_pq, out_psc, out_pw);
 }
 
 int oracle_num_threads(void) {

@@ -29,14 +29,23 @@ MUTANTS = {
     "proxy gate sums instead of averaging (Eq. 4)": ("pw[j] = sum / count;", "pw[j] = sum;"),
     "fp8 ties round up": ("((lo & 1) ? hi : lo)", "hi"),
     "bf16 ties round up": ("(rest == 0x8000u && (keep & 1u))", "(rest == 0x8000u)"),
-    "proxy scan past t0 (Eq. 5)": ("int64_t n = t0 + 1;                                          /* Eq. (5) */",
-                                   "int64_t n = t0 + gs;"),
+    "proxy scan past t0 (Eq. 5)": ("int64_t lim = (W > 0 && window_kind == 0) ? t0 - W : t0;",
+                                   "int64_t lim = (W > 0 && window_kind == 0) ? t0 - W : t0 + gs - 1;"),
     "guardrail inverted (Alg. 1)": ("if (mode == OR_DENSE || t0 < dense_below)", "if (mode == OR_DENSE || t0 >= dense_below)"),
     "guardrail off (Alg. 1)": ("if (mode == OR_DENSE || t0 < dense_below)", "if (mode == OR_DENSE)"),
     "reuse not shared (Eq. 6)": ("for (int t = 1; t < gs; ++t) memcpy(og + (size_t)t * m, og, sizeof(int32_t) * (size_t)m);", ""),
-    "candidate budget k instead of c (Eq. 7)": ("int nc = topk(f, pos, n, c, cand);", "int nc = topk(f, pos, n, m, cand);"),
-    "refine re-scores with the proxy (Eq. 8)": ("score_positions(&K, qg + (size_t)t * rowb, sg ? (double)sg[t] : 1.0,\n                                wg + (size_t)t * H, cand, nc, fc);",
-                                                "score_positions(&K, pq, fmt == OR_FP8 ? (double)psc : 1.0, pw, cand, nc, fc);"),
+    "candidate budget k instead of c (Eq. 7)": ("int proxy_slots = (W > 0 && window_kind == 0) ? c - wg : c;",
+                                                "int proxy_slots = (W > 0 && window_kind == 0) ? c - wg : m;"),
+    "refine re-scores with the proxy (Eq. 8)": ("score_positions(&K, qg + (size_t)t * rowb, sg ? (double)sg[t] : 1.0,\n                                wg_ + (size_t)t * H, use, nu, fc);",
+                                                "score_positions(&K, pq, fmt == OR_FP8 ? (double)psc : 1.0, pw, use, nu, fc);"),
+    "window union starts one late (App. B)": ("int64_t p = t0 - W + 1 + u;", "int64_t p = t0 - W + 2 + u;"),
+    "prefill proxy part overlaps the window (App. B)": ("int64_t lim = (W > 0 && window_kind == 0) ? t0 - W : t0;",
+                                                        "int64_t lim = t0;"),
+    "window slots past the member kept (causality)": ("if (p < 0 || p > tt) continue;", "if (p < 0) continue;"),
+    "decode window not per query (App. B)": ("if (W > 0 && window_kind == 1 && i >= c && p < tt - W + 1) continue;", ""),
+    "decode pool duplicates kept (App. B)": ("if (cand[i] == (int32_t)p) { ok = 0; break; }", "if (cand[i] == (int32_t)p) { break; }"),
+    "window reserves W slots, not W + g - 1 (App. B)": ("const int wg = W > 0 ? W + g - 1 : 0;", "const int wg = W;"),
+    "first and last member swapped": ("int t = (agg == OR_AGG_LAST) ? gs - 1 : 0;", "int t = (agg == OR_AGG_FIRST) ? gs - 1 : 0;"),
     "proxy scale from amax/240": ("amax / 448.0f", "amax / 240.0f"),
 }
 

@@ -375,3 +375,176 @@ def test_group_count_and_ragged_tail():
     chunked = np.concatenate([run(x, oracle.REUSE, g=4, c=8, topk=5, p0=p, n_q=min(16, 45 - p))["idx"]
                               for p in range(0, 45, 16)])
     assert np.array_equal(chunked, r)                         # chunks of a multiple of g
+
+
+# ------------------------------------------------ App. B window, aggregation
+def _topk_brute(f, pos, m):
+    order = sorted(range(len(pos)), key=lambda i: (-f[i], pos[i]))[:m]
+    return sorted(int(pos[i]) for i in order)
+
+
+def _scores(x, t, pos):
+    return oracle.scores_at(x.dtype, x.q[t], 1.0 if x.q_scale is None else x.q_scale[t], x.w[t], x.k, x.k_scale,
+                            np.asarray(pos, dtype=np.int32))
+
+
+@pytest.mark.parametrize("fmt", ["bf16", "fp8"])
+@pytest.mark.parametrize("W", [1, 3, 6])
+def test_prefill_window_with_full_budget_is_dense(fmt, W):
+    """App. B: with the window, a candidate budget that covers the sequence
+    makes Refine equal dense for every member, guardrail off (without the
+    window the later members of a group could not reach (t0, t])."""
+    x = small(fmt, L=48)
+    g, m = 4, 6
+    dense = run(x, oracle.DENSE, topk=m)["idx"]
+    r = run(x, oracle.REFINE, g=g, c=48 + g, topk=m, dense_below=0, window=W)["idx"]
+    assert np.array_equal(np.sort(r, 1), np.sort(dense, 1))
+    plain = run(x, oracle.REFINE, g=g, c=48 + g, topk=m, dense_below=0)["idx"]
+    assert not np.array_equal(np.sort(plain, 1), np.sort(dense, 1))
+
+
+@pytest.mark.parametrize("fmt", ["bf16", "fp8"])
+@pytest.mark.parametrize("W,g", [(2, 4), (4, 4), (5, 2), (4, 3)])
+def test_prefill_window_brute_force(fmt, W, g):
+    """App. B prefill, restated in Python: C = (proxy top-(c - w_g) over
+    [0, t0 - W]) followed by the window union t0-W+1 .. t0+g-1 (w_g = W+g-1
+    slots, -1 where no member reaches); member t re-scores C within [0, t]."""
+    x = small(fmt, L=70)
+    c, m = 20, 5
+    res = run(x, oracle.REFINE, g=g, c=c, topk=m, dense_below=0, window=W, want_cand=True, want_proxy=True)
+    wg = W + g - 1
+    L = 70
+    for j in range((L + g - 1) // g):
+        t0, gs = j * g, min(g, L - j * g)
+        fp = oracle.scores_at(x.dtype, res["pq"][j], res["psc"][j], res["pw"][j], x.k, x.k_scale,
+                              np.arange(max(0, t0 - W + 1), dtype=np.int32))
+        proxy = _topk_brute(fp, list(range(max(0, t0 - W + 1))), c - wg)
+        proxy = proxy if len(proxy) == c - wg else proxy + [-1] * (c - wg - len(proxy))
+        union = [p if 0 <= p <= t0 + gs - 1 else -1 for p in range(t0 - W + 1, t0 - W + 1 + wg)]
+        cand = res["cand"][j]
+        assert sorted(cand[:c - wg].tolist()) == sorted(proxy), j
+        assert cand[c - wg:].tolist() == union, j
+        for t in range(t0, t0 + gs):
+            use = [int(p) for p in cand if 0 <= p <= t]
+            exp = _topk_brute(_scores(x, t, use), use, m)
+            got = sorted(v for v in res["idx"][t].tolist() if v >= 0)
+            assert got == exp, (j, t)
+            assert set(range(max(0, t - W + 1), t + 1)) <= set(use)   # its own window is in reach
+
+
+@pytest.mark.parametrize("fmt", ["bf16", "fp8"])
+@pytest.mark.parametrize("W,g", [(2, 2), (4, 2), (5, 3)])
+def test_decode_window_brute_force(fmt, W, g):
+    """App. B decode: the pool is the proxy top-c over [0, t0]; each query adds
+    its own window [t-W+1, t] (duplicates removed); W >= g."""
+    x = small(fmt, L=60)
+    c, m = 12, 5
+    p0 = 60 - g
+    res = run(x, oracle.REFINE, g=g, c=c, topk=m, dense_below=0, window=W, window_kind=oracle.WINDOW_PER_QUERY,
+              want_cand=True, want_proxy=True, p0=p0, n_q=g)
+    cand = res["cand"][0]
+    assert len(cand) == c + W + g - 1
+    fp = oracle.scores_at(x.dtype, res["pq"][0], res["psc"][0], res["pw"][0], x.k, x.k_scale,
+                          np.arange(p0 + 1, dtype=np.int32))
+    pool = _topk_brute(fp, list(range(p0 + 1)), c)
+    assert sorted(cand[:c].tolist()) == pool
+    valid = cand[cand >= 0]
+    assert len(set(valid.tolist())) == len(valid)                     # no position twice
+    for i in range(g):
+        t = p0 + i
+        use = sorted(set(pool) | set(range(max(0, t - W + 1), t + 1)))
+        exp = _topk_brute(_scores(x, t, use), use, m)
+        assert sorted(v for v in res["idx"][i].tolist() if v >= 0) == exp, t
+
+
+@pytest.mark.parametrize("fmt", ["bf16", "fp8"])
+def test_window_zero_is_the_plain_candidate_set(fmt):
+    x = small(fmt, L=64)
+    for kind in (oracle.WINDOW_SHARED, oracle.WINDOW_PER_QUERY):
+        a = run(x, oracle.REFINE, g=4, c=20, topk=6, window=0, window_kind=kind, want_cand=True)
+        b = run(x, oracle.REFINE, g=4, c=20, topk=6, want_cand=True)
+        assert np.array_equal(a["idx"], b["idx"]) and np.array_equal(a["cand"], b["cand"])
+
+
+def test_window_argument_checks():
+    x = small("fp8", L=32)
+    with pytest.raises(ValueError):                    # Reuse has no refine step
+        run(x, oracle.REUSE, g=4, c=16, topk=4, window=2)
+    with pytest.raises(ValueError):                    # decode needs W >= g
+        run(x, oracle.REFINE, g=4, c=16, topk=4, window=3, window_kind=oracle.WINDOW_PER_QUERY)
+    with pytest.raises(ValueError):                    # prefill needs c >= W + g - 1
+        run(x, oracle.REFINE, g=4, c=6, topk=4, window=4)
+
+
+@pytest.mark.parametrize("fmt", ["bf16", "fp8"])
+def test_first_and_last_member_aggregation(fmt):
+    """The endpoint proxies of the aggregation ablation (Sec. 5.4): the proxy is
+    that member's row unchanged, so Reuse hands every member the top-k of the
+    first (last) member's own scores over [0, t0]."""
+    x = small(fmt, L=50)
+    g, m = 4, 5
+    for agg, pick in ((oracle.AGG_FIRST, lambda t0, gs: t0), (oracle.AGG_LAST, lambda t0, gs: t0 + gs - 1)):
+        res = run(x, oracle.REUSE, g=g, c=8, topk=m, dense_below=0, agg=agg, want_proxy=True)
+        for j in range((50 + g - 1) // g):
+            t0, gs = j * g, min(g, 50 - j * g)
+            src = pick(t0, gs)
+            assert np.array_equal(res["pq"][j], x.q[src]) and np.array_equal(res["pw"][j], x.w[src])
+            exp = _topk_brute(_scores(x, src, list(range(t0 + 1))), list(range(t0 + 1)), m)
+            for t in range(t0, t0 + gs):
+                assert sorted(v for v in res["idx"][t].tolist() if v >= 0) == exp, (agg, t)
+
+
+def _decode_case(fmt, g, W, copies):
+    """A decode sequence of 60 keys whose key rows at the given positions are
+    replaced by copies of chosen rows (so their scores tie with those rows)."""
+    x = small(fmt, L=60)
+    p0 = 60 - g
+    pre = run(x, oracle.REFINE, g=g, c=4, topk=2, dense_below=0, want_proxy=True, p0=p0, n_q=g)
+    fp = oracle.scores_at(x.dtype, pre["pq"][0], pre["psc"][0], pre["pw"][0], x.k, x.k_scale,
+                          np.arange(p0 + 1, dtype=np.int32))
+    order = [int(s) for s in np.argsort(-fp, kind="stable")]
+    for dst, rank in copies:
+        x.k[dst] = x.k[order[rank]]
+        if x.k_scale is not None:
+            x.k_scale[dst] = x.k_scale[order[rank]]
+    return x, p0
+
+
+@pytest.mark.parametrize("fmt", ["bf16", "fp8"])
+def test_decode_window_removes_pool_duplicates(fmt):
+    """The window's positions up to t0 carry the proxy's best key, so the pool
+    holds them; the window part must not list them again."""
+    g, W, c, m = 2, 4, 12, 6
+    p0 = 60 - g
+    x, p0 = _decode_case(fmt, g, W, [(p, 0) for p in range(p0 - W + 1, p0 + 1)])
+    res = run(x, oracle.REFINE, g=g, c=c, topk=m, dense_below=0, window=W, window_kind=oracle.WINDOW_PER_QUERY,
+              want_cand=True, p0=p0, n_q=g)
+    cand = res["cand"][0]
+    assert set(range(p0 - W + 1, p0 + 1)) <= set(cand[:c].tolist())      # the pool holds them
+    valid = cand[cand >= 0]
+    assert len(set(valid.tolist())) == len(valid)
+    for i in range(g):
+        row = res["idx"][i][res["idx"][i] >= 0]
+        assert len(set(row.tolist())) == len(row)
+
+
+@pytest.mark.parametrize("fmt", ["bf16", "fp8"])
+def test_decode_window_is_per_query(fmt):
+    """Two early positions carry the proxy's best key (the pool, c = 2); every
+    window position carries its second best.  The last query may not use the
+    union positions older than its own window, which would otherwise win the
+    ties by lower position."""
+    g, W, c, m = 3, 4, 2, 5
+    p0 = 60 - g
+    union = list(range(p0 - W + 1, p0 + g))
+    x, p0 = _decode_case(fmt, g, W, [(5, 0), (6, 0)] + [(p, 1) for p in union])
+    res = run(x, oracle.REFINE, g=g, c=c, topk=m, dense_below=0, window=W, window_kind=oracle.WINDOW_PER_QUERY,
+              want_cand=True, p0=p0, n_q=g)
+    pool = sorted(res["cand"][0][:c].tolist())
+    assert pool == [5, 6]
+    t = p0 + g - 1
+    use = sorted(set(pool) | set(range(t - W + 1, t + 1)))
+    exp = _topk_brute(_scores(x, g - 1 + p0, use), use, m)
+    got = sorted(v for v in res["idx"][g - 1].tolist() if v >= 0)
+    assert got == exp
+    assert not set(got) & set(range(p0 - W + 1, t - W + 1))
