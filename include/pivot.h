@@ -140,6 +140,57 @@ pivot_status pivot_dense_index(const pivot_args* a);
 pivot_status pivot_group_index(const pivot_args* a, int32_t mode, int32_t g, int32_t c,
                                int32_t dense_below, int32_t* out_cand);
 
+/* App. B's local window: how the window is added to the candidate set. */
+typedef enum {
+  PIVOT_WINDOW_SHARED = 0,    /* prefill: one set per group holds the window union */
+  PIVOT_WINDOW_PER_QUERY = 1  /* decode: each query adds its own window to the pool */
+} pivot_window_kind;
+
+/* How a group is collapsed into its proxy query. */
+typedef enum {
+  PIVOT_AGG_MEAN = 0,   /* the per-head mean of Eq. 4 */
+  PIVOT_AGG_FIRST = 1,  /* the group's first member, unchanged */
+  PIVOT_AGG_LAST = 2    /* the group's last member, unchanged */
+} pivot_aggregate;
+
+typedef struct {
+  int32_t mode;         /* PIVOT_REUSE or PIVOT_REFINE */
+  int32_t g, c;         /* group size, candidate budget (as pivot_group_index) */
+  int32_t dense_below;  /* guardrail threshold (as pivot_group_index) */
+  int32_t window;       /* W >= 0, Refine only; 0 = no window */
+  int32_t window_kind;  /* pivot_window_kind */
+  int32_t aggregate;    /* pivot_aggregate */
+  int32_t* out_cand;    /* optional dev int32 [B, ceil(n_q/g), pivot_cand_width()] */
+} pivot_group_opts;
+
+/*
+ * PIVOT with the options of App. B and of the aggregation ablation (Sec. 5.4);
+ * opts {mode, g, c, dense_below, 0, 0, PIVOT_AGG_MEAN, out_cand} is exactly
+ * pivot_group_index.  With window W > 0 (Refine only), for a group with first
+ * position t0 and gs members:
+ *   - PIVOT_WINDOW_SHARED (prefill): the union of the members' windows,
+ *     positions t0-W+1 .. t0+g-1, takes w = W+g-1 of the c candidate slots
+ *     (slots for positions below 0 or past the last member hold -1); the
+ *     proxy fills the other c - w slots with its top over [0, t0-W].  Needs
+ *     c >= W + g - 1.
+ *   - PIVOT_WINDOW_PER_QUERY (decode): the proxy's top-c over [0, t0] is the
+ *     pool; the union follows it in W+g-1 more slots, with positions already
+ *     in the pool replaced by -1.  Needs W >= g.
+ *   Member t re-scores the candidates at positions <= t (and, for a union
+ *   slot of the per-query kind, >= t-W+1) and keeps its top-k; fewer valid
+ *   candidates than k are padded with -1.
+ * Requirements as pivot_group_index, with topk <= pivot_cand_width() <= 8192;
+ * other values return PIVOT_ERR_INVALID_ARG (PIVOT_ERR_UNSUPPORTED past 8192).
+ * The candidate slots of a group are c + W + g - 1 for PIVOT_WINDOW_PER_QUERY
+ * with W > 0, else c (pivot_cand_width(); 0 for a NULL opts).
+ * pivot_group_workspace_size: workspace bytes for pivot_group_index_opts with
+ * these opts and shapes (dense_below as given), 0 if they are invalid; the
+ * rules of pivot_workspace_size apply.  opts is read, never kept.
+ */
+int32_t pivot_cand_width(const pivot_group_opts* o);
+size_t pivot_group_workspace_size(const pivot_args* a, const pivot_group_opts* o);
+pivot_status pivot_group_index_opts(const pivot_args* a, const pivot_group_opts* o);
+
 /*
  * Stage: proxy rows of Eq. 4 for one sequence's queries q [n_q, H, d] /
  * q_scale [n_q] / w [n_q, H] split into runs of g (last may be shorter).

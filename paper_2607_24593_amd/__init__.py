@@ -22,9 +22,12 @@ PIVOT_DT_BF16, PIVOT_DT_FP8_E4M3 = 0, 1
 PIVOT_REUSE, PIVOT_REFINE = 0, 1
 PIVOT_DENSE = -1
 PIVOT_MAX_KEYS = 1 << 27
+PIVOT_WINDOW_SHARED, PIVOT_WINDOW_PER_QUERY = 0, 1
+PIVOT_AGG_MEAN, PIVOT_AGG_FIRST, PIVOT_AGG_LAST = 0, 1, 2
 H, D = 64, 128
 
-EXPORTED = ["pivot_workspace_size", "pivot_dense_index", "pivot_group_index", "pivot_proxy_rows",
+EXPORTED = ["pivot_workspace_size", "pivot_dense_index", "pivot_group_index", "pivot_cand_width",
+            "pivot_group_workspace_size", "pivot_group_index_opts", "pivot_proxy_rows",
             "pivot_score_rows", "pivot_topk_rows", "pivot_encode_e4m3", "pivot_profile_begin",
             "pivot_profile_end", "pivot_status_string", "pivot_last_error", "pivot_version"]
 KERNELS = ["proxy", "score", "select", "refine", "fill", "lin"]
@@ -53,6 +56,24 @@ class pivot_args(ctypes.Structure):
     ]
 
 
+class pivot_group_opts(ctypes.Structure):
+    _fields_ = [
+        ("mode", ctypes.c_int32), ("g", ctypes.c_int32), ("c", ctypes.c_int32),
+        ("dense_below", ctypes.c_int32), ("window", ctypes.c_int32), ("window_kind", ctypes.c_int32),
+        ("aggregate", ctypes.c_int32), ("out_cand", ctypes.c_void_p),
+    ]
+
+
+def group_opts(mode, g, c, dense_below=-1, window=0, window_kind=PIVOT_WINDOW_SHARED,
+               aggregate=PIVOT_AGG_MEAN, out_cand=None) -> pivot_group_opts:
+    o = pivot_group_opts()
+    o.mode, o.g, o.c, o.dense_below = int(mode), int(g), int(c), int(dense_below)
+    o.window, o.window_kind, o.aggregate = int(window), int(window_kind), int(aggregate)
+    o.out_cand = _ptr(out_cand)
+    o._keep = out_cand
+    return o
+
+
 _lib = None
 
 
@@ -71,6 +92,13 @@ def lib():
         L.pivot_dense_index.argtypes = [A]
         L.pivot_group_index.restype = I32
         L.pivot_group_index.argtypes = [A, I32, I32, I32, I32, P]
+        O = ctypes.POINTER(pivot_group_opts)
+        L.pivot_cand_width.restype = I32
+        L.pivot_cand_width.argtypes = [O]
+        L.pivot_group_workspace_size.restype = ctypes.c_size_t
+        L.pivot_group_workspace_size.argtypes = [A, O]
+        L.pivot_group_index_opts.restype = I32
+        L.pivot_group_index_opts.argtypes = [A, O]
         L.pivot_proxy_rows.restype = I32
         L.pivot_proxy_rows.argtypes = [I32, I32, I32, I32, I32, P, P, P, P, P, P, P]
         L.pivot_score_rows.restype = I32
@@ -214,6 +242,34 @@ def pivot_group_index(q, q_scale, w, k, k_scale, q_pos0, n_k, topk, mode, g, c, 
     _attach_workspace(a, mode, g, c, ws, q.device)
     _check(lib().pivot_group_index(ctypes.byref(a), int(mode), int(g), int(c), int(dense_below),
                                    _ptr(out_cand)), "pivot_group_index")
+    return out
+
+
+def pivot_cand_width(o: pivot_group_opts) -> int:
+    return int(lib().pivot_cand_width(ctypes.byref(o)))
+
+
+def pivot_group_workspace_size(a: pivot_args, o: pivot_group_opts) -> int:
+    return int(lib().pivot_group_workspace_size(ctypes.byref(a), ctypes.byref(o)))
+
+
+def pivot_group_index_opts(q, q_scale, w, k, k_scale, q_pos0, n_k, topk, mode, g, c, dense_below=-1,
+                           window=0, window_kind=PIVOT_WINDOW_SHARED, aggregate=PIVOT_AGG_MEAN,
+                           out=None, out_cand=None, ws=None, stream=None):
+    """PIVOT with App. B's local window and the first / last proxy aggregation;
+    out_cand, when given, is int32 [B, n_groups, pivot_cand_width(opts)]."""
+    squeeze = q.dim() == 3
+    shape = (q.shape[0], topk) if squeeze else (q.shape[0], q.shape[1], topk)
+    out = torch.empty(shape, dtype=torch.int32, device=q.device) if out is None else out
+    a = make_args(q, q_scale, w, k, k_scale, q_pos0, n_k, topk, out, stream=stream)
+    o = group_opts(mode, g, c, dense_below, window, window_kind, aggregate, out_cand)
+    need = pivot_group_workspace_size(a, o)
+    if need > 0 or a.n_q == 0:
+        buf = ws if ws is not None else workspace(need, q.device)
+        a.workspace = _ptr(buf)
+        a.workspace_bytes = buf.numel() * buf.element_size()
+        a._ws = buf
+    _check(lib().pivot_group_index_opts(ctypes.byref(a), ctypes.byref(o)), "pivot_group_index_opts")
     return out
 
 

@@ -98,6 +98,12 @@ struct Plan {
   size_t off_qlin = 0, off_qlsc = 0, off_plin = 0, off_plsc = 0;  // fp8 epilogue's linear term
   size_t off_rsc = 0;                                              // Refine member scores
   bool qlin = false, plin = false;
+  // App. B window and the proxy aggregation
+  int W = 0, wkind = PIVOT_WINDOW_SHARED, agg = PIVOT_AGG_MEAN;
+  int wg = 0;          // window union slots (W + g - 1, or 0)
+  int width = 0;       // candidate slots per group
+  int proxy_m = 0;     // slots the proxy fills (c, or c - wg for the shared window)
+  int scan_shift = 0;  // the proxy scans [0, t0 - scan_shift]
 };
 
 pivot_status check_args(const pivot_args* a) {
@@ -132,21 +138,49 @@ pivot_status check_args(const pivot_args* a) {
 
 // ext_cand: Refine writes its candidate sets to the caller's buffer, so the
 // workspace reserves none.
-pivot_status make_plan(const pivot_args* a, int mode, int g, int c, int dense_below, bool ext_cand, Plan& p) {
+// Width of a group's candidate row (App. B): c, plus the window union for the
+// per-query window.
+int cand_width(int c, int g, int W, int wkind) {
+  return (W > 0 && wkind == PIVOT_WINDOW_PER_QUERY) ? c + W + g - 1 : c;
+}
+
+pivot_status make_plan(const pivot_args* a, int mode, int g, int c, int dense_below, bool ext_cand, Plan& p,
+                       int W = 0, int wkind = PIVOT_WINDOW_SHARED, int agg = PIVOT_AGG_MEAN) {
   pivot_status s = check_args(a);
   if (s != PIVOT_OK) return s;
   if (mode != PIVOT_DENSE && mode != PIVOT_REUSE && mode != PIVOT_REFINE)
     return fail(PIVOT_ERR_INVALID_ARG, "mode %d", mode);
+  if (agg != PIVOT_AGG_MEAN && agg != PIVOT_AGG_FIRST && agg != PIVOT_AGG_LAST)
+    return fail(PIVOT_ERR_INVALID_ARG, "aggregate %d", agg);
+  if (wkind != PIVOT_WINDOW_SHARED && wkind != PIVOT_WINDOW_PER_QUERY)
+    return fail(PIVOT_ERR_INVALID_ARG, "window_kind %d", wkind);
+  if (W < 0) return fail(PIVOT_ERR_INVALID_ARG, "window must be >= 0");
   if (mode != PIVOT_DENSE) {
     if (g < 1) return fail(PIVOT_ERR_INVALID_ARG, "g must be >= 1");
     if (c < 0) return fail(PIVOT_ERR_INVALID_ARG, "c must be >= 0");
-    if (mode == PIVOT_REFINE && c < a->topk) return fail(PIVOT_ERR_INVALID_ARG, "Refine needs c >= topk");
-    if (mode == PIVOT_REFINE && c > 8192) return fail(PIVOT_ERR_UNSUPPORTED, "Refine supports c <= 8192");
+    if (W > 0 && mode != PIVOT_REFINE) return fail(PIVOT_ERR_INVALID_ARG, "the window applies to Refine only");
+    if (W > 0 && wkind == PIVOT_WINDOW_SHARED && c < W + g - 1)
+      return fail(PIVOT_ERR_INVALID_ARG, "the shared window needs c >= W + g - 1");
+    if (W > 0 && wkind == PIVOT_WINDOW_PER_QUERY && W < g)
+      return fail(PIVOT_ERR_INVALID_ARG, "the per-query window needs W >= g");
+    const int64_t width = mode == PIVOT_REFINE ? (int64_t)cand_width(c, g, W, wkind) : c;
+    if (mode == PIVOT_REFINE && width < a->topk)
+      return fail(PIVOT_ERR_INVALID_ARG, "Refine needs topk <= candidate slots (%lld)", (long long)width);
+    if (mode == PIVOT_REFINE && width > 8192) return fail(PIVOT_ERR_UNSUPPORTED, "Refine supports <= 8192 candidates");
     if (mode == PIVOT_REFINE && g > 65535) return fail(PIVOT_ERR_UNSUPPORTED, "Refine supports g <= 65535");
   } else {
     g = 1;
     c = 0;
+    W = 0;
+    agg = PIVOT_AGG_MEAN;
   }
+  p.W = W;
+  p.wkind = wkind;
+  p.agg = agg;
+  p.wg = W > 0 ? W + g - 1 : 0;
+  p.width = mode == PIVOT_REFINE ? cand_width(c, g, W, wkind) : c;
+  p.proxy_m = (W > 0 && wkind == PIVOT_WINDOW_SHARED) ? c - p.wg : c;
+  p.scan_shift = (W > 0 && wkind == PIVOT_WINDOW_SHARED) ? W : 0;
   p.mode = mode;
   p.g = g;
   p.c = c;
@@ -209,9 +243,9 @@ pivot_status make_plan(const pivot_args* a, int mode, int g, int c, int dense_be
     off = align_up(off + ng * kH * sizeof(float));
     if (mode == PIVOT_REFINE) {
       p.off_rsc = off;
-      off = align_up(off + ng * (size_t)g * c * sizeof(float));
+      off = align_up(off + ng * (size_t)g * p.width * sizeof(float));
       p.off_cand = off;
-      if (!ext_cand) off = align_up(off + ng * (size_t)c * sizeof(int32_t));
+      if (!ext_cand) off = align_up(off + ng * (size_t)p.width * sizeof(int32_t));
     }
   }
   p.off_scores = off;
@@ -243,12 +277,14 @@ size_t recommended_bytes(const Plan& p) {
   return p.fixed + (size_t)scores;
 }
 
-SeqTable table_for(const Plan& p, int b0, int nb) {
+// shift: subtracted from the query positions for the row limits (the shared
+// window's proxy scans [0, t0 - W]); may make early limits negative.
+SeqTable table_for(const Plan& p, int b0, int nb, int shift = 0) {
   SeqTable st;
   memset(&st, 0, sizeof st);
   st.n = nb;
   for (int u = 0; u < nb; ++u) {
-    st.q_pos0[u] = p.q_pos0[b0 + u];
+    st.q_pos0[u] = p.q_pos0[b0 + u] - shift;
     st.dense_rows[u] = p.dense_rows[b0 + u];
     st.first_proxy[u] = p.first_proxy[b0 + u];
   }
@@ -280,7 +316,7 @@ struct RowData {
 // Score and select rows [lo, hi) of each sequence, tiled to the score budget.
 pivot_status run_rows(const pivot_args* a, const Plan& p, int kind, int lo, int hi, int step, int per_seq,
                       const RowData& rd_all, OutDesc od_all, float* scores, int64_t score_bytes,
-                      hipStream_t stream) {
+                      hipStream_t stream, int lim_shift = 0) {
   if (hi <= lo) return PIVOT_OK;
   const int64_t ld_max = ld_for(p.max_nk);
   const int64_t row_bytes = ld_max * 4;
@@ -299,7 +335,7 @@ pivot_status run_rows(const pivot_args* a, const Plan& p, int kind, int lo, int 
     return fail(PIVOT_ERR_WORKSPACE, "workspace too small for one score tile");
   for (int b0 = 0; b0 < p.B; b0 += seqs_per_tile) {
     const int nb = std::min(seqs_per_tile, p.B - b0);
-    SeqTable st = table_for(p, b0, nb);
+    SeqTable st = table_for(p, b0, nb, lim_shift);
     RowData rd = rd_all;
     rd.q = (const uint8_t*)rd_all.q + (size_t)b0 * rd_all.seq_rows * p.row_bytes;
     rd.qs = rd_all.qs ? rd_all.qs + (size_t)b0 * rd_all.seq_rows : nullptr;
@@ -309,17 +345,18 @@ pivot_status run_rows(const pivot_args* a, const Plan& p, int kind, int lo, int 
     const uint8_t* kb = (const uint8_t*)a->k + (size_t)b0 * a->k_seq_stride * kD * p.EB;
     const float* ksb = a->k_scale ? a->k_scale + (size_t)b0 * a->k_seq_stride : nullptr;
     OutDesc od = od_all;
-    od.base = od_all.base + (size_t)b0 * od_all.per_seq * od_all.m;
+    od.base = od_all.base + (size_t)b0 * od_all.per_seq * od_all.ld;
     for (int i0 = lo; i0 < hi; i0 += rows_per_tile) {
       RowSpace rs{i0, std::min(hi, i0 + rows_per_tile), step, kind};
       const int64_t lim = max_limit(st, rs);
-      if (lim < 0) continue;
-      const int64_t ld = ld_for(lim + 1);
-      pivot_status s = hip_check(timed(PIVOT_KERNEL_SCORE, stream, [&] {
-                                   return launch_score(p.dtype, rd.q, rd.qs, rd.w, rd.lin, rd.lsc, rd.seq_rows, kb,
-                                                       ksb, a->k_seq_stride, st, rs, lim, scores, ld, stream);
-                                 }),
-                                 "score kernel");
+      const int64_t ld = ld_for(std::max<int64_t>(lim, 0) + 1);
+      pivot_status s = PIVOT_OK;
+      if (lim >= 0)  // no key in reach (shifted limits): the select only pads with -1
+        s = hip_check(timed(PIVOT_KERNEL_SCORE, stream, [&] {
+                        return launch_score(p.dtype, rd.q, rd.qs, rd.w, rd.lin, rd.lsc, rd.seq_rows, kb, ksb,
+                                            a->k_seq_stride, st, rs, lim, scores, ld, stream);
+                      }),
+                      "score kernel");
       if (s != PIVOT_OK) return s;
       s = hip_check(timed(PIVOT_KERNEL_SELECT, stream,
                           [&] {
@@ -371,49 +408,35 @@ pivot_status dense_part(const pivot_args* a, const Plan& p, float* scores, int64
   const bool fp8 = a->dtype == PIVOT_DT_FP8_E4M3;
   RowData rd{a->q, fp8 ? a->q_scale : nullptr, a->w, fp8 ? ws + p.off_qlin : nullptr,
              fp8 ? reinterpret_cast<const float*>(ws + p.off_qlsc) : nullptr, p.n_q};
-  OutDesc od{a->out_idx, p.topk, p.n_q, 0, p.n_q};
+  OutDesc od{a->out_idx, p.topk, p.n_q, 0, p.n_q, p.topk};
   const int kind = p.mode == PIVOT_DENSE ? kAll : kDenseRows;
   return run_rows(a, p, kind, 0, p.dense_hi, 1, p.n_q, rd, od, scores, score_bytes, stream);
 }
 
-}  // namespace
-
-extern "C" {
-
-size_t pivot_workspace_size(const pivot_args* a, int32_t mode, int32_t g, int32_t c) {
-  if (!a) return 0;
+// Sizing validates the shape only: the pointers get non-null stand-ins.
+pivot_args shape_of(const pivot_args* a) {
   pivot_args shape = *a;
-  // pointers are not read for sizing: give the validator non-null stand-ins
   static const float dummy = 0.f;
   shape.q = shape.k = &dummy;
   shape.w = shape.q_scale = shape.k_scale = &dummy;
   shape.out_idx = reinterpret_cast<int32_t*>(const_cast<float*>(&dummy));
-  Plan p;
-  if (make_plan(&shape, mode, g, c, c, false, p) != PIVOT_OK) return 0;
-  return recommended_bytes(p);
+  return shape;
 }
 
-pivot_status pivot_dense_index(const pivot_args* a) {
-  Plan p;
-  pivot_status s = make_plan(a, PIVOT_DENSE, 1, 0, 0, false, p);
-  if (s != PIVOT_OK) return s;
-  if (p.n_q == 0) return PIVOT_OK;
-  int64_t score_bytes;
-  s = check_workspace(a, p, score_bytes);
-  if (s != PIVOT_OK) return s;
-  float* scores = reinterpret_cast<float*>((uint8_t*)a->workspace + p.off_scores);
-  s = query_lin(a, p, (uint8_t*)a->workspace, (hipStream_t)a->stream);
-  if (s != PIVOT_OK) return s;
-  return dense_part(a, p, scores, score_bytes, (hipStream_t)a->stream);
+pivot_status group_plan(const pivot_args* a, const pivot_group_opts* o, bool ext_cand, Plan& p) {
+  if (!o) return fail(PIVOT_ERR_INVALID_ARG, "opts is NULL");
+  if (o->mode != PIVOT_REUSE && o->mode != PIVOT_REFINE) return fail(PIVOT_ERR_INVALID_ARG, "mode %d", o->mode);
+  return make_plan(a, o->mode, o->g, o->c, o->dense_below, ext_cand, p, o->window, o->window_kind, o->aggregate);
 }
 
-pivot_status pivot_group_index(const pivot_args* a, int32_t mode, int32_t g, int32_t c, int32_t dense_below,
-                               int32_t* out_cand) {
-  if (mode != PIVOT_REUSE && mode != PIVOT_REFINE) return fail(PIVOT_ERR_INVALID_ARG, "mode %d", mode);
+pivot_status group_index(const pivot_args* a, const pivot_group_opts* o) {
   Plan p;
-  pivot_status s = make_plan(a, mode, g, c, dense_below, out_cand != nullptr && mode == PIVOT_REFINE, p);
+  pivot_status s = group_plan(a, o, o && o->out_cand != nullptr && o->mode == PIVOT_REFINE, p);
   if (s != PIVOT_OK) return s;
   if (p.n_q == 0) return PIVOT_OK;
+  const int mode = p.mode;
+  int32_t* out_cand = mode == PIVOT_REFINE ? o->out_cand : nullptr;
+  const int width = p.width;
   hipStream_t stream = (hipStream_t)a->stream;
   int64_t score_bytes;
   s = check_workspace(a, p, score_bytes);
@@ -430,7 +453,7 @@ pivot_status pivot_group_index(const pivot_args* a, int32_t mode, int32_t g, int
   const bool any_proxy = p.proxy_lo < p.n_groups;
 
   if (any_proxy)
-    for (int b0 = 0; b0 < p.B; b0 += kMaxSeq) {  // Eq. 4 proxies
+    for (int b0 = 0; b0 < p.B; b0 += kMaxSeq) {  // Eq. 4 proxies (or the first / last member)
       const int nb = std::min(kMaxSeq, p.B - b0);
       SeqTable st = table_for(p, b0, nb);
       const size_t qoff = (size_t)b0 * p.n_q;
@@ -438,7 +461,7 @@ pivot_status pivot_group_index(const pivot_args* a, int32_t mode, int32_t g, int
       s = hip_check(timed(PIVOT_KERNEL_PROXY, stream, [&] {
                       return launch_proxy(p.dtype, (const uint8_t*)a->q + qoff * p.row_bytes,
                                           qs ? qs + qoff : nullptr, a->w + qoff * kH, p.n_q, p.g, p.n_groups, st,
-                                          p.proxy_lo, p.n_groups, false, (uint8_t*)pq + poff * p.row_bytes,
+                                          p.proxy_lo, p.n_groups, false, p.agg, (uint8_t*)pq + poff * p.row_bytes,
                                           psc + poff, pw + poff * kH, stream);
                     }),
                     "proxy kernel");
@@ -466,13 +489,13 @@ pivot_status pivot_group_index(const pivot_args* a, int32_t mode, int32_t g, int
   s = dense_part(a, p, scores, score_bytes, stream);  // guardrail groups (Algorithm 1)
   if (s != PIVOT_OK) return s;
   if (!any_proxy) {
-    if (out_cand && mode == PIVOT_REFINE)
+    if (out_cand)
       for (int b0 = 0; b0 < p.B; b0 += kMaxSeq) {
         const int nb = std::min(kMaxSeq, p.B - b0);
         SeqTable st = table_for(p, b0, nb);
         s = hip_check(timed(PIVOT_KERNEL_FILL, stream, [&] {
-                        return launch_fill_guardrail(out_cand + (size_t)b0 * p.n_groups * c, p.n_groups, c, st,
-                                                     0, p.n_groups, -1, stream);
+                        return launch_fill_guardrail(out_cand + (size_t)b0 * p.n_groups * width, p.n_groups, width,
+                                                     st, 0, p.n_groups, -1, stream);
                       }),
                       "fill kernel");
         if (s != PIVOT_OK) return s;
@@ -481,25 +504,38 @@ pivot_status pivot_group_index(const pivot_args* a, int32_t mode, int32_t g, int
   }
 
   // Eq. 5 proxy scan, then Eq. 6 (Reuse: top-k shared by the members) or
-  // Eq. 7 (Refine: top-c candidates)
+  // Eq. 7 (Refine: top-c candidates; before a shared window, the top c - W - g + 1
+  // over [0, t0 - W])
   RowData rd{pq, p.dtype == PIVOT_DT_FP8_E4M3 ? psc : nullptr, pw, plin, plsc, p.n_groups};
-  OutDesc od = (mode == PIVOT_REUSE) ? OutDesc{a->out_idx, p.topk, p.n_q, p.g, p.n_q}
-                                     : OutDesc{cand, c, p.n_groups, 0, 0};
-  s = run_rows(a, p, kProxyRows, p.proxy_lo, p.n_groups, p.g, p.n_groups, rd, od, scores, score_bytes, stream);
-  if (s != PIVOT_OK) return s;
+  OutDesc od = (mode == PIVOT_REUSE) ? OutDesc{a->out_idx, p.topk, p.n_q, p.g, p.n_q, p.topk}
+                                     : OutDesc{cand, p.proxy_m, p.n_groups, 0, 0, width};
+  if (od.m > 0) {
+    s = run_rows(a, p, kProxyRows, p.proxy_lo, p.n_groups, p.g, p.n_groups, rd, od, scores, score_bytes, stream,
+                 p.scan_shift);
+    if (s != PIVOT_OK) return s;
+  }
   if (mode == PIVOT_REUSE) return PIVOT_OK;
 
-  for (int b0 = 0; b0 < p.B; b0 += kMaxSeq) {  // Eqs. 8-9
+  for (int b0 = 0; b0 < p.B; b0 += kMaxSeq) {  // App. B window, Eqs. 8-9
     const int nb = std::min(kMaxSeq, p.B - b0);
     SeqTable st = table_for(p, b0, nb);
     const size_t qoff = (size_t)b0 * p.n_q;
-    int32_t* cb = cand + (size_t)b0 * p.n_groups * c;
+    int32_t* cb = cand + (size_t)b0 * p.n_groups * width;
     if (out_cand) {
       s = hip_check(timed(PIVOT_KERNEL_FILL, stream,
-                          [&] { return launch_fill_guardrail(cb, p.n_groups, c, st, 0, p.n_groups, -1, stream); }),
+                          [&] { return launch_fill_guardrail(cb, p.n_groups, width, st, 0, p.n_groups, -1, stream); }),
                     "fill kernel");
       if (s != PIVOT_OK) return s;
     }
+    if (p.W > 0) {
+      s = hip_check(timed(PIVOT_KERNEL_FILL, stream, [&] {
+                      return launch_window(cb, p.n_q, p.g, p.n_groups, st, p.proxy_lo, p.n_groups, width, p.proxy_m,
+                                           p.W, p.wkind == PIVOT_WINDOW_PER_QUERY, stream);
+                    }),
+                    "window kernel");
+      if (s != PIVOT_OK) return s;
+    }
+    const int wslot = p.wkind == PIVOT_WINDOW_PER_QUERY ? p.proxy_m : width;
     s = hip_check(timed(PIVOT_KERNEL_REFINE, stream, [&] {
                     return launch_refine(p.dtype, (const uint8_t*)a->q + qoff * p.row_bytes,
                                          qs ? qs + qoff : nullptr, a->w + qoff * kH,
@@ -509,9 +545,9 @@ pivot_status pivot_group_index(const pivot_args* a, int32_t mode, int32_t g, int
                                          p.n_q, p.g, p.n_groups,
                                          (const uint8_t*)a->k + (size_t)b0 * a->k_seq_stride * kD * p.EB,
                                          a->k_scale ? a->k_scale + (size_t)b0 * a->k_seq_stride : nullptr,
-                                         a->k_seq_stride, st, p.proxy_lo, p.n_groups, cb, c, p.topk,
+                                         a->k_seq_stride, st, p.proxy_lo, p.n_groups, cb, width, p.W, wslot, p.topk,
                                          reinterpret_cast<float*>(ws + p.off_rsc) +
-                                             (size_t)b0 * p.n_groups * p.g * c,
+                                             (size_t)b0 * p.n_groups * p.g * width,
                                          a->out_idx + qoff * p.topk, stream);
                   }),
                   "refine kernel");
@@ -519,6 +555,73 @@ pivot_status pivot_group_index(const pivot_args* a, int32_t mode, int32_t g, int
   }
   return PIVOT_OK;
 }
+
+pivot_group_opts plain_opts(int32_t mode, int32_t g, int32_t c, int32_t dense_below, int32_t* out_cand) {
+  pivot_group_opts o;
+  memset(&o, 0, sizeof o);
+  o.mode = mode;
+  o.g = g;
+  o.c = c;
+  o.dense_below = dense_below;
+  o.window = 0;
+  o.window_kind = PIVOT_WINDOW_SHARED;
+  o.aggregate = PIVOT_AGG_MEAN;
+  o.out_cand = out_cand;
+  return o;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t pivot_workspace_size(const pivot_args* a, int32_t mode, int32_t g, int32_t c) {
+  if (!a) return 0;
+  if (mode == PIVOT_DENSE) {
+    pivot_args shape = shape_of(a);
+    Plan p;
+    if (make_plan(&shape, PIVOT_DENSE, 1, 0, 0, false, p) != PIVOT_OK) return 0;
+    return recommended_bytes(p);
+  }
+  const pivot_group_opts o = plain_opts(mode, g, c, c, nullptr);
+  return pivot_group_workspace_size(a, &o);
+}
+
+int32_t pivot_cand_width(const pivot_group_opts* o) {
+  if (!o) return 0;
+  return cand_width(o->c, o->g, o->window, o->window_kind);
+}
+
+size_t pivot_group_workspace_size(const pivot_args* a, const pivot_group_opts* o) {
+  if (!a || !o) return 0;
+  pivot_args shape = shape_of(a);
+  pivot_group_opts oc = *o;
+  oc.out_cand = nullptr;
+  Plan p;
+  if (group_plan(&shape, &oc, false, p) != PIVOT_OK) return 0;
+  return recommended_bytes(p);
+}
+
+pivot_status pivot_dense_index(const pivot_args* a) {
+  Plan p;
+  pivot_status s = make_plan(a, PIVOT_DENSE, 1, 0, 0, false, p);
+  if (s != PIVOT_OK) return s;
+  if (p.n_q == 0) return PIVOT_OK;
+  int64_t score_bytes;
+  s = check_workspace(a, p, score_bytes);
+  if (s != PIVOT_OK) return s;
+  float* scores = reinterpret_cast<float*>((uint8_t*)a->workspace + p.off_scores);
+  s = query_lin(a, p, (uint8_t*)a->workspace, (hipStream_t)a->stream);
+  if (s != PIVOT_OK) return s;
+  return dense_part(a, p, scores, score_bytes, (hipStream_t)a->stream);
+}
+
+pivot_status pivot_group_index(const pivot_args* a, int32_t mode, int32_t g, int32_t c, int32_t dense_below,
+                               int32_t* out_cand) {
+  const pivot_group_opts o = plain_opts(mode, g, c, dense_below, out_cand);
+  return group_index(a, &o);
+}
+
+pivot_status pivot_group_index_opts(const pivot_args* a, const pivot_group_opts* o) { return group_index(a, o); }
 
 pivot_status pivot_proxy_rows(int32_t dtype, int32_t heads, int32_t dim, int32_t n_q, int32_t g, const void* q,
                               const float* q_scale, const float* w, void* out_q, float* out_scale, float* out_w,
@@ -534,7 +637,7 @@ pivot_status pivot_proxy_rows(int32_t dtype, int32_t heads, int32_t dim, int32_t
   st.n = 1;
   const int ng = (int)cdiv(n_q, g);
   return hip_check(launch_proxy(dtype, q, dtype == PIVOT_DT_FP8_E4M3 ? q_scale : nullptr, w, n_q, g, ng, st, 0, ng,
-                                true, out_q, out_scale, out_w, (hipStream_t)stream),
+                                true, PIVOT_AGG_MEAN, out_q, out_scale, out_w, (hipStream_t)stream),
                    "proxy kernel");
 }
 
@@ -592,7 +695,7 @@ pivot_status pivot_topk_rows(int32_t n_rows, const float* scores, int64_t ld, in
   st.n = 1;
   st.q_pos0[0] = (int32_t)(n0 - 1);
   RowSpace rs{0, n_rows, n_step, kAll};
-  OutDesc od{out, m, n_rows, 0, 0};
+  OutDesc od{out, m, n_rows, 0, 0, m};
   return hip_check(launch_topk(scores, ld, st, rs, od, n_max - 1, (hipStream_t)stream), "top-k kernel");
 }
 

@@ -8,22 +8,25 @@
 
 namespace pivot {
 
-// Where a row's top-m indices go: row (b, i) writes out rows
+// Where a row's top-m indices go: row (b, i) writes entries [0, m) of out rows
 //   fan_g == 0: b * per_seq + i
 //   fan_g  > 0: b * per_seq + i * fan_g + u, u < min(fan_g, fan_n - i * fan_g)
-// (the fan-out shares a proxy's top-k with the members of its group).
+// (the fan-out shares a proxy's top-k with the members of its group); out rows
+// are ld >= m entries apart (a candidate row keeps window slots after m).
 struct OutDesc {
   int32_t* base;
   int32_t m;
   int32_t per_seq;
   int32_t fan_g;
   int32_t fan_n;
+  int32_t ld;
 };
 
 // Proxy rows (Eq. 4) of groups [j0, j1) of each sequence; q rows are
 // [B, n_q, H, d], proxies [B, n_groups, H, d].  all_groups ignores first_proxy.
+// agg: PIVOT_AGG_MEAN (Eq. 4), or PIVOT_AGG_FIRST / LAST (that member's row).
 hipError_t launch_proxy(int dtype, const void* q, const float* q_scale, const float* w, int n_q, int g,
-                        int n_groups, const SeqTable& st, int j0, int j1, bool all_groups, void* pq,
+                        int n_groups, const SeqTable& st, int j0, int j1, bool all_groups, int agg, void* pq,
                         float* psc, float* pw, hipStream_t stream);
 
 // The fp8 epilogue's linear term (mfma_tile.h) for flat rows [r0, r1) of an
@@ -56,12 +59,21 @@ hipError_t launch_topk(const float* scores, int64_t ld, const SeqTable& st, cons
                        const OutDesc& od, int64_t lim_max, hipStream_t stream);
 
 // Refine (Eqs. 8-9) for groups [j0, j1) with j >= first_proxy[b]: re-score
-// the candidates into rescore [B, n_groups, g, c] fp32, then select top-m.
+// the candidate rows [B, n_groups, c] into rescore [B, n_groups, g, c] fp32,
+// then select top-m.  W = 0: plain rows (the first min(c, t0 + 1) slots hold
+// positions).  W > 0 (App. B window): any slot may be empty (-1); member t
+// uses positions in [0, t], from slot wslot on also >= t - W + 1.
 hipError_t launch_refine(int dtype, const void* q, const float* q_scale, const float* w, const uint8_t* lin,
                          const float* lin_scale, int n_q, int g, int n_groups, const void* k,
                          const float* k_scale, int64_t k_seq_stride, const SeqTable& st, int j0, int j1,
-                         const int32_t* cand, int c, int m, float* rescore, int32_t* out_idx,
+                         const int32_t* cand, int c, int W, int wslot, int m, float* rescore, int32_t* out_idx,
                          hipStream_t stream);
+
+// App. B window union of groups [j0, j1) (j >= first_proxy[b]) into slots
+// [slot0, slot0 + W + g - 1) of the [B, n_groups, width] candidate rows;
+// dedupe empties positions already among the first slot0 slots.
+hipError_t launch_window(int32_t* cand, int n_q, int g, int n_groups, const SeqTable& st, int j0, int j1, int width,
+                         int slot0, int W, bool dedupe, hipStream_t stream);
 
 // Fill rows (b, j) with j < first_proxy[b], j in [j0, j1), of a [B, per_seq, width] int32 array.
 hipError_t launch_fill_guardrail(int32_t* base, int per_seq, int width, const SeqTable& st, int j0, int j1,

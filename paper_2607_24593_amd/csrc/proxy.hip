@@ -7,9 +7,11 @@
 // contraction disabled, so the result is reproducible bit for bit:
 //   fp8 : mean of (qscale_t * q8_t); scale = amax / 448; codes = RNE(mean / scale)
 //   bf16: mean of q_t; RNE to bf16
-// A group of one is copied unchanged.
+// A group of one is copied unchanged, and so is the chosen member for the
+// first / last aggregation (Sec. 5.4).
 #include "launch.h"
 #include "mfma_tile.h"
+#include "pivot.h"
 
 namespace pivot {
 
@@ -40,7 +42,7 @@ template <int DT>
 __global__ __launch_bounds__(256) void proxy_kernel(const uint8_t* __restrict__ q,
                                                     const float* __restrict__ q_scale,
                                                     const float* __restrict__ w, int n_q, int g, int n_groups,
-                                                    SeqTable st, int j0, int all_groups,
+                                                    SeqTable st, int j0, int all_groups, int agg,
                                                     uint8_t* __restrict__ pq, float* __restrict__ psc,
                                                     float* __restrict__ pw) {
 #pragma clang fp contract(off)
@@ -56,13 +58,14 @@ __global__ __launch_bounds__(256) void proxy_kernel(const uint8_t* __restrict__ 
   const int tid = threadIdx.x;
   const int e0 = tid * PER;
 
-  if (gs == 1) {
-    const uint4* src = reinterpret_cast<const uint4*>(q + r0 * ROW_BYTES + e0 * EB);
+  if (gs == 1 || agg != PIVOT_AGG_MEAN) {
+    const int64_t rc = r0 + (agg == PIVOT_AGG_LAST ? gs - 1 : 0);
+    const uint4* src = reinterpret_cast<const uint4*>(q + rc * ROW_BYTES + e0 * EB);
     uint4* dst = reinterpret_cast<uint4*>(pq + pr * ROW_BYTES + e0 * EB);
 #pragma unroll
     for (int v = 0; v < PER * EB / 16; ++v) dst[v] = src[v];
-    if (tid == 0) psc[pr] = (DT == kFp8) ? q_scale[r0] : 1.0f;
-    if (tid < kH) pw[pr * kH + tid] = w[r0 * kH + tid];
+    if (tid == 0) psc[pr] = (DT == kFp8) ? q_scale[rc] : 1.0f;
+    if (tid < kH) pw[pr * kH + tid] = w[rc * kH + tid];
     return;
   }
 
@@ -137,16 +140,16 @@ __global__ __launch_bounds__(256) void proxy_kernel(const uint8_t* __restrict__ 
 }
 
 hipError_t launch_proxy(int dtype, const void* q, const float* q_scale, const float* w, int n_q, int g,
-                        int n_groups, const SeqTable& st, int j0, int j1, bool all_groups, void* pq,
+                        int n_groups, const SeqTable& st, int j0, int j1, bool all_groups, int agg, void* pq,
                         float* psc, float* pw, hipStream_t stream) {
   if (j1 <= j0 || st.n <= 0) return hipSuccess;
   dim3 grid((unsigned)(j1 - j0), (unsigned)st.n);
   if (dtype == kFp8)
     hipLaunchKernelGGL(proxy_kernel<kFp8>, grid, dim3(256), 0, stream, (const uint8_t*)q, q_scale, w, n_q, g,
-                       n_groups, st, j0, (int)all_groups, (uint8_t*)pq, psc, pw);
+                       n_groups, st, j0, (int)all_groups, agg, (uint8_t*)pq, psc, pw);
   else
     hipLaunchKernelGGL(proxy_kernel<kBf16>, grid, dim3(256), 0, stream, (const uint8_t*)q, q_scale, w, n_q, g,
-                       n_groups, st, j0, (int)all_groups, (uint8_t*)pq, psc, pw);
+                       n_groups, st, j0, (int)all_groups, agg, (uint8_t*)pq, psc, pw);
   return hipGetLastError();
 }
 

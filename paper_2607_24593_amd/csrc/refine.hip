@@ -14,6 +14,12 @@
 // scores; each thread keeps its share of (key, position) pairs in registers
 // (both read with coalesced loads) and block_select() takes the top-k, ties
 // broken by lower position.
+//
+// App. B local window: window_kernel writes the union of the members' windows
+// into the candidate row after the proxy's slots.  A candidate row then has
+// `width` slots; member t re-scores all of them (empty slots read key 0) and
+// its select keeps the slots it may use: position in [0, t], and for a union
+// slot of the per-query window also position >= t - W + 1.
 #include <algorithm>
 
 #include "block_select.h"
@@ -29,7 +35,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void r
     const uint8_t* __restrict__ q, const float* __restrict__ q_scale, const float* __restrict__ w,
     const uint8_t* __restrict__ lin, const float* __restrict__ lin_scale, int n_q, int g, int n_groups,
     const uint8_t* __restrict__ k, const float* __restrict__ k_scale, int64_t k_seq_stride, SeqTable st, int j0,
-    const int32_t* __restrict__ cand, int c, int parts, float* __restrict__ rsc) {
+    const int32_t* __restrict__ cand, int c, int all_slots, int parts, float* __restrict__ rsc) {
   using Tile = RowTile<DT, R>;
   constexpr int EB = Tile::EB;
   __shared__ int32_t spos[kMaxCand];
@@ -41,7 +47,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void r
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
   const int64_t t0 = (int64_t)st.q_pos0[b] + (int64_t)j * g;
-  const int nc = (int)min((int64_t)c, t0 + 1);
+  // without a window only the first t0 + 1 slots can hold a position
+  const int nc = all_slots ? c : (int)min((int64_t)c, t0 + 1);
   const int rows_here = min(R, gs - R * blk);
   const int32_t* crow = cand + ((int64_t)b * n_groups + j) * c;
   const int64_t r0 = (int64_t)b * n_q + (int64_t)j * g + R * blk;
@@ -83,7 +90,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void r
   const uint32_t my_off = (uint32_t)(qr * c + cbeg) * 4u;
   const int nfrag = fend - fbeg;
   constexpr int S = 4;  // fragment stride between the waves
-  auto pos_of = [&](int f) { return spos[min(16 * f + lr, ncs - 1)]; };
+  auto pos_of = [&](int f) { return max(spos[min(16 * f + lr, ncs - 1)], 0); };  // empty slots: key 0
   auto emit = [&](float acc, float ks, int f) {
     const int slot = 16 * f + lr;
     const uint32_t off = (writer && slot < ncs) ? my_off + 4u * (uint32_t)slot : 0xFFFFFFFFu;
@@ -117,48 +124,80 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void r
 template <int V>
 struct RegSource {
   uint32_t key[V];
-  int32_t pos[V];
-  int count;
+  int32_t pos[V];  // -1: not a candidate of this member
   template <class F>
   __device__ __forceinline__ void visit(F f) const {
 #pragma unroll
     for (int v = 0; v < V; ++v)
-      if ((int)threadIdx.x + 256 * v < count) f(key[v], pos[v]);
+      if (pos[v] >= 0) f(key[v], pos[v]);
   }
+};
+
+// Candidate slots a member may use (App. B): slots >= wslot are per-query
+// window slots with the lower bound t - W + 1; window == 0 means a plain
+// candidate row whose first min(c, t0 + 1) slots are all usable.
+struct SlotRule {
+  int32_t window;
+  int32_t wslot;
 };
 
 template <int V>
 __global__ __launch_bounds__(256) void topk_short_kernel(const float* __restrict__ rsc,
                                                          const int32_t* __restrict__ cand, int n_q, int g,
-                                                         int n_groups, SeqTable st, int j0, int c, int m,
-                                                         int32_t* __restrict__ out_idx) {
+                                                         int n_groups, SeqTable st, int j0, int c, SlotRule rule,
+                                                         int m, int32_t* __restrict__ out_idx) {
   __shared__ SelectShared sel;
   __shared__ uint32_t hist[4096];
-  __shared__ int32_t lcount;
+  __shared__ int32_t lcount, nvalid_sh;
   const int j = j0 + blockIdx.x, b = blockIdx.y, member = blockIdx.z;
   if (b >= st.n || j >= n_groups || j < st.first_proxy[b]) return;
   const int gs = min(g, n_q - j * g);
   if (member >= gs) return;
   const int tid = threadIdx.x;
   const int64_t t0 = (int64_t)st.q_pos0[b] + (int64_t)j * g;
-  const int nc = (int)min((int64_t)c, t0 + 1);
+  const int64_t tt = t0 + member;
+  const bool win = rule.window > 0;
+  const int nc = win ? c : (int)min((int64_t)c, t0 + 1);
   const int64_t grp = (int64_t)b * n_groups + j;
   const float* srow = rsc + (grp * g + member) * (int64_t)c;
   const int32_t* crow = cand + grp * c;
   int32_t* orow = out_idx + ((int64_t)b * n_q + (int64_t)j * g + member) * m;
 
   RegSource<V> src;
-  src.count = nc;
+  int mine = 0;
 #pragma unroll
   for (int v = 0; v < V; ++v) {
     const int e = tid + 256 * v;
-    const bool ok = e < nc;
-    src.key[v] = ok ? float_key(srow[e]) : 0u;
-    src.pos[v] = ok ? crow[e] : 0;
+    const bool in = e < nc;
+    const int32_t p = in ? crow[e] : -1;
+    bool ok = in;
+    if (win) ok = p >= 0 && p <= tt && !(e >= rule.wslot && p < tt - rule.window + 1);
+    src.key[v] = in ? float_key(srow[e]) : 0u;
+    src.pos[v] = ok ? p : -1;
+    mine += ok;
   }
-  if (nc <= m) {  // every candidate is selected
-    for (int p = tid; p < m; p += 256) orow[p] = p < nc ? crow[p] : -1;
-    return;
+  if (!win) {
+    if (nc <= m) {  // every candidate is selected
+      for (int p = tid; p < m; p += 256) orow[p] = p < nc ? crow[p] : -1;
+      return;
+    }
+  } else {
+    if (tid == 0) {
+      nvalid_sh = 0;
+      sel.emitted = 0;
+    }
+    __syncthreads();
+    atomicAdd(&nvalid_sh, mine);
+    __syncthreads();
+    const int nvalid = nvalid_sh;
+    if (nvalid <= m) {  // every usable slot is selected, then -1 padding
+#pragma unroll
+      for (int v = 0; v < V; ++v)
+        wave_append(src.pos[v] >= 0, &sel.emitted, [&](int slot) { orow[slot] = src.pos[v]; });
+      for (int p = nvalid + tid; p < m; p += 256) orow[p] = -1;
+      return;
+    }
+    __syncthreads();  // sel.emitted is cleared again below
   }
   if (tid == 0) sel.emitted = 0;
   __syncthreads();
@@ -168,13 +207,56 @@ __global__ __launch_bounds__(256) void topk_short_kernel(const float* __restrict
     block_select<256, true>(src, (uint32_t)m, sel, put);
 }
 
+// App. B window union: slot0 + u (u < wg) of every candidate row of the
+// groups [j0, j1) with j >= first_proxy[b] takes position t0 - W + 1 + u, or
+// -1 below 0, past the group's last member, or (dedupe) when it is already
+// among the row's first slot0 slots.
+__global__ __launch_bounds__(256) void window_kernel(int32_t* __restrict__ cand, int n_q, int g, int n_groups,
+                                                     SeqTable st, int j0, int width, int slot0, int W, int wg,
+                                                     int dedupe) {
+  __shared__ uint8_t seen[kMaxCand];
+  const int j = j0 + blockIdx.x, b = blockIdx.y;
+  if (b >= st.n || j >= n_groups || j < st.first_proxy[b]) return;
+  const int tid = threadIdx.x;
+  const int gs = min(g, n_q - j * g);
+  const int64_t t0 = (int64_t)st.q_pos0[b] + (int64_t)j * g;
+  const int64_t lo = t0 - W + 1;
+  int32_t* row = cand + ((int64_t)b * n_groups + j) * width;
+  if (dedupe) {
+    for (int u = tid; u < wg; u += 256) seen[u] = 0;
+    __syncthreads();
+    for (int i = tid; i < slot0; i += 256) {
+      const int64_t p = row[i];
+      if (p >= lo && p < lo + wg) seen[p - lo] = 1;
+    }
+    __syncthreads();
+  }
+  for (int u = tid; u < wg; u += 256) {
+    const int64_t p = lo + u;
+    const bool ok = p >= 0 && p <= t0 + gs - 1 && !(dedupe && seen[u]);
+    row[slot0 + u] = ok ? (int32_t)p : -1;
+  }
+}
+
+hipError_t launch_window(int32_t* cand, int n_q, int g, int n_groups, const SeqTable& st, int j0, int j1, int width,
+                         int slot0, int W, bool dedupe, hipStream_t stream) {
+  const int wg = W + g - 1;
+  if (j1 <= j0 || st.n <= 0 || W <= 0) return hipSuccess;
+  if (width > kMaxCand || slot0 < 0 || slot0 + wg > width) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(window_kernel, dim3((unsigned)(j1 - j0), (unsigned)st.n), dim3(256), 0, stream, cand, n_q, g,
+                     n_groups, st, j0, width, slot0, W, wg, (int)dedupe);
+  return hipGetLastError();
+}
+
 hipError_t launch_refine(int dtype, const void* q, const float* q_scale, const float* w, const uint8_t* lin,
                          const float* lin_scale, int n_q, int g, int n_groups, const void* k,
                          const float* k_scale, int64_t k_seq_stride, const SeqTable& st, int j0, int j1,
-                         const int32_t* cand, int c, int m, float* rescore, int32_t* out_idx,
+                         const int32_t* cand, int c, int W, int wslot, int m, float* rescore, int32_t* out_idx,
                          hipStream_t stream) {
   if (j1 <= j0 || st.n <= 0) return hipSuccess;
   if (c > kMaxCand) return hipErrorInvalidValue;
+  const SlotRule rule{W, wslot};
+  const int all_slots = W > 0;
   // few groups (decode): split the candidates so the launch still fills the GPU
   const int R = dtype == kFp8 ? 4 : 2;
   const int64_t wgs = (int64_t)(j1 - j0) * st.n * ((g + R - 1) / R);
@@ -184,24 +266,24 @@ hipError_t launch_refine(int dtype, const void* q, const float* q_scale, const f
   const dim3 grid((unsigned)(j1 - j0), (unsigned)st.n, (unsigned)(((g + R - 1) / R) * parts));
   if (dtype == kFp8)
     hipLaunchKernelGGL((rescore_kernel<kFp8, 4>), grid, dim3(256), 0, stream, (const uint8_t*)q, q_scale, w, lin,
-                       lin_scale, n_q, g, n_groups, (const uint8_t*)k, k_scale, k_seq_stride, st, j0, cand, c, parts,
-                       rescore);
+                       lin_scale, n_q, g, n_groups, (const uint8_t*)k, k_scale, k_seq_stride, st, j0, cand, c,
+                       all_slots, parts, rescore);
   else
     hipLaunchKernelGGL((rescore_kernel<kBf16, 2>), grid, dim3(256), 0, stream, (const uint8_t*)q, q_scale, w, lin,
-                       lin_scale, n_q, g, n_groups, (const uint8_t*)k, nullptr, k_seq_stride, st, j0, cand, c, parts,
-                       rescore);
+                       lin_scale, n_q, g, n_groups, (const uint8_t*)k, nullptr, k_seq_stride, st, j0, cand, c,
+                       all_slots, parts, rescore);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   dim3 sgrid((unsigned)(j1 - j0), (unsigned)st.n, (unsigned)g);
   if (c <= 1024)
     hipLaunchKernelGGL(topk_short_kernel<4>, sgrid, dim3(256), 0, stream, rescore, cand, n_q, g, n_groups, st, j0, c,
-                       m, out_idx);
+                       rule, m, out_idx);
   else if (c <= 4096)
     hipLaunchKernelGGL(topk_short_kernel<16>, sgrid, dim3(256), 0, stream, rescore, cand, n_q, g, n_groups, st, j0,
-                       c, m, out_idx);
+                       c, rule, m, out_idx);
   else
     hipLaunchKernelGGL(topk_short_kernel<32>, sgrid, dim3(256), 0, stream, rescore, cand, n_q, g, n_groups, st, j0,
-                       c, m, out_idx);
+                       c, rule, m, out_idx);
   return hipGetLastError();
 }
 

@@ -156,7 +156,7 @@ __global__ __launch_bounds__(T) void topk_rows_kernel(const float* __restrict__ 
     ndest = min(od.fan_g, od.fan_n - i * od.fan_g);
   }
   auto put = [&](int p, int32_t v) {
-    for (int u = 0; u < ndest; ++u) od.base[(dest0 + u) * m + p] = v;
+    for (int u = 0; u < ndest; ++u) od.base[(dest0 + u) * od.ld + p] = v;
   };
   if (n <= m) {
     for (int p = tid; p < m; p += T) put(p, p < n ? p : -1);

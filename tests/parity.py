@@ -51,14 +51,18 @@ def check_row(gpu, ora, f_of, rtol, in_domain, label=""):
 
 
 def check_pivot(fmt, q, qs, w, p0, k, ks, n_k, *, mode, g, c, topk, dense_below, gpu_idx,
-                gpu_cand=None, groups=None, label=""):
+                gpu_cand=None, groups=None, label="", window=0, window_kind=0, agg=0):
     """Check one sequence's GPU result against the oracle (Algorithm 1).
 
     q / qs / w: the call's n_q query rows (numpy); k / ks: the sequence's keys.
-    mode: oracle.DENSE / REUSE / REFINE.  Refine needs gpu_cand ([n_groups, c])
-    for the two-stage check: (1) the candidate set against the oracle's proxy
-    top-c, (2) each member's set against the oracle's Refine run on the GPU's
-    own candidates.  Returns the number of boundary swaps accepted."""
+    mode: oracle.DENSE / REUSE / REFINE.  Refine needs gpu_cand ([n_groups,
+    width]) for the two-stage check: (1) the candidate set against the
+    oracle's proxy top-c, (2) each member's set against the oracle's Refine
+    run on the GPU's own candidates.  With App. B's window (window > 0) the
+    proxy's slots are checked as in (1) over the proxy's own range, the window
+    union exactly (it follows from t0, W, g and, per query, the GPU's pool),
+    and member t against the oracle's Refine over the slots it may use.
+    agg: the proxy aggregation.  Returns the number of boundary swaps accepted."""
     import oracle
 
     rtol = RTOL[fmt]
@@ -69,7 +73,8 @@ def check_pivot(fmt, q, qs, w, p0, k, ks, n_k, *, mode, g, c, topk, dense_below,
         db = c if dense_below < 0 else dense_below
     res = oracle.index(fmt, q, qs, w, p0, k, ks, n_k, mode=mode, g=g, c=c, topk=topk,
                        dense_below=(0 if mode == oracle.DENSE else db), groups=groups,
-                       want_cand=(mode == oracle.REFINE), want_proxy=(mode != oracle.DENSE))
+                       want_cand=(mode == oracle.REFINE), want_proxy=(mode != oracle.DENSE),
+                       window=window, window_kind=window_kind, agg=agg)
     n_groups = (n_q + g - 1) // g
     sel = range(n_groups) if groups is None else groups
     swaps = 0
@@ -102,10 +107,48 @@ def check_pivot(fmt, q, qs, w, p0, k, ks, n_k, *, mode, g, c, topk, dense_below,
             for r in rows:
                 swaps += check_row(gpu_idx[r], res["idx"][r], fbar, rtol, dom0, f"{label} reuse row {r}")
             continue
+        if window > 0:
+            swaps += _check_window_group(fmt, q, qs, w, k, ks, rows, t0, gs, c, g, topk, window, window_kind,
+                                         gpu_idx, gpu_cand[j], res["cand"][j], fbar, rtol, member_scores,
+                                         f"{label} group {j}")
+            continue
         swaps += check_row(gpu_cand[j], res["cand"][j], fbar, rtol, dom0, f"{label} candidates of group {j}")
         C = gpu_cand[j][gpu_cand[j] >= 0]
         ref2 = oracle.refine_on(fmt, q[rows], None if qs is None else qs[rows], w[rows], k, ks, C, topk)
         for u, r in enumerate(rows):
             swaps += check_row(gpu_idx[r], ref2[u], member_scores(r), rtol,
                                lambda idx, C=C: np.isin(idx, C), f"{label} refine row {r}")
+    return swaps
+
+
+def _check_window_group(fmt, q, qs, w, k, ks, rows, t0, gs, c, g, topk, W, kind, gpu_idx, gcand, ocand, fbar,
+                        rtol, member_scores, label):
+    """One Refine group with App. B's window (see check_pivot)."""
+    import oracle
+
+    wg = W + g - 1
+    per_query = kind == oracle.WINDOW_PER_QUERY
+    npx = c if per_query else c - wg                      # the proxy's slots
+    hi = t0 if per_query else t0 - W                      # the proxy scans [0, hi]
+    gcand = np.asarray(gcand)
+    swaps = 0
+    if npx > 0:
+        swaps += check_row(gcand[:npx], ocand[:npx], fbar, rtol, lambda idx: (idx >= 0) & (idx <= hi),
+                           f"{label} proxy slots")
+    pool = set(gcand[:npx][gcand[:npx] >= 0].tolist())
+    want = []
+    for u in range(wg):
+        p = t0 - W + 1 + u
+        ok = 0 <= p <= t0 + gs - 1 and not (per_query and p in pool)
+        want.append(p if ok else -1)
+    if gcand[npx:npx + wg].tolist() != want:
+        raise ParityError(f"{label}: window slots {gcand[npx:npx + wg].tolist()} != {want}")
+    for t, r in enumerate(rows):
+        tt = t0 + t
+        use = [int(p) for i, p in enumerate(gcand)
+               if 0 <= p <= tt and not (per_query and i >= npx and p < tt - W + 1)]
+        C = np.array(use, dtype=np.int32)
+        ref = oracle.refine_on(fmt, q[[r]], None if qs is None else qs[[r]], w[[r]], k, ks, C, topk)[0]
+        swaps += check_row(gpu_idx[r], ref, member_scores(r), rtol, lambda idx, C=C: np.isin(idx, C),
+                           f"{label} window refine row {r}")
     return swaps

@@ -114,6 +114,60 @@ def test_group_validation(mode, g, c, status):
     assert group(args(), mode, g, c) == status
 
 
+def opts(mode=pv.PIVOT_REFINE, g=4, c=16, db=-1, window=0, kind=pv.PIVOT_WINDOW_SHARED, agg=pv.PIVOT_AGG_MEAN):
+    return pv.group_opts(mode, g, c, db, window, kind, agg)
+
+
+def group_opts(a, o):
+    return pv.lib().pivot_group_index_opts(ctypes.byref(a), ctypes.byref(o))
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(window=-1), pv.PIVOT_ERR_INVALID_ARG),
+    (dict(window=2, mode=pv.PIVOT_REUSE), pv.PIVOT_ERR_INVALID_ARG),              # the window is Refine only
+    (dict(window=14, c=16), pv.PIVOT_ERR_INVALID_ARG),                            # shared: c < W + g - 1
+    (dict(window=3, kind=pv.PIVOT_WINDOW_PER_QUERY), pv.PIVOT_ERR_INVALID_ARG),   # per-query: W < g
+    (dict(window=4, kind=2), pv.PIVOT_ERR_INVALID_ARG),
+    (dict(agg=3), pv.PIVOT_ERR_INVALID_ARG),
+    (dict(agg=-1), pv.PIVOT_ERR_INVALID_ARG),
+    (dict(c=4, window=8, kind=pv.PIVOT_WINDOW_PER_QUERY), pv.PIVOT_ERR_WORKSPACE),  # 4 + 11 >= topk: valid
+    (dict(c=4), pv.PIVOT_ERR_INVALID_ARG),                                         # c < topk, no window
+    (dict(c=8100, window=100, kind=pv.PIVOT_WINDOW_PER_QUERY), pv.PIVOT_ERR_UNSUPPORTED),  # 8203 slots
+    (dict(c=16, window=13), pv.PIVOT_ERR_WORKSPACE),                               # c == W + g - 1: valid
+    (dict(mode=pv.PIVOT_DENSE), pv.PIVOT_ERR_INVALID_ARG),
+])
+def test_group_opts_validation(kw, status):
+    assert group_opts(args(ws_bytes=0), opts(**kw)) == status
+    assert pv.last_error() != ""
+
+
+def test_group_opts_null_and_plain_equivalence():
+    L = pv.lib()
+    assert L.pivot_group_index_opts(ctypes.byref(args()), None) == pv.PIVOT_ERR_INVALID_ARG
+    assert L.pivot_cand_width(None) == 0
+    assert L.pivot_group_workspace_size(None, ctypes.byref(opts())) == 0
+    assert L.pivot_group_workspace_size(ctypes.byref(args()), None) == 0
+    # without window and with the mean, the opts form sizes exactly as pivot_group_index
+    a = args(n_q=100, q_pos0=900)
+    for mode in (pv.PIVOT_REUSE, pv.PIVOT_REFINE):
+        assert pv.pivot_group_workspace_size(a, opts(mode=mode, db=16)) == pv.pivot_workspace_size(a, mode, 4, 16)
+
+
+def test_cand_width_and_window_workspace():
+    assert pv.pivot_cand_width(opts(c=16)) == 16
+    assert pv.pivot_cand_width(opts(c=16, window=5)) == 16                       # shared: inside c
+    assert pv.pivot_cand_width(opts(c=16, window=5, kind=pv.PIVOT_WINDOW_PER_QUERY)) == 16 + 5 + 3
+    up = lambda n: (n + 255) // 256 * 256  # noqa: E731
+    a = args(n_q=100, q_pos0=900)
+    base = pv.pivot_group_workspace_size(a, opts(db=16))
+    per_q = pv.pivot_group_workspace_size(a, opts(db=16, window=5, kind=pv.PIVOT_WINDOW_PER_QUERY))
+    ng, width = 25, 24
+    # the candidate rows and the members' re-scores grow from c to c + W + g - 1 slots
+    assert per_q - base == (up(ng * width * 4) + up(ng * 4 * width * 4)) - (up(ng * 16 * 4) + up(ng * 4 * 16 * 4))
+    assert pv.pivot_group_workspace_size(a, opts(db=16, window=5)) == base
+    assert pv.pivot_group_workspace_size(a, opts(window=3, kind=pv.PIVOT_WINDOW_PER_QUERY)) == 0  # invalid
+
+
 def test_workspace_checks():
     a = args(ws_bytes=0)
     assert dense(a) == pv.PIVOT_ERR_WORKSPACE

@@ -1,0 +1,77 @@
+"""The GPU parity rule itself, on the CPU: the oracle's own Refine results
+with App. B's window pass check_pivot, and planted mistakes in a candidate row
+or a member's set are caught."""
+import numpy as np
+import pytest
+
+import oracle
+from parity import ParityError, check_pivot
+from workload.gen import make_prefill
+
+H, D = 8, 16
+
+
+@pytest.fixture(scope="module")
+def x():
+    return make_prefill(160, "fp8", seed=91, H=H, d=D, threads=2)
+
+
+def _run(x, W, kind, p0=0, g=4, c=24, m=8, db=0):
+    n_q = x.q.shape[0] - p0
+    q, qs, w = x.q[p0:], x.q_scale[p0:], x.w[p0:]
+    n_k = x.q.shape[0]
+    res = oracle.index("fp8", q, qs, w, p0, x.k, x.k_scale, n_k, mode=oracle.REFINE, g=g, c=c, topk=m,
+                       dense_below=db, want_cand=True, window=W, window_kind=kind)
+    return res, (q, qs, w, n_k, g, c, m, db)
+
+
+def _check(x, res, shape, W, kind, idx=None, cand=None):
+    q, qs, w, n_k, g, c, m, db = shape
+    return check_pivot("fp8", q, qs, w, 0, x.k, x.k_scale, n_k, mode=oracle.REFINE, g=g, c=c, topk=m,
+                       dense_below=db, gpu_idx=res["idx"] if idx is None else idx,
+                       gpu_cand=res["cand"] if cand is None else cand, window=W, window_kind=kind)
+
+
+@pytest.mark.parametrize("W,kind", [(6, oracle.WINDOW_SHARED), (5, oracle.WINDOW_PER_QUERY)])
+def test_oracle_passes_its_own_rule(x, W, kind):
+    res, shape = _run(x, W, kind)
+    assert _check(x, res, shape, W, kind) == 0
+
+
+def test_wrong_union_slot_is_caught(x):
+    W, kind = 5, oracle.WINDOW_PER_QUERY
+    res, shape = _run(x, W, kind)
+    cand = res["cand"].copy()
+    j = 20
+    union = cand[j, 24:]
+    u = int(np.flatnonzero(union >= 0)[0])
+    cand[j, 24 + u] = -1                      # a window position dropped
+    with pytest.raises(ParityError, match="window slots"):
+        _check(x, res, shape, W, kind, cand=cand)
+
+
+def test_member_outside_its_window_is_caught(x):
+    """Member 0 of a per-query group may not use the last member's position."""
+    W, kind = 5, oracle.WINDOW_PER_QUERY
+    res, shape = _run(x, W, kind, m=24)
+    j, g = 20, 4
+    t0 = j * g
+    idx = res["idx"].copy()
+    row = idx[j * g]
+    assert (row == t0 + g - 1).sum() == 0
+    row[np.flatnonzero(row >= 0)[0]] = t0 + g - 1
+    with pytest.raises(ParityError):
+        _check(x, res, shape, W, kind, idx=idx)
+
+
+def test_shared_proxy_slot_past_its_range_is_caught(x):
+    """The shared window's proxy slots hold positions <= t0 - W only."""
+    W, kind = 6, oracle.WINDOW_SHARED
+    res, shape = _run(x, W, kind)
+    cand = res["cand"].copy()
+    j, g, c = 30, 4, 24
+    t0 = j * g
+    proxy = cand[j, :c - (W + g - 1)]
+    proxy[np.argmin(proxy)] = t0 - W + 1       # a union position in a proxy slot
+    with pytest.raises(ParityError):
+        _check(x, res, shape, W, kind, cand=cand)
