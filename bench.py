@@ -8,8 +8,9 @@ top-c, and the per-member gather / re-score / top-k.  Inputs are synthetic
 (workload.gen, the 128K prefill recipe) and resident in HBM before timing.
 
 Reported besides the headline queries/s: the dense indexer and PIVOT-Reuse on
-the same prefill (speedup), a group-size sweep, MTP decode (32 x 131072 cached
-keys, g=2), per-kernel times from HIP events recorded around each launch
+the same prefill (speedup), a group-size sweep, Refine with App. B's local
+window (W=4), MTP decode (32 x 131072 cached keys, g=2, also with the
+per-query window), per-kernel times from HIP events recorded around each launch
 inside the timed steps, the roofline fraction of the dominant kernel, and the
 CPU oracle timed on a sample of the same workload.
 
@@ -104,7 +105,7 @@ class Prefill:
         self.ws = torch.empty(need, dtype=torch.uint8, device="cuda")
         log(f"workspace {need / 2**30:.2f} GiB")
 
-    def run(self, mode, g):
+    def run(self, mode, g, window=0):
         pv, wl = self.pv, self.wl
         for p0, n in self.chunks:
             sl = slice(p0, p0 + n)
@@ -112,6 +113,9 @@ class Prefill:
                     None if self.ks is None else self.ks[:p0 + n], p0, p0 + n, wl.topk)
             if mode == "dense":
                 pv.pivot_dense_index(*args, out=self.out[sl], ws=self.ws)
+            elif window:  # App. B's prefill window (Refine)
+                pv.pivot_group_index_opts(*args, mode=pv.PIVOT_REFINE, g=g, c=wl.c, window=window,
+                                          window_kind=pv.PIVOT_WINDOW_SHARED, out=self.out[sl], ws=self.ws)
             else:
                 pv.pivot_group_index(*args, mode=pv.PIVOT_REUSE if mode == "reuse" else pv.PIVOT_REFINE,
                                      g=g, c=wl.c, out=self.out[sl], ws=self.ws)
@@ -141,9 +145,13 @@ def decode_bench(reps):
     pos, nk = [L - g] * B, [L] * B
     out = torch.empty((B, g, wl.topk), dtype=torch.int32, device="cuda")
     res = {}
-    for mode in ("dense", "reuse", "refine"):
+    for mode in ("dense", "reuse", "refine", "refine_W4"):
         if mode == "dense":
             fn = lambda: pv.pivot_dense_index(q, qs, w, k, ks, pos, nk, wl.topk, out=out)  # noqa: E731
+        elif mode == "refine_W4":  # App. B's per-query window, W = 4
+            fn = lambda: pv.pivot_group_index_opts(q, qs, w, k, ks, pos, nk, wl.topk, mode=pv.PIVOT_REFINE,  # noqa
+                                                   g=g, c=wl.c, window=4, window_kind=pv.PIVOT_WINDOW_PER_QUERY,
+                                                   out=out)
         else:
             m = pv.PIVOT_REUSE if mode == "reuse" else pv.PIVOT_REFINE
             fn = lambda m=m: pv.pivot_group_index(q, qs, w, k, ks, pos, nk, wl.topk, mode=m, g=g, c=wl.c,  # noqa
@@ -151,7 +159,7 @@ def decode_bench(reps):
         fn()
         sec = timed(fn, reps)
         res[mode] = {"us_per_step": sec * 1e6, "queries_per_s": B * g / sec}
-    for mode in ("reuse", "refine"):
+    for mode in ("reuse", "refine", "refine_W4"):
         res[mode]["speedup_vs_dense"] = res["dense"]["us_per_step"] / res[mode]["us_per_step"]
     key_bytes = B * L * (128 + 4)
     res["dense"]["key_stream_GBps"] = key_bytes / (res["dense"]["us_per_step"] * 1e-6) / 1e9
@@ -323,6 +331,11 @@ def main():
             modes[f"{mode}_g{gg}"] = {"ms_per_pass": s * 1e3, "queries_per_s": wl.L / s,
                                       "speedup_vs_dense": dense_s / s}
             log(f"{mode} g={gg}: {s * 1e3:.2f} ms ({dense_s / s:.2f}x)")
+    if not args.no_compare:  # App. B's local window at the paper's W = 4
+        s = timed(lambda: pf.run("refine", g, window=4), args.reps)
+        modes[f"refine_g{g}_W4"] = {"ms_per_pass": s * 1e3, "queries_per_s": wl.L / s,
+                                    "speedup_vs_dense": dense_s / s}
+        log(f"refine g={g} W=4: {s * 1e3:.2f} ms ({dense_s / s:.2f}x)")
 
     dec = None if args.no_decode else decode_bench(reps=50)
     cpu = None if args.no_cpu_baseline else cpu_baseline(pf, g)

@@ -281,6 +281,9 @@ hipError_t launch_refine(int dtype, const void* q, const float* q_scale, const f
   else if (c <= 4096)
     hipLaunchKernelGGL(topk_short_kernel<16>, sgrid, dim3(256), 0, stream, rescore, cand, n_q, g, n_groups, st, j0,
                        c, rule, m, out_idx);
+  else if (c <= 5120)  // c = 4096 plus a window union
+    hipLaunchKernelGGL(topk_short_kernel<20>, sgrid, dim3(256), 0, stream, rescore, cand, n_q, g, n_groups, st, j0,
+                       c, rule, m, out_idx);
   else
     hipLaunchKernelGGL(topk_short_kernel<32>, sgrid, dim3(256), 0, stream, rescore, cand, n_q, g, n_groups, st, j0,
                        c, rule, m, out_idx);

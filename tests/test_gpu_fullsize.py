@@ -28,31 +28,36 @@ class Resident:
         self.q, self.qs, self.w = dev(self.x.q), dev(self.x.q_scale), dev(self.x.w)
         self.k, self.ks = dev(self.x.k), dev(self.x.k_scale)
 
-    def run_chunk(self, mode, g, p0, n):
+    def run_chunk(self, mode, g, p0, n, window=0, dense_below=-1):
         wl = self.wl
         sl = slice(p0, p0 + n)
         args = (self.q[sl], None if self.qs is None else self.qs[sl], self.w[sl], self.k[:p0 + n],
                 None if self.ks is None else self.ks[:p0 + n], p0, p0 + n, wl.topk)
-        say(wl.name, mode, "g", g, "chunk", p0, n)
+        say(wl.name, mode, "g", g, "chunk", p0, n, "W", window, "db", dense_below)
         cand = None
         if mode == "dense":
             idx = pv.pivot_dense_index(*args)
         else:
             ng = (n + g - 1) // g
             ct = torch.full((1, ng, wl.c), -7, dtype=torch.int32, device="cuda") if mode == "refine" else None
-            idx = pv.pivot_group_index(*args, mode=pv.PIVOT_REUSE if mode == "reuse" else pv.PIVOT_REFINE,
-                                       g=g, c=wl.c, out_cand=ct)
+            pm = pv.PIVOT_REUSE if mode == "reuse" else pv.PIVOT_REFINE
+            if window:  # App. B's prefill window
+                idx = pv.pivot_group_index_opts(*args, mode=pm, g=g, c=wl.c, dense_below=dense_below,
+                                                window=window, window_kind=pv.PIVOT_WINDOW_SHARED, out_cand=ct)
+            else:
+                idx = pv.pivot_group_index(*args, mode=pm, g=g, c=wl.c, dense_below=dense_below, out_cand=ct)
             cand = None if ct is None else host(ct)[0]
         return host(idx), cand
 
-    def check_chunk(self, mode, g, p0, n, groups, label):
-        idx, cand = self.run_chunk(mode, g, p0, n)
+    def check_chunk(self, mode, g, p0, n, groups, label, window=0, dense_below=-1):
+        idx, cand = self.run_chunk(mode, g, p0, n, window, dense_below)
         x, wl = self.x, self.wl
         sl = slice(p0, p0 + n)
         return check_pivot(x.dtype, x.q[sl], None if x.q_scale is None else x.q_scale[sl], x.w[sl], p0,
                            x.k[:p0 + n], None if x.k_scale is None else x.k_scale[:p0 + n], p0 + n,
                            mode=MODES[mode], g=g if mode != "dense" else 1, c=wl.c, topk=wl.topk,
-                           dense_below=-1, gpu_idx=idx, gpu_cand=cand, groups=groups, label=label)
+                           dense_below=dense_below, gpu_idx=idx, gpu_cand=cand, groups=groups, label=label,
+                           window=window, window_kind=oracle.WINDOW_SHARED)
 
 
 def sample_groups(p0, n, g, c, rng, count=8):
@@ -106,6 +111,21 @@ def test_prefill_128k_fp8_chunks(cfg2, mode, g):
         cfg2.check_chunk(mode, g, p0, wl.chunk, groups, f"128k {mode} g{g} p0 {p0}")
 
 
+@pytest.mark.parametrize("dense_below", [-1, 0])
+def test_prefill_128k_fp8_window(cfg2, dense_below):
+    """App. B's window at the paper's W = 4 (g = 4, c = 4096): the first chunk
+    (with and without the guardrail) and the last chunk."""
+    wl = cfg2.wl
+    g, W = 4, 4
+    rng = np.random.default_rng(21)
+    for p0 in ((0,) if dense_below == 0 else (0, wl.L - wl.chunk)):
+        groups = sample_groups(p0, wl.chunk, g, wl.c, rng, 4)
+        if p0 == 0:
+            groups = sorted(set(groups) | {1, 2})      # proxy ranges [0, t0 - W] empty or short
+        cfg2.check_chunk("refine", g, p0, wl.chunk, groups, f"128k W{W} db{dense_below} p0 {p0}", window=W,
+                         dense_below=dense_below)
+
+
 def test_prefill_128k_fp8_dense(cfg2):
     wl = cfg2.wl
     rng = np.random.default_rng(7)
@@ -135,6 +155,23 @@ def test_decode_32x128k(mode):
         check_pivot("fp8", x.q[b], x.q_scale[b], x.w[b], L - g, x.k[b], x.k_scale[b], L, mode=MODES[mode], g=g,
                     c=wl.c, topk=wl.topk, dense_below=-1, gpu_idx=idx[b],
                     gpu_cand=None if cand is None else cand[b], label=f"decode {mode} b{b}")
+
+
+def test_decode_32x128k_window():
+    """Decode with App. B's per-query window (W = 4 >= g = 2): c + W + g - 1 slots per group."""
+    wl = WORKLOADS["decode-32x128k-fp8"]
+    x = make(wl, threads=16)
+    B, L, g, W = wl.batch, wl.L, wl.g[0], 4
+    say("decode window", B, L, g, W)
+    q, qs, w, k, ks = dev(x.q), dev(x.q_scale), dev(x.w), dev(x.k), dev(x.k_scale)
+    ct = torch.full((B, 1, wl.c + W + g - 1), -7, dtype=torch.int32, device="cuda")
+    idx = pv.pivot_group_index_opts(q, qs, w, k, ks, [L - g] * B, [L] * B, wl.topk, mode=pv.PIVOT_REFINE, g=g,
+                                    c=wl.c, window=W, window_kind=pv.PIVOT_WINDOW_PER_QUERY, out_cand=ct)
+    idx, cand = host(idx), host(ct)
+    for b in (0, 7, 19, 31):
+        check_pivot("fp8", x.q[b], x.q_scale[b], x.w[b], L - g, x.k[b], x.k_scale[b], L, mode=oracle.REFINE, g=g,
+                    c=wl.c, topk=wl.topk, dense_below=-1, gpu_idx=idx[b], gpu_cand=cand[b],
+                    label=f"decode W{W} b{b}", window=W, window_kind=oracle.WINDOW_PER_QUERY)
 
 
 @pytest.fixture(scope="module")
