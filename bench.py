@@ -19,6 +19,7 @@ CPU oracle timed on a sample of the same workload.
 from __future__ import annotations
 
 import argparse
+import gc
 import json
 import math
 import os
@@ -121,14 +122,28 @@ class Prefill:
                                      g=g, c=wl.c, out=self.out[sl], ws=self.ws)
 
 
+class no_gc:
+    """Python's cyclic collector paused around a timed loop: a full collection
+    over the interpreter's heap (torch, the workload's arrays) takes tens of ms
+    on the host and would show up as an idle GPU inside the timed region."""
+
+    def __enter__(self):
+        gc.collect()
+        gc.disable()
+
+    def __exit__(self, *exc):
+        gc.enable()
+
+
 def timed(fn, reps):
     import torch
     torch.cuda.synchronize()
-    t = time.perf_counter()
-    for _ in range(reps):
-        fn()
-    torch.cuda.synchronize()
-    return (time.perf_counter() - t) / reps
+    with no_gc():
+        t = time.perf_counter()
+        for _ in range(reps):
+            fn()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t) / reps
 
 
 def decode_bench(reps):
@@ -277,13 +292,14 @@ def main():
     for _ in range(args.warmup):
         pf.run("refine", g)
     torch.cuda.synchronize()
-    pv.pivot_profile_begin()
-    t = time.perf_counter()
-    for _ in range(args.steps):
-        pf.run("refine", g)
-    torch.cuda.synchronize()
-    step_s = (time.perf_counter() - t) / args.steps
-    prof = pv.pivot_profile_end()
+    with no_gc():
+        pv.pivot_profile_begin()
+        t = time.perf_counter()
+        for _ in range(args.steps):
+            pf.run("refine", g)
+        torch.cuda.synchronize()
+        step_s = (time.perf_counter() - t) / args.steps
+        prof = pv.pivot_profile_end()
     log(f"refine g={g}: {step_s * 1e3:.2f} ms/step; kernels {prof}")
     qps = wl.L / step_s
 

@@ -228,6 +228,19 @@ pivot_status pivot_topk_rows(int32_t n_rows, const float* scores, int64_t ld, in
                              int32_t n_step, int32_t m, int32_t* out, void* stream);
 
 /*
+ * Stage: pivot_topk_rows with a device workspace (256-B aligned, or NULL).
+ * With at least pivot_topk_rows_workspace_size(n_rows) bytes, a call of at
+ * most 256 rows whose longest row has >= 16384 entries splits every row over
+ * several workgroups (the decode shape of the index paths); otherwise it
+ * runs as pivot_topk_rows.  The result is the same either way.
+ * pivot_topk_rows_workspace_size returns 0 for n_rows outside [1, 256].
+ */
+size_t pivot_topk_rows_workspace_size(int32_t n_rows);
+pivot_status pivot_topk_rows_ws(int32_t n_rows, const float* scores, int64_t ld, int64_t n0,
+                                int32_t n_step, int32_t m, int32_t* out, void* workspace,
+                                size_t workspace_bytes, void* stream);
+
+/*
  * Utility: x [n] fp32 -> E4M3FN codes out [n] with the same conversion the
  * proxy kernel uses (round to nearest even).  Dev pointers.
  */

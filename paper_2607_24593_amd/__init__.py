@@ -28,7 +28,8 @@ H, D = 64, 128
 
 EXPORTED = ["pivot_workspace_size", "pivot_dense_index", "pivot_group_index", "pivot_cand_width",
             "pivot_group_workspace_size", "pivot_group_index_opts", "pivot_proxy_rows",
-            "pivot_score_rows", "pivot_topk_rows", "pivot_encode_e4m3", "pivot_profile_begin",
+            "pivot_score_rows", "pivot_topk_rows", "pivot_topk_rows_workspace_size", "pivot_topk_rows_ws",
+            "pivot_encode_e4m3", "pivot_profile_begin",
             "pivot_profile_end", "pivot_status_string", "pivot_last_error", "pivot_version"]
 KERNELS = ["proxy", "score", "select", "refine", "fill", "lin"]
 
@@ -105,6 +106,10 @@ def lib():
         L.pivot_score_rows.argtypes = [I32, I32, I32, I32, P, P, P, P, P, I64, I32, P, I64, P, ctypes.c_size_t, P]
         L.pivot_topk_rows.restype = I32
         L.pivot_topk_rows.argtypes = [I32, P, I64, I64, I32, I32, P, P]
+        L.pivot_topk_rows_workspace_size.restype = ctypes.c_size_t
+        L.pivot_topk_rows_workspace_size.argtypes = [I32]
+        L.pivot_topk_rows_ws.restype = I32
+        L.pivot_topk_rows_ws.argtypes = [I32, P, I64, I64, I32, I32, P, P, ctypes.c_size_t, P]
         L.pivot_encode_e4m3.restype = I32
         L.pivot_encode_e4m3.argtypes = [P, P, I64, P]
         L.pivot_profile_begin.restype = I32
@@ -310,6 +315,23 @@ def pivot_topk_rows(scores, n0, n_step, m, out=None, stream=None):
     out = torch.empty((n, m), dtype=torch.int32, device=scores.device) if out is None else out
     _check(lib().pivot_topk_rows(n, _ptr(scores), ld, int(n0), int(n_step), int(m), _ptr(out), _stream(stream)),
            "pivot_topk_rows")
+    return out
+
+
+def pivot_topk_rows_workspace_size(n_rows: int) -> int:
+    return int(lib().pivot_topk_rows_workspace_size(int(n_rows)))
+
+
+def pivot_topk_rows_ws(scores, n0, n_step, m, out=None, ws=None, stream=None):
+    """pivot_topk_rows with a workspace (few long rows are split over several workgroups)."""
+    n, ld = scores.shape
+    out = torch.empty((n, m), dtype=torch.int32, device=scores.device) if out is None else out
+    need = pivot_topk_rows_workspace_size(n)
+    if ws is None and need > 0:
+        ws = workspace(need, scores.device)
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(lib().pivot_topk_rows_ws(n, _ptr(scores), ld, int(n0), int(n_step), int(m), _ptr(out), _ptr(ws),
+                                    nbytes, _stream(stream)), "pivot_topk_rows_ws")
     return out
 
 

@@ -97,6 +97,7 @@ struct Plan {
   size_t off_pq = 0, off_psc = 0, off_pw = 0, off_cand = 0, off_scores = 0, fixed = 0;
   size_t off_qlin = 0, off_qlsc = 0, off_plin = 0, off_plsc = 0;  // fp8 epilogue's linear term
   size_t off_rsc = 0;                                              // Refine member scores
+  size_t off_sel = 0, sel_bytes = 0;                               // split select scratch
   bool qlin = false, plin = false;
   // App. B window and the proxy aggregation
   int W = 0, wkind = PIVOT_WINDOW_SHARED, agg = PIVOT_AGG_MEAN;
@@ -248,6 +249,12 @@ pivot_status make_plan(const pivot_args* a, int mode, int g, int c, int dense_be
       if (!ext_cand) off = align_up(off + ng * (size_t)p.width * sizeof(int32_t));
     }
   }
+  if (p.max_nk >= kSplitMinKeys) {  // few long rows per select launch (decode) split over workgroups
+    const int64_t rows = (int64_t)p.B * std::max(p.n_q, p.n_groups);
+    p.off_sel = off;
+    p.sel_bytes = split_scratch_bytes(std::min<int64_t>(kSplitMaxRows, rows));
+    off = align_up(off + p.sel_bytes);
+  }
   p.off_scores = off;
   p.fixed = off;
   return PIVOT_OK;
@@ -360,7 +367,9 @@ pivot_status run_rows(const pivot_args* a, const Plan& p, int kind, int lo, int 
       if (s != PIVOT_OK) return s;
       s = hip_check(timed(PIVOT_KERNEL_SELECT, stream,
                           [&] {
-                            return launch_topk(scores, ld, st, rs, od, lim, stream);
+                            return launch_topk(scores, ld, st, rs, od, lim,
+                                               p.sel_bytes ? (uint8_t*)a->workspace + p.off_sel : nullptr,
+                                               p.sel_bytes, stream);
                           }),
                     "top-k kernel");
       if (s != PIVOT_OK) return s;
@@ -682,8 +691,20 @@ pivot_status pivot_score_rows(int32_t dtype, int32_t heads, int32_t dim, int32_t
                    "score kernel");
 }
 
+size_t pivot_topk_rows_workspace_size(int32_t n_rows) {
+  if (n_rows <= 0 || n_rows > kSplitMaxRows) return 0;
+  return split_scratch_bytes(n_rows);
+}
+
 pivot_status pivot_topk_rows(int32_t n_rows, const float* scores, int64_t ld, int64_t n0, int32_t n_step, int32_t m,
                              int32_t* out, void* stream) {
+  return pivot_topk_rows_ws(n_rows, scores, ld, n0, n_step, m, out, nullptr, 0, stream);
+}
+
+pivot_status pivot_topk_rows_ws(int32_t n_rows, const float* scores, int64_t ld, int64_t n0, int32_t n_step,
+                                int32_t m, int32_t* out, void* workspace, size_t workspace_bytes, void* stream) {
+  if (workspace && reinterpret_cast<uintptr_t>(workspace) % kAlign)
+    return fail(PIVOT_ERR_INVALID_ARG, "workspace must be %zu-byte aligned", kAlign);
   if (n_rows < 0 || n0 < 0 || n_step < 0 || m < 1) return fail(PIVOT_ERR_INVALID_ARG, "bad size");
   if (n_rows == 0) return PIVOT_OK;
   if (!scores || !out) return fail(PIVOT_ERR_INVALID_ARG, "null pointer");
@@ -696,7 +717,9 @@ pivot_status pivot_topk_rows(int32_t n_rows, const float* scores, int64_t ld, in
   st.q_pos0[0] = (int32_t)(n0 - 1);
   RowSpace rs{0, n_rows, n_step, kAll};
   OutDesc od{out, m, n_rows, 0, 0, m};
-  return hip_check(launch_topk(scores, ld, st, rs, od, n_max - 1, (hipStream_t)stream), "top-k kernel");
+  return hip_check(launch_topk(scores, ld, st, rs, od, n_max - 1, workspace, workspace ? workspace_bytes : 0,
+                               (hipStream_t)stream),
+                   "top-k kernel");
 }
 
 pivot_status pivot_encode_e4m3(const float* x, uint8_t* out, int64_t n, void* stream) {

@@ -251,21 +251,41 @@ __device__ bool bucket_select(const Src& src, uint32_t need, uint32_t* hist, uin
     }
   });
   __syncthreads();
-  for (int t0 = 0; t0 < (int)in_b; t0 += THREADS) {
-    const int t = t0 + tid;
-    bool take = false;
+  // rank of each listed member = members ranking above it; G threads share a
+  // member (THREADS >= kBucketList >= in_b), each counting over a part of the
+  // list with 8 loads issued before the compares, then summed across lanes
+  constexpr int G = THREADS / kBucketList;
+  static_assert(G >= 1 && (G & (G - 1)) == 0 && G <= 64, "threads per listed member");
+  {
+    const int t = tid / G, part = tid % G;
+    const bool mine = t < (int)in_b;
+    uint32_t key = 0, rank = 0;
     int32_t pos = 0;
-    if (t < (int)in_b) {
-      const uint32_t key = lkey[t];
+    if (mine) {
+      key = lkey[t];
       pos = lpos[t];
-      uint32_t rank = 0;
-      for (int u = 0; u < (int)in_b; ++u) {
+      const int span = ((int)in_b + G - 1) / G;
+      const int u1 = min((int)in_b, (part + 1) * span);
+      int u = part * span;
+      for (; u + 8 <= u1; u += 8) {
+        uint32_t ku[8];
+        int32_t pu[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          ku[j] = lkey[u + j];
+          pu[j] = lpos[u + j];
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) rank += (ku[j] > key) || (ku[j] == key && pu[j] < pos);
+      }
+      for (; u < u1; ++u) {
         const uint32_t ku = lkey[u];
         rank += (ku > key) || (ku == key && lpos[u] < pos);
       }
-      take = rank < rem;
     }
-    wave_append(take, &sh.emitted, [&](int slot) { put(slot, pos); });
+#pragma unroll
+    for (int o = 1; o < G; o <<= 1) rank += __shfl_xor(rank, o, 64);
+    wave_append(mine && part == 0 && rank < rem, &sh.emitted, [&](int slot) { put(slot, pos); });
   }
   __syncthreads();
   return true;

@@ -53,10 +53,15 @@ hipError_t launch_score(int dtype, const void* q, const float* q_scale, const fl
                         int64_t ld, hipStream_t stream);
 
 // Top-m of score rows: row (b, i) has limit + 1 valid entries; lim_max is
-// the largest limit.  Up to 256 long rows (decode) get one 1024-thread
-// workgroup each, more rows one 512-thread workgroup each.
+// the largest limit.  Up to 256 long rows (decode) are split over several
+// workgroups each when `scratch` holds split_scratch_bytes(rows) (else one
+// 1024-thread workgroup each); more rows take one 512-thread workgroup each.
 hipError_t launch_topk(const float* scores, int64_t ld, const SeqTable& st, const RowSpace& rs,
-                       const OutDesc& od, int64_t lim_max, hipStream_t stream);
+                       const OutDesc& od, int64_t lim_max, void* scratch, size_t scratch_bytes,
+                       hipStream_t stream);
+size_t split_scratch_bytes(int64_t rows);
+constexpr int kSplitMaxRows = 256;   // launches with more rows do not split
+constexpr int kSplitMinKeys = 16384; // nor do launches whose rows are all shorter
 
 // Refine (Eqs. 8-9) for groups [j0, j1) with j >= first_proxy[b]: re-score
 // the candidate rows [B, n_groups, c] into rescore [B, n_groups, g, c] fp32,

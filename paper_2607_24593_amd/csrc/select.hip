@@ -15,6 +15,11 @@
 //              they include every key >= the m-th largest of the row, ties
 //              included, so block_select() over them is exact; otherwise the
 //              row takes the two-pass path below.
+// Few long rows (decode) with a scratch buffer: steps 1-2 run in
+// topk_slice_kernel on P workgroups per row (each takes the same sample and
+// threshold and compacts 1/P of the row into scratch), step 3 in
+// topk_merge_kernel, which gathers the row's compacted keys into LDS; one
+// workgroup per row could not pull its row fast enough on its own.
 // Other rows: two_level_select() (block_select.h) over the row in global
 // memory: pass 1 builds a 4096-bin histogram of the top 12 key bits, pass 2
 // emits the keys above the threshold bin and compacts that bin into LDS, where
@@ -30,14 +35,21 @@ namespace pivot {
 
 constexpr int kSelThreads = 512;
 constexpr int kSelThreadsWide = 1024;  // few long rows: one workgroup per row must pull the row alone
-constexpr int kWideMaxRows = 256;      // "few": at most one row per CU
+constexpr int kWideMaxRows = kSplitMaxRows;  // "few": at most one row per CU
 // LDS candidates: 16 KiB histogram + 32 KiB -> three workgroups per CU, or
 // + 62.5 KiB -> two
 constexpr int kSelCapSmall = 4096;
 constexpr int kSelCapLarge = 8000;
-constexpr int kSampleMinLen = 16384;  // shorter rows take the two-pass path
+constexpr int kSampleMinLen = kSplitMinKeys;  // shorter rows take the two-pass path
 constexpr int kChunk4 = 16;           // float4 per sampled chunk (256 bytes)
 constexpr int kSampleChunks = 128;    // at most 8192 sampled scores
+// split select: scratch entries per row over its P slices (each slice may hold
+// twice its even share of the merge capacity), P in [kSplitMinP, kSplitMaxP]
+constexpr int kSplitThreads = 256;
+constexpr int kSplitSlots = 2 * kSelCapLarge;
+constexpr int kSplitMinP = 4, kSplitMaxP = 16;
+constexpr int kSplitPerMax = kSplitSlots / kSplitMinP;
+constexpr int kSplitTargetBlocks = 1024;
 
 // Elements of a score row, visited with 16-byte vector loads (U in flight per
 // thread) when aligned.
@@ -130,11 +142,65 @@ __device__ uint32_t sample_prefix(const Src& src, uint32_t ts, uint32_t* hist, S
   return thr;
 }
 
+// Steps 1 of the one-read path for a long aligned row: false (before any
+// load) when the expected compacted count ts n / s would not leave room for
+// its spread in CAP entries; else the threshold score fthr (every key with
+// prefix >= thr compares >= fthr as a float).  Uniform over the workgroup.
+template <int T, int CAP>
+__device__ bool sample_threshold(const float* row, int n, int m, uint32_t* hist, SelectShared& sel, float& fthr) {
+  constexpr int SV = kSampleChunks * kChunk4 / T;  // sampled float4 per thread
+  const int tid = threadIdx.x;
+  const int nch = n / (4 * kChunk4);
+  const int stride = max(16, (nch + kSampleChunks - 1) / kSampleChunks);
+  const int sch = (nch + stride - 1) / stride;  // chunks 0, stride, 2 stride, ... < nch
+  const int s = sch * 4 * kChunk4;
+  const float rm = (float)s * (float)m / (float)n;
+  const uint32_t ts = (uint32_t)ceilf(rm + 4.0f * sqrtf(rm)) + 1u;
+  if (!(ts < (uint32_t)s && (float)ts * (float)n <= 0.8f * (float)CAP * (float)s)) return false;
+  const float4* r4 = reinterpret_cast<const float4*>(row);
+  SampleSource<SV> smp;
+#pragma unroll
+  for (int v = 0; v < SV; ++v) {
+    const int qi = tid + T * v;
+    smp.ok[v] = qi < sch * kChunk4;
+    const float4 a = smp.ok[v] ? r4[(int64_t)(qi / kChunk4) * stride * kChunk4 + qi % kChunk4]
+                               : make_float4(0.f, 0.f, 0.f, 0.f);
+    smp.key[4 * v] = float_key(a.x);
+    smp.key[4 * v + 1] = float_key(a.y);
+    smp.key[4 * v + 2] = float_key(a.z);
+    smp.key[4 * v + 3] = float_key(a.w);
+  }
+  const uint32_t thr = sample_prefix<T>(smp, ts, hist, sel);
+  // key >> 12 >= thr  <=>  score >= the smallest score with that prefix
+  // (the key map is monotone; -0 and +0 share a key and compare equal)
+  fthr = key_float(thr << 12);
+  return true;
+}
+
+// Where row (b, i)'s indices go (OutDesc).
+struct RowDest {
+  int32_t* base;
+  int64_t dest0;
+  int ndest;
+  int ld;
+  __device__ RowDest(const OutDesc& od, int b, int i) : base(od.base), ld(od.ld) {
+    if (od.fan_g == 0) {
+      dest0 = (int64_t)b * od.per_seq + i;
+      ndest = 1;
+    } else {
+      dest0 = (int64_t)b * od.per_seq + (int64_t)i * od.fan_g;
+      ndest = min(od.fan_g, od.fan_n - i * od.fan_g);
+    }
+  }
+  __device__ __forceinline__ void operator()(int p, int32_t v) const {
+    for (int u = 0; u < ndest; ++u) base[(dest0 + u) * ld + p] = v;
+  }
+};
+
 template <int CAP, int T>
 __global__ __launch_bounds__(T) void topk_rows_kernel(const float* __restrict__ scores, int64_t ld, SeqTable st,
                                                       RowSpace rs, OutDesc od) {
   constexpr int U = T == kSelThreads ? 4 : 8;       // row loads in flight per thread
-  constexpr int SV = kSampleChunks * kChunk4 / T;   // sampled float4 per thread
   __shared__ TwoLevelShared<CAP> sh;
   const int nrows = rs.i1 - rs.i0;
   const int b = blockIdx.x / nrows;
@@ -145,19 +211,7 @@ __global__ __launch_bounds__(T) void topk_rows_kernel(const float* __restrict__ 
   const int n = (int)max((int64_t)0, n64);
   const float* row = scores + ((int64_t)b * nrows + (i - rs.i0)) * ld;
   const int m = od.m;
-
-  int64_t dest0;
-  int ndest;
-  if (od.fan_g == 0) {
-    dest0 = (int64_t)b * od.per_seq + i;
-    ndest = 1;
-  } else {
-    dest0 = (int64_t)b * od.per_seq + (int64_t)i * od.fan_g;
-    ndest = min(od.fan_g, od.fan_n - i * od.fan_g);
-  }
-  auto put = [&](int p, int32_t v) {
-    for (int u = 0; u < ndest; ++u) od.base[(dest0 + u) * od.ld + p] = v;
-  };
+  const RowDest put(od, b, i);
   if (n <= m) {
     for (int p = tid; p < m; p += T) put(p, p < n ? p : -1);
     return;
@@ -165,34 +219,11 @@ __global__ __launch_bounds__(T) void topk_rows_kernel(const float* __restrict__ 
   if (tid == 0) sh.sel.emitted = 0;
   RowSource<T, U> src{row, n};
   const bool aligned = (reinterpret_cast<uintptr_t>(row) & 15u) == 0;
+  float fthr;
   if (n >= kSampleMinLen && aligned) {
-    const int nch = n / (4 * kChunk4);
-    const int stride = max(16, (nch + kSampleChunks - 1) / kSampleChunks);
-    const int sch = (nch + stride - 1) / stride;  // chunks 0, stride, 2 stride, ... < nch
-    const float4* r4 = reinterpret_cast<const float4*>(row);
-    SampleSource<SV> smp;
-#pragma unroll
-    for (int v = 0; v < SV; ++v) {
-      const int qi = tid + T * v;
-      smp.ok[v] = qi < sch * kChunk4;
-      const float4 a = smp.ok[v] ? r4[(int64_t)(qi / kChunk4) * stride * kChunk4 + qi % kChunk4]
-                                 : make_float4(0.f, 0.f, 0.f, 0.f);
-      smp.key[4 * v] = float_key(a.x);
-      smp.key[4 * v + 1] = float_key(a.y);
-      smp.key[4 * v + 2] = float_key(a.z);
-      smp.key[4 * v + 3] = float_key(a.w);
-    }
-    const int s = sch * 4 * kChunk4;
-    const float rm = (float)s * (float)m / (float)n;
-    const uint32_t ts = (uint32_t)ceilf(rm + 4.0f * sqrtf(rm)) + 1u;
-    // expected compacted count ts n / s: leave room for its spread
-    if (ts < (uint32_t)s && (float)ts * (float)n <= 0.8f * (float)CAP * (float)s) {
-      const uint32_t thr = sample_prefix<T>(smp, ts, sh.hist, sh.sel);
+    if (sample_threshold<T, CAP>(row, n, m, sh.hist, sh.sel, fthr)) {
       if (tid == 0) sh.ncand = 0;
       __syncthreads();
-      // key >> 12 >= thr  <=>  score >= the smallest score with that prefix
-      // (the key map is monotone; -0 and +0 share a key and compare equal)
-      const float fthr = key_float(thr << 12);
       src.visit_raw([&](float v, int32_t pos) {
         if (v >= fthr) {  // a few percent of the row: plain LDS atomics
           const int c = atomicAdd(&sh.ncand, 1);
@@ -218,12 +249,180 @@ __global__ __launch_bounds__(T) void topk_rows_kernel(const float* __restrict__ 
   two_level_select<T>(src, (uint32_t)m, sh, put);
 }
 
+// Split select, steps 1-2: workgroup (r, s) of a launch over rows r (as in
+// topk_rows_kernel) takes the row's sample and threshold, compacts the keys
+// >= the threshold among float4s [s per4, (s+1) per4) of the row (the last
+// slice also takes the n mod 4 tail) into LDS, and writes them to
+// cand[(r P + s) per ..] with their count in cnt[r P + s]: -1 when the row
+// takes the two-pass path (n <= m, short or unaligned row, sample declined),
+// -2 when the slice held more than `per` keys.
+template <int CAP>
+__global__ __launch_bounds__(kSplitThreads) void topk_slice_kernel(const float* __restrict__ scores, int64_t ld,
+                                                                   SeqTable st, RowSpace rs, int m, int P, int per,
+                                                                   uint2* __restrict__ cand,
+                                                                   int32_t* __restrict__ cnt) {
+  constexpr int T = kSplitThreads, U = 8;
+  __shared__ uint32_t hist[4096];
+  __shared__ SelectShared sel;
+  __shared__ uint2 lc[kSplitPerMax];
+  __shared__ int32_t nc;
+  const int nrows = rs.i1 - rs.i0;
+  const int r = blockIdx.x, slice = blockIdx.y;
+  const int b = r / nrows;
+  const int i = rs.i0 + r % nrows;
+  if (!row_active(st, rs, b, i)) return;
+  const int tid = threadIdx.x;
+  const int n = (int)max((int64_t)0, row_limit(st, rs, b, i) + 1);
+  const float* row = scores + ((int64_t)b * nrows + (i - rs.i0)) * ld;
+  int32_t* my_cnt = cnt + (int64_t)r * P + slice;
+  const bool aligned = (reinterpret_cast<uintptr_t>(row) & 15u) == 0;
+  float fthr;
+  if (n <= m || n < kSampleMinLen || !aligned || !sample_threshold<T, CAP>(row, n, m, hist, sel, fthr)) {
+    if (tid == 0) *my_cnt = -1;
+    return;
+  }
+  if (tid == 0) nc = 0;
+  __syncthreads();
+  auto take = [&](float v, int pos) {
+    if (v >= fthr) {
+      const int c = atomicAdd(&nc, 1);
+      if (c < per) lc[c] = make_uint2(float_key(v), (uint32_t)pos);
+    }
+  };
+  const int n4 = n >> 2;
+  const int per4 = (n4 + P - 1) / P;
+  const int a4 = slice * per4, e4 = min(n4, a4 + per4);
+  const float4* r4 = reinterpret_cast<const float4*>(row);
+  int q = a4 + tid;
+  for (; q + (U - 1) * T < e4; q += U * T) {
+    float4 x[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) x[u] = r4[q + u * T];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int p = 4 * (q + u * T);
+      take(x[u].x, p); take(x[u].y, p + 1); take(x[u].z, p + 2); take(x[u].w, p + 3);
+    }
+  }
+  for (; q < e4; q += T) {
+    const float4 x = r4[q];
+    take(x.x, 4 * q); take(x.y, 4 * q + 1); take(x.z, 4 * q + 2); take(x.w, 4 * q + 3);
+  }
+  if (slice == P - 1)
+    for (int e = 4 * n4 + tid; e < n; e += T) take(row[e], e);
+  __syncthreads();
+  const int c = nc;
+  if (tid == 0) *my_cnt = c <= per ? c : -2;
+  if (c <= per) {
+    uint2* dst = cand + ((int64_t)r * P + slice) * per;
+    for (int e = tid; e < c; e += T) dst[e] = lc[e];
+  }
+}
+
+// Split select, step 3: one workgroup per row gathers the keys its slices
+// compacted (when every slice kept its keys and they number m .. CAP) into
+// LDS and selects exactly over them; any other row takes the two-pass path.
+template <int CAP, int T>
+__global__ __launch_bounds__(T) void topk_merge_kernel(const float* __restrict__ scores, int64_t ld, SeqTable st,
+                                                       RowSpace rs, OutDesc od, int P, int per,
+                                                       const uint2* __restrict__ cand,
+                                                       const int32_t* __restrict__ cnt) {
+  constexpr int U = 8;
+  constexpr int V = (CAP + T - 1) / T;  // gathered keys per thread
+  __shared__ TwoLevelShared<CAP> sh;
+  __shared__ int32_t pre[kSplitMaxP + 1];
+  const int nrows = rs.i1 - rs.i0;
+  const int r = blockIdx.x;
+  const int b = r / nrows;
+  const int i = rs.i0 + r % nrows;
+  if (!row_active(st, rs, b, i)) return;
+  const int tid = threadIdx.x;
+  const int n = (int)max((int64_t)0, row_limit(st, rs, b, i) + 1);
+  const float* row = scores + ((int64_t)b * nrows + (i - rs.i0)) * ld;
+  const int m = od.m;
+  const RowDest put(od, b, i);
+  if (n <= m) {
+    for (int p = tid; p < m; p += T) put(p, p < n ? p : -1);
+    return;
+  }
+  if (tid == 0) {
+    sh.sel.emitted = 0;
+    int tot = 0;
+    bool ok = true;
+    for (int s = 0; s < P; ++s) {
+      const int c = cnt[(int64_t)r * P + s];
+      pre[s] = tot;
+      ok = ok && c >= 0;
+      tot += c >= 0 ? c : 0;
+    }
+    pre[P] = ok ? tot : -1;
+  }
+  __syncthreads();
+  const int total = pre[P];
+  if (total >= m && total <= CAP) {
+    // every thread fetches its (at most V) keys at once, then stores them
+    uint2 v[V];
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+      const int e = tid + j * T;
+      v[j] = make_uint2(0u, 0u);
+      if (e < total) {
+        int s = 0;
+        while (s + 1 < P && pre[s + 1] <= e) ++s;
+        v[j] = cand[((int64_t)r * P + s) * per + (e - pre[s])];
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+      const int e = tid + j * T;
+      if (e < total) {
+        sh.ckey[e] = v[j].x;
+        sh.cpos[e] = (int32_t)v[j].y;
+      }
+    }
+    __syncthreads();
+    ArraySource<T> src{sh.ckey, sh.cpos, total};
+    if (!bucket_select<T>(src, (uint32_t)m, sh.hist, sh.hist, reinterpret_cast<int32_t*>(sh.hist + kBucketList),
+                          &sh.lcount, sh.sel, put))
+      block_select<T, false>(src, (uint32_t)m, sh.sel, put);
+    return;
+  }
+  RowSource<T, U> src{row, n};
+  two_level_select<T>(src, (uint32_t)m, sh, put);
+}
+
+size_t split_scratch_bytes(int64_t rows) {
+  return (size_t)rows * ((size_t)kSplitSlots * sizeof(uint2) + (size_t)kSplitMaxP * sizeof(int32_t));
+}
+
 hipError_t launch_topk(const float* scores, int64_t ld, const SeqTable& st, const RowSpace& rs,
-                       const OutDesc& od, int64_t lim_max, hipStream_t stream) {
+                       const OutDesc& od, int64_t lim_max, void* scratch, size_t scratch_bytes,
+                       hipStream_t stream) {
   const int nrows = rs.i1 - rs.i0;
   if (nrows <= 0 || st.n <= 0) return hipSuccess;
   const int64_t blocks = (int64_t)st.n * nrows;
   if (blocks > 0x7FFFFFFF) return hipErrorInvalidConfiguration;
+  if (blocks <= kWideMaxRows && lim_max + 1 >= kSampleMinLen && scratch &&
+      scratch_bytes >= split_scratch_bytes(blocks)) {
+    // few long rows: P slice workgroups per row, then one merge workgroup
+    const int P = (int)std::max<int64_t>(kSplitMinP, std::min<int64_t>(kSplitMaxP, kSplitTargetBlocks / blocks));
+    const int per = kSplitSlots / P;
+    uint2* cand = reinterpret_cast<uint2*>(scratch);
+    int32_t* cnt = reinterpret_cast<int32_t*>(cand + (size_t)blocks * kSplitSlots);
+    const dim3 sgrid((unsigned)blocks, (unsigned)P);
+    if (od.m <= kSelCapSmall / 2) {
+      hipLaunchKernelGGL((topk_slice_kernel<kSelCapSmall>), sgrid, dim3(kSplitThreads), 0, stream, scores, ld, st, rs,
+                         od.m, P, per, cand, cnt);
+      hipLaunchKernelGGL((topk_merge_kernel<kSelCapSmall, kSelThreadsWide>), dim3((unsigned)blocks),
+                         dim3(kSelThreadsWide), 0, stream, scores, ld, st, rs, od, P, per, cand, cnt);
+    } else {
+      hipLaunchKernelGGL((topk_slice_kernel<kSelCapLarge>), sgrid, dim3(kSplitThreads), 0, stream, scores, ld, st, rs,
+                         od.m, P, per, cand, cnt);
+      hipLaunchKernelGGL((topk_merge_kernel<kSelCapLarge, kSelThreadsWide>), dim3((unsigned)blocks),
+                         dim3(kSelThreadsWide), 0, stream, scores, ld, st, rs, od, P, per, cand, cnt);
+    }
+    return hipGetLastError();
+  }
   if (blocks <= kWideMaxRows && lim_max + 1 >= kSampleMinLen) {
     // few long rows (decode): one wide workgroup per row
     if (od.m <= kSelCapSmall / 2)

@@ -206,9 +206,14 @@ def test_workspace_size_closed_form():
         lin(100) + lin(ng) + proxies + cand + ng * ld(1000) * 4
     # Reuse: no candidate buffer, no member rows to re-score
     assert pv.pivot_workspace_size(a, pv.PIVOT_REUSE, 4, 16) == lin(ng) + proxies + ng * ld(1000) * 4
-    # long prefix: score tiles stay near 1 GiB
+    # long prefix: score tiles stay near 1 GiB, plus the split select's scratch
+    # for up to 256 long rows (16000 (key, position) pairs and 16 counts each)
+    split = lambda rows: rows * (16000 * 8 + 16 * 4)  # noqa: E731
     a = args(n_q=16384, q_pos0=262144 - 16384)
-    assert pv.pivot_workspace_size(a, pv.PIVOT_DENSE) == lin(16384) + (1 << 30)
+    assert pv.pivot_workspace_size(a, pv.PIVOT_DENSE) == lin(16384) + split(256) + (1 << 30)
+    assert pv.pivot_topk_rows_workspace_size(32) == split(32)
+    assert pv.pivot_topk_rows_workspace_size(256) == split(256)
+    assert pv.pivot_topk_rows_workspace_size(257) == 0 and pv.pivot_topk_rows_workspace_size(0) == 0
 
 
 def test_stage_validation():
@@ -224,6 +229,9 @@ def test_stage_validation():
         pv.PIVOT_ERR_WORKSPACE
     assert L.pivot_topk_rows(2, FAKE, 10, 8, 4, 4, FAKE, None) == pv.PIVOT_ERR_INVALID_ARG  # 12 > ld
     assert L.pivot_topk_rows(0, None, 0, 0, 0, 4, None, None) == pv.PIVOT_OK
+    assert L.pivot_topk_rows_ws(2, FAKE, 64, 8, 4, 4, FAKE, FAKE + 4, 1 << 20, None) == \
+        pv.PIVOT_ERR_INVALID_ARG                               # misaligned workspace
+    assert L.pivot_topk_rows_ws(2, FAKE, 10, 8, 4, 4, FAKE, FAKE, 1 << 20, None) == pv.PIVOT_ERR_INVALID_ARG
     assert L.pivot_proxy_rows(1, 64, 128, 8, 0, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == \
         pv.PIVOT_ERR_INVALID_ARG
     assert L.pivot_encode_e4m3(None, None, 0, None) == pv.PIVOT_OK

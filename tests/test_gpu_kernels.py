@@ -67,13 +67,17 @@ def _expect_topk(row, n, m):
     return oracle.topk(row[:n].astype(np.float64), np.arange(n, dtype=np.int32), m)
 
 
+@pytest.mark.parametrize("split", [False, True])
 @pytest.mark.parametrize("case", ["normal", "ties", "signed_zeros", "short", "exact", "long2k", "long4k",
                                   "ragged", "constant", "sample_miss", "sample_ragged", "heavy_tail", "small_m",
-                                  "unaligned", "m4k_normal"])
-def test_topk_rows_exact(case):
+                                  "unaligned", "m4k_normal", "slice_skew", "decode_shape"])
+def test_topk_rows_exact(case, split):
     """Rows of 16384+ scores with m <= 2048 take the sampled one-pass path; the
     sample_miss rows put the sample's largest keys where the rest of the row is
-    low, so the pass finds fewer than m keys and falls back to two passes."""
+    low, so the pass finds fewer than m keys and falls back to two passes.
+    split: with a workspace, calls of at most 256 rows split each long row over
+    several workgroups; slice_skew puts every high score in the first slice,
+    which overflows its share of the scratch and falls back."""
     rng = np.random.default_rng(zlib.crc32(case.encode()))
     n0, step, m = 5000, 0, 100
     if case == "normal":
@@ -106,11 +110,19 @@ def test_topk_rows_exact(case):
         rows = rng.standard_normal((4, 40001)); n0, step, m = 39990, 3, 1000
     elif case == "m4k_normal":
         rows = rng.standard_normal((3, 70000)); n0, m = 70000, 4096
+    elif case == "slice_skew":
+        rows = rng.standard_normal((2, 131072)) * 0.1
+        rows[:, :4096] += 5.0; n0, m = 131072, 2048
+    elif case == "decode_shape":
+        rows = rng.standard_normal((32, 131071)); n0, m = 131071, 4096
     else:
         rows = np.full((2, 20000), 3.5); n0, m = 20000, 700
     rows = rows.astype(np.float32)
-    say("topk_rows", case, rows.shape, n0, step, m)
-    got = host(pv.pivot_topk_rows(dev(rows), n0, step, m))
+    say("topk_rows", case, rows.shape, n0, step, m, "split" if split else "")
+    if split:
+        got = host(pv.pivot_topk_rows_ws(dev(rows), n0, step, m))
+    else:
+        got = host(pv.pivot_topk_rows(dev(rows), n0, step, m))
     for r in range(rows.shape[0]):
         n = n0 + r * step
         exp = _expect_topk(rows[r], n, m)
