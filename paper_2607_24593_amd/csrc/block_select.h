@@ -206,18 +206,21 @@ __device__ void block_select(const Src& src, uint32_t need, SelectShared& sh, Pu
 }
 
 // Fast exact top-`need` of a source whose keys spread over a range of values
-// (a candidate set): one reduction for the key range, one pass over a
-// 4096-bin histogram of the value bucketed linearly over that range (a
+// (a candidate set): one reduction for the key range, one pass over an
+// NB-bin histogram of the value bucketed linearly over that range (a
 // monotone map), and one pass that emits every element of the buckets above
 // the one holding the need-th element and lists that bucket's members in
 // LDS; each listed member then counts the members ranking above it (key
 // descending, position ascending).  Returns false, having emitted nothing,
 // when the keys are all equal or the bucket holds more than kBucketList
-// elements; the caller then uses block_select().
-// hist: 4096 LDS words; lkey / lpos: kBucketList LDS entries; lcount: an LDS word.
+// elements; the caller then uses block_select().  NB: about one bin per
+// element keeps the bucket short for long-tailed sets.
+// hist: NB LDS words; lkey / lpos: kBucketList LDS entries (they may alias
+// hist: the histogram is dead by the time the list is written); lcount: an
+// LDS word.
 constexpr int kBucketList = 256;
 
-template <int THREADS, class Src, class Put>
+template <int THREADS, int NB = 4096, class Src, class Put>
 __device__ bool bucket_select(const Src& src, uint32_t need, uint32_t* hist, uint32_t* lkey, int32_t* lpos,
                               int32_t* lcount, SelectShared& sh, Put put) {
   const int tid = threadIdx.x;
@@ -227,16 +230,17 @@ __device__ bool bucket_select(const Src& src, uint32_t need, uint32_t* hist, uin
     kmax = max(kmax, key);
   });
   block_pair_reduce<THREADS, true>(kmin, kmax, sh);
+  static_assert(NB % THREADS == 0 || NB < THREADS, "bins per thread");
   const float fmin = key_float(kmin);
-  const float scale = 4096.0f / (key_float(kmax) - fmin);
+  const float scale = (float)NB / (key_float(kmax) - fmin);
   if (kmin == kmax || !(scale > 0.0f && scale < __builtin_inff())) return false;
-  auto bucket = [&](uint32_t key) { return min(4095, (int)((key_float(key) - fmin) * scale)); };
-  for (int k = tid; k < 4096; k += THREADS) hist[k] = 0;
+  auto bucket = [&](uint32_t key) { return min(NB - 1, (int)((key_float(key) - fmin) * scale)); };
+  for (int k = tid; k < NB; k += THREADS) hist[k] = 0;
   if (tid == 0) *lcount = 0;
   __syncthreads();
   src.visit([&](uint32_t key, int32_t) { atomicAdd(&hist[bucket(key)], 1u); });
   __syncthreads();
-  find_digit<THREADS, true>(hist, sh, need, 4096);
+  find_digit<THREADS, true>(hist, sh, need, NB);
   const int bsel = (int)sh.digit;
   const uint32_t rem = need - sh.before, in_b = sh.equal;
   __syncthreads();
@@ -244,7 +248,7 @@ __device__ bool bucket_select(const Src& src, uint32_t need, uint32_t* hist, uin
   src.visit([&](uint32_t key, int32_t pos) {
     const int bk = bucket(key);
     wave_append(bk > bsel, &sh.emitted, [&](int slot) { put(slot, pos); });
-    if (bk == bsel) {
+    if (bk == bsel) {  // a few elements: a plain LDS atomic
       const int c = atomicAdd(lcount, 1);
       lkey[c] = key;
       lpos[c] = pos;

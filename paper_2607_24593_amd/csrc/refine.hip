@@ -120,9 +120,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void r
   }
 }
 
-// (key, position) pairs e = tid + 256 v held in registers.
+// (key, position) pairs held in registers: entry 4 q + u is element
+// 4 (tid + 256 q) + u of the row (loaded four at a time).
 template <int V>
 struct RegSource {
+  static_assert(V % 4 == 0, "quads of elements");
   uint32_t key[V];
   int32_t pos[V];  // -1: not a candidate of this member
   template <class F>
@@ -147,7 +149,7 @@ __global__ __launch_bounds__(256) void topk_short_kernel(const float* __restrict
                                                          int n_groups, SeqTable st, int j0, int c, SlotRule rule,
                                                          int m, int32_t* __restrict__ out_idx) {
   __shared__ SelectShared sel;
-  __shared__ uint32_t hist[4096];
+  __shared__ uint32_t hist[4 * 256];  // bucket_select's histogram, then its list
   __shared__ int32_t lcount, nvalid_sh;
   const int j = j0 + blockIdx.x, b = blockIdx.y, member = blockIdx.z;
   if (b >= st.n || j >= n_groups || j < st.first_proxy[b]) return;
@@ -165,16 +167,39 @@ __global__ __launch_bounds__(256) void topk_short_kernel(const float* __restrict
 
   RegSource<V> src;
   int mine = 0;
+  // quads of scores and positions with 16-byte loads when the rows allow it
+  const bool vec = (c & 3) == 0 && ((reinterpret_cast<uintptr_t>(srow) | reinterpret_cast<uintptr_t>(crow)) & 15u) == 0;
 #pragma unroll
-  for (int v = 0; v < V; ++v) {
-    const int e = tid + 256 * v;
-    const bool in = e < nc;
-    const int32_t p = in ? crow[e] : -1;
-    bool ok = in;
-    if (win) ok = p >= 0 && p <= tt && !(e >= rule.wslot && p < tt - rule.window + 1);
-    src.key[v] = in ? float_key(srow[e]) : 0u;
-    src.pos[v] = ok ? p : -1;
-    mine += ok;
+  for (int q4 = 0; q4 < V / 4; ++q4) {
+    const int e0 = 4 * (tid + 256 * q4);
+    float kv[4] = {0.f, 0.f, 0.f, 0.f};
+    int32_t pv[4] = {-1, -1, -1, -1};
+    if (vec) {
+      if (e0 < nc) {  // c is a multiple of 4: the quad lies inside the row
+        const float4 a = *reinterpret_cast<const float4*>(srow + e0);
+        const int4 q = *reinterpret_cast<const int4*>(crow + e0);
+        kv[0] = a.x; kv[1] = a.y; kv[2] = a.z; kv[3] = a.w;
+        pv[0] = q.x; pv[1] = q.y; pv[2] = q.z; pv[3] = q.w;
+      }
+    } else {
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (e0 + u < nc) {
+          kv[u] = srow[e0 + u];
+          pv[u] = crow[e0 + u];
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int e = e0 + u;
+      const bool in = e < nc;
+      const int32_t p = in ? pv[u] : -1;
+      bool ok = in;
+      if (win) ok = p >= 0 && p <= tt && !(e >= rule.wslot && p < tt - rule.window + 1);
+      src.key[4 * q4 + u] = in ? float_key(kv[u]) : 0u;
+      src.pos[4 * q4 + u] = ok ? p : -1;
+      mine += ok;
+    }
   }
   if (!win) {
     if (nc <= m) {  // every candidate is selected
@@ -202,8 +227,8 @@ __global__ __launch_bounds__(256) void topk_short_kernel(const float* __restrict
   if (tid == 0) sel.emitted = 0;
   __syncthreads();
   auto put = [&](int slot, int32_t p) { orow[slot] = p; };
-  if (!bucket_select<256>(src, (uint32_t)m, hist, hist, reinterpret_cast<int32_t*>(hist + kBucketList), &lcount, sel,
-                          put))
+  if (!bucket_select<256, 1024>(src, (uint32_t)m, hist, hist, reinterpret_cast<int32_t*>(hist + kBucketList), &lcount,
+                                sel, put))
     block_select<256, true>(src, (uint32_t)m, sel, put);
 }
 
