@@ -192,6 +192,45 @@ size_t pivot_group_workspace_size(const pivot_args* a, const pivot_group_opts* o
 pivot_status pivot_group_index_opts(const pivot_args* a, const pivot_group_opts* o);
 
 /*
+ * Batch layouts beyond the padded, contiguous one of pivot_args: packed
+ * variable-length query runs (one per request of a batch) and a paged key
+ * cache.  A NULL layout, or one whose two pointers are NULL, is pivot_args'
+ * own layout.
+ *   cu_q (host [B+1], or NULL): sequence b owns query rows cu_q[b] ..
+ *     cu_q[b+1]-1 of the packed q / q_scale / w / out_idx (cu_q[0] = 0,
+ *     nondecreasing); a->n_q is ignored.  Groups restart at every sequence's
+ *     first query, so no group spans two requests (Sec. 4.1); candidate rows
+ *     (out_cand) are packed the same way, sum over b of ceil(n_b / g) rows.
+ *   block_table (dev int32 [B, max_pages], or NULL): key s < n_k[b] of
+ *     sequence b is row block_table[b * max_pages + s / page_size] *
+ *     page_size + s % page_size of k / k_scale, a pool of pool_keys rows;
+ *     a->k_seq_stride is ignored.  Entries outside [0, pool_keys / page_size)
+ *     are clamped into it (the result is then meaningless, but no access
+ *     leaves the pool).  page_size is a power of two in [16, 65536];
+ *     pool_keys is a multiple of page_size with pool_keys * bytes-per-key
+ *     at most 2^31 (128 B per fp8 key, 256 B per bf16 key); n_k[b] <=
+ *     max_pages * page_size.
+ * Invalid layouts return PIVOT_ERR_INVALID_ARG (PIVOT_ERR_UNSUPPORTED for a
+ * pool past the 2^31-byte limit).  The layout is read, never kept.
+ */
+typedef struct {
+  const int32_t* cu_q;
+  const int32_t* block_table;
+  int32_t max_pages;
+  int32_t page_size;
+  int64_t pool_keys;
+} pivot_layout;
+
+/*
+ * pivot_dense_index and pivot_group_index_opts with a layout.  The workspace
+ * size for such a call is pivot_workspace_size_layout(a, l, o) with o the
+ * options, or NULL for the dense index.
+ */
+pivot_status pivot_dense_index_layout(const pivot_args* a, const pivot_layout* l);
+pivot_status pivot_group_index_layout(const pivot_args* a, const pivot_layout* l, const pivot_group_opts* o);
+size_t pivot_workspace_size_layout(const pivot_args* a, const pivot_layout* l, const pivot_group_opts* o);
+
+/*
  * Stage: proxy rows of Eq. 4 for one sequence's queries q [n_q, H, d] /
  * q_scale [n_q] / w [n_q, H] split into runs of g (last may be shorter).
  * Writes out_q [ceil(n_q/g), H, d] (same format as q), out_scale

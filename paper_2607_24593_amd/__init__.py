@@ -27,7 +27,8 @@ PIVOT_AGG_MEAN, PIVOT_AGG_FIRST, PIVOT_AGG_LAST = 0, 1, 2
 H, D = 64, 128
 
 EXPORTED = ["pivot_workspace_size", "pivot_dense_index", "pivot_group_index", "pivot_cand_width",
-            "pivot_group_workspace_size", "pivot_group_index_opts", "pivot_proxy_rows",
+            "pivot_group_workspace_size", "pivot_group_index_opts", "pivot_dense_index_layout",
+            "pivot_group_index_layout", "pivot_workspace_size_layout", "pivot_proxy_rows",
             "pivot_score_rows", "pivot_topk_rows", "pivot_topk_rows_workspace_size", "pivot_topk_rows_ws",
             "pivot_encode_e4m3", "pivot_profile_begin",
             "pivot_profile_end", "pivot_status_string", "pivot_last_error", "pivot_version"]
@@ -65,6 +66,31 @@ class pivot_group_opts(ctypes.Structure):
     ]
 
 
+class pivot_layout(ctypes.Structure):
+    _fields_ = [
+        ("cu_q", ctypes.POINTER(ctypes.c_int32)), ("block_table", ctypes.c_void_p),
+        ("max_pages", ctypes.c_int32), ("page_size", ctypes.c_int32), ("pool_keys", ctypes.c_int64),
+    ]
+
+
+def make_layout(cu_q=None, block_table=None, page_size=0, pool_keys=0) -> pivot_layout:
+    """cu_q: host ints [B+1] (packed query runs) or None; block_table: dev int32
+    [B, max_pages] (paged keys) or None."""
+    lo = pivot_layout()
+    if cu_q is not None:
+        lo._cu = (ctypes.c_int32 * len(cu_q))(*[int(v) for v in cu_q])
+        lo.cu_q = ctypes.cast(lo._cu, ctypes.POINTER(ctypes.c_int32))
+    if block_table is not None:
+        if block_table.dtype != torch.int32 or block_table.dim() != 2 or not block_table.is_contiguous():
+            raise ValueError("block_table must be a contiguous int32 [B, max_pages] tensor")
+        lo.block_table = _ptr(block_table)
+        lo.max_pages = block_table.shape[1]
+        lo.page_size = int(page_size)
+        lo.pool_keys = int(pool_keys)
+        lo._bt = block_table
+    return lo
+
+
 def group_opts(mode, g, c, dense_below=-1, window=0, window_kind=PIVOT_WINDOW_SHARED,
                aggregate=PIVOT_AGG_MEAN, out_cand=None) -> pivot_group_opts:
     o = pivot_group_opts()
@@ -100,6 +126,13 @@ def lib():
         L.pivot_group_workspace_size.argtypes = [A, O]
         L.pivot_group_index_opts.restype = I32
         L.pivot_group_index_opts.argtypes = [A, O]
+        Lo = ctypes.POINTER(pivot_layout)
+        L.pivot_dense_index_layout.restype = I32
+        L.pivot_dense_index_layout.argtypes = [A, Lo]
+        L.pivot_group_index_layout.restype = I32
+        L.pivot_group_index_layout.argtypes = [A, Lo, O]
+        L.pivot_workspace_size_layout.restype = ctypes.c_size_t
+        L.pivot_workspace_size_layout.argtypes = [A, Lo, O]
         L.pivot_proxy_rows.restype = I32
         L.pivot_proxy_rows.argtypes = [I32, I32, I32, I32, I32, P, P, P, P, P, P, P]
         L.pivot_score_rows.restype = I32
@@ -275,6 +308,70 @@ def pivot_group_index_opts(q, q_scale, w, k, k_scale, q_pos0, n_k, topk, mode, g
         a.workspace_bytes = buf.numel() * buf.element_size()
         a._ws = buf
     _check(lib().pivot_group_index_opts(ctypes.byref(a), ctypes.byref(o)), "pivot_group_index_opts")
+    return out
+
+
+def make_args_batch(q, q_scale, w, k, k_scale, q_pos0, n_k, topk, out_idx, stream=None):
+    """pivot_args for packed query rows q [rows, H, d] / w [rows, H] of len(q_pos0)
+    sequences (their runs given by a layout's cu_q) and keys k: a page pool
+    [keys, d] (with a layout's block_table), or contiguous sequences [B, S, d]."""
+    for t in (q, w, k, out_idx) + tuple(x for x in (q_scale, k_scale) if x is not None):
+        if not t.is_contiguous():
+            raise ValueError("tensors must be contiguous")
+    B = len(q_pos0)
+    a = pivot_args()
+    a.dtype = _dtype_code(q)
+    a.heads, a.dim = q.shape[1], q.shape[2]
+    a.batch, a.n_q = B, 0
+    a._pos = (ctypes.c_int32 * B)(*[int(v) for v in q_pos0])
+    a._nk = (ctypes.c_int32 * B)(*[int(v) for v in n_k])
+    a.q_pos0 = ctypes.cast(a._pos, ctypes.POINTER(ctypes.c_int32))
+    a.n_k = ctypes.cast(a._nk, ctypes.POINTER(ctypes.c_int32))
+    a.q, a.q_scale, a.w = _ptr(q), _ptr(q_scale), _ptr(w)
+    a.k, a.k_scale = _ptr(k), _ptr(k_scale)
+    a.k_seq_stride = k.shape[1] if k.dim() == 3 else k.shape[0]  # [B, S, d]: contiguous sequences of S keys
+    a.topk = int(topk)
+    a.out_idx = _ptr(out_idx)
+    a.stream = _stream(stream)
+    a._keep = (q, q_scale, w, k, k_scale, out_idx)
+    return a
+
+
+def pivot_workspace_size_layout(a: pivot_args, lo: pivot_layout, o=None) -> int:
+    return int(lib().pivot_workspace_size_layout(ctypes.byref(a), ctypes.byref(lo),
+                                                 None if o is None else ctypes.byref(o)))
+
+
+def _attach(a, need, ws, device):
+    if need > 0:
+        buf = ws if ws is not None else workspace(need, device)
+        a.workspace = _ptr(buf)
+        a.workspace_bytes = buf.numel() * buf.element_size()
+        a._ws = buf
+
+
+def pivot_dense_index_layout(q, q_scale, w, k, k_scale, q_pos0, n_k, topk, layout, out=None, ws=None,
+                             stream=None):
+    """Dense index of packed query runs (layout.cu_q) over contiguous or paged keys:
+    returns int32 [rows, topk]."""
+    out = torch.empty((q.shape[0], topk), dtype=torch.int32, device=q.device) if out is None else out
+    a = make_args_batch(q, q_scale, w, k, k_scale, q_pos0, n_k, topk, out, stream=stream)
+    _attach(a, pivot_workspace_size_layout(a, layout), ws, q.device)
+    _check(lib().pivot_dense_index_layout(ctypes.byref(a), ctypes.byref(layout)), "pivot_dense_index_layout")
+    return out
+
+
+def pivot_group_index_layout(q, q_scale, w, k, k_scale, q_pos0, n_k, topk, layout, mode, g, c, dense_below=-1,
+                             window=0, window_kind=PIVOT_WINDOW_SHARED, aggregate=PIVOT_AGG_MEAN, out=None,
+                             out_cand=None, ws=None, stream=None):
+    """PIVOT over packed query runs (groups restart at every run) and contiguous or
+    paged keys: returns int32 [rows, topk]."""
+    out = torch.empty((q.shape[0], topk), dtype=torch.int32, device=q.device) if out is None else out
+    a = make_args_batch(q, q_scale, w, k, k_scale, q_pos0, n_k, topk, out, stream=stream)
+    o = group_opts(mode, g, c, dense_below, window, window_kind, aggregate, out_cand)
+    _attach(a, pivot_workspace_size_layout(a, layout, o), ws, q.device)
+    _check(lib().pivot_group_index_layout(ctypes.byref(a), ctypes.byref(layout), ctypes.byref(o)),
+           "pivot_group_index_layout")
     return out
 
 

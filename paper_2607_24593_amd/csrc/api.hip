@@ -81,18 +81,26 @@ int64_t ld_for(int64_t n) {
 }
 int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
-// The group plan: for each sequence, how many leading query rows take the dense
-// path (the guardrail of Algorithm 1) and from which group on the proxy path runs.
+// The group plan: for each sequence, its query rows and groups, how many
+// leading query rows take the dense path (the guardrail of Algorithm 1) and
+// from which group on the proxy path runs.
 struct Plan {
   int mode = PIVOT_DENSE;  // PIVOT_DENSE, PIVOT_REUSE or PIVOT_REFINE
   int g = 1, c = 0, dense_below = 0;
-  int n_groups = 0;
-  int B = 0, n_q = 0, topk = 0, dtype = 0, EB = 1;
+  int B = 0, topk = 0, dtype = 0, EB = 1;
+  int n_q = 0;       // most query rows of a sequence
+  int n_groups = 0;  // most groups of a sequence
+  int64_t rows_total = 0, groups_total = 0;
   size_t row_bytes = 0;
-  std::vector<int32_t> dense_rows, first_proxy, q_pos0, n_k;
-  int dense_hi = 0;     // max dense_rows over sequences
-  int proxy_lo = 0;     // min first_proxy over sequences
+  std::vector<int32_t> dense_rows, first_proxy, q_pos0, n_k, nq, row0, ng, grp0;
+  int dense_hi = 0;       // max dense_rows over sequences
+  int proxy_lo = 0;       // min first_proxy over sequences
+  bool any_proxy = false;  // some sequence has a group on the proxy path
   int64_t max_nk = 0;
+  // keys: contiguous (stride) or paged
+  const int32_t* pages = nullptr;
+  int32_t max_pages = 0, page_shift = 0, n_pages = 0;
+  int64_t k_stride = 0;
   // workspace layout
   size_t off_pq = 0, off_psc = 0, off_pw = 0, off_cand = 0, off_scores = 0, fixed = 0;
   size_t off_qlin = 0, off_qlsc = 0, off_plin = 0, off_plsc = 0;  // fp8 epilogue's linear term
@@ -107,28 +115,61 @@ struct Plan {
   int scan_shift = 0;  // the proxy scans [0, t0 - scan_shift]
 };
 
-pivot_status check_args(const pivot_args* a) {
+bool layout_varlen(const pivot_layout* l) { return l && l->cu_q; }
+bool layout_paged(const pivot_layout* l) { return l && l->block_table; }
+
+// Checks that need no plan; `nq` receives each sequence's query rows.
+pivot_status check_args(const pivot_args* a, const pivot_layout* l, std::vector<int32_t>& nq) {
   if (!a) return fail(PIVOT_ERR_INVALID_ARG, "args is NULL");
   if (a->dtype != PIVOT_DT_BF16 && a->dtype != PIVOT_DT_FP8_E4M3)
     return fail(PIVOT_ERR_UNSUPPORTED, "dtype %d not supported", a->dtype);
   if (a->heads != kH || a->dim != kD)
     return fail(PIVOT_ERR_UNSUPPORTED, "heads=%d dim=%d: this build specialises H=64, d=128", a->heads, a->dim);
   if (a->batch < 1) return fail(PIVOT_ERR_INVALID_ARG, "batch must be >= 1");
-  if (a->n_q < 0) return fail(PIVOT_ERR_INVALID_ARG, "n_q must be >= 0");
   if (a->topk < 1) return fail(PIVOT_ERR_INVALID_ARG, "topk must be >= 1");
   if (!a->q_pos0 || !a->n_k) return fail(PIVOT_ERR_INVALID_ARG, "q_pos0 and n_k (host arrays) are required");
+  nq.assign(a->batch, 0);
+  if (layout_varlen(l)) {
+    if (l->cu_q[0] != 0) return fail(PIVOT_ERR_INVALID_ARG, "cu_q[0] must be 0");
+    for (int b = 0; b < a->batch; ++b) {
+      if (l->cu_q[b + 1] < l->cu_q[b]) return fail(PIVOT_ERR_INVALID_ARG, "cu_q must be nondecreasing (at %d)", b);
+      nq[b] = l->cu_q[b + 1] - l->cu_q[b];
+    }
+  } else {
+    if (a->n_q < 0) return fail(PIVOT_ERR_INVALID_ARG, "n_q must be >= 0");
+    nq.assign(a->batch, a->n_q);
+  }
+  const bool paged = layout_paged(l);
+  const int64_t key_bytes = (int64_t)kD * (a->dtype == PIVOT_DT_FP8_E4M3 ? 1 : 2);
+  if (paged) {
+    const int P = l->page_size;
+    if (P < 16 || P > 65536 || (P & (P - 1)))
+      return fail(PIVOT_ERR_INVALID_ARG, "page_size=%d must be a power of two in [16, 65536]", P);
+    if (l->max_pages < 1) return fail(PIVOT_ERR_INVALID_ARG, "max_pages must be >= 1");
+    if (l->pool_keys < P || l->pool_keys % P)
+      return fail(PIVOT_ERR_INVALID_ARG, "pool_keys=%lld must be a positive multiple of page_size",
+                  (long long)l->pool_keys);
+    if (l->pool_keys * key_bytes > ((int64_t)1 << 31))  // 32-bit buffer offsets with room for a drop offset
+      return fail(PIVOT_ERR_UNSUPPORTED, "key pool of %lld keys exceeds 2^31 bytes", (long long)l->pool_keys);
+  }
+  int64_t total = 0;
   for (int b = 0; b < a->batch; ++b) {
     if (a->q_pos0[b] < 0) return fail(PIVOT_ERR_INVALID_ARG, "q_pos0[%d] < 0", b);
-    if ((int64_t)a->q_pos0[b] + a->n_q > a->n_k[b])
-      return fail(PIVOT_ERR_INVALID_ARG, "n_k[%d]=%d < q_pos0+n_q=%lld", b, a->n_k[b],
-                  (long long)a->q_pos0[b] + a->n_q);
-    if (a->n_k[b] > a->k_seq_stride)
+    if ((int64_t)a->q_pos0[b] + nq[b] > a->n_k[b])
+      return fail(PIVOT_ERR_INVALID_ARG, "n_k[%d]=%d < q_pos0+n_q=%lld", b, a->n_k[b], (long long)a->q_pos0[b] + nq[b]);
+    if (paged) {
+      if ((int64_t)a->n_k[b] > (int64_t)l->max_pages * l->page_size)
+        return fail(PIVOT_ERR_INVALID_ARG, "n_k[%d]=%d exceeds max_pages*page_size", b, a->n_k[b]);
+    } else if (a->n_k[b] > a->k_seq_stride) {
       return fail(PIVOT_ERR_INVALID_ARG, "n_k[%d]=%d exceeds k_seq_stride=%lld", b, a->n_k[b],
                   (long long)a->k_seq_stride);
+    }
     if (a->n_k[b] > PIVOT_MAX_KEYS)
       return fail(PIVOT_ERR_UNSUPPORTED, "n_k[%d]=%d exceeds PIVOT_MAX_KEYS=%d", b, a->n_k[b], PIVOT_MAX_KEYS);
+    total += nq[b];
   }
-  if (a->n_q > 0) {
+  if (total > 0x7FFFFFFF) return fail(PIVOT_ERR_UNSUPPORTED, "more than 2^31 query rows");
+  if (total > 0) {
     if (!a->q || !a->w || !a->k || !a->out_idx)
       return fail(PIVOT_ERR_INVALID_ARG, "q, w, k and out_idx are required");
     if (a->dtype == PIVOT_DT_FP8_E4M3 && (!a->q_scale || !a->k_scale))
@@ -137,17 +178,18 @@ pivot_status check_args(const pivot_args* a) {
   return PIVOT_OK;
 }
 
-// ext_cand: Refine writes its candidate sets to the caller's buffer, so the
-// workspace reserves none.
 // Width of a group's candidate row (App. B): c, plus the window union for the
 // per-query window.
 int cand_width(int c, int g, int W, int wkind) {
   return (W > 0 && wkind == PIVOT_WINDOW_PER_QUERY) ? c + W + g - 1 : c;
 }
 
-pivot_status make_plan(const pivot_args* a, int mode, int g, int c, int dense_below, bool ext_cand, Plan& p,
-                       int W = 0, int wkind = PIVOT_WINDOW_SHARED, int agg = PIVOT_AGG_MEAN) {
-  pivot_status s = check_args(a);
+// ext_cand: Refine writes its candidate sets to the caller's buffer, so the
+// workspace reserves none.
+pivot_status make_plan(const pivot_args* a, const pivot_layout* l, int mode, int g, int c, int dense_below,
+                       bool ext_cand, Plan& p, int W = 0, int wkind = PIVOT_WINDOW_SHARED,
+                       int agg = PIVOT_AGG_MEAN) {
+  pivot_status s = check_args(a, l, p.nq);
   if (s != PIVOT_OK) return s;
   if (mode != PIVOT_DENSE && mode != PIVOT_REUSE && mode != PIVOT_REFINE)
     return fail(PIVOT_ERR_INVALID_ARG, "mode %d", mode);
@@ -187,43 +229,72 @@ pivot_status make_plan(const pivot_args* a, int mode, int g, int c, int dense_be
   p.c = c;
   p.dense_below = (mode == PIVOT_DENSE) ? 0 : (dense_below < 0 ? c : dense_below);
   p.B = a->batch;
-  p.n_q = a->n_q;
   p.topk = a->topk;
   p.dtype = a->dtype;
   p.EB = a->dtype == PIVOT_DT_FP8_E4M3 ? 1 : 2;
   p.row_bytes = (size_t)kH * kD * p.EB;
-  p.n_groups = (int)cdiv(p.n_q, g);
-  p.dense_rows.resize(p.B);
-  p.first_proxy.resize(p.B);
   p.q_pos0.assign(a->q_pos0, a->q_pos0 + p.B);
   p.n_k.assign(a->n_k, a->n_k + p.B);
+  p.dense_rows.resize(p.B);
+  p.first_proxy.resize(p.B);
+  p.row0.resize(p.B);
+  p.ng.resize(p.B);
+  p.grp0.resize(p.B);
+  p.n_q = 0;
+  p.n_groups = 0;
+  p.rows_total = 0;
+  p.groups_total = 0;
+  for (int b = 0; b < p.B; ++b) {
+    p.row0[b] = (int32_t)p.rows_total;
+    p.grp0[b] = (int32_t)p.groups_total;
+    p.ng[b] = (int32_t)cdiv(p.nq[b], g);
+    p.rows_total += p.nq[b];
+    p.groups_total += p.ng[b];
+    p.n_q = std::max(p.n_q, p.nq[b]);
+    p.n_groups = std::max(p.n_groups, p.ng[b]);
+  }
+  if (p.groups_total > 0x7FFFFFFF / std::max(1, p.width))
+    return fail(PIVOT_ERR_UNSUPPORTED, "candidate rows exceed 2^31 entries");
+  if (layout_paged(l)) {
+    p.pages = l->block_table;
+    p.max_pages = l->max_pages;
+    p.page_shift = __builtin_ctz((unsigned)l->page_size);
+    p.n_pages = (int32_t)(l->pool_keys / l->page_size);
+  } else {
+    p.k_stride = a->k_seq_stride;
+  }
   p.dense_hi = 0;
   p.proxy_lo = p.n_groups;
+  p.any_proxy = false;
   p.max_nk = 0;
   for (int b = 0; b < p.B; ++b) {
     int J;
     if (mode == PIVOT_DENSE) {
-      J = p.n_groups;
+      J = p.ng[b];
     } else {
       const int64_t gap = (int64_t)p.dense_below - p.q_pos0[b];  // groups with t0 < dense_below
-      J = gap <= 0 ? 0 : (int)std::min<int64_t>(cdiv(gap, g), p.n_groups);
+      J = gap <= 0 ? 0 : (int)std::min<int64_t>(cdiv(gap, g), p.ng[b]);
     }
     p.first_proxy[b] = J;
-    p.dense_rows[b] = (int)std::min<int64_t>((int64_t)J * g, p.n_q);
+    p.dense_rows[b] = (int)std::min<int64_t>((int64_t)J * g, p.nq[b]);
     p.dense_hi = std::max(p.dense_hi, p.dense_rows[b]);
-    p.proxy_lo = std::min(p.proxy_lo, J);
+    if (J < p.ng[b]) {
+      p.proxy_lo = std::min(p.proxy_lo, J);
+      p.any_proxy = mode != PIVOT_DENSE;
+    }
     p.max_nk = std::max<int64_t>(p.max_nk, p.n_k[b]);
   }
+  if (!p.any_proxy) p.proxy_lo = p.n_groups;
   // workspace layout
   size_t off = 0;
-  const size_t ng = (size_t)p.B * p.n_groups;
+  const size_t ng = (size_t)p.groups_total;
   const bool fp8 = p.dtype == PIVOT_DT_FP8_E4M3;
-  const bool proxies = mode != PIVOT_DENSE && p.proxy_lo < p.n_groups;
+  const bool proxies = p.any_proxy;
   // query rows need the linear term when scored densely or re-scored by Refine
   p.qlin = fp8 && (p.dense_hi > 0 || (proxies && mode == PIVOT_REFINE));
   p.plin = fp8 && proxies;
   if (p.qlin) {
-    const size_t nq = (size_t)p.B * p.n_q;
+    const size_t nq = (size_t)p.rows_total;
     p.off_qlin = off;
     off = align_up(off + nq * kLinBytes);
     p.off_qlsc = off;
@@ -266,14 +337,15 @@ void score_need(const Plan& p, int64_t& full, int64_t& min_tile) {
   min_tile = 0;
   const int64_t ld = ld_for(p.max_nk);
   if (p.dense_hi > 0) {
-    const int64_t rows = (p.B == 1) ? p.dense_hi : (int64_t)p.B * p.n_q;
+    const int64_t rows = (p.B == 1) ? p.dense_hi : (int64_t)p.B * p.dense_hi;
     full = std::max(full, rows * ld * 4);
-    min_tile = std::max(min_tile, ((p.B == 1) ? std::min<int64_t>(16, rows) : p.n_q) * ld * 4);
+    min_tile = std::max(min_tile, std::min<int64_t>(16, p.dense_hi) * ld * 4);
   }
-  if (p.mode != PIVOT_DENSE && p.proxy_lo < p.n_groups) {
-    const int64_t rows = (p.B == 1) ? (p.n_groups - p.proxy_lo) : (int64_t)p.B * p.n_groups;
+  if (p.any_proxy) {
+    const int64_t span = p.n_groups - p.proxy_lo;
+    const int64_t rows = (p.B == 1) ? span : (int64_t)p.B * span;
     full = std::max(full, rows * ld * 4);
-    min_tile = std::max(min_tile, ((p.B == 1) ? std::min<int64_t>(16, rows) : p.n_groups) * ld * 4);
+    min_tile = std::max(min_tile, std::min<int64_t>(16, span) * ld * 4);
   }
 }
 
@@ -284,8 +356,11 @@ size_t recommended_bytes(const Plan& p) {
   return p.fixed + (size_t)scores;
 }
 
-// shift: subtracted from the query positions for the row limits (the shared
-// window's proxy scans [0, t0 - W]); may make early limits negative.
+// Sequences b0 .. b0 + nb - 1 as one launch sees them: row and group offsets
+// relative to the first, so the launch's array pointers start at
+// row0[b0] / grp0[b0].  shift: subtracted from the query positions for the
+// row limits (the shared window's proxy scans [0, t0 - W]); may make early
+// limits negative.
 SeqTable table_for(const Plan& p, int b0, int nb, int shift = 0) {
   SeqTable st;
   memset(&st, 0, sizeof st);
@@ -294,15 +369,42 @@ SeqTable table_for(const Plan& p, int b0, int nb, int shift = 0) {
     st.q_pos0[u] = p.q_pos0[b0 + u] - shift;
     st.dense_rows[u] = p.dense_rows[b0 + u];
     st.first_proxy[u] = p.first_proxy[b0 + u];
+    st.n_rows[u] = p.nq[b0 + u];
+    st.row0[u] = p.row0[b0 + u] - p.row0[b0];
+    st.grp0[u] = p.grp0[b0 + u] - p.grp0[b0];
   }
   return st;
+}
+
+// Keys of sequences b0 .. : the key arrays' base and the map of a launch.
+struct KeyBase {
+  const uint8_t* k;
+  const float* ks;
+  KeyMap map;
+};
+KeyBase keys_for(const pivot_args* a, const Plan& p, int b0) {
+  KeyBase kb;
+  kb.map.max_pages = p.max_pages;
+  kb.map.shift = p.page_shift;
+  kb.map.n_pages = p.n_pages;
+  kb.map.stride = p.k_stride;
+  if (p.pages) {  // the pool is shared: only the page table moves
+    kb.k = (const uint8_t*)a->k;
+    kb.ks = a->k_scale;
+    kb.map.pages = p.pages + (size_t)b0 * p.max_pages;
+  } else {
+    kb.k = (const uint8_t*)a->k + (size_t)b0 * p.k_stride * kD * p.EB;
+    kb.ks = a->k_scale ? a->k_scale + (size_t)b0 * p.k_stride : nullptr;
+    kb.map.pages = nullptr;
+  }
+  return kb;
 }
 
 // Largest limit of an active row of rs in any sequence of st.
 int64_t max_limit(const SeqTable& st, const RowSpace& rs) {
   int64_t lim = -1;
   for (int b = 0; b < st.n; ++b) {
-    int hi = rs.i1;
+    int hi = std::min(rs.i1, rs.kind == kProxyRows ? (st.n_rows[b] + rs.step - 1) / rs.step : st.n_rows[b]);
     int lo = rs.i0;
     if (rs.kind == kDenseRows) hi = std::min(hi, st.dense_rows[b]);
     if (rs.kind == kProxyRows) lo = std::max(lo, st.first_proxy[b]);
@@ -317,42 +419,42 @@ struct RowData {
   const float* w;
   const uint8_t* lin;  // fp8 only
   const float* lsc;
-  int64_t seq_rows;  // rows per sequence in q
+  bool groups;         // the rows are groups (proxies), else query rows
 };
 
-// Score and select rows [lo, hi) of each sequence, tiled to the score budget.
-pivot_status run_rows(const pivot_args* a, const Plan& p, int kind, int lo, int hi, int step, int per_seq,
+// Score and select rows [lo, hi) of each sequence, tiled to the score budget:
+// several whole sequences per tile when they fit, else row tiles of one.
+pivot_status run_rows(const pivot_args* a, const Plan& p, int kind, int lo, int hi, int step,
                       const RowData& rd_all, OutDesc od_all, float* scores, int64_t score_bytes,
                       hipStream_t stream, int lim_shift = 0) {
   if (hi <= lo) return PIVOT_OK;
   const int64_t ld_max = ld_for(p.max_nk);
   const int64_t row_bytes = ld_max * 4;
   int seqs_per_tile, rows_per_tile;
-  if (p.B == 1) {
+  if (p.B > 1 && score_bytes / (row_bytes * (hi - lo)) >= 1) {
+    rows_per_tile = hi - lo;
+    seqs_per_tile = (int)std::min<int64_t>(score_bytes / (row_bytes * (hi - lo)), kMaxSeq);
+  } else {
     seqs_per_tile = 1;
     int64_t r = score_bytes / row_bytes;
     r = std::max<int64_t>(16, r / 16 * 16);
     rows_per_tile = (int)std::min<int64_t>(r, hi - lo);
-  } else {
-    rows_per_tile = hi - lo;
-    int64_t s = score_bytes / (row_bytes * (hi - lo));
-    seqs_per_tile = (int)std::max<int64_t>(1, std::min<int64_t>(s, kMaxSeq));
   }
   if ((int64_t)seqs_per_tile * rows_per_tile * row_bytes > score_bytes)
     return fail(PIVOT_ERR_WORKSPACE, "workspace too small for one score tile");
   for (int b0 = 0; b0 < p.B; b0 += seqs_per_tile) {
     const int nb = std::min(seqs_per_tile, p.B - b0);
     SeqTable st = table_for(p, b0, nb, lim_shift);
+    const size_t r0 = rd_all.groups ? (size_t)p.grp0[b0] : (size_t)p.row0[b0];
     RowData rd = rd_all;
-    rd.q = (const uint8_t*)rd_all.q + (size_t)b0 * rd_all.seq_rows * p.row_bytes;
-    rd.qs = rd_all.qs ? rd_all.qs + (size_t)b0 * rd_all.seq_rows : nullptr;
-    rd.w = rd_all.w + (size_t)b0 * rd_all.seq_rows * kH;
-    rd.lin = rd_all.lin ? rd_all.lin + (size_t)b0 * rd_all.seq_rows * kLinBytes : nullptr;
-    rd.lsc = rd_all.lsc ? rd_all.lsc + (size_t)b0 * rd_all.seq_rows * kLinLevels : nullptr;
-    const uint8_t* kb = (const uint8_t*)a->k + (size_t)b0 * a->k_seq_stride * kD * p.EB;
-    const float* ksb = a->k_scale ? a->k_scale + (size_t)b0 * a->k_seq_stride : nullptr;
+    rd.q = (const uint8_t*)rd_all.q + r0 * p.row_bytes;
+    rd.qs = rd_all.qs ? rd_all.qs + r0 : nullptr;
+    rd.w = rd_all.w + r0 * kH;
+    rd.lin = rd_all.lin ? rd_all.lin + r0 * kLinBytes : nullptr;
+    rd.lsc = rd_all.lsc ? rd_all.lsc + r0 * kLinLevels : nullptr;
+    const KeyBase kb = keys_for(a, p, b0);
     OutDesc od = od_all;
-    od.base = od_all.base + (size_t)b0 * od_all.per_seq * od_all.ld;
+    od.base = od_all.base + (size_t)(od_all.fan_g == 0 && od_all.groups ? p.grp0[b0] : p.row0[b0]) * od_all.ld;
     for (int i0 = lo; i0 < hi; i0 += rows_per_tile) {
       RowSpace rs{i0, std::min(hi, i0 + rows_per_tile), step, kind};
       const int64_t lim = max_limit(st, rs);
@@ -360,8 +462,8 @@ pivot_status run_rows(const pivot_args* a, const Plan& p, int kind, int lo, int 
       pivot_status s = PIVOT_OK;
       if (lim >= 0)  // no key in reach (shifted limits): the select only pads with -1
         s = hip_check(timed(PIVOT_KERNEL_SCORE, stream, [&] {
-                        return launch_score(p.dtype, rd.q, rd.qs, rd.w, rd.lin, rd.lsc, rd.seq_rows, kb, ksb,
-                                            a->k_seq_stride, st, rs, lim, scores, ld, stream);
+                        return launch_score(p.dtype, rd.q, rd.qs, rd.w, rd.lin, rd.lsc, kb.k, kb.ks, kb.map, st, rs,
+                                            lim, scores, ld, stream);
                       }),
                       "score kernel");
       if (s != PIVOT_OK) return s;
@@ -375,7 +477,6 @@ pivot_status run_rows(const pivot_args* a, const Plan& p, int kind, int lo, int 
       if (s != PIVOT_OK) return s;
     }
   }
-  (void)per_seq;
   return PIVOT_OK;
 }
 
@@ -394,12 +495,11 @@ pivot_status check_workspace(const pivot_args* a, const Plan& p, int64_t& score_
   return PIVOT_OK;
 }
 
-// Linear-term rows (mfma_tile.h) of the call's queries: all of them for a
-// batch or when Refine re-scores members, else the leading dense rows.
-// Query rows that need the fp8 linear term: the dense rows, or every row when
-// Refine re-scores the members.
+// Query rows that need the fp8 linear term (mfma_tile.h): the leading dense
+// rows of a single sequence, else every row (a batch, or Refine re-scoring
+// the members).
 int64_t query_lin_rows(const Plan& p) {
-  return (p.B == 1 && p.mode != PIVOT_REFINE) ? p.dense_hi : (int64_t)p.B * p.n_q;
+  return (p.B == 1 && p.mode != PIVOT_REFINE) ? p.dense_hi : p.rows_total;
 }
 
 pivot_status query_lin(const pivot_args* a, const Plan& p, uint8_t* ws, hipStream_t stream) {
@@ -416,10 +516,10 @@ pivot_status dense_part(const pivot_args* a, const Plan& p, float* scores, int64
   uint8_t* ws = (uint8_t*)a->workspace;
   const bool fp8 = a->dtype == PIVOT_DT_FP8_E4M3;
   RowData rd{a->q, fp8 ? a->q_scale : nullptr, a->w, fp8 ? ws + p.off_qlin : nullptr,
-             fp8 ? reinterpret_cast<const float*>(ws + p.off_qlsc) : nullptr, p.n_q};
-  OutDesc od{a->out_idx, p.topk, p.n_q, 0, p.n_q, p.topk};
+             fp8 ? reinterpret_cast<const float*>(ws + p.off_qlsc) : nullptr, false};
+  OutDesc od{a->out_idx, p.topk, 0, 0, p.topk};
   const int kind = p.mode == PIVOT_DENSE ? kAll : kDenseRows;
-  return run_rows(a, p, kind, 0, p.dense_hi, 1, p.n_q, rd, od, scores, score_bytes, stream);
+  return run_rows(a, p, kind, 0, p.dense_hi, 1, rd, od, scores, score_bytes, stream);
 }
 
 // Sizing validates the shape only: the pointers get non-null stand-ins.
@@ -432,17 +532,32 @@ pivot_args shape_of(const pivot_args* a) {
   return shape;
 }
 
-pivot_status group_plan(const pivot_args* a, const pivot_group_opts* o, bool ext_cand, Plan& p) {
+pivot_status group_plan(const pivot_args* a, const pivot_layout* l, const pivot_group_opts* o, bool ext_cand,
+                        Plan& p) {
   if (!o) return fail(PIVOT_ERR_INVALID_ARG, "opts is NULL");
   if (o->mode != PIVOT_REUSE && o->mode != PIVOT_REFINE) return fail(PIVOT_ERR_INVALID_ARG, "mode %d", o->mode);
-  return make_plan(a, o->mode, o->g, o->c, o->dense_below, ext_cand, p, o->window, o->window_kind, o->aggregate);
+  return make_plan(a, l, o->mode, o->g, o->c, o->dense_below, ext_cand, p, o->window, o->window_kind, o->aggregate);
 }
 
-pivot_status group_index(const pivot_args* a, const pivot_group_opts* o) {
+pivot_status dense_index(const pivot_args* a, const pivot_layout* l) {
   Plan p;
-  pivot_status s = group_plan(a, o, o && o->out_cand != nullptr && o->mode == PIVOT_REFINE, p);
+  pivot_status s = make_plan(a, l, PIVOT_DENSE, 1, 0, 0, false, p);
   if (s != PIVOT_OK) return s;
-  if (p.n_q == 0) return PIVOT_OK;
+  if (p.rows_total == 0) return PIVOT_OK;
+  int64_t score_bytes;
+  s = check_workspace(a, p, score_bytes);
+  if (s != PIVOT_OK) return s;
+  float* scores = reinterpret_cast<float*>((uint8_t*)a->workspace + p.off_scores);
+  s = query_lin(a, p, (uint8_t*)a->workspace, (hipStream_t)a->stream);
+  if (s != PIVOT_OK) return s;
+  return dense_part(a, p, scores, score_bytes, (hipStream_t)a->stream);
+}
+
+pivot_status group_index(const pivot_args* a, const pivot_layout* l, const pivot_group_opts* o) {
+  Plan p;
+  pivot_status s = group_plan(a, l, o, o && o->out_cand != nullptr && o->mode == PIVOT_REFINE, p);
+  if (s != PIVOT_OK) return s;
+  if (p.rows_total == 0) return PIVOT_OK;
   const int mode = p.mode;
   int32_t* out_cand = mode == PIVOT_REFINE ? o->out_cand : nullptr;
   const int width = p.width;
@@ -459,19 +574,18 @@ pivot_status group_index(const pivot_args* a, const pivot_group_opts* o) {
   int32_t* cand = (mode == PIVOT_REFINE) ? (out_cand ? out_cand : reinterpret_cast<int32_t*>(ws + p.off_cand))
                                          : nullptr;
   const float* qs = p.dtype == PIVOT_DT_FP8_E4M3 ? a->q_scale : nullptr;
-  const bool any_proxy = p.proxy_lo < p.n_groups;
 
-  if (any_proxy)
+  if (p.any_proxy)
     for (int b0 = 0; b0 < p.B; b0 += kMaxSeq) {  // Eq. 4 proxies (or the first / last member)
       const int nb = std::min(kMaxSeq, p.B - b0);
       SeqTable st = table_for(p, b0, nb);
-      const size_t qoff = (size_t)b0 * p.n_q;
-      const size_t poff = (size_t)b0 * p.n_groups;
+      const size_t qoff = (size_t)p.row0[b0];
+      const size_t poff = (size_t)p.grp0[b0];
       s = hip_check(timed(PIVOT_KERNEL_PROXY, stream, [&] {
                       return launch_proxy(p.dtype, (const uint8_t*)a->q + qoff * p.row_bytes,
-                                          qs ? qs + qoff : nullptr, a->w + qoff * kH, p.n_q, p.g, p.n_groups, st,
-                                          p.proxy_lo, p.n_groups, false, p.agg, (uint8_t*)pq + poff * p.row_bytes,
-                                          psc + poff, pw + poff * kH, stream);
+                                          qs ? qs + qoff : nullptr, a->w + qoff * kH, p.g, st, p.proxy_lo,
+                                          p.n_groups, false, p.agg, (uint8_t*)pq + poff * p.row_bytes, psc + poff,
+                                          pw + poff * kH, stream);
                     }),
                     "proxy kernel");
       if (s != PIVOT_OK) return s;
@@ -487,7 +601,7 @@ pivot_status group_index(const pivot_args* a, const pivot_group_opts* o) {
       qset = LinRows{(const uint8_t*)a->q, a->q_scale, a->w, 0, query_lin_rows(p), ws + p.off_qlin,
                      reinterpret_cast<float*>(ws + p.off_qlsc)};
     if (p.plin)
-      pset = LinRows{(const uint8_t*)pq, psc, pw, p.B == 1 ? p.proxy_lo : 0, (int64_t)p.B * p.n_groups, plin, plsc};
+      pset = LinRows{(const uint8_t*)pq, psc, pw, p.B == 1 ? p.proxy_lo : 0, p.groups_total, plin, plsc};
     if (p.qlin || p.plin) {
       s = hip_check(timed(PIVOT_KERNEL_LIN, stream, [&] { return launch_lin(qset, pset, stream); }),
                     "linear-term kernel");
@@ -497,14 +611,14 @@ pivot_status group_index(const pivot_args* a, const pivot_group_opts* o) {
 
   s = dense_part(a, p, scores, score_bytes, stream);  // guardrail groups (Algorithm 1)
   if (s != PIVOT_OK) return s;
-  if (!any_proxy) {
+  if (!p.any_proxy) {
     if (out_cand)
       for (int b0 = 0; b0 < p.B; b0 += kMaxSeq) {
         const int nb = std::min(kMaxSeq, p.B - b0);
         SeqTable st = table_for(p, b0, nb);
         s = hip_check(timed(PIVOT_KERNEL_FILL, stream, [&] {
-                        return launch_fill_guardrail(out_cand + (size_t)b0 * p.n_groups * width, p.n_groups, width,
-                                                     st, 0, p.n_groups, -1, stream);
+                        return launch_fill_guardrail(out_cand + (size_t)p.grp0[b0] * width, width, st, 0, p.n_groups,
+                                                     -1, stream);
                       }),
                       "fill kernel");
         if (s != PIVOT_OK) return s;
@@ -515,12 +629,11 @@ pivot_status group_index(const pivot_args* a, const pivot_group_opts* o) {
   // Eq. 5 proxy scan, then Eq. 6 (Reuse: top-k shared by the members) or
   // Eq. 7 (Refine: top-c candidates; before a shared window, the top c - W - g + 1
   // over [0, t0 - W])
-  RowData rd{pq, p.dtype == PIVOT_DT_FP8_E4M3 ? psc : nullptr, pw, plin, plsc, p.n_groups};
-  OutDesc od = (mode == PIVOT_REUSE) ? OutDesc{a->out_idx, p.topk, p.n_q, p.g, p.n_q, p.topk}
-                                     : OutDesc{cand, p.proxy_m, p.n_groups, 0, 0, width};
+  RowData rd{pq, p.dtype == PIVOT_DT_FP8_E4M3 ? psc : nullptr, pw, plin, plsc, true};
+  OutDesc od = (mode == PIVOT_REUSE) ? OutDesc{a->out_idx, p.topk, p.g, 0, p.topk}
+                                     : OutDesc{cand, p.proxy_m, 0, 1, width};
   if (od.m > 0) {
-    s = run_rows(a, p, kProxyRows, p.proxy_lo, p.n_groups, p.g, p.n_groups, rd, od, scores, score_bytes, stream,
-                 p.scan_shift);
+    s = run_rows(a, p, kProxyRows, p.proxy_lo, p.n_groups, p.g, rd, od, scores, score_bytes, stream, p.scan_shift);
     if (s != PIVOT_OK) return s;
   }
   if (mode == PIVOT_REUSE) return PIVOT_OK;
@@ -528,35 +641,33 @@ pivot_status group_index(const pivot_args* a, const pivot_group_opts* o) {
   for (int b0 = 0; b0 < p.B; b0 += kMaxSeq) {  // App. B window, Eqs. 8-9
     const int nb = std::min(kMaxSeq, p.B - b0);
     SeqTable st = table_for(p, b0, nb);
-    const size_t qoff = (size_t)b0 * p.n_q;
-    int32_t* cb = cand + (size_t)b0 * p.n_groups * width;
+    const size_t qoff = (size_t)p.row0[b0];
+    const size_t goff = (size_t)p.grp0[b0];
+    int32_t* cb = cand + goff * width;
     if (out_cand) {
       s = hip_check(timed(PIVOT_KERNEL_FILL, stream,
-                          [&] { return launch_fill_guardrail(cb, p.n_groups, width, st, 0, p.n_groups, -1, stream); }),
+                          [&] { return launch_fill_guardrail(cb, width, st, 0, p.n_groups, -1, stream); }),
                     "fill kernel");
       if (s != PIVOT_OK) return s;
     }
     if (p.W > 0) {
       s = hip_check(timed(PIVOT_KERNEL_FILL, stream, [&] {
-                      return launch_window(cb, p.n_q, p.g, p.n_groups, st, p.proxy_lo, p.n_groups, width, p.proxy_m,
-                                           p.W, p.wkind == PIVOT_WINDOW_PER_QUERY, stream);
+                      return launch_window(cb, p.g, st, p.proxy_lo, p.n_groups, width, p.proxy_m, p.W,
+                                           p.wkind == PIVOT_WINDOW_PER_QUERY, stream);
                     }),
                     "window kernel");
       if (s != PIVOT_OK) return s;
     }
     const int wslot = p.wkind == PIVOT_WINDOW_PER_QUERY ? p.proxy_m : width;
+    const KeyBase kb = keys_for(a, p, b0);
     s = hip_check(timed(PIVOT_KERNEL_REFINE, stream, [&] {
                     return launch_refine(p.dtype, (const uint8_t*)a->q + qoff * p.row_bytes,
                                          qs ? qs + qoff : nullptr, a->w + qoff * kH,
                                          p.qlin ? ws + p.off_qlin + qoff * kLinBytes : nullptr,
                                          p.qlin ? reinterpret_cast<const float*>(ws + p.off_qlsc) + qoff * kLinLevels
                                                 : nullptr,
-                                         p.n_q, p.g, p.n_groups,
-                                         (const uint8_t*)a->k + (size_t)b0 * a->k_seq_stride * kD * p.EB,
-                                         a->k_scale ? a->k_scale + (size_t)b0 * a->k_seq_stride : nullptr,
-                                         a->k_seq_stride, st, p.proxy_lo, p.n_groups, cb, width, p.W, wslot, p.topk,
-                                         reinterpret_cast<float*>(ws + p.off_rsc) +
-                                             (size_t)b0 * p.n_groups * p.g * width,
+                                         p.g, kb.k, kb.ks, kb.map, st, p.proxy_lo, p.n_groups, cb, width, p.W, wslot,
+                                         p.topk, reinterpret_cast<float*>(ws + p.off_rsc) + goff * p.g * width,
                                          a->out_idx + qoff * p.topk, stream);
                   }),
                   "refine kernel");
@@ -583,16 +694,25 @@ pivot_group_opts plain_opts(int32_t mode, int32_t g, int32_t c, int32_t dense_be
 
 extern "C" {
 
-size_t pivot_workspace_size(const pivot_args* a, int32_t mode, int32_t g, int32_t c) {
+size_t pivot_workspace_size_layout(const pivot_args* a, const pivot_layout* l, const pivot_group_opts* o) {
   if (!a) return 0;
-  if (mode == PIVOT_DENSE) {
-    pivot_args shape = shape_of(a);
-    Plan p;
-    if (make_plan(&shape, PIVOT_DENSE, 1, 0, 0, false, p) != PIVOT_OK) return 0;
+  pivot_args shape = shape_of(a);
+  Plan p;
+  if (!o) {
+    if (make_plan(&shape, l, PIVOT_DENSE, 1, 0, 0, false, p) != PIVOT_OK) return 0;
     return recommended_bytes(p);
   }
+  pivot_group_opts oc = *o;
+  oc.out_cand = nullptr;
+  if (group_plan(&shape, l, &oc, false, p) != PIVOT_OK) return 0;
+  return recommended_bytes(p);
+}
+
+size_t pivot_workspace_size(const pivot_args* a, int32_t mode, int32_t g, int32_t c) {
+  if (!a) return 0;
+  if (mode == PIVOT_DENSE) return pivot_workspace_size_layout(a, nullptr, nullptr);
   const pivot_group_opts o = plain_opts(mode, g, c, c, nullptr);
-  return pivot_group_workspace_size(a, &o);
+  return pivot_workspace_size_layout(a, nullptr, &o);
 }
 
 int32_t pivot_cand_width(const pivot_group_opts* o) {
@@ -601,36 +721,27 @@ int32_t pivot_cand_width(const pivot_group_opts* o) {
 }
 
 size_t pivot_group_workspace_size(const pivot_args* a, const pivot_group_opts* o) {
-  if (!a || !o) return 0;
-  pivot_args shape = shape_of(a);
-  pivot_group_opts oc = *o;
-  oc.out_cand = nullptr;
-  Plan p;
-  if (group_plan(&shape, &oc, false, p) != PIVOT_OK) return 0;
-  return recommended_bytes(p);
+  if (!o) return 0;
+  return pivot_workspace_size_layout(a, nullptr, o);
 }
 
-pivot_status pivot_dense_index(const pivot_args* a) {
-  Plan p;
-  pivot_status s = make_plan(a, PIVOT_DENSE, 1, 0, 0, false, p);
-  if (s != PIVOT_OK) return s;
-  if (p.n_q == 0) return PIVOT_OK;
-  int64_t score_bytes;
-  s = check_workspace(a, p, score_bytes);
-  if (s != PIVOT_OK) return s;
-  float* scores = reinterpret_cast<float*>((uint8_t*)a->workspace + p.off_scores);
-  s = query_lin(a, p, (uint8_t*)a->workspace, (hipStream_t)a->stream);
-  if (s != PIVOT_OK) return s;
-  return dense_part(a, p, scores, score_bytes, (hipStream_t)a->stream);
-}
+pivot_status pivot_dense_index(const pivot_args* a) { return dense_index(a, nullptr); }
+
+pivot_status pivot_dense_index_layout(const pivot_args* a, const pivot_layout* l) { return dense_index(a, l); }
 
 pivot_status pivot_group_index(const pivot_args* a, int32_t mode, int32_t g, int32_t c, int32_t dense_below,
                                int32_t* out_cand) {
   const pivot_group_opts o = plain_opts(mode, g, c, dense_below, out_cand);
-  return group_index(a, &o);
+  return group_index(a, nullptr, &o);
 }
 
-pivot_status pivot_group_index_opts(const pivot_args* a, const pivot_group_opts* o) { return group_index(a, o); }
+pivot_status pivot_group_index_opts(const pivot_args* a, const pivot_group_opts* o) {
+  return group_index(a, nullptr, o);
+}
+
+pivot_status pivot_group_index_layout(const pivot_args* a, const pivot_layout* l, const pivot_group_opts* o) {
+  return group_index(a, l, o);
+}
 
 pivot_status pivot_proxy_rows(int32_t dtype, int32_t heads, int32_t dim, int32_t n_q, int32_t g, const void* q,
                               const float* q_scale, const float* w, void* out_q, float* out_scale, float* out_w,
@@ -644,9 +755,10 @@ pivot_status pivot_proxy_rows(int32_t dtype, int32_t heads, int32_t dim, int32_t
   SeqTable st;
   memset(&st, 0, sizeof st);
   st.n = 1;
+  st.n_rows[0] = n_q;
   const int ng = (int)cdiv(n_q, g);
-  return hip_check(launch_proxy(dtype, q, dtype == PIVOT_DT_FP8_E4M3 ? q_scale : nullptr, w, n_q, g, ng, st, 0, ng,
-                                true, PIVOT_AGG_MEAN, out_q, out_scale, out_w, (hipStream_t)stream),
+  return hip_check(launch_proxy(dtype, q, dtype == PIVOT_DT_FP8_E4M3 ? q_scale : nullptr, w, g, st, 0, ng, true,
+                                PIVOT_AGG_MEAN, out_q, out_scale, out_w, (hipStream_t)stream),
                    "proxy kernel");
 }
 
@@ -680,14 +792,17 @@ pivot_status pivot_score_rows(int32_t dtype, int32_t heads, int32_t dim, int32_t
   memset(&st, 0, sizeof st);
   st.n = 1;
   st.q_pos0[0] = (int32_t)lim0;
+  st.n_rows[0] = n_rows;
   RowSpace rs{0, n_rows, lim_step, kAll};
   if (fp8) {
     pivot_status s = hip_check(launch_lin(q, q_scale, w, 0, n_rows, lin, lsc, (hipStream_t)stream),
                                "linear-term kernel");
     if (s != PIVOT_OK) return s;
   }
-  return hip_check(launch_score(dtype, q, fp8 ? q_scale : nullptr, w, lin, lsc, n_rows, k, fp8 ? k_scale : nullptr, 0,
-                                st, rs, lim_max, out, ld, (hipStream_t)stream),
+  KeyMap km;
+  memset(&km, 0, sizeof km);  // one sequence of contiguous keys
+  return hip_check(launch_score(dtype, q, fp8 ? q_scale : nullptr, w, lin, lsc, k, fp8 ? k_scale : nullptr, km, st,
+                                rs, lim_max, out, ld, (hipStream_t)stream),
                    "score kernel");
 }
 
@@ -715,8 +830,9 @@ pivot_status pivot_topk_rows_ws(int32_t n_rows, const float* scores, int64_t ld,
   memset(&st, 0, sizeof st);
   st.n = 1;
   st.q_pos0[0] = (int32_t)(n0 - 1);
+  st.n_rows[0] = n_rows;
   RowSpace rs{0, n_rows, n_step, kAll};
-  OutDesc od{out, m, n_rows, 0, 0, m};
+  OutDesc od{out, m, 0, 0, m};
   return hip_check(launch_topk(scores, ld, st, rs, od, n_max - 1, workspace, workspace ? workspace_bytes : 0,
                                (hipStream_t)stream),
                    "top-k kernel");

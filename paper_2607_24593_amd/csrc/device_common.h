@@ -14,16 +14,26 @@ constexpr int kWave = 64;     // CDNA wavefront size
 enum Dtype : int { kBf16 = 0, kFp8 = 1 };
 
 // Sequences of one launch, passed by value as a kernel argument.  Positions of
-// row i of sequence b are q_pos0[b] + i * step (RowSpace.step).
+// row i of sequence b are q_pos0[b] + i * step (RowSpace.step).  Sequence b
+// owns query rows row0[b] .. row0[b] + n_rows[b] - 1 of the launch's query
+// arrays (q, q_scale, w, linear terms, outputs) and groups grp0[b] .. of its
+// group arrays (proxies, candidate rows); a padded batch has row0 = b n_q.
 struct SeqTable {
   int32_t n;
   int32_t q_pos0[kMaxSeq];
   int32_t dense_rows[kMaxSeq];   // query rows [0, dense_rows) go through the dense path
   int32_t first_proxy[kMaxSeq];  // groups [first_proxy, n_groups) go through the proxy path
+  int32_t n_rows[kMaxSeq];       // query rows of the sequence in this call
+  int32_t row0[kMaxSeq];
+  int32_t grp0[kMaxSeq];
 };
 
+// Groups of g consecutive query rows of sequence b (the last may be shorter).
+__device__ __forceinline__ int seq_groups(const SeqTable& st, int b, int g) { return (st.n_rows[b] + g - 1) / g; }
+
 // The rows one launch covers: for every sequence b < SeqTable.n, the local rows
-// [i0, i1).  Output/score row of (b, i) is b * (i1 - i0) + (i - i0).
+// [i0, i1).  Score row of (b, i) is b * (i1 - i0) + (i - i0).  Rows of kind
+// kProxyRows are groups (step = g), the others query rows.
 struct RowSpace {
   int32_t i0, i1;
   int32_t step;     // position step between consecutive local rows
@@ -31,16 +41,43 @@ struct RowSpace {
 };
 enum RowKind : int { kAll = 0, kDenseRows = 1, kProxyRows = 2 };
 
+// Rows of sequence b of the RowSpace's kind.
+__device__ __forceinline__ int row_count(const SeqTable& st, const RowSpace& rs, int b) {
+  return rs.kind == kProxyRows ? seq_groups(st, b, rs.step) : st.n_rows[b];
+}
+
 __device__ __forceinline__ bool row_active(const SeqTable& st, const RowSpace& rs, int b, int i) {
-  if (b >= st.n || i < rs.i0 || i >= rs.i1) return false;
+  if (b >= st.n || i < rs.i0 || i >= rs.i1 || i >= row_count(st, rs, b)) return false;
   if (rs.kind == kDenseRows) return i < st.dense_rows[b];
   if (rs.kind == kProxyRows) return i >= st.first_proxy[b];
   return true;
 }
 
+// Index of row (b, i) in the launch's query (or, for kProxyRows, group) arrays.
+__device__ __forceinline__ int64_t row_index(const SeqTable& st, const RowSpace& rs, int b, int i) {
+  return (int64_t)(rs.kind == kProxyRows ? st.grp0[b] : st.row0[b]) + i;
+}
+
 __device__ __forceinline__ int64_t row_limit(const SeqTable& st, const RowSpace& rs, int b, int i) {
   return (int64_t)st.q_pos0[b] + (int64_t)i * rs.step;
 }
+
+// Where key s of sequence b of a launch lives in the key arrays: row
+// b * stride + s, or, with a page table, row page * page_size + s mod
+// page_size with page = pages[b * max_pages + s / page_size] (clamped into
+// the pool, so a bad entry cannot address memory outside it).
+struct KeyMap {
+  const int32_t* pages;  // dev [sequences, max_pages], or nullptr: contiguous keys
+  int64_t stride;        // contiguous: key rows between consecutive sequences
+  int32_t max_pages;
+  int32_t shift;         // log2(page_size)
+  int32_t n_pages;       // pages in the pool
+  __device__ __forceinline__ int64_t row(int b, int64_t s) const {
+    if (!pages) return (int64_t)b * stride + s;
+    const int32_t pg = min(max(pages[(int64_t)b * max_pages + (s >> shift)], 0), n_pages - 1);
+    return ((int64_t)pg << shift) | (s & ((1 << shift) - 1));
+  }
+};
 
 // Order-preserving map of a float onto uint32 (larger float -> larger key);
 // -0 and +0 map to the same key.

@@ -41,8 +41,8 @@ __device__ __forceinline__ uint16_t bf16_rne(float f) {
 template <int DT>
 __global__ __launch_bounds__(256) void proxy_kernel(const uint8_t* __restrict__ q,
                                                     const float* __restrict__ q_scale,
-                                                    const float* __restrict__ w, int n_q, int g, int n_groups,
-                                                    SeqTable st, int j0, int all_groups, int agg,
+                                                    const float* __restrict__ w, int g, SeqTable st, int j0,
+                                                    int all_groups, int agg,
                                                     uint8_t* __restrict__ pq, float* __restrict__ psc,
                                                     float* __restrict__ pw) {
 #pragma clang fp contract(off)
@@ -50,11 +50,11 @@ __global__ __launch_bounds__(256) void proxy_kernel(const uint8_t* __restrict__ 
   constexpr int ROW_BYTES = kH * kD * EB;
   constexpr int PER = 32;  // elements per thread
   const int j = j0 + blockIdx.x, b = blockIdx.y;
-  if (b >= st.n || j >= n_groups) return;
+  if (b >= st.n || j >= seq_groups(st, b, g)) return;
   if (!all_groups && j < st.first_proxy[b]) return;
-  const int gs = min(g, n_q - j * g);
-  const int64_t r0 = (int64_t)b * n_q + (int64_t)j * g;
-  const int64_t pr = (int64_t)b * n_groups + j;
+  const int gs = min(g, st.n_rows[b] - j * g);
+  const int64_t r0 = (int64_t)st.row0[b] + (int64_t)j * g;
+  const int64_t pr = (int64_t)st.grp0[b] + j;
   const int tid = threadIdx.x;
   const int e0 = tid * PER;
 
@@ -139,17 +139,16 @@ __global__ __launch_bounds__(256) void proxy_kernel(const uint8_t* __restrict__ 
   }
 }
 
-hipError_t launch_proxy(int dtype, const void* q, const float* q_scale, const float* w, int n_q, int g,
-                        int n_groups, const SeqTable& st, int j0, int j1, bool all_groups, int agg, void* pq,
-                        float* psc, float* pw, hipStream_t stream) {
+hipError_t launch_proxy(int dtype, const void* q, const float* q_scale, const float* w, int g, const SeqTable& st,
+                        int j0, int j1, bool all_groups, int agg, void* pq, float* psc, float* pw, hipStream_t stream) {
   if (j1 <= j0 || st.n <= 0) return hipSuccess;
   dim3 grid((unsigned)(j1 - j0), (unsigned)st.n);
   if (dtype == kFp8)
-    hipLaunchKernelGGL(proxy_kernel<kFp8>, grid, dim3(256), 0, stream, (const uint8_t*)q, q_scale, w, n_q, g,
-                       n_groups, st, j0, (int)all_groups, agg, (uint8_t*)pq, psc, pw);
+    hipLaunchKernelGGL(proxy_kernel<kFp8>, grid, dim3(256), 0, stream, (const uint8_t*)q, q_scale, w, g, st, j0,
+                       (int)all_groups, agg, (uint8_t*)pq, psc, pw);
   else
-    hipLaunchKernelGGL(proxy_kernel<kBf16>, grid, dim3(256), 0, stream, (const uint8_t*)q, q_scale, w, n_q, g,
-                       n_groups, st, j0, (int)all_groups, agg, (uint8_t*)pq, psc, pw);
+    hipLaunchKernelGGL(proxy_kernel<kBf16>, grid, dim3(256), 0, stream, (const uint8_t*)q, q_scale, w, g, st, j0,
+                       (int)all_groups, agg, (uint8_t*)pq, psc, pw);
   return hipGetLastError();
 }
 

@@ -33,16 +33,16 @@ constexpr int kMaxCand = 8192;
 template <int DT, int R>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void rescore_kernel(
     const uint8_t* __restrict__ q, const float* __restrict__ q_scale, const float* __restrict__ w,
-    const uint8_t* __restrict__ lin, const float* __restrict__ lin_scale, int n_q, int g, int n_groups,
-    const uint8_t* __restrict__ k, const float* __restrict__ k_scale, int64_t k_seq_stride, SeqTable st, int j0,
+    const uint8_t* __restrict__ lin, const float* __restrict__ lin_scale, int g,
+    const uint8_t* __restrict__ k, const float* __restrict__ k_scale, KeyMap km, SeqTable st, int j0,
     const int32_t* __restrict__ cand, int c, int all_slots, int parts, float* __restrict__ rsc) {
   using Tile = RowTile<DT, R>;
   constexpr int EB = Tile::EB;
   __shared__ int32_t spos[kMaxCand];
   // members [R blk, R blk + R); candidate fragments of slice `part`
   const int j = j0 + blockIdx.x, b = blockIdx.y, blk = blockIdx.z / parts, part = blockIdx.z % parts;
-  if (b >= st.n || j >= n_groups || j < st.first_proxy[b]) return;
-  const int gs = min(g, n_q - j * g);
+  if (b >= st.n || j >= seq_groups(st, b, g) || j < st.first_proxy[b]) return;
+  const int gs = min(g, st.n_rows[b] - j * g);
   if (R * blk >= gs) return;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
@@ -50,17 +50,23 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void r
   // without a window only the first t0 + 1 slots can hold a position
   const int nc = all_slots ? c : (int)min((int64_t)c, t0 + 1);
   const int rows_here = min(R, gs - R * blk);
-  const int32_t* crow = cand + ((int64_t)b * n_groups + j) * c;
-  const int64_t r0 = (int64_t)b * n_q + (int64_t)j * g + R * blk;
-  const uint8_t* kb = k + (int64_t)b * k_seq_stride * kD * EB;
-  const float* ksb = DT == kFp8 ? k_scale + (int64_t)b * k_seq_stride : nullptr;
+  const int64_t grp = (int64_t)st.grp0[b] + j;
+  const int32_t* crow = cand + grp * c;
+  const int64_t r0 = (int64_t)st.row0[b] + (int64_t)j * g + R * blk;
+  // contiguous keys: the sequence's base, staged positions; paged keys: the
+  // pool, positions staged as pool rows (empty slots as key 0's row)
+  const uint8_t* kb = km.pages ? k : k + km.row(b, 0) * kD * EB;
+  const float* ksb = DT == kFp8 ? (km.pages ? k_scale : k_scale + km.row(b, 0)) : nullptr;
   const int lr = lane & 15, kg = lane >> 4;
   const int nfrag_all = (nc + 15) >> 4;
   const int fpp = (nfrag_all + parts - 1) / parts;
   const int fbeg = min(nfrag_all, part * fpp), fend = min(nfrag_all, fbeg + fpp);
   if (fbeg >= fend) return;
   const int cbeg = 16 * fbeg, ncs = min(nc, 16 * fend) - cbeg;  // this slice's candidates
-  for (int e = tid; e < ncs; e += 256) spos[e] = crow[cbeg + e];
+  if (km.pages)
+    for (int e = tid; e < ncs; e += 256) spos[e] = (int32_t)km.row(b, max(crow[cbeg + e], 0));
+  else
+    for (int e = tid; e < ncs; e += 256) spos[e] = crow[cbeg + e];
 
   const uint8_t* rows[R];
   const float* wrows[R];
@@ -86,7 +92,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void r
   // lanes with nothing to store give an offset past its end (dropped), so
   // every lane issues the same memory operations and the waits stay exact
   const __amdgpu_buffer_rsrc_t orr =
-      buffer_rsrc(rsc + (((int64_t)b * n_groups + j) * g + R * blk) * (int64_t)c, (uint32_t)(R * c * 4));
+      buffer_rsrc(rsc + (grp * g + R * blk) * (int64_t)c, (uint32_t)(R * c * 4));
   const uint32_t my_off = (uint32_t)(qr * c + cbeg) * 4u;
   const int nfrag = fend - fbeg;
   constexpr int S = 4;  // fragment stride between the waves
@@ -145,25 +151,25 @@ struct SlotRule {
 
 template <int V>
 __global__ __launch_bounds__(256) void topk_short_kernel(const float* __restrict__ rsc,
-                                                         const int32_t* __restrict__ cand, int n_q, int g,
-                                                         int n_groups, SeqTable st, int j0, int c, SlotRule rule,
-                                                         int m, int32_t* __restrict__ out_idx) {
+                                                         const int32_t* __restrict__ cand, int g, SeqTable st,
+                                                         int j0, int c, SlotRule rule, int m,
+                                                         int32_t* __restrict__ out_idx) {
   __shared__ SelectShared sel;
   __shared__ uint32_t hist[4 * 256];  // bucket_select's histogram, then its list
   __shared__ int32_t lcount, nvalid_sh;
   const int j = j0 + blockIdx.x, b = blockIdx.y, member = blockIdx.z;
-  if (b >= st.n || j >= n_groups || j < st.first_proxy[b]) return;
-  const int gs = min(g, n_q - j * g);
+  if (b >= st.n || j >= seq_groups(st, b, g) || j < st.first_proxy[b]) return;
+  const int gs = min(g, st.n_rows[b] - j * g);
   if (member >= gs) return;
   const int tid = threadIdx.x;
   const int64_t t0 = (int64_t)st.q_pos0[b] + (int64_t)j * g;
   const int64_t tt = t0 + member;
   const bool win = rule.window > 0;
   const int nc = win ? c : (int)min((int64_t)c, t0 + 1);
-  const int64_t grp = (int64_t)b * n_groups + j;
+  const int64_t grp = (int64_t)st.grp0[b] + j;
   const float* srow = rsc + (grp * g + member) * (int64_t)c;
   const int32_t* crow = cand + grp * c;
-  int32_t* orow = out_idx + ((int64_t)b * n_q + (int64_t)j * g + member) * m;
+  int32_t* orow = out_idx + ((int64_t)st.row0[b] + (int64_t)j * g + member) * m;
 
   RegSource<V> src;
   int mine = 0;
@@ -236,17 +242,16 @@ __global__ __launch_bounds__(256) void topk_short_kernel(const float* __restrict
 // groups [j0, j1) with j >= first_proxy[b] takes position t0 - W + 1 + u, or
 // -1 below 0, past the group's last member, or (dedupe) when it is already
 // among the row's first slot0 slots.
-__global__ __launch_bounds__(256) void window_kernel(int32_t* __restrict__ cand, int n_q, int g, int n_groups,
-                                                     SeqTable st, int j0, int width, int slot0, int W, int wg,
-                                                     int dedupe) {
+__global__ __launch_bounds__(256) void window_kernel(int32_t* __restrict__ cand, int g, SeqTable st, int j0,
+                                                     int width, int slot0, int W, int wg, int dedupe) {
   __shared__ uint8_t seen[kMaxCand];
   const int j = j0 + blockIdx.x, b = blockIdx.y;
-  if (b >= st.n || j >= n_groups || j < st.first_proxy[b]) return;
+  if (b >= st.n || j >= seq_groups(st, b, g) || j < st.first_proxy[b]) return;
   const int tid = threadIdx.x;
-  const int gs = min(g, n_q - j * g);
+  const int gs = min(g, st.n_rows[b] - j * g);
   const int64_t t0 = (int64_t)st.q_pos0[b] + (int64_t)j * g;
   const int64_t lo = t0 - W + 1;
-  int32_t* row = cand + ((int64_t)b * n_groups + j) * width;
+  int32_t* row = cand + ((int64_t)st.grp0[b] + j) * width;
   if (dedupe) {
     for (int u = tid; u < wg; u += 256) seen[u] = 0;
     __syncthreads();
@@ -263,21 +268,20 @@ __global__ __launch_bounds__(256) void window_kernel(int32_t* __restrict__ cand,
   }
 }
 
-hipError_t launch_window(int32_t* cand, int n_q, int g, int n_groups, const SeqTable& st, int j0, int j1, int width,
-                         int slot0, int W, bool dedupe, hipStream_t stream) {
+hipError_t launch_window(int32_t* cand, int g, const SeqTable& st, int j0, int j1, int width, int slot0, int W,
+                         bool dedupe, hipStream_t stream) {
   const int wg = W + g - 1;
   if (j1 <= j0 || st.n <= 0 || W <= 0) return hipSuccess;
   if (width > kMaxCand || slot0 < 0 || slot0 + wg > width) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(window_kernel, dim3((unsigned)(j1 - j0), (unsigned)st.n), dim3(256), 0, stream, cand, n_q, g,
-                     n_groups, st, j0, width, slot0, W, wg, (int)dedupe);
+  hipLaunchKernelGGL(window_kernel, dim3((unsigned)(j1 - j0), (unsigned)st.n), dim3(256), 0, stream, cand, g, st, j0,
+                     width, slot0, W, wg, (int)dedupe);
   return hipGetLastError();
 }
 
 hipError_t launch_refine(int dtype, const void* q, const float* q_scale, const float* w, const uint8_t* lin,
-                         const float* lin_scale, int n_q, int g, int n_groups, const void* k,
-                         const float* k_scale, int64_t k_seq_stride, const SeqTable& st, int j0, int j1,
-                         const int32_t* cand, int c, int W, int wslot, int m, float* rescore, int32_t* out_idx,
-                         hipStream_t stream) {
+                         const float* lin_scale, int g, const void* k, const float* k_scale, const KeyMap& km,
+                         const SeqTable& st, int j0, int j1, const int32_t* cand, int c, int W, int wslot, int m,
+                         float* rescore, int32_t* out_idx, hipStream_t stream) {
   if (j1 <= j0 || st.n <= 0) return hipSuccess;
   if (c > kMaxCand) return hipErrorInvalidValue;
   const SlotRule rule{W, wslot};
@@ -291,26 +295,26 @@ hipError_t launch_refine(int dtype, const void* q, const float* q_scale, const f
   const dim3 grid((unsigned)(j1 - j0), (unsigned)st.n, (unsigned)(((g + R - 1) / R) * parts));
   if (dtype == kFp8)
     hipLaunchKernelGGL((rescore_kernel<kFp8, 4>), grid, dim3(256), 0, stream, (const uint8_t*)q, q_scale, w, lin,
-                       lin_scale, n_q, g, n_groups, (const uint8_t*)k, k_scale, k_seq_stride, st, j0, cand, c,
+                       lin_scale, g, (const uint8_t*)k, k_scale, km, st, j0, cand, c,
                        all_slots, parts, rescore);
   else
     hipLaunchKernelGGL((rescore_kernel<kBf16, 2>), grid, dim3(256), 0, stream, (const uint8_t*)q, q_scale, w, lin,
-                       lin_scale, n_q, g, n_groups, (const uint8_t*)k, nullptr, k_seq_stride, st, j0, cand, c,
+                       lin_scale, g, (const uint8_t*)k, nullptr, km, st, j0, cand, c,
                        all_slots, parts, rescore);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   dim3 sgrid((unsigned)(j1 - j0), (unsigned)st.n, (unsigned)g);
   if (c <= 1024)
-    hipLaunchKernelGGL(topk_short_kernel<4>, sgrid, dim3(256), 0, stream, rescore, cand, n_q, g, n_groups, st, j0, c,
+    hipLaunchKernelGGL(topk_short_kernel<4>, sgrid, dim3(256), 0, stream, rescore, cand, g, st, j0, c,
                        rule, m, out_idx);
   else if (c <= 4096)
-    hipLaunchKernelGGL(topk_short_kernel<16>, sgrid, dim3(256), 0, stream, rescore, cand, n_q, g, n_groups, st, j0,
+    hipLaunchKernelGGL(topk_short_kernel<16>, sgrid, dim3(256), 0, stream, rescore, cand, g, st, j0,
                        c, rule, m, out_idx);
   else if (c <= 5120)  // c = 4096 plus a window union
-    hipLaunchKernelGGL(topk_short_kernel<20>, sgrid, dim3(256), 0, stream, rescore, cand, n_q, g, n_groups, st, j0,
+    hipLaunchKernelGGL(topk_short_kernel<20>, sgrid, dim3(256), 0, stream, rescore, cand, g, st, j0,
                        c, rule, m, out_idx);
   else
-    hipLaunchKernelGGL(topk_short_kernel<32>, sgrid, dim3(256), 0, stream, rescore, cand, n_q, g, n_groups, st, j0,
+    hipLaunchKernelGGL(topk_short_kernel<32>, sgrid, dim3(256), 0, stream, rescore, cand, g, st, j0,
                        c, rule, m, out_idx);
   return hipGetLastError();
 }

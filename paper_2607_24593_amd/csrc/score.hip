@@ -22,14 +22,18 @@
 
 namespace pivot {
 
-template <int DT, int R, bool KSPLIT>
+// A key offset past every paged pool (pools stay below 2^31 bytes): its
+// loads read zeros, and adding a fragment's lane offset cannot wrap it.
+constexpr uint32_t kDropOffset = 0x80000000u;
+
+template <int DT, int R, bool KSPLIT, bool PAGED>
 __global__ __launch_bounds__(256) void score_kernel(const uint8_t* __restrict__ q,
                                                     const float* __restrict__ q_scale,
                                                     const float* __restrict__ w,
                                                     const uint8_t* __restrict__ lin,
-                                                    const float* __restrict__ lin_scale, int64_t q_seq_rows,
+                                                    const float* __restrict__ lin_scale,
                                                     const uint8_t* __restrict__ k,
-                                                    const float* __restrict__ k_scale, int64_t k_seq_stride,
+                                                    const float* __restrict__ k_scale, KeyMap km,
                                                     SeqTable st, RowSpace rs, float* __restrict__ out,
                                                     int64_t ld, int seg_keys) {
   using Tile = RowTile<DT, R>;
@@ -66,10 +70,10 @@ __global__ __launch_bounds__(256) void score_kernel(const uint8_t* __restrict__ 
   const uint8_t* lrows[R];
   const float* lsc[R];
   float qs[R];
+  const int last = row_count(st, rs, b) - 1;  // >= 0: the workgroup has an active row
 #pragma unroll
   for (int r = 0; r < R; ++r) {
-    int64_t i = min((int64_t)(i_w + r), q_seq_rows - 1);
-    int64_t row = (int64_t)b * q_seq_rows + i;
+    const int64_t row = row_index(st, rs, b, min(i_w + r, last));
     rows[r] = q + row * Tile::ROW_BYTES;
     wrows[r] = w + row * kH;
     qs[r] = (DT == kFp8) ? q_scale[row] : 1.0f;
@@ -82,26 +86,40 @@ __global__ __launch_bounds__(256) void score_kernel(const uint8_t* __restrict__ 
   // overlap and the scales can be written to LDS without waiting for the rest.
   constexpr int KS_PER = 4096 / 256;
   float ksv[KS_PER];
-  if constexpr (DT == kFp8) {
-    const __amdgpu_buffer_rsrc_t ksr = buffer_rsrc(k_scale + (int64_t)b * k_seq_stride + seg0, (uint32_t)nseg_keys * 4);
+  if constexpr (DT == kFp8 && !PAGED) {
+    const __amdgpu_buffer_rsrc_t ksr = buffer_rsrc(k_scale + km.row(b, seg0), (uint32_t)nseg_keys * 4);
 #pragma unroll
     for (int u = 0; u < KS_PER; ++u)
       ksv[u] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(ksr, (uint32_t)(tid + 256 * u) * 4u, 0, 0));
   }
+  if constexpr (DT == kFp8 && PAGED) {  // gathered through the page table
+#pragma unroll
+    for (int u = 0; u < KS_PER; ++u) {
+      const int e = tid + 256 * u;
+      ksv[u] = e < nseg_keys ? k_scale[km.row(b, seg0 + e)] : 0.0f;
+    }
+  }
   Tile tile;
   tile.load(rows, wrows, qs, lrows, lsc, lane);
 
-  // keys of the segment through a range-checked buffer resource: offsets are
-  // 32-bit and fragments that run past the wave's last key read zeros
+  // keys through a range-checked buffer resource with 32-bit offsets: the
+  // segment's contiguous keys (fragments that run past the wave's last key
+  // read zeros), or the page pool (keys past the wave's last one are sent to
+  // kDropOffset)
   const __amdgpu_buffer_rsrc_t kr =
-      buffer_rsrc(k + ((int64_t)b * k_seq_stride + seg0) * KB, (uint32_t)nkeys * KB);
+      PAGED ? buffer_rsrc(k, (uint32_t)(((int64_t)km.n_pages << km.shift) * KB))
+            : buffer_rsrc(k + km.row(b, seg0) * KB, (uint32_t)nkeys * KB);
+  auto key_off = [&](int e) -> uint32_t {  // e: key index within the segment
+    if constexpr (PAGED) return e < nkeys ? (uint32_t)(km.row(b, seg0 + e) * KB) : kDropOffset;
+    else return (uint32_t)e * KB;
+  };
   const int S = KSPLIT ? 64 : 16;
   int t = KSPLIT ? 16 * wave : 0;  // key offset within the segment
   const int lr0 = lane & 15, kg0 = lane >> 4;
   KeyFrag<DT> f0, f1, f2;
-  f0.load(kr, (uint32_t)(t + lr0) * KB, kg0);
-  f1.load(kr, (uint32_t)(t + S + lr0) * KB, kg0);
-  f2.load(kr, (uint32_t)(t + 2 * S + lr0) * KB, kg0);
+  f0.load(kr, key_off(t + lr0), kg0);
+  f1.load(kr, key_off(t + S + lr0), kg0);
+  f2.load(kr, key_off(t + 2 * S + lr0), kg0);
 
   if constexpr (DT == kFp8) {
 #pragma unroll
@@ -136,11 +154,11 @@ __global__ __launch_bounds__(256) void score_kernel(const uint8_t* __restrict__ 
   // their stores are dropped.
   for (; t < nkeys; t += 3 * S) {
     emit(tile.score(f0), t);
-    f0.load(kr, (uint32_t)(t + 3 * S + lr) * KB, kg);
+    f0.load(kr, key_off(t + 3 * S + lr), kg);
     emit(tile.score(f1), t + S);
-    f1.load(kr, (uint32_t)(t + 4 * S + lr) * KB, kg);
+    f1.load(kr, key_off(t + 4 * S + lr), kg);
     emit(tile.score(f2), t + 2 * S);
-    f2.load(kr, (uint32_t)(t + 5 * S + lr) * KB, kg);
+    f2.load(kr, key_off(t + 5 * S + lr), kg);
   }
 }
 
@@ -150,7 +168,7 @@ constexpr int64_t kTargetWorkgroups = 2048;
 
 template <int DT, int R, bool KSPLIT>
 static hipError_t run_score(const void* q, const float* qs, const float* w, const uint8_t* lin, const float* lsc,
-                            int64_t q_seq_rows, const void* k, const float* ks, int64_t kstride, const SeqTable& st,
+                            const void* k, const float* ks, const KeyMap& km, const SeqTable& st,
                             const RowSpace& rs, int64_t lim_max, float* out, int64_t ld, int max_seg,
                             hipStream_t stream) {
   constexpr int RB = KSPLIT ? R : 4 * R;
@@ -162,38 +180,41 @@ static hipError_t run_score(const void* q, const float* qs, const float* w, cons
   while (seg > 512 && nblk * ((lim_max + seg) / seg) < kTargetWorkgroups) seg >>= 1;
   const int64_t nseg = (lim_max + seg) / seg;
   if (nseg > 0x7FFFFFFF || nblk > 65535) return hipErrorInvalidConfiguration;
-  hipLaunchKernelGGL((score_kernel<DT, R, KSPLIT>), dim3((unsigned)nseg, (unsigned)nblk), dim3(256), 0, stream,
-                     (const uint8_t*)q, qs, w, lin, lsc, q_seq_rows, (const uint8_t*)k, ks, kstride, st, rs, out,
-                     ld, seg);
+  if (km.pages)
+    hipLaunchKernelGGL((score_kernel<DT, R, KSPLIT, true>), dim3((unsigned)nseg, (unsigned)nblk), dim3(256), 0,
+                       stream, (const uint8_t*)q, qs, w, lin, lsc, (const uint8_t*)k, ks, km, st, rs, out, ld, seg);
+  else
+    hipLaunchKernelGGL((score_kernel<DT, R, KSPLIT, false>), dim3((unsigned)nseg, (unsigned)nblk), dim3(256), 0,
+                       stream, (const uint8_t*)q, qs, w, lin, lsc, (const uint8_t*)k, ks, km, st, rs, out, ld, seg);
   return hipGetLastError();
 }
 
 hipError_t launch_score(int dtype, const void* q, const float* q_scale, const float* w, const uint8_t* lin,
-                        const float* lin_scale, int64_t q_seq_rows, const void* k, const float* k_scale,
-                        int64_t k_seq_stride, const SeqTable& st, const RowSpace& rs, int64_t lim_max, float* out,
-                        int64_t ld, hipStream_t stream) {
+                        const float* lin_scale, const void* k, const float* k_scale, const KeyMap& km,
+                        const SeqTable& st, const RowSpace& rs, int64_t lim_max, float* out, int64_t ld,
+                        hipStream_t stream) {
   const int nrows = rs.i1 - rs.i0;
   if (nrows <= 0 || lim_max < 0 || st.n <= 0) return hipSuccess;
   if (dtype == kFp8) {
     if (nrows >= 16)
-      return run_score<kFp8, 4, false>(q, q_scale, w, lin, lin_scale, q_seq_rows, k, k_scale, k_seq_stride, st, rs, lim_max,
+      return run_score<kFp8, 4, false>(q, q_scale, w, lin, lin_scale, k, k_scale, km, st, rs, lim_max,
                                        out, ld, 4096, stream);
     if (nrows == 1)
-      return run_score<kFp8, 1, true>(q, q_scale, w, lin, lin_scale, q_seq_rows, k, k_scale, k_seq_stride, st, rs, lim_max,
+      return run_score<kFp8, 1, true>(q, q_scale, w, lin, lin_scale, k, k_scale, km, st, rs, lim_max,
                                       out, ld, 2048, stream);
     if (nrows == 2)
-      return run_score<kFp8, 2, true>(q, q_scale, w, lin, lin_scale, q_seq_rows, k, k_scale, k_seq_stride, st, rs, lim_max,
+      return run_score<kFp8, 2, true>(q, q_scale, w, lin, lin_scale, k, k_scale, km, st, rs, lim_max,
                                       out, ld, 2048, stream);
-    return run_score<kFp8, 4, true>(q, q_scale, w, lin, lin_scale, q_seq_rows, k, k_scale, k_seq_stride, st, rs, lim_max, out,
+    return run_score<kFp8, 4, true>(q, q_scale, w, lin, lin_scale, k, k_scale, km, st, rs, lim_max, out,
                                     ld, 2048, stream);
   }
   if (nrows >= 16)
-    return run_score<kBf16, 2, false>(q, nullptr, w, nullptr, nullptr, q_seq_rows, k, nullptr, k_seq_stride, st, rs, lim_max,
+    return run_score<kBf16, 2, false>(q, nullptr, w, nullptr, nullptr, k, nullptr, km, st, rs, lim_max,
                                       out, ld, 2048, stream);
   if (nrows == 1)
-    return run_score<kBf16, 1, true>(q, nullptr, w, nullptr, nullptr, q_seq_rows, k, nullptr, k_seq_stride, st, rs, lim_max,
+    return run_score<kBf16, 1, true>(q, nullptr, w, nullptr, nullptr, k, nullptr, km, st, rs, lim_max,
                                      out, ld, 2048, stream);
-  return run_score<kBf16, 2, true>(q, nullptr, w, nullptr, nullptr, q_seq_rows, k, nullptr, k_seq_stride, st, rs, lim_max, out,
+  return run_score<kBf16, 2, true>(q, nullptr, w, nullptr, nullptr, k, nullptr, km, st, rs, lim_max, out,
                                    ld, 2048, stream);
 }
 

@@ -183,13 +183,13 @@ struct RowDest {
   int64_t dest0;
   int ndest;
   int ld;
-  __device__ RowDest(const OutDesc& od, int b, int i) : base(od.base), ld(od.ld) {
+  __device__ RowDest(const OutDesc& od, const SeqTable& st, int b, int i) : base(od.base), ld(od.ld) {
     if (od.fan_g == 0) {
-      dest0 = (int64_t)b * od.per_seq + i;
+      dest0 = (int64_t)(od.groups ? st.grp0[b] : st.row0[b]) + i;
       ndest = 1;
     } else {
-      dest0 = (int64_t)b * od.per_seq + (int64_t)i * od.fan_g;
-      ndest = min(od.fan_g, od.fan_n - i * od.fan_g);
+      dest0 = (int64_t)st.row0[b] + (int64_t)i * od.fan_g;
+      ndest = min(od.fan_g, st.n_rows[b] - i * od.fan_g);
     }
   }
   __device__ __forceinline__ void operator()(int p, int32_t v) const {
@@ -211,7 +211,7 @@ __global__ __launch_bounds__(T) void topk_rows_kernel(const float* __restrict__ 
   const int n = (int)max((int64_t)0, n64);
   const float* row = scores + ((int64_t)b * nrows + (i - rs.i0)) * ld;
   const int m = od.m;
-  const RowDest put(od, b, i);
+  const RowDest put(od, st, b, i);
   if (n <= m) {
     for (int p = tid; p < m; p += T) put(p, p < n ? p : -1);
     return;
@@ -340,7 +340,7 @@ __global__ __launch_bounds__(T) void topk_merge_kernel(const float* __restrict__
   const int n = (int)max((int64_t)0, row_limit(st, rs, b, i) + 1);
   const float* row = scores + ((int64_t)b * nrows + (i - rs.i0)) * ld;
   const int m = od.m;
-  const RowDest put(od, b, i);
+  const RowDest put(od, st, b, i);
   if (n <= m) {
     for (int p = tid; p < m; p += T) put(p, p < n ? p : -1);
     return;
@@ -442,18 +442,18 @@ hipError_t launch_topk(const float* scores, int64_t ld, const SeqTable& st, cons
   return hipGetLastError();
 }
 
-__global__ void fill_guardrail_kernel(int32_t* base, int per_seq, int width, SeqTable st, int j0, int32_t value) {
+__global__ void fill_guardrail_kernel(int32_t* base, int width, SeqTable st, int j0, int32_t value) {
   const int j = j0 + blockIdx.x, b = blockIdx.y;
   if (b >= st.n || j >= st.first_proxy[b]) return;
-  int32_t* row = base + ((int64_t)b * per_seq + j) * width;
+  int32_t* row = base + ((int64_t)st.grp0[b] + j) * width;
   for (int e = threadIdx.x; e < width; e += blockDim.x) row[e] = value;
 }
 
-hipError_t launch_fill_guardrail(int32_t* base, int per_seq, int width, const SeqTable& st, int j0, int j1,
-                                 int32_t value, hipStream_t stream) {
+hipError_t launch_fill_guardrail(int32_t* base, int width, const SeqTable& st, int j0, int j1, int32_t value,
+                                 hipStream_t stream) {
   if (j1 <= j0 || st.n <= 0) return hipSuccess;
   hipLaunchKernelGGL(fill_guardrail_kernel, dim3((unsigned)(j1 - j0), (unsigned)st.n), dim3(256), 0, stream, base,
-                     per_seq, width, st, j0, value);
+                     width, st, j0, value);
   return hipGetLastError();
 }
 

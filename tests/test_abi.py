@@ -168,6 +168,78 @@ def test_cand_width_and_window_workspace():
     assert pv.pivot_group_workspace_size(a, opts(window=3, kind=pv.PIVOT_WINDOW_PER_QUERY)) == 0  # invalid
 
 
+def layout(cu_q=None, page_size=0, pool_keys=0, max_pages=0, table=False):
+    lo = pv.pivot_layout()
+    if cu_q is not None:
+        lo._cu = (ctypes.c_int32 * len(cu_q))(*cu_q)
+        lo.cu_q = ctypes.cast(lo._cu, ctypes.POINTER(ctypes.c_int32))
+    if table:
+        lo.block_table = FAKE
+        lo.max_pages, lo.page_size, lo.pool_keys = max_pages, page_size, pool_keys
+    return lo
+
+
+def dense_layout(a, lo):
+    return pv.lib().pivot_dense_index_layout(ctypes.byref(a), ctypes.byref(lo))
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(cu_q=[1, 64]), pv.PIVOT_ERR_INVALID_ARG),                          # cu_q[0] != 0
+    (dict(cu_q=[0, 40, 30]), pv.PIVOT_ERR_INVALID_ARG),                      # decreasing
+    (dict(cu_q=[0, 40, 80]), pv.PIVOT_ERR_INVALID_ARG),                      # run 2 needs n_k >= 40
+    (dict(table=True, page_size=24, pool_keys=96, max_pages=4), pv.PIVOT_ERR_INVALID_ARG),   # not a power of 2
+    (dict(table=True, page_size=8, pool_keys=96, max_pages=8), pv.PIVOT_ERR_INVALID_ARG),    # below 16
+    (dict(table=True, page_size=16, pool_keys=100, max_pages=4), pv.PIVOT_ERR_INVALID_ARG),  # not a multiple
+    (dict(table=True, page_size=16, pool_keys=64, max_pages=2), pv.PIVOT_ERR_INVALID_ARG),   # n_k=64 > 2 pages
+    (dict(table=True, page_size=16, pool_keys=64, max_pages=0), pv.PIVOT_ERR_INVALID_ARG),
+    (dict(table=True, page_size=16, pool_keys=(1 << 24) + 16, max_pages=4), pv.PIVOT_ERR_UNSUPPORTED),  # > 2^31 B
+    (dict(table=True, page_size=16, pool_keys=64, max_pages=4), pv.PIVOT_ERR_WORKSPACE),     # valid
+    (dict(cu_q=[0, 64], table=True, page_size=64, pool_keys=128, max_pages=1), pv.PIVOT_ERR_WORKSPACE),
+])
+def test_layout_validation(kw, status):
+    B = len(kw["cu_q"]) - 1 if "cu_q" in kw else 1
+    a = args(B=B, ws_bytes=0)
+    if B == 2:
+        a._pos = (ctypes.c_int32 * 2)(0, 0)
+        a._nk = (ctypes.c_int32 * 2)(64, 30)
+        a.q_pos0 = ctypes.cast(a._pos, ctypes.POINTER(ctypes.c_int32))
+        a.n_k = ctypes.cast(a._nk, ctypes.POINTER(ctypes.c_int32))
+    lo = layout(**kw)
+    assert dense_layout(a, lo) == status
+    assert pv.lib().pivot_group_index_layout(ctypes.byref(a), ctypes.byref(lo), ctypes.byref(opts())) == status
+
+
+def test_layout_workspace_sizes():
+    """A one-run varlen layout sizes as the padded call; a ragged batch sizes its
+    candidate rows by the sum of its runs' groups."""
+    up = lambda n: (n + 255) // 256 * 256  # noqa: E731
+    a = args(n_q=100, q_pos0=900)
+    lo = layout(cu_q=[0, 100])
+    L = pv.lib()
+    for o in (None, opts(db=16), opts(mode=pv.PIVOT_REUSE, db=16)):
+        ob = None if o is None else ctypes.byref(o)
+        ref = pv.pivot_workspace_size(a, pv.PIVOT_DENSE) if o is None else pv.pivot_group_workspace_size(a, o)
+        assert L.pivot_workspace_size_layout(ctypes.byref(a), ctypes.byref(lo), ob) == ref
+    assert L.pivot_workspace_size_layout(ctypes.byref(a), None, None) == pv.pivot_workspace_size(a, pv.PIVOT_DENSE)
+    # two runs of 10 and 7 rows: 3 + 2 groups of 4, 17 query rows; the score
+    # tile holds both sequences' 3 group rows of ld(910) = 960 floats
+    lin = lambda rows: up(rows * 512) + up(rows * 16)  # noqa: E731
+    b = args(B=2, n_q=10, q_pos0=900)
+    ragged = L.pivot_workspace_size_layout(ctypes.byref(b), ctypes.byref(layout(cu_q=[0, 10, 17])),
+                                           ctypes.byref(opts(db=16)))
+    ng = 5
+    proxies = up(ng * 64 * 128) + up(ng * 4) + up(ng * 64 * 4)
+    cand = up(ng * 16 * 4) + up(ng * 4 * 16 * 4)
+    assert ragged == lin(17) + lin(ng) + proxies + cand + 2 * 3 * 960 * 4
+
+
+def test_empty_runs_need_no_workspace():
+    a = args(B=2, ws_bytes=0, ws_addr=None)
+    lo = layout(cu_q=[0, 0, 0])
+    assert dense_layout(a, lo) == pv.PIVOT_OK
+    assert pv.lib().pivot_group_index_layout(ctypes.byref(a), ctypes.byref(lo), ctypes.byref(opts())) == pv.PIVOT_OK
+
+
 def test_workspace_checks():
     a = args(ws_bytes=0)
     assert dense(a) == pv.PIVOT_ERR_WORKSPACE
