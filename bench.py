@@ -10,7 +10,8 @@ top-c, and the per-member gather / re-score / top-k.  Inputs are synthetic
 Reported besides the headline queries/s: the dense indexer and PIVOT-Reuse on
 the same prefill (speedup), a group-size sweep, Refine with App. B's local
 window (W=4), MTP decode (32 x 131072 cached keys, g=2, also with the
-per-query window), per-kernel times from HIP events recorded around each launch
+per-query window), the batch layouts (paged decode keys, a packed batch of
+four prefill requests), per-kernel times from HIP events recorded around each launch
 inside the timed steps, the roofline fraction of the dominant kernel, and the
 CPU oracle timed on a sample of the same workload.
 
@@ -182,6 +183,89 @@ def decode_bench(reps):
     return res
 
 
+def layout_bench(reps):
+    """The batch layouts: the 32 x 131072-key decode with keys in a paged pool
+    (pages of 64 keys, shuffled) against the same keys contiguous, and a
+    prefill batch of four requests (8K, 16K, 24K and 32K fp8 tokens, their
+    last 4096 queries each) as one packed call against one call per request."""
+    import numpy as np
+    import torch
+    import paper_2607_24593_amd as pv
+    from workload.gen import WORKLOADS, make, make_prefill
+    res = {}
+    wl = WORKLOADS["decode-32x128k-fp8"]
+    x = make(wl, threads=16)
+    B, L, g = wl.batch, wl.L, wl.g[0]
+    d = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()  # noqa: E731
+    q, qs, w = d(x.q), d(x.q_scale), d(x.w)
+    page = 64
+    per = L // page
+    perm = np.random.default_rng(0).permutation(B * per).astype(np.int32)
+    table = perm.reshape(B, per)
+    pool = np.empty((B * per * page, x.k.shape[2]), dtype=x.k.dtype)
+    pool_s = np.empty(B * per * page, dtype=np.float32)
+    kv = x.k.reshape(B, per, page, -1)
+    sv = x.k_scale.reshape(B, per, page)
+    for b in range(B):
+        pool.reshape(B * per, page, -1)[table[b]] = kv[b]
+        pool_s.reshape(B * per, page)[table[b]] = sv[b]
+    k, ks, kp, ksp, bt = d(x.k), d(x.k_scale), d(pool), d(pool_s), d(table)
+    lay = pv.make_layout(cu_q=[g * b for b in range(B + 1)], block_table=bt, page_size=page, pool_keys=pool.shape[0])
+    pos, nk = [L - g] * B, [L] * B
+    out = torch.empty((B, g, wl.topk), dtype=torch.int32, device="cuda")
+    outf = out.view(B * g, wl.topk)
+    qf, qsf, wf = q.view(B * g, 64, 128), qs.view(B * g), w.view(B * g, 64)
+    dec = {}
+    for mode in ("dense", "reuse", "refine"):
+        if mode == "dense":
+            fc = lambda: pv.pivot_dense_index(q, qs, w, k, ks, pos, nk, wl.topk, out=out)  # noqa: E731
+            fp = lambda: pv.pivot_dense_index_layout(qf, qsf, wf, kp, ksp, pos, nk, wl.topk, lay, out=outf)  # noqa
+        else:
+            m = pv.PIVOT_REUSE if mode == "reuse" else pv.PIVOT_REFINE
+            fc = lambda m=m: pv.pivot_group_index(q, qs, w, k, ks, pos, nk, wl.topk, mode=m, g=g, c=wl.c,  # noqa
+                                                  out=out)
+            fp = lambda m=m: pv.pivot_group_index_layout(qf, qsf, wf, kp, ksp, pos, nk, wl.topk, lay, mode=m,  # noqa
+                                                         g=g, c=wl.c, out=outf)
+        fc(); fp()  # noqa: E702
+        tc, tp = timed(fc, reps), timed(fp, reps)
+        dec[mode] = {"contiguous_us": tc * 1e6, "paged_us": tp * 1e6, "paged_over_contiguous": tp / tc}
+    res["decode_paged"] = dec
+    # a prefill batch of four requests
+    lens = [8192, 16384, 24576, 32768]
+    n_last = 4096
+    xs = [make_prefill(Lr, "fp8", seed=123 + i, threads=16) for i, Lr in enumerate(lens)]
+    qp = d(np.concatenate([xr.q[Lr - n_last:] for xr, Lr in zip(xs, lens)]))
+    qsp = d(np.concatenate([xr.q_scale[Lr - n_last:] for xr, Lr in zip(xs, lens)]))
+    wp = d(np.concatenate([xr.w[Lr - n_last:] for xr, Lr in zip(xs, lens)]))
+    S = max(lens)
+    kb = np.zeros((len(lens), S, 128), dtype=np.uint8)
+    kbs = np.zeros((len(lens), S), dtype=np.float32)
+    for i, (xr, Lr) in enumerate(zip(xs, lens)):
+        kb[i, :Lr] = xr.k
+        kbs[i, :Lr] = xr.k_scale
+    kb_t, kbs_t = d(kb), d(kbs)
+    cu = [n_last * i for i in range(len(lens) + 1)]
+    lay2 = pv.make_layout(cu_q=cu)
+    pos2, nk2 = [Lr - n_last for Lr in lens], lens
+    outp = torch.empty((n_last * len(lens), 2048), dtype=torch.int32, device="cuda")
+
+    def packed():
+        pv.pivot_group_index_layout(qp, qsp, wp, kb_t, kbs_t, pos2, nk2, 2048, lay2, mode=pv.PIVOT_REFINE, g=4,
+                                    c=4096, out=outp)
+
+    def separate():
+        for i, Lr in enumerate(lens):
+            sl = slice(cu[i], cu[i + 1])
+            pv.pivot_group_index(qp[sl], qsp[sl], wp[sl], kb_t[i, :Lr], kbs_t[i, :Lr], Lr - n_last, Lr, 2048,
+                                 mode=pv.PIVOT_REFINE, g=4, c=4096, out=outp[sl])
+    packed(); separate()  # noqa: E702
+    tpk, tsep = timed(packed, reps), timed(separate, reps)
+    res["prefill_batch"] = {"requests": lens, "queries_each": n_last, "mode": "refine g=4 c=4096 k=2048",
+                            "packed_ms": tpk * 1e3, "per_request_calls_ms": tsep * 1e3,
+                            "packed_queries_per_s": n_last * len(lens) / tpk}
+    return res
+
+
 def cpu_baseline(pf, g, budget_s=12.0, max_groups=4096):
     """The oracle (C, fp64, OpenMP) on a sample of PIVOT-Refine groups of the same
     prefill: groups at uniformly random positions past the guardrail, drawn until
@@ -257,6 +341,7 @@ def main():
     ap.add_argument("--reps", type=int, default=2, help="passes per mode for the comparison table")
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--no-layouts", action="store_true", help="skip the paged / packed-batch measurement")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-compare", action="store_true", help="skip the dense / Reuse / sweep passes")
     ap.add_argument("--score-tile-mb", type=int, default=None,
@@ -354,6 +439,7 @@ def main():
         log(f"refine g={g} W=4: {s * 1e3:.2f} ms ({dense_s / s:.2f}x)")
 
     dec = None if args.no_decode else decode_bench(reps=50)
+    layouts = None if args.no_layouts else layout_bench(reps=20)
     cpu = None if args.no_cpu_baseline else cpu_baseline(pf, g)
 
     line = {
@@ -378,6 +464,7 @@ def main():
         "kernels": kern,
         "modes": modes,
         "decode": dec,
+        "layouts": layouts,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

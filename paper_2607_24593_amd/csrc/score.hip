@@ -41,6 +41,8 @@ __global__ __launch_bounds__(256) void score_kernel(const uint8_t* __restrict__ 
   constexpr int KB = kD * EB;  // bytes per key
   constexpr int RB = KSPLIT ? R : 4 * R;
   __shared__ float sks[4096];  // the segment's key scales (fp8)
+  __shared__ int32_t spg[PAGED ? 256 : 1];  // the segment's pages (paged keys; a segment of <= 4096 keys
+                                            // starts on a page boundary or lies inside one page)
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
   const int nrows = rs.i1 - rs.i0;
@@ -109,22 +111,40 @@ __global__ __launch_bounds__(256) void score_kernel(const uint8_t* __restrict__ 
   const __amdgpu_buffer_rsrc_t kr =
       PAGED ? buffer_rsrc(k, (uint32_t)(((int64_t)km.n_pages << km.shift) * KB))
             : buffer_rsrc(k + km.row(b, seg0) * KB, (uint32_t)nkeys * KB);
-  auto key_off = [&](int e) -> uint32_t {  // e: key index within the segment
+  // e: key index within the segment; the prologue reads the page table in
+  // global memory, the loop the segment's pages staged in LDS
+  const int64_t page0 = PAGED ? seg0 >> km.shift : 0;
+  if constexpr (PAGED) {
+    const int n_ent = (int)(((seg0 + nseg_keys - 1) >> km.shift) - page0 + 1);
+    if (tid < n_ent) spg[tid] = min(max(km.pages[(int64_t)b * km.max_pages + page0 + tid], 0), km.n_pages - 1);
+  }
+  auto key_off0 = [&](int e) -> uint32_t {
     if constexpr (PAGED) return e < nkeys ? (uint32_t)(km.row(b, seg0 + e) * KB) : kDropOffset;
     else return (uint32_t)e * KB;
+  };
+  auto key_off = [&](int e) -> uint32_t {
+    if constexpr (PAGED) {
+      if (e >= nkeys) return kDropOffset;
+      const int64_t s = seg0 + e;
+      return (uint32_t)((((int64_t)spg[(s >> km.shift) - page0] << km.shift) | (s & ((1 << km.shift) - 1))) * KB);
+    } else {
+      return (uint32_t)e * KB;
+    }
   };
   const int S = KSPLIT ? 64 : 16;
   int t = KSPLIT ? 16 * wave : 0;  // key offset within the segment
   const int lr0 = lane & 15, kg0 = lane >> 4;
   KeyFrag<DT> f0, f1, f2;
-  f0.load(kr, key_off(t + lr0), kg0);
-  f1.load(kr, key_off(t + S + lr0), kg0);
-  f2.load(kr, key_off(t + 2 * S + lr0), kg0);
+  f0.load(kr, key_off0(t + lr0), kg0);
+  f1.load(kr, key_off0(t + S + lr0), kg0);
+  f2.load(kr, key_off0(t + 2 * S + lr0), kg0);
 
   if constexpr (DT == kFp8) {
 #pragma unroll
     for (int u = 0; u < KS_PER; ++u) sks[tid + 256 * u] = ksv[u];  // zeros past the segment
     __syncthreads();
+  } else if constexpr (PAGED) {
+    __syncthreads();  // the staged pages
   }
   if (nkeys == 0) return;  // no workgroup barrier follows
 
