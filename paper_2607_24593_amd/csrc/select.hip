@@ -345,31 +345,44 @@ __global__ __launch_bounds__(T) void topk_merge_kernel(const float* __restrict__
     for (int p = tid; p < m; p += T) put(p, p < n ? p : -1);
     return;
   }
-  if (tid == 0) {
-    sh.sel.emitted = 0;
-    int tot = 0;
-    bool ok = true;
-    for (int s = 0; s < P; ++s) {
-      const int c = cnt[(int64_t)r * P + s];
-      pre[s] = tot;
-      ok = ok && c >= 0;
-      tot += c >= 0 ? c : 0;
+  if (tid < 64) {  // the slices' counts, one per lane, and their prefix sums
+    const int c = tid < P ? cnt[(int64_t)r * P + tid] : 0;
+    int incl = max(c, 0);
+#pragma unroll
+    for (int o = 1; o < kSplitMaxP; o <<= 1) {
+      const int t = __shfl_up(incl, o, 64);
+      if (tid >= o) incl += t;
     }
-    pre[P] = ok ? tot : -1;
+    const bool ok = __ballot(tid < P && c < 0) == 0;
+    if (tid < P) pre[tid] = incl - max(c, 0);
+    const int tot = __shfl(incl, P - 1, 64);
+    if (tid == 0) {
+      pre[P] = ok ? tot : -1;
+      sh.sel.emitted = 0;
+    }
   }
   __syncthreads();
   const int total = pre[P];
   if (total >= m && total <= CAP) {
-    // every thread fetches its (at most V) keys at once, then stores them
+    // every thread fetches its (at most V) keys at once, then stores them;
+    // an element's slice comes from the prefix sums held in registers
+    int pr[kSplitMaxP];
+#pragma unroll
+    for (int k = 0; k < kSplitMaxP; ++k) pr[k] = k < P ? pre[k] : 0x7FFFFFFF;
     uint2 v[V];
 #pragma unroll
     for (int j = 0; j < V; ++j) {
       const int e = tid + j * T;
       v[j] = make_uint2(0u, 0u);
       if (e < total) {
-        int s = 0;
-        while (s + 1 < P && pre[s + 1] <= e) ++s;
-        v[j] = cand[((int64_t)r * P + s) * per + (e - pre[s])];
+        int s = 0, base = 0;
+#pragma unroll
+        for (int k = 1; k < kSplitMaxP; ++k)
+          if (e >= pr[k]) {
+            s = k;
+            base = pr[k];
+          }
+        v[j] = cand[((int64_t)r * P + s) * per + (e - base)];
       }
     }
 #pragma unroll
