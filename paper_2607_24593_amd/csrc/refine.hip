@@ -3,7 +3,7 @@
 // and keeps its own top-k (Eq. 9).
 //
 // rescore_kernel: one workgroup (4 waves) per group and block of R members
-// (R = 4 for fp8, 2 for bf16), held as the A operands of the MFMA row tile
+// (R = 4 for fp8 groups of more than two, else 2), held as the A operands of the MFMA row tile
 // (mfma_tile.h); the waves split C into 16-candidate fragments.  The candidate positions are staged in
 // LDS, so each lane reads its position there and gathers 32 bytes of that key
 // (and, for fp8, its scale) three fragments ahead of its use.  Scores go to a
@@ -286,15 +286,20 @@ hipError_t launch_refine(int dtype, const void* q, const float* q_scale, const f
   if (c > kMaxCand) return hipErrorInvalidValue;
   const SlotRule rule{W, wslot};
   const int all_slots = W > 0;
-  // few groups (decode): split the candidates so the launch still fills the GPU
-  const int R = dtype == kFp8 ? 4 : 2;
+  // few groups (decode): split the candidates so the launch still fills the GPU;
+  // fp8 groups of at most two members take the 2-row tile (half the MFMA work)
+  const int R = (dtype == kFp8 && g > 2) ? 4 : 2;
   const int64_t wgs = (int64_t)(j1 - j0) * st.n * ((g + R - 1) / R);
   const int nfrag = (c + 15) / 16;
   // (at least 6 fragments per wave: the loop runs in steps of 3)
   const int parts = (int)std::max<int64_t>(1, std::min<int64_t>(std::max(1, nfrag / 24), (512 + wgs - 1) / wgs));
   const dim3 grid((unsigned)(j1 - j0), (unsigned)st.n, (unsigned)(((g + R - 1) / R) * parts));
-  if (dtype == kFp8)
+  if (dtype == kFp8 && R == 4)
     hipLaunchKernelGGL((rescore_kernel<kFp8, 4>), grid, dim3(256), 0, stream, (const uint8_t*)q, q_scale, w, lin,
+                       lin_scale, g, (const uint8_t*)k, k_scale, km, st, j0, cand, c,
+                       all_slots, parts, rescore);
+  else if (dtype == kFp8)
+    hipLaunchKernelGGL((rescore_kernel<kFp8, 2>), grid, dim3(256), 0, stream, (const uint8_t*)q, q_scale, w, lin,
                        lin_scale, g, (const uint8_t*)k, k_scale, km, st, j0, cand, c,
                        all_slots, parts, rescore);
   else

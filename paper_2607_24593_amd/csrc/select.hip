@@ -15,11 +15,12 @@
 //              they include every key >= the m-th largest of the row, ties
 //              included, so block_select() over them is exact; otherwise the
 //              row takes the two-pass path below.
-// Few long rows (decode) with a scratch buffer: steps 1-2 run in
-// topk_slice_kernel on P workgroups per row (each takes the same sample and
-// threshold and compacts 1/P of the row into scratch), step 3 in
-// topk_merge_kernel, which gathers the row's compacted keys into LDS; one
-// workgroup per row could not pull its row fast enough on its own.
+// Few long rows (decode) with a scratch buffer: step 1 runs in
+// topk_thr_kernel (one workgroup per row writes the row's threshold), step 2
+// in topk_slice_kernel on P workgroups per row (each compacts 1/P of the row
+// into scratch), step 3 in topk_merge_kernel, which gathers the row's
+// compacted keys into LDS; one workgroup per row could not pull its row fast
+// enough on its own.
 // Other rows: two_level_select() (block_select.h) over the row in global
 // memory: pass 1 builds a 4096-bin histogram of the top 12 key bits, pass 2
 // emits the keys above the threshold bin and compacts that bin into LDS, where
@@ -249,21 +250,39 @@ __global__ __launch_bounds__(T) void topk_rows_kernel(const float* __restrict__ 
   two_level_select<T>(src, (uint32_t)m, sh, put);
 }
 
-// Split select, steps 1-2: workgroup (r, s) of a launch over rows r (as in
-// topk_rows_kernel) takes the row's sample and threshold, compacts the keys
-// >= the threshold among float4s [s per4, (s+1) per4) of the row (the last
-// slice also takes the n mod 4 tail) into LDS, and writes them to
-// cand[(r P + s) per ..] with their count in cnt[r P + s]: -1 when the row
-// takes the two-pass path (n <= m, short or unaligned row, sample declined),
-// -2 when the slice held more than `per` keys.
-template <int CAP>
+// Split select, step 1: workgroup r writes row r's threshold score to
+// thr[r], or NaN when the row takes the two-pass path (n <= m, short or
+// unaligned row, sample declined).
+template <int CAP, int T>
+__global__ __launch_bounds__(T) void topk_thr_kernel(const float* __restrict__ scores, int64_t ld, SeqTable st,
+                                                     RowSpace rs, int m, float* __restrict__ thr) {
+  __shared__ uint32_t hist[4096];
+  __shared__ SelectShared sel;
+  const int nrows = rs.i1 - rs.i0;
+  const int r = blockIdx.x;
+  const int b = r / nrows;
+  const int i = rs.i0 + r % nrows;
+  if (!row_active(st, rs, b, i)) return;
+  const int n = (int)max((int64_t)0, row_limit(st, rs, b, i) + 1);
+  const float* row = scores + ((int64_t)b * nrows + (i - rs.i0)) * ld;
+  const bool aligned = (reinterpret_cast<uintptr_t>(row) & 15u) == 0;
+  float fthr;
+  if (n <= m || n < kSampleMinLen || !aligned || !sample_threshold<T, CAP>(row, n, m, hist, sel, fthr))
+    fthr = __builtin_nanf("");
+  if (threadIdx.x == 0) thr[r] = fthr;
+}
+
+// Split select, step 2: workgroup (r, s) compacts the keys >= thr[r] among
+// float4s [s per4, (s+1) per4) of row r (the last slice also takes the
+// n mod 4 tail) into LDS and writes them to cand[(r P + s) per ..] with their
+// count in cnt[r P + s]: -1 when the row takes the two-pass path (thr[r] is
+// NaN), -2 when the slice held more than `per` keys.
 __global__ __launch_bounds__(kSplitThreads) void topk_slice_kernel(const float* __restrict__ scores, int64_t ld,
-                                                                   SeqTable st, RowSpace rs, int m, int P, int per,
+                                                                   SeqTable st, RowSpace rs, int P, int per,
+                                                                   const float* __restrict__ thr,
                                                                    uint2* __restrict__ cand,
                                                                    int32_t* __restrict__ cnt) {
   constexpr int T = kSplitThreads, U = 8;
-  __shared__ uint32_t hist[4096];
-  __shared__ SelectShared sel;
   __shared__ uint2 lc[kSplitPerMax];
   __shared__ int32_t nc;
   const int nrows = rs.i1 - rs.i0;
@@ -275,9 +294,8 @@ __global__ __launch_bounds__(kSplitThreads) void topk_slice_kernel(const float* 
   const int n = (int)max((int64_t)0, row_limit(st, rs, b, i) + 1);
   const float* row = scores + ((int64_t)b * nrows + (i - rs.i0)) * ld;
   int32_t* my_cnt = cnt + (int64_t)r * P + slice;
-  const bool aligned = (reinterpret_cast<uintptr_t>(row) & 15u) == 0;
-  float fthr;
-  if (n <= m || n < kSampleMinLen || !aligned || !sample_threshold<T, CAP>(row, n, m, hist, sel, fthr)) {
+  const float fthr = thr[r];
+  if (__builtin_isnan(fthr)) {
     if (tid == 0) *my_cnt = -1;
     return;
   }
@@ -405,7 +423,7 @@ __global__ __launch_bounds__(T) void topk_merge_kernel(const float* __restrict__
 }
 
 size_t split_scratch_bytes(int64_t rows) {
-  return (size_t)rows * ((size_t)kSplitSlots * sizeof(uint2) + (size_t)kSplitMaxP * sizeof(int32_t));
+  return (size_t)rows * ((size_t)kSplitSlots * sizeof(uint2) + (size_t)kSplitMaxP * sizeof(int32_t) + sizeof(float));
 }
 
 hipError_t launch_topk(const float* scores, int64_t ld, const SeqTable& st, const RowSpace& rs,
@@ -422,18 +440,23 @@ hipError_t launch_topk(const float* scores, int64_t ld, const SeqTable& st, cons
     const int per = kSplitSlots / P;
     uint2* cand = reinterpret_cast<uint2*>(scratch);
     int32_t* cnt = reinterpret_cast<int32_t*>(cand + (size_t)blocks * kSplitSlots);
+    float* thr = reinterpret_cast<float*>(cnt + (size_t)blocks * kSplitMaxP);
     const dim3 sgrid((unsigned)blocks, (unsigned)P);
-    if (od.m <= kSelCapSmall / 2) {
-      hipLaunchKernelGGL((topk_slice_kernel<kSelCapSmall>), sgrid, dim3(kSplitThreads), 0, stream, scores, ld, st, rs,
-                         od.m, P, per, cand, cnt);
+    const bool small = od.m <= kSelCapSmall / 2;
+    if (small)
+      hipLaunchKernelGGL((topk_thr_kernel<kSelCapSmall, kSelThreadsWide>), dim3((unsigned)blocks),
+                         dim3(kSelThreadsWide), 0, stream, scores, ld, st, rs, od.m, thr);
+    else
+      hipLaunchKernelGGL((topk_thr_kernel<kSelCapLarge, kSelThreadsWide>), dim3((unsigned)blocks),
+                         dim3(kSelThreadsWide), 0, stream, scores, ld, st, rs, od.m, thr);
+    hipLaunchKernelGGL(topk_slice_kernel, sgrid, dim3(kSplitThreads), 0, stream, scores, ld, st, rs, P, per, thr,
+                       cand, cnt);
+    if (small)
       hipLaunchKernelGGL((topk_merge_kernel<kSelCapSmall, kSelThreadsWide>), dim3((unsigned)blocks),
                          dim3(kSelThreadsWide), 0, stream, scores, ld, st, rs, od, P, per, cand, cnt);
-    } else {
-      hipLaunchKernelGGL((topk_slice_kernel<kSelCapLarge>), sgrid, dim3(kSplitThreads), 0, stream, scores, ld, st, rs,
-                         od.m, P, per, cand, cnt);
+    else
       hipLaunchKernelGGL((topk_merge_kernel<kSelCapLarge, kSelThreadsWide>), dim3((unsigned)blocks),
                          dim3(kSelThreadsWide), 0, stream, scores, ld, st, rs, od, P, per, cand, cnt);
-    }
     return hipGetLastError();
   }
   if (blocks <= kWideMaxRows && lim_max + 1 >= kSampleMinLen) {

@@ -279,8 +279,9 @@ def test_workspace_size_closed_form():
     # Reuse: no candidate buffer, no member rows to re-score
     assert pv.pivot_workspace_size(a, pv.PIVOT_REUSE, 4, 16) == lin(ng) + proxies + ng * ld(1000) * 4
     # long prefix: score tiles stay near 1 GiB, plus the split select's scratch
-    # for up to 256 long rows (16000 (key, position) pairs and 16 counts each)
-    split = lambda rows: rows * (16000 * 8 + 16 * 4)  # noqa: E731
+    # for up to 256 long rows (16000 (key, position) pairs, 16 counts and a
+    # threshold each)
+    split = lambda rows: rows * (16000 * 8 + 16 * 4 + 4)  # noqa: E731
     a = args(n_q=16384, q_pos0=262144 - 16384)
     assert pv.pivot_workspace_size(a, pv.PIVOT_DENSE) == lin(16384) + split(256) + (1 << 30)
     assert pv.pivot_topk_rows_workspace_size(32) == split(32)
