@@ -205,3 +205,41 @@ def test_paged_decode_batch(mode):
                     mode=MODES[mode], g=1 if mode == "dense" else g, c=c, topk=topk, dense_below=-1,
                     gpu_idx=got[b * g:(b + 1) * g], gpu_cand=None if cand is None else cand[b:b + 1],
                     label=f"paged decode b{b}")
+
+
+@pytest.mark.parametrize("mode", ["dense", "reuse", "refine"])
+def test_more_sequences_than_one_launch(mode):
+    """80 decode sequences (a launch's sequence table holds 64): the host splits
+    every stage; packed runs of 1 to 3 queries with their own lengths."""
+    B, L, topk, c = 80, 3000, 128, 512
+    x = make_decode(B, L, 3, "bf16", seed=97, threads=8)
+    rng = np.random.default_rng(13)
+    runs = [int(v) for v in rng.integers(1, 4, B)]           # 1..3 queries per sequence
+    lens = [int(v) for v in rng.integers(2000, L + 1, B)]
+    pos = [lens[b] - runs[b] for b in range(B)]
+    q = np.concatenate([x.q[b, :runs[b]] for b in range(B)])
+    w = np.concatenate([x.w[b, :runs[b]] for b in range(B)])
+    cu = [0] + np.cumsum(runs).tolist()
+    kp = x.k.copy()
+    layout = pv.make_layout(cu_q=cu)
+    g = 2
+    say("80 sequences", mode)
+    cand = None
+    if mode == "dense":
+        idx = pv.pivot_dense_index_layout(dev(q), None, dev(w), dev(kp), None, pos, lens, topk, layout)
+    else:
+        ng = sum((r + g - 1) // g for r in runs)
+        ct = torch.full((ng, c), -7, dtype=torch.int32, device="cuda") if mode == "refine" else None
+        idx = pv.pivot_group_index_layout(dev(q), None, dev(w), dev(kp), None, pos, lens, topk, layout,
+                                          mode=PV_MODE[mode], g=g, c=c, dense_below=0, out_cand=ct)
+        cand = None if ct is None else host(ct)
+    idx = host(idx)
+    g0 = 0
+    for b in range(B):
+        ng_b = 1 if mode == "dense" else (runs[b] + g - 1) // g
+        if b in (0, 1, 63, 64, 65, B - 1) or b % 11 == 0:
+            check_pivot("bf16", x.q[b, :runs[b]], None, x.w[b, :runs[b]], pos[b], kp[b, :lens[b]], None, lens[b],
+                        mode=MODES[mode], g=1 if mode == "dense" else g, c=c, topk=topk, dense_below=0,
+                        gpu_idx=idx[cu[b]:cu[b + 1]],
+                        gpu_cand=None if cand is None else cand[g0:g0 + ng_b], label=f"seq {b}")
+        g0 += (runs[b] + g - 1) // g if mode != "dense" else 0
