@@ -3,17 +3,18 @@
 // and keeps its own top-k (Eq. 9).
 //
 // rescore_kernel: one workgroup (4 waves) per group and block of R members
-// (R = 4 for fp8 groups of more than two, else 2), held as the A operands of the MFMA row tile
-// (mfma_tile.h); the waves split C into 16-candidate fragments.  The candidate positions are staged in
-// LDS, so each lane reads its position there and gathers 32 bytes of that key
-// (and, for fp8, its scale) three fragments ahead of its use.  Scores go to a
+// (R = 4 for fp8 groups of more than two, else 2), held as the A operands of
+// the MFMA row tile (mfma_tile.h); the waves split C into 16-candidate
+// fragments.  The candidate positions are staged in LDS, so each lane reads
+// its position there and gathers 32 bytes of that key (and, for fp8, its
+// scale) three fragments ahead of its use.  Scores go to a
 // [group, member, |C|] fp32 buffer (it stays in the last-level cache for the
 // select that follows).
 //
 // topk_short_kernel: one workgroup per (group, member) row of |C| <= 8192
 // scores; each thread keeps its share of (key, position) pairs in registers
-// (both read with coalesced loads) and block_select() takes the top-k, ties
-// broken by lower position.
+// (read four at a time with 16-byte loads) and the bucket select (else
+// block_select()) takes the top-k, ties broken by lower position.
 //
 // App. B local window: window_kernel writes the union of the members' windows
 // into the candidate row after the proxy's slots.  A candidate row then has

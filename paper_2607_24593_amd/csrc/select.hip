@@ -1,5 +1,7 @@
 // Per-row top-m selection over fp32 score rows (the TopK of Sec. 3.1 and of
-// Eqs. 6-7): one 512-thread workgroup per row.
+// Eqs. 6-7): one 512-thread workgroup per row (1024 threads when a launch
+// holds at most 256 long rows), or, for such a launch given scratch (decode),
+// the split select described below.
 //
 // Long rows (n >= kSampleMinLen) are read once when the expected number of
 // compacted keys fits in LDS:
@@ -10,7 +12,9 @@
 //              where ts is the sample's expected share of m plus four
 //              standard deviations;
 //   2 compact  one pass over the row appends every key with prefix >= thr to
-//              LDS (at most CAP: 4096 for m <= 2048, else 8000);
+//              LDS (at most CAP: 4096 for m <= 2048, else 8000)
+//              (a row whose ts, scaled to the whole row, would fill more
+//              than 80% of CAP skips the sample and takes the two-pass path);
 //   3 select   if the pass found at least m keys (and no more than CAP),
 //              they include every key >= the m-th largest of the row, ties
 //              included, so block_select() over them is exact; otherwise the
