@@ -12,10 +12,12 @@
 //              where ts is the sample's expected share of m plus four
 //              standard deviations;
 //   2 compact  one pass over the row appends every key with prefix >= thr to
-//              LDS (at most CAP: 4096 for m <= 2048, else 8000)
+//              LDS (at most CAP: 4096 for m <= 2048, else 8000; each wave
+//              fills its own CAP / waves entries, slots from a ballot prefix)
 //              (a row whose ts, scaled to the whole row, would fill more
 //              than 80% of CAP skips the sample and takes the two-pass path);
-//   3 select   if the pass found at least m keys (and no more than CAP),
+//   3 select   if the pass found at least m keys (and no wave more than its
+//              share of CAP),
 //              they include every key >= the m-th largest of the row, ties
 //              included, so block_select() over them is exact; otherwise the
 //              row takes the two-pass path below.
@@ -85,26 +87,6 @@ struct RowSource {
     } else {
       for (int e = tid; e < count; e += T) f(float_key(row[e]), e);
     }
-  }
-  // the same walk (aligned rows only) handing over the raw scores
-  template <class F>
-  __device__ __forceinline__ void visit_raw(F f) const {
-    const int tid = threadIdx.x;
-    const int n4 = count >> 2;
-    const float4* r4 = reinterpret_cast<const float4*>(row);
-    auto each = [&](const float4& a, int i) {
-      f(a.x, 4 * i); f(a.y, 4 * i + 1); f(a.z, 4 * i + 2); f(a.w, 4 * i + 3);
-    };
-    int i = tid;
-    for (; i + (U - 1) * T < n4; i += U * T) {
-      float4 a[U];
-#pragma unroll
-      for (int u = 0; u < U; ++u) a[u] = r4[i + u * T];
-#pragma unroll
-      for (int u = 0; u < U; ++u) each(a[u], i + u * T);
-    }
-    for (; i < n4; i += T) each(r4[i], i);
-    for (int e = 4 * n4 + tid; e < count; e += T) f(row[e], e);
   }
 };
 
@@ -182,6 +164,95 @@ __device__ bool sample_threshold(const float* row, int n, int m, uint32_t* hist,
   return true;
 }
 
+// Step 2 of the one-read path: wave w appends the keys >= fthr it reads to
+// its own segment [w SEG, (w + 1) SEG) of (ckey, cpos), a ballot prefix
+// giving each lane its slot (no LDS atomics in the stream), then the segments
+// are packed to the front.  The loops are uniform over the wave, so the
+// running count stays the same in every lane.  Returns the number of keys, or
+// CAP + 1 when a segment overflowed.  Aligned rows only.
+template <int T, int U, int CAP>
+__device__ __forceinline__ int stream_compact(const float* row, int n, float fthr, uint32_t* ckey, int32_t* cpos,
+                                              int32_t* wcnt) {
+  constexpr int NW = T / 64, SEG = CAP / NW, R = (SEG + 63) / 64;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  uint32_t* mk = ckey + wv * SEG;
+  int32_t* mp = cpos + wv * SEG;
+  int wc = 0;
+  auto take = [&](bool valid, float v, int pos) {
+    const bool t = valid && v >= fthr;
+    const uint64_t bal = __ballot(t);
+    if (bal) {
+      const int slot =
+          wc + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
+      if (t && slot < SEG) {
+        mk[slot] = float_key(v);
+        mp[slot] = pos;
+      }
+      wc += (int)__popcll((unsigned long long)bal);
+    }
+  };
+  const int n4 = n >> 2;
+  const float4* r4 = reinterpret_cast<const float4*>(row);
+  int base = 0;
+  for (; base + U * T <= n4; base += U * T) {
+    float4 a[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) a[u] = r4[base + u * T + tid];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int p = 4 * (base + u * T + tid);
+      take(true, a[u].x, p); take(true, a[u].y, p + 1); take(true, a[u].z, p + 2); take(true, a[u].w, p + 3);
+    }
+  }
+  for (; base < n4; base += T) {
+    const int q = base + tid;
+    const bool ok = q < n4;
+    const float4 a = ok ? r4[q] : make_float4(0.f, 0.f, 0.f, 0.f);
+    take(ok, a.x, 4 * q); take(ok, a.y, 4 * q + 1); take(ok, a.z, 4 * q + 2); take(ok, a.w, 4 * q + 3);
+  }
+  if (4 * n4 < n) {  // the n mod 4 tail
+    const int e = 4 * n4 + tid;
+    const bool ok = e < n;
+    take(ok, ok ? row[e] : 0.f, e);
+  }
+  if (lane == 0) wcnt[wv] = wc;
+  __syncthreads();
+  int pre = 0, tot = 0;
+  bool over = false;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    const int c = wcnt[w];
+    pre += w < wv ? c : 0;
+    tot += c;
+    over |= c > SEG;
+  }
+  if (over) return CAP + 1;
+  // a segment moves left onto space other waves may still be reading:
+  // through registers, with a barrier in between
+  uint32_t kk[R];
+  int32_t pp[R];
+#pragma unroll
+  for (int j = 0; j < R; ++j) {
+    const int e = lane + 64 * j;
+    if (e < wc) {
+      kk[j] = mk[e];
+      pp[j] = mp[e];
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < R; ++j) {
+    const int e = lane + 64 * j;
+    if (e < wc) {
+      ckey[pre + e] = kk[j];
+      cpos[pre + e] = pp[j];
+    }
+  }
+  __syncthreads();
+  return tot;
+}
+
 // Where row (b, i)'s indices go (OutDesc).
 struct RowDest {
   int32_t* base;
@@ -202,9 +273,13 @@ struct RowDest {
   }
 };
 
-template <int CAP, int T>
-__global__ __launch_bounds__(T) void topk_rows_kernel(const float* __restrict__ scores, int64_t ld, SeqTable st,
-                                                      RowSpace rs, OutDesc od) {
+// SAMPLE: the launch holds rows long enough for the one-read path (a launch
+// of short rows only takes the kernel without it, which keeps the two-pass
+// loops as lean as they compile alone).  Register budget: as many 512-thread
+// workgroups per CU as LDS allows (three for CAP 4096, else two).
+template <int CAP, int T, bool SAMPLE>
+__global__ __launch_bounds__(T) __attribute__((amdgpu_waves_per_eu(CAP == kSelCapSmall && T == kSelThreads ? 6 : 4)))
+void topk_rows_kernel(const float* __restrict__ scores, int64_t ld, SeqTable st, RowSpace rs, OutDesc od) {
   constexpr int U = T == kSelThreads ? 4 : 8;       // row loads in flight per thread
   __shared__ TwoLevelShared<CAP> sh;
   const int nrows = rs.i1 - rs.i0;
@@ -225,22 +300,10 @@ __global__ __launch_bounds__(T) void topk_rows_kernel(const float* __restrict__ 
   RowSource<T, U> src{row, n};
   const bool aligned = (reinterpret_cast<uintptr_t>(row) & 15u) == 0;
   float fthr;
-  if (n >= kSampleMinLen && aligned) {
+  if (SAMPLE && n >= kSampleMinLen && aligned) {
     if (sample_threshold<T, CAP>(row, n, m, sh.hist, sh.sel, fthr)) {
-      if (tid == 0) sh.ncand = 0;
-      __syncthreads();
-      src.visit_raw([&](float v, int32_t pos) {
-        if (v >= fthr) {  // a few percent of the row: plain LDS atomics
-          const int c = atomicAdd(&sh.ncand, 1);
-          if (c < CAP) {
-            sh.ckey[c] = float_key(v);
-            sh.cpos[c] = pos;
-          }
-        }
-      });
-      __syncthreads();
-      const int found = sh.ncand;
-      __syncthreads();  // every thread has read the count before it is reused
+      __shared__ int32_t wcnt[T / 64];
+      const int found = stream_compact<T, U, CAP>(row, n, fthr, sh.ckey, sh.cpos, wcnt);
       if (found >= m && found <= CAP) {
         ArraySource<T> cand{sh.ckey, sh.cpos, found};
         // the sample's histogram is free: it serves the bucket pass and its list
@@ -466,19 +529,27 @@ hipError_t launch_topk(const float* scores, int64_t ld, const SeqTable& st, cons
   if (blocks <= kWideMaxRows && lim_max + 1 >= kSampleMinLen) {
     // few long rows (decode): one wide workgroup per row
     if (od.m <= kSelCapSmall / 2)
-      hipLaunchKernelGGL((topk_rows_kernel<kSelCapSmall, kSelThreadsWide>), dim3((unsigned)blocks),
+      hipLaunchKernelGGL((topk_rows_kernel<kSelCapSmall, kSelThreadsWide, true>), dim3((unsigned)blocks),
                          dim3(kSelThreadsWide), 0, stream, scores, ld, st, rs, od);
     else
-      hipLaunchKernelGGL((topk_rows_kernel<kSelCapLarge, kSelThreadsWide>), dim3((unsigned)blocks),
+      hipLaunchKernelGGL((topk_rows_kernel<kSelCapLarge, kSelThreadsWide, true>), dim3((unsigned)blocks),
                          dim3(kSelThreadsWide), 0, stream, scores, ld, st, rs, od);
     return hipGetLastError();
   }
-  if (od.m <= kSelCapSmall / 2)
-    hipLaunchKernelGGL((topk_rows_kernel<kSelCapSmall, kSelThreads>), dim3((unsigned)blocks), dim3(kSelThreads), 0, stream, scores,
-                       ld, st, rs, od);
+  const bool small = od.m <= kSelCapSmall / 2, sample = lim_max + 1 >= kSampleMinLen;
+  const dim3 grid((unsigned)blocks), block(kSelThreads);
+  if (small && sample)
+    hipLaunchKernelGGL((topk_rows_kernel<kSelCapSmall, kSelThreads, true>), grid, block, 0, stream, scores, ld, st, rs,
+                       od);
+  else if (small)
+    hipLaunchKernelGGL((topk_rows_kernel<kSelCapSmall, kSelThreads, false>), grid, block, 0, stream, scores, ld, st,
+                       rs, od);
+  else if (sample)
+    hipLaunchKernelGGL((topk_rows_kernel<kSelCapLarge, kSelThreads, true>), grid, block, 0, stream, scores, ld, st, rs,
+                       od);
   else
-    hipLaunchKernelGGL((topk_rows_kernel<kSelCapLarge, kSelThreads>), dim3((unsigned)blocks), dim3(kSelThreads), 0, stream, scores,
-                       ld, st, rs, od);
+    hipLaunchKernelGGL((topk_rows_kernel<kSelCapLarge, kSelThreads, false>), grid, block, 0, stream, scores, ld, st,
+                       rs, od);
   return hipGetLastError();
 }
 

@@ -70,14 +70,19 @@ def _expect_topk(row, n, m):
 @pytest.mark.parametrize("split", [False, True])
 @pytest.mark.parametrize("case", ["normal", "ties", "signed_zeros", "short", "exact", "long2k", "long4k",
                                   "ragged", "constant", "sample_miss", "sample_ragged", "heavy_tail", "small_m",
-                                  "unaligned", "m4k_normal", "slice_skew", "decode_shape"])
+                                  "unaligned", "m4k_normal", "slice_skew", "decode_shape", "many_rows",
+                                  "wave_skew"])
 def test_topk_rows_exact(case, split):
     """Rows of 16384+ scores with m <= 2048 take the sampled one-pass path; the
     sample_miss rows put the sample's largest keys where the rest of the row is
     low, so the pass finds fewer than m keys and falls back to two passes.
     split: with a workspace, calls of at most 256 rows split each long row over
     several workgroups; slice_skew puts every high score in the first slice,
-    which overflows its share of the scratch and falls back."""
+    which overflows its share of the scratch and falls back.  Calls of more
+    than 256 rows take one 512-thread workgroup per row, whose waves compact
+    into segments of their own: wave_skew puts every high score in the columns
+    wave 0 reads (elements e with e mod 2048 < 256), which overflows its
+    segment and falls back."""
     rng = np.random.default_rng(zlib.crc32(case.encode()))
     n0, step, m = 5000, 0, 100
     if case == "normal":
@@ -115,6 +120,11 @@ def test_topk_rows_exact(case, split):
         rows[:, :4096] += 5.0; n0, m = 131072, 2048
     elif case == "decode_shape":
         rows = rng.standard_normal((32, 131071)); n0, m = 131071, 4096
+    elif case == "many_rows":
+        rows = rng.standard_normal((300, 20000)); n0, step, m = 16384, 12, 2048
+    elif case == "wave_skew":
+        rows = rng.standard_normal((300, 32768)) * 0.1
+        rows[:, np.arange(32768) % 2048 < 256] += 5.0; n0, m = 32768, 2048
     else:
         rows = np.full((2, 20000), 3.5); n0, m = 20000, 700
     rows = rows.astype(np.float32)
