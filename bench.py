@@ -9,7 +9,7 @@ top-c, and the per-member gather / re-score / top-k.  Inputs are synthetic
 
 Reported besides the headline queries/s: the dense indexer and PIVOT-Reuse on
 the same prefill (speedup), a group-size sweep, Refine with App. B's local
-window (W=4), MTP decode (32 x 131072 cached keys, g=2, also with the
+window (W=4), the bf16 scoring kernel's MFMA fraction (the 128K prefill in bf16), MTP decode (32 x 131072 cached keys, g=2, also with the
 per-query window), the batch layouts (paged decode keys, a packed batch of
 four prefill requests), per-kernel times from HIP events recorded around each launch
 inside the timed steps, the roofline fraction of the dominant kernel, and the
@@ -181,6 +181,45 @@ def decode_bench(reps):
     res["dense"]["key_stream_GBps"] = key_bytes / (res["dense"]["us_per_step"] * 1e-6) / 1e9
     res["workload"] = wl.name
     return res
+
+
+def bf16_score_bench(reps, L=131072, chunk=8192):
+    """The bf16 scoring kernel: dense indexer passes over an L-token bf16
+    prefill (the 128K prefill recipe with bf16 queries and keys), in chunks of
+    `chunk` queries against their causal prefix; the score kernel's time from
+    HIP events on its launches, against the bf16 MFMA peak."""
+    import torch
+    import paper_2607_24593_amd as pv
+    from workload.gen import make_prefill
+    t = time.time()
+    x = make_prefill(L, "bf16", seed=1, rho=0.9, threads=16)
+    log(f"generated a {L}-token bf16 prefill in {time.time() - t:.1f}s")
+    d = lambda a: torch.from_numpy(a.view("int16") if a.dtype.name == "uint16" else a).cuda()  # noqa: E731
+    q, w, k = d(x.q), d(x.w), d(x.k)
+    topk = 2048
+    out = torch.empty((L, topk), dtype=torch.int32, device="cuda")
+    chunks = [(p0, min(chunk, L - p0)) for p0 in range(0, L, chunk)]
+
+    def run():
+        for p0, n in chunks:
+            pv.pivot_dense_index(q[p0:p0 + n], None, w[p0:p0 + n], k[:p0 + n], None, p0, p0 + n, topk,
+                                 out=out[p0:p0 + n])
+    run()
+    torch.cuda.synchronize()
+    with no_gc():
+        pv.pivot_profile_begin()
+        t = time.perf_counter()
+        for _ in range(reps):
+            run()
+        torch.cuda.synchronize()
+        sec = (time.perf_counter() - t) / reps
+        prof = pv.pivot_profile_end()
+    n_sc, ms_sc = prof["score"]
+    flops = sum(p0 + i + 1 for p0, n in chunks for i in range(n)) * FLOP_PER_PAIR
+    tf = flops * reps / (ms_sc * 1e-3) / 1e12
+    return {"workload": f"prefill-{L // 1024}k-bf16 (dense, {len(chunks)} calls of {chunk} queries)",
+            "ms_per_pass": sec * 1e3, "score_launches_per_pass": n_sc / reps,
+            "score_ms_per_pass": ms_sc / reps, "score_TFLOPs": tf, "peak": PEAK["bf16"], "frac": tf / PEAK["bf16"]}
 
 
 def layout_bench(reps):
@@ -438,6 +477,9 @@ def main():
                                     "speedup_vs_dense": dense_s / s}
         log(f"refine g={g} W=4: {s * 1e3:.2f} ms ({dense_s / s:.2f}x)")
 
+    bf16 = None if args.no_compare else bf16_score_bench(reps=args.reps)
+    if bf16 is not None:
+        log(f"bf16 score kernel: {bf16['score_TFLOPs']:.0f} TFLOP/s ({100 * bf16['frac']:.1f}% of peak)")
     dec = None if args.no_decode else decode_bench(reps=50)
     layouts = None if args.no_layouts else layout_bench(reps=20)
     cpu = None if args.no_cpu_baseline else cpu_baseline(pf, g)
@@ -460,6 +502,7 @@ def main():
                    "workspace_bytes": int(pf.ws.numel())},
         "speedup_vs_dense": None if dense_s is None else dense_s / step_s,
         "mfma_frac_score_kernel": kern.get("score", {}).get("frac"),
+        "score_bf16": bf16,
         "roofline": roofline,
         "kernels": kern,
         "modes": modes,

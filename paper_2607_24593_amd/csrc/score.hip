@@ -13,10 +13,14 @@
 //              from L2 once and served to 4 waves from the vector L1;
 //   keys mode  (< 16 rows per sequence, decode): the 4 waves hold the same rows
 //              and split the keys.
-// Grid: x = key segment, y = row block, in linear order, so the causal
-// triangle's active (row block, segment) pairs spread evenly over the 8 XCDs
+// Grid: rows mode runs a 1-D grid whose linear index is segment * row blocks
+// + row block, so consecutive workgroups take the row blocks of one key
+// segment: dispatched round-robin over the 8 XCDs, the ~64 workgroups resident
+// on an XCD share one or two segments in its L2, and the causal triangle's
+// active (row block, segment) pairs still spread evenly over the XCDs
 // (pinning segments to XCDs would idle the XCDs that own the late segments of
-// short prefixes).  The segment length adapts to the launch size.
+// short prefixes).  Keys mode runs x = key segment, y = sequence.  The segment
+// length adapts to the launch size.
 #include "launch.h"
 #include "mfma_tile.h"
 
@@ -47,10 +51,13 @@ __global__ __launch_bounds__(256) void score_kernel(const uint8_t* __restrict__ 
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
   const int nrows = rs.i1 - rs.i0;
   const int nbps = (nrows + RB - 1) / RB;
-  const int b = blockIdx.y / nbps;
+  const uint32_t nblk = (uint32_t)(st.n * nbps);
+  const uint32_t yb = KSPLIT ? blockIdx.y : blockIdx.x % nblk;  // row block
+  const uint32_t xs = KSPLIT ? blockIdx.x : blockIdx.x / nblk;  // key segment
+  const int b = (int)(yb / nbps);
   if (b >= st.n) return;
-  const int i_blk = rs.i0 + (blockIdx.y % nbps) * RB;
-  const int64_t seg0 = (int64_t)blockIdx.x * seg_keys;
+  const int i_blk = rs.i0 + (int)(yb % nbps) * RB;
+  const int64_t seg0 = (int64_t)xs * seg_keys;
 
   // the workgroup's key range (uniform, so every wave reaches the barrier)
   int64_t lim_blk = -1;
@@ -199,13 +206,15 @@ static hipError_t run_score(const void* q, const float* qs, const float* w, cons
   int seg = max_seg;  // <= 4096: the key scales of a segment are staged in LDS
   while (seg > 512 && nblk * ((lim_max + seg) / seg) < kTargetWorkgroups) seg >>= 1;
   const int64_t nseg = (lim_max + seg) / seg;
-  if (nseg > 0x7FFFFFFF || nblk > 65535) return hipErrorInvalidConfiguration;
+  if (KSPLIT ? (nseg > 0x7FFFFFFF || nblk > 65535) : nseg * nblk > 0x7FFFFFFF)
+    return hipErrorInvalidConfiguration;
+  const dim3 grid = KSPLIT ? dim3((unsigned)nseg, (unsigned)nblk) : dim3((unsigned)(nseg * nblk));
   if (km.pages)
-    hipLaunchKernelGGL((score_kernel<DT, R, KSPLIT, true>), dim3((unsigned)nseg, (unsigned)nblk), dim3(256), 0,
-                       stream, (const uint8_t*)q, qs, w, lin, lsc, (const uint8_t*)k, ks, km, st, rs, out, ld, seg);
+    hipLaunchKernelGGL((score_kernel<DT, R, KSPLIT, true>), grid, dim3(256), 0, stream, (const uint8_t*)q, qs, w, lin,
+                       lsc, (const uint8_t*)k, ks, km, st, rs, out, ld, seg);
   else
-    hipLaunchKernelGGL((score_kernel<DT, R, KSPLIT, false>), dim3((unsigned)nseg, (unsigned)nblk), dim3(256), 0,
-                       stream, (const uint8_t*)q, qs, w, lin, lsc, (const uint8_t*)k, ks, km, st, rs, out, ld, seg);
+    hipLaunchKernelGGL((score_kernel<DT, R, KSPLIT, false>), grid, dim3(256), 0, stream, (const uint8_t*)q, qs, w,
+                       lin, lsc, (const uint8_t*)k, ks, km, st, rs, out, ld, seg);
   return hipGetLastError();
 }
 
