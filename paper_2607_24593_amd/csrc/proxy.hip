@@ -69,30 +69,50 @@ __global__ __launch_bounds__(256) void proxy_kernel(const uint8_t* __restrict__ 
     return;
   }
 
+  // Members are read MB at a time: every load of a batch is issued before the
+  // first is used, then the batch is summed in ascending member order.
+  constexpr int VPM = PER * EB / 16;      // 16-byte loads per member and thread
+  constexpr int MB = DT == kFp8 ? 8 : 4;  // members per batch
   float sum[PER];
 #pragma unroll
   for (int e = 0; e < PER; ++e) sum[e] = 0.0f;
-  for (int u = 0; u < gs; ++u) {
-    const uint4* src = reinterpret_cast<const uint4*>(q + (r0 + u) * ROW_BYTES + e0 * EB);
-    if constexpr (DT == kFp8) {
-      const float sq = q_scale[r0 + u];
-      uint4 v0 = src[0], v1 = src[1];
-      uint32_t words[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+  float wsum = 0.0f;
+  for (int u0 = 0; u0 < gs; u0 += MB) {
+    uint4 v[MB][VPM];
+    float sq[MB], wv[MB];
 #pragma unroll
-      for (int e = 0; e < PER; ++e) {
-        float x = decode_e4m3(words[e >> 2], e & 3);
-        float deq = sq * x;
-        sum[e] = sum[e] + deq;
+    for (int k = 0; k < MB; ++k) {
+      const int64_t row = r0 + u0 + k;
+      if (u0 + k < gs) {
+        const uint4* src = reinterpret_cast<const uint4*>(q + row * ROW_BYTES + e0 * EB);
+#pragma unroll
+        for (int x = 0; x < VPM; ++x) v[k][x] = src[x];
+        sq[k] = (DT == kFp8) ? q_scale[row] : 1.0f;
+        wv[k] = tid < kH ? w[row * kH + tid] : 0.0f;
       }
-    } else {
+    }
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        uint4 pkt = src[v];
-        uint32_t words[4] = {pkt.x, pkt.y, pkt.z, pkt.w};
+    for (int k = 0; k < MB; ++k) {
+      if (u0 + k >= gs) break;
+      wsum = wsum + wv[k];
+      if constexpr (DT == kFp8) {
+        const uint32_t words[8] = {v[k][0].x, v[k][0].y, v[k][0].z, v[k][0].w,
+                                   v[k][1].x, v[k][1].y, v[k][1].z, v[k][1].w};
 #pragma unroll
-        for (int h = 0; h < 4; ++h) {
-          sum[8 * v + 2 * h] = sum[8 * v + 2 * h] + __uint_as_float(words[h] << 16);
-          sum[8 * v + 2 * h + 1] = sum[8 * v + 2 * h + 1] + __uint_as_float(words[h] & 0xFFFF0000u);
+        for (int e = 0; e < PER; ++e) {
+          float x = decode_e4m3(words[e >> 2], e & 3);
+          float deq = sq[k] * x;
+          sum[e] = sum[e] + deq;
+        }
+      } else {
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+          const uint32_t words[4] = {v[k][x].x, v[k][x].y, v[k][x].z, v[k][x].w};
+#pragma unroll
+          for (int h = 0; h < 4; ++h) {
+            sum[8 * x + 2 * h] = sum[8 * x + 2 * h] + __uint_as_float(words[h] << 16);
+            sum[8 * x + 2 * h + 1] = sum[8 * x + 2 * h + 1] + __uint_as_float(words[h] & 0xFFFF0000u);
+          }
         }
       }
     }
@@ -105,11 +125,7 @@ __global__ __launch_bounds__(256) void proxy_kernel(const uint8_t* __restrict__ 
     amax = fmaxf(amax, fabsf(sum[e]));
   }
 
-  if (tid < kH) {
-    float s = 0.0f;
-    for (int u = 0; u < gs; ++u) s = s + w[(r0 + u) * kH + tid];
-    pw[pr * kH + tid] = s / count;
-  }
+  if (tid < kH) pw[pr * kH + tid] = wsum / count;
 
   if constexpr (DT == kFp8) {
     __shared__ float wmax[4];
