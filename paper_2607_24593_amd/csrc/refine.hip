@@ -235,8 +235,13 @@ __global__ __launch_bounds__(256) void topk_short_kernel(const float* __restrict
   __syncthreads();
   auto put = [&](int slot, int32_t p) { orow[slot] = p; };
   if (!bucket_select<256, 1024>(src, (uint32_t)m, hist, hist, reinterpret_cast<int32_t*>(hist + kBucketList), &lcount,
-                                sel, put))
-    block_select<256, true>(src, (uint32_t)m, sel, put);
+                                sel, put)) {
+    // block_select() takes its source by reference; handing it a copy keeps
+    // `src` itself in registers on the bucket path (a referenced array of 32
+    // pairs would otherwise live in scratch memory)
+    const RegSource<V> fb = src;
+    block_select<256, true>(fb, (uint32_t)m, sel, put);
+  }
 }
 
 // App. B window union: slot0 + u (u < wg) of every candidate row of the

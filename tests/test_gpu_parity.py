@@ -220,3 +220,14 @@ def test_many_long_rows(long20k_fp8, mode):
     rng = np.random.default_rng(5)
     groups = sorted({0, n_q // g - 1} | set(int(v) for v in rng.integers(0, n_q // g, 10)))
     check(x, mode, p0, n_q, 2048, g=g, c=4096, groups=groups, label=f"20k {mode}")
+
+
+@pytest.mark.parametrize("c", [6000, 8192])
+def test_large_candidate_budget(long20k_fp8, c):
+    """Refine with c above 5120 (up to the 8192-slot limit): each member's
+    select holds 32 (score, position) pairs per thread."""
+    x = long20k_fp8
+    p0, n_q, g = 20000 - 2048, 2048, 4
+    rng = np.random.default_rng(c)
+    groups = sorted({0, n_q // g - 1} | set(int(v) for v in rng.integers(0, n_q // g, 8)))
+    check(x, "refine", p0, n_q, 2048, g=g, c=c, groups=groups, label=f"20k refine c{c}")
