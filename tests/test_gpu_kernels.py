@@ -27,8 +27,11 @@ def test_encode_e4m3_matches_oracle_rne():
 
 
 @pytest.mark.parametrize("fmt", ["fp8", "bf16"])
-@pytest.mark.parametrize("g", [1, 2, 3, 4, 8])
+@pytest.mark.parametrize("g", [1, 2, 3, 4, 5, 8, 9, 16, 37])
 def test_proxy_rows_bit_exact(fmt, g):
+    """Proxies of 37 rows in groups of g (ragged last group), bit for bit; the
+    kernel reads members in batches of 8 (fp8) or 4 (bf16), so g = 5, 9, 16
+    and 37 span several batches, some partial."""
     x = make_prefill(37, fmt, seed=100 + g, threads=1)
     say("proxy_rows", fmt, "g", g)
     pq, ps, pw = pv.pivot_proxy_rows(dev(x.q), dev(x.q_scale), dev(x.w), g)
