@@ -64,10 +64,29 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void r
   const int fbeg = min(nfrag_all, part * fpp), fend = min(nfrag_all, fbeg + fpp);
   if (fbeg >= fend) return;
   const int cbeg = 16 * fbeg, ncs = min(nc, 16 * fend) - cbeg;  // this slice's candidates
-  if (km.pages)
-    for (int e = tid; e < ncs; e += 256) spos[e] = (int32_t)km.row(b, max(crow[cbeg + e], 0));
-  else
-    for (int e = tid; e < ncs; e += 256) spos[e] = crow[cbeg + e];
+  // positions staged eight per thread at a time: the loads of a batch are
+  // issued before the first is used (then, for paged keys, the batch's
+  // page-table loads), one or two memory round trips per batch instead of
+  // one per element
+  for (int e0 = 0; e0 < ncs; e0 += 8 * 256) {
+    constexpr int SB = 8;
+    int32_t pv[SB];
+#pragma unroll
+    for (int k = 0; k < SB; ++k) {
+      const int e = e0 + tid + 256 * k;
+      pv[k] = e < ncs ? crow[cbeg + e] : 0;
+    }
+    if (km.pages) {
+#pragma unroll
+      for (int k = 0; k < SB; ++k)
+        if (e0 + tid + 256 * k < ncs) pv[k] = (int32_t)km.row(b, max(pv[k], 0));
+    }
+#pragma unroll
+    for (int k = 0; k < SB; ++k) {
+      const int e = e0 + tid + 256 * k;
+      if (e < ncs) spos[e] = pv[k];
+    }
+  }
 
   const uint8_t* rows[R];
   const float* wrows[R];
@@ -83,10 +102,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void r
     lrows[r] = (DT == kFp8) ? lin + row * kLinBytes : nullptr;
     lsc[r] = (DT == kFp8) ? lin_scale + row * kLinLevels : nullptr;
   }
-  Tile tile;
-  tile.load(rows, wrows, qs, lrows, lsc, lane);
-  __syncthreads();  // candidate positions staged
-
   const int qr = kg / Tile::G;
   const bool writer = (kg % Tile::G) == 0 && qr < rows_here;
   // scores leave through a buffer resource over the block's R member rows;
@@ -98,25 +113,35 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void r
   const int nfrag = fend - fbeg;
   constexpr int S = 4;  // fragment stride between the waves
   auto pos_of = [&](int f) { return max(spos[min(16 * f + lr, ncs - 1)], 0); };  // empty slots: key 0
+  // the same position read from global memory (before the LDS copy is staged)
+  auto pos_glob = [&](int f) {
+    const int p = max(crow[cbeg + min(16 * f + lr, ncs - 1)], 0);
+    return km.pages ? (int)km.row(b, p) : p;
+  };
   auto emit = [&](float acc, float ks, int f) {
     const int slot = 16 * f + lr;
     const uint32_t off = (writer && slot < ncs) ? my_off + 4u * (uint32_t)slot : 0xFFFFFFFFu;
     __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc * ks), orr, off, 0, 0);
   };
   auto scale_of = [&](int p) { return DT == kFp8 ? ksb[p] : 1.0f; };
-  auto fetch = [&](KeyFrag<DT>& kf, float& sc, int ff) {
-    const int p = pos_of(ff);
+  auto fetch_at = [&](KeyFrag<DT>& kf, float& sc, int p) {
     sc = scale_of(p);
     kf.load(kb + (int64_t)p * kD * EB, kg);
   };
+  auto fetch = [&](KeyFrag<DT>& kf, float& sc, int ff) { fetch_at(kf, sc, pos_of(ff)); };
   // three fragments in flight per wave, with no exits in the loop body:
-  // fragments past the end repeat the last candidate and are not stored
+  // fragments past the end repeat the last candidate and are not stored.
+  // The first three are requested before the row tile and the barrier, so
+  // their loads overlap the tile's.
   int f = wave;
   KeyFrag<DT> k0, k1, k2;
   float s0, s1, s2;
-  fetch(k0, s0, f);
-  fetch(k1, s1, f + S);
-  fetch(k2, s2, f + 2 * S);
+  fetch_at(k0, s0, pos_glob(f));
+  fetch_at(k1, s1, pos_glob(f + S));
+  fetch_at(k2, s2, pos_glob(f + 2 * S));
+  Tile tile;
+  tile.load(rows, wrows, qs, lrows, lsc, lane);
+  __syncthreads();  // candidate positions staged
   for (; f < nfrag; f += 3 * S) {
     emit(tile.score(k0), s0, f);
     fetch(k0, s0, f + 3 * S);
