@@ -53,20 +53,23 @@ def plan_chunk(p0, n_q, g, c, mode):
 
 
 def units(chunks, mode, g, c, topk, eb_q=1, eb_k=1):
-    """Algorithmic work per pass: score pairs, select bytes, refine bytes and flops, proxy bytes."""
+    """Algorithmic work per pass: score pairs, select bytes, refine bytes and flops, proxy bytes.
+    The library stores score rows as bf16 for fp8 inputs (2 bytes per score
+    read by the select) and as fp32 for bf16 inputs."""
     row_q = 64 * 128 * eb_q + 4 + 4 * 64
+    eb_s = 2 if eb_q == 1 else 4
     pairs = sel_bytes = ref_bytes = ref_flops = prox_bytes = 0
     for p0, n_q in chunks:
         dense_rows, proxies = plan_chunk(p0, n_q, g, c, mode)
         dp = sum(p0 + i + 1 for i in range(dense_rows))
         pairs += dp
-        sel_bytes += 4 * dp + 4 * topk * dense_rows
+        sel_bytes += eb_s * dp + 4 * topk * dense_rows
         for t0, gs in proxies:
             n = t0 + 1
             pairs += n
             m = topk if mode == "reuse" else c
             fan = gs if mode == "reuse" else 1
-            sel_bytes += 4 * n + 4 * min(m, n) * fan
+            sel_bytes += eb_s * n + 4 * min(m, n) * fan
             prox_bytes += (gs + 1) * row_q if gs > 1 else 0
             if mode == "refine":
                 nc = min(c, n)

@@ -80,6 +80,11 @@ int64_t ld_for(int64_t n) {
   return (u | 1) * 64;
 }
 int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+// Score rows hold bf16 for fp8 inputs (half the bytes the select streams; the
+// rounding, at most 2^-9 relative, is far inside the fp8 score tolerance) and
+// fp32 for bf16 inputs.
+bool bf16_scores(int dtype) { return dtype == PIVOT_DT_FP8_E4M3; }
+int64_t score_eb(int dtype) { return bf16_scores(dtype) ? 2 : 4; }
 
 // The group plan: for each sequence, its query rows and groups, how many
 // leading query rows take the dense path (the guardrail of Algorithm 1) and
@@ -335,17 +340,17 @@ pivot_status make_plan(const pivot_args* a, const pivot_layout* l, int mode, int
 void score_need(const Plan& p, int64_t& full, int64_t& min_tile) {
   full = 0;
   min_tile = 0;
-  const int64_t ld = ld_for(p.max_nk);
+  const int64_t ld = ld_for(p.max_nk), eb = score_eb(p.dtype);
   if (p.dense_hi > 0) {
     const int64_t rows = (p.B == 1) ? p.dense_hi : (int64_t)p.B * p.dense_hi;
-    full = std::max(full, rows * ld * 4);
-    min_tile = std::max(min_tile, std::min<int64_t>(16, p.dense_hi) * ld * 4);
+    full = std::max(full, rows * ld * eb);
+    min_tile = std::max(min_tile, std::min<int64_t>(16, p.dense_hi) * ld * eb);
   }
   if (p.any_proxy) {
     const int64_t span = p.n_groups - p.proxy_lo;
     const int64_t rows = (p.B == 1) ? span : (int64_t)p.B * span;
-    full = std::max(full, rows * ld * 4);
-    min_tile = std::max(min_tile, std::min<int64_t>(16, span) * ld * 4);
+    full = std::max(full, rows * ld * eb);
+    min_tile = std::max(min_tile, std::min<int64_t>(16, span) * ld * eb);
   }
 }
 
@@ -425,11 +430,12 @@ struct RowData {
 // Score and select rows [lo, hi) of each sequence, tiled to the score budget:
 // several whole sequences per tile when they fit, else row tiles of one.
 pivot_status run_rows(const pivot_args* a, const Plan& p, int kind, int lo, int hi, int step,
-                      const RowData& rd_all, OutDesc od_all, float* scores, int64_t score_bytes,
+                      const RowData& rd_all, OutDesc od_all, void* scores, int64_t score_bytes,
                       hipStream_t stream, int lim_shift = 0) {
   if (hi <= lo) return PIVOT_OK;
   const int64_t ld_max = ld_for(p.max_nk);
-  const int64_t row_bytes = ld_max * 4;
+  const int64_t row_bytes = ld_max * score_eb(p.dtype);
+  const bool sb16 = bf16_scores(p.dtype);
   int seqs_per_tile, rows_per_tile;
   if (p.B > 1 && score_bytes / (row_bytes * (hi - lo)) >= 1) {
     rows_per_tile = hi - lo;
@@ -463,13 +469,13 @@ pivot_status run_rows(const pivot_args* a, const Plan& p, int kind, int lo, int 
       if (lim >= 0)  // no key in reach (shifted limits): the select only pads with -1
         s = hip_check(timed(PIVOT_KERNEL_SCORE, stream, [&] {
                         return launch_score(p.dtype, rd.q, rd.qs, rd.w, rd.lin, rd.lsc, kb.k, kb.ks, kb.map, st, rs,
-                                            lim, scores, ld, stream);
+                                            lim, scores, sb16, ld, stream);
                       }),
                       "score kernel");
       if (s != PIVOT_OK) return s;
       s = hip_check(timed(PIVOT_KERNEL_SELECT, stream,
                           [&] {
-                            return launch_topk(scores, ld, st, rs, od, lim,
+                            return launch_topk(scores, sb16, ld, st, rs, od, lim,
                                                p.sel_bytes ? (uint8_t*)a->workspace + p.off_sel : nullptr,
                                                p.sel_bytes, stream);
                           }),
@@ -512,7 +518,7 @@ pivot_status query_lin(const pivot_args* a, const Plan& p, uint8_t* ws, hipStrea
                    "linear-term kernel");
 }
 
-pivot_status dense_part(const pivot_args* a, const Plan& p, float* scores, int64_t score_bytes, hipStream_t stream) {
+pivot_status dense_part(const pivot_args* a, const Plan& p, void* scores, int64_t score_bytes, hipStream_t stream) {
   uint8_t* ws = (uint8_t*)a->workspace;
   const bool fp8 = a->dtype == PIVOT_DT_FP8_E4M3;
   RowData rd{a->q, fp8 ? a->q_scale : nullptr, a->w, fp8 ? ws + p.off_qlin : nullptr,
@@ -547,7 +553,7 @@ pivot_status dense_index(const pivot_args* a, const pivot_layout* l) {
   int64_t score_bytes;
   s = check_workspace(a, p, score_bytes);
   if (s != PIVOT_OK) return s;
-  float* scores = reinterpret_cast<float*>((uint8_t*)a->workspace + p.off_scores);
+  void* scores = (uint8_t*)a->workspace + p.off_scores;
   s = query_lin(a, p, (uint8_t*)a->workspace, (hipStream_t)a->stream);
   if (s != PIVOT_OK) return s;
   return dense_part(a, p, scores, score_bytes, (hipStream_t)a->stream);
@@ -566,7 +572,7 @@ pivot_status group_index(const pivot_args* a, const pivot_layout* l, const pivot
   s = check_workspace(a, p, score_bytes);
   if (s != PIVOT_OK) return s;
   uint8_t* ws = (uint8_t*)a->workspace;
-  float* scores = reinterpret_cast<float*>(ws + p.off_scores);
+  void* scores = ws + p.off_scores;
 
   void* pq = ws + p.off_pq;
   float* psc = reinterpret_cast<float*>(ws + p.off_psc);
@@ -802,7 +808,7 @@ pivot_status pivot_score_rows(int32_t dtype, int32_t heads, int32_t dim, int32_t
   KeyMap km;
   memset(&km, 0, sizeof km);  // one sequence of contiguous keys
   return hip_check(launch_score(dtype, q, fp8 ? q_scale : nullptr, w, lin, lsc, k, fp8 ? k_scale : nullptr, km, st,
-                                rs, lim_max, out, ld, (hipStream_t)stream),
+                                rs, lim_max, out, false, ld, (hipStream_t)stream),
                    "score kernel");
 }
 
@@ -833,7 +839,7 @@ pivot_status pivot_topk_rows_ws(int32_t n_rows, const float* scores, int64_t ld,
   st.n_rows[0] = n_rows;
   RowSpace rs{0, n_rows, n_step, kAll};
   OutDesc od{out, m, 0, 0, m};
-  return hip_check(launch_topk(scores, ld, st, rs, od, n_max - 1, workspace, workspace ? workspace_bytes : 0,
+  return hip_check(launch_topk(scores, false, ld, st, rs, od, n_max - 1, workspace, workspace ? workspace_bytes : 0,
                                (hipStream_t)stream),
                    "top-k kernel");
 }

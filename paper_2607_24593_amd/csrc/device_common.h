@@ -87,6 +87,42 @@ __device__ __forceinline__ uint32_t float_key(float f) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
+// bf16 bits of an fp32 value, rounded to nearest even (finite values).
+__device__ __forceinline__ uint16_t bf16_rne(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+// Score rows hold fp32 or bf16 values (the fp8 path stores bf16 scores); E is
+// float or bf16_t (bf16 bits).  A 16-byte vector holds N scores, widened to
+// fp32 exactly (a bf16 value is the high half of an fp32 word).
+using bf16_t = uint16_t;
+template <class E>
+struct ScoreVec;
+template <>
+struct ScoreVec<float> {
+  static constexpr int N = 4;
+  __device__ static __forceinline__ void unpack(const uint4& a, float (&v)[4]) {
+    v[0] = __uint_as_float(a.x); v[1] = __uint_as_float(a.y);
+    v[2] = __uint_as_float(a.z); v[3] = __uint_as_float(a.w);
+  }
+  __device__ static __forceinline__ float one(const float* row, int64_t e) { return row[e]; }
+};
+template <>
+struct ScoreVec<bf16_t> {
+  static constexpr int N = 8;
+  __device__ static __forceinline__ void unpack(const uint4& a, float (&v)[8]) {
+    v[0] = __uint_as_float(a.x << 16); v[1] = __uint_as_float(a.x & 0xFFFF0000u);
+    v[2] = __uint_as_float(a.y << 16); v[3] = __uint_as_float(a.y & 0xFFFF0000u);
+    v[4] = __uint_as_float(a.z << 16); v[5] = __uint_as_float(a.z & 0xFFFF0000u);
+    v[6] = __uint_as_float(a.w << 16); v[7] = __uint_as_float(a.w & 0xFFFF0000u);
+  }
+  __device__ static __forceinline__ float one(const bf16_t* row, int64_t e) {
+    return __uint_as_float((uint32_t)row[e] << 16);
+  }
+};
+
 // Wavefront reductions (wave64) through cross-lane shuffles.
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll

@@ -45,17 +45,19 @@ hipError_t launch_lin(const void* q, const float* q_scale, const float* w, int64
 
 // Score rows rs (row data [rows, H, d] indexed by row_index(), with lin /
 // lin_scale rows in the same order for fp8) against each sequence's keys
-// 0 .. limit; out [B * (i1 - i0), ld].  lim_max: largest limit of any active row.
+// 0 .. limit; out [B * (i1 - i0), ld] of fp32, or of bf16 when out_bf16 (fp8
+// inputs only).  lim_max: largest limit of any active row.
 hipError_t launch_score(int dtype, const void* q, const float* q_scale, const float* w, const uint8_t* lin,
                         const float* lin_scale, const void* k, const float* k_scale, const KeyMap& km,
-                        const SeqTable& st, const RowSpace& rs, int64_t lim_max, float* out, int64_t ld,
-                        hipStream_t stream);
+                        const SeqTable& st, const RowSpace& rs, int64_t lim_max, void* out, bool out_bf16,
+                        int64_t ld, hipStream_t stream);
 
-// Top-m of score rows: row (b, i) has limit + 1 valid entries; lim_max is
-// the largest limit.  Up to 256 long rows (decode) are split over several
-// workgroups each when `scratch` holds split_scratch_bytes(rows) (else one
-// 1024-thread workgroup each); more rows take one 512-thread workgroup each.
-hipError_t launch_topk(const float* scores, int64_t ld, const SeqTable& st, const RowSpace& rs,
+// Top-m of score rows (fp32, or bf16 when scores_bf16): row (b, i) has
+// limit + 1 valid entries; lim_max is the largest limit.  Up to 256 long rows
+// (decode) are split over several workgroups each when `scratch` holds
+// split_scratch_bytes(rows) (else one 1024-thread workgroup each); more rows
+// take one 512-thread workgroup each.
+hipError_t launch_topk(const void* scores, bool scores_bf16, int64_t ld, const SeqTable& st, const RowSpace& rs,
                        const OutDesc& od, int64_t lim_max, void* scratch, size_t scratch_bytes,
                        hipStream_t stream);
 size_t split_scratch_bytes(int64_t rows);

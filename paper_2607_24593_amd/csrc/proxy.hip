@@ -32,12 +32,6 @@ __device__ __forceinline__ float decode_e4m3(uint32_t word, int byte) {
   }
 }
 
-__device__ __forceinline__ uint16_t bf16_rne(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
-}
-
 template <int DT>
 __global__ __launch_bounds__(256) void proxy_kernel(const uint8_t* __restrict__ q,
                                                     const float* __restrict__ q_scale,

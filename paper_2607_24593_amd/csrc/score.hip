@@ -5,7 +5,8 @@
 // sequence's keys straight from global memory (each lane loads 32 contiguous
 // bytes; a fragment is one contiguous 2 KiB (fp8) block).  The ReLU, the
 // gate-and-scale weighting and the head reduction run in the MFMA epilogue
-// (mfma_tile.h), so every (row, key) pair leaves the kernel as one fp32.
+// (mfma_tile.h), so every (row, key) pair leaves the kernel as one fp32, or
+// one bf16 (round to nearest even) where the caller asks for bf16 score rows.
 //
 // Two wave arrangements:
 //   rows mode  (>= 16 rows per sequence, prefill): the 4 waves hold 4 different
@@ -30,7 +31,8 @@ namespace pivot {
 // loads read zeros, and adding a fragment's lane offset cannot wrap it.
 constexpr uint32_t kDropOffset = 0x80000000u;
 
-template <int DT, int R, bool KSPLIT, bool PAGED>
+// OB16: scores leave as bf16 (RNE) instead of fp32.
+template <int DT, int R, bool KSPLIT, bool PAGED, bool OB16>
 __global__ __launch_bounds__(256) void score_kernel(const uint8_t* __restrict__ q,
                                                     const float* __restrict__ q_scale,
                                                     const float* __restrict__ w,
@@ -38,8 +40,9 @@ __global__ __launch_bounds__(256) void score_kernel(const uint8_t* __restrict__ 
                                                     const float* __restrict__ lin_scale,
                                                     const uint8_t* __restrict__ k,
                                                     const float* __restrict__ k_scale, KeyMap km,
-                                                    SeqTable st, RowSpace rs, float* __restrict__ out,
+                                                    SeqTable st, RowSpace rs, void* __restrict__ out,
                                                     int64_t ld, int seg_keys) {
+  constexpr int SE = OB16 ? 2 : 4;  // bytes per score
   using Tile = RowTile<DT, R>;
   constexpr int EB = Tile::EB;
   constexpr int KB = kD * EB;  // bytes per key
@@ -165,15 +168,19 @@ __global__ __launch_bounds__(256) void score_kernel(const uint8_t* __restrict__ 
   // hardware drops.  Every lane issues the same stores, so the count of
   // outstanding memory operations never depends on the data and the waits
   // before each fragment stay exact.  (The host keeps R * ld * 4 < 2^31.)
-  const __amdgpu_buffer_rsrc_t orr = buffer_rsrc(out + ((int64_t)b * nrows + (i_w - rs.i0)) * ld + seg0,
-                                                 (uint32_t)(((int64_t)(R - 1) * ld + nkeys) * 4));
-  const uint32_t my_off = (uint32_t)((int64_t)qr * ld * 4);
+  const __amdgpu_buffer_rsrc_t orr =
+      buffer_rsrc((uint8_t*)out + (((int64_t)b * nrows + (i_w - rs.i0)) * ld + seg0) * SE,
+                  (uint32_t)(((int64_t)(R - 1) * ld + nkeys) * SE));
+  const uint32_t my_off = (uint32_t)((int64_t)qr * ld * SE);
 
   auto emit = [&](float acc, int base) {
     const int s = base + lr;
     if constexpr (DT == kFp8) acc *= sks[s & 4095];
-    const uint32_t off = (writer && s < my_n) ? my_off + 4u * (uint32_t)s : 0xFFFFFFFFu;
-    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc), orr, off, 0, 0);
+    const uint32_t off = (writer && s < my_n) ? my_off + (uint32_t)SE * (uint32_t)s : 0xFFFFFFFFu;
+    if constexpr (OB16)
+      __builtin_amdgcn_raw_buffer_store_b16(bf16_rne(acc), orr, off, 0, 0);
+    else
+      __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc), orr, off, 0, 0);
   };
   // Three key fragments rotate: while one is scored the next two are loading.
   // The loop body has no exits, so the compiler keeps each reload right after
@@ -193,10 +200,10 @@ __global__ __launch_bounds__(256) void score_kernel(const uint8_t* __restrict__ 
 // causal tail: 256 CUs x 2 resident workgroups x 4 rounds.
 constexpr int64_t kTargetWorkgroups = 2048;
 
-template <int DT, int R, bool KSPLIT>
+template <int DT, int R, bool KSPLIT, bool OB16>
 static hipError_t run_score(const void* q, const float* qs, const float* w, const uint8_t* lin, const float* lsc,
                             const void* k, const float* ks, const KeyMap& km, const SeqTable& st,
-                            const RowSpace& rs, int64_t lim_max, float* out, int64_t ld, int max_seg,
+                            const RowSpace& rs, int64_t lim_max, void* out, int64_t ld, int max_seg,
                             hipStream_t stream) {
   constexpr int RB = KSPLIT ? R : 4 * R;
   const int nrows = rs.i1 - rs.i0;
@@ -210,41 +217,52 @@ static hipError_t run_score(const void* q, const float* qs, const float* w, cons
     return hipErrorInvalidConfiguration;
   const dim3 grid = KSPLIT ? dim3((unsigned)nseg, (unsigned)nblk) : dim3((unsigned)(nseg * nblk));
   if (km.pages)
-    hipLaunchKernelGGL((score_kernel<DT, R, KSPLIT, true>), grid, dim3(256), 0, stream, (const uint8_t*)q, qs, w, lin,
-                       lsc, (const uint8_t*)k, ks, km, st, rs, out, ld, seg);
+    hipLaunchKernelGGL((score_kernel<DT, R, KSPLIT, true, OB16>), grid, dim3(256), 0, stream, (const uint8_t*)q, qs,
+                       w, lin, lsc, (const uint8_t*)k, ks, km, st, rs, out, ld, seg);
   else
-    hipLaunchKernelGGL((score_kernel<DT, R, KSPLIT, false>), grid, dim3(256), 0, stream, (const uint8_t*)q, qs, w,
-                       lin, lsc, (const uint8_t*)k, ks, km, st, rs, out, ld, seg);
+    hipLaunchKernelGGL((score_kernel<DT, R, KSPLIT, false, OB16>), grid, dim3(256), 0, stream, (const uint8_t*)q, qs,
+                       w, lin, lsc, (const uint8_t*)k, ks, km, st, rs, out, ld, seg);
   return hipGetLastError();
+}
+
+template <bool OB16>
+static hipError_t score_fp8(const void* q, const float* q_scale, const float* w, const uint8_t* lin,
+                            const float* lin_scale, const void* k, const float* k_scale, const KeyMap& km,
+                            const SeqTable& st, const RowSpace& rs, int64_t lim_max, void* out, int64_t ld,
+                            hipStream_t stream) {
+  const int nrows = rs.i1 - rs.i0;
+  if (nrows >= 16)
+    return run_score<kFp8, 4, false, OB16>(q, q_scale, w, lin, lin_scale, k, k_scale, km, st, rs, lim_max, out,
+                                           ld, 4096, stream);
+  if (nrows == 1)
+    return run_score<kFp8, 1, true, OB16>(q, q_scale, w, lin, lin_scale, k, k_scale, km, st, rs, lim_max, out,
+                                          ld, 2048, stream);
+  if (nrows == 2)
+    return run_score<kFp8, 2, true, OB16>(q, q_scale, w, lin, lin_scale, k, k_scale, km, st, rs, lim_max, out,
+                                          ld, 2048, stream);
+  return run_score<kFp8, 4, true, OB16>(q, q_scale, w, lin, lin_scale, k, k_scale, km, st, rs, lim_max, out, ld,
+                                        2048, stream);
 }
 
 hipError_t launch_score(int dtype, const void* q, const float* q_scale, const float* w, const uint8_t* lin,
                         const float* lin_scale, const void* k, const float* k_scale, const KeyMap& km,
-                        const SeqTable& st, const RowSpace& rs, int64_t lim_max, float* out, int64_t ld,
-                        hipStream_t stream) {
+                        const SeqTable& st, const RowSpace& rs, int64_t lim_max, void* out, bool out_bf16,
+                        int64_t ld, hipStream_t stream) {
   const int nrows = rs.i1 - rs.i0;
   if (nrows <= 0 || lim_max < 0 || st.n <= 0) return hipSuccess;
-  if (dtype == kFp8) {
-    if (nrows >= 16)
-      return run_score<kFp8, 4, false>(q, q_scale, w, lin, lin_scale, k, k_scale, km, st, rs, lim_max,
-                                       out, ld, 4096, stream);
-    if (nrows == 1)
-      return run_score<kFp8, 1, true>(q, q_scale, w, lin, lin_scale, k, k_scale, km, st, rs, lim_max,
-                                      out, ld, 2048, stream);
-    if (nrows == 2)
-      return run_score<kFp8, 2, true>(q, q_scale, w, lin, lin_scale, k, k_scale, km, st, rs, lim_max,
-                                      out, ld, 2048, stream);
-    return run_score<kFp8, 4, true>(q, q_scale, w, lin, lin_scale, k, k_scale, km, st, rs, lim_max, out,
-                                    ld, 2048, stream);
-  }
+  if (dtype == kFp8)
+    return out_bf16 ? score_fp8<true>(q, q_scale, w, lin, lin_scale, k, k_scale, km, st, rs, lim_max, out, ld, stream)
+                    : score_fp8<false>(q, q_scale, w, lin, lin_scale, k, k_scale, km, st, rs, lim_max, out, ld,
+                                       stream);
+  if (out_bf16) return hipErrorInvalidValue;  // bf16 inputs keep fp32 scores
   if (nrows >= 16)
-    return run_score<kBf16, 2, false>(q, nullptr, w, nullptr, nullptr, k, nullptr, km, st, rs, lim_max,
-                                      out, ld, 2048, stream);
+    return run_score<kBf16, 2, false, false>(q, nullptr, w, nullptr, nullptr, k, nullptr, km, st, rs, lim_max,
+                                             out, ld, 2048, stream);
   if (nrows == 1)
-    return run_score<kBf16, 1, true>(q, nullptr, w, nullptr, nullptr, k, nullptr, km, st, rs, lim_max,
-                                     out, ld, 2048, stream);
-  return run_score<kBf16, 2, true>(q, nullptr, w, nullptr, nullptr, k, nullptr, km, st, rs, lim_max, out,
-                                   ld, 2048, stream);
+    return run_score<kBf16, 1, true, false>(q, nullptr, w, nullptr, nullptr, k, nullptr, km, st, rs, lim_max,
+                                            out, ld, 2048, stream);
+  return run_score<kBf16, 2, true, false>(q, nullptr, w, nullptr, nullptr, k, nullptr, km, st, rs, lim_max, out,
+                                          ld, 2048, stream);
 }
 
 }  // namespace pivot

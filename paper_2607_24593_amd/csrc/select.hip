@@ -1,12 +1,13 @@
-// Per-row top-m selection over fp32 score rows (the TopK of Sec. 3.1 and of
-// Eqs. 6-7): one 512-thread workgroup per row (1024 threads when a launch
+// Per-row top-m selection over score rows of fp32, or of bf16 (the rows the
+// fp8 path writes; every bf16 value widens exactly to the fp32 it selects
+// on), for the TopK of Sec. 3.1 and of Eqs. 6-7: one 512-thread workgroup per row (1024 threads when a launch
 // holds at most 256 long rows), or, for such a launch given scratch (decode),
 // the split select described below.
 //
 // Long rows (n >= kSampleMinLen) are read once when the expected number of
 // compacted keys fits in LDS:
 //   1 sample   every stride-th 256-byte chunk of the row (at most 8192
-//              scores) is held in registers; two histogram passes over the
+//              fp32 or 16384 bf16 scores) is held in registers; two histogram passes over the
 //              sample (top 12, then next 8 key bits) find a 20-bit prefix
 //              `thr` such that at least ts sampled keys have prefix >= thr,
 //              where ts is the sample's expected share of m plus four
@@ -58,49 +59,55 @@ constexpr int kSplitMinP = 4, kSplitMaxP = 16;
 constexpr int kSplitPerMax = kSplitSlots / kSplitMinP;
 constexpr int kSplitTargetBlocks = 1024;
 
-// Elements of a score row, visited with 16-byte vector loads (U in flight per
-// thread) when aligned.
-template <int T, int U>
+// Elements of a score row (fp32 or bf16, E), visited with 16-byte vector
+// loads (U in flight per thread) when aligned.
+template <int T, int U, class E>
 struct RowSource {
-  const float* row;
+  using SV = ScoreVec<E>;
+  static constexpr int N = SV::N;
+  const E* row;
   int count;
   template <class F>
   __device__ __forceinline__ void visit(F f) const {
     const int tid = threadIdx.x;
     if ((reinterpret_cast<uintptr_t>(row) & 15u) == 0) {
-      const int n4 = count >> 2;
-      const float4* r4 = reinterpret_cast<const float4*>(row);
-      auto each = [&](const float4& a, int i) {
-        f(float_key(a.x), 4 * i); f(float_key(a.y), 4 * i + 1);
-        f(float_key(a.z), 4 * i + 2); f(float_key(a.w), 4 * i + 3);
+      const int nv = count / N;
+      const uint4* r16 = reinterpret_cast<const uint4*>(row);
+      auto each = [&](const uint4& a, int i) {
+        float v[N];
+        SV::unpack(a, v);
+#pragma unroll
+        for (int j = 0; j < N; ++j) f(float_key(v[j]), N * i + j);
       };
       int i = tid;
-      for (; i + (U - 1) * T < n4; i += U * T) {
-        float4 a[U];
+      for (; i + (U - 1) * T < nv; i += U * T) {
+        uint4 a[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) a[u] = r4[i + u * T];
+        for (int u = 0; u < U; ++u) a[u] = r16[i + u * T];
 #pragma unroll
         for (int u = 0; u < U; ++u) each(a[u], i + u * T);
       }
-      for (; i < n4; i += T) each(r4[i], i);
-      for (int e = 4 * n4 + tid; e < count; e += T) f(float_key(row[e]), e);
+      for (; i < nv; i += T) each(r16[i], i);
+      for (int e = N * nv + tid; e < count; e += T) f(float_key(SV::one(row, e)), e);
     } else {
-      for (int e = tid; e < count; e += T) f(float_key(row[e]), e);
+      for (int e = tid; e < count; e += T) f(float_key(SV::one(row, e)), e);
     }
   }
 };
 
-// The sampled keys (positions are not needed): V float4 per thread.
-template <int V>
+// The sampled keys (positions are not needed): V 16-byte vectors of N
+// scores per thread.
+template <int V, int N>
 struct SampleSource {
-  uint32_t key[4 * V];
+  uint32_t key[N * V];
   bool ok[V];
   template <class F>
   __device__ __forceinline__ void visit(F f) const {
 #pragma unroll
     for (int v = 0; v < V; ++v)
       if (ok[v]) {
-        f(key[4 * v], 0); f(key[4 * v + 1], 0); f(key[4 * v + 2], 0); f(key[4 * v + 3], 0);
+#pragma unroll
+        for (int j = 0; j < N; ++j) f(key[N * v + j], 0);
       }
   }
 };
@@ -133,29 +140,30 @@ __device__ uint32_t sample_prefix(const Src& src, uint32_t ts, uint32_t* hist, S
 // load) when the expected compacted count ts n / s would not leave room for
 // its spread in CAP entries; else the threshold score fthr (every key with
 // prefix >= thr compares >= fthr as a float).  Uniform over the workgroup.
-template <int T, int CAP>
-__device__ bool sample_threshold(const float* row, int n, int m, uint32_t* hist, SelectShared& sel, float& fthr) {
-  constexpr int SV = kSampleChunks * kChunk4 / T;  // sampled float4 per thread
+template <int T, int CAP, class E>
+__device__ bool sample_threshold(const E* row, int n, int m, uint32_t* hist, SelectShared& sel, float& fthr) {
+  using SVec = ScoreVec<E>;
+  constexpr int N = SVec::N;
+  constexpr int SV = kSampleChunks * kChunk4 / T;  // sampled 16-byte vectors per thread
   const int tid = threadIdx.x;
-  const int nch = n / (4 * kChunk4);
+  const int nch = n / (N * kChunk4);
   const int stride = max(16, (nch + kSampleChunks - 1) / kSampleChunks);
   const int sch = (nch + stride - 1) / stride;  // chunks 0, stride, 2 stride, ... < nch
-  const int s = sch * 4 * kChunk4;
+  const int s = sch * N * kChunk4;
   const float rm = (float)s * (float)m / (float)n;
   const uint32_t ts = (uint32_t)ceilf(rm + 4.0f * sqrtf(rm)) + 1u;
   if (!(ts < (uint32_t)s && (float)ts * (float)n <= 0.8f * (float)CAP * (float)s)) return false;
-  const float4* r4 = reinterpret_cast<const float4*>(row);
-  SampleSource<SV> smp;
+  const uint4* r16 = reinterpret_cast<const uint4*>(row);
+  SampleSource<SV, N> smp;
 #pragma unroll
   for (int v = 0; v < SV; ++v) {
     const int qi = tid + T * v;
     smp.ok[v] = qi < sch * kChunk4;
-    const float4 a = smp.ok[v] ? r4[(int64_t)(qi / kChunk4) * stride * kChunk4 + qi % kChunk4]
-                               : make_float4(0.f, 0.f, 0.f, 0.f);
-    smp.key[4 * v] = float_key(a.x);
-    smp.key[4 * v + 1] = float_key(a.y);
-    smp.key[4 * v + 2] = float_key(a.z);
-    smp.key[4 * v + 3] = float_key(a.w);
+    const uint4 a = smp.ok[v] ? r16[(int64_t)(qi / kChunk4) * stride * kChunk4 + qi % kChunk4] : make_uint4(0u, 0u, 0u, 0u);
+    float x[N];
+    SVec::unpack(a, x);
+#pragma unroll
+    for (int j = 0; j < N; ++j) smp.key[N * v + j] = float_key(x[j]);
   }
   const uint32_t thr = sample_prefix<T>(smp, ts, hist, sel);
   // key >> 12 >= thr  <=>  score >= the smallest score with that prefix
@@ -170,9 +178,11 @@ __device__ bool sample_threshold(const float* row, int n, int m, uint32_t* hist,
 // are packed to the front.  The loops are uniform over the wave, so the
 // running count stays the same in every lane.  Returns the number of keys, or
 // CAP + 1 when a segment overflowed.  Aligned rows only.
-template <int T, int U, int CAP>
-__device__ __forceinline__ int stream_compact(const float* row, int n, float fthr, uint32_t* ckey, int32_t* cpos,
+template <int T, int U, int CAP, class E>
+__device__ __forceinline__ int stream_compact(const E* row, int n, float fthr, uint32_t* ckey, int32_t* cpos,
                                               int32_t* wcnt) {
+  using SV = ScoreVec<E>;
+  constexpr int N = SV::N;
   constexpr int NW = T / 64, SEG = CAP / NW, R = (SEG + 63) / 64;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -192,29 +202,34 @@ __device__ __forceinline__ int stream_compact(const float* row, int n, float fth
       wc += (int)__popcll((unsigned long long)bal);
     }
   };
-  const int n4 = n >> 2;
-  const float4* r4 = reinterpret_cast<const float4*>(row);
+  const int nv = n / N;
+  const uint4* r16 = reinterpret_cast<const uint4*>(row);
   int base = 0;
-  for (; base + U * T <= n4; base += U * T) {
-    float4 a[U];
+  for (; base + U * T <= nv; base += U * T) {
+    uint4 a[U];
 #pragma unroll
-    for (int u = 0; u < U; ++u) a[u] = r4[base + u * T + tid];
+    for (int u = 0; u < U; ++u) a[u] = r16[base + u * T + tid];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int p = 4 * (base + u * T + tid);
-      take(true, a[u].x, p); take(true, a[u].y, p + 1); take(true, a[u].z, p + 2); take(true, a[u].w, p + 3);
+      float x[N];
+      SV::unpack(a[u], x);
+      const int p = N * (base + u * T + tid);
+#pragma unroll
+      for (int j = 0; j < N; ++j) take(true, x[j], p + j);
     }
   }
-  for (; base < n4; base += T) {
+  for (; base < nv; base += T) {
     const int q = base + tid;
-    const bool ok = q < n4;
-    const float4 a = ok ? r4[q] : make_float4(0.f, 0.f, 0.f, 0.f);
-    take(ok, a.x, 4 * q); take(ok, a.y, 4 * q + 1); take(ok, a.z, 4 * q + 2); take(ok, a.w, 4 * q + 3);
+    const bool ok = q < nv;
+    float x[N];
+    SV::unpack(ok ? r16[q] : make_uint4(0u, 0u, 0u, 0u), x);
+#pragma unroll
+    for (int j = 0; j < N; ++j) take(ok, x[j], N * q + j);
   }
-  if (4 * n4 < n) {  // the n mod 4 tail
-    const int e = 4 * n4 + tid;
+  if (N * nv < n) {  // the n mod N tail
+    const int e = N * nv + tid;
     const bool ok = e < n;
-    take(ok, ok ? row[e] : 0.f, e);
+    take(ok, ok ? SV::one(row, e) : 0.f, e);
   }
   if (lane == 0) wcnt[wv] = wc;
   __syncthreads();
@@ -277,10 +292,12 @@ struct RowDest {
 // of short rows only takes the kernel without it, which keeps the two-pass
 // loops as lean as they compile alone).  Register budget: as many 512-thread
 // workgroups per CU as LDS allows (three for CAP 4096, else two).
-template <int CAP, int T, bool SAMPLE>
+template <int CAP, int T, bool SAMPLE, class E>
 __global__ __launch_bounds__(T) __attribute__((amdgpu_waves_per_eu(CAP == kSelCapSmall && T == kSelThreads ? 6 : 4)))
-void topk_rows_kernel(const float* __restrict__ scores, int64_t ld, SeqTable st, RowSpace rs, OutDesc od) {
-  constexpr int U = T == kSelThreads ? 4 : 8;       // row loads in flight per thread
+void topk_rows_kernel(const E* __restrict__ scores, int64_t ld, SeqTable st, RowSpace rs, OutDesc od) {
+  // 16-byte row loads in flight per thread (the same count of scores for bf16
+  // rows, whose vectors hold twice as many)
+  constexpr int U = (T == kSelThreads ? 4 : 8) * (int)sizeof(E) / 4;
   __shared__ TwoLevelShared<CAP> sh;
   const int nrows = rs.i1 - rs.i0;
   const int b = blockIdx.x / nrows;
@@ -289,7 +306,7 @@ void topk_rows_kernel(const float* __restrict__ scores, int64_t ld, SeqTable st,
   const int tid = threadIdx.x;
   const int64_t n64 = row_limit(st, rs, b, i) + 1;
   const int n = (int)max((int64_t)0, n64);
-  const float* row = scores + ((int64_t)b * nrows + (i - rs.i0)) * ld;
+  const E* row = scores + ((int64_t)b * nrows + (i - rs.i0)) * ld;
   const int m = od.m;
   const RowDest put(od, st, b, i);
   if (n <= m) {
@@ -297,7 +314,7 @@ void topk_rows_kernel(const float* __restrict__ scores, int64_t ld, SeqTable st,
     return;
   }
   if (tid == 0) sh.sel.emitted = 0;
-  RowSource<T, U> src{row, n};
+  RowSource<T, U, E> src{row, n};
   const bool aligned = (reinterpret_cast<uintptr_t>(row) & 15u) == 0;
   float fthr;
   if (SAMPLE && n >= kSampleMinLen && aligned) {
@@ -320,8 +337,8 @@ void topk_rows_kernel(const float* __restrict__ scores, int64_t ld, SeqTable st,
 // Split select, step 1: workgroup r writes row r's threshold score to
 // thr[r], or NaN when the row takes the two-pass path (n <= m, short or
 // unaligned row, sample declined).
-template <int CAP, int T>
-__global__ __launch_bounds__(T) void topk_thr_kernel(const float* __restrict__ scores, int64_t ld, SeqTable st,
+template <int CAP, int T, class E>
+__global__ __launch_bounds__(T) void topk_thr_kernel(const E* __restrict__ scores, int64_t ld, SeqTable st,
                                                      RowSpace rs, int m, float* __restrict__ thr) {
   __shared__ uint32_t hist[4096];
   __shared__ SelectShared sel;
@@ -331,7 +348,7 @@ __global__ __launch_bounds__(T) void topk_thr_kernel(const float* __restrict__ s
   const int i = rs.i0 + r % nrows;
   if (!row_active(st, rs, b, i)) return;
   const int n = (int)max((int64_t)0, row_limit(st, rs, b, i) + 1);
-  const float* row = scores + ((int64_t)b * nrows + (i - rs.i0)) * ld;
+  const E* row = scores + ((int64_t)b * nrows + (i - rs.i0)) * ld;
   const bool aligned = (reinterpret_cast<uintptr_t>(row) & 15u) == 0;
   float fthr;
   if (n <= m || n < kSampleMinLen || !aligned || !sample_threshold<T, CAP>(row, n, m, hist, sel, fthr))
@@ -340,16 +357,19 @@ __global__ __launch_bounds__(T) void topk_thr_kernel(const float* __restrict__ s
 }
 
 // Split select, step 2: workgroup (r, s) compacts the keys >= thr[r] among
-// float4s [s per4, (s+1) per4) of row r (the last slice also takes the
-// n mod 4 tail) into LDS and writes them to cand[(r P + s) per ..] with their
-// count in cnt[r P + s]: -1 when the row takes the two-pass path (thr[r] is
-// NaN), -2 when the slice held more than `per` keys.
-__global__ __launch_bounds__(kSplitThreads) void topk_slice_kernel(const float* __restrict__ scores, int64_t ld,
+// 16-byte vectors [s per_v, (s+1) per_v) of row r (the last slice also takes
+// the n mod N tail) into LDS and writes them to cand[(r P + s) per ..] with
+// their count in cnt[r P + s]: -1 when the row takes the two-pass path
+// (thr[r] is NaN), -2 when the slice held more than `per` keys.
+template <class E>
+__global__ __launch_bounds__(kSplitThreads) void topk_slice_kernel(const E* __restrict__ scores, int64_t ld,
                                                                    SeqTable st, RowSpace rs, int P, int per,
                                                                    const float* __restrict__ thr,
                                                                    uint2* __restrict__ cand,
                                                                    int32_t* __restrict__ cnt) {
-  constexpr int T = kSplitThreads, U = 8;
+  using SV = ScoreVec<E>;
+  constexpr int N = SV::N;
+  constexpr int T = kSplitThreads, U = 8 * (int)sizeof(E) / 4;
   __shared__ uint2 lc[kSplitPerMax];
   __shared__ int32_t nc;
   const int nrows = rs.i1 - rs.i0;
@@ -359,7 +379,7 @@ __global__ __launch_bounds__(kSplitThreads) void topk_slice_kernel(const float* 
   if (!row_active(st, rs, b, i)) return;
   const int tid = threadIdx.x;
   const int n = (int)max((int64_t)0, row_limit(st, rs, b, i) + 1);
-  const float* row = scores + ((int64_t)b * nrows + (i - rs.i0)) * ld;
+  const E* row = scores + ((int64_t)b * nrows + (i - rs.i0)) * ld;
   int32_t* my_cnt = cnt + (int64_t)r * P + slice;
   const float fthr = thr[r];
   if (__builtin_isnan(fthr)) {
@@ -374,27 +394,32 @@ __global__ __launch_bounds__(kSplitThreads) void topk_slice_kernel(const float* 
       if (c < per) lc[c] = make_uint2(float_key(v), (uint32_t)pos);
     }
   };
-  const int n4 = n >> 2;
-  const int per4 = (n4 + P - 1) / P;
-  const int a4 = slice * per4, e4 = min(n4, a4 + per4);
-  const float4* r4 = reinterpret_cast<const float4*>(row);
-  int q = a4 + tid;
-  for (; q + (U - 1) * T < e4; q += U * T) {
-    float4 x[U];
+  const int nv = n / N;
+  const int per_v = (nv + P - 1) / P;
+  const int a_v = slice * per_v, e_v = min(nv, a_v + per_v);
+  const uint4* r16 = reinterpret_cast<const uint4*>(row);
+  int q = a_v + tid;
+  for (; q + (U - 1) * T < e_v; q += U * T) {
+    uint4 x[U];
 #pragma unroll
-    for (int u = 0; u < U; ++u) x[u] = r4[q + u * T];
+    for (int u = 0; u < U; ++u) x[u] = r16[q + u * T];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int p = 4 * (q + u * T);
-      take(x[u].x, p); take(x[u].y, p + 1); take(x[u].z, p + 2); take(x[u].w, p + 3);
+      float v[N];
+      SV::unpack(x[u], v);
+      const int p = N * (q + u * T);
+#pragma unroll
+      for (int j = 0; j < N; ++j) take(v[j], p + j);
     }
   }
-  for (; q < e4; q += T) {
-    const float4 x = r4[q];
-    take(x.x, 4 * q); take(x.y, 4 * q + 1); take(x.z, 4 * q + 2); take(x.w, 4 * q + 3);
+  for (; q < e_v; q += T) {
+    float v[N];
+    SV::unpack(r16[q], v);
+#pragma unroll
+    for (int j = 0; j < N; ++j) take(v[j], N * q + j);
   }
   if (slice == P - 1)
-    for (int e = 4 * n4 + tid; e < n; e += T) take(row[e], e);
+    for (int e = N * nv + tid; e < n; e += T) take(SV::one(row, e), e);
   __syncthreads();
   const int c = nc;
   if (tid == 0) *my_cnt = c <= per ? c : -2;
@@ -407,12 +432,12 @@ __global__ __launch_bounds__(kSplitThreads) void topk_slice_kernel(const float* 
 // Split select, step 3: one workgroup per row gathers the keys its slices
 // compacted (when every slice kept its keys and they number m .. CAP) into
 // LDS and selects exactly over them; any other row takes the two-pass path.
-template <int CAP, int T>
-__global__ __launch_bounds__(T) void topk_merge_kernel(const float* __restrict__ scores, int64_t ld, SeqTable st,
+template <int CAP, int T, class E>
+__global__ __launch_bounds__(T) void topk_merge_kernel(const E* __restrict__ scores, int64_t ld, SeqTable st,
                                                        RowSpace rs, OutDesc od, int P, int per,
                                                        const uint2* __restrict__ cand,
                                                        const int32_t* __restrict__ cnt) {
-  constexpr int U = 8;
+  constexpr int U = 8 * (int)sizeof(E) / 4;  // 16-byte loads in flight (fallback path)
   constexpr int V = (CAP + T - 1) / T;  // gathered keys per thread
   __shared__ TwoLevelShared<CAP> sh;
   __shared__ int32_t pre[kSplitMaxP + 1];
@@ -423,7 +448,7 @@ __global__ __launch_bounds__(T) void topk_merge_kernel(const float* __restrict__
   if (!row_active(st, rs, b, i)) return;
   const int tid = threadIdx.x;
   const int n = (int)max((int64_t)0, row_limit(st, rs, b, i) + 1);
-  const float* row = scores + ((int64_t)b * nrows + (i - rs.i0)) * ld;
+  const E* row = scores + ((int64_t)b * nrows + (i - rs.i0)) * ld;
   const int m = od.m;
   const RowDest put(od, st, b, i);
   if (n <= m) {
@@ -485,7 +510,7 @@ __global__ __launch_bounds__(T) void topk_merge_kernel(const float* __restrict__
       block_select<T, false>(src, (uint32_t)m, sh.sel, put);
     return;
   }
-  RowSource<T, U> src{row, n};
+  RowSource<T, U, E> src{row, n};
   two_level_select<T>(src, (uint32_t)m, sh, put);
 }
 
@@ -493,9 +518,10 @@ size_t split_scratch_bytes(int64_t rows) {
   return (size_t)rows * ((size_t)kSplitSlots * sizeof(uint2) + (size_t)kSplitMaxP * sizeof(int32_t) + sizeof(float));
 }
 
-hipError_t launch_topk(const float* scores, int64_t ld, const SeqTable& st, const RowSpace& rs,
-                       const OutDesc& od, int64_t lim_max, void* scratch, size_t scratch_bytes,
-                       hipStream_t stream) {
+template <class E>
+static hipError_t topk_launch(const E* scores, int64_t ld, const SeqTable& st, const RowSpace& rs,
+                              const OutDesc& od, int64_t lim_max, void* scratch, size_t scratch_bytes,
+                              hipStream_t stream) {
   const int nrows = rs.i1 - rs.i0;
   if (nrows <= 0 || st.n <= 0) return hipSuccess;
   const int64_t blocks = (int64_t)st.n * nrows;
@@ -511,46 +537,54 @@ hipError_t launch_topk(const float* scores, int64_t ld, const SeqTable& st, cons
     const dim3 sgrid((unsigned)blocks, (unsigned)P);
     const bool small = od.m <= kSelCapSmall / 2;
     if (small)
-      hipLaunchKernelGGL((topk_thr_kernel<kSelCapSmall, kSelThreadsWide>), dim3((unsigned)blocks),
+      hipLaunchKernelGGL((topk_thr_kernel<kSelCapSmall, kSelThreadsWide, E>), dim3((unsigned)blocks),
                          dim3(kSelThreadsWide), 0, stream, scores, ld, st, rs, od.m, thr);
     else
-      hipLaunchKernelGGL((topk_thr_kernel<kSelCapLarge, kSelThreadsWide>), dim3((unsigned)blocks),
+      hipLaunchKernelGGL((topk_thr_kernel<kSelCapLarge, kSelThreadsWide, E>), dim3((unsigned)blocks),
                          dim3(kSelThreadsWide), 0, stream, scores, ld, st, rs, od.m, thr);
-    hipLaunchKernelGGL(topk_slice_kernel, sgrid, dim3(kSplitThreads), 0, stream, scores, ld, st, rs, P, per, thr,
+    hipLaunchKernelGGL(topk_slice_kernel<E>, sgrid, dim3(kSplitThreads), 0, stream, scores, ld, st, rs, P, per, thr,
                        cand, cnt);
     if (small)
-      hipLaunchKernelGGL((topk_merge_kernel<kSelCapSmall, kSelThreadsWide>), dim3((unsigned)blocks),
+      hipLaunchKernelGGL((topk_merge_kernel<kSelCapSmall, kSelThreadsWide, E>), dim3((unsigned)blocks),
                          dim3(kSelThreadsWide), 0, stream, scores, ld, st, rs, od, P, per, cand, cnt);
     else
-      hipLaunchKernelGGL((topk_merge_kernel<kSelCapLarge, kSelThreadsWide>), dim3((unsigned)blocks),
+      hipLaunchKernelGGL((topk_merge_kernel<kSelCapLarge, kSelThreadsWide, E>), dim3((unsigned)blocks),
                          dim3(kSelThreadsWide), 0, stream, scores, ld, st, rs, od, P, per, cand, cnt);
     return hipGetLastError();
   }
   if (blocks <= kWideMaxRows && lim_max + 1 >= kSampleMinLen) {
     // few long rows (decode): one wide workgroup per row
     if (od.m <= kSelCapSmall / 2)
-      hipLaunchKernelGGL((topk_rows_kernel<kSelCapSmall, kSelThreadsWide, true>), dim3((unsigned)blocks),
+      hipLaunchKernelGGL((topk_rows_kernel<kSelCapSmall, kSelThreadsWide, true, E>), dim3((unsigned)blocks),
                          dim3(kSelThreadsWide), 0, stream, scores, ld, st, rs, od);
     else
-      hipLaunchKernelGGL((topk_rows_kernel<kSelCapLarge, kSelThreadsWide, true>), dim3((unsigned)blocks),
+      hipLaunchKernelGGL((topk_rows_kernel<kSelCapLarge, kSelThreadsWide, true, E>), dim3((unsigned)blocks),
                          dim3(kSelThreadsWide), 0, stream, scores, ld, st, rs, od);
     return hipGetLastError();
   }
   const bool small = od.m <= kSelCapSmall / 2, sample = lim_max + 1 >= kSampleMinLen;
   const dim3 grid((unsigned)blocks), block(kSelThreads);
   if (small && sample)
-    hipLaunchKernelGGL((topk_rows_kernel<kSelCapSmall, kSelThreads, true>), grid, block, 0, stream, scores, ld, st, rs,
+    hipLaunchKernelGGL((topk_rows_kernel<kSelCapSmall, kSelThreads, true, E>), grid, block, 0, stream, scores, ld, st, rs,
                        od);
   else if (small)
-    hipLaunchKernelGGL((topk_rows_kernel<kSelCapSmall, kSelThreads, false>), grid, block, 0, stream, scores, ld, st,
+    hipLaunchKernelGGL((topk_rows_kernel<kSelCapSmall, kSelThreads, false, E>), grid, block, 0, stream, scores, ld, st,
                        rs, od);
   else if (sample)
-    hipLaunchKernelGGL((topk_rows_kernel<kSelCapLarge, kSelThreads, true>), grid, block, 0, stream, scores, ld, st, rs,
+    hipLaunchKernelGGL((topk_rows_kernel<kSelCapLarge, kSelThreads, true, E>), grid, block, 0, stream, scores, ld, st, rs,
                        od);
   else
-    hipLaunchKernelGGL((topk_rows_kernel<kSelCapLarge, kSelThreads, false>), grid, block, 0, stream, scores, ld, st,
+    hipLaunchKernelGGL((topk_rows_kernel<kSelCapLarge, kSelThreads, false, E>), grid, block, 0, stream, scores, ld, st,
                        rs, od);
   return hipGetLastError();
+}
+
+hipError_t launch_topk(const void* scores, bool scores_bf16, int64_t ld, const SeqTable& st, const RowSpace& rs,
+                       const OutDesc& od, int64_t lim_max, void* scratch, size_t scratch_bytes,
+                       hipStream_t stream) {
+  if (scores_bf16)
+    return topk_launch(static_cast<const bf16_t*>(scores), ld, st, rs, od, lim_max, scratch, scratch_bytes, stream);
+  return topk_launch(static_cast<const float*>(scores), ld, st, rs, od, lim_max, scratch, scratch_bytes, stream);
 }
 
 __global__ void fill_guardrail_kernel(int32_t* base, int width, SeqTable st, int j0, int32_t value) {

@@ -222,7 +222,7 @@ def test_layout_workspace_sizes():
         assert L.pivot_workspace_size_layout(ctypes.byref(a), ctypes.byref(lo), ob) == ref
     assert L.pivot_workspace_size_layout(ctypes.byref(a), None, None) == pv.pivot_workspace_size(a, pv.PIVOT_DENSE)
     # two runs of 10 and 7 rows: 3 + 2 groups of 4, 17 query rows; the score
-    # tile holds both sequences' 3 group rows of ld(910) = 960 floats
+    # tile holds both sequences' 3 group rows of ld(910) = 960 bf16 scores
     lin = lambda rows: up(rows * 512) + up(rows * 16)  # noqa: E731
     b = args(B=2, n_q=10, q_pos0=900)
     ragged = L.pivot_workspace_size_layout(ctypes.byref(b), ctypes.byref(layout(cu_q=[0, 10, 17])),
@@ -230,7 +230,7 @@ def test_layout_workspace_sizes():
     ng = 5
     proxies = up(ng * 64 * 128) + up(ng * 4) + up(ng * 64 * 4)
     cand = up(ng * 16 * 4) + up(ng * 4 * 16 * 4)
-    assert ragged == lin(17) + lin(ng) + proxies + cand + 2 * 3 * 960 * 4
+    assert ragged == lin(17) + lin(ng) + proxies + cand + 2 * 3 * 960 * 2
 
 
 def test_empty_runs_need_no_workspace():
@@ -264,9 +264,10 @@ def test_workspace_size_closed_form():
     lin = lambda rows: up(rows * 512) + up(rows * 16)  # noqa: E731  (fp8 epilogue's linear term)
     ld = lambda n: (((n + 63) // 64) | 1) * 64  # noqa: E731  (row stride: an odd multiple of 64 floats)
     assert ld(1000) == 1088 and ld(1024) == 1088 and ld(1088) == 1088
-    # dense, one sequence: 100 rows x ld(1000)=1088 fp32
+    # dense, one sequence: 100 rows x ld(1000)=1088 scores, bf16 for fp8
+    # inputs, fp32 for bf16 inputs
     a = args(n_q=100, q_pos0=900)
-    assert pv.pivot_workspace_size(a, pv.PIVOT_DENSE) == lin(100) + 100 * ld(1000) * 4
+    assert pv.pivot_workspace_size(a, pv.PIVOT_DENSE) == lin(100) + 100 * ld(1000) * 2
     b = args(n_q=100, q_pos0=900, dtype=pv.PIVOT_DT_BF16, scales=False)
     assert pv.pivot_workspace_size(b, pv.PIVOT_DENSE) == 100 * ld(1000) * 4
     # Refine, g=4, c=16, guardrail at c: all 25 groups start at t0 >= 900 >= c;
@@ -275,9 +276,9 @@ def test_workspace_size_closed_form():
     proxies = up(ng * 64 * 128) + up(ng * 4) + up(ng * 64 * 4)
     cand = up(ng * 16 * 4) + up(ng * 4 * 16 * 4)   # candidate sets + members' re-scores
     assert pv.pivot_workspace_size(a, pv.PIVOT_REFINE, 4, 16) == \
-        lin(100) + lin(ng) + proxies + cand + ng * ld(1000) * 4
+        lin(100) + lin(ng) + proxies + cand + ng * ld(1000) * 2
     # Reuse: no candidate buffer, no member rows to re-score
-    assert pv.pivot_workspace_size(a, pv.PIVOT_REUSE, 4, 16) == lin(ng) + proxies + ng * ld(1000) * 4
+    assert pv.pivot_workspace_size(a, pv.PIVOT_REUSE, 4, 16) == lin(ng) + proxies + ng * ld(1000) * 2
     # long prefix: score tiles stay near 1 GiB, plus the split select's scratch
     # for up to 256 long rows (16000 (key, position) pairs, 16 counts and a
     # threshold each)
