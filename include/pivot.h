@@ -20,7 +20,11 @@
  *   - positions are 0-based; a query at position t may select any s <= t;
  *   - an index set is k int32 positions in unspecified order; when fewer than
  *     k positions are valid, all of them are returned followed by -1;
- *   - TopK ranks by score, then by lower position among equal scores;
+ *   - TopK ranks by score, then by lower position among equal scores; with
+ *     fp8 inputs the full-prefix scans (dense, and the proxy scan of Reuse /
+ *     Refine) keep their score rows in bf16 (round to nearest even, relative
+ *     error at most 2^-9, far inside what fp8 inputs resolve) and rank those,
+ *     while Refine ranks its re-scores in fp32; bf16 inputs keep fp32 rows;
  *   - "dev" pointers are device memory on the current HIP device, "host"
  *     pointers are host memory read during the call;
  *   - the caller owns every buffer; the library never allocates device memory
@@ -104,8 +108,9 @@ typedef struct {
  * Workspace bytes needed by pivot_dense_index (mode = PIVOT_DENSE) or by
  * pivot_group_index (mode = PIVOT_REUSE / PIVOT_REFINE with g, c and the
  * guardrail at c) for the shapes in `a`; only the host arrays q_pos0 / n_k are
- * read.  Returns 0 if the shapes are invalid.  The fp32 score rows are tiled so
- * that this size stays near 1 GiB for long prefixes.  Any workspace of at
+ * read.  Returns 0 if the shapes are invalid.  The score rows (bf16 for fp8
+ * inputs, fp32 for bf16 inputs) are tiled so that this size stays near 1 GiB
+ * for long prefixes.  Any workspace of at
  * least this size works; smaller ones down to one score tile also work (more
  * tiles), and below that the entry points return PIVOT_ERR_WORKSPACE.
  */
