@@ -22,9 +22,9 @@
  *     k positions are valid, all of them are returned followed by -1;
  *   - TopK ranks by score, then by lower position among equal scores; with
  *     fp8 inputs the full-prefix scans (dense, and the proxy scan of Reuse /
- *     Refine) keep their score rows in bf16 (round to nearest even, relative
- *     error at most 2^-9, far inside what fp8 inputs resolve) and rank those,
- *     while Refine ranks its re-scores in fp32; bf16 inputs keep fp32 rows;
+ *     Refine) and Refine's member re-scores keep their scores in bf16 (round
+ *     to nearest even, relative error at most 2^-9, far inside what fp8
+ *     inputs resolve) and rank those; bf16 inputs keep fp32 scores;
  *   - "dev" pointers are device memory on the current HIP device, "host"
  *     pointers are host memory read during the call;
  *   - the caller owns every buffer; the library never allocates device memory
@@ -297,6 +297,10 @@ pivot_status pivot_encode_e4m3(const float* x, uint8_t* out, int64_t n, void* st
  * per kernel kind, the number of launches and the summed event-to-event time;
  * it then stops recording.  Event objects are host-side resources created on
  * first use; no device memory is allocated.  One profile at a time per process.
+ * pivot_profile_begin_kinds(mask) brackets only the kinds whose bit
+ * (1 << PIVOT_KERNEL_*) is set, so that the events of other kernels add no
+ * gaps to a timed run; a mask of 0 or with bits past PIVOT_KERNEL_KINDS is
+ * INVALID_ARG.
  */
 enum {
   PIVOT_KERNEL_PROXY = 0,   /* proxy aggregation, Eq. 4 */
@@ -314,6 +318,7 @@ typedef struct {
 } pivot_profile;
 
 pivot_status pivot_profile_begin(void);
+pivot_status pivot_profile_begin_kinds(uint32_t kinds);
 pivot_status pivot_profile_end(pivot_profile* out);
 
 /* Static description of a status code. */

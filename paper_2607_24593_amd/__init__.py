@@ -30,7 +30,7 @@ EXPORTED = ["pivot_workspace_size", "pivot_dense_index", "pivot_group_index", "p
             "pivot_group_workspace_size", "pivot_group_index_opts", "pivot_dense_index_layout",
             "pivot_group_index_layout", "pivot_workspace_size_layout", "pivot_proxy_rows",
             "pivot_score_rows", "pivot_topk_rows", "pivot_topk_rows_workspace_size", "pivot_topk_rows_ws",
-            "pivot_encode_e4m3", "pivot_profile_begin",
+            "pivot_encode_e4m3", "pivot_profile_begin", "pivot_profile_begin_kinds",
             "pivot_profile_end", "pivot_status_string", "pivot_last_error", "pivot_version"]
 KERNELS = ["proxy", "score", "select", "refine", "fill", "lin"]
 
@@ -147,6 +147,8 @@ def lib():
         L.pivot_encode_e4m3.argtypes = [P, P, I64, P]
         L.pivot_profile_begin.restype = I32
         L.pivot_profile_begin.argtypes = []
+        L.pivot_profile_begin_kinds.restype = I32
+        L.pivot_profile_begin_kinds.argtypes = [ctypes.c_uint32]
         L.pivot_profile_end.restype = I32
         L.pivot_profile_end.argtypes = [ctypes.POINTER(pivot_profile)]
         L.pivot_status_string.restype = ctypes.c_char_p
@@ -432,8 +434,15 @@ def pivot_topk_rows_ws(scores, n0, n_step, m, out=None, ws=None, stream=None):
     return out
 
 
-def pivot_profile_begin():
-    _check(lib().pivot_profile_begin(), "pivot_profile_begin")
+def pivot_profile_begin(kinds=None):
+    """Time every kernel kind, or only the names in `kinds` (from KERNELS)."""
+    if kinds is None:
+        _check(lib().pivot_profile_begin(), "pivot_profile_begin")
+        return
+    mask = 0
+    for name in kinds:
+        mask |= 1 << KERNELS.index(name)
+    _check(lib().pivot_profile_begin_kinds(mask), "pivot_profile_begin_kinds")
 
 
 def pivot_profile_end() -> dict:

@@ -37,6 +37,7 @@ struct ProfRecord {
 };
 std::mutex g_prof_mu;
 bool g_prof_on = false;
+uint32_t g_prof_mask = 0;  // kernel kinds bracketed while a profile runs
 std::vector<ProfRecord> g_prof_recs;
 std::vector<hipEvent_t> g_prof_pool;
 
@@ -54,7 +55,7 @@ hipEvent_t prof_event() {
 // Run one launcher; with profiling on, bracket it with events on `stream`.
 template <class F>
 hipError_t timed(int kind, hipStream_t stream, F launch) {
-  if (!g_prof_on) return launch();
+  if (!g_prof_on || !((g_prof_mask >> kind) & 1u)) return launch();
   std::lock_guard<std::mutex> lk(g_prof_mu);
   ProfRecord r{kind, prof_event(), prof_event()};
   if (!r.start || !r.stop) return hipErrorOutOfMemory;
@@ -320,7 +321,7 @@ pivot_status make_plan(const pivot_args* a, const pivot_layout* l, int mode, int
     off = align_up(off + ng * kH * sizeof(float));
     if (mode == PIVOT_REFINE) {
       p.off_rsc = off;
-      off = align_up(off + ng * (size_t)g * p.width * sizeof(float));
+      off = align_up(off + ng * (size_t)g * p.width * score_eb(p.dtype));
       p.off_cand = off;
       if (!ext_cand) off = align_up(off + ng * (size_t)p.width * sizeof(int32_t));
     }
@@ -673,7 +674,7 @@ pivot_status group_index(const pivot_args* a, const pivot_layout* l, const pivot
                                          p.qlin ? reinterpret_cast<const float*>(ws + p.off_qlsc) + qoff * kLinLevels
                                                 : nullptr,
                                          p.g, kb.k, kb.ks, kb.map, st, p.proxy_lo, p.n_groups, cb, width, p.W, wslot,
-                                         p.topk, reinterpret_cast<float*>(ws + p.off_rsc) + goff * p.g * width,
+                                         p.topk, ws + p.off_rsc + goff * p.g * width * score_eb(p.dtype),
                                          a->out_idx + qoff * p.topk, stream);
                   }),
                   "refine kernel");
@@ -851,13 +852,19 @@ pivot_status pivot_encode_e4m3(const float* x, uint8_t* out, int64_t n, void* st
   return hip_check(launch_encode_e4m3(x, out, n, (hipStream_t)stream), "encode kernel");
 }
 
-pivot_status pivot_profile_begin(void) {
+pivot_status pivot_profile_begin_kinds(uint32_t kinds) {
   std::lock_guard<std::mutex> lk(g_prof_mu);
   if (g_prof_on) return fail(PIVOT_ERR_INVALID_ARG, "a profile is already running");
+  if (kinds == 0 || (kinds >> PIVOT_KERNEL_KINDS) != 0)
+    return fail(PIVOT_ERR_INVALID_ARG, "kernel kind mask 0x%x outside 1 .. 0x%x", kinds,
+                (1u << PIVOT_KERNEL_KINDS) - 1);
   g_prof_recs.clear();
+  g_prof_mask = kinds;
   g_prof_on = true;
   return PIVOT_OK;
 }
+
+pivot_status pivot_profile_begin(void) { return pivot_profile_begin_kinds((1u << PIVOT_KERNEL_KINDS) - 1); }
 
 pivot_status pivot_profile_end(pivot_profile* out) {
   std::lock_guard<std::mutex> lk(g_prof_mu);

@@ -8,13 +8,17 @@
 // fragments.  The candidate positions are staged in LDS, so each lane reads
 // its position there and gathers 32 bytes of that key (and, for fp8, its
 // scale) three fragments ahead of its use.  Scores go to a
-// [group, member, |C|] fp32 buffer (it stays in the last-level cache for the
-// select that follows).
+// [group, member, |C|] buffer (it stays in the last-level cache for the
+// select that follows): bf16 (round to nearest even) for fp8 inputs, like the
+// full-prefix score rows, fp32 for bf16 inputs.
 //
 // topk_short_kernel: one workgroup per (group, member) row of |C| <= 8192
 // scores; each thread keeps its share of (key, position) pairs in registers
-// (read four at a time with 16-byte loads) and the bucket select (else
-// block_select()) takes the top-k, ties broken by lower position.
+// (read four at a time: 16-byte position loads, 16- or 8-byte score loads)
+// and the bucket select (else block_select()) takes the top-k, ties broken by
+// lower position.  The g member rows of a group run as consecutive
+// workgroups of one XCD, so the group's candidate positions are read from
+// HBM once and then from that XCD's L2.
 //
 // App. B local window: window_kernel writes the union of the members' windows
 // into the candidate row after the proxy's slots.  A candidate row then has
@@ -31,13 +35,14 @@ namespace pivot {
 
 constexpr int kMaxCand = 8192;
 
-template <int DT, int R>
+template <int DT, int R, bool OB16>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void rescore_kernel(
     const uint8_t* __restrict__ q, const float* __restrict__ q_scale, const float* __restrict__ w,
     const uint8_t* __restrict__ lin, const float* __restrict__ lin_scale, int g,
     const uint8_t* __restrict__ k, const float* __restrict__ k_scale, KeyMap km, SeqTable st, int j0,
-    const int32_t* __restrict__ cand, int c, int all_slots, int parts, float* __restrict__ rsc) {
+    const int32_t* __restrict__ cand, int c, int all_slots, int parts, void* __restrict__ rsc) {
   using Tile = RowTile<DT, R>;
+  constexpr uint32_t SE = OB16 ? 2 : 4;  // bytes per stored score
   constexpr int EB = Tile::EB;
   __shared__ int32_t spos[kMaxCand];
   // members [R blk, R blk + R); candidate fragments of slice `part`
@@ -107,9 +112,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void r
   // scores leave through a buffer resource over the block's R member rows;
   // lanes with nothing to store give an offset past its end (dropped), so
   // every lane issues the same memory operations and the waits stay exact
-  const __amdgpu_buffer_rsrc_t orr =
-      buffer_rsrc(rsc + (grp * g + R * blk) * (int64_t)c, (uint32_t)(R * c * 4));
-  const uint32_t my_off = (uint32_t)(qr * c + cbeg) * 4u;
+  const __amdgpu_buffer_rsrc_t orr = buffer_rsrc(static_cast<uint8_t*>(rsc) + (grp * g + R * blk) * (int64_t)c * SE,
+                                                 (uint32_t)(R * c) * SE);
+  const uint32_t my_off = (uint32_t)(qr * c + cbeg) * SE;
   const int nfrag = fend - fbeg;
   constexpr int S = 4;  // fragment stride between the waves
   auto pos_of = [&](int f) { return max(spos[min(16 * f + lr, ncs - 1)], 0); };  // empty slots: key 0
@@ -120,8 +125,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void r
   };
   auto emit = [&](float acc, float ks, int f) {
     const int slot = 16 * f + lr;
-    const uint32_t off = (writer && slot < ncs) ? my_off + 4u * (uint32_t)slot : 0xFFFFFFFFu;
-    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc * ks), orr, off, 0, 0);
+    const uint32_t off = (writer && slot < ncs) ? my_off + SE * (uint32_t)slot : 0xFFFFFFFFu;
+    if constexpr (OB16)
+      __builtin_amdgcn_raw_buffer_store_b16(bf16_rne(acc * ks), orr, off, 0, 0);
+    else
+      __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc * ks), orr, off, 0, 0);
   };
   auto scale_of = [&](int p) { return DT == kFp8 ? ksb[p] : 1.0f; };
   auto fetch_at = [&](KeyFrag<DT>& kf, float& sc, int p) {
@@ -175,15 +183,33 @@ struct SlotRule {
   int32_t wslot;
 };
 
-template <int V>
-__global__ __launch_bounds__(256) void topk_short_kernel(const float* __restrict__ rsc,
+// Workgroup x of a sequence's g * n row selects -> (group, member): in each
+// full chunk of 8 g workgroups, group 8 c + x % 8 takes workgroups x, x + 8,
+// .., x + 8 (g - 1) of the chunk, which the round-robin dispatch places on one
+// XCD one after another; the partial last chunk is taken in plain order.
+__device__ __forceinline__ void member_of(int x, int g, int n, int& j, int& member) {
+  const int chunk = 8 * g, full = (g * n) / chunk * chunk;
+  if (x < full) {
+    const int r = x % chunk;
+    j = (x / chunk) * 8 + r % 8;
+    member = r / 8;
+  } else {
+    j = x / g;
+    member = x % g;
+  }
+}
+
+template <int V, class E>
+__global__ __launch_bounds__(256) void topk_short_kernel(const E* __restrict__ rsc,
                                                          const int32_t* __restrict__ cand, int g, SeqTable st,
-                                                         int j0, int c, SlotRule rule, int m,
+                                                         int j0, int nj, int c, SlotRule rule, int m,
                                                          int32_t* __restrict__ out_idx) {
   __shared__ SelectShared sel;
   __shared__ uint32_t hist[4 * 256];  // bucket_select's histogram, then its list
   __shared__ int32_t lcount, nvalid_sh;
-  const int j = j0 + blockIdx.x, b = blockIdx.y, member = blockIdx.z;
+  int jl, member;
+  member_of((int)blockIdx.x, g, nj, jl, member);
+  const int j = j0 + jl, b = blockIdx.y;
   if (b >= st.n || j >= seq_groups(st, b, g) || j < st.first_proxy[b]) return;
   const int gs = min(g, st.n_rows[b] - j * g);
   if (member >= gs) return;
@@ -193,14 +219,15 @@ __global__ __launch_bounds__(256) void topk_short_kernel(const float* __restrict
   const bool win = rule.window > 0;
   const int nc = win ? c : (int)min((int64_t)c, t0 + 1);
   const int64_t grp = (int64_t)st.grp0[b] + j;
-  const float* srow = rsc + (grp * g + member) * (int64_t)c;
+  const E* srow = rsc + (grp * g + member) * (int64_t)c;
   const int32_t* crow = cand + grp * c;
   int32_t* orow = out_idx + ((int64_t)st.row0[b] + (int64_t)j * g + member) * m;
 
   RegSource<V> src;
   int mine = 0;
   // quads of scores and positions with 16-byte loads when the rows allow it
-  const bool vec = (c & 3) == 0 && ((reinterpret_cast<uintptr_t>(srow) | reinterpret_cast<uintptr_t>(crow)) & 15u) == 0;
+  const bool vec = (c & 3) == 0 && (reinterpret_cast<uintptr_t>(srow) & (4 * sizeof(E) - 1)) == 0 &&
+                   (reinterpret_cast<uintptr_t>(crow) & 15u) == 0;
 #pragma unroll
   for (int q4 = 0; q4 < V / 4; ++q4) {
     const int e0 = 4 * (tid + 256 * q4);
@@ -208,16 +235,25 @@ __global__ __launch_bounds__(256) void topk_short_kernel(const float* __restrict
     int32_t pv[4] = {-1, -1, -1, -1};
     if (vec) {
       if (e0 < nc) {  // c is a multiple of 4: the quad lies inside the row
-        const float4 a = *reinterpret_cast<const float4*>(srow + e0);
+        if constexpr (sizeof(E) == 4) {
+          const float4 a = *reinterpret_cast<const float4*>(srow + e0);
+          kv[0] = a.x; kv[1] = a.y; kv[2] = a.z; kv[3] = a.w;
+        } else {
+          const uint2 a = *reinterpret_cast<const uint2*>(srow + e0);
+          kv[0] = __uint_as_float(a.x << 16); kv[1] = __uint_as_float(a.x & 0xFFFF0000u);
+          kv[2] = __uint_as_float(a.y << 16); kv[3] = __uint_as_float(a.y & 0xFFFF0000u);
+        }
         const int4 q = *reinterpret_cast<const int4*>(crow + e0);
-        kv[0] = a.x; kv[1] = a.y; kv[2] = a.z; kv[3] = a.w;
         pv[0] = q.x; pv[1] = q.y; pv[2] = q.z; pv[3] = q.w;
       }
     } else {
 #pragma unroll
       for (int u = 0; u < 4; ++u)
         if (e0 + u < nc) {
-          kv[u] = srow[e0 + u];
+          if constexpr (sizeof(E) == 4)
+            kv[u] = srow[e0 + u];
+          else
+            kv[u] = __uint_as_float((uint32_t)srow[e0 + u] << 16);
           pv[u] = crow[e0 + u];
         }
     }
@@ -309,10 +345,32 @@ hipError_t launch_window(int32_t* cand, int g, const SeqTable& st, int j0, int j
   return hipGetLastError();
 }
 
+// Member selects of groups [j0, j1): one workgroup per (group, member) row,
+// x = the sequence's g (j1 - j0) rows in member_of() order.
+template <class E>
+hipError_t launch_short(const E* rescore, const int32_t* cand, int g, const SeqTable& st, int j0, int j1, int c,
+                        SlotRule rule, int m, int32_t* out_idx, hipStream_t stream) {
+  const int nj = j1 - j0;
+  const dim3 sgrid((unsigned)(nj * g), (unsigned)st.n);
+  if (c <= 1024)
+    hipLaunchKernelGGL((topk_short_kernel<4, E>), sgrid, dim3(256), 0, stream, rescore, cand, g, st, j0, nj, c, rule,
+                       m, out_idx);
+  else if (c <= 4096)
+    hipLaunchKernelGGL((topk_short_kernel<16, E>), sgrid, dim3(256), 0, stream, rescore, cand, g, st, j0, nj, c,
+                       rule, m, out_idx);
+  else if (c <= 5120)  // c = 4096 plus a window union
+    hipLaunchKernelGGL((topk_short_kernel<20, E>), sgrid, dim3(256), 0, stream, rescore, cand, g, st, j0, nj, c,
+                       rule, m, out_idx);
+  else
+    hipLaunchKernelGGL((topk_short_kernel<32, E>), sgrid, dim3(256), 0, stream, rescore, cand, g, st, j0, nj, c,
+                       rule, m, out_idx);
+  return hipGetLastError();
+}
+
 hipError_t launch_refine(int dtype, const void* q, const float* q_scale, const float* w, const uint8_t* lin,
                          const float* lin_scale, int g, const void* k, const float* k_scale, const KeyMap& km,
                          const SeqTable& st, int j0, int j1, const int32_t* cand, int c, int W, int wslot, int m,
-                         float* rescore, int32_t* out_idx, hipStream_t stream) {
+                         void* rescore, int32_t* out_idx, hipStream_t stream) {
   if (j1 <= j0 || st.n <= 0) return hipSuccess;
   if (c > kMaxCand) return hipErrorInvalidValue;
   const SlotRule rule{W, wslot};
@@ -326,33 +384,22 @@ hipError_t launch_refine(int dtype, const void* q, const float* q_scale, const f
   const int parts = (int)std::max<int64_t>(1, std::min<int64_t>(std::max(1, nfrag / 24), (512 + wgs - 1) / wgs));
   const dim3 grid((unsigned)(j1 - j0), (unsigned)st.n, (unsigned)(((g + R - 1) / R) * parts));
   if (dtype == kFp8 && R == 4)
-    hipLaunchKernelGGL((rescore_kernel<kFp8, 4>), grid, dim3(256), 0, stream, (const uint8_t*)q, q_scale, w, lin,
-                       lin_scale, g, (const uint8_t*)k, k_scale, km, st, j0, cand, c,
+    hipLaunchKernelGGL((rescore_kernel<kFp8, 4, true>), grid, dim3(256), 0, stream, (const uint8_t*)q, q_scale, w,
+                       lin, lin_scale, g, (const uint8_t*)k, k_scale, km, st, j0, cand, c,
                        all_slots, parts, rescore);
   else if (dtype == kFp8)
-    hipLaunchKernelGGL((rescore_kernel<kFp8, 2>), grid, dim3(256), 0, stream, (const uint8_t*)q, q_scale, w, lin,
-                       lin_scale, g, (const uint8_t*)k, k_scale, km, st, j0, cand, c,
+    hipLaunchKernelGGL((rescore_kernel<kFp8, 2, true>), grid, dim3(256), 0, stream, (const uint8_t*)q, q_scale, w,
+                       lin, lin_scale, g, (const uint8_t*)k, k_scale, km, st, j0, cand, c,
                        all_slots, parts, rescore);
   else
-    hipLaunchKernelGGL((rescore_kernel<kBf16, 2>), grid, dim3(256), 0, stream, (const uint8_t*)q, q_scale, w, lin,
-                       lin_scale, g, (const uint8_t*)k, nullptr, km, st, j0, cand, c,
+    hipLaunchKernelGGL((rescore_kernel<kBf16, 2, false>), grid, dim3(256), 0, stream, (const uint8_t*)q, q_scale, w,
+                       lin, lin_scale, g, (const uint8_t*)k, nullptr, km, st, j0, cand, c,
                        all_slots, parts, rescore);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  dim3 sgrid((unsigned)(j1 - j0), (unsigned)st.n, (unsigned)g);
-  if (c <= 1024)
-    hipLaunchKernelGGL(topk_short_kernel<4>, sgrid, dim3(256), 0, stream, rescore, cand, g, st, j0, c,
-                       rule, m, out_idx);
-  else if (c <= 4096)
-    hipLaunchKernelGGL(topk_short_kernel<16>, sgrid, dim3(256), 0, stream, rescore, cand, g, st, j0,
-                       c, rule, m, out_idx);
-  else if (c <= 5120)  // c = 4096 plus a window union
-    hipLaunchKernelGGL(topk_short_kernel<20>, sgrid, dim3(256), 0, stream, rescore, cand, g, st, j0,
-                       c, rule, m, out_idx);
-  else
-    hipLaunchKernelGGL(topk_short_kernel<32>, sgrid, dim3(256), 0, stream, rescore, cand, g, st, j0,
-                       c, rule, m, out_idx);
-  return hipGetLastError();
+  if (dtype == kFp8) return launch_short(static_cast<const bf16_t*>(rescore), cand, g, st, j0, j1, c, rule, m, out_idx,
+                                         stream);
+  return launch_short(static_cast<const float*>(rescore), cand, g, st, j0, j1, c, rule, m, out_idx, stream);
 }
 
 }  // namespace pivot

@@ -163,7 +163,7 @@ def test_cand_width_and_window_workspace():
     per_q = pv.pivot_group_workspace_size(a, opts(db=16, window=5, kind=pv.PIVOT_WINDOW_PER_QUERY))
     ng, width = 25, 24
     # the candidate rows and the members' re-scores grow from c to c + W + g - 1 slots
-    assert per_q - base == (up(ng * width * 4) + up(ng * 4 * width * 4)) - (up(ng * 16 * 4) + up(ng * 4 * 16 * 4))
+    assert per_q - base == (up(ng * width * 4) + up(ng * 4 * width * 2)) - (up(ng * 16 * 4) + up(ng * 4 * 16 * 2))
     assert pv.pivot_group_workspace_size(a, opts(db=16, window=5)) == base
     assert pv.pivot_group_workspace_size(a, opts(window=3, kind=pv.PIVOT_WINDOW_PER_QUERY)) == 0  # invalid
 
@@ -229,7 +229,7 @@ def test_layout_workspace_sizes():
                                            ctypes.byref(opts(db=16)))
     ng = 5
     proxies = up(ng * 64 * 128) + up(ng * 4) + up(ng * 64 * 4)
-    cand = up(ng * 16 * 4) + up(ng * 4 * 16 * 4)
+    cand = up(ng * 16 * 4) + up(ng * 4 * 16 * 2)
     assert ragged == lin(17) + lin(ng) + proxies + cand + 2 * 3 * 960 * 2
 
 
@@ -274,7 +274,7 @@ def test_workspace_size_closed_form():
     # members need the linear term (Refine re-scores them), and so do proxies
     ng = 25
     proxies = up(ng * 64 * 128) + up(ng * 4) + up(ng * 64 * 4)
-    cand = up(ng * 16 * 4) + up(ng * 4 * 16 * 4)   # candidate sets + members' re-scores
+    cand = up(ng * 16 * 4) + up(ng * 4 * 16 * 2)   # candidate sets + members' re-scores
     assert pv.pivot_workspace_size(a, pv.PIVOT_REFINE, 4, 16) == \
         lin(100) + lin(ng) + proxies + cand + ng * ld(1000) * 2
     # Reuse: no candidate buffer, no member rows to re-score
@@ -316,3 +316,15 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(pv, "_lib", None)
     with pytest.raises(RuntimeError, match="HIP library missing"):
         pv.lib()
+
+
+def test_profile_kind_mask():
+    """pivot_profile_begin_kinds: empty or out-of-range masks are rejected, a
+    valid one starts a profile that ends with no launches counted."""
+    L = pv.lib()
+    assert L.pivot_profile_begin_kinds(0) == pv.PIVOT_ERR_INVALID_ARG
+    assert L.pivot_profile_begin_kinds(1 << len(pv.KERNELS)) == pv.PIVOT_ERR_INVALID_ARG
+    pv.pivot_profile_begin(["score", "select"])
+    assert L.pivot_profile_begin() == pv.PIVOT_ERR_INVALID_ARG     # one profile at a time
+    prof = pv.pivot_profile_end()
+    assert all(n == 0 for n, _ in prof.values())

@@ -111,9 +111,9 @@ def test_guardrail_threshold(long_fp8, dense_below):
 def test_group_of_one_equals_dense(long_fp8):
     """App. A identity on the GPU: g = 1 Reuse and Refine give the dense sets.
     Reuse ranks the same stored score rows as the dense path, so its sets are
-    identical; Refine ranks its own fp32 re-scores while fp8 dense rows are
-    stored in bf16, so near-ties at the boundary may swap, within the fp8
-    tolerance on the oracle's scores."""
+    identical; Refine ranks its own re-scores (another kernel, another
+    summation order before the bf16 rounding), so near-ties at the boundary
+    may swap, within the fp8 tolerance on the oracle's scores."""
     x = long_fp8
     p0, n_q = 3000, 64
     d, _, (q, qs, w, n_k) = run_gpu(x, "dense", p0, n_q, 100)
