@@ -582,35 +582,48 @@ pivot_status group_index(const pivot_args* a, const pivot_layout* l, const pivot
                                          : nullptr;
   const float* qs = p.dtype == PIVOT_DT_FP8_E4M3 ? a->q_scale : nullptr;
 
+  // fp8 linear terms (mfma_tile.h): the proxy kernel writes those of the
+  // proxies, and for Refine those of the members it reads, unless some
+  // sequence of a batch also has dense rows (then every query row is done by
+  // the linear-term kernel, which needs a contiguous range)
+  uint8_t* plin = p.plin ? ws + p.off_plin : nullptr;
+  float* plsc = p.plin ? reinterpret_cast<float*>(ws + p.off_plsc) : nullptr;
+  uint8_t* qlin = p.qlin ? ws + p.off_qlin : nullptr;
+  float* qlsc = p.qlin ? reinterpret_cast<float*>(ws + p.off_qlsc) : nullptr;
+  const bool member_lin = p.plin && p.qlin && mode == PIVOT_REFINE && (p.B == 1 || p.dense_hi == 0);
   if (p.any_proxy)
     for (int b0 = 0; b0 < p.B; b0 += kMaxSeq) {  // Eq. 4 proxies (or the first / last member)
       const int nb = std::min(kMaxSeq, p.B - b0);
       SeqTable st = table_for(p, b0, nb);
       const size_t qoff = (size_t)p.row0[b0];
       const size_t poff = (size_t)p.grp0[b0];
+      LinOut lo;
+      if (p.plin) {
+        lo.plin = plin + poff * kLinBytes;
+        lo.plsc = plsc + poff * kLinLevels;
+      }
+      if (member_lin) {
+        lo.qlin = qlin + qoff * kLinBytes;
+        lo.qlsc = qlsc + qoff * kLinLevels;
+      }
       s = hip_check(timed(PIVOT_KERNEL_PROXY, stream, [&] {
                       return launch_proxy(p.dtype, (const uint8_t*)a->q + qoff * p.row_bytes,
                                           qs ? qs + qoff : nullptr, a->w + qoff * kH, p.g, st, p.proxy_lo,
                                           p.n_groups, false, p.agg, (uint8_t*)pq + poff * p.row_bytes, psc + poff,
-                                          pw + poff * kH, stream);
+                                          pw + poff * kH, stream, lo);
                     }),
                     "proxy kernel");
       if (s != PIVOT_OK) return s;
     }
 
-  // the fp8 linear terms of the query rows (dense rows, Refine members) and of
-  // the proxies, in one launch
-  uint8_t* plin = p.plin ? ws + p.off_plin : nullptr;
-  float* plsc = p.plin ? reinterpret_cast<float*>(ws + p.off_plsc) : nullptr;
-  {
-    LinRows qset, pset;
-    if (p.qlin)
-      qset = LinRows{(const uint8_t*)a->q, a->q_scale, a->w, 0, query_lin_rows(p), ws + p.off_qlin,
-                     reinterpret_cast<float*>(ws + p.off_qlsc)};
-    if (p.plin)
-      pset = LinRows{(const uint8_t*)pq, psc, pw, p.B == 1 ? p.proxy_lo : 0, p.groups_total, plin, plsc};
-    if (p.qlin || p.plin) {
-      s = hip_check(timed(PIVOT_KERNEL_LIN, stream, [&] { return launch_lin(qset, pset, stream); }),
+  // the remaining query rows' linear terms: the dense rows, or every row
+  if (p.qlin) {
+    const int64_t rows = member_lin ? (p.B == 1 ? p.dense_hi : 0) : query_lin_rows(p);
+    if (rows > 0) {
+      s = hip_check(timed(PIVOT_KERNEL_LIN, stream, [&] {
+                      return launch_lin(LinRows{(const uint8_t*)a->q, a->q_scale, a->w, 0, rows, qlin, qlsc},
+                                        LinRows{}, stream);
+                    }),
                     "linear-term kernel");
       if (s != PIVOT_OK) return s;
     }

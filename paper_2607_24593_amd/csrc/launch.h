@@ -25,8 +25,18 @@ struct OutDesc {
 // Proxy rows (Eq. 4) of groups [j0, j1) of each sequence (query rows and
 // proxies placed as SeqTable says).  all_groups ignores first_proxy.
 // agg: PIVOT_AGG_MEAN (Eq. 4), or PIVOT_AGG_FIRST / LAST (that member's row).
+// Optional fp8 outputs of the proxy kernel: the linear terms (lin_kernel's
+// layout) of each proxy (plin / plsc, indexed like pq) and of each member row
+// of the groups it handles (qlin / qlsc, indexed like q); NULL: not written.
+struct LinOut {
+  uint8_t* plin = nullptr;
+  float* plsc = nullptr;
+  uint8_t* qlin = nullptr;
+  float* qlsc = nullptr;
+};
 hipError_t launch_proxy(int dtype, const void* q, const float* q_scale, const float* w, int g, const SeqTable& st,
-                        int j0, int j1, bool all_groups, int agg, void* pq, float* psc, float* pw, hipStream_t stream);
+                        int j0, int j1, bool all_groups, int agg, void* pq, float* psc, float* pw, hipStream_t stream,
+                        const LinOut& lo = LinOut{});
 
 // The fp8 epilogue's linear term (mfma_tile.h) for flat rows [r0, r1) of an
 // fp8 row array: lin [rows, 4 * 128] codes, lin_scale [rows, 4].  The two-set

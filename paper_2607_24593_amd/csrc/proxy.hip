@@ -8,7 +8,9 @@
 //   fp8 : mean of (qscale_t * q8_t); scale = amax / 448; codes = RNE(mean / scale)
 //   bf16: mean of q_t; RNE to bf16
 // A group of one is copied unchanged, and so is the chosen member for the
-// first / last aggregation (Sec. 5.4).
+// first / last aggregation (Sec. 5.4).  For fp8 the kernel can also write the
+// score epilogue's linear terms (lin_row) of the proxy and of the members,
+// which saves a pass over the member rows.
 #include "launch.h"
 #include "mfma_tile.h"
 #include "pivot.h"
@@ -32,13 +34,71 @@ __device__ __forceinline__ float decode_e4m3(uint32_t word, int byte) {
   }
 }
 
+// The linear part of the fp8 epilogue (mfma_tile.h) for one row, by one wave:
+// u = sum_j (w_j * qscale / 2) * q8_j, a 128-vector, stored as four fp8
+// levels: level l holds codes c_l = RNE((u - sum_{l'<l} sigma_l' c_l') /
+// sigma_l) with sigma_l = max|residual| / 448, so the remaining error shrinks
+// ~16x per level.  Lane l reads the 16-byte slices (dims 16 (l / 8) ..) of
+// heads l % 8, l % 8 + 8, ..: eight loads per lane, all in flight at once;
+// the eight partial sums of a dim are added across lanes (xor 1, 2, 4) in a
+// fixed order, and lane l then keeps dims 2l and 2l+1 to quantise.  qr and wr
+// may point to global memory or LDS.  Every operation is explicit (no
+// contraction), so each caller gets the same bits.
+__device__ __forceinline__ void lin_row(const uint8_t* qr, const float* wr, float qscale, uint8_t* out,
+                                        float* out_scale, int lane) {
+#pragma clang fp contract(off)
+  const float half_scale = qscale * 0.5f;
+  const int hs = lane & 7, db = lane >> 3;
+  uint4 v[8];
+  float wh[8];
+#pragma unroll
+  for (int it = 0; it < 8; ++it) {
+    const int h = 8 * it + hs;
+    v[it] = *reinterpret_cast<const uint4*>(qr + h * kD + 16 * db);
+    wh[it] = wr[h];
+  }
+  float u[16];
+#pragma unroll
+  for (int e = 0; e < 16; ++e) u[e] = 0.f;
+#pragma unroll
+  for (int it = 0; it < 8; ++it) {
+    const float x = wh[it] * half_scale;
+    const uint32_t words[4] = {v[it].x, v[it].y, v[it].z, v[it].w};
+#pragma unroll
+    for (int e = 0; e < 16; ++e) u[e] = fmaf(x, decode_e4m3(words[e >> 2], e & 3), u[e]);
+  }
+#pragma unroll
+  for (int e = 0; e < 16; ++e) {
+    u[e] = u[e] + __shfl_xor(u[e], 1);
+    u[e] = u[e] + __shfl_xor(u[e], 2);
+    u[e] = u[e] + __shfl_xor(u[e], 4);
+  }
+  // dims 2 lane, 2 lane + 1 = elements 2 hs, 2 hs + 1 of this lane's block
+  float u0 = u[0], u1 = u[1];
+#pragma unroll
+  for (int e = 1; e < 8; ++e) {
+    u0 = hs == e ? u[2 * e] : u0;
+    u1 = hs == e ? u[2 * e + 1] : u1;
+  }
+#pragma unroll
+  for (int l = 0; l < kLinLevels; ++l) {
+    const float amax = wave_max(fmaxf(fabsf(u0), fabsf(u1)));
+    const float sigma = amax > 0.f ? amax / 448.0f : 1.0f;
+    const int word = __builtin_amdgcn_cvt_pk_fp8_f32(u0 / sigma, u1 / sigma, 0, false);
+    *reinterpret_cast<uint16_t*>(out + l * kD + 2 * lane) = (uint16_t)word;
+    u0 = u0 - sigma * __builtin_amdgcn_cvt_f32_fp8(word, 0);
+    u1 = u1 - sigma * __builtin_amdgcn_cvt_f32_fp8(word, 1);
+    if (lane == 0) out_scale[l] = sigma;
+  }
+}
+
 template <int DT>
 __global__ __launch_bounds__(256) void proxy_kernel(const uint8_t* __restrict__ q,
                                                     const float* __restrict__ q_scale,
                                                     const float* __restrict__ w, int g, SeqTable st, int j0,
                                                     int all_groups, int agg,
                                                     uint8_t* __restrict__ pq, float* __restrict__ psc,
-                                                    float* __restrict__ pw) {
+                                                    float* __restrict__ pw, LinOut lo) {
 #pragma clang fp contract(off)
   constexpr int EB = DT == kFp8 ? 1 : 2;
   constexpr int ROW_BYTES = kH * kD * EB;
@@ -60,6 +120,16 @@ __global__ __launch_bounds__(256) void proxy_kernel(const uint8_t* __restrict__ 
     for (int v = 0; v < PER * EB / 16; ++v) dst[v] = src[v];
     if (tid == 0) psc[pr] = (DT == kFp8) ? q_scale[rc] : 1.0f;
     if (tid < kH) pw[pr * kH + tid] = w[rc * kH + tid];
+    if constexpr (DT == kFp8) {
+      const int wave = tid >> 6, lane = tid & 63;
+      if (lo.plin && wave == (gs & 3))  // the proxy's linear term: that of row rc
+        lin_row(q + rc * ROW_BYTES, w + rc * kH, q_scale[rc], lo.plin + pr * kLinBytes, lo.plsc + pr * kLinLevels,
+                lane);
+      if (lo.qlin)
+        for (int r = wave; r < gs; r += 4)
+          lin_row(q + (r0 + r) * ROW_BYTES, w + (r0 + r) * kH, q_scale[r0 + r], lo.qlin + (r0 + r) * kLinBytes,
+                  lo.qlsc + (r0 + r) * kLinLevels, lane);
+    }
     return;
   }
 
@@ -138,6 +208,25 @@ __global__ __launch_bounds__(256) void proxy_kernel(const uint8_t* __restrict__ 
     dst[0] = uint4{out[0], out[1], out[2], out[3]};
     dst[1] = uint4{out[4], out[5], out[6], out[7]};
     if (tid == 0) psc[pr] = sigma;
+    // the linear terms: the proxy's from its codes and gates staged in LDS,
+    // the members' (Refine re-scores them) from their rows, which this
+    // workgroup has just read
+    __shared__ uint4 prow[ROW_BYTES / 16];
+    __shared__ float pws[kH];
+    if (lo.plin) {
+      prow[2 * tid] = uint4{out[0], out[1], out[2], out[3]};
+      prow[2 * tid + 1] = uint4{out[4], out[5], out[6], out[7]};
+      if (tid < kH) pws[tid] = wsum / count;
+      __syncthreads();
+    }
+    const int wave = tid >> 6, lane = tid & 63;
+    if (lo.plin && wave == (gs & 3))
+      lin_row(reinterpret_cast<const uint8_t*>(prow), pws, sigma, lo.plin + pr * kLinBytes,
+              lo.plsc + pr * kLinLevels, lane);
+    if (lo.qlin)
+      for (int r = wave; r < gs; r += 4)
+        lin_row(q + (r0 + r) * ROW_BYTES, w + (r0 + r) * kH, q_scale[r0 + r], lo.qlin + (r0 + r) * kLinBytes,
+                lo.qlsc + (r0 + r) * kLinLevels, lane);
   } else {
     uint32_t out[16];
 #pragma unroll
@@ -150,15 +239,17 @@ __global__ __launch_bounds__(256) void proxy_kernel(const uint8_t* __restrict__ 
 }
 
 hipError_t launch_proxy(int dtype, const void* q, const float* q_scale, const float* w, int g, const SeqTable& st,
-                        int j0, int j1, bool all_groups, int agg, void* pq, float* psc, float* pw, hipStream_t stream) {
+                        int j0, int j1, bool all_groups, int agg, void* pq, float* psc, float* pw, hipStream_t stream,
+                        const LinOut& lo) {
+  if (dtype != kFp8 && (lo.plin || lo.qlin)) return hipErrorInvalidValue;  // linear terms are fp8 only
   if (j1 <= j0 || st.n <= 0) return hipSuccess;
   dim3 grid((unsigned)(j1 - j0), (unsigned)st.n);
   if (dtype == kFp8)
     hipLaunchKernelGGL(proxy_kernel<kFp8>, grid, dim3(256), 0, stream, (const uint8_t*)q, q_scale, w, g, st, j0,
-                       (int)all_groups, agg, (uint8_t*)pq, psc, pw);
+                       (int)all_groups, agg, (uint8_t*)pq, psc, pw, lo);
   else
     hipLaunchKernelGGL(proxy_kernel<kBf16>, grid, dim3(256), 0, stream, (const uint8_t*)q, q_scale, w, g, st, j0,
-                       (int)all_groups, agg, (uint8_t*)pq, psc, pw);
+                       (int)all_groups, agg, (uint8_t*)pq, psc, pw, LinOut{});
   return hipGetLastError();
 }
 
@@ -186,39 +277,14 @@ hipError_t launch_encode_e4m3(const float* x, uint8_t* out, int64_t n, hipStream
 
 namespace pivot {
 
-// The linear part of the fp8 epilogue (mfma_tile.h): for each row,
-// u = sum_j (w_j * qscale / 2) * q8_j, a 128-vector, stored as four fp8 levels:
-// level l holds codes c_l = RNE((u - sum_{l'<l} sigma_l' c_l') / sigma_l) with
-// sigma_l = max|residual| / 448, so the remaining error shrinks ~16x per level.
-// One wave per row; lane l owns dims 2l and 2l+1.
+// Linear terms (lin_row) of flat row ranges, one wave per row.
 __global__ __launch_bounds__(256) void lin_kernel(LinRows set0, LinRows set1, int64_t blocks0) {
   const bool first = blockIdx.x < blocks0;
   const LinRows rs = first ? set0 : set1;
-  const int lane = threadIdx.x & 63;
   const int64_t row = rs.r0 + ((int64_t)blockIdx.x - (first ? 0 : blocks0)) * 4 + (threadIdx.x >> 6);
   if (row >= rs.r1) return;
-  const uint8_t* qr = rs.q + row * (int64_t)(kH * kD);
-  const float* wr = rs.w + row * kH;
-  const float half_scale = rs.q_scale[row] * 0.5f;
-  float u0 = 0.f, u1 = 0.f;
-#pragma unroll 16
-  for (int h = 0; h < kH; ++h) {
-    const float wh = wr[h] * half_scale;
-    const uint32_t pair = *reinterpret_cast<const uint16_t*>(qr + h * kD + 2 * lane);
-    u0 = fmaf(wh, __builtin_amdgcn_cvt_f32_fp8((int)pair, 0), u0);
-    u1 = fmaf(wh, __builtin_amdgcn_cvt_f32_fp8((int)pair, 1), u1);
-  }
-  uint8_t* out = rs.lin + row * (int64_t)kLinBytes;
-#pragma unroll
-  for (int l = 0; l < kLinLevels; ++l) {
-    const float amax = wave_max(fmaxf(fabsf(u0), fabsf(u1)));
-    const float sigma = amax > 0.f ? amax / 448.0f : 1.0f;
-    const int word = __builtin_amdgcn_cvt_pk_fp8_f32(u0 / sigma, u1 / sigma, 0, false);
-    *reinterpret_cast<uint16_t*>(out + l * kD + 2 * lane) = (uint16_t)word;
-    u0 -= sigma * __builtin_amdgcn_cvt_f32_fp8(word, 0);
-    u1 -= sigma * __builtin_amdgcn_cvt_f32_fp8(word, 1);
-    if (lane == 0) rs.lin_scale[row * kLinLevels + l] = sigma;
-  }
+  lin_row(rs.q + row * (int64_t)(kH * kD), rs.w + row * kH, rs.q_scale[row], rs.lin + row * (int64_t)kLinBytes,
+          rs.lin_scale + row * kLinLevels, threadIdx.x & 63);
 }
 
 hipError_t launch_lin(const LinRows& set0, const LinRows& set1, hipStream_t stream) {
