@@ -161,7 +161,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void r
 }
 
 // (key, position) pairs held in registers: entry 4 q + u is element
-// 4 (tid + 256 q) + u of the row (loaded four at a time).
+// 4 (tid + T q) + u of the row (loaded four at a time; T threads).
 template <int V>
 struct RegSource {
   static_assert(V % 4 == 0, "quads of elements");
@@ -199,8 +199,8 @@ __device__ __forceinline__ void member_of(int x, int g, int n, int& j, int& memb
   }
 }
 
-template <int V, class E>
-__global__ __launch_bounds__(256) void topk_short_kernel(const E* __restrict__ rsc,
+template <int V, class E, int T>
+__global__ __launch_bounds__(T) void topk_short_kernel(const E* __restrict__ rsc,
                                                          const int32_t* __restrict__ cand, int g, SeqTable st,
                                                          int j0, int nj, int c, SlotRule rule, int m,
                                                          int32_t* __restrict__ out_idx) {
@@ -230,7 +230,7 @@ __global__ __launch_bounds__(256) void topk_short_kernel(const E* __restrict__ r
                    (reinterpret_cast<uintptr_t>(crow) & 15u) == 0;
 #pragma unroll
   for (int q4 = 0; q4 < V / 4; ++q4) {
-    const int e0 = 4 * (tid + 256 * q4);
+    const int e0 = 4 * (tid + T * q4);
     float kv[4] = {0.f, 0.f, 0.f, 0.f};
     int32_t pv[4] = {-1, -1, -1, -1};
     if (vec) {
@@ -271,7 +271,7 @@ __global__ __launch_bounds__(256) void topk_short_kernel(const E* __restrict__ r
   }
   if (!win) {
     if (nc <= m) {  // every candidate is selected
-      for (int p = tid; p < m; p += 256) orow[p] = p < nc ? crow[p] : -1;
+      for (int p = tid; p < m; p += T) orow[p] = p < nc ? crow[p] : -1;
       return;
     }
   } else {
@@ -287,7 +287,7 @@ __global__ __launch_bounds__(256) void topk_short_kernel(const E* __restrict__ r
 #pragma unroll
       for (int v = 0; v < V; ++v)
         wave_append(src.pos[v] >= 0, &sel.emitted, [&](int slot) { orow[slot] = src.pos[v]; });
-      for (int p = nvalid + tid; p < m; p += 256) orow[p] = -1;
+      for (int p = nvalid + tid; p < m; p += T) orow[p] = -1;
       return;
     }
     __syncthreads();  // sel.emitted is cleared again below
@@ -295,13 +295,13 @@ __global__ __launch_bounds__(256) void topk_short_kernel(const E* __restrict__ r
   if (tid == 0) sel.emitted = 0;
   __syncthreads();
   auto put = [&](int slot, int32_t p) { orow[slot] = p; };
-  if (!bucket_select<256, 1024>(src, (uint32_t)m, hist, hist, reinterpret_cast<int32_t*>(hist + kBucketList), &lcount,
+  if (!bucket_select<T, 1024>(src, (uint32_t)m, hist, hist, reinterpret_cast<int32_t*>(hist + kBucketList), &lcount,
                                 sel, put)) {
     // block_select() takes its source by reference; handing it a copy keeps
     // `src` itself in registers on the bucket path (a referenced array of 32
     // pairs would otherwise live in scratch memory)
     const RegSource<V> fb = src;
-    block_select<256, true>(fb, (uint32_t)m, sel, put);
+    block_select<T, true>(fb, (uint32_t)m, sel, put);
   }
 }
 
@@ -346,24 +346,31 @@ hipError_t launch_window(int32_t* cand, int g, const SeqTable& st, int j0, int j
 }
 
 // Member selects of groups [j0, j1): one workgroup per (group, member) row,
-// x = the sequence's g (j1 - j0) rows in member_of() order.
+// x = the sequence's g (j1 - j0) rows in member_of() order; 256 threads, or
+// 1024 when the launch has too few rows to fill the GPU (decode), so each
+// row's select runs on more threads.
 template <class E>
 hipError_t launch_short(const E* rescore, const int32_t* cand, int g, const SeqTable& st, int j0, int j1, int c,
                         SlotRule rule, int m, int32_t* out_idx, hipStream_t stream) {
   const int nj = j1 - j0;
   const dim3 sgrid((unsigned)(nj * g), (unsigned)st.n);
+  const bool few = (int64_t)nj * g * st.n < 256;
+#define PIVOT_SHORT(V, T)                                                                                         \
+  hipLaunchKernelGGL((topk_short_kernel<V, E, T>), sgrid, dim3(T), 0, stream, rescore, cand, g, st, j0, nj, c, rule, \
+                     m, out_idx)
   if (c <= 1024)
-    hipLaunchKernelGGL((topk_short_kernel<4, E>), sgrid, dim3(256), 0, stream, rescore, cand, g, st, j0, nj, c, rule,
-                       m, out_idx);
+    PIVOT_SHORT(4, 256);
+  else if (few && c <= 4096)
+    PIVOT_SHORT(4, 1024);
+  else if (few)
+    PIVOT_SHORT(8, 1024);
   else if (c <= 4096)
-    hipLaunchKernelGGL((topk_short_kernel<16, E>), sgrid, dim3(256), 0, stream, rescore, cand, g, st, j0, nj, c,
-                       rule, m, out_idx);
+    PIVOT_SHORT(16, 256);
   else if (c <= 5120)  // c = 4096 plus a window union
-    hipLaunchKernelGGL((topk_short_kernel<20, E>), sgrid, dim3(256), 0, stream, rescore, cand, g, st, j0, nj, c,
-                       rule, m, out_idx);
+    PIVOT_SHORT(20, 256);
   else
-    hipLaunchKernelGGL((topk_short_kernel<32, E>), sgrid, dim3(256), 0, stream, rescore, cand, g, st, j0, nj, c,
-                       rule, m, out_idx);
+    PIVOT_SHORT(32, 256);
+#undef PIVOT_SHORT
   return hipGetLastError();
 }
 
