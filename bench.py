@@ -52,6 +52,9 @@ def plan_chunk(p0, n_q, g, c, mode):
     return dense_rows, proxies
 
 
+LIN_ROW_BYTES = 4 * 128 + 4 * 4
+
+
 def units(chunks, mode, g, c, topk, eb_q=1, eb_k=1):
     """Algorithmic work per pass: score pairs, select bytes, refine bytes and flops, proxy bytes.
     The library stores score rows as bf16 for fp8 inputs (2 bytes per score
@@ -71,6 +74,9 @@ def units(chunks, mode, g, c, topk, eb_q=1, eb_k=1):
             fan = gs if mode == "reuse" else 1
             sel_bytes += eb_s * n + 4 * min(m, n) * fan
             prox_bytes += (gs + 1) * row_q if gs > 1 else 0
+            if eb_q == 1:  # fp8: the epilogue's linear terms (4 x 128 codes + 4 scales) of the
+                # proxy, and for Refine of the members, written by the proxy kernel
+                prox_bytes += LIN_ROW_BYTES * (1 + (gs if mode == "refine" else 0))
             if mode == "refine":
                 nc = min(c, n)
                 ref_bytes += nc * (128 * eb_k + 4) + 4 * nc + gs * row_q + 4 * gs * topk
