@@ -2,10 +2,10 @@
 // re-scores the group's candidate set C with its own query and gates (Eq. 8)
 // and keeps its own top-k (Eq. 9).
 //
-// rescore_kernel: one workgroup (4 waves) per group and block of R members
-// (R = 4 for fp8 groups of more than two, else 2), held as the A operands of
-// the MFMA row tile (mfma_tile.h); the waves split C into 16-candidate
-// fragments.  The candidate positions are staged in LDS, so each lane reads
+// rescore_kernel: a block of R members of a group (R = 4 for fp8 groups of
+// more than two, else 2), held as the A operands of the MFMA row tile
+// (mfma_tile.h), scores C in 16-candidate fragments: one wave per block with
+// many groups (prefill), or the 4 waves of a workgroup splitting C (decode).  The candidate positions are staged in LDS, so each lane reads
 // its position there and gathers 32 bytes of that key (and, for fp8, its
 // scale) three fragments ahead of its use.  Scores go to a
 // [group, member, |C|] buffer (it stays in the last-level cache for the
@@ -35,7 +35,14 @@ namespace pivot {
 
 constexpr int kMaxCand = 8192;
 
-template <int DT, int R, bool OB16>
+// WPG: each wave takes its own (group, member block) unit and all of the
+// group's candidates (at most kWpgCand), with no workgroup barrier, so a wave
+// loads its row tile once per |C| candidates rather than per |C| / 4;
+// otherwise the 4 waves of a workgroup share one unit (and slice) and split
+// its fragments.
+constexpr int kWpgCand = 4096;
+
+template <int DT, int R, bool OB16, bool WPG>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void rescore_kernel(
     const uint8_t* __restrict__ q, const float* __restrict__ q_scale, const float* __restrict__ w,
     const uint8_t* __restrict__ lin, const float* __restrict__ lin_scale, int g,
@@ -44,14 +51,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void r
   using Tile = RowTile<DT, R>;
   constexpr uint32_t SE = OB16 ? 2 : 4;  // bytes per stored score
   constexpr int EB = Tile::EB;
-  __shared__ int32_t spos[kMaxCand];
+  __shared__ int32_t spos_all[WPG ? 4 * kWpgCand : kMaxCand];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
   // members [R blk, R blk + R); candidate fragments of slice `part`
-  const int j = j0 + blockIdx.x, b = blockIdx.y, blk = blockIdx.z / parts, part = blockIdx.z % parts;
+  const int nblk = (g + R - 1) / R, unit = 4 * (int)blockIdx.x + wave;
+  const int j = j0 + (WPG ? unit / nblk : (int)blockIdx.x), b = blockIdx.y;
+  const int blk = WPG ? unit % nblk : (int)blockIdx.z / parts, part = WPG ? 0 : (int)blockIdx.z % parts;
   if (b >= st.n || j >= seq_groups(st, b, g) || j < st.first_proxy[b]) return;
   const int gs = min(g, st.n_rows[b] - j * g);
   if (R * blk >= gs) return;
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
+  int32_t* spos = WPG ? spos_all + wave * kWpgCand : spos_all;
+  constexpr int ST = WPG ? 64 : 256;  // threads staging the positions
+  const int sid = WPG ? lane : tid;
   const int64_t t0 = (int64_t)st.q_pos0[b] + (int64_t)j * g;
   // without a window only the first t0 + 1 slots can hold a position
   const int nc = all_slots ? c : (int)min((int64_t)c, t0 + 1);
@@ -73,22 +85,22 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void r
   // issued before the first is used (then, for paged keys, the batch's
   // page-table loads), one or two memory round trips per batch instead of
   // one per element
-  for (int e0 = 0; e0 < ncs; e0 += 8 * 256) {
+  for (int e0 = 0; e0 < ncs; e0 += 8 * ST) {
     constexpr int SB = 8;
     int32_t pv[SB];
 #pragma unroll
     for (int k = 0; k < SB; ++k) {
-      const int e = e0 + tid + 256 * k;
+      const int e = e0 + sid + ST * k;
       pv[k] = e < ncs ? crow[cbeg + e] : 0;
     }
     if (km.pages) {
 #pragma unroll
       for (int k = 0; k < SB; ++k)
-        if (e0 + tid + 256 * k < ncs) pv[k] = (int32_t)km.row(b, max(pv[k], 0));
+        if (e0 + sid + ST * k < ncs) pv[k] = (int32_t)km.row(b, max(pv[k], 0));
     }
 #pragma unroll
     for (int k = 0; k < SB; ++k) {
-      const int e = e0 + tid + 256 * k;
+      const int e = e0 + sid + ST * k;
       if (e < ncs) spos[e] = pv[k];
     }
   }
@@ -116,7 +128,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void r
                                                  (uint32_t)(R * c) * SE);
   const uint32_t my_off = (uint32_t)(qr * c + cbeg) * SE;
   const int nfrag = fend - fbeg;
-  constexpr int S = 4;  // fragment stride between the waves
+  constexpr int S = WPG ? 1 : 4;  // fragment stride between the waves
   auto pos_of = [&](int f) { return max(spos[min(16 * f + lr, ncs - 1)], 0); };  // empty slots: key 0
   // the same position read from global memory (before the LDS copy is staged)
   auto pos_glob = [&](int f) {
@@ -141,7 +153,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void r
   // fragments past the end repeat the last candidate and are not stored.
   // The first three are requested before the row tile and the barrier, so
   // their loads overlap the tile's.
-  int f = wave;
+  int f = WPG ? 0 : wave;
   KeyFrag<DT> k0, k1, k2;
   float s0, s1, s2;
   fetch_at(k0, s0, pos_glob(f));
@@ -149,7 +161,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void r
   fetch_at(k2, s2, pos_glob(f + 2 * S));
   Tile tile;
   tile.load(rows, wrows, qs, lrows, lsc, lane);
-  __syncthreads();  // candidate positions staged
+  if constexpr (WPG) {  // this wave's own positions: its LDS writes precede its reads
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  } else {
+    __syncthreads();  // candidate positions staged
+  }
   for (; f < nfrag; f += 3 * S) {
     emit(tile.score(k0), s0, f);
     fetch(k0, s0, f + 3 * S);
@@ -389,19 +407,25 @@ hipError_t launch_refine(int dtype, const void* q, const float* q_scale, const f
   const int nfrag = (c + 15) / 16;
   // (at least 6 fragments per wave: the loop runs in steps of 3)
   const int parts = (int)std::max<int64_t>(1, std::min<int64_t>(std::max(1, nfrag / 24), (512 + wgs - 1) / wgs));
-  const dim3 grid((unsigned)(j1 - j0), (unsigned)st.n, (unsigned)(((g + R - 1) / R) * parts));
-  if (dtype == kFp8 && R == 4)
-    hipLaunchKernelGGL((rescore_kernel<kFp8, 4, true>), grid, dim3(256), 0, stream, (const uint8_t*)q, q_scale, w,
-                       lin, lin_scale, g, (const uint8_t*)k, k_scale, km, st, j0, cand, c,
-                       all_slots, parts, rescore);
-  else if (dtype == kFp8)
-    hipLaunchKernelGGL((rescore_kernel<kFp8, 2, true>), grid, dim3(256), 0, stream, (const uint8_t*)q, q_scale, w,
-                       lin, lin_scale, g, (const uint8_t*)k, k_scale, km, st, j0, cand, c,
-                       all_slots, parts, rescore);
-  else
-    hipLaunchKernelGGL((rescore_kernel<kBf16, 2, false>), grid, dim3(256), 0, stream, (const uint8_t*)q, q_scale, w,
-                       lin, lin_scale, g, (const uint8_t*)k, nullptr, km, st, j0, cand, c,
-                       all_slots, parts, rescore);
+  // many groups (prefill): one unit per wave when the candidate rows fit its LDS share
+  const bool wpg = parts == 1 && c <= kWpgCand;
+  const int64_t units = (int64_t)(j1 - j0) * ((g + R - 1) / R);
+  const dim3 grid = wpg ? dim3((unsigned)((units + 3) / 4), (unsigned)st.n, 1u)
+                        : dim3((unsigned)(j1 - j0), (unsigned)st.n, (unsigned)(((g + R - 1) / R) * parts));
+#define PIVOT_RESCORE(DTV, RV, OB, WP, KS)                                                                        \
+  hipLaunchKernelGGL((rescore_kernel<DTV, RV, OB, WP>), grid, dim3(256), 0, stream, (const uint8_t*)q, q_scale, w, \
+                     lin, lin_scale, g, (const uint8_t*)k, KS, km, st, j0, cand, c, all_slots, parts, rescore)
+  if (dtype == kFp8 && R == 4) {
+    if (wpg) PIVOT_RESCORE(kFp8, 4, true, true, k_scale);
+    else PIVOT_RESCORE(kFp8, 4, true, false, k_scale);
+  } else if (dtype == kFp8) {
+    if (wpg) PIVOT_RESCORE(kFp8, 2, true, true, k_scale);
+    else PIVOT_RESCORE(kFp8, 2, true, false, k_scale);
+  } else {
+    if (wpg) PIVOT_RESCORE(kBf16, 2, false, true, nullptr);
+    else PIVOT_RESCORE(kBf16, 2, false, false, nullptr);
+  }
+#undef PIVOT_RESCORE
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (dtype == kFp8) return launch_short(static_cast<const bf16_t*>(rescore), cand, g, st, j0, j1, c, rule, m, out_idx,
