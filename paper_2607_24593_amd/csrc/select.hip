@@ -295,9 +295,9 @@ struct RowDest {
 template <int CAP, int T, bool SAMPLE, class E>
 __global__ __launch_bounds__(T) __attribute__((amdgpu_waves_per_eu(CAP == kSelCapSmall && T == kSelThreads ? 6 : 4)))
 void topk_rows_kernel(const E* __restrict__ scores, int64_t ld, SeqTable st, RowSpace rs, OutDesc od) {
-  // 16-byte row loads in flight per thread (the same count of scores for bf16
-  // rows, whose vectors hold twice as many)
-  constexpr int U = (T == kSelThreads ? 4 : 8) * (int)sizeof(E) / 4;
+  // 16-byte row loads in flight per thread (the same bytes for bf16 rows,
+  // whose vectors hold twice as many scores)
+  constexpr int U = T == kSelThreads ? 4 : 8;
   __shared__ TwoLevelShared<CAP> sh;
   const int nrows = rs.i1 - rs.i0;
   const int b = blockIdx.x / nrows;
@@ -369,7 +369,7 @@ __global__ __launch_bounds__(kSplitThreads) void topk_slice_kernel(const E* __re
                                                                    int32_t* __restrict__ cnt) {
   using SV = ScoreVec<E>;
   constexpr int N = SV::N;
-  constexpr int T = kSplitThreads, U = 8 * (int)sizeof(E) / 4;
+  constexpr int T = kSplitThreads, U = 8;  // 16-byte loads in flight per thread
   __shared__ uint2 lc[kSplitPerMax];
   __shared__ int32_t nc;
   const int nrows = rs.i1 - rs.i0;
