@@ -4,7 +4,8 @@ Only the test suite, the package smoke check and the benchmark's CPU-baseline
 leg may import this package.  It wraps `pivot_oracle.c`, a plain fp64 C
 restatement of the lightning-indexer score (Sec. 3.1 Eq. 1, App. A), TopK, and
 Algorithm 1 of App. E (grouping Eqs. 2-3, proxy Eq. 4, proxy scan Eq. 5,
-Reuse Eq. 6, Refine Eqs. 7-9, short-group guardrail).  The library is built
+Reuse Eq. 6, Refine Eqs. 7-9, short-group guardrail), and its composition with
+IndexCache across layers (Sec. 5.1 "Baselines").  The library is built
 with gcc; nothing here touches the GPU path.
 """
 from __future__ import annotations
@@ -70,6 +71,7 @@ def lib():
                                    I, I, I, I, I, P, I, P, P, P, P, P]
         L.oracle_index_ex.argtypes = [I, I, I, P, P, P, I, I64, P, P, I64,
                                       I, I, I, I, I, I, I, I, P, I, P, P, P, P, P]
+        L.oracle_index_layers.argtypes = [I, I, I, I, P, P, P, P, I, I64, P, P, I64, I, I, I, I, I, P]
         L.oracle_num_threads.restype = I
         _lib = L
     return _lib
@@ -220,3 +222,46 @@ def index(fmt: str, q, q_scale, w, p0: int, k, k_scale, n_k: int, *, mode: int, 
     if want_proxy:
         res.update(pq=pq, psc=psc, pw=pw)
     return res
+
+
+def layer_anchors(n_layers: int, stride: int) -> np.ndarray:
+    """Anchor layers every `stride` layers from layer 0."""
+    return (np.arange(n_layers) % stride == 0).astype(np.uint8)
+
+
+def index_layers(fmt: str, layers, p0: int, n_k: int, *, mode: int, g: int = 1, c: int = 0, topk: int,
+                 dense_below: int | None = None, stride: int | None = None, anchors=None):
+    """PIVOT (or the dense indexer) composed with IndexCache over consecutive
+    layers.  layers: a list of (q [n_q,H,d], q_scale, w, k, k_scale), one per
+    layer (entries of non-anchor layers may be None).  Anchors: `anchors`
+    (one flag per layer) or every `stride`-th layer from 0.  Returns one
+    [n_q, topk] index array per layer."""
+    n_layers = len(layers)
+    anc = layer_anchors(n_layers, stride) if anchors is None else np.asarray(anchors, dtype=np.uint8)
+    if dense_below is None:
+        dense_below = c if mode != DENSE else 0
+    ref = next(L for L in layers if L is not None)
+    n_q, H, d = ref[0].shape
+    keep, qp, sp, wp, kp, ksp, outs = [], [], [], [], [], [], []
+    for L in layers:
+        if L is None:
+            L = (None, None, None, None, None)
+        q, qs, w, k, ks = L
+        arrs = (_c(q, _code_dtype(fmt)), _c(qs, np.float32) if fmt == "fp8" else None, _c(w, np.float32),
+                _c(k, _code_dtype(fmt)), _c(ks, np.float32) if fmt == "fp8" else None)
+        keep.append(arrs)
+        for lst, a in zip((qp, sp, wp, kp, ksp), arrs):
+            lst.append(None if a is None else a.ctypes.data)
+        outs.append(np.full((n_q, topk), -2, dtype=np.int32))
+    P = ctypes.c_void_p
+    arr = lambda xs: (P * n_layers)(*xs)  # noqa: E731
+    anc = np.ascontiguousarray(anc)
+    if anc.shape != (n_layers,):
+        raise ValueError("one anchor flag per layer")
+    rc = lib().oracle_index_layers(FMT[fmt], H, d, n_layers, _p(anc), arr(qp),
+                                   arr(sp) if fmt == "fp8" else None, arr(wp), n_q, int(p0), arr(kp),
+                                   arr(ksp) if fmt == "fp8" else None, int(n_k), mode, g, c, topk,
+                                   dense_below, (P * n_layers)(*[o.ctypes.data for o in outs]))
+    if rc != 0:
+        raise ValueError("oracle_index_layers rejected its arguments")
+    return outs

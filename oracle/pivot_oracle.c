@@ -20,6 +20,9 @@
  *     overall order of the steps:         App. E, Algorithm 1
  *   - local window W (prefill / decode):  App. B
  *   - first / last member as the proxy:   Sec. 5.4 (query aggregation ablation)
+ *   - PIVOT composed with IndexCache
+ *     (index sets shared across layers):  Sec. 5.1 "Baselines", the +IC rows
+ *                                         of Table 1; Sec. 2 (layer axis)
  *
  * Readings where the paper is silent (the same list is kept with the design
  * notes of the repository):
@@ -45,7 +48,11 @@
  *         positions already in the pool emptied; W >= g;
  *       member t re-scores the slots it may use: position <= t, and, for a
  *         union slot of the per-query kind, position >= t - W + 1;
- *   - first / last aggregation: the proxy is that member's row, unchanged.
+ *   - first / last aggregation: the proxy is that member's row, unchanged;
+ *   - IndexCache composition (the paper gives no layer pattern): layers are
+ *     taken in order; an anchor layer runs the indexer on its own inputs, and
+ *     every other layer takes the index sets of the nearest anchor before it,
+ *     unchanged; the first layer is an anchor.
  *
  * Floating point: every score is accumulated in double.  For fp8 inputs the
  * inner products are exact in double (codes are multiples of 2^-9 with
@@ -442,6 +449,36 @@ int oracle_index(int fmt, int H, int d,
                  void* out_pq, float* out_psc, float* out_pw) {
     return oracle_index_ex(fmt, H, d, q, q_scale, w, n_q, p0, k, k_scale, n_k, mode, g, c, m, dense_below,
                            0, 0, OR_AGG_MEAN, sel, n_sel, out_idx, out_cand, out_pq, out_psc, out_pw);
+}
+
+/*
+ * PIVOT composed with IndexCache (Sec. 5.1 "Baselines"; the +IC rows of
+ * Table 1).  IndexCache shares index sets along the layer axis (Sec. 2): one
+ * layer's T_t serves nearby layers.  Layer l (0 <= l < n_layers) is an anchor
+ * when anchor[l] != 0: it runs the indexer (mode as oracle_index: dense, or
+ * Algorithm 1 with Reuse / Refine) on its own q[l], q_scale[l], w[l], k[l],
+ * k_scale[l].  Any other layer's out_idx[l] [n_q, m] receives the sets of
+ * the nearest anchor before it; its inputs are not read.  Layer 0 must be an
+ * anchor.  Returns 0, or 1 for rejected arguments.
+ */
+int oracle_index_layers(int fmt, int H, int d, int n_layers, const uint8_t* anchor,
+                        const void* const* q, const float* const* q_scale, const float* const* w,
+                        int n_q, int64_t p0, const void* const* k, const float* const* k_scale, int64_t n_k,
+                        int mode, int g, int c, int m, int dense_below, int32_t* const* out_idx) {
+    if (n_layers < 1 || !anchor || !anchor[0] || n_q < 0 || m < 1) return 1;
+    int src = 0;                                  /* the layer whose sets are shared */
+    for (int l = 0; l < n_layers; ++l) {
+        if (anchor[l]) {
+            int rc = oracle_index(fmt, H, d, q[l], q_scale ? q_scale[l] : NULL, w[l], n_q, p0, k[l],
+                                  k_scale ? k_scale[l] : NULL, n_k, mode, g, c, m, dense_below, NULL, 0,
+                                  out_idx[l], NULL, NULL, NULL, NULL);
+            if (rc != 0) return rc;
+            src = l;
+        } else {
+            memcpy(out_idx[l], out_idx[src], sizeof(int32_t) * (size_t)n_q * (size_t)m);
+        }
+    }
+    return 0;
 }
 
 int oracle_num_threads(void) {

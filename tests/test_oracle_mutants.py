@@ -47,6 +47,9 @@ MUTANTS = {
     "window reserves W slots, not W + g - 1 (App. B)": ("const int wg = W > 0 ? W + g - 1 : 0;", "const int wg = W;"),
     "first and last member swapped": ("int t = (agg == OR_AGG_LAST) ? gs - 1 : 0;", "int t = (agg == OR_AGG_FIRST) ? gs - 1 : 0;"),
     "proxy scale from amax/240": ("amax / 448.0f", "amax / 240.0f"),
+    "IndexCache followers reuse layer 0 (Sec. 5.1)": ("            src = l;", "            src = 0;"),
+    "IndexCache followers index themselves (Sec. 5.1)": ("        if (anchor[l]) {", "        if (1) {"),
+    "IndexCache only the first layer indexes (Sec. 5.1)": ("        if (anchor[l]) {", "        if (l == 0) {"),
 }
 
 

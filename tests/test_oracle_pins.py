@@ -548,3 +548,94 @@ def test_decode_window_is_per_query(fmt):
     got = sorted(v for v in res["idx"][g - 1].tolist() if v >= 0)
     assert got == exp
     assert not set(got) & set(range(p0 - W + 1, t - W + 1))
+
+
+# ------------------------------------------------ IndexCache composition (Sec. 5.1, Table 1 +IC)
+def _layers(fmt, n_layers, L=64):
+    """Distinct inputs per layer (the same positions, another seed each)."""
+    xs = [small(fmt, L=L, seed=300 + l) for l in range(n_layers)]
+    return xs, [(x.q, x.q_scale, x.w, x.k, x.k_scale) for x in xs]
+
+
+def _own(x, mode, **kw):
+    """The layer's own indexer result (Algorithm 1, pinned above)."""
+    return run(x, mode, **kw)["idx"]
+
+
+IC_KW = dict(g=4, c=12, topk=6)
+
+
+@pytest.mark.parametrize("fmt", ["bf16", "fp8"])
+@pytest.mark.parametrize("mode", [oracle.REUSE, oracle.REFINE, oracle.DENSE])
+def test_indexcache_stride_one_is_per_layer(fmt, mode):
+    """Every layer an anchor: each layer is indexed on its own inputs."""
+    xs, layers = _layers(fmt, 3)
+    kw = dict(IC_KW) if mode != oracle.DENSE else dict(topk=6)
+    got = oracle.index_layers(fmt, layers, 0, 64, mode=mode, stride=1, **kw)
+    for l, x in enumerate(xs):
+        assert np.array_equal(got[l], _own(x, mode, **kw)), l
+
+
+@pytest.mark.parametrize("fmt", ["bf16", "fp8"])
+@pytest.mark.parametrize("stride", [2, 3])
+def test_indexcache_followers_take_the_anchor_before_them(fmt, stride):
+    """Stride r: layers l .. l+r-1 of a block all hold the anchor l's sets,
+    which differ from what the followers' own inputs would give."""
+    n_layers = 5
+    xs, layers = _layers(fmt, n_layers)
+    own = [_own(x, oracle.REFINE, **IC_KW) for x in xs]
+    got = oracle.index_layers(fmt, layers, 0, 64, mode=oracle.REFINE, stride=stride, **IC_KW)
+    differs = 0
+    for l in range(n_layers):
+        a = l - l % stride
+        assert np.array_equal(got[l], own[a]), (l, a)
+        differs += not np.array_equal(own[l], own[a])
+    assert differs >= 1  # the inputs tell anchors and followers apart
+
+
+@pytest.mark.parametrize("fmt", ["bf16", "fp8"])
+def test_indexcache_explicit_anchor_pattern(fmt):
+    """An irregular pattern: each follower takes the NEAREST anchor before it
+    (not the first layer, not the next anchor)."""
+    anchors = [1, 0, 0, 1, 0, 1]
+    xs, layers = _layers(fmt, len(anchors))
+    own = [_own(x, oracle.REUSE, **IC_KW) for x in xs]
+    for l, a in enumerate(anchors):  # the followers' inputs are never read
+        if not a:
+            layers[l] = None
+    got = oracle.index_layers(fmt, layers, 0, 64, mode=oracle.REUSE, anchors=anchors, **IC_KW)
+    src = [0, 0, 0, 3, 3, 5]
+    for l in range(len(anchors)):
+        assert np.array_equal(got[l], own[src[l]]), l
+    assert not np.array_equal(own[4], own[3]) or not np.array_equal(own[4], own[0])
+
+
+def test_indexcache_stride_past_the_layers_and_identical_layers():
+    """A stride beyond the layer count shares layer 0's sets everywhere; layers
+    with identical inputs give the per-layer result for any stride."""
+    xs, layers = _layers("fp8", 4)
+    own0 = _own(xs[0], oracle.REFINE, **IC_KW)
+    for out in oracle.index_layers("fp8", layers, 0, 64, mode=oracle.REFINE, stride=10, **IC_KW):
+        assert np.array_equal(out, own0)
+    same = [layers[0]] * 4
+    for stride in (1, 2, 3):
+        for out in oracle.index_layers("fp8", same, 0, 64, mode=oracle.REFINE, stride=stride, **IC_KW):
+            assert np.array_equal(out, own0)
+
+
+def test_indexcache_chunk_offset_and_guardrail():
+    """A later chunk (queries 32 .. 63 against keys 0 .. 63) with the guardrail
+    at c: the layer function passes the call's positions through."""
+    xs, _ = _layers("fp8", 3)
+    p0 = 32
+    layers = [(x.q[p0:], x.q_scale[p0:], x.w[p0:], x.k, x.k_scale) for x in xs]
+    got = oracle.index_layers("fp8", layers, p0, 64, mode=oracle.REFINE, stride=2, g=4, c=40, topk=6)
+    for l in range(3):
+        a = l - l % 2
+        assert np.array_equal(got[l], _own(xs[a], oracle.REFINE, p0=p0, g=4, c=40, topk=6)), l
+
+
+def test_indexcache_first_layer_must_be_an_anchor():
+    _, layers = _layers("bf16", 2)
+    with pytest.raises(ValueError):
+        oracle.index_layers("bf16", layers, 0, 64, mode=oracle.REUSE, anchors=[0, 1], **IC_KW)
