@@ -236,6 +236,37 @@ pivot_status pivot_group_index_layout(const pivot_args* a, const pivot_layout* l
 size_t pivot_workspace_size_layout(const pivot_args* a, const pivot_layout* l, const pivot_group_opts* o);
 
 /*
+ * PIVOT composed with IndexCache (Sec. 5.1 "Baselines"; the +IC rows of
+ * Table 1).  IndexCache works on the layer axis (Sec. 2): one layer's index
+ * sets T_t serve the layers after it; composed with PIVOT, the layers that do
+ * index run PIVOT.
+ *   layers[0 .. n_layers-1]: consecutive indexer layers over the same query
+ *     and key positions.  Each has its own q, q_scale, w, k, k_scale and
+ *     out_idx (layouts as in pivot_args); every other field must equal
+ *     layers[0]'s: dtype, heads, dim, batch, n_q, topk, k_seq_stride, and the
+ *     contents of q_pos0 and n_k.
+ *   Layer l is an anchor when anchors[l] != 0 (anchors: host [n_layers]) or,
+ *     with anchors NULL, when l % stride == 0 (stride >= 1).  Layer 0 must be
+ *     an anchor.
+ *   An anchor layer is indexed as pivot_group_index_opts(&layers[l], o) would
+ *     index it (o NULL: as pivot_dense_index, i.e. IndexCache alone).  Every
+ *     other layer receives in its out_idx the sets of the nearest anchor
+ *     before it; its q, q_scale, w, k and k_scale are not read (they may be
+ *     NULL).
+ *   All work is enqueued on layers[0].stream in layer order and uses
+ *     layers[0].workspace, which needs the bytes of one anchor call,
+ *     pivot_workspace_size_layout(&layers[0], NULL, o); the other layers'
+ *     workspace and stream fields are ignored.  o->out_cand must be NULL.
+ * Every layer is validated before the first launch: a layer that differs from
+ * layer 0, a missing pointer, stride < 1 without anchors, n_layers < 1 or an
+ * unset anchor 0 return PIVOT_ERR_INVALID_ARG; an anchor's own checks return
+ * what its single-layer call would.  A follower costs one copy of the index
+ * sets; a run of followers reads the anchor's sets once.
+ */
+pivot_status pivot_index_layers(const pivot_args* layers, int32_t n_layers, int32_t stride,
+                                const uint8_t* anchors, const pivot_group_opts* o);
+
+/*
  * Stage: proxy rows of Eq. 4 for one sequence's queries q [n_q, H, d] /
  * q_scale [n_q] / w [n_q, H] split into runs of g (last may be shorter).
  * Writes out_q [ceil(n_q/g), H, d] (same format as q), out_scale
@@ -309,7 +340,8 @@ enum {
   PIVOT_KERNEL_REFINE = 3,  /* Refine gather, re-score and select, Eqs. 8-9 */
   PIVOT_KERNEL_FILL = 4,    /* -1 fill of guardrail candidate rows */
   PIVOT_KERNEL_LIN = 5,     /* per-row linear term of the fp8 score epilogue */
-  PIVOT_KERNEL_KINDS = 6
+  PIVOT_KERNEL_COPY = 6,    /* index sets copied to IndexCache follower layers */
+  PIVOT_KERNEL_KINDS = 7
 };
 
 typedef struct {

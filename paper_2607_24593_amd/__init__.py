@@ -30,9 +30,9 @@ EXPORTED = ["pivot_workspace_size", "pivot_dense_index", "pivot_group_index", "p
             "pivot_group_workspace_size", "pivot_group_index_opts", "pivot_dense_index_layout",
             "pivot_group_index_layout", "pivot_workspace_size_layout", "pivot_proxy_rows",
             "pivot_score_rows", "pivot_topk_rows", "pivot_topk_rows_workspace_size", "pivot_topk_rows_ws",
-            "pivot_encode_e4m3", "pivot_profile_begin", "pivot_profile_begin_kinds",
+            "pivot_encode_e4m3", "pivot_profile_begin", "pivot_profile_begin_kinds", "pivot_index_layers",
             "pivot_profile_end", "pivot_status_string", "pivot_last_error", "pivot_version"]
-KERNELS = ["proxy", "score", "select", "refine", "fill", "lin"]
+KERNELS = ["proxy", "score", "select", "refine", "fill", "lin", "copy"]
 
 
 class PivotError(RuntimeError):
@@ -42,7 +42,7 @@ class PivotError(RuntimeError):
 
 
 class pivot_profile(ctypes.Structure):
-    _fields_ = [("launches", ctypes.c_int64 * 6), ("total_ms", ctypes.c_double * 6)]
+    _fields_ = [("launches", ctypes.c_int64 * 7), ("total_ms", ctypes.c_double * 7)]
 
 
 class pivot_args(ctypes.Structure):
@@ -133,6 +133,8 @@ def lib():
         L.pivot_group_index_layout.argtypes = [A, Lo, O]
         L.pivot_workspace_size_layout.restype = ctypes.c_size_t
         L.pivot_workspace_size_layout.argtypes = [A, Lo, O]
+        L.pivot_index_layers.restype = I32
+        L.pivot_index_layers.argtypes = [A, I32, I32, P, O]
         L.pivot_proxy_rows.restype = I32
         L.pivot_proxy_rows.argtypes = [I32, I32, I32, I32, I32, P, P, P, P, P, P, P]
         L.pivot_score_rows.restype = I32
@@ -201,14 +203,31 @@ def _check(status: int, where: str):
 _WS = {}
 
 
-def workspace(nbytes: int, device) -> torch.Tensor:
-    """A cached device buffer of at least nbytes (256-byte aligned by torch)."""
+def _torch_stream(stream, device):
+    """The torch stream object for a call's `stream` argument (None: current)."""
     dev = torch.device(device)
-    key = (dev.type, dev.index)
+    if stream is None:
+        return torch.cuda.current_stream(dev)
+    if isinstance(stream, torch.cuda.Stream):
+        return stream
+    return torch.cuda.ExternalStream(int(stream), device=dev)
+
+
+def workspace(nbytes: int, device, stream=None) -> torch.Tensor:
+    """A cached device buffer of at least nbytes (256-byte aligned by torch) for
+    calls on `stream` (None: the current stream).  There is one buffer per
+    (device, stream): calls on one stream run in order, so they may share it,
+    while calls on two streams would write one buffer concurrently.  The buffer
+    is allocated with that stream current, so torch's caching allocator orders
+    its reuse after the work already queued on the stream when it is replaced."""
+    dev = torch.device(device)
+    s = _torch_stream(stream, dev)
+    key = (dev.type, dev.index, s.cuda_stream)
     buf = _WS.get(key)
     if buf is None or buf.numel() < nbytes:
         _WS.pop(key, None)
-        buf = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=dev)
+        with torch.cuda.stream(s):
+            buf = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=dev)
         _WS[key] = buf
     return buf
 
@@ -251,11 +270,11 @@ def pivot_workspace_size(a: pivot_args, mode: int = PIVOT_DENSE, g: int = 1, c: 
     return int(lib().pivot_workspace_size(ctypes.byref(a), int(mode), int(g), int(c)))
 
 
-def _attach_workspace(a, mode, g, c, ws, device):
+def _attach_workspace(a, mode, g, c, ws, device, stream=None):
     need = pivot_workspace_size(a, mode, g, c)
     if need == 0 and a.n_q > 0:
         return  # invalid shapes: the entry point reports the reason
-    buf = ws if ws is not None else workspace(need, device)
+    buf = ws if ws is not None else workspace(need, device, stream)
     a.workspace = _ptr(buf)
     a.workspace_bytes = buf.numel() * buf.element_size()
     a._ws = buf
@@ -267,7 +286,7 @@ def pivot_dense_index(q, q_scale, w, k, k_scale, q_pos0, n_k, topk, out=None, ws
     shape = (q.shape[0], topk) if squeeze else (q.shape[0], q.shape[1], topk)
     out = torch.empty(shape, dtype=torch.int32, device=q.device) if out is None else out
     a = make_args(q, q_scale, w, k, k_scale, q_pos0, n_k, topk, out, stream=stream)
-    _attach_workspace(a, PIVOT_DENSE, 1, 0, ws, q.device)
+    _attach_workspace(a, PIVOT_DENSE, 1, 0, ws, q.device, stream)
     _check(lib().pivot_dense_index(ctypes.byref(a)), "pivot_dense_index")
     return out
 
@@ -279,7 +298,9 @@ def pivot_group_index(q, q_scale, w, k, k_scale, q_pos0, n_k, topk, mode, g, c, 
     shape = (q.shape[0], topk) if squeeze else (q.shape[0], q.shape[1], topk)
     out = torch.empty(shape, dtype=torch.int32, device=q.device) if out is None else out
     a = make_args(q, q_scale, w, k, k_scale, q_pos0, n_k, topk, out, stream=stream)
-    _attach_workspace(a, mode, g, c, ws, q.device)
+    # sized for this call's guardrail (pivot_workspace_size assumes dense_below = c)
+    o = group_opts(mode, g, c, dense_below)
+    _attach(a, pivot_group_workspace_size(a, o), ws, q.device, stream)
     _check(lib().pivot_group_index(ctypes.byref(a), int(mode), int(g), int(c), int(dense_below),
                                    _ptr(out_cand)), "pivot_group_index")
     return out
@@ -303,14 +324,51 @@ def pivot_group_index_opts(q, q_scale, w, k, k_scale, q_pos0, n_k, topk, mode, g
     out = torch.empty(shape, dtype=torch.int32, device=q.device) if out is None else out
     a = make_args(q, q_scale, w, k, k_scale, q_pos0, n_k, topk, out, stream=stream)
     o = group_opts(mode, g, c, dense_below, window, window_kind, aggregate, out_cand)
-    need = pivot_group_workspace_size(a, o)
-    if need > 0 or a.n_q == 0:
-        buf = ws if ws is not None else workspace(need, q.device)
-        a.workspace = _ptr(buf)
-        a.workspace_bytes = buf.numel() * buf.element_size()
-        a._ws = buf
+    _attach(a, pivot_group_workspace_size(a, o), ws, q.device, stream)
     _check(lib().pivot_group_index_opts(ctypes.byref(a), ctypes.byref(o)), "pivot_group_index_opts")
     return out
+
+
+def pivot_index_layers(layers, q_pos0, n_k, topk, *, stride=1, anchors=None, mode=None, g=1, c=0, dense_below=-1,
+                       window=0, window_kind=PIVOT_WINDOW_SHARED, aggregate=PIVOT_AGG_MEAN, outs=None, ws=None,
+                       stream=None):
+    """PIVOT (mode PIVOT_REUSE / PIVOT_REFINE) or the dense indexer (mode None)
+    composed with IndexCache over consecutive layers.  layers: one (q, q_scale,
+    w, k, k_scale) per layer, shaped as for pivot_dense_index; a non-anchor
+    layer's entry may be None (its inputs are not read).  Anchors: `anchors`
+    (one flag per layer) or every `stride`-th layer from 0.  Returns one int32
+    index tensor per layer (or fills `outs`)."""
+    n_layers = len(layers)
+    ref = layers[0]
+    if ref is None:
+        raise ValueError("layer 0 is an anchor and needs its inputs")
+    q0 = ref[0]
+    squeeze = q0.dim() == 3
+    shape = (q0.shape[0], topk) if squeeze else (q0.shape[0], q0.shape[1], topk)
+    if outs is None:
+        outs = [torch.empty(shape, dtype=torch.int32, device=q0.device) for _ in range(n_layers)]
+    arr = (pivot_args * n_layers)()
+    keep = []
+    for l, L in enumerate(layers):
+        src = ref if L is None else L
+        a = make_args(*src, q_pos0, n_k, topk, outs[l], stream=stream)
+        if L is None:
+            a.q = a.q_scale = a.w = a.k = a.k_scale = None
+        arr[l] = a
+        keep.append(a)
+    o = None if mode is None else group_opts(mode, g, c, dense_below, window, window_kind, aggregate)
+    need = int(lib().pivot_workspace_size_layout(ctypes.byref(arr[0]), None, None if o is None else ctypes.byref(o)))
+    if need > 0:
+        buf = ws if ws is not None else workspace(need, q0.device, stream)
+        arr[0].workspace = _ptr(buf)
+        arr[0].workspace_bytes = buf.numel() * buf.element_size()
+        keep.append(buf)
+    anc = None
+    if anchors is not None:
+        anc = (ctypes.c_uint8 * n_layers)(*[1 if v else 0 for v in anchors])
+    _check(lib().pivot_index_layers(arr, n_layers, int(stride), anc, None if o is None else ctypes.byref(o)),
+           "pivot_index_layers")
+    return outs
 
 
 def make_args_batch(q, q_scale, w, k, k_scale, q_pos0, n_k, topk, out_idx, stream=None):
@@ -344,9 +402,9 @@ def pivot_workspace_size_layout(a: pivot_args, lo: pivot_layout, o=None) -> int:
                                                  None if o is None else ctypes.byref(o)))
 
 
-def _attach(a, need, ws, device):
+def _attach(a, need, ws, device, stream=None):
     if need > 0:
-        buf = ws if ws is not None else workspace(need, device)
+        buf = ws if ws is not None else workspace(need, device, stream)
         a.workspace = _ptr(buf)
         a.workspace_bytes = buf.numel() * buf.element_size()
         a._ws = buf
@@ -358,7 +416,7 @@ def pivot_dense_index_layout(q, q_scale, w, k, k_scale, q_pos0, n_k, topk, layou
     returns int32 [rows, topk]."""
     out = torch.empty((q.shape[0], topk), dtype=torch.int32, device=q.device) if out is None else out
     a = make_args_batch(q, q_scale, w, k, k_scale, q_pos0, n_k, topk, out, stream=stream)
-    _attach(a, pivot_workspace_size_layout(a, layout), ws, q.device)
+    _attach(a, pivot_workspace_size_layout(a, layout), ws, q.device, stream)
     _check(lib().pivot_dense_index_layout(ctypes.byref(a), ctypes.byref(layout)), "pivot_dense_index_layout")
     return out
 
@@ -371,7 +429,7 @@ def pivot_group_index_layout(q, q_scale, w, k, k_scale, q_pos0, n_k, topk, layou
     out = torch.empty((q.shape[0], topk), dtype=torch.int32, device=q.device) if out is None else out
     a = make_args_batch(q, q_scale, w, k, k_scale, q_pos0, n_k, topk, out, stream=stream)
     o = group_opts(mode, g, c, dense_below, window, window_kind, aggregate, out_cand)
-    _attach(a, pivot_workspace_size_layout(a, layout, o), ws, q.device)
+    _attach(a, pivot_workspace_size_layout(a, layout, o), ws, q.device, stream)
     _check(lib().pivot_group_index_layout(ctypes.byref(a), ctypes.byref(layout), ctypes.byref(o)),
            "pivot_group_index_layout")
     return out
@@ -401,7 +459,7 @@ def pivot_score_rows(q, q_scale, w, k, k_scale, lim0, lim_step, ld=None, out=Non
     ld = lim_max + 1 if ld is None else ld
     out = torch.full((n, ld), float("nan"), dtype=torch.float32, device=q.device) if out is None else out
     nbytes = score_rows_workspace(n) if _dtype_code(q) == PIVOT_DT_FP8_E4M3 else 0
-    ws = workspace(nbytes, q.device) if nbytes else None
+    ws = workspace(nbytes, q.device, stream) if nbytes else None
     _check(lib().pivot_score_rows(_dtype_code(q), q.shape[1], q.shape[2], n, _ptr(q), _ptr(q_scale), _ptr(w),
                                   _ptr(k), _ptr(k_scale), int(lim0), int(lim_step), _ptr(out), int(ld), _ptr(ws),
                                   nbytes, _stream(stream)), "pivot_score_rows")
@@ -427,7 +485,7 @@ def pivot_topk_rows_ws(scores, n0, n_step, m, out=None, ws=None, stream=None):
     out = torch.empty((n, m), dtype=torch.int32, device=scores.device) if out is None else out
     need = pivot_topk_rows_workspace_size(n)
     if ws is None and need > 0:
-        ws = workspace(need, scores.device)
+        ws = workspace(need, scores.device, stream)
     nbytes = 0 if ws is None else ws.numel() * ws.element_size()
     _check(lib().pivot_topk_rows_ws(n, _ptr(scores), ld, int(n0), int(n_step), int(m), _ptr(out), _ptr(ws),
                                     nbytes, _stream(stream)), "pivot_topk_rows_ws")

@@ -696,6 +696,87 @@ pivot_status group_index(const pivot_args* a, const pivot_layout* l, const pivot
   return PIVOT_OK;
 }
 
+// PIVOT composed with IndexCache over n_layers layers (Sec. 5.1, the +IC rows
+// of Table 1): anchors are indexed on their own inputs, each run of followers
+// gets the preceding anchor's sets through one fan-out copy.  Everything is
+// validated before the first launch.
+pivot_status index_layers(const pivot_args* L, int n_layers, int stride, const uint8_t* anchors,
+                          const pivot_group_opts* o) {
+  if (!L) return fail(PIVOT_ERR_INVALID_ARG, "layers is NULL");
+  if (n_layers < 1) return fail(PIVOT_ERR_INVALID_ARG, "n_layers must be >= 1");
+  if (!anchors && stride < 1) return fail(PIVOT_ERR_INVALID_ARG, "stride must be >= 1");
+  auto anchor = [&](int l) { return anchors ? anchors[l] != 0 : l % stride == 0; };
+  if (!anchor(0)) return fail(PIVOT_ERR_INVALID_ARG, "layer 0 must be an anchor");
+  if (o && o->out_cand) return fail(PIVOT_ERR_INVALID_ARG, "out_cand must be NULL across layers");
+  const pivot_args& a0 = L[0];
+  std::vector<int32_t> nq0;
+  pivot_status s = check_args(&a0, nullptr, nq0);
+  if (s != PIVOT_OK) return s;
+  const int64_t rows = (int64_t)a0.batch * a0.n_q;
+  for (int l = 1; l < n_layers; ++l) {
+    const pivot_args& a = L[l];
+    if (a.dtype != a0.dtype || a.heads != a0.heads || a.dim != a0.dim || a.batch != a0.batch || a.n_q != a0.n_q ||
+        a.topk != a0.topk || a.k_seq_stride != a0.k_seq_stride)
+      return fail(PIVOT_ERR_INVALID_ARG, "layer %d: shape or parameters differ from layer 0", l);
+    if (!a.q_pos0 || !a.n_k) return fail(PIVOT_ERR_INVALID_ARG, "layer %d: q_pos0 and n_k are required", l);
+    for (int b = 0; b < a0.batch; ++b)
+      if (a.q_pos0[b] != a0.q_pos0[b] || a.n_k[b] != a0.n_k[b])
+        return fail(PIVOT_ERR_INVALID_ARG, "layer %d: positions of sequence %d differ from layer 0", l, b);
+    if (rows > 0 && !a.out_idx) return fail(PIVOT_ERR_INVALID_ARG, "layer %d: out_idx is required", l);
+  }
+  // every anchor as its own call would see it: layer 0's workspace and stream
+  auto as_anchor = [&](int l) {
+    pivot_args a = L[l];
+    a.workspace = a0.workspace;
+    a.workspace_bytes = a0.workspace_bytes;
+    a.stream = a0.stream;
+    return a;
+  };
+  // arguments of every anchor first, then the workspace each one needs
+  for (int pass = 0; pass < 2; ++pass)
+    for (int l = 0; l < n_layers; ++l) {
+      if (!anchor(l)) continue;
+      const pivot_args a = as_anchor(l);
+      Plan p;
+      s = o ? group_plan(&a, nullptr, o, false, p) : make_plan(&a, nullptr, PIVOT_DENSE, 1, 0, 0, false, p);
+      if (s == PIVOT_OK && pass == 1 && p.rows_total > 0) {
+        int64_t score_bytes;
+        s = check_workspace(&a, p, score_bytes);
+      }
+      if (s != PIVOT_OK) {
+        char why[sizeof g_err];
+        snprintf(why, sizeof why, "%s", g_err);
+        return fail(s, "layer %d: %s", l, why);
+      }
+    }
+  if (rows == 0) return PIVOT_OK;
+  hipStream_t stream = (hipStream_t)a0.stream;
+  const int64_t n = rows * a0.topk;
+  int src = 0;
+  for (int l = 0; l < n_layers;) {
+    if (anchor(l)) {
+      const pivot_args a = as_anchor(l);
+      s = o ? group_index(&a, nullptr, o) : dense_index(&a, nullptr);
+      if (s != PIVOT_OK) return s;
+      src = l++;
+      continue;
+    }
+    int e = l;
+    while (e < n_layers && !anchor(e)) ++e;
+    for (int f = l; f < e; f += kMaxCopyDst) {  // one read of the anchor's sets per launch
+      int32_t* dst[kMaxCopyDst];
+      const int nd = std::min(kMaxCopyDst, e - f);
+      for (int u = 0; u < nd; ++u) dst[u] = L[f + u].out_idx;
+      s = hip_check(timed(PIVOT_KERNEL_COPY, stream,
+                          [&] { return launch_copy_fanout(L[src].out_idx, dst, nd, n, stream); }),
+                    "copy kernel");
+      if (s != PIVOT_OK) return s;
+    }
+    l = e;
+  }
+  return PIVOT_OK;
+}
+
 pivot_group_opts plain_opts(int32_t mode, int32_t g, int32_t c, int32_t dense_below, int32_t* out_cand) {
   pivot_group_opts o;
   memset(&o, 0, sizeof o);
@@ -761,6 +842,11 @@ pivot_status pivot_group_index_opts(const pivot_args* a, const pivot_group_opts*
 
 pivot_status pivot_group_index_layout(const pivot_args* a, const pivot_layout* l, const pivot_group_opts* o) {
   return group_index(a, l, o);
+}
+
+pivot_status pivot_index_layers(const pivot_args* layers, int32_t n_layers, int32_t stride, const uint8_t* anchors,
+                                const pivot_group_opts* o) {
+  return index_layers(layers, n_layers, stride, anchors, o);
 }
 
 pivot_status pivot_proxy_rows(int32_t dtype, int32_t heads, int32_t dim, int32_t n_q, int32_t g, const void* q,

@@ -98,4 +98,9 @@ hipError_t launch_fill_guardrail(int32_t* base, int width, const SeqTable& st, i
 
 hipError_t launch_encode_e4m3(const float* x, uint8_t* out, int64_t n, hipStream_t stream);
 
+// n int32 of src copied to each of dst[0 .. n_dst) (n_dst <= kMaxCopyDst): one
+// read of src, n_dst writes (IndexCache follower layers).
+constexpr int kMaxCopyDst = 16;
+hipError_t launch_copy_fanout(const int32_t* src, int32_t* const* dst, int n_dst, int64_t n, hipStream_t stream);
+
 }  // namespace pivot

@@ -11,8 +11,16 @@
 // Tile rows are assigned so that every lane group belongs to ONE query row:
 // with G = 4/R lane groups per row, tile j row 4q + i is head
 // 4G j + 4 (q mod G) + i of query row q / G.  Each lane therefore folds its
-// heads into a running fp32 sum with no cross-lane traffic; only G > 1 needs
-// log2(G) shuffles per 16 keys at the end.
+// heads into fp32 sums with no cross-lane traffic; only G > 1 needs log2(G)
+// shuffles per 16 keys at the end.
+//
+// Summation order.  Every tile shape adds a (row, key) pair's 64 heads in the
+// same order, so a score has the same bits whichever R computed it (the
+// dense, proxy and Refine launches pick R by their row counts): four partial
+// sums P_p, p = 0..3, each an FMA chain over heads 16 j + 4 p + i (j, then i,
+// ascending), combined as ((P_0 + P_1) + P_2) + P_3; the fp8 linear term is
+// added last.  With G lane groups per row a lane holds R = 4 / G of the
+// partials (tile j feeds partial j mod R) and shuffles bring in the others.
 //
 // fp8 epilogue.  With x = q8 . k8 and w' = w * qscale,
 //   sum_j w'_j ReLU(x_j) = sum_j (w'_j / 2) |x_j|  +  u . k8,
@@ -20,9 +28,10 @@
 // because ReLU(x) = (x + |x|) / 2.  The first sum costs one FMA per element
 // (|x| is a free source modifier) instead of a max and an FMA.  The second is
 // linear in the key: u is stored as four fp8 levels u ~ sum_l sigma_l c_l
-// (each level quantises the residual of the previous ones, so the error is
-// ~2^-16 of max|u|), and one more MFMA tile per 16 keys computes c_l . k8 for
-// the R rows' levels.  bf16 rows use (w/2)|x| + (w/2)x directly (two FMAs).
+// (each level quantises the residual of the previous ones at a scale 16x
+// finer, sigma_l = sigma_0 16^-l, so the error is below 2^-19 of max|u|),
+// and one more MFMA tile per 16 keys computes c_l . k8 for the R rows'
+// levels, combined as sigma_0 (c_0 + 2^-4 c_1 + 2^-8 c_2 + 2^-12 c_3).  bf16 rows use (w/2)|x| + (w/2)x directly (two FMAs).
 //
 // K split.  Lane l supplies dims 32 (l / 16) .. 32 (l / 16) + 31 of its A row
 // and of its B column.  Any assignment of dims to (lane group, register slot)
@@ -40,6 +49,8 @@ typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 
 constexpr int kLinLevels = 4;
 constexpr int kLinBytes = kLinLevels * kD;  // fp8 codes of the four levels of u, per row
+// sigma_l / sigma_0 of the levels (powers of two, so the products are exact)
+__device__ constexpr float kLinStep[kLinLevels] = {1.0f, 0x1p-4f, 0x1p-8f, 0x1p-12f};
 
 template <int DT>
 struct KeyFrag;
@@ -96,7 +107,7 @@ struct RowTile {
   KeyFrag<DT> a[T];   // A operand, same register format as a key fragment
   float wv[T][4];     // w * qscale / 2 (bf16: qscale = 1)
   KeyFrag<kFp8> al;   // fp8: the four levels of u of the wave's rows
-  float ls[4];        // fp8: level scales of this lane's row (0 in non-owning lane groups)
+  float ls0;          // fp8: sigma_0 of this lane's row (0 in non-owning lane groups)
 
   // rows[r]: the R query rows' codes; wrow[r]: gates; qscale[r]: per-row scale;
   // lin[r] / lscale[r]: the rows' levels of u and their scales (fp8 only).
@@ -121,42 +132,77 @@ struct RowTile {
       for (int i = 0; i < 4; ++i) wv[j][i] = wr[4 * G * j + 4 * (gq % G) + i] * sc;
     if constexpr (DT == kFp8) {
       al.load(lin[gq_a / G] + i_a * kD, kg);
-      const bool own = (gq % G) == 0;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) ls[i] = own ? lscale[qr][i] : 0.f;
+      ls0 = (gq % G) == 0 ? lscale[qr][0] : 0.f;
     }
   }
 
   // Gate-weighted ReLU sum over all heads of row (lane >> 4) / G for key
-  // (lane & 15) of the fragment b; identical in every lane group of the row.
+  // (lane & 15) of the fragment b, in the lanes that store it (lane group
+  // (lane >> 4) % G == 0; the other lane groups of the row lack the fp8
+  // linear term).  The tiles are visited partial by partial (tile R j'' + p
+  // feeds partial p, j'' ascending), so a partial's FMA chain runs without a
+  // break and is folded as soon as it ends: two sums are live.
+  static constexpr int TPR = T / R;  // tiles per partial
+  __device__ __forceinline__ static constexpr int tile_at(int jj) { return R * (jj % TPR) + jj / TPR; }
+
+  // Folds partial p, just finished in `part`, into ((P_0 + P_1) + P_2) + P_3:
+  // `hold` carries the running sum, `tot` receives the whole sum with the
+  // last partial (valid in the lane groups that store the row).
+  __device__ __forceinline__ static void fold(int p, float part, float& hold, float& tot) {
+    if constexpr (R == 4) {  // partials in order, one lane
+      if (p == 0) hold = part;
+      if (p == 1 || p == 2) hold = hold + part;
+      if (p == 3) tot = hold + part;
+    } else if constexpr (R == 2) {  // lane group parity q holds P_q (p = 0) and P_{2+q} (p = 1)
+      const float other = __shfl_xor(part, 16, kWave);
+      if (p == 0) {
+        hold = part + other;  // P_0 + P_1 (additions commute)
+      } else {
+        const bool q0 = ((threadIdx.x >> 4) & 1) == 0;
+        tot = (hold + (q0 ? part : other)) + (q0 ? other : part);
+      }
+    } else {  // lane group q holds P_q; lane group 0 gathers the others
+      const float p1 = __shfl_xor(part, 16, kWave), p2 = __shfl_xor(part, 32, kWave);
+      const float p3 = __shfl_xor(part, 48, kWave);
+      tot = ((part + p1) + p2) + p3;
+    }
+  }
+
   __device__ __forceinline__ float score(const KeyFrag<DT>& b) const {
-    float acc = 0.f;
+    float part = 0.f, hold = 0.f, tot = 0.f;
     if constexpr (DT == kFp8) {
-      // Software pipeline: the MFMA of tile j+2 is issued before the epilogue
-      // of tile j, so the matrix core and the VALU work side by side with
-      // three accumulators live.  The scheduling barriers keep the compiler
-      // from hoisting all MFMAs ahead (which would need 4 (T+1) accumulator
-      // registers and push operands into AGPRs).
+      // Software pipeline: the MFMA of the tile two ahead is issued before the
+      // epilogue of the current one, so the matrix core and the VALU work side
+      // by side with three accumulators live.  The scheduling barriers keep
+      // the compiler from hoisting all MFMAs ahead (which would need 4 (T+1)
+      // accumulator registers and push operands into AGPRs).
       v4f cl = mfma_fp8(al.v, b.v);
-      v4f c0 = mfma_fp8(a[0].v, b.v);
-      v4f c1 = mfma_fp8(a[1].v, b.v);
+      v4f c0 = mfma_fp8(a[tile_at(0)].v, b.v);
+      v4f c1 = mfma_fp8(a[tile_at(1)].v, b.v);
 #pragma unroll
-      for (int j = 2; j <= T + 1; ++j) {
+      for (int jj = 2; jj <= T + 1; ++jj) {
         v4f nxt = c1;
-        if (j < T) nxt = mfma_fp8(a[j].v, b.v);
+        if (jj < T) nxt = mfma_fp8(a[tile_at(jj)].v, b.v);
         __builtin_amdgcn_sched_barrier(0);
+        const int e = jj - 2, j = tile_at(e);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) acc = fmaf(wv[j - 2][i], fabsf(c0[i]), acc);
-        asm volatile("" : "+v"(acc));  // pins this epilogue between the barriers
+        for (int i = 0; i < 4; ++i) part = fmaf(wv[j][i], fabsf(c0[i]), part);
+        asm volatile("" : "+v"(part));  // pins this epilogue between the barriers
         __builtin_amdgcn_sched_barrier(0);
+        if ((e + 1) % TPR == 0) {
+          fold(e / TPR, part, hold, tot);
+          part = 0.f;
+        }
         c0 = c1;
         c1 = nxt;
       }
-#pragma unroll
-      for (int i = 0; i < 4; ++i) acc = fmaf(ls[i], cl[i], acc);
+      // the levels' dot products, finest first scaled in, then sigma_0
+      const float lin = fmaf(cl[3], kLinStep[3], fmaf(cl[2], kLinStep[2], fmaf(cl[1], kLinStep[1], cl[0])));
+      return fmaf(ls0, lin, tot);
     } else {
 #pragma unroll
-      for (int j = 0; j < T; ++j) {
+      for (int jj = 0; jj < T; ++jj) {
+        const int j = tile_at(jj);
         v4f c = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int s = 0; s < 4; ++s)
@@ -164,12 +210,14 @@ struct RowTile {
                                                       __builtin_bit_cast(v8bf, b.v[s]), c, 0, 0, 0);
         // w ReLU(x) = (w/2) |x| + (w/2) x: two FMAs, no max
 #pragma unroll
-        for (int i = 0; i < 4; ++i) acc = fmaf(wv[j][i], c[i], fmaf(wv[j][i], fabsf(c[i]), acc));
+        for (int i = 0; i < 4; ++i) part = fmaf(wv[j][i], c[i], fmaf(wv[j][i], fabsf(c[i]), part));
+        if ((jj + 1) % TPR == 0) {
+          fold(jj / TPR, part, hold, tot);
+          part = 0.f;
+        }
       }
+      return tot;
     }
-    if constexpr (G >= 2) acc += __shfl_xor(acc, 16, kWave);
-    if constexpr (G >= 4) acc += __shfl_xor(acc, 32, kWave);
-    return acc;
   }
 };
 

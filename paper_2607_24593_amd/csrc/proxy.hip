@@ -37,9 +37,13 @@ __device__ __forceinline__ float decode_e4m3(uint32_t word, int byte) {
 // The linear part of the fp8 epilogue (mfma_tile.h) for one row, by one wave:
 // u = sum_j (w_j * qscale / 2) * q8_j, a 128-vector, stored as four fp8
 // levels: level l holds codes c_l = RNE((u - sum_{l'<l} sigma_l' c_l') /
-// sigma_l) with sigma_l = max|residual| / 448, so the remaining error shrinks
-// ~16x per level.  Lane l reads the 16-byte slices (dims 16 (l / 8) ..) of
-// heads l % 8, l % 8 + 8, ..: eight loads per lane, all in flight at once;
+// sigma_l) with sigma_0 = max|u| / 448 and sigma_l = sigma_0 16^-l.  No level
+// saturates (a residual is at most half a code step of the level before,
+// <= 256 sigma_l), and the last residual is at most sigma_0 / 1024, about
+// 2^-19 of max|u|.  The fixed ratio leaves one scale per row for the
+// epilogue; out_scale still receives all four.
+// Lane l reads the 16-byte slices (dims 16 (l / 8) ..) of heads l % 8,
+// l % 8 + 8, ..: eight loads per lane, all in flight at once;
 // the eight partial sums of a dim are added across lanes (xor 1, 2, 4) in a
 // fixed order, and lane l then keeps dims 2l and 2l+1 to quantise.  qr and wr
 // may point to global memory or LDS.  Every operation is explicit (no
@@ -80,10 +84,11 @@ __device__ __forceinline__ void lin_row(const uint8_t* qr, const float* wr, floa
     u0 = hs == e ? u[2 * e] : u0;
     u1 = hs == e ? u[2 * e + 1] : u1;
   }
+  const float amax = wave_max(fmaxf(fabsf(u0), fabsf(u1)));
+  const float sigma0 = amax > 0.f ? amax / 448.0f : 1.0f;
 #pragma unroll
   for (int l = 0; l < kLinLevels; ++l) {
-    const float amax = wave_max(fmaxf(fabsf(u0), fabsf(u1)));
-    const float sigma = amax > 0.f ? amax / 448.0f : 1.0f;
+    const float sigma = sigma0 * kLinStep[l];  // exact: a power of two
     const int word = __builtin_amdgcn_cvt_pk_fp8_f32(u0 / sigma, u1 / sigma, 0, false);
     *reinterpret_cast<uint16_t*>(out + l * kD + 2 * lane) = (uint16_t)word;
     u0 = u0 - sigma * __builtin_amdgcn_cvt_f32_fp8(word, 0);
@@ -98,8 +103,12 @@ __global__ __launch_bounds__(256) void proxy_kernel(const uint8_t* __restrict__ 
                                                     const float* __restrict__ w, int g, SeqTable st, int j0,
                                                     int all_groups, int agg,
                                                     uint8_t* __restrict__ pq, float* __restrict__ psc,
-                                                    float* __restrict__ pw, LinOut lo) {
+                                                    float* __restrict__ pw, LinOut lo, int stage) {
 #pragma clang fp contract(off)
+  // stage (fp8, members' linear terms wanted, g <= MB): the mean pass copies
+  // each member row it loads into dynamic LDS (g x 8 KiB), and the members'
+  // linear terms are computed from there rather than read again from HBM
+  extern __shared__ uint4 mrows[];
   constexpr int EB = DT == kFp8 ? 1 : 2;
   constexpr int ROW_BYTES = kH * kD * EB;
   constexpr int PER = 32;  // elements per thread
@@ -154,6 +163,13 @@ __global__ __launch_bounds__(256) void proxy_kernel(const uint8_t* __restrict__ 
         sq[k] = (DT == kFp8) ? q_scale[row] : 1.0f;
         wv[k] = tid < kH ? w[row * kH + tid] : 0.0f;
       }
+    }
+    if (stage) {  // one batch holds every member (g <= MB)
+#pragma unroll
+      for (int k = 0; k < MB; ++k)
+        if (k < gs)
+#pragma unroll
+          for (int x = 0; x < VPM; ++x) mrows[k * (ROW_BYTES / 16) + VPM * tid + x] = v[k][x];
     }
 #pragma unroll
     for (int k = 0; k < MB; ++k) {
@@ -223,10 +239,11 @@ __global__ __launch_bounds__(256) void proxy_kernel(const uint8_t* __restrict__ 
     if (lo.plin && wave == (gs & 3))
       lin_row(reinterpret_cast<const uint8_t*>(prow), pws, sigma, lo.plin + pr * kLinBytes,
               lo.plsc + pr * kLinLevels, lane);
-    if (lo.qlin)
+    if (lo.qlin)  // the staged rows were written before the amax barrier above
       for (int r = wave; r < gs; r += 4)
-        lin_row(q + (r0 + r) * ROW_BYTES, w + (r0 + r) * kH, q_scale[r0 + r], lo.qlin + (r0 + r) * kLinBytes,
-                lo.qlsc + (r0 + r) * kLinLevels, lane);
+        lin_row(stage ? reinterpret_cast<const uint8_t*>(mrows + r * (ROW_BYTES / 16)) : q + (r0 + r) * ROW_BYTES,
+                w + (r0 + r) * kH, q_scale[r0 + r], lo.qlin + (r0 + r) * kLinBytes, lo.qlsc + (r0 + r) * kLinLevels,
+                lane);
   } else {
     uint32_t out[16];
 #pragma unroll
@@ -244,12 +261,15 @@ hipError_t launch_proxy(int dtype, const void* q, const float* q_scale, const fl
   if (dtype != kFp8 && (lo.plin || lo.qlin)) return hipErrorInvalidValue;  // linear terms are fp8 only
   if (j1 <= j0 || st.n <= 0) return hipSuccess;
   dim3 grid((unsigned)(j1 - j0), (unsigned)st.n);
+  // members staged in LDS for their linear terms when one load batch holds a group
+  const int stage = dtype == kFp8 && lo.qlin && agg == PIVOT_AGG_MEAN && g > 1 && g <= 8;
+  const size_t shmem = stage ? (size_t)g * kH * kD : 0;
   if (dtype == kFp8)
-    hipLaunchKernelGGL(proxy_kernel<kFp8>, grid, dim3(256), 0, stream, (const uint8_t*)q, q_scale, w, g, st, j0,
-                       (int)all_groups, agg, (uint8_t*)pq, psc, pw, lo);
+    hipLaunchKernelGGL(proxy_kernel<kFp8>, grid, dim3(256), shmem, stream, (const uint8_t*)q, q_scale, w, g, st, j0,
+                       (int)all_groups, agg, (uint8_t*)pq, psc, pw, lo, stage);
   else
     hipLaunchKernelGGL(proxy_kernel<kBf16>, grid, dim3(256), 0, stream, (const uint8_t*)q, q_scale, w, g, st, j0,
-                       (int)all_groups, agg, (uint8_t*)pq, psc, pw, LinOut{});
+                       (int)all_groups, agg, (uint8_t*)pq, psc, pw, LinOut{}, 0);
   return hipGetLastError();
 }
 

@@ -35,6 +35,7 @@
 // overflows LDS (e.g. many equal scores) selects directly over the row.
 // A row with no more than m valid entries returns all of them, then -1.
 #include <algorithm>
+#include <cstring>
 
 #include "block_select.h"
 #include "launch.h"
@@ -599,6 +600,50 @@ hipError_t launch_fill_guardrail(int32_t* base, int width, const SeqTable& st, i
   if (j1 <= j0 || st.n <= 0) return hipSuccess;
   hipLaunchKernelGGL(fill_guardrail_kernel, dim3((unsigned)(j1 - j0), (unsigned)st.n), dim3(256), 0, stream, base,
                      width, st, j0, value);
+  return hipGetLastError();
+}
+
+struct CopyDst {
+  int32_t* p[kMaxCopyDst];
+  int32_t n;
+};
+
+// Grid-stride copy of src[0, n) to every destination; vec: every pointer is
+// 16-byte aligned, so the bulk moves as int4.
+__global__ __launch_bounds__(256) void copy_fanout_kernel(const int32_t* __restrict__ src, CopyDst dst, int64_t n,
+                                                          int vec) {
+  const int64_t step = (int64_t)gridDim.x * blockDim.x;
+  const int64_t i0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  int64_t tail = 0;
+  if (vec) {
+    const int64_t n4 = n / 4;
+    const int4* s4 = reinterpret_cast<const int4*>(src);
+    for (int64_t j = i0; j < n4; j += step) {
+      const int4 v = s4[j];
+      for (int d = 0; d < dst.n; ++d) reinterpret_cast<int4*>(dst.p[d])[j] = v;
+    }
+    tail = 4 * n4;
+  }
+  for (int64_t e = tail + i0; e < n; e += step) {
+    const int32_t v = src[e];
+    for (int d = 0; d < dst.n; ++d) dst.p[d][e] = v;
+  }
+}
+
+hipError_t launch_copy_fanout(const int32_t* src, int32_t* const* dst, int n_dst, int64_t n, hipStream_t stream) {
+  if (n <= 0 || n_dst <= 0) return hipSuccess;
+  if (n_dst > kMaxCopyDst) return hipErrorInvalidValue;
+  CopyDst cd;
+  memset(&cd, 0, sizeof cd);
+  cd.n = n_dst;
+  bool vec = (reinterpret_cast<uintptr_t>(src) & 15u) == 0;
+  for (int d = 0; d < n_dst; ++d) {
+    cd.p[d] = dst[d];
+    vec = vec && (reinterpret_cast<uintptr_t>(dst[d]) & 15u) == 0;
+  }
+  const int64_t units = vec ? std::max<int64_t>(n / 4, 1) : n;
+  const int64_t blocks = std::min<int64_t>((units + 255) / 256, 4096);
+  hipLaunchKernelGGL(copy_fanout_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, src, cd, n, (int)vec);
   return hipGetLastError();
 }
 

@@ -328,3 +328,49 @@ def test_profile_kind_mask():
     assert L.pivot_profile_begin() == pv.PIVOT_ERR_INVALID_ARG     # one profile at a time
     prof = pv.pivot_profile_end()
     assert all(n == 0 for n, _ in prof.values())
+
+
+def layers_call(layers, stride=1, anchors=None, o=None):
+    arr = (pv.pivot_args * len(layers))(*layers)
+    anc = None if anchors is None else (ctypes.c_uint8 * len(anchors))(*anchors)
+    return pv.lib().pivot_index_layers(arr, len(layers), stride, anc, None if o is None else ctypes.byref(o))
+
+
+def _mismatch(field, value):
+    b = args(ws_bytes=0)
+    setattr(b, field, value)
+    return [args(ws_bytes=0), b]
+
+
+@pytest.mark.parametrize("make,kw,status", [
+    (lambda: [args()], dict(stride=0), pv.PIVOT_ERR_INVALID_ARG),                   # stride < 1, no anchors
+    (lambda: [args(), args()], dict(anchors=[0, 1]), pv.PIVOT_ERR_INVALID_ARG),     # layer 0 not an anchor
+    (lambda: _mismatch("n_q", 32), {}, pv.PIVOT_ERR_INVALID_ARG),
+    (lambda: _mismatch("topk", 4), {}, pv.PIVOT_ERR_INVALID_ARG),
+    (lambda: _mismatch("dtype", pv.PIVOT_DT_BF16), {}, pv.PIVOT_ERR_INVALID_ARG),
+    (lambda: [args(), args(q_pos0=1, n_k=65)], {}, pv.PIVOT_ERR_INVALID_ARG),       # positions differ
+    (lambda: _mismatch("out_idx", None), dict(stride=2), pv.PIVOT_ERR_INVALID_ARG),  # follower without output
+    (lambda: [args(ws_bytes=0), args(ws_bytes=0)], dict(stride=2), pv.PIVOT_ERR_WORKSPACE),
+    (lambda: [args(ws_bytes=0), args(ws_bytes=0)], dict(stride=1), pv.PIVOT_ERR_WORKSPACE),
+    (lambda: [args(topk=0), args(topk=0)], dict(stride=2), pv.PIVOT_ERR_INVALID_ARG),  # anchor's own check
+])
+def test_index_layers_validation(make, kw, status):
+    """Every layer is checked before a launch; a follower's inputs may be NULL."""
+    assert layers_call(make(), **kw) == status
+    assert pv.last_error() != ""
+
+
+def test_index_layers_follower_inputs_unread_and_opts_checked():
+    L = pv.lib()
+    assert L.pivot_index_layers(None, 1, 1, None, None) == pv.PIVOT_ERR_INVALID_ARG
+    follower = args(ws_bytes=0)
+    follower.q = follower.w = follower.k = follower.q_scale = follower.k_scale = None
+    # validation reaches layer 0's workspace check: the NULL follower inputs are accepted
+    assert layers_call([args(ws_bytes=0), follower], stride=2, o=opts()) == pv.PIVOT_ERR_WORKSPACE
+    # the same NULL inputs on an anchor layer are rejected
+    assert layers_call([args(ws_bytes=0), follower], stride=1, o=opts()) == pv.PIVOT_ERR_INVALID_ARG
+    o = opts()
+    o.out_cand = FAKE
+    assert layers_call([args(), args()], stride=1, o=o) == pv.PIVOT_ERR_INVALID_ARG
+    assert layers_call([args(ws_bytes=0)], stride=1, o=opts(g=0)) == pv.PIVOT_ERR_INVALID_ARG
+

@@ -57,12 +57,17 @@ def test_score_rows_match_oracle(fmt, n_rows, lim0, step):
     ld = lim_max + 1 + 13
     say("score_rows", fmt, n_rows, lim0, step)
     got = host(pv.pivot_score_rows(dev(q), dev(qs), dev(w), dev(x.k), dev(x.k_scale), lim0, step, ld=ld))
+    # bf16: fp32 MFMA sums of exact bf16 products, so every element is within
+    # a few fp32 ulps of the row's largest |score| (1e-5 of it); fp8 adds the
+    # four-level linear term of the epilogue, whose residual is below 2^-16 of
+    # max|u| per level chain, bounded here by 1e-4 of the row's largest |score|
+    tol = 1e-5 if fmt == "bf16" else 1e-4
     for r in range(n_rows):
         lim = lim0 + r * step
         f = oracle.scores(fmt, q[r], 1.0 if qs is None else qs[r], w[r], x.k, x.k_scale, lim)
         scale = np.abs(f).max() + 1e-30
-        err = np.abs(got[r, :lim + 1] - f).max() / scale
-        assert err < 1e-4, (r, err)
+        err = np.abs(got[r, :lim + 1] - f) / scale
+        assert err.max() < tol, (r, int(err.argmax()), float(err.max()))
         assert np.isnan(got[r, lim + 1:]).all(), r   # nothing written past the row's limit
 
 

@@ -8,7 +8,7 @@ import pytest
 import oracle
 import paper_2607_24593_amd as pv
 from gpu_util import dev, host, say
-from parity import RTOL, check_pivot, check_row
+from parity import check_pivot
 from workload.gen import make_decode, make_prefill
 
 pytestmark = pytest.mark.gpu
@@ -109,23 +109,33 @@ def test_guardrail_threshold(long_fp8, dense_below):
 
 
 def test_group_of_one_equals_dense(long_fp8):
-    """App. A identity on the GPU: g = 1 Reuse and Refine give the dense sets.
-    Reuse ranks the same stored score rows as the dense path, so its sets are
-    identical; Refine ranks its own re-scores (another kernel, another
-    summation order before the bf16 rounding), so near-ties at the boundary
-    may swap, within the fp8 tolerance on the oracle's scores."""
+    """App. A identity on the GPU: g = 1 Reuse and Refine give the dense sets
+    exactly.  A group of one is its own proxy; every tile shape adds a score's
+    heads in the same order, so the proxy scan and Refine's re-score produce
+    the dense path's score bits, and the top-k of the top-c is the top-k."""
     x = long_fp8
-    p0, n_q = 3000, 64
-    d, _, (q, qs, w, n_k) = run_gpu(x, "dense", p0, n_q, 100)
-    r, _, _ = run_gpu(x, "reuse", p0, n_q, 100, g=1, c=200, dense_below=0)
-    assert np.array_equal(np.sort(r, 1), np.sort(d, 1)), "reuse"
-    r, _, _ = run_gpu(x, "refine", p0, n_q, 100, g=1, c=200, dense_below=0)
-    for i in range(n_q):
-        t = p0 + i
-        f_of = lambda idx, i=i: oracle.scores_at(x.dtype, q[i], 1.0 if qs is None else qs[i], w[i],
-                                                 x.k[:n_k], x.k_scale[:n_k], idx)
-        check_row(r[i], d[i], f_of, RTOL[x.dtype], lambda idx, t=t: (idx >= 0) & (idx <= t),
-                  f"refine g1 row {i}")
+    for p0, n_q in ((3000, 64), (1024, 2000)):
+        d, _, _ = run_gpu(x, "dense", p0, n_q, 100)
+        r, _, _ = run_gpu(x, "reuse", p0, n_q, 100, g=1, c=200, dense_below=0)
+        assert np.array_equal(np.sort(r, 1), np.sort(d, 1)), ("reuse", p0)
+        r, _, _ = run_gpu(x, "refine", p0, n_q, 100, g=1, c=200, dense_below=0)
+        assert np.array_equal(np.sort(r, 1), np.sort(d, 1)), ("refine", p0)
+
+
+@pytest.mark.parametrize("L", [5000, 20000])
+def test_group_of_one_equals_dense_decode(L):
+    """The same identity at decode shapes (one query per sequence, keys-mode
+    scan with one row per wave, the split select for 20000-key contexts)."""
+    B = 5
+    x = make_decode(B, L, 1, "fp8", seed=48, threads=6)
+    q, qs, w, k, ks = dev(x.q), dev(x.q_scale), dev(x.w), dev(x.k), dev(x.k_scale)
+    pos, nk = [L - 1] * B, [L] * B
+    say("decode g=1 identity", L)
+    d = host(pv.pivot_dense_index(q, qs, w, k, ks, pos, nk, 256))
+    for mode in ("reuse", "refine"):
+        r = host(pv.pivot_group_index(q, qs, w, k, ks, pos, nk, 256, mode=PV_MODE[mode], g=1, c=1024,
+                                      dense_below=0))
+        assert np.array_equal(np.sort(r, -1), np.sort(d, -1)), mode
 
 
 @pytest.mark.parametrize("B,L", [(6, 5000), (5, 20000)])
