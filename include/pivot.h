@@ -267,6 +267,27 @@ pivot_status pivot_index_layers(const pivot_args* layers, int32_t n_layers, int3
                                 const uint8_t* anchors, const pivot_group_opts* o);
 
 /*
+ * pivot_group_index_opts that allocates nothing, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  a->workspace and a->workspace_bytes are
+ * ignored: the call uses a scratch array of PIVOT_NOALLOC_SCRATCH_BYTES that
+ * the library holds on each device it runs on (in its code object, until the
+ * process ends).  Its address on the current device is looked up on the first
+ * call there.  The call itself makes no allocation, frees nothing and
+ * synchronises nothing; results are those of pivot_group_index_opts.
+ *   - A call whose workspace minimum (fixed regions plus one score tile, see
+ *     pivot_group_workspace_size) exceeds the scratch returns
+ *     PIVOT_ERR_WORKSPACE before touching the device (e.g. 32 decode
+ *     sequences of 131072 keys need ~18 MB; a 2048-query prefill chunk with
+ *     g = 4, c = 4096 ~35 MB; an 8192-query chunk does not fit).
+ *   - Calls share the device's scratch and each leaves its contents behind;
+ *     no region needs to start at zero.  Calls that overlap on one device
+ *     (two streams, two threads) race on it: order them on one stream.
+ */
+#define PIVOT_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+pivot_status pivot_group_index_noalloc(const pivot_args* a, const pivot_group_opts* o);
+
+/*
  * Stage: proxy rows of Eq. 4 for one sequence's queries q [n_q, H, d] /
  * q_scale [n_q] / w [n_q, H] split into runs of g (last may be shorter).
  * Writes out_q [ceil(n_q/g), H, d] (same format as q), out_scale

@@ -22,6 +22,7 @@ PIVOT_DT_BF16, PIVOT_DT_FP8_E4M3 = 0, 1
 PIVOT_REUSE, PIVOT_REFINE = 0, 1
 PIVOT_DENSE = -1
 PIVOT_MAX_KEYS = 1 << 27
+PIVOT_NOALLOC_SCRATCH_BYTES = 64 << 20
 PIVOT_WINDOW_SHARED, PIVOT_WINDOW_PER_QUERY = 0, 1
 PIVOT_AGG_MEAN, PIVOT_AGG_FIRST, PIVOT_AGG_LAST = 0, 1, 2
 H, D = 64, 128
@@ -31,6 +32,7 @@ EXPORTED = ["pivot_workspace_size", "pivot_dense_index", "pivot_group_index", "p
             "pivot_group_index_layout", "pivot_workspace_size_layout", "pivot_proxy_rows",
             "pivot_score_rows", "pivot_topk_rows", "pivot_topk_rows_workspace_size", "pivot_topk_rows_ws",
             "pivot_encode_e4m3", "pivot_profile_begin", "pivot_profile_begin_kinds", "pivot_index_layers",
+            "pivot_group_index_noalloc",
             "pivot_profile_end", "pivot_status_string", "pivot_last_error", "pivot_version"]
 KERNELS = ["proxy", "score", "select", "refine", "fill", "lin", "copy"]
 
@@ -133,6 +135,8 @@ def lib():
         L.pivot_group_index_layout.argtypes = [A, Lo, O]
         L.pivot_workspace_size_layout.restype = ctypes.c_size_t
         L.pivot_workspace_size_layout.argtypes = [A, Lo, O]
+        L.pivot_group_index_noalloc.restype = I32
+        L.pivot_group_index_noalloc.argtypes = [A, O]
         L.pivot_index_layers.restype = I32
         L.pivot_index_layers.argtypes = [A, I32, I32, P, O]
         L.pivot_proxy_rows.restype = I32

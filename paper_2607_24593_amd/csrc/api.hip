@@ -13,6 +13,11 @@
 
 using namespace pivot;
 
+// Scratch of pivot_group_index_noalloc: one copy per device in the code
+// object.  Host code uses the device address hipGetSymbolAddress returns
+// (g_scratch_ptr), never this name.
+static __device__ __align__(256) uint8_t scratch[PIVOT_NOALLOC_SCRATCH_BYTES];
+
 namespace {
 
 thread_local char g_err[512] = "";
@@ -777,6 +782,51 @@ pivot_status index_layers(const pivot_args* L, int n_layers, int stride, const u
   return PIVOT_OK;
 }
 
+// ---- the no-alloc variant's scratch address per device ----
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's address of `scratch`, looked up once per device.
+pivot_status static_scratch(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_check(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(PIVOT_ERR_UNSUPPORTED, "device %d: scratch tracked for %d devices", dev,
+                                                 kMaxDevices);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_check(e, "hipGetSymbolAddress(scratch)");
+    if (!p) return fail(PIVOT_ERR_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return PIVOT_OK;
+}
+
+pivot_status group_index_noalloc(const pivot_args* a, const pivot_group_opts* o) {
+  if (!a) return fail(PIVOT_ERR_INVALID_ARG, "args is NULL");
+  Plan p;  // the size check comes before any HIP call
+  pivot_status s = group_plan(a, nullptr, o, o && o->out_cand != nullptr && o->mode == PIVOT_REFINE, p);
+  if (s != PIVOT_OK) return s;
+  if (p.rows_total == 0) return PIVOT_OK;
+  int64_t full, min_tile;
+  score_need(p, full, min_tile);
+  const size_t need = p.fixed + (size_t)min_tile;
+  if (need > PIVOT_NOALLOC_SCRATCH_BYTES)
+    return fail(PIVOT_ERR_WORKSPACE, "the call needs %zu bytes of scratch; the no-alloc scratch holds %zu", need,
+                (size_t)PIVOT_NOALLOC_SCRATCH_BYTES);
+  void* ws = nullptr;
+  s = static_scratch(&ws);
+  if (s != PIVOT_OK) return s;
+  pivot_args b = *a;
+  b.workspace = ws;
+  b.workspace_bytes = PIVOT_NOALLOC_SCRATCH_BYTES;
+  return group_index(&b, nullptr, o);
+}
+
 pivot_group_opts plain_opts(int32_t mode, int32_t g, int32_t c, int32_t dense_below, int32_t* out_cand) {
   pivot_group_opts o;
   memset(&o, 0, sizeof o);
@@ -842,6 +892,10 @@ pivot_status pivot_group_index_opts(const pivot_args* a, const pivot_group_opts*
 
 pivot_status pivot_group_index_layout(const pivot_args* a, const pivot_layout* l, const pivot_group_opts* o) {
   return group_index(a, l, o);
+}
+
+pivot_status pivot_group_index_noalloc(const pivot_args* a, const pivot_group_opts* o) {
+  return group_index_noalloc(a, o);
 }
 
 pivot_status pivot_index_layers(const pivot_args* layers, int32_t n_layers, int32_t stride, const uint8_t* anchors,

@@ -374,3 +374,16 @@ def test_index_layers_follower_inputs_unread_and_opts_checked():
     assert layers_call([args(), args()], stride=1, o=o) == pv.PIVOT_ERR_INVALID_ARG
     assert layers_call([args(ws_bytes=0)], stride=1, o=opts(g=0)) == pv.PIVOT_ERR_INVALID_ARG
 
+
+def test_noalloc_size_check_precedes_the_device():
+    """pivot_group_index_noalloc checks its arguments and its scratch budget
+    before any HIP call: these fail the same way with no GPU."""
+    L = pv.lib()
+    assert L.pivot_group_index_noalloc(None, ctypes.byref(opts())) == pv.PIVOT_ERR_INVALID_ARG
+    assert L.pivot_group_index_noalloc(ctypes.byref(args()), None) == pv.PIVOT_ERR_INVALID_ARG
+    big = args(n_q=8192, q_pos0=131072 - 8192, topk=2048)
+    o = opts(mode=pv.PIVOT_REFINE, g=4, c=4096)
+    assert L.pivot_group_index_noalloc(ctypes.byref(big), ctypes.byref(o)) == pv.PIVOT_ERR_WORKSPACE
+    assert "no-alloc scratch" in pv.last_error()
+    empty = args(n_q=0)
+    assert L.pivot_group_index_noalloc(ctypes.byref(empty), ctypes.byref(o)) == pv.PIVOT_OK
