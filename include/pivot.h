@@ -324,6 +324,13 @@ pivot_status pivot_topk_rows(int32_t n_rows, const float* scores, int64_t ld, in
                              int32_t n_step, int32_t m, int32_t* out, void* stream);
 
 /*
+ * Stage: pivot_topk_rows over rows of bf16 scores (uint16 bits), the score
+ * rows the fp8 index paths rank; ties and padding as pivot_topk_rows.
+ */
+pivot_status pivot_topk_rows_bf16(int32_t n_rows, const uint16_t* scores, int64_t ld, int64_t n0, int32_t n_step,
+                                  int32_t m, int32_t* out, void* stream);
+
+/*
  * Stage: pivot_topk_rows with a device workspace (256-B aligned, or NULL).
  * With at least pivot_topk_rows_workspace_size(n_rows) bytes, a call of at
  * most 256 rows whose longest row has >= 16384 entries splits every row over

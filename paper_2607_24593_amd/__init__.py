@@ -31,6 +31,7 @@ EXPORTED = ["pivot_workspace_size", "pivot_dense_index", "pivot_group_index", "p
             "pivot_group_workspace_size", "pivot_group_index_opts", "pivot_dense_index_layout",
             "pivot_group_index_layout", "pivot_workspace_size_layout", "pivot_proxy_rows",
             "pivot_score_rows", "pivot_topk_rows", "pivot_topk_rows_workspace_size", "pivot_topk_rows_ws",
+            "pivot_topk_rows_bf16",
             "pivot_encode_e4m3", "pivot_profile_begin", "pivot_profile_begin_kinds", "pivot_index_layers",
             "pivot_group_index_noalloc",
             "pivot_profile_end", "pivot_status_string", "pivot_last_error", "pivot_version"]
@@ -145,6 +146,8 @@ def lib():
         L.pivot_score_rows.argtypes = [I32, I32, I32, I32, P, P, P, P, P, I64, I32, P, I64, P, ctypes.c_size_t, P]
         L.pivot_topk_rows.restype = I32
         L.pivot_topk_rows.argtypes = [I32, P, I64, I64, I32, I32, P, P]
+        L.pivot_topk_rows_bf16.restype = I32
+        L.pivot_topk_rows_bf16.argtypes = [I32, P, I64, I64, I32, I32, P, P]
         L.pivot_topk_rows_workspace_size.restype = ctypes.c_size_t
         L.pivot_topk_rows_workspace_size.argtypes = [I32]
         L.pivot_topk_rows_ws.restype = I32
@@ -476,6 +479,17 @@ def pivot_topk_rows(scores, n0, n_step, m, out=None, stream=None):
     out = torch.empty((n, m), dtype=torch.int32, device=scores.device) if out is None else out
     _check(lib().pivot_topk_rows(n, _ptr(scores), ld, int(n0), int(n_step), int(m), _ptr(out), _stream(stream)),
            "pivot_topk_rows")
+    return out
+
+
+def pivot_topk_rows_bf16(scores, n0, n_step, m, out=None, stream=None):
+    """pivot_topk_rows over bf16 score rows (an int16 / bfloat16 tensor [n, ld] of bf16 bits)."""
+    n, ld = scores.shape
+    if scores.element_size() != 2:
+        raise ValueError("bf16 rows hold 2-byte scores")
+    out = torch.empty((n, m), dtype=torch.int32, device=scores.device) if out is None else out
+    _check(lib().pivot_topk_rows_bf16(n, _ptr(scores), ld, int(n0), int(n_step), int(m), _ptr(out),
+                                      _stream(stream)), "pivot_topk_rows_bf16")
     return out
 
 

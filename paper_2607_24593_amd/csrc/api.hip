@@ -976,6 +976,25 @@ pivot_status pivot_topk_rows(int32_t n_rows, const float* scores, int64_t ld, in
   return pivot_topk_rows_ws(n_rows, scores, ld, n0, n_step, m, out, nullptr, 0, stream);
 }
 
+pivot_status pivot_topk_rows_bf16(int32_t n_rows, const uint16_t* scores, int64_t ld, int64_t n0, int32_t n_step,
+                                  int32_t m, int32_t* out, void* stream) {
+  if (n_rows < 0 || n0 < 0 || n_step < 0 || m < 1) return fail(PIVOT_ERR_INVALID_ARG, "bad size");
+  if (n_rows == 0) return PIVOT_OK;
+  if (!scores || !out) return fail(PIVOT_ERR_INVALID_ARG, "null pointer");
+  const int64_t n_max = n0 + (int64_t)(n_rows - 1) * n_step;
+  if (n_max > ld) return fail(PIVOT_ERR_INVALID_ARG, "row length %lld exceeds ld", (long long)n_max);
+  if (n_max > 0x7FFFFFFE) return fail(PIVOT_ERR_INVALID_ARG, "rows exceed int32 positions");
+  SeqTable st;
+  memset(&st, 0, sizeof st);
+  st.n = 1;
+  st.q_pos0[0] = (int32_t)(n0 - 1);
+  st.n_rows[0] = n_rows;
+  RowSpace rs{0, n_rows, n_step, kAll};
+  OutDesc od{out, m, 0, 0, m};
+  return hip_check(launch_topk(scores, true, ld, st, rs, od, n_max - 1, nullptr, 0, (hipStream_t)stream),
+                   "top-k kernel");
+}
+
 pivot_status pivot_topk_rows_ws(int32_t n_rows, const float* scores, int64_t ld, int64_t n0, int32_t n_step,
                                 int32_t m, int32_t* out, void* workspace, size_t workspace_bytes, void* stream) {
   if (workspace && reinterpret_cast<uintptr_t>(workspace) % kAlign)

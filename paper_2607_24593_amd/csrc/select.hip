@@ -35,6 +35,7 @@
 // overflows LDS (e.g. many equal scores) selects directly over the row.
 // A row with no more than m valid entries returns all of them, then -1.
 #include <algorithm>
+#include <climits>
 #include <cstring>
 
 #include "block_select.h"
@@ -49,6 +50,7 @@ constexpr int kWideMaxRows = kSplitMaxRows;  // "few": at most one row per CU
 // + 62.5 KiB -> two
 constexpr int kSelCapSmall = 4096;
 constexpr int kSelCapLarge = 8000;
+constexpr int kSelCap16 = 7680;  // bf16 rows: 6-byte candidates, three 512-thread workgroups per CU
 constexpr int kSampleMinLen = kSplitMinKeys;  // shorter rows take the two-pass path
 constexpr int kChunk4 = 16;           // float4 per sampled chunk (256 bytes)
 constexpr int kSampleChunks = 128;    // at most 8192 sampled scores
@@ -178,16 +180,19 @@ __device__ bool sample_threshold(const E* row, int n, int m, uint32_t* hist, Sel
 // giving each lane its slot (no LDS atomics in the stream), then the segments
 // are packed to the front.  The loops are uniform over the wave, so the
 // running count stays the same in every lane.  Returns the number of keys, or
-// CAP + 1 when a segment overflowed.  Aligned rows only.
-template <int T, int U, int CAP, class E>
-__device__ __forceinline__ int stream_compact(const E* row, int n, float fthr, uint32_t* ckey, int32_t* cpos,
+// CAP + 1 when a segment overflowed.  Aligned rows only.  KT: the stored key,
+// the order-preserving uint32 key, or its upper half for bf16 rows (whose
+// keys have 16 significant bits, key16_expand() restores them).
+template <int T, int U, int CAP, class E, class KT = uint32_t>
+__device__ __forceinline__ int stream_compact(const E* row, int n, float fthr, KT* ckey, int32_t* cpos,
                                               int32_t* wcnt) {
   using SV = ScoreVec<E>;
   constexpr int N = SV::N;
   constexpr int NW = T / 64, SEG = CAP / NW, R = (SEG + 63) / 64;
+  constexpr int KSHIFT = 32 - 8 * (int)sizeof(KT);
   const int tid = threadIdx.x, lane = tid & 63;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
-  uint32_t* mk = ckey + wv * SEG;
+  KT* mk = ckey + wv * SEG;
   int32_t* mp = cpos + wv * SEG;
   int wc = 0;
   auto take = [&](bool valid, float v, int pos) {
@@ -197,7 +202,7 @@ __device__ __forceinline__ int stream_compact(const E* row, int n, float fthr, u
       const int slot =
           wc + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
       if (t && slot < SEG) {
-        mk[slot] = float_key(v);
+        mk[slot] = (KT)(float_key(v) >> KSHIFT);
         mp[slot] = pos;
       }
       wc += (int)__popcll((unsigned long long)bal);
@@ -246,7 +251,7 @@ __device__ __forceinline__ int stream_compact(const E* row, int n, float fthr, u
   if (over) return CAP + 1;
   // a segment moves left onto space other waves may still be reading:
   // through registers, with a barrier in between
-  uint32_t kk[R];
+  KT kk[R];
   int32_t pp[R];
 #pragma unroll
   for (int j = 0; j < R; ++j) {
@@ -333,6 +338,348 @@ void topk_rows_kernel(const E* __restrict__ scores, int64_t ld, SeqTable st, Row
     }
   }
   two_level_select<T>(src, (uint32_t)m, sh, put);
+}
+
+// The order-preserving key of a bf16 score from its upper half: the lower
+// half of a bf16 value's fp32 key is 0 for +0 and positive values, 0xFFFF for
+// negative ones (float_key complements them).
+__device__ __forceinline__ uint32_t key16_expand(uint32_t k16) {
+  return (k16 << 16) | ((k16 & 0x8000u) ? 0u : 0xFFFFu);
+}
+
+// Elements e = tid, tid + THREADS, ... < count of (16-bit key, position) arrays.
+template <int THREADS>
+struct ArraySource16 {
+  const uint16_t* key;
+  const int32_t* pos;
+  int count;
+  template <class F>
+  __device__ __forceinline__ void visit(F f) const {
+    for (int e = threadIdx.x; e < count; e += THREADS) f(key16_expand(key[e]), pos[e]);
+  }
+};
+
+// Members of one tied value (equal keys): positions only.
+template <int THREADS>
+struct TieSource {
+  const int32_t* pos;
+  int count;
+  template <class F>
+  __device__ __forceinline__ void visit(F f) const {
+    for (int e = threadIdx.x; e < count; e += THREADS) f(0u, pos[e]);
+  }
+};
+
+// The candidates of stream_compact16 in place: wave w's wcnt[w] entries
+// start at w * SEG; element e of the concatenation lies in the segment whose
+// prefix count it reaches.
+template <int THREADS, int NW, int SEG>
+struct SegSource16 {
+  const uint16_t* key;
+  const int32_t* pos;
+  int pre[NW + 1];  // prefix counts of the segments
+  __device__ SegSource16(const uint16_t* k, const int32_t* p, const int32_t* wcnt) : key(k), pos(p) {
+    pre[0] = 0;  // uniform: scalar registers
+#pragma unroll
+    for (int w = 0; w < NW; ++w) pre[w + 1] = __builtin_amdgcn_readfirstlane(pre[w] + wcnt[w]);
+  }
+  __device__ __forceinline__ int count() const { return pre[NW]; }
+  __device__ __forceinline__ int index(int e) const {
+    int w = 0, base = 0;  // compares, not an indexed read (which would put pre[] in scratch)
+#pragma unroll
+    for (int k = 1; k < NW; ++k)
+      if (e >= pre[k]) {
+        w = k;
+        base = pre[k];
+      }
+    return w * SEG + (e - base);
+  }
+  template <class F>
+  __device__ __forceinline__ void visit(F f) const {
+    for (int e = threadIdx.x; e < pre[NW]; e += THREADS) {
+      const int i = index(e);
+      f(key16_expand(key[i]), pos[i]);
+    }
+  }
+};
+
+// LDS of topk_rows16_kernel: one region serves, in turn, the sampling
+// histogram (4096 words), the candidates (16-bit keys and int32 positions,
+// CAP each) with the exact select's histogram (kNB16 words), or, for a row
+// that falls back, the two-level select's buffers (TwoLevelShared<CAP2>).
+constexpr int kNB16 = 1024;
+template <int CAP>
+struct Rows16Lds {
+  static constexpr int KEY_BYTES = (2 * CAP + 15) / 16 * 16;
+  static constexpr int POS_BYTES = 4 * CAP;
+  static constexpr int MAIN = KEY_BYTES + POS_BYTES + 4 * kNB16;
+  static constexpr int CAP2 = ((MAIN - (int)sizeof(TwoLevelShared<0>)) / 8) / 64 * 64;
+  static constexpr int RAW = MAIN > 4 * 4096 ? MAIN : 4 * 4096;
+  static_assert((int)sizeof(TwoLevelShared<CAP2>) <= RAW, "fallback fits the region");
+};
+
+// The 16-bit order-preserving keys of the 8 bf16 scores of a 16-byte vector,
+// two per word (key16_expand(k) == float_key(score)).
+__device__ __forceinline__ uint32_t key16_pair(uint32_t w) {
+  uint32_t out = 0;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const uint32_t b = (w >> (16 * h)) & 0xFFFFu;
+    const uint32_t k = (b & 0x7FFFu) == 0 ? 0x8000u : ((b & 0x8000u) ? (~b & 0xFFFFu) : (b | 0x8000u));
+    out |= k << (16 * h);
+  }
+  return out;
+}
+
+// The sampled keys of bf16 rows, packed two per register: V 16-byte vectors
+// per thread.
+template <int V>
+struct SampleSource16 {
+  uint32_t pk[4 * V];
+  bool ok[V];
+  template <class F>
+  __device__ __forceinline__ void visit(F f) const {
+#pragma unroll
+    for (int v = 0; v < V; ++v)
+      if (ok[v]) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) f(key16_expand((pk[4 * v + j / 2] >> (16 * (j & 1))) & 0xFFFFu), 0);
+      }
+  }
+};
+
+// sample_threshold for bf16 rows with the sample held as packed 16-bit keys,
+// at most SCH chunks: 32 (4096 scores, 1/32 of a 131072-score row) for the
+// large candidate buffer, where the count above the threshold spreads by ~8%
+// of m inside the room CAP leaves; 64 for the small one (m <= 2048), whose
+// room is tighter.  base16 receives the 16-bit key below which no kept key
+// lies.
+template <int T, int CAP, int SCH>
+__device__ bool sample_threshold16(const bf16_t* row, int n, int m, uint32_t* hist, SelectShared& sel, float& fthr,
+                                   uint32_t& base16) {
+  constexpr int N = 8;
+  constexpr int SV = (SCH * kChunk4 + T - 1) / T;  // sampled 16-byte vectors per thread
+  const int tid = threadIdx.x;
+  const int nch = n / (N * kChunk4);
+  const int stride = max(16, (nch + SCH - 1) / SCH);
+  const int sch = (nch + stride - 1) / stride;
+  const int s = sch * N * kChunk4;
+  const float rm = (float)s * (float)m / (float)n;
+  const uint32_t ts = (uint32_t)ceilf(rm + 4.0f * sqrtf(rm)) + 1u;
+  if (!(ts < (uint32_t)s && (float)ts * (float)n <= 0.8f * (float)CAP * (float)s)) return false;
+  const uint4* r16 = reinterpret_cast<const uint4*>(row);
+  SampleSource16<SV> smp;
+#pragma unroll
+  for (int v = 0; v < SV; ++v) {
+    const int qi = tid + T * v;
+    smp.ok[v] = qi < sch * kChunk4;
+    const uint4 a = smp.ok[v] ? r16[(int64_t)(qi / kChunk4) * stride * kChunk4 + qi % kChunk4] : make_uint4(0u, 0u, 0u, 0u);
+    smp.pk[4 * v + 0] = key16_pair(a.x);
+    smp.pk[4 * v + 1] = key16_pair(a.y);
+    smp.pk[4 * v + 2] = key16_pair(a.z);
+    smp.pk[4 * v + 3] = key16_pair(a.w);
+  }
+  const uint32_t thr = sample_prefix<T>(smp, ts, hist, sel);
+  fthr = key_float(thr << 12);
+  base16 = thr >> 4;
+  return true;
+}
+
+// Step 2 for bf16 rows: stream_compact storing 16-bit keys, with the next U
+// vectors' loads issued before the current ones are examined, and every kept
+// key counted in `hist` (kNB16 words, zeroed by the caller) at its distance
+// above the threshold, bin min(k16 - base16, kNB16 - 1): below the top bin,
+// one bin per bf16 value.  The waves' segments stay where they are (counts in
+// wcnt; SegSource16 reads them in place).
+template <int T, int U, int CAP>
+__device__ __forceinline__ int stream_compact16(const bf16_t* row, int n, float fthr, uint32_t base16,
+                                                uint16_t* ckey, int32_t* cpos, uint32_t* hist, int32_t* wcnt) {
+  static_assert(8 * U <= 32, "one 32-bit mask per batch");
+  using SV = ScoreVec<bf16_t>;
+  constexpr int N = SV::N;
+  constexpr int NW = T / 64, SEG = CAP / NW;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  uint16_t* mk = ckey + wv * SEG;
+  int32_t* mp = cpos + wv * SEG;
+  int wc = 0;  // keys this wave has kept (the same in every lane)
+  // Appends the kept scores of a batch (bit 8 u + j of `bits`: score j of the
+  // lane's vector u, which is vector q0 + u T of the row): a wave prefix sum
+  // of the lanes' counts gives each lane its first slot, then every lane
+  // writes its own keys, vector by vector, a loop over its set bits (rarely
+  // more than two per vector).
+  auto append = [&](const uint4 (&a)[U], uint32_t bits, int q0) {
+    const int cnt = __popc(bits);
+    int incl = cnt;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int t = __shfl_up(incl, o, 64);
+      if (lane >= o) incl += t;
+    }
+    int slot = wc + incl - cnt;
+    wc += __shfl(incl, 63, 64);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {  // a static vector index: its words stay in registers
+      uint32_t mu = (bits >> (N * u)) & 0xFFu;
+      const uint64_t lo = ((uint64_t)a[u].y << 32) | a[u].x, hi = ((uint64_t)a[u].w << 32) | a[u].z;
+      while (mu) {
+        const int j = __builtin_ctz(mu);
+        mu &= mu - 1;
+        const uint32_t h = (uint32_t)(((j & 4) ? hi : lo) >> (16 * (j & 3))) & 0xFFFFu;
+        const uint32_t k16 = (h & 0x7FFFu) == 0 ? 0x8000u : ((h & 0x8000u) ? (~h & 0xFFFFu) : (h | 0x8000u));
+        atomicAdd(&hist[min(k16 - base16, (uint32_t)(kNB16 - 1))], 1u);
+        if (slot < SEG) {
+          mk[slot] = (uint16_t)k16;
+          mp[slot] = N * (q0 + u * T) + j;
+        }
+        ++slot;
+      }
+    }
+  };
+  auto mask_of = [&](const uint4& a, int u) {
+    float x[N];
+    SV::unpack(a, x);
+    uint32_t bits = 0;
+#pragma unroll
+    for (int j = 0; j < N; ++j) bits |= (x[j] >= fthr ? 1u : 0u) << (N * u + j);
+    return bits;
+  };
+  const int nv = n / N;
+  const uint4* r16 = reinterpret_cast<const uint4*>(row);
+  int base = 0;
+  for (; base + U * T <= nv; base += U * T) {
+    uint4 a[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) a[u] = r16[base + u * T + tid];
+    uint32_t bits = 0;
+#pragma unroll
+    for (int u = 0; u < U; ++u) bits |= mask_of(a[u], u);
+    append(a, bits, base + tid);
+  }
+  for (; base < nv; base += T) {  // fewer than U T vectors left: one per lane
+    const int q = base + tid;
+    uint4 a[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) a[u] = make_uint4(0u, 0u, 0u, 0u);
+    if (q < nv) a[0] = r16[q];
+    append(a, q < nv ? mask_of(a[0], 0) : 0u, q);
+  }
+  if (N * nv < n) {  // the n mod N tail: score e is element e mod N of vector e / N
+    const int e = N * nv + tid;
+    const bool ok = e < n;
+    const int j = e & (N - 1);
+    const uint32_t h = ok ? (uint32_t)row[e] : 0u;
+    const uint32_t w = (j & 1) ? (h << 16) : h;
+    uint4 a[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) a[u] = make_uint4(0u, 0u, 0u, 0u);
+    a[0] = make_uint4((j >> 1) == 0 ? w : 0u, (j >> 1) == 1 ? w : 0u, (j >> 1) == 2 ? w : 0u, (j >> 1) == 3 ? w : 0u);
+    const bool t = ok && __uint_as_float(h << 16) >= fthr;
+    append(a, t ? (1u << j) : 0u, e / N);
+  }
+  if (lane == 0) wcnt[wv] = wc;
+  __syncthreads();
+  int tot = 0;
+  bool over = false;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    tot += wcnt[w];
+    over |= wcnt[w] > SEG;
+  }
+  return over ? CAP + 1 : tot;
+}
+
+// Step 3 for bf16 rows, from the histogram the compaction built: b* = the bin
+// holding the m-th largest key; every candidate in a higher bin is taken, and
+// bin b* (below the top bin) holds one bf16 value, so its members tie and the
+// lowest positions among them complete the set.  Returns false, having
+// emitted nothing, when b* is the top bin or holds more than kNB16
+// members.  lpos: kNB16 LDS words (may alias hist).
+template <int T, class Src, class Put>
+__device__ bool select16(const Src& cand, uint32_t base16, uint32_t m, uint32_t* hist, int32_t* lpos,
+                         int32_t* lcount, SelectShared& sh, Put put) {
+  const int tid = threadIdx.x;
+  find_digit<T, true>(hist, sh, m, kNB16);  // ends with a barrier
+  const uint32_t bsel = sh.digit, rem = m - sh.before, in_b = sh.equal;
+  if (bsel == (uint32_t)(kNB16 - 1) || in_b > (uint32_t)kNB16) return false;
+  if (tid == 0) *lcount = 0;
+  __syncthreads();
+  cand.visit([&](uint32_t key, int32_t p) {
+    const uint32_t d = min((key >> 16) - base16, (uint32_t)(kNB16 - 1));
+    wave_append(d > bsel, &sh.emitted, [&](int slot) { put(slot, p); });
+    if (d == bsel) lpos[atomicAdd(lcount, 1)] = p;
+  });
+  __syncthreads();
+  if (in_b <= (uint32_t)kBucketList) {  // rank each tied member by its position
+    static_assert(T >= kBucketList, "one thread per tied member");
+    const bool mine = tid < (int)in_b;
+    const int32_t p = mine ? lpos[tid] : 0;
+    uint32_t r = 0;
+    if (mine)
+      for (int u = 0; u < (int)in_b; ++u) r += (uint32_t)(lpos[u] < p);
+    wave_append(mine && r < rem, &sh.emitted, [&](int slot) { put(slot, p); });
+    __syncthreads();
+  } else {  // many ties: a radix select on their positions (the keys are equal)
+    const TieSource<T> ties{lpos, (int)in_b};
+    block_select<T, false>(ties, rem, sh, put);
+  }
+  return true;
+}
+
+// topk_rows_kernel's one-read path for bf16 score rows (fp8 inputs) of a
+// launch holding rows of 16384+ scores: candidates take 6 bytes (16-bit key,
+// int32 position) instead of 8, and the sampling histogram, the candidates
+// and the row fallback share one LDS region (they are never live together),
+// so three 512-thread workgroups fit a CU instead of two.
+template <int CAP, int T>
+__global__ __launch_bounds__(T) __attribute__((amdgpu_waves_per_eu(6)))
+void topk_rows16_kernel(const bf16_t* __restrict__ scores, int64_t ld, SeqTable st, RowSpace rs, OutDesc od) {
+  using Lds = Rows16Lds<CAP>;
+  constexpr int U = 4;
+  __shared__ __attribute__((aligned(16))) uint8_t raw[Lds::RAW];
+  __shared__ SelectShared sel;
+  __shared__ int32_t lcount;
+  __shared__ int32_t wcnt[T / 64];
+  const int nrows = rs.i1 - rs.i0;
+  const int b = blockIdx.x / nrows;
+  const int i = rs.i0 + blockIdx.x % nrows;
+  if (!row_active(st, rs, b, i)) return;
+  const int tid = threadIdx.x;
+  const int n = (int)max((int64_t)0, row_limit(st, rs, b, i) + 1);
+  const bf16_t* row = scores + ((int64_t)b * nrows + (i - rs.i0)) * ld;
+  const int m = od.m;
+  const RowDest put(od, st, b, i);
+  if (n <= m) {
+    for (int p = tid; p < m; p += T) put(p, p < n ? p : -1);
+    return;
+  }
+  if (tid == 0) sel.emitted = 0;
+  const bool aligned = (reinterpret_cast<uintptr_t>(row) & 15u) == 0;
+  uint16_t* ckey = reinterpret_cast<uint16_t*>(raw);
+  int32_t* cpos = reinterpret_cast<int32_t*>(raw + Lds::KEY_BYTES);
+  uint32_t* hist = reinterpret_cast<uint32_t*>(raw + Lds::KEY_BYTES + Lds::POS_BYTES);
+  for (int k = tid; k < kNB16; k += T) hist[k] = 0;  // outside the sampling histogram's words
+  float fthr;
+  uint32_t base16;
+  if (n >= kSampleMinLen && aligned &&
+      sample_threshold16<T, CAP, CAP == kSelCapSmall ? 64 : 32>(row, n, m, reinterpret_cast<uint32_t*>(raw), sel,
+                                                               fthr, base16)) {
+    const int found = stream_compact16<T, U, CAP>(row, n, fthr, base16, ckey, cpos, hist, wcnt);
+    if (found >= m && found <= CAP) {
+      const SegSource16<T, T / 64, CAP / (T / 64)> cand(ckey, cpos, wcnt);
+      if (select16<T>(cand, base16, (uint32_t)m, hist, reinterpret_cast<int32_t*>(hist), &lcount, sel, put))
+        return;
+      if (!bucket_select<T, kNB16>(cand, (uint32_t)m, hist, hist, reinterpret_cast<int32_t*>(hist + kBucketList),
+                                   &lcount, sel, put))
+        block_select<T, false>(cand, (uint32_t)m, sel, put);
+      return;
+    }
+  }
+  TwoLevelShared<Lds::CAP2>& fb = *reinterpret_cast<TwoLevelShared<Lds::CAP2>*>(raw);
+  __syncthreads();  // the region's previous use has ended in every wave
+  if (tid == 0) fb.sel.emitted = 0;
+  RowSource<T, U, bf16_t> src{row, n};
+  two_level_select<T>(src, (uint32_t)m, fb, put);
 }
 
 // Split select, step 1: workgroup r writes row r's threshold score to
@@ -519,6 +866,19 @@ size_t split_scratch_bytes(int64_t rows) {
   return (size_t)rows * ((size_t)kSplitSlots * sizeof(uint2) + (size_t)kSplitMaxP * sizeof(int32_t) + sizeof(float));
 }
 
+// Smallest limit of an active row of rs (limits grow with the row index).
+static int64_t min_limit(const SeqTable& st, const RowSpace& rs) {
+  int64_t lim = INT64_MAX;
+  for (int b = 0; b < st.n; ++b) {
+    const int cnt = rs.kind == kProxyRows ? (st.n_rows[b] + rs.step - 1) / rs.step : st.n_rows[b];
+    int hi = std::min(rs.i1, cnt), lo = rs.i0;
+    if (rs.kind == kDenseRows) hi = std::min(hi, st.dense_rows[b]);
+    if (rs.kind == kProxyRows) lo = std::max(lo, st.first_proxy[b]);
+    if (hi > lo) lim = std::min(lim, (int64_t)st.q_pos0[b] + (int64_t)lo * rs.step);
+  }
+  return lim;
+}
+
 template <class E>
 static hipError_t topk_launch(const E* scores, int64_t ld, const SeqTable& st, const RowSpace& rs,
                               const OutDesc& od, int64_t lim_max, void* scratch, size_t scratch_bytes,
@@ -565,6 +925,19 @@ static hipError_t topk_launch(const E* scores, int64_t ld, const SeqTable& st, c
   }
   const bool small = od.m <= kSelCapSmall / 2, sample = lim_max + 1 >= kSampleMinLen;
   const dim3 grid((unsigned)blocks), block(kSelThreads);
+  if constexpr (sizeof(E) == 2) {  // bf16 rows: 6-byte candidates, three workgroups per CU
+    // only when every row takes the sampled path (a short row would fall back
+    // to a two-level select with the smaller buffer the shared region leaves)
+    if (sample && min_limit(st, rs) + 1 >= kSampleMinLen) {
+      if (small)
+        hipLaunchKernelGGL((topk_rows16_kernel<kSelCapSmall, kSelThreads>), grid, block, 0, stream, scores, ld, st,
+                           rs, od);
+      else
+        hipLaunchKernelGGL((topk_rows16_kernel<kSelCap16, kSelThreads>), grid, block, 0, stream, scores, ld, st, rs,
+                           od);
+      return hipGetLastError();
+    }
+  }
   if (small && sample)
     hipLaunchKernelGGL((topk_rows_kernel<kSelCapSmall, kSelThreads, true, E>), grid, block, 0, stream, scores, ld, st, rs,
                        od);

@@ -8,7 +8,7 @@ import torch
 import oracle
 import paper_2607_24593_amd as pv
 from gpu_util import dev, host, say
-from workload.gen import make_prefill
+from workload.gen import encode_bf16, make_prefill
 
 pytestmark = pytest.mark.gpu
 
@@ -75,7 +75,7 @@ def _expect_topk(row, n, m):
     return oracle.topk(row[:n].astype(np.float64), np.arange(n, dtype=np.int32), m)
 
 
-@pytest.mark.parametrize("split", [False, True])
+@pytest.mark.parametrize("split", [False, True, "bf16"])
 @pytest.mark.parametrize("case", ["normal", "ties", "signed_zeros", "short", "exact", "long2k", "long4k",
                                   "ragged", "constant", "sample_miss", "sample_ragged", "heavy_tail", "small_m",
                                   "unaligned", "m4k_normal", "slice_skew", "decode_shape", "many_rows",
@@ -136,8 +136,12 @@ def test_topk_rows_exact(case, split):
     else:
         rows = np.full((2, 20000), 3.5); n0, m = 20000, 700
     rows = rows.astype(np.float32)
-    say("topk_rows", case, rows.shape, n0, step, m, "split" if split else "")
-    if split:
+    say("topk_rows", case, rows.shape, n0, step, m, split)
+    if split == "bf16":  # the rows the fp8 index paths rank: rounded to bf16 first
+        bits = encode_bf16(rows)
+        rows = (bits.astype(np.uint32) << 16).view(np.float32)
+        got = host(pv.pivot_topk_rows_bf16(dev(bits), n0, step, m))
+    elif split:
         got = host(pv.pivot_topk_rows_ws(dev(rows), n0, step, m))
     else:
         got = host(pv.pivot_topk_rows(dev(rows), n0, step, m))
