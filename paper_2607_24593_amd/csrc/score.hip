@@ -1,19 +1,21 @@
 // Lightning-indexer scoring kernel for gfx950 (Sec. 3.1 Eq. 1; App. A fp8 form).
 //
 // One workgroup = 4 waves.  A wave keeps R query rows (all 64 heads x 128
-// dims) in registers as MFMA A operands and streams 16-key fragments of the
-// sequence's keys straight from global memory (each lane loads 32 contiguous
-// bytes; a fragment is one contiguous 2 KiB (fp8) block).  The ReLU, the
+// dims) in registers as MFMA A operands and scores 16-key fragments of the
+// sequence's keys against them (a lane takes 32 contiguous bytes of a key
+// row per MFMA step; a fragment is one contiguous 2 KiB (fp8) or 4 KiB
+// (bf16) block).  The ReLU, the
 // gate-and-scale weighting and the head reduction run in the MFMA epilogue
 // (mfma_tile.h), so every (row, key) pair leaves the kernel as one fp32, or
 // one bf16 (round to nearest even) where the caller asks for bf16 score rows.
 //
 // Two wave arrangements:
 //   rows mode  (>= 16 rows per sequence, prefill): the 4 waves hold 4 different
-//              row groups and walk the same keys, so a key fragment is fetched
-//              from L2 once and served to 4 waves from the vector L1;
+//              row groups and walk the same keys, so the workgroup fetches
+//              each key once into LDS and the 4 waves read it from there;
 //   keys mode  (< 16 rows per sequence, decode): the 4 waves hold the same rows
-//              and split the keys.
+//              and split the keys, each loading its fragments from global
+//              memory into registers.
 // Grid: rows mode runs a 1-D grid whose linear index is segment * row blocks
 // + row block, so consecutive workgroups take the row blocks of one key
 // segment: dispatched round-robin over the 8 XCDs, the ~64 workgroups resident
@@ -30,6 +32,13 @@ namespace pivot {
 // A key offset past every paged pool (pools stay below 2^31 bytes): its
 // loads read zeros, and adding a fragment's lane offset cannot wrap it.
 constexpr uint32_t kDropOffset = 0x80000000u;
+
+// Rows mode stages keys through LDS 4 KiB at a time: 32 fp8 or 16 bf16 keys,
+// each row padded by 16 bytes.
+template <int DT>
+constexpr int kStageKeys = DT == kFp8 ? 32 : 16;
+template <int DT>
+constexpr int kStageSlot = kStageKeys<DT> * (kD * (DT == kFp8 ? 1 : 2) + 16);
 
 // OB16: scores leave as bf16 (RNE) instead of fp32.
 template <int DT, int R, bool KSPLIT, bool PAGED, bool OB16>
@@ -48,6 +57,7 @@ __global__ __launch_bounds__(256) void score_kernel(const uint8_t* __restrict__ 
   constexpr int KB = kD * EB;  // bytes per key
   constexpr int RB = KSPLIT ? R : 4 * R;
   __shared__ float sks[4096];  // the segment's key scales (fp8)
+  __shared__ __align__(16) uint8_t kst[KSPLIT ? 16 : 3 * kStageSlot<DT>];  // rows mode: staged keys
   __shared__ int32_t spg[PAGED ? 256 : 1];  // the segment's pages (paged keys; a segment of <= 4096 keys
                                             // starts on a page boundary or lies inside one page)
   const int tid = threadIdx.x, lane = tid & 63;
@@ -115,12 +125,12 @@ __global__ __launch_bounds__(256) void score_kernel(const uint8_t* __restrict__ 
   tile.load(rows, wrows, qs, lrows, lsc, lane);
 
   // keys through a range-checked buffer resource with 32-bit offsets: the
-  // segment's contiguous keys (fragments that run past the wave's last key
-  // read zeros), or the page pool (keys past the wave's last one are sent to
-  // kDropOffset)
+  // segment's contiguous keys (reads past the workgroup's last key in rows
+  // mode, the wave's in keys mode, return zeros), or the page pool (such keys
+  // are sent to kDropOffset)
   const __amdgpu_buffer_rsrc_t kr =
       PAGED ? buffer_rsrc(k, (uint32_t)(((int64_t)km.n_pages << km.shift) * KB))
-            : buffer_rsrc(k + km.row(b, seg0) * KB, (uint32_t)nkeys * KB);
+            : buffer_rsrc(k + km.row(b, seg0) * KB, (uint32_t)(KSPLIT ? nkeys : nseg_keys) * KB);
   // e: key index within the segment; the prologue reads the page table in
   // global memory, the loop the segment's pages staged in LDS
   const int64_t page0 = PAGED ? seg0 >> km.shift : 0;
@@ -141,23 +151,6 @@ __global__ __launch_bounds__(256) void score_kernel(const uint8_t* __restrict__ 
       return (uint32_t)e * KB;
     }
   };
-  const int S = KSPLIT ? 64 : 16;
-  int t = KSPLIT ? 16 * wave : 0;  // key offset within the segment
-  const int lr0 = lane & 15, kg0 = lane >> 4;
-  KeyFrag<DT> f0, f1, f2;
-  f0.load(kr, key_off0(t + lr0), kg0);
-  f1.load(kr, key_off0(t + S + lr0), kg0);
-  f2.load(kr, key_off0(t + 2 * S + lr0), kg0);
-
-  if constexpr (DT == kFp8) {
-#pragma unroll
-    for (int u = 0; u < KS_PER; ++u) sks[tid + 256 * u] = ksv[u];  // zeros past the segment
-    __syncthreads();
-  } else if constexpr (PAGED) {
-    __syncthreads();  // the staged pages
-  }
-  if (nkeys == 0) return;  // no workgroup barrier follows
-
   const int lr = lane & 15, kg = lane >> 4;
   const int qr = kg / Tile::G;
   const int my_i = i_w + qr;
@@ -182,17 +175,99 @@ __global__ __launch_bounds__(256) void score_kernel(const uint8_t* __restrict__ 
     else
       __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc), orr, off, 0, 0);
   };
-  // Three key fragments rotate: while one is scored the next two are loading.
-  // The loop body has no exits, so the compiler keeps each reload right after
-  // the fragment's last use; fragments past the wave's keys read zeros and
-  // their stores are dropped.
-  for (; t < nkeys; t += 3 * S) {
-    emit(tile.score(f0), t);
-    f0.load(kr, key_off(t + 3 * S + lr), kg);
-    emit(tile.score(f1), t + S);
-    f1.load(kr, key_off(t + 4 * S + lr), kg);
-    emit(tile.score(f2), t + 2 * S);
-    f2.load(kr, key_off(t + 5 * S + lr), kg);
+  if constexpr (KSPLIT) {
+    // keys mode: each wave walks its own 16-key fragments, three rotating
+    // (one scored while the next two load).  The loop body has no exits, so
+    // the compiler keeps each reload right after the fragment's last use;
+    // fragments past the wave's keys read zeros and their stores are dropped.
+    constexpr int S = 64;
+    int t = 16 * wave;  // key offset within the segment
+    KeyFrag<DT> f0, f1, f2;
+    f0.load(kr, key_off0(t + lr), kg);
+    f1.load(kr, key_off0(t + S + lr), kg);
+    f2.load(kr, key_off0(t + 2 * S + lr), kg);
+    if constexpr (DT == kFp8) {
+#pragma unroll
+      for (int u = 0; u < KS_PER; ++u) sks[tid + 256 * u] = ksv[u];  // zeros past the segment
+      __syncthreads();
+    } else if constexpr (PAGED) {
+      __syncthreads();  // the staged pages
+    }
+    for (; t < nkeys; t += 3 * S) {
+      emit(tile.score(f0), t);
+      f0.load(kr, key_off(t + 3 * S + lr), kg);
+      emit(tile.score(f1), t + S);
+      f1.load(kr, key_off(t + 4 * S + lr), kg);
+      emit(tile.score(f2), t + 2 * S);
+      f2.load(kr, key_off(t + 5 * S + lr), kg);
+    }
+  } else {
+    // rows mode: the 4 waves score the same keys, so the workgroup fetches
+    // each 4 KiB stage of keys once (every thread one 16-byte piece, the
+    // stage one contiguous block) and the waves read their fragments from
+    // LDS.  Three LDS slots rotate with one barrier per stage: stage i + 1 is
+    // written while stage i is scored, and the slot it overwrites held stage
+    // i - 2, which every wave finished before the previous barrier.  Each
+    // thread keeps three stages' loads in flight (registers r0..r2 hold
+    // stages 3 n, 3 n + 1, 3 n + 2).  Key rows sit KB + 16 bytes apart in LDS,
+    // so the 16 rows of a fragment start in 16 different 16-byte bank
+    // groups.  Every wave runs every stage of the workgroup's key range (the
+    // barriers are uniform).
+    const int nst = (nseg_keys + kStageKeys<DT> - 1) / kStageKeys<DT>;
+    const int my_key = tid / (KB / 16), my_piece = tid % (KB / 16);
+    uint8_t* const put_at = kst + my_key * (KB + 16) + 16 * my_piece;
+    // prologue fetches (before the first barrier) read the page table in
+    // global memory, later ones the copy staged in LDS
+    auto fetch = [&](int st_i, bool prologue = false) -> v4i {
+      const int e = st_i * kStageKeys<DT> + my_key;
+      uint32_t off;
+      if constexpr (PAGED) {
+        if (e >= nseg_keys) {
+          off = kDropOffset;
+        } else if (prologue) {
+          off = (uint32_t)(km.row(b, seg0 + e) * KB);
+        } else {
+          const int64_t s = seg0 + e;
+          off = (uint32_t)((((int64_t)spg[(s >> km.shift) - page0] << km.shift) | (s & ((1 << km.shift) - 1))) * KB);
+        }
+      } else {
+        off = (uint32_t)e * KB;  // past the segment: zeros (range-checked resource)
+      }
+      return __builtin_amdgcn_raw_buffer_load_b128(kr, off + 16 * my_piece, 0, 0);
+    };
+    v4i r0 = fetch(0, true), r1 = fetch(1, true), r2 = fetch(2, true);
+    if constexpr (DT == kFp8) {
+#pragma unroll
+      for (int u = 0; u < KS_PER; ++u) sks[tid + 256 * u] = ksv[u];  // zeros past the segment
+    }
+    *reinterpret_cast<v4i*>(put_at) = r0;
+    r0 = fetch(3, true);
+    __syncthreads();
+    auto stage = [&](int i, v4i& r, int slot_put, int slot) {
+      *reinterpret_cast<v4i*>(put_at + slot_put * kStageSlot<DT>) = r;  // stage i + 1
+      r = fetch(i + 4);
+      __syncthreads();
+      const int t = i * kStageKeys<DT>;
+#pragma unroll
+      for (int f = 0; f < kStageKeys<DT> / 16; ++f) {
+        KeyFrag<DT> fr;
+        fr.load(kst + slot * kStageSlot<DT> + (16 * f + lr) * (KB + 16), kg);
+        emit(tile.score(fr), t + 16 * f);
+      }
+    };
+    // Every stage issues the same loads and stores (a wave's stages past its
+    // own keys are scored too, their stores dropped; rows of a workgroup end
+    // within 16 keys of each other), so the compiler's memory-counter waits
+    // stay exact across the loop and each staged register waits only for its
+    // own load.
+    int i = 0;
+    for (; i + 3 <= nst; i += 3) {
+      stage(i, r1, 1, 0);
+      stage(i + 1, r2, 2, 1);
+      stage(i + 2, r0, 0, 2);
+    }
+    if (i < nst) stage(i, r1, 1, 0);
+    if (i + 1 < nst) stage(i + 1, r2, 2, 1);
   }
 }
 
