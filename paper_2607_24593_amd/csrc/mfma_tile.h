@@ -154,17 +154,20 @@ struct RowTile {
       if (p == 1 || p == 2) hold = hold + part;
       if (p == 3) tot = hold + part;
     } else if constexpr (R == 2) {  // lane group parity q holds P_q (p = 0) and P_{2+q} (p = 1)
-      const float other = __shfl_xor(part, 16, kWave);
-      if (p == 0) {
-        hold = part + other;  // P_0 + P_1 (additions commute)
-      } else {
-        const bool q0 = ((threadIdx.x >> 4) & 1) == 0;
-        tot = (hold + (q0 ? part : other)) + (q0 ? other : part);
-      }
+      // v_permlane16_swap of a value with itself leaves, in every lane, the
+      // even lane group's value of the pair in the first result and the odd
+      // one's in the second
+      const auto e = __builtin_amdgcn_permlane16_swap(__float_as_uint(part), __float_as_uint(part), false, false);
+      const float even = __uint_as_float(e[0]), odd = __uint_as_float(e[1]);
+      if (p == 0) hold = even + odd;   // P_0 + P_1
+      else tot = (hold + even) + odd;  // + P_2, + P_3
     } else {  // lane group q holds P_q; lane group 0 gathers the others
-      const float p1 = __shfl_xor(part, 16, kWave), p2 = __shfl_xor(part, 32, kWave);
-      const float p3 = __shfl_xor(part, 48, kWave);
-      tot = ((part + p1) + p2) + p3;
+      // after the 16-lane swap: (P_0 | P_2) and (P_1 | P_3) in each half;
+      // the 32-lane swaps bring the upper half's values (P_2, P_3) down
+      const auto e = __builtin_amdgcn_permlane16_swap(__float_as_uint(part), __float_as_uint(part), false, false);
+      const auto h0 = __builtin_amdgcn_permlane32_swap(e[0], e[0], false, false);
+      const auto h1 = __builtin_amdgcn_permlane32_swap(e[1], e[1], false, false);
+      tot = ((__uint_as_float(e[0]) + __uint_as_float(e[1])) + __uint_as_float(h0[1])) + __uint_as_float(h1[1]);
     }
   }
 
