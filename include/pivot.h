@@ -158,6 +158,21 @@ typedef enum {
   PIVOT_AGG_LAST = 2    /* the group's last member, unchanged */
 } pivot_aggregate;
 
+/* How Refine runs Eqs. 8-9; every path gives the same top-k sets.
+ *   PIVOT_REFINE_SPLIT: re-score every member into the workspace, then one
+ *     select launch over the member rows.
+ *   PIVOT_REFINE_FUSED: one launch; each group's member scores stay on chip
+ *     and its members select there.  Applies to fp8 inputs with g <= 4, no
+ *     window and pivot_cand_width() <= 4096; other calls take the split path.
+ *   PIVOT_REFINE_AUTO: the faster path for the shapes at hand; currently
+ *     always the split one (the fused launch runs two workgroups per CU,
+ *     too few to hide its selects' latency). */
+typedef enum {
+  PIVOT_REFINE_AUTO = 0,
+  PIVOT_REFINE_FUSED = 1,
+  PIVOT_REFINE_SPLIT = 2
+} pivot_refine_path;
+
 typedef struct {
   int32_t mode;         /* PIVOT_REUSE or PIVOT_REFINE */
   int32_t g, c;         /* group size, candidate budget (as pivot_group_index) */
@@ -166,12 +181,14 @@ typedef struct {
   int32_t window_kind;  /* pivot_window_kind */
   int32_t aggregate;    /* pivot_aggregate */
   int32_t* out_cand;    /* optional dev int32 [B, ceil(n_q/g), pivot_cand_width()] */
+  int32_t refine_path;  /* pivot_refine_path (0 = PIVOT_REFINE_AUTO) */
 } pivot_group_opts;
 
 /*
  * PIVOT with the options of App. B and of the aggregation ablation (Sec. 5.4);
- * opts {mode, g, c, dense_below, 0, 0, PIVOT_AGG_MEAN, out_cand} is exactly
- * pivot_group_index.  With window W > 0 (Refine only), for a group with first
+ * opts {mode, g, c, dense_below, 0, 0, PIVOT_AGG_MEAN, out_cand,
+ * PIVOT_REFINE_AUTO} is exactly pivot_group_index; refine_path picks how
+ * Refine runs (pivot_refine_path; any other value is PIVOT_ERR_INVALID_ARG).  With window W > 0 (Refine only), for a group with first
  * position t0 and gs members:
  *   - PIVOT_WINDOW_SHARED (prefill): the union of the members' windows,
  *     positions t0-W+1 .. t0+g-1, takes w = W+g-1 of the c candidate slots

@@ -25,6 +25,7 @@ PIVOT_MAX_KEYS = 1 << 27
 PIVOT_NOALLOC_SCRATCH_BYTES = 64 << 20
 PIVOT_WINDOW_SHARED, PIVOT_WINDOW_PER_QUERY = 0, 1
 PIVOT_AGG_MEAN, PIVOT_AGG_FIRST, PIVOT_AGG_LAST = 0, 1, 2
+PIVOT_REFINE_AUTO, PIVOT_REFINE_FUSED, PIVOT_REFINE_SPLIT = 0, 1, 2
 H, D = 64, 128
 
 EXPORTED = ["pivot_workspace_size", "pivot_dense_index", "pivot_group_index", "pivot_cand_width",
@@ -65,7 +66,7 @@ class pivot_group_opts(ctypes.Structure):
     _fields_ = [
         ("mode", ctypes.c_int32), ("g", ctypes.c_int32), ("c", ctypes.c_int32),
         ("dense_below", ctypes.c_int32), ("window", ctypes.c_int32), ("window_kind", ctypes.c_int32),
-        ("aggregate", ctypes.c_int32), ("out_cand", ctypes.c_void_p),
+        ("aggregate", ctypes.c_int32), ("out_cand", ctypes.c_void_p), ("refine_path", ctypes.c_int32),
     ]
 
 
@@ -95,11 +96,12 @@ def make_layout(cu_q=None, block_table=None, page_size=0, pool_keys=0) -> pivot_
 
 
 def group_opts(mode, g, c, dense_below=-1, window=0, window_kind=PIVOT_WINDOW_SHARED,
-               aggregate=PIVOT_AGG_MEAN, out_cand=None) -> pivot_group_opts:
+               aggregate=PIVOT_AGG_MEAN, out_cand=None, refine_path=PIVOT_REFINE_AUTO) -> pivot_group_opts:
     o = pivot_group_opts()
     o.mode, o.g, o.c, o.dense_below = int(mode), int(g), int(c), int(dense_below)
     o.window, o.window_kind, o.aggregate = int(window), int(window_kind), int(aggregate)
     o.out_cand = _ptr(out_cand)
+    o.refine_path = int(refine_path)
     o._keep = out_cand
     return o
 
@@ -323,14 +325,15 @@ def pivot_group_workspace_size(a: pivot_args, o: pivot_group_opts) -> int:
 
 def pivot_group_index_opts(q, q_scale, w, k, k_scale, q_pos0, n_k, topk, mode, g, c, dense_below=-1,
                            window=0, window_kind=PIVOT_WINDOW_SHARED, aggregate=PIVOT_AGG_MEAN,
-                           out=None, out_cand=None, ws=None, stream=None):
+                           out=None, out_cand=None, ws=None, stream=None, refine_path=PIVOT_REFINE_AUTO):
     """PIVOT with App. B's local window and the first / last proxy aggregation;
-    out_cand, when given, is int32 [B, n_groups, pivot_cand_width(opts)]."""
+    out_cand, when given, is int32 [B, n_groups, pivot_cand_width(opts)];
+    refine_path: PIVOT_REFINE_AUTO / _FUSED / _SPLIT (same results)."""
     squeeze = q.dim() == 3
     shape = (q.shape[0], topk) if squeeze else (q.shape[0], q.shape[1], topk)
     out = torch.empty(shape, dtype=torch.int32, device=q.device) if out is None else out
     a = make_args(q, q_scale, w, k, k_scale, q_pos0, n_k, topk, out, stream=stream)
-    o = group_opts(mode, g, c, dense_below, window, window_kind, aggregate, out_cand)
+    o = group_opts(mode, g, c, dense_below, window, window_kind, aggregate, out_cand, refine_path)
     _attach(a, pivot_group_workspace_size(a, o), ws, q.device, stream)
     _check(lib().pivot_group_index_opts(ctypes.byref(a), ctypes.byref(o)), "pivot_group_index_opts")
     return out
@@ -430,12 +433,12 @@ def pivot_dense_index_layout(q, q_scale, w, k, k_scale, q_pos0, n_k, topk, layou
 
 def pivot_group_index_layout(q, q_scale, w, k, k_scale, q_pos0, n_k, topk, layout, mode, g, c, dense_below=-1,
                              window=0, window_kind=PIVOT_WINDOW_SHARED, aggregate=PIVOT_AGG_MEAN, out=None,
-                             out_cand=None, ws=None, stream=None):
+                             out_cand=None, ws=None, stream=None, refine_path=PIVOT_REFINE_AUTO):
     """PIVOT over packed query runs (groups restart at every run) and contiguous or
     paged keys: returns int32 [rows, topk]."""
     out = torch.empty((q.shape[0], topk), dtype=torch.int32, device=q.device) if out is None else out
     a = make_args_batch(q, q_scale, w, k, k_scale, q_pos0, n_k, topk, out, stream=stream)
-    o = group_opts(mode, g, c, dense_below, window, window_kind, aggregate, out_cand)
+    o = group_opts(mode, g, c, dense_below, window, window_kind, aggregate, out_cand, refine_path)
     _attach(a, pivot_workspace_size_layout(a, layout, o), ws, q.device, stream)
     _check(lib().pivot_group_index_layout(ctypes.byref(a), ctypes.byref(layout), ctypes.byref(o)),
            "pivot_group_index_layout")

@@ -120,6 +120,7 @@ struct Plan {
   bool qlin = false, plin = false;
   // App. B window and the proxy aggregation
   int W = 0, wkind = PIVOT_WINDOW_SHARED, agg = PIVOT_AGG_MEAN;
+  int rpath = PIVOT_REFINE_AUTO;  // pivot_refine_path
   int wg = 0;          // window union slots (W + g - 1, or 0)
   int width = 0;       // candidate slots per group
   int proxy_m = 0;     // slots the proxy fills (c, or c - wg for the shared window)
@@ -199,7 +200,7 @@ int cand_width(int c, int g, int W, int wkind) {
 // workspace reserves none.
 pivot_status make_plan(const pivot_args* a, const pivot_layout* l, int mode, int g, int c, int dense_below,
                        bool ext_cand, Plan& p, int W = 0, int wkind = PIVOT_WINDOW_SHARED,
-                       int agg = PIVOT_AGG_MEAN) {
+                       int agg = PIVOT_AGG_MEAN, int rpath = PIVOT_REFINE_AUTO) {
   pivot_status s = check_args(a, l, p.nq);
   if (s != PIVOT_OK) return s;
   if (mode != PIVOT_DENSE && mode != PIVOT_REUSE && mode != PIVOT_REFINE)
@@ -209,6 +210,8 @@ pivot_status make_plan(const pivot_args* a, const pivot_layout* l, int mode, int
   if (wkind != PIVOT_WINDOW_SHARED && wkind != PIVOT_WINDOW_PER_QUERY)
     return fail(PIVOT_ERR_INVALID_ARG, "window_kind %d", wkind);
   if (W < 0) return fail(PIVOT_ERR_INVALID_ARG, "window must be >= 0");
+  if (rpath != PIVOT_REFINE_AUTO && rpath != PIVOT_REFINE_FUSED && rpath != PIVOT_REFINE_SPLIT)
+    return fail(PIVOT_ERR_INVALID_ARG, "refine_path %d", rpath);
   if (mode != PIVOT_DENSE) {
     if (g < 1) return fail(PIVOT_ERR_INVALID_ARG, "g must be >= 1");
     if (c < 0) return fail(PIVOT_ERR_INVALID_ARG, "c must be >= 0");
@@ -231,6 +234,7 @@ pivot_status make_plan(const pivot_args* a, const pivot_layout* l, int mode, int
   p.W = W;
   p.wkind = wkind;
   p.agg = agg;
+  p.rpath = rpath;
   p.wg = W > 0 ? W + g - 1 : 0;
   p.width = mode == PIVOT_REFINE ? cand_width(c, g, W, wkind) : c;
   p.proxy_m = (W > 0 && wkind == PIVOT_WINDOW_SHARED) ? c - p.wg : c;
@@ -548,7 +552,8 @@ pivot_status group_plan(const pivot_args* a, const pivot_layout* l, const pivot_
                         Plan& p) {
   if (!o) return fail(PIVOT_ERR_INVALID_ARG, "opts is NULL");
   if (o->mode != PIVOT_REUSE && o->mode != PIVOT_REFINE) return fail(PIVOT_ERR_INVALID_ARG, "mode %d", o->mode);
-  return make_plan(a, l, o->mode, o->g, o->c, o->dense_below, ext_cand, p, o->window, o->window_kind, o->aggregate);
+  return make_plan(a, l, o->mode, o->g, o->c, o->dense_below, ext_cand, p, o->window, o->window_kind, o->aggregate,
+                   o->refine_path);
 }
 
 pivot_status dense_index(const pivot_args* a, const pivot_layout* l) {
@@ -693,7 +698,7 @@ pivot_status group_index(const pivot_args* a, const pivot_layout* l, const pivot
                                                 : nullptr,
                                          p.g, kb.k, kb.ks, kb.map, st, p.proxy_lo, p.n_groups, cb, width, p.W, wslot,
                                          p.topk, ws + p.off_rsc + goff * p.g * width * score_eb(p.dtype),
-                                         a->out_idx + qoff * p.topk, stream);
+                                         a->out_idx + qoff * p.topk, p.rpath, stream);
                   }),
                   "refine kernel");
     if (s != PIVOT_OK) return s;

@@ -79,11 +79,12 @@ constexpr int kSplitMinKeys = 16384; // nor do launches whose rows are all short
 // for fp8 inputs, fp32 for bf16 inputs), then
 // select top-m.  W = 0: plain rows (the first min(c, t0 + 1) slots hold
 // positions).  W > 0 (App. B window): any slot may be empty (-1); member t
-// uses positions in [0, t], from slot wslot on also >= t - W + 1.
+// uses positions in [0, t], from slot wslot on also >= t - W + 1.  path: a
+// pivot_refine_path (the fused launch needs no `rescore` buffer).
 hipError_t launch_refine(int dtype, const void* q, const float* q_scale, const float* w, const uint8_t* lin,
                          const float* lin_scale, int g, const void* k, const float* k_scale, const KeyMap& km,
                          const SeqTable& st, int j0, int j1, const int32_t* cand, int c, int W, int wslot, int m,
-                         void* rescore, int32_t* out_idx, hipStream_t stream);
+                         void* rescore, int32_t* out_idx, int path, hipStream_t stream);
 
 // App. B window union of groups [j0, j1) (j >= first_proxy[b]) into slots
 // [slot0, slot0 + W + g - 1) of the [groups, width] candidate rows; dedupe

@@ -30,6 +30,7 @@
 #include "block_select.h"
 #include "launch.h"
 #include "mfma_tile.h"
+#include "pivot.h"
 
 namespace pivot {
 
@@ -55,7 +56,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void r
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
   // members [R blk, R blk + R); candidate fragments of slice `part`
-  const int nblk = (g + R - 1) / R, unit = 4 * (int)blockIdx.x + wave;
+  // WPG: workgroups are dealt round-robin to the 8 XCDs; XCD x % 8 takes a
+  // contiguous run of groups (consecutive groups share most candidates, so
+  // their gathers hit that XCD's L2); a partial last round keeps its order
+  const int nwg = (int)gridDim.x, full = nwg - nwg % 8, bx = (int)blockIdx.x;
+  const int wgx = WPG && bx < full ? (bx % 8) * (full / 8) + bx / 8 : bx;
+  const int nblk = (g + R - 1) / R, unit = 4 * wgx + wave;
   const int j = j0 + (WPG ? unit / nblk : (int)blockIdx.x), b = blockIdx.y;
   const int blk = WPG ? unit % nblk : (int)blockIdx.z / parts, part = WPG ? 0 : (int)blockIdx.z % parts;
   if (b >= st.n || j >= seq_groups(st, b, g) || j < st.first_proxy[b]) return;
@@ -176,6 +182,283 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void r
     emit(tile.score(k2), s2, f + 2 * S);
     fetch(k2, s2, f + 5 * S);
   }
+}
+
+// Fused fine step (Eqs. 8-9 in one launch) for fp8 groups of at most four
+// members whose candidate rows have no window slots and at most kFuseCand
+// entries: one workgroup per group.  The 4 waves split the group's candidate
+// fragments (gathered three ahead, as in rescore_kernel) and write the
+// members' bf16 scores into LDS; after one barrier wave t selects member t's
+// top-m from there, so the scores never leave the CU.  The select keys a
+// score as its 16-bit order key plus one (0 marks an unusable slot), each
+// lane holding 64 (key, position) pairs in registers, and finds
+//   K  = the key with fewer than m entries above it and at least m at or
+//        above it (two radix passes, high byte then low byte, over a 256-bin
+//        LDS histogram of the wave's own),
+//   P  = the smallest position with enough entries of key K at positions
+//        <= P to fill the row (bisection over the tied positions, compacted
+//        into LDS),
+// which picks exactly the top m by (score desc, position asc).
+constexpr int kFuseCand = 4096;
+
+template <int R, bool PAGED>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void rescore_select_kernel(
+    const uint8_t* __restrict__ q, const float* __restrict__ q_scale, const float* __restrict__ w,
+    const uint8_t* __restrict__ lin, const float* __restrict__ lin_scale, int g, const uint8_t* __restrict__ k,
+    const float* __restrict__ k_scale, KeyMap km, SeqTable st, int j0, const int32_t* __restrict__ cand, int c,
+    int m, int32_t* __restrict__ out_idx) {
+  using Tile = RowTile<kFp8, R>;
+  constexpr int NV = kFuseCand / 64;  // (key, position) pairs per lane in the select
+  __shared__ int32_t spos[kFuseCand];                  // candidate positions
+  __shared__ int32_t sprow[PAGED ? kFuseCand : 1];     // their pool rows (paged keys)
+  __shared__ uint16_t ssc[R * kFuseCand];              // member scores, bf16 bits
+  __shared__ uint32_t shist[4 * 257];                  // each wave's select histogram (+ a sink bin)
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  // workgroups are dealt round-robin to the 8 XCDs: XCD x % 8 takes a
+  // contiguous run of groups (consecutive groups share most candidates, so
+  // their gathers hit that XCD's L2); a partial last round keeps its order
+  const int nwg = (int)gridDim.x, full = nwg - nwg % 8, bx = (int)blockIdx.x;
+  const int j = j0 + (bx < full ? (bx % 8) * (full / 8) + bx / 8 : bx), b = blockIdx.y;
+  if (b >= st.n || j >= seq_groups(st, b, g) || j < st.first_proxy[b]) return;
+  const int gs = min(g, st.n_rows[b] - j * g);  // members, <= R
+  const int64_t t0 = (int64_t)st.q_pos0[b] + (int64_t)j * g;
+  const int nc = (int)min((int64_t)c, t0 + 1);  // usable slots: the first min(c, t0 + 1)
+  const int32_t* crow = cand + ((int64_t)st.grp0[b] + j) * c;
+  const int64_t r0 = (int64_t)st.row0[b] + (int64_t)j * g;
+  const uint8_t* kb = PAGED ? k : k + km.row(b, 0) * kD;
+  const float* ksb = PAGED ? k_scale : k_scale + km.row(b, 0);
+
+  // positions: all loads of a thread issued before the first store
+  {
+    constexpr int SB = kFuseCand / 256;
+    int32_t pv[SB];
+#pragma unroll
+    for (int u = 0; u < SB; ++u) pv[u] = tid + 256 * u < nc ? crow[tid + 256 * u] : 0;
+#pragma unroll
+    for (int u = 0; u < SB; ++u)
+      if (tid + 256 * u < nc) {
+        spos[tid + 256 * u] = pv[u];
+        if constexpr (PAGED) sprow[tid + 256 * u] = (int32_t)km.row(b, max(pv[u], 0));
+      }
+  }
+  const int lr = lane & 15, kg = lane >> 4;
+  // key row of slot 16 f + lr (slots past the row repeat its last one;
+  // empty slots read key 0), from LDS or, before the barrier, global memory
+  auto row_lds = [&](int f) {
+    const int e = min(16 * f + lr, nc - 1);
+    return PAGED ? sprow[e] : max(spos[e], 0);
+  };
+  auto row_glob = [&](int f) {
+    const int p = max(crow[min(16 * f + lr, nc - 1)], 0);
+    return PAGED ? (int)km.row(b, p) : p;
+  };
+  auto fetch = [&](KeyFrag<kFp8>& kf, float& sc, int row) {
+    sc = ksb[row];
+    kf.load(kb + (int64_t)row * kD, kg);
+  };
+  constexpr int S = 4;  // fragment stride between the waves
+  const int nfrag = (nc + 15) >> 4;
+  int f = wave;
+  KeyFrag<kFp8> k0, k1, k2;
+  float s0, s1, s2;
+  fetch(k0, s0, row_glob(f));
+  fetch(k1, s1, row_glob(f + S));
+  fetch(k2, s2, row_glob(f + 2 * S));
+  const uint8_t* rows[R];
+  const float* wrows[R];
+  const uint8_t* lrows[R];
+  const float* lsc[R];
+  float qs[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int64_t row = r0 + min(r, gs - 1);
+    rows[r] = q + row * Tile::ROW_BYTES;
+    wrows[r] = w + row * kH;
+    qs[r] = q_scale[row];
+    lrows[r] = lin + row * kLinBytes;
+    lsc[r] = lin_scale + row * kLinLevels;
+  }
+  Tile tile;
+  tile.load(rows, wrows, qs, lrows, lsc, lane);
+  const int qr = kg / Tile::G;
+  const bool writer = (kg % Tile::G) == 0 && qr < gs;
+  uint16_t* my_sc = ssc + qr * kFuseCand;
+  auto emit = [&](float acc, float ks, int ff) {
+    const int slot = 16 * ff + lr;
+    if (writer && slot < nc) my_sc[slot] = bf16_rne(acc * ks);
+  };
+  __syncthreads();  // positions staged
+  for (; f < nfrag; f += 3 * S) {
+    emit(tile.score(k0), s0, f);
+    fetch(k0, s0, row_lds(f + 3 * S));
+    emit(tile.score(k1), s1, f + S);
+    fetch(k1, s1, row_lds(f + 4 * S));
+    emit(tile.score(k2), s2, f + 2 * S);
+    fetch(k2, s2, row_lds(f + 5 * S));
+  }
+  __syncthreads();  // scores staged
+
+  if (wave >= gs) return;
+  int32_t* orow = out_idx + (r0 + wave) * m;
+  if (nc <= m) {  // every usable slot is selected
+    for (int p = lane; p < m; p += 64) orow[p] = p < nc ? spos[p] : -1;
+    return;
+  }
+  const uint16_t* row_sc = ssc + wave * kFuseCand;
+  uint32_t key[NV];
+  int32_t pos[NV];
+#pragma unroll
+  for (int v = 0; v < NV; ++v) {
+    const int e = lane + 64 * v;
+    const bool in = e < nc;
+    const int32_t p = in ? spos[e] : -1;
+    const uint32_t k16 = float_key(__uint_as_float((uint32_t)(in ? row_sc[e] : 0) << 16)) >> 16;
+    key[v] = p >= 0 ? k16 + 1u : 0u;
+    pos[v] = p;
+  }
+  auto count = [&](auto pred) {
+    int n = 0;
+#pragma unroll
+    for (int v = 0; v < NV; ++v) n += __popcll(__ballot(pred(v)));
+    return n;
+  };
+  // the row's m outputs through a range-checked resource: lanes without an
+  // entry store past its end (dropped), so no per-element branches
+  const __amdgpu_buffer_rsrc_t orr = buffer_rsrc(orow, (uint32_t)m * 4u);
+  auto emit_sel = [&](auto pred, int base) {  // compacts the chosen positions into orow[base ..]
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      const bool take = pred(v);
+      const uint64_t bal = __ballot(take);
+      const int below = __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0));
+      __builtin_amdgcn_raw_buffer_store_b32(pos[v], orr, take ? 4u * (uint32_t)(base + below) : 0xFFFFFFFFu, 0, 0);
+      base += __popcll(bal);
+    }
+    return base;
+  };
+  auto wave_sum = [](int n) {
+    for (int o = 32; o > 0; o >>= 1) n += __shfl_xor(n, o, 64);
+    return n;
+  };
+  auto wave_max = [](int32_t x) {
+    for (int o = 32; o > 0; o >>= 1) x = max(x, __shfl_xor(x, o, 64));
+    return x;
+  };
+  int n_valid = 0;
+#pragma unroll
+  for (int v = 0; v < NV; ++v) n_valid += key[v] != 0u ? 1 : 0;
+  n_valid = wave_sum(n_valid);
+  if (n_valid <= m) {  // every usable candidate, then padding
+    const int n = emit_sel([&](int v) { return key[v] != 0u; }, 0);
+    for (int p = n + lane; p < m; p += 64) orow[p] = -1;
+    return;
+  }
+  // Two radix passes over a 256-bin histogram of this wave's own (LDS
+  // atomics; a wave's LDS operations complete in order): the high byte of
+  // k16 = key - 1, then the low byte among keys in the chosen high bin.
+  uint32_t* hist = shist + wave * 257;
+  auto wave_sync = [] {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  };
+  // the bin b with count(digit > b) < need <= count(digit >= b); returns b
+  // and sets `above` = count(digit > b), `in_bin` = count(digit == b)
+  auto pick = [&](int need_here, int& above, int& in_bin) {
+    uint32_t h[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) h[i] = hist[4 * lane + i];
+    const int blk = (int)(h[0] + h[1] + h[2] + h[3]);
+    int suf = blk;  // bins 4 lane .. 255
+    for (int o = 1; o < 64; o <<= 1) {
+      const int t = __shfl_down(suf, o, 64);
+      if (lane + o < 64) suf += t;
+    }
+    int over = suf - blk, bin = -1, ab = 0, ib = 0;  // over: bins above this lane's four
+#pragma unroll
+    for (int i = 3; i >= 0; --i) {
+      if (bin < 0 && over < need_here && over + (int)h[i] >= need_here) {
+        bin = 4 * lane + i;
+        ab = over;
+        ib = (int)h[i];
+      }
+      over += (int)h[i];
+    }
+    const uint64_t who = __ballot(bin >= 0);
+    const int src = (int)__builtin_ctzll(who);
+    above = __shfl(ab, src, 64);
+    in_bin = __shfl(ib, src, 64);
+    return __shfl(bin, src, 64);
+  };
+  // (bin 256 takes the entries a pass skips, so every lane adds every time)
+#pragma unroll
+  for (int i = 0; i < 4; ++i) hist[4 * lane + i] = 0u;
+  wave_sync();
+#pragma unroll
+  for (int v = 0; v < NV; ++v) atomicAdd(&hist[key[v] != 0u ? (key[v] - 1u) >> 8 : 256u], 1u);
+  wave_sync();
+  int above1, in1;
+  const int hb = pick(m, above1, in1);
+  wave_sync();
+#pragma unroll
+  for (int i = 0; i < 4; ++i) hist[4 * lane + i] = 0u;
+  wave_sync();
+  const uint32_t khb = ((uint32_t)hb << 8) + 1u;  // the high bin's keys: khb .. khb + 255
+#pragma unroll
+  for (int v = 0; v < NV; ++v) atomicAdd(&hist[key[v] - khb < 256u ? key[v] - khb : 256u], 1u);
+  wave_sync();
+  int above2, ties;
+  const int lb = pick(m - above1, above2, ties);
+  const uint32_t K = (uint32_t)((hb << 8) | lb) + 1u;
+  const int n_gt = above1 + above2;  // < m entries above K, all taken
+  const int need = m - n_gt;         // >= 1 of the `ties` entries of key K
+  emit_sel([&](int v) { return key[v] > K; }, 0);
+  // from here key[v] holds the position of a tied entry, else INT32_MAX
+#pragma unroll
+  for (int v = 0; v < NV; ++v) key[v] = key[v] == K ? (uint32_t)pos[v] : 0x7FFFFFFFu;
+  int32_t P = 0x7FFFFFFE;  // every tie when they are exactly enough (positions < 2^31 - 1)
+  if (ties > need) {
+    // the tied positions, compacted into this wave's score row (read into
+    // registers above, so free) when they fit, else searched in registers
+    int32_t* tl = reinterpret_cast<int32_t*>(ssc + wave * kFuseCand);
+    constexpr int kTieCap = kFuseCand / 2 - 1;
+    int32_t top = -1;
+#pragma unroll
+    for (int v = 0; v < NV; ++v) top = max(top, key[v] != 0x7FFFFFFFu ? (int32_t)key[v] : -1);
+    top = wave_max(top);
+    const bool listed = ties <= kTieCap;
+    if (listed) {
+      wave_sync();
+      int base = 0;
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        const bool t = key[v] != 0x7FFFFFFFu;
+        const uint64_t bal = __ballot(t);
+        const int below =
+            __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0));
+        tl[t ? base + below : kTieCap] = (int32_t)key[v];  // slot kTieCap: a sink for the others
+        base += __popcll(bal);
+      }
+      wave_sync();
+    }
+    // P: count(tied, pos <= plo) < need <= count(tied, pos <= phi)
+    int64_t plo = -1, phi = top;
+    while (phi - plo > 1) {
+      const int32_t mid = (int32_t)(plo + ((phi - plo) >> 1));
+      int n = 0;
+      if (listed) {
+        for (int e = lane; e < ties; e += 64) n += tl[e] <= mid;
+        n = wave_sum(n);
+      } else {
+        n = count([&](int v) { return (int32_t)key[v] <= mid; });
+      }
+      if (n >= need) phi = mid;
+      else plo = mid;
+    }
+    P = (int32_t)phi;
+  }
+  emit_sel([&](int v) { return (int32_t)key[v] <= P; }, n_gt);
 }
 
 // (key, position) pairs held in registers: entry 4 q + u is element
@@ -395,9 +678,29 @@ hipError_t launch_short(const E* rescore, const int32_t* cand, int g, const SeqT
 hipError_t launch_refine(int dtype, const void* q, const float* q_scale, const float* w, const uint8_t* lin,
                          const float* lin_scale, int g, const void* k, const float* k_scale, const KeyMap& km,
                          const SeqTable& st, int j0, int j1, const int32_t* cand, int c, int W, int wslot, int m,
-                         void* rescore, int32_t* out_idx, hipStream_t stream) {
+                         void* rescore, int32_t* out_idx, int path, hipStream_t stream) {
   if (j1 <= j0 || st.n <= 0) return hipSuccess;
   if (c > kMaxCand) return hipErrorInvalidValue;
+  // the fused re-score and select on request, where it applies.  Not the
+  // default: at two workgroups per CU (the 4-row tile's registers) a group's
+  // member selects cannot hide their latency behind other groups' scoring,
+  // and the split path (many small select workgroups per CU) is faster.
+  const bool fusable = dtype == kFp8 && W == 0 && g <= 4 && c <= kFuseCand;
+  if (fusable && path == PIVOT_REFINE_FUSED) {
+    const dim3 grid((unsigned)(j1 - j0), (unsigned)st.n);
+#define PIVOT_FUSED(RV, PG)                                                                                         \
+  hipLaunchKernelGGL((rescore_select_kernel<RV, PG>), grid, dim3(256), 0, stream, (const uint8_t*)q, q_scale, w, lin, \
+                     lin_scale, g, (const uint8_t*)k, k_scale, km, st, j0, cand, c, m, out_idx)
+    if (g > 2) {
+      if (km.pages) PIVOT_FUSED(4, true);
+      else PIVOT_FUSED(4, false);
+    } else {
+      if (km.pages) PIVOT_FUSED(2, true);
+      else PIVOT_FUSED(2, false);
+    }
+#undef PIVOT_FUSED
+    return hipGetLastError();
+  }
   const SlotRule rule{W, wslot};
   const int all_slots = W > 0;
   // few groups (decode): split the candidates so the launch still fills the GPU;

@@ -114,8 +114,9 @@ def test_group_validation(mode, g, c, status):
     assert group(args(), mode, g, c) == status
 
 
-def opts(mode=pv.PIVOT_REFINE, g=4, c=16, db=-1, window=0, kind=pv.PIVOT_WINDOW_SHARED, agg=pv.PIVOT_AGG_MEAN):
-    return pv.group_opts(mode, g, c, db, window, kind, agg)
+def opts(mode=pv.PIVOT_REFINE, g=4, c=16, db=-1, window=0, kind=pv.PIVOT_WINDOW_SHARED, agg=pv.PIVOT_AGG_MEAN,
+         path=pv.PIVOT_REFINE_AUTO):
+    return pv.group_opts(mode, g, c, db, window, kind, agg, refine_path=path)
 
 
 def group_opts(a, o):
@@ -135,6 +136,10 @@ def group_opts(a, o):
     (dict(c=8100, window=100, kind=pv.PIVOT_WINDOW_PER_QUERY), pv.PIVOT_ERR_UNSUPPORTED),  # 8203 slots
     (dict(c=16, window=13), pv.PIVOT_ERR_WORKSPACE),                               # c == W + g - 1: valid
     (dict(mode=pv.PIVOT_DENSE), pv.PIVOT_ERR_INVALID_ARG),
+    (dict(path=3), pv.PIVOT_ERR_INVALID_ARG),
+    (dict(path=-1), pv.PIVOT_ERR_INVALID_ARG),
+    (dict(path=pv.PIVOT_REFINE_FUSED), pv.PIVOT_ERR_WORKSPACE),                    # valid: reaches the workspace check
+    (dict(path=pv.PIVOT_REFINE_SPLIT), pv.PIVOT_ERR_WORKSPACE),
 ])
 def test_group_opts_validation(kw, status):
     assert group_opts(args(ws_bytes=0), opts(**kw)) == status
