@@ -4,6 +4,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <atomic>
 #include <mutex>
 #include <vector>
 
@@ -41,8 +42,9 @@ struct ProfRecord {
   hipEvent_t start, stop;
 };
 std::mutex g_prof_mu;
-bool g_prof_on = false;
-uint32_t g_prof_mask = 0;  // kernel kinds bracketed while a profile runs
+// read without the lock on every launch; written under g_prof_mu
+std::atomic<bool> g_prof_on{false};
+std::atomic<uint32_t> g_prof_mask{0};  // kernel kinds bracketed while a profile runs
 std::vector<ProfRecord> g_prof_recs;
 std::vector<hipEvent_t> g_prof_pool;
 
@@ -60,8 +62,10 @@ hipEvent_t prof_event() {
 // Run one launcher; with profiling on, bracket it with events on `stream`.
 template <class F>
 hipError_t timed(int kind, hipStream_t stream, F launch) {
-  if (!g_prof_on || !((g_prof_mask >> kind) & 1u)) return launch();
+  if (!g_prof_on.load(std::memory_order_relaxed) || !((g_prof_mask.load(std::memory_order_relaxed) >> kind) & 1u))
+    return launch();
   std::lock_guard<std::mutex> lk(g_prof_mu);
+  if (!g_prof_on.load(std::memory_order_relaxed)) return launch();  // ended meanwhile
   ProfRecord r{kind, prof_event(), prof_event()};
   if (!r.start || !r.stop) return hipErrorOutOfMemory;
   hipError_t e = hipEventRecord(r.start, stream);

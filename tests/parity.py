@@ -8,21 +8,59 @@ domain D) and GPU set G, both padded with -1:
     O \\ G has f(s) <= tau + tol.
 rtol is 2e-3 for bf16 inputs and 2e-2 for fp8 inputs (scores compared with the
 fp64 oracle).  Scores are only computed for rows whose sets differ.
+
+Besides the tolerance, the swaps must fit the error model of the path
+(SWAP_BOUND, relative to |tau|): with fp8 inputs the GPU ranks bf16-rounded
+scores (unit roundoff 2^-8), so two scores change order only when their exact
+values lie within 2 * 2^-8 of each other, plus at most 2e-3 for the fp8
+linear term's last residual and the fp32 sums; bf16 inputs rank fp32 sums.
 """
 from __future__ import annotations
 
 import numpy as np
 
 RTOL = {"bf16": 2e-3, "fp8": 2e-2}
+SWAP_BOUND = {"bf16": 1e-4, "fp8": 2 * 2.0 ** -8 + 2e-3}
 
 
 class ParityError(AssertionError):
     pass
 
 
-def check_row(gpu, ora, f_of, rtol, in_domain, label=""):
+class Budget:
+    """How much of the tolerance the checked rows used: rows checked, rows
+    whose set differs from the oracle's, boundary swaps (GPU entries outside
+    the oracle set), the most swaps in one row, and the largest |f - tau| /
+    |tau| over swapped entries (compare with rtol)."""
+
+    def __init__(self):
+        self.rows = self.rows_diff = self.swaps = self.max_row_swaps = 0
+        self.max_rel = 0.0
+        self.worst = 0.0  # largest max_rel / SWAP_BOUND of the rows' format
+
+    def add(self, swaps, rel, bound=None):
+        self.rows += 1
+        if swaps:
+            self.rows_diff += 1
+            self.swaps += swaps
+            self.max_row_swaps = max(self.max_row_swaps, swaps)
+            self.max_rel = max(self.max_rel, rel)
+            if bound:
+                self.worst = max(self.worst, rel / bound)
+
+    def summary(self):
+        return (f"{self.rows} rows, {self.rows_diff} not identical to the oracle's set, {self.swaps} boundary "
+                f"swaps (at most {self.max_row_swaps} in a row), largest |f - tau|/|tau| of a swapped entry "
+                f"{self.max_rel:.2e}")
+
+
+BUDGET = Budget()  # accumulated by check_row; tests reset and report it
+
+
+def check_row(gpu, ora, f_of, rtol, in_domain, label="", swap_bound=None):
     """gpu, ora: int arrays (-1 padded); f_of(idx array) -> oracle fp64 scores;
-    in_domain(idx array) -> bool array.  Returns the number of boundary swaps."""
+    in_domain(idx array) -> bool array; swap_bound: the path's SWAP_BOUND,
+    recorded in BUDGET.  Returns the number of boundary swaps."""
     gpu = np.asarray(gpu)
     ora = np.asarray(ora)
     G = gpu[gpu >= 0]
@@ -37,6 +75,7 @@ def check_row(gpu, ora, f_of, rtol, in_domain, label=""):
         raise ParityError(f"{label}: indices outside the domain: {G[~in_domain(G)][:5]}")
     sg, so = set(G.tolist()), set(O.tolist())
     if sg == so:
+        BUDGET.add(0, 0.0)
         return 0
     extra = np.array(sorted(sg - so), dtype=np.int64)
     missing = np.array(sorted(so - sg), dtype=np.int64)
@@ -47,6 +86,8 @@ def check_row(gpu, ora, f_of, rtol, in_domain, label=""):
     if (fe < tau - tol).any() or (fm > tau + tol).any():
         raise ParityError(f"{label}: tau={tau:.6g} tol={tol:.3g}; extra f={np.sort(fe)[:4]}, "
                           f"missing f={np.sort(fm)[-4:]}")
+    dev = max(float(np.max(tau - fe, initial=0.0)), float(np.max(fm - tau, initial=0.0)))
+    BUDGET.add(len(extra), dev / abs(tau) if tau != 0 else 0.0, swap_bound)
     return len(extra)
 
 
@@ -66,6 +107,7 @@ def check_pivot(fmt, q, qs, w, p0, k, ks, n_k, *, mode, g, c, topk, dense_below,
     import oracle
 
     rtol = RTOL[fmt]
+    sb = SWAP_BOUND[fmt]
     n_q = q.shape[0]
     if mode == oracle.DENSE:
         g, db = 1, n_k + 1
@@ -90,7 +132,7 @@ def check_pivot(fmt, q, qs, w, p0, k, ks, n_k, *, mode, g, c, topk, dense_below,
             for r in rows:
                 t = p0 + r
                 swaps += check_row(gpu_idx[r], res["idx"][r], member_scores(r), rtol,
-                                   lambda idx, t=t: (idx >= 0) & (idx <= t), f"{label} dense row {r}")
+                                   lambda idx, t=t: (idx >= 0) & (idx <= t), f"{label} dense row {r}", swap_bound=sb)
             if mode == oracle.REFINE and gpu_cand is not None:
                 if not (gpu_cand[j] == -1).all():
                     raise ParityError(f"{label}: guardrail group {j} has candidates")
@@ -105,19 +147,21 @@ def check_pivot(fmt, q, qs, w, p0, k, ks, n_k, *, mode, g, c, topk, dense_below,
 
         if mode == oracle.REUSE:
             for r in rows:
-                swaps += check_row(gpu_idx[r], res["idx"][r], fbar, rtol, dom0, f"{label} reuse row {r}")
+                swaps += check_row(gpu_idx[r], res["idx"][r], fbar, rtol, dom0, f"{label} reuse row {r}",
+                                   swap_bound=sb)
             continue
         if window > 0:
             swaps += _check_window_group(fmt, q, qs, w, k, ks, rows, t0, gs, c, g, topk, window, window_kind,
                                          gpu_idx, gpu_cand[j], res["cand"][j], fbar, rtol, member_scores,
                                          f"{label} group {j}")
             continue
-        swaps += check_row(gpu_cand[j], res["cand"][j], fbar, rtol, dom0, f"{label} candidates of group {j}")
+        swaps += check_row(gpu_cand[j], res["cand"][j], fbar, rtol, dom0, f"{label} candidates of group {j}",
+                           swap_bound=sb)
         C = gpu_cand[j][gpu_cand[j] >= 0]
         ref2 = oracle.refine_on(fmt, q[rows], None if qs is None else qs[rows], w[rows], k, ks, C, topk)
         for u, r in enumerate(rows):
             swaps += check_row(gpu_idx[r], ref2[u], member_scores(r), rtol,
-                               lambda idx, C=C: np.isin(idx, C), f"{label} refine row {r}")
+                               lambda idx, C=C: np.isin(idx, C), f"{label} refine row {r}", swap_bound=sb)
     return swaps
 
 
@@ -126,6 +170,7 @@ def _check_window_group(fmt, q, qs, w, k, ks, rows, t0, gs, c, g, topk, W, kind,
     """One Refine group with App. B's window (see check_pivot)."""
     import oracle
 
+    sb = SWAP_BOUND[fmt]
     wg = W + g - 1
     per_query = kind == oracle.WINDOW_PER_QUERY
     npx = c if per_query else c - wg                      # the proxy's slots
@@ -134,7 +179,7 @@ def _check_window_group(fmt, q, qs, w, k, ks, rows, t0, gs, c, g, topk, W, kind,
     swaps = 0
     if npx > 0:
         swaps += check_row(gcand[:npx], ocand[:npx], fbar, rtol, lambda idx: (idx >= 0) & (idx <= hi),
-                           f"{label} proxy slots")
+                           f"{label} proxy slots", swap_bound=sb)
     pool = set(gcand[:npx][gcand[:npx] >= 0].tolist())
     want = []
     for u in range(wg):
@@ -150,5 +195,5 @@ def _check_window_group(fmt, q, qs, w, k, ks, rows, t0, gs, c, g, topk, W, kind,
         C = np.array(use, dtype=np.int32)
         ref = oracle.refine_on(fmt, q[[r]], None if qs is None else qs[[r]], w[[r]], k, ks, C, topk)[0]
         swaps += check_row(gpu_idx[r], ref, member_scores(r), rtol, lambda idx, C=C: np.isin(idx, C),
-                           f"{label} window refine row {r}")
+                           f"{label} window refine row {r}", swap_bound=sb)
     return swaps

@@ -10,10 +10,22 @@ import torch
 import oracle
 import paper_2607_24593_amd as pv
 from gpu_util import dev, host, say
+import parity
 from parity import check_pivot
 from workload.gen import WORKLOADS, make
 
 pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def tolerance_budget(request):
+    """Reports, per test, how many checked rows differ from the oracle's set
+    and how much of the tolerance their boundary swaps used, and requires the
+    swaps to fit the path's error model (parity.SWAP_BOUND), not just rtol."""
+    parity.BUDGET = parity.Budget()
+    yield
+    say("tolerance budget", request.node.name, parity.BUDGET.summary())
+    assert parity.BUDGET.worst <= 1.0, ("boundary swaps beyond the error model", parity.BUDGET.summary())
 
 MODES = {"dense": oracle.DENSE, "reuse": oracle.REUSE, "refine": oracle.REFINE}
 

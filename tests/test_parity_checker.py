@@ -75,3 +75,24 @@ def test_shared_proxy_slot_past_its_range_is_caught(x):
     proxy[np.argmin(proxy)] = t0 - W + 1       # a union position in a proxy slot
     with pytest.raises(ParityError):
         _check(x, res, shape, W, kind, cand=cand)
+
+
+def test_budget_records_swaps_against_the_error_model():
+    """A boundary swap inside rtol is accepted; the budget records its distance
+    from tau relative to the path's error model, so one beyond the model (but
+    inside rtol) is visible and a full-size test can reject it."""
+    import parity
+    f = {0: 10.0, 1: 9.0, 2: 8.0, 3: 7.97, 4: 7.9}  # oracle top-3 = {0, 1, 2}, tau = 8.0
+    f_of = lambda idx: np.array([f[int(i)] for i in idx], dtype=np.float64)  # noqa: E731
+    dom = lambda idx: np.ones(len(idx), bool)  # noqa: E731
+    ora = np.array([0, 1, 2])
+    bound = parity.SWAP_BOUND["fp8"]
+    parity.BUDGET = parity.Budget()
+    assert parity.check_row(np.array([0, 1, 2]), ora, f_of, 2e-2, dom, swap_bound=bound) == 0
+    assert parity.check_row(np.array([0, 1, 3]), ora, f_of, 2e-2, dom, swap_bound=bound) == 1   # 0.375% below tau
+    assert parity.BUDGET.rows == 2 and parity.BUDGET.rows_diff == 1
+    assert abs(parity.BUDGET.max_rel - 0.03 / 8.0) < 1e-12 and parity.BUDGET.worst <= 1.0
+    assert parity.check_row(np.array([0, 1, 4]), ora, f_of, 2e-2, dom, swap_bound=bound) == 1   # 1.25%: inside rtol
+    assert parity.BUDGET.worst > 1.0
+    with pytest.raises(ParityError):
+        parity.check_row(np.array([0, 1, 4]), ora, f_of, 1e-2, dom)                             # outside rtol
