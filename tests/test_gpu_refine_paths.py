@@ -99,3 +99,22 @@ def test_fused_paged_equals_split():
             dev(x.q[p0:p0 + n_q]), dev(x.q_scale[p0:p0 + n_q]), dev(x.w[p0:p0 + n_q]), dev(pool), dev(pool_s),
             [p0], [p0 + n_q], 1024, lay, mode=pv.PIVOT_REFINE, g=4, c=2048, refine_path=path))
     _same_sets(outs[pv.PIVOT_REFINE_FUSED], outs[pv.PIVOT_REFINE_SPLIT], "paged")
+
+
+@pytest.mark.parametrize("case", ["bf16", "window"])
+def test_fused_request_outside_its_scope_takes_the_split_path(case):
+    """PIVOT_REFINE_FUSED applies to fp8 groups without a window; a bf16 call
+    or a windowed one asking for it runs the split path and returns its sets."""
+    fmt = "bf16" if case == "bf16" else "fp8"
+    x = make_prefill(3000, fmt, seed=64, threads=8)
+    p0, n_q, g, c, topk = 1000, 2000, 4, 1024, 256
+    n_k = p0 + n_q
+    W = 4 if case == "window" else 0
+    outs = {}
+    for path in (pv.PIVOT_REFINE_FUSED, pv.PIVOT_REFINE_SPLIT):
+        say("out-of-scope fused request", case, "path", path)
+        outs[path] = host(pv.pivot_group_index_opts(
+            dev(x.q[p0:n_k]), dev(None if x.q_scale is None else x.q_scale[p0:n_k]), dev(x.w[p0:n_k]),
+            dev(x.k[:n_k]), dev(None if x.k_scale is None else x.k_scale[:n_k]), p0, n_k, topk,
+            mode=pv.PIVOT_REFINE, g=g, c=c, window=W, refine_path=path))
+    _same_sets(outs[pv.PIVOT_REFINE_FUSED], outs[pv.PIVOT_REFINE_SPLIT], case)
