@@ -457,7 +457,7 @@ def cpu_model():
 
 
 # The paper's own indexer speedups (NVIDIA H20, DeepSeek-V3.2 / GLM-5.1
-# activations): reported beside this build's numbers as context, not as a
+# activations): reported beside this library's numbers as context, not as a
 # target (other hardware, other inputs).
 PAPER_CONTEXT = {
     "hardware": "NVIDIA H20",
@@ -539,7 +539,7 @@ def main():
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for {max(args.gpus, world)})",
+        print(f"bench.py measures one GPU: this library has no multi-GPU path (asked for {max(args.gpus, world)})",
               file=sys.stderr)
         sys.exit(2)
 

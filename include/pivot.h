@@ -49,7 +49,7 @@ extern "C" {
 typedef enum {
   PIVOT_OK = 0,
   PIVOT_ERR_INVALID_ARG = 1,  /* null pointer, inconsistent size or parameter */
-  PIVOT_ERR_UNSUPPORTED = 2,  /* shape or dtype this build does not specialise */
+  PIVOT_ERR_UNSUPPORTED = 2,  /* shape or dtype this library does not specialise */
   PIVOT_ERR_WORKSPACE = 3,    /* workspace_bytes below pivot_workspace_size() */
   PIVOT_ERR_HIP = 4           /* a HIP launch failed; see pivot_last_error() */
 } pivot_status;
@@ -60,7 +60,7 @@ typedef enum { PIVOT_REUSE = 0, PIVOT_REFINE = 1 } pivot_mode;
 
 /* Passed as `mode` to pivot_workspace_size() for a dense call. */
 #define PIVOT_DENSE (-1)
-/* Keys per sequence (and score row length) this build handles: 2^27.  The
+/* Keys per sequence (and score row length) this library handles: 2^27.  The
  * scoring kernel addresses four score rows through one 32-bit range. */
 #define PIVOT_MAX_KEYS (1 << 27)
 

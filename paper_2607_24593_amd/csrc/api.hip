@@ -140,7 +140,7 @@ pivot_status check_args(const pivot_args* a, const pivot_layout* l, std::vector<
   if (a->dtype != PIVOT_DT_BF16 && a->dtype != PIVOT_DT_FP8_E4M3)
     return fail(PIVOT_ERR_UNSUPPORTED, "dtype %d not supported", a->dtype);
   if (a->heads != kH || a->dim != kD)
-    return fail(PIVOT_ERR_UNSUPPORTED, "heads=%d dim=%d: this build specialises H=64, d=128", a->heads, a->dim);
+    return fail(PIVOT_ERR_UNSUPPORTED, "heads=%d dim=%d: this library specialises H=64, d=128", a->heads, a->dim);
   if (a->batch < 1) return fail(PIVOT_ERR_INVALID_ARG, "batch must be >= 1");
   if (a->topk < 1) return fail(PIVOT_ERR_INVALID_ARG, "topk must be >= 1");
   if (!a->q_pos0 || !a->n_k) return fail(PIVOT_ERR_INVALID_ARG, "q_pos0 and n_k (host arrays) are required");

@@ -6,7 +6,7 @@
 
 namespace pivot {
 
-constexpr int kH = 64;        // indexer heads (the only H this build specialises)
+constexpr int kH = 64;        // indexer heads (the only H this library specialises)
 constexpr int kD = 128;       // head dimension
 constexpr int kMaxSeq = 64;   // sequences per launch (the host splits larger batches)
 constexpr int kWave = 64;     // CDNA wavefront size
