@@ -220,6 +220,20 @@ __device__ void block_select(const Src& src, uint32_t need, SelectShared& sh, Pu
 // LDS word.
 constexpr int kBucketList = 256;
 
+// bucket_select's emission pass: elements of buckets above bsel go out
+// through put (one LDS atomic per wave and element, wave_append), members of
+// bucket bsel go to list(key, pos).  Sources with a faster form overload it
+// (found by argument-dependent lookup).
+template <class Src, class Bk, class Put, class List>
+__device__ __forceinline__ void emit_bucket(const Src& src, Bk bucket, int bsel, SelectShared& sh, Put put,
+                                            List list) {
+  src.visit([&](uint32_t key, int32_t pos) {
+    const int bk = bucket(key);
+    wave_append(bk > bsel, &sh.emitted, [&](int slot) { put(slot, pos); });
+    if (bk == bsel) list(key, pos);
+  });
+}
+
 template <int THREADS, int NB = 4096, class Src, class Put>
 __device__ bool bucket_select(const Src& src, uint32_t need, uint32_t* hist, uint32_t* lkey, int32_t* lpos,
                               int32_t* lcount, SelectShared& sh, Put put) {
@@ -245,14 +259,10 @@ __device__ bool bucket_select(const Src& src, uint32_t need, uint32_t* hist, uin
   const uint32_t rem = need - sh.before, in_b = sh.equal;
   __syncthreads();
   if (in_b > (uint32_t)kBucketList) return false;
-  src.visit([&](uint32_t key, int32_t pos) {
-    const int bk = bucket(key);
-    wave_append(bk > bsel, &sh.emitted, [&](int slot) { put(slot, pos); });
-    if (bk == bsel) {  // a few elements: a plain LDS atomic
-      const int c = atomicAdd(lcount, 1);
-      lkey[c] = key;
-      lpos[c] = pos;
-    }
+  emit_bucket(src, bucket, bsel, sh, put, [&](uint32_t key, int32_t pos) {  // a few elements: a plain LDS atomic
+    const int c = atomicAdd(lcount, 1);
+    lkey[c] = key;
+    lpos[c] = pos;
   });
   __syncthreads();
   // rank of each listed member = members ranking above it; G threads share a

@@ -476,6 +476,39 @@ struct RegSource {
   }
 };
 
+// bucket_select's emission for pairs held in registers: the taken entries of
+// a lane form a bit mask, the wave reserves its slots with ONE LDS atomic,
+// and each entry index then goes out with a ballot prefix (consecutive slots
+// per store, as with wave_append, without an atomic per entry).
+template <int V, class Bk, class Put, class List>
+__device__ __forceinline__ void emit_bucket(const RegSource<V>& src, Bk bucket, int bsel, SelectShared& sh,
+                                            Put put, List list) {
+  static_assert(V <= 32, "one mask word");
+  uint32_t take = 0;
+#pragma unroll
+  for (int v = 0; v < V; ++v) {
+    if (src.pos[v] < 0) continue;
+    const int bk = bucket(src.key[v]);
+    take |= (bk > bsel ? 1u : 0u) << v;
+    if (bk == bsel) list(src.key[v], src.pos[v]);
+  }
+  int total = 0;
+#pragma unroll
+  for (int v = 0; v < V; ++v) total += __popcll(__ballot((take >> v) & 1u));
+  if (total == 0) return;  // uniform
+  int base = 0;
+  if ((threadIdx.x & 63) == 0) base = atomicAdd(&sh.emitted, total);
+  base = __shfl(base, 0, 64);
+#pragma unroll
+  for (int v = 0; v < V; ++v) {
+    const bool t = (take >> v) & 1u;
+    const uint64_t bal = __ballot(t);
+    if (t) put(base + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u)),
+               src.pos[v]);
+    base += __popcll(bal);
+  }
+}
+
 // Candidate slots a member may use (App. B): slots >= wslot are per-query
 // window slots with the lower bound t - W + 1; window == 0 means a plain
 // candidate row whose first min(c, t0 + 1) slots are all usable.
