@@ -418,17 +418,33 @@ struct Rows16Lds {
   static_assert((int)sizeof(TwoLevelShared<CAP2>) <= RAW, "fallback fits the region");
 };
 
-// The 16-bit order-preserving keys of the 8 bf16 scores of a 16-byte vector,
-// two per word (key16_expand(k) == float_key(score)).
+// The 16-bit order-preserving keys of the two bf16 scores of a word
+// (key16_expand(k) == float_key(score)), without branches: a half with its
+// sign bit set is complemented, any other gets its sign bit set; -0 (0x8000)
+// then lands on 0x7FFF, one below +0's key 0x8000, and is moved up to it.
 __device__ __forceinline__ uint32_t key16_pair(uint32_t w) {
-  uint32_t out = 0;
-#pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const uint32_t b = (w >> (16 * h)) & 0xFFFFu;
-    const uint32_t k = (b & 0x7FFFu) == 0 ? 0x8000u : ((b & 0x8000u) ? (~b & 0xFFFFu) : (b | 0x8000u));
-    out |= k << (16 * h);
-  }
-  return out;
+  const uint32_t t = (w >> 15) & 0x00010001u;  // the sign of each half in its bit 0
+  const uint32_t k = w ^ (t * 0x7FFFu | 0x80008000u);
+  return k + (((k & 0xFFFFu) == 0x7FFFu ? 1u : 0u) | ((k >> 16) == 0x7FFFu ? 0x10000u : 0u));
+}
+
+// The 16-bit order key of one bf16 value (key16_pair of one half).
+__device__ __forceinline__ uint32_t key16_one(uint32_t h) {
+  const uint32_t k = h ^ ((h & 0x8000u) ? 0xFFFFu : 0x8000u);
+  return k + (k == 0x7FFFu ? 1u : 0u);
+}
+
+// Inclusive prefix sum over the 64 lanes of a wave: row shifts within each
+// row of 16 lanes, then row broadcasts of lanes 15 and 31 (DPP: no LDS round
+// trips, unlike a shuffle ladder).
+__device__ __forceinline__ uint32_t wave_incl_sum(uint32_t x) {
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xF, 0xF, true);   // row_shr:1
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xF, 0xF, true);   // row_shr:2
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xF, 0xF, true);   // row_shr:4
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xF, 0xF, true);   // row_shr:8
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xA, 0xF, false);  // row_bcast:15 -> rows 1, 3
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xC, 0xF, false);  // row_bcast:31 -> rows 2, 3
+  return x;
 }
 
 // The sampled keys of bf16 rows, packed two per register: V 16-byte vectors
@@ -509,15 +525,10 @@ __device__ __forceinline__ int stream_compact16(const bf16_t* row, int n, float 
   // writes its own keys, vector by vector, a loop over its set bits (rarely
   // more than two per vector).
   auto append = [&](const uint4 (&a)[U], uint32_t bits, int q0) {
-    const int cnt = __popc(bits);
-    int incl = cnt;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const int t = __shfl_up(incl, o, 64);
-      if (lane >= o) incl += t;
-    }
-    int slot = wc + incl - cnt;
-    wc += __shfl(incl, 63, 64);
+    const uint32_t cnt = (uint32_t)__popc(bits);
+    const uint32_t incl = wave_incl_sum(cnt);
+    int slot = wc + (int)(incl - cnt);
+    wc += __builtin_amdgcn_readlane((int)incl, 63);
 #pragma unroll
     for (int u = 0; u < U; ++u) {  // a static vector index: its words stay in registers
       uint32_t mu = (bits >> (N * u)) & 0xFFu;
@@ -526,7 +537,7 @@ __device__ __forceinline__ int stream_compact16(const bf16_t* row, int n, float 
         const int j = __builtin_ctz(mu);
         mu &= mu - 1;
         const uint32_t h = (uint32_t)(((j & 4) ? hi : lo) >> (16 * (j & 3))) & 0xFFFFu;
-        const uint32_t k16 = (h & 0x7FFFu) == 0 ? 0x8000u : ((h & 0x8000u) ? (~h & 0xFFFFu) : (h | 0x8000u));
+        const uint32_t k16 = key16_one(h);
         atomicAdd(&hist[min(k16 - base16, (uint32_t)(kNB16 - 1))], 1u);
         if (slot < SEG) {
           mk[slot] = (uint16_t)k16;
