@@ -52,37 +52,44 @@ struct SelectShared {
   int32_t emitted;
 };
 
+// Inclusive prefix sum over the 64 lanes of a wave: row shifts within each
+// row of 16 lanes, then row broadcasts of lanes 15 and 31 (DPP: no LDS round
+// trips, unlike a shuffle ladder).
+__device__ __forceinline__ uint32_t wave_incl_sum(uint32_t x) {
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xF, 0xF, true);   // row_shr:1
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xF, 0xF, true);   // row_shr:2
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xF, 0xF, true);   // row_shr:4
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xF, 0xF, true);   // row_shr:8
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xA, 0xF, false);  // row_bcast:15 -> rows 1, 3
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xC, 0xF, false);  // row_bcast:31 -> rows 2, 3
+  return x;
+}
+
 // Find the digit d (of `bins`) where the running count crosses `rem`, scanning
-// digits downwards (desc) or upwards (!desc); every thread owns bins/THREADS
-// consecutive digits.  Writes sh.digit, sh.before (count strictly before d in
-// scan order) and sh.equal (count at d).  Contains workgroup barriers.
+// digits downwards (desc) or upwards (!desc).  Threads take the digits in scan
+// order, bins/THREADS consecutive ones each (one, or none, when bins is
+// smaller): with DESC thread 0 holds the highest digits, so one ascending
+// scan over the lanes and waves serves both directions.  Writes sh.digit,
+// sh.before (count strictly before d in scan order) and sh.equal (count at
+// d).  Contains workgroup barriers.
 template <int THREADS, bool DESC>
 __device__ __forceinline__ void find_digit(const uint32_t* hist, SelectShared& sh, uint32_t rem, int bins) {
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int per = bins / THREADS;  // bins is a multiple of THREADS, or smaller
-  const int lo = per > 0 ? per * tid : tid;
   const int cnt = per > 0 ? per : (tid < bins ? 1 : 0);
+  const int first = per > 0 ? (DESC ? bins - 1 - per * tid : per * tid) : (DESC ? bins - 1 - tid : tid);
+  auto digit = [&](int k) { return DESC ? first - k : first + k; };  // k-th digit of this thread in scan order
   uint32_t tot = 0;
-  for (int k = 0; k < cnt; ++k) tot += hist[lo + k];
-  uint32_t s = tot;  // inclusive scan over lanes in scan order
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    uint32_t t = DESC ? __shfl_down(s, o, 64) : __shfl_up(s, o, 64);
-    if (DESC ? (lane + o < 64) : (lane >= o)) s += t;
-  }
-  if (DESC ? lane == 0 : lane == 63) sh.wsum[wv] = s;
+  for (int k = 0; k < cnt; ++k) tot += hist[digit(k)];
+  const uint32_t s = wave_incl_sum(tot);
+  if (lane == 63) sh.wsum[wv] = s;
   __syncthreads();
   uint32_t before = s - tot;
-  if (DESC) {
-    for (int w = wv + 1; w < THREADS / 64; ++w) before += sh.wsum[w];
-  } else {
-    for (int w = 0; w < wv; ++w) before += sh.wsum[w];
-  }
-  for (int kk = 0; kk < cnt; ++kk) {
-    const int k = DESC ? cnt - 1 - kk : kk;
-    const uint32_t h = hist[lo + k];
+  for (int w = 0; w < wv; ++w) before += sh.wsum[w];
+  for (int k = 0; k < cnt; ++k) {
+    const uint32_t h = hist[digit(k)];
     if (before < rem && rem <= before + h) {
-      sh.digit = lo + k;
+      sh.digit = digit(k);
       sh.before = before;
       sh.equal = h;
     }

@@ -434,19 +434,6 @@ __device__ __forceinline__ uint32_t key16_one(uint32_t h) {
   return k + (k == 0x7FFFu ? 1u : 0u);
 }
 
-// Inclusive prefix sum over the 64 lanes of a wave: row shifts within each
-// row of 16 lanes, then row broadcasts of lanes 15 and 31 (DPP: no LDS round
-// trips, unlike a shuffle ladder).
-__device__ __forceinline__ uint32_t wave_incl_sum(uint32_t x) {
-  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xF, 0xF, true);   // row_shr:1
-  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xF, 0xF, true);   // row_shr:2
-  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xF, 0xF, true);   // row_shr:4
-  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xF, 0xF, true);   // row_shr:8
-  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xA, 0xF, false);  // row_bcast:15 -> rows 1, 3
-  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xC, 0xF, false);  // row_bcast:31 -> rows 2, 3
-  return x;
-}
-
 // The sampled keys of bf16 rows, packed two per register: V 16-byte vectors
 // per thread.
 template <int V>
