@@ -179,6 +179,31 @@ struct RowTile {
       // by side with three accumulators live.  The scheduling barriers keep
       // the compiler from hoisting all MFMAs ahead (which would need 4 (T+1)
       // accumulator registers and push operands into AGPRs).
+      if constexpr (R == 4) {
+        // four partial sums live, tiles in natural order (tile j feeds
+        // partial j % 4): each partial still sees its tiles and heads in
+        // the same order, but consecutive tiles no longer wait on each other
+        float ps[4] = {0.f, 0.f, 0.f, 0.f};
+        v4f cl = mfma_fp8(al.v, b.v);
+        v4f c0 = mfma_fp8(a[0].v, b.v);
+        v4f c1 = mfma_fp8(a[1].v, b.v);
+#pragma unroll
+        for (int jj = 2; jj <= T + 1; ++jj) {
+          v4f nxt = c1;
+          if (jj < T) nxt = mfma_fp8(a[jj].v, b.v);
+          __builtin_amdgcn_sched_barrier(0);
+          const int e = jj - 2;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) ps[e % 4] = fmaf(wv[e][i], fabsf(c0[i]), ps[e % 4]);
+          asm volatile("" : "+v"(ps[e % 4]));
+          __builtin_amdgcn_sched_barrier(0);
+          c0 = c1;
+          c1 = nxt;
+        }
+        tot = ((ps[0] + ps[1]) + ps[2]) + ps[3];
+        const float lin = fmaf(cl[3], kLinStep[3], fmaf(cl[2], kLinStep[2], fmaf(cl[1], kLinStep[1], cl[0])));
+        return fmaf(ls0, lin, tot);
+      }
       v4f cl = mfma_fp8(al.v, b.v);
       v4f c0 = mfma_fp8(a[tile_at(0)].v, b.v);
       v4f c1 = mfma_fp8(a[tile_at(1)].v, b.v);
