@@ -139,9 +139,11 @@ struct RowTile {
   // Gate-weighted ReLU sum over all heads of row (lane >> 4) / G for key
   // (lane & 15) of the fragment b, in the lanes that store it (lane group
   // (lane >> 4) % G == 0; the other lane groups of the row lack the fp8
-  // linear term).  The tiles are visited partial by partial (tile R j'' + p
-  // feeds partial p, j'' ascending), so a partial's FMA chain runs without a
-  // break and is folded as soon as it ends: two sums are live.
+  // linear term).  Tile R j'' + p feeds partial p, j'' ascending.  The fp8
+  // 4-row tile keeps its four partials live and visits the tiles in natural
+  // order; the other shapes visit them partial by partial, so a partial's
+  // FMA chain runs without a break and is folded as soon as it ends (two
+  // sums live).  Every shape adds a partial's terms in the same order.
   static constexpr int TPR = T / R;  // tiles per partial
   __device__ __forceinline__ static constexpr int tile_at(int jj) { return R * (jj % TPR) + jj / TPR; }
 
