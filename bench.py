@@ -10,7 +10,7 @@ top-c, and the per-member gather / re-score / top-k.  Inputs are synthetic
 Reported besides the headline queries/s: the dense indexer and PIVOT-Reuse on
 the same prefill (speedup), a group-size sweep, Refine with App. B's local
 window (W=4), the bf16 scoring kernel's MFMA fraction (the 128K prefill in bf16), MTP decode (32 x 131072 cached keys, g=2, also with the
-per-query window), the batch layouts (paged decode keys, a packed batch of
+per-query window; each call launched eagerly and replayed from a captured HIP graph), the batch layouts (paged decode keys, a packed batch of
 four prefill requests), per-kernel times from HIP events recorded around each launch
 inside the timed steps, the roofline fraction of the dominant kernel, and the
 CPU oracle timed on a sample of the same workload.
@@ -269,22 +269,38 @@ def decode_bench(reps):
     pos, nk = [L - g] * B, [L] * B
     out = torch.empty((B, g, wl.topk), dtype=torch.int32, device="cuda")
     res = {}
-    for mode in ("dense", "reuse", "refine", "refine_W4"):
+
+    def call(mode, ws=None):
         if mode == "dense":
-            fn = lambda: pv.pivot_dense_index(q, qs, w, k, ks, pos, nk, wl.topk, out=out)  # noqa: E731
-        elif mode == "refine_W4":  # App. B's per-query window, W = 4
-            fn = lambda: pv.pivot_group_index_opts(q, qs, w, k, ks, pos, nk, wl.topk, mode=pv.PIVOT_REFINE,  # noqa
-                                                   g=g, c=wl.c, window=4, window_kind=pv.PIVOT_WINDOW_PER_QUERY,
-                                                   out=out)
-        else:
-            m = pv.PIVOT_REUSE if mode == "reuse" else pv.PIVOT_REFINE
-            fn = lambda m=m: pv.pivot_group_index(q, qs, w, k, ks, pos, nk, wl.topk, mode=m, g=g, c=wl.c,  # noqa
-                                                  out=out)
+            return lambda: pv.pivot_dense_index(q, qs, w, k, ks, pos, nk, wl.topk, out=out, ws=ws)
+        if mode == "refine_W4":  # App. B's per-query window, W = 4
+            return lambda: pv.pivot_group_index_opts(q, qs, w, k, ks, pos, nk, wl.topk, mode=pv.PIVOT_REFINE, g=g,
+                                                     c=wl.c, window=4, window_kind=pv.PIVOT_WINDOW_PER_QUERY,
+                                                     out=out, ws=ws)
+        m = pv.PIVOT_REUSE if mode == "reuse" else pv.PIVOT_REFINE
+        return lambda: pv.pivot_group_index(q, qs, w, k, ks, pos, nk, wl.topk, mode=m, g=g, c=wl.c, out=out,
+                                            ws=ws)
+
+    modes = ("dense", "reuse", "refine", "refine_W4")
+    for mode in modes:
+        fn = call(mode)
         fn()
         sec = timed(fn, reps)
         res[mode] = {"us_per_step": sec * 1e6, "queries_per_s": B * g / sec}
+    # the same calls replayed from a HIP graph captured once per mode (the
+    # library makes no allocation, copy or memset inside a call, so a call
+    # captures whole): the chain's launch gaps without host work per step
+    ws = pv.workspace(0, q.device)  # the cached workspace, sized by the calls above
+    for mode in modes:
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            call(mode, ws)()
+        graph.replay()
+        res[mode]["graph_us_per_step"] = timed(graph.replay, reps) * 1e6
+        del graph
     for mode in ("reuse", "refine", "refine_W4"):
         res[mode]["speedup_vs_dense"] = res["dense"]["us_per_step"] / res[mode]["us_per_step"]
+        res[mode]["graph_speedup_vs_dense"] = res["dense"]["graph_us_per_step"] / res[mode]["graph_us_per_step"]
     key_bytes = B * L * (128 + 4)
     res["dense"]["key_stream_GBps"] = key_bytes / (res["dense"]["us_per_step"] * 1e-6) / 1e9
     res["workload"] = wl.name
@@ -635,6 +651,9 @@ def main():
     if bf16 is not None:
         log(f"bf16 score kernel: {bf16['score_TFLOPs']:.0f} TFLOP/s ({100 * bf16['frac']:.1f}% of peak)")
     dec = None if args.no_decode else decode_bench(reps=50)
+    if dec is not None:
+        log("decode us/step (eager | graph): " + ", ".join(
+            f"{m} {dec[m]['us_per_step']:.1f} | {dec[m]['graph_us_per_step']:.1f}" for m in ("dense", "reuse", "refine")))
     layouts = None if args.no_layouts else layout_bench(reps=20)
     cpu = None if args.no_cpu_baseline else cpu_baseline(pf, g)
     ws_bytes = int(pf.ws.numel())
