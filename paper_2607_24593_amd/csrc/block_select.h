@@ -25,6 +25,7 @@
 #pragma once
 
 #include "device_common.h"
+#include "dpp.h"
 
 namespace pivot {
 
@@ -107,13 +108,9 @@ __device__ __forceinline__ float key_float(uint32_t k) {
 template <int THREADS, bool MINMAX>
 __device__ __forceinline__ void block_pair_reduce(uint32_t& a, uint32_t& o, SelectShared& sh) {
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-#pragma unroll
-  for (int d = 32; d > 0; d >>= 1) {
-    const uint32_t x = __shfl_xor(a, d, 64), y = __shfl_xor(o, d, 64);
-    a = MINMAX ? min(a, x) : (a & x);
-    o = MINMAX ? max(o, y) : (o | y);
-  }
-  if (lane == 0) {
+  a = wave_total_at63(a, ~0u, [](uint32_t x, uint32_t y) { return MINMAX ? min(x, y) : (x & y); });
+  o = wave_total_at63(o, 0u, [](uint32_t x, uint32_t y) { return MINMAX ? max(x, y) : (x | y); });
+  if (lane == 63) {
     sh.wand[wv] = a;
     sh.wor[wv] = o;
   }

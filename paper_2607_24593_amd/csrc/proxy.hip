@@ -11,6 +11,9 @@
 // first / last aggregation (Sec. 5.4).  For fp8 the kernel can also write the
 // score epilogue's linear terms (lin_row) of the proxy and of the members,
 // which saves a pass over the member rows.
+#include <algorithm>
+
+#include "dpp.h"
 #include "launch.h"
 #include "mfma_tile.h"
 #include "pivot.h"
@@ -44,8 +47,8 @@ __device__ __forceinline__ float decode_e4m3(uint32_t word, int byte) {
 // epilogue; out_scale still receives all four.
 // Lane l reads the 16-byte slices (dims 16 (l / 8) ..) of heads l % 8,
 // l % 8 + 8, ..: eight loads per lane, all in flight at once;
-// the eight partial sums of a dim are added across lanes (xor 1, 2, 4) in a
-// fixed order, and lane l then keeps dims 2l and 2l+1 to quantise.  qr and wr
+// the eight partial sums of a dim are added across lanes (xor 1, 2, 4, as DPP
+// steps) in a fixed order, and lane l then keeps dims 2l and 2l+1 to quantise.  qr and wr
 // may point to global memory or LDS.  Every operation is explicit (no
 // contraction), so each caller gets the same bits.
 __device__ __forceinline__ void lin_row(const uint8_t* qr, const float* wr, float qscale, uint8_t* out,
@@ -73,9 +76,9 @@ __device__ __forceinline__ void lin_row(const uint8_t* qr, const float* wr, floa
   }
 #pragma unroll
   for (int e = 0; e < 16; ++e) {
-    u[e] = u[e] + __shfl_xor(u[e], 1);
-    u[e] = u[e] + __shfl_xor(u[e], 2);
-    u[e] = u[e] + __shfl_xor(u[e], 4);
+    u[e] = u[e] + lane_xor1(u[e]);
+    u[e] = u[e] + lane_xor2(u[e]);
+    u[e] = u[e] + lane_xor4(u[e]);
   }
   // dims 2 lane, 2 lane + 1 = elements 2 hs, 2 hs + 1 of this lane's block
   float u0 = u[0], u1 = u[1];
@@ -84,7 +87,7 @@ __device__ __forceinline__ void lin_row(const uint8_t* qr, const float* wr, floa
     u0 = hs == e ? u[2 * e] : u0;
     u1 = hs == e ? u[2 * e + 1] : u1;
   }
-  const float amax = wave_max(fmaxf(fabsf(u0), fabsf(u1)));
+  const float amax = wave_reduce(fmaxf(fabsf(u0), fabsf(u1)), [](float a, float b) { return fmaxf(a, b); });
   const float sigma0 = amax > 0.f ? amax / 448.0f : 1.0f;
 #pragma unroll
   for (int l = 0; l < kLinLevels; ++l) {
@@ -107,7 +110,10 @@ __global__ __launch_bounds__(256) void proxy_kernel(const uint8_t* __restrict__ 
 #pragma clang fp contract(off)
   // stage (fp8, members' linear terms wanted, g <= MB): the mean pass copies
   // each member row it loads into dynamic LDS (g x 8 KiB), and the members'
-  // linear terms are computed from there rather than read again from HBM
+  // linear terms are computed from there rather than read again from HBM.
+  // The proxy's codes, for its own linear term, take the region's first 8 KiB
+  // (member 0's slot, once the members' terms are done), so a workgroup of
+  // four members holds 32 KiB and four fit a CU.
   extern __shared__ uint4 mrows[];
   constexpr int EB = DT == kFp8 ? 1 : 2;
   constexpr int ROW_BYTES = kH * kD * EB;
@@ -198,18 +204,27 @@ __global__ __launch_bounds__(256) void proxy_kernel(const uint8_t* __restrict__ 
     }
   }
   const float count = (float)gs;
+  // correctly rounded fp32 divides; by a power of two the product with its
+  // exact reciprocal is the same correctly rounded value
+  if ((gs & (gs - 1)) == 0) {
+    const float inv = 1.0f / count;
+#pragma unroll
+    for (int e = 0; e < PER; ++e) sum[e] = sum[e] * inv;
+    wsum = wsum * inv;
+  } else {
+#pragma unroll
+    for (int e = 0; e < PER; ++e) sum[e] = sum[e] / count;
+    wsum = wsum / count;
+  }
   float amax = 0.0f;
 #pragma unroll
-  for (int e = 0; e < PER; ++e) {
-    sum[e] = sum[e] / count;  // correctly rounded fp32 divide
-    amax = fmaxf(amax, fabsf(sum[e]));
-  }
+  for (int e = 0; e < PER; ++e) amax = fmaxf(amax, fabsf(sum[e]));
 
-  if (tid < kH) pw[pr * kH + tid] = wsum / count;
+  if (tid < kH) pw[pr * kH + tid] = wsum;
 
   if constexpr (DT == kFp8) {
     __shared__ float wmax[4];
-    amax = wave_max(amax);
+    amax = wave_reduce(amax, [](float a, float b) { return fmaxf(a, b); });
     if ((tid & 63) == 0) wmax[tid >> 6] = amax;
     __syncthreads();
     amax = fmaxf(fmaxf(wmax[0], wmax[1]), fmaxf(wmax[2], wmax[3]));
@@ -224,26 +239,27 @@ __global__ __launch_bounds__(256) void proxy_kernel(const uint8_t* __restrict__ 
     dst[0] = uint4{out[0], out[1], out[2], out[3]};
     dst[1] = uint4{out[4], out[5], out[6], out[7]};
     if (tid == 0) psc[pr] = sigma;
-    // the linear terms: the proxy's from its codes and gates staged in LDS,
-    // the members' (Refine re-scores them) from their rows, which this
-    // workgroup has just read
-    __shared__ uint4 prow[ROW_BYTES / 16];
-    __shared__ float pws[kH];
-    if (lo.plin) {
-      prow[2 * tid] = uint4{out[0], out[1], out[2], out[3]};
-      prow[2 * tid + 1] = uint4{out[4], out[5], out[6], out[7]};
-      if (tid < kH) pws[tid] = wsum / count;
-      __syncthreads();
-    }
+    // the linear terms: the members' (Refine re-scores them) from their rows,
+    // which this workgroup has just read, then the proxy's from its codes and
+    // gates staged in LDS
     const int wave = tid >> 6, lane = tid & 63;
-    if (lo.plin && wave == (gs & 3))
-      lin_row(reinterpret_cast<const uint8_t*>(prow), pws, sigma, lo.plin + pr * kLinBytes,
-              lo.plsc + pr * kLinLevels, lane);
     if (lo.qlin)  // the staged rows were written before the amax barrier above
       for (int r = wave; r < gs; r += 4)
         lin_row(stage ? reinterpret_cast<const uint8_t*>(mrows + r * (ROW_BYTES / 16)) : q + (r0 + r) * ROW_BYTES,
                 w + (r0 + r) * kH, q_scale[r0 + r], lo.qlin + (r0 + r) * kLinBytes, lo.qlsc + (r0 + r) * kLinLevels,
                 lane);
+    if (lo.plin) {
+      uint4* prow = mrows;  // member 0's staged row is no longer read past the barrier
+      __shared__ float pws[kH];
+      if (stage) __syncthreads();
+      prow[2 * tid] = uint4{out[0], out[1], out[2], out[3]};
+      prow[2 * tid + 1] = uint4{out[4], out[5], out[6], out[7]};
+      if (tid < kH) pws[tid] = wsum;
+      __syncthreads();
+      if (wave == (gs & 3))
+        lin_row(reinterpret_cast<const uint8_t*>(prow), pws, sigma, lo.plin + pr * kLinBytes,
+                lo.plsc + pr * kLinLevels, lane);
+    }
   } else {
     uint32_t out[16];
 #pragma unroll
@@ -263,7 +279,8 @@ hipError_t launch_proxy(int dtype, const void* q, const float* q_scale, const fl
   dim3 grid((unsigned)(j1 - j0), (unsigned)st.n);
   // members staged in LDS for their linear terms when one load batch holds a group
   const int stage = dtype == kFp8 && lo.qlin && agg == PIVOT_AGG_MEAN && g > 1 && g <= 8;
-  const size_t shmem = stage ? (size_t)g * kH * kD : 0;
+  // dynamic LDS: the staged members, and the proxy's codes (in the first slot)
+  const size_t shmem = std::max(stage ? (size_t)g * kH * kD : 0, dtype == kFp8 && lo.plin ? (size_t)kH * kD : 0);
   if (dtype == kFp8)
     hipLaunchKernelGGL(proxy_kernel<kFp8>, grid, dim3(256), shmem, stream, (const uint8_t*)q, q_scale, w, g, st, j0,
                        (int)all_groups, agg, (uint8_t*)pq, psc, pw, lo, stage);

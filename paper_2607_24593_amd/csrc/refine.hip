@@ -533,8 +533,11 @@ __device__ __forceinline__ void member_of(int x, int g, int n, int& j, int& memb
   }
 }
 
+// Up to 16 pairs per thread the select fits 8 waves per SIMD: the compiler is
+// held to that occupancy (a few scalar values move to VGPR lanes instead of
+// holding it to 7 with their scalar registers).
 template <int V, class E, int T>
-__global__ __launch_bounds__(T) void topk_short_kernel(const E* __restrict__ rsc,
+__global__ __launch_bounds__(T) __attribute__((amdgpu_waves_per_eu(V <= 16 ? 8 : 1))) void topk_short_kernel(const E* __restrict__ rsc,
                                                          const int32_t* __restrict__ cand, int g, SeqTable st,
                                                          int j0, int nj, int c, SlotRule rule, int m,
                                                          int32_t* __restrict__ out_idx) {
