@@ -87,12 +87,11 @@ __device__ __forceinline__ uint32_t float_key(float f) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-// bf16 bits of an fp32 value, rounded to nearest even (finite values).
-__device__ __forceinline__ uint16_t bf16_rne(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
-}
+// bf16 bits of an fp32 value, rounded to nearest even: gfx950's conversion
+// instruction (one VALU operation; the same bits as rounding the upper half
+// by hand for every finite value, subnormals and overflow to infinity
+// included).
+__device__ __forceinline__ uint16_t bf16_rne(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
 
 // Score rows hold fp32 or bf16 values (the fp8 path stores bf16 scores); E is
 // float or bf16_t (bf16 bits).  A 16-byte vector holds N scores, widened to
