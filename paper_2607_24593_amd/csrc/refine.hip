@@ -107,7 +107,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void r
 #pragma unroll
     for (int k = 0; k < SB; ++k) {
       const int e = e0 + sid + ST * k;
-      if (e < ncs) spos[e] = pv[k];
+      if (e < ncs) spos[e] = max(pv[k], 0);  // empty slots (-1): key 0's row
     }
   }
 
@@ -135,7 +135,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void r
   const uint32_t my_off = (uint32_t)(qr * c + cbeg) * SE;
   const int nfrag = fend - fbeg;
   constexpr int S = WPG ? 1 : 4;  // fragment stride between the waves
-  auto pos_of = [&](int f) { return max(spos[min(16 * f + lr, ncs - 1)], 0); };  // empty slots: key 0
+  auto pos_of = [&](int f) { return spos[min(16 * f + lr, ncs - 1)]; };
   // the same position read from global memory (before the LDS copy is staged)
   auto pos_glob = [&](int f) {
     const int p = max(crow[cbeg + min(16 * f + lr, ncs - 1)], 0);

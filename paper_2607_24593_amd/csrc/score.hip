@@ -56,7 +56,10 @@ __global__ __launch_bounds__(256) void score_kernel(const uint8_t* __restrict__ 
   constexpr int EB = Tile::EB;
   constexpr int KB = kD * EB;  // bytes per key
   constexpr int RB = KSPLIT ? R : 4 * R;
-  __shared__ float sks[4096];  // the segment's key scales (fp8)
+  // the segment's key scales (fp8); a key index never reaches 4096 (rows
+  // mode: at most 127 stages of 32 keys; keys mode: 2048-key segments plus
+  // two fragment strides), and 32 spare words keep a stray read inside
+  __shared__ float sks[4096 + 32];
   __shared__ __align__(16) uint8_t kst[KSPLIT ? 16 : 3 * kStageSlot<DT>];  // rows mode: staged keys
   __shared__ int32_t spg[PAGED ? 256 : 1];  // the segment's pages (paged keys; a segment of <= 4096 keys
                                             // starts on a page boundary or lies inside one page)
@@ -168,7 +171,7 @@ __global__ __launch_bounds__(256) void score_kernel(const uint8_t* __restrict__ 
 
   auto emit = [&](float acc, int base) {
     const int s = base + lr;
-    if constexpr (DT == kFp8) acc *= sks[s & 4095];
+    if constexpr (DT == kFp8) acc *= sks[s];
     const uint32_t off = (writer && s < my_n) ? my_off + (uint32_t)SE * (uint32_t)s : 0xFFFFFFFFu;
     if constexpr (OB16)
       __builtin_amdgcn_raw_buffer_store_b16(bf16_rne(acc), orr, off, 0, 0);
