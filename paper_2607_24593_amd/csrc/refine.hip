@@ -26,6 +26,7 @@
 // its select keeps the slots it may use: position in [0, t], and for a union
 // slot of the per-query window also position >= t - W + 1.
 #include <algorithm>
+#include <climits>
 
 #include "block_select.h"
 #include "launch.h"
@@ -132,7 +133,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void r
   // every lane issues the same memory operations and the waits stay exact
   const __amdgpu_buffer_rsrc_t orr = buffer_rsrc(static_cast<uint8_t*>(rsc) + (grp * g + R * blk) * (int64_t)c * SE,
                                                  (uint32_t)(R * c) * SE);
-  const uint32_t my_off = (uint32_t)(qr * c + cbeg) * SE;
+  const uint32_t my_off = (uint32_t)(qr * c + cbeg + lr) * SE;
+  // slot 16 f + lr is stored when 16 f < my_lim (one compare of the
+  // fragment's uniform base against a lane constant)
+  const int my_lim = writer ? ncs - lr : INT_MIN;
   const int nfrag = fend - fbeg;
   constexpr int S = WPG ? 1 : 4;  // fragment stride between the waves
   auto pos_of = [&](int f) { return spos[min(16 * f + lr, ncs - 1)]; };
@@ -142,8 +146,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void r
     return km.pages ? (int)km.row(b, p) : p;
   };
   auto emit = [&](float acc, float ks, int f) {
-    const int slot = 16 * f + lr;
-    const uint32_t off = (writer && slot < ncs) ? my_off + SE * (uint32_t)slot : 0xFFFFFFFFu;
+    const uint32_t off = 16 * f < my_lim ? my_off + SE * (uint32_t)(16 * f) : 0xFFFFFFFFu;
     if constexpr (OB16)
       __builtin_amdgcn_raw_buffer_store_b16(bf16_rne(acc * ks), orr, off, 0, 0);
     else

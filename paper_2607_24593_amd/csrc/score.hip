@@ -24,6 +24,8 @@
 // (pinning segments to XCDs would idle the XCDs that own the late segments of
 // short prefixes).  Keys mode runs x = key segment, y = sequence.  The segment
 // length adapts to the launch size.
+#include <climits>
+
 #include "launch.h"
 #include "mfma_tile.h"
 
@@ -167,12 +169,14 @@ __global__ __launch_bounds__(256) void score_kernel(const uint8_t* __restrict__ 
   const __amdgpu_buffer_rsrc_t orr =
       buffer_rsrc((uint8_t*)out + (((int64_t)b * nrows + (i_w - rs.i0)) * ld + seg0) * SE,
                   (uint32_t)(((int64_t)(R - 1) * ld + nkeys) * SE));
-  const uint32_t my_off = (uint32_t)((int64_t)qr * ld * SE);
+  const uint32_t my_off = (uint32_t)((int64_t)qr * ld * SE) + (uint32_t)SE * (uint32_t)lr;
+  // key base + lr is stored when base < my_lim (the fragment's base is the
+  // same in every lane, so the test is one compare against a lane constant)
+  const int my_lim = writer ? my_n - lr : INT_MIN;
 
   auto emit = [&](float acc, int base) {
-    const int s = base + lr;
-    if constexpr (DT == kFp8) acc *= sks[s];
-    const uint32_t off = (writer && s < my_n) ? my_off + (uint32_t)SE * (uint32_t)s : 0xFFFFFFFFu;
+    if constexpr (DT == kFp8) acc *= sks[base + lr];
+    const uint32_t off = base < my_lim ? my_off + (uint32_t)SE * (uint32_t)base : 0xFFFFFFFFu;
     if constexpr (OB16)
       __builtin_amdgcn_raw_buffer_store_b16(bf16_rne(acc), orr, off, 0, 0);
     else
