@@ -43,8 +43,16 @@ constexpr int kMaxCand = 8192;
 // otherwise the 4 waves of a workgroup share one unit (and slice) and split
 // its fragments.
 constexpr int kWpgCand = 4096;
+// Staged positions run kPosPad entries past a wave's (WPG) or workgroup's
+// candidates, holding key 0, so the fetch three fragments ahead (at most
+// 5 fragment strides past the loop's last fragment) reads a position without
+// clamping its index.
+constexpr int kPosPadWpg = 96, kPosPad = 384;
 
-template <int DT, int R, bool OB16, bool WPG>
+// B32: the keys (and scales) a launch can gather span less than 2^31 bytes,
+// so they are read through buffer resources with 32-bit offsets (fewer
+// address operations per fragment than 64-bit pointers).
+template <int DT, int R, bool OB16, bool WPG, bool B32>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void rescore_kernel(
     const uint8_t* __restrict__ q, const float* __restrict__ q_scale, const float* __restrict__ w,
     const uint8_t* __restrict__ lin, const float* __restrict__ lin_scale, int g,
@@ -53,7 +61,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void r
   using Tile = RowTile<DT, R>;
   constexpr uint32_t SE = OB16 ? 2 : 4;  // bytes per stored score
   constexpr int EB = Tile::EB;
-  __shared__ int32_t spos_all[WPG ? 4 * kWpgCand : kMaxCand];
+  constexpr int PAD = WPG ? kPosPadWpg : kPosPad;
+  __shared__ int32_t spos_all[WPG ? 4 * (kWpgCand + kPosPadWpg) : kMaxCand + kPosPad];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
   // members [R blk, R blk + R); candidate fragments of slice `part`
@@ -68,7 +77,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void r
   if (b >= st.n || j >= seq_groups(st, b, g) || j < st.first_proxy[b]) return;
   const int gs = min(g, st.n_rows[b] - j * g);
   if (R * blk >= gs) return;
-  int32_t* spos = WPG ? spos_all + wave * kWpgCand : spos_all;
+  int32_t* spos = WPG ? spos_all + wave * (kWpgCand + kPosPadWpg) : spos_all;
   constexpr int ST = WPG ? 64 : 256;  // threads staging the positions
   const int sid = WPG ? lane : tid;
   const int64_t t0 = (int64_t)st.q_pos0[b] + (int64_t)j * g;
@@ -111,6 +120,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void r
       if (e < ncs) spos[e] = max(pv[k], 0);  // empty slots (-1): key 0's row
     }
   }
+  {
+    const int32_t key0 = km.pages ? (int32_t)km.row(b, 0) : 0;
+    for (int e = ncs + sid; e < ncs + PAD; e += ST) spos[e] = key0;
+  }
 
   const uint8_t* rows[R];
   const float* wrows[R];
@@ -139,7 +152,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void r
   const int my_lim = writer ? ncs - lr : INT_MIN;
   const int nfrag = fend - fbeg;
   constexpr int S = WPG ? 1 : 4;  // fragment stride between the waves
-  auto pos_of = [&](int f) { return spos[min(16 * f + lr, ncs - 1)]; };
+  auto pos_of = [&](int f) { return spos[16 * f + lr]; };  // past the candidates: key 0
   // the same position read from global memory (before the LDS copy is staged)
   auto pos_glob = [&](int f) {
     const int p = max(crow[cbeg + min(16 * f + lr, ncs - 1)], 0);
@@ -152,10 +165,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void r
     else
       __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc * ks), orr, off, 0, 0);
   };
-  auto scale_of = [&](int p) { return DT == kFp8 ? ksb[p] : 1.0f; };
+  // the rows a launch can gather: the pool (paged) or a sequence's stride
+  const int64_t key_rows = km.pages ? ((int64_t)km.n_pages << km.shift) : km.stride;
+  const __amdgpu_buffer_rsrc_t krs = buffer_rsrc(kb, B32 ? (uint32_t)(key_rows * kD * EB) : 0u);
+  const __amdgpu_buffer_rsrc_t srs = buffer_rsrc(ksb, B32 && DT == kFp8 ? (uint32_t)(key_rows * 4) : 0u);
   auto fetch_at = [&](KeyFrag<DT>& kf, float& sc, int p) {
-    sc = scale_of(p);
-    kf.load(kb + (int64_t)p * kD * EB, kg);
+    if constexpr (B32) {
+      sc = DT == kFp8 ? __int_as_float(__builtin_amdgcn_raw_buffer_load_b32(srs, (uint32_t)p * 4u, 0, 0)) : 1.0f;
+      kf.load(krs, (uint32_t)p * (uint32_t)(kD * EB), kg);
+    } else {
+      sc = DT == kFp8 ? ksb[p] : 1.0f;
+      kf.load(kb + (int64_t)p * kD * EB, kg);
+    }
   };
   auto fetch = [&](KeyFrag<DT>& kf, float& sc, int ff) { fetch_at(kf, sc, pos_of(ff)); };
   // three fragments in flight per wave, with no exits in the loop body:
@@ -754,9 +775,19 @@ hipError_t launch_refine(int dtype, const void* q, const float* q_scale, const f
   const int64_t units = (int64_t)(j1 - j0) * ((g + R - 1) / R);
   const dim3 grid = wpg ? dim3((unsigned)((units + 3) / 4), (unsigned)st.n, 1u)
                         : dim3((unsigned)(j1 - j0), (unsigned)st.n, (unsigned)(((g + R - 1) / R) * parts));
+  // 32-bit gather offsets when every gatherable key row lies below 2^31 bytes
+  // (a paged pool always does)
+  const int eb = dtype == kFp8 ? 1 : 2;
+  const bool b32 = km.pages || km.stride * kD * eb < ((int64_t)1 << 31);
 #define PIVOT_RESCORE(DTV, RV, OB, WP, KS)                                                                        \
-  hipLaunchKernelGGL((rescore_kernel<DTV, RV, OB, WP>), grid, dim3(256), 0, stream, (const uint8_t*)q, q_scale, w, \
-                     lin, lin_scale, g, (const uint8_t*)k, KS, km, st, j0, cand, c, all_slots, parts, rescore)
+  if (b32)                                                                                                        \
+    hipLaunchKernelGGL((rescore_kernel<DTV, RV, OB, WP, true>), grid, dim3(256), 0, stream, (const uint8_t*)q,     \
+                       q_scale, w, lin, lin_scale, g, (const uint8_t*)k, KS, km, st, j0, cand, c, all_slots, parts, \
+                       rescore);                                                                                  \
+  else                                                                                                            \
+    hipLaunchKernelGGL((rescore_kernel<DTV, RV, OB, WP, false>), grid, dim3(256), 0, stream, (const uint8_t*)q,    \
+                       q_scale, w, lin, lin_scale, g, (const uint8_t*)k, KS, km, st, j0, cand, c, all_slots, parts, \
+                       rescore)
   if (dtype == kFp8 && R == 4) {
     if (wpg) PIVOT_RESCORE(kFp8, 4, true, true, k_scale);
     else PIVOT_RESCORE(kFp8, 4, true, false, k_scale);
