@@ -37,6 +37,20 @@ __device__ __forceinline__ float decode_e4m3(uint32_t word, int byte) {
   }
 }
 
+// a / b rounded once, from y = RN(1 / b) (Markstein's division step): q0 =
+// RN(a y) lies within an ulp of a / b, so the remainder q0 b - a is exact and
+// q0 - (q0 b - a) y rounds to RN(a / b).  Taking the remainder as q0 b - a
+// keeps the sign of a zero quotient.  For b in [2^-80, 2^100] this is a / b
+// rounded once whenever |a / b| >= 2^-11 (a is then at least 2^-91, far from
+// the subnormals where the remainder could round); a smaller quotient may be
+// an ulp off, and both round to the same signed zero in E4M3.  Three VALU
+// operations in place of the eleven of a general fp32 divide.
+__device__ __forceinline__ float div_rn(float a, float b, float y) {
+  const float q0 = a * y;
+  return fmaf(fmaf(q0, b, -a), -y, q0);
+}
+__device__ __forceinline__ bool div_rn_ok(float b) { return b >= 0x1p-80f && b <= 0x1p100f; }
+
 // The linear part of the fp8 epilogue (mfma_tile.h) for one row, by one wave:
 // u = sum_j (w_j * qscale / 2) * q8_j, a 128-vector, stored as four fp8
 // levels: level l holds codes c_l = RNE((u - sum_{l'<l} sigma_l' c_l') /
@@ -46,11 +60,12 @@ __device__ __forceinline__ float decode_e4m3(uint32_t word, int byte) {
 // 2^-19 of max|u|.  The fixed ratio leaves one scale per row for the
 // epilogue; out_scale still receives all four.
 // Lane l reads the 16-byte slices (dims 16 (l / 8) ..) of heads l % 8,
-// l % 8 + 8, ..: eight loads per lane, all in flight at once;
-// the eight partial sums of a dim are added across lanes (xor 1, 2, 4, as DPP
-// steps) in a fixed order, and lane l then keeps dims 2l and 2l+1 to quantise.  qr and wr
-// may point to global memory or LDS.  Every operation is explicit (no
-// contraction), so each caller gets the same bits.
+// l % 8 + 8, ..: eight loads per lane, all in flight at once.  The eight
+// partial sums of a dim are then added across lanes (xor 1, 2, 4, as DPP
+// steps) in a fixed order, halving the vector at each step, so that lane l
+// ends with dims 2l and 2l+1 to quantise.  qr and wr may point to global
+// memory or LDS.  Every operation is explicit (no contraction), so each
+// caller gets the same bits.
 __device__ __forceinline__ void lin_row(const uint8_t* qr, const float* wr, float qscale, uint8_t* out,
                                         float* out_scale, int lane) {
 #pragma clang fp contract(off)
@@ -74,29 +89,56 @@ __device__ __forceinline__ void lin_row(const uint8_t* qr, const float* wr, floa
 #pragma unroll
     for (int e = 0; e < 16; ++e) u[e] = fmaf(x, decode_e4m3(words[e >> 2], e & 3), u[e]);
   }
+  // Reduce-scatter over the 8 lanes hs of a dim block.  After the xor-1 step
+  // a lane keeps the elements whose bit 1 equals its hs bit 0, after xor 2
+  // those whose bit 2 equals hs bit 1, after xor 4 bit 3 = hs bit 2: lane hs
+  // is left with elements 2 hs and 2 hs + 1.  Every add takes the same two
+  // partial sums as a full butterfly, so the bits are unchanged.
+  const bool h0 = hs & 1, h1 = hs & 2, h2 = hs & 4;
+  float s8[8];  // index (e3 e2 e0)
 #pragma unroll
-  for (int e = 0; e < 16; ++e) {
-    u[e] = u[e] + lane_xor1(u[e]);
-    u[e] = u[e] + lane_xor2(u[e]);
-    u[e] = u[e] + lane_xor4(u[e]);
+  for (int i = 0; i < 8; ++i) {
+    const int lo = ((i & 6) << 1) | (i & 1);  // element with bit 1 clear
+    const float keep = h0 ? u[lo | 2] : u[lo], send = h0 ? u[lo] : u[lo | 2];
+    s8[i] = keep + lane_xor1(send);
   }
-  // dims 2 lane, 2 lane + 1 = elements 2 hs, 2 hs + 1 of this lane's block
-  float u0 = u[0], u1 = u[1];
+  float s4[4];  // index (e3 e0)
 #pragma unroll
-  for (int e = 1; e < 8; ++e) {
-    u0 = hs == e ? u[2 * e] : u0;
-    u1 = hs == e ? u[2 * e + 1] : u1;
+  for (int j = 0; j < 4; ++j) {
+    const int lo = ((j & 2) << 1) | (j & 1);  // s8 index with e2 clear
+    const float keep = h1 ? s8[lo | 2] : s8[lo], send = h1 ? s8[lo] : s8[lo | 2];
+    s4[j] = keep + lane_xor2(send);
+  }
+  float u0, u1;
+  {
+    const float keep0 = h2 ? s4[2] : s4[0], send0 = h2 ? s4[0] : s4[2];
+    const float keep1 = h2 ? s4[3] : s4[1], send1 = h2 ? s4[1] : s4[3];
+    u0 = keep0 + lane_xor4(send0);
+    u1 = keep1 + lane_xor4(send1);
   }
   const float amax = wave_reduce(fmaxf(fabsf(u0), fabsf(u1)), [](float a, float b) { return fmaxf(a, b); });
   const float sigma0 = amax > 0.f ? amax / 448.0f : 1.0f;
-#pragma unroll
-  for (int l = 0; l < kLinLevels; ++l) {
+  const float y0 = 1.0f / sigma0;
+  auto level = [&](int l, float q0, float q1) {
     const float sigma = sigma0 * kLinStep[l];  // exact: a power of two
-    const int word = __builtin_amdgcn_cvt_pk_fp8_f32(u0 / sigma, u1 / sigma, 0, false);
+    const int word = __builtin_amdgcn_cvt_pk_fp8_f32(q0, q1, 0, false);
     *reinterpret_cast<uint16_t*>(out + l * kD + 2 * lane) = (uint16_t)word;
     u0 = u0 - sigma * __builtin_amdgcn_cvt_f32_fp8(word, 0);
     u1 = u1 - sigma * __builtin_amdgcn_cvt_f32_fp8(word, 1);
     if (lane == 0) out_scale[l] = sigma;
+  };
+  if (div_rn_ok(sigma0) && div_rn_ok(sigma0 * kLinStep[kLinLevels - 1])) {
+#pragma unroll
+    for (int l = 0; l < kLinLevels; ++l) {
+      const float sigma = sigma0 * kLinStep[l], y = y0 * (float)(1 << (4 * l));  // both exact
+      level(l, div_rn(u0, sigma, y), div_rn(u1, sigma, y));
+    }
+  } else {
+#pragma unroll
+    for (int l = 0; l < kLinLevels; ++l) {
+      const float sigma = sigma0 * kLinStep[l];
+      level(l, u0 / sigma, u1 / sigma);
+    }
   }
 }
 
@@ -110,13 +152,14 @@ __global__ __launch_bounds__(256) void proxy_kernel(const uint8_t* __restrict__ 
 #pragma clang fp contract(off)
   // stage (fp8, members' linear terms wanted, g <= MB): the mean pass copies
   // each member row it loads into dynamic LDS (g x 8 KiB), and the members'
-  // linear terms are computed from there rather than read again from HBM.
-  // The proxy's codes, for its own linear term, take the region's first 8 KiB
+  // linear terms are computed from there rather than read again from HBM;
+  // their gates follow the rows (g x 256 B).  The proxy's codes, for its own linear term, take the region's first 8 KiB
   // (member 0's slot, once the members' terms are done), so a workgroup of
-  // four members holds 32 KiB and four fit a CU.
+  // four members holds 33 KiB and four fit a CU.
   extern __shared__ uint4 mrows[];
   constexpr int EB = DT == kFp8 ? 1 : 2;
   constexpr int ROW_BYTES = kH * kD * EB;
+  float* const mgates = reinterpret_cast<float*>(mrows + g * (ROW_BYTES / 16));
   constexpr int PER = 32;  // elements per thread
   const int j = j0 + blockIdx.x, b = blockIdx.y;
   if (b >= st.n || j >= seq_groups(st, b, g)) return;
@@ -176,6 +219,10 @@ __global__ __launch_bounds__(256) void proxy_kernel(const uint8_t* __restrict__ 
         if (k < gs)
 #pragma unroll
           for (int x = 0; x < VPM; ++x) mrows[k * (ROW_BYTES / 16) + VPM * tid + x] = v[k][x];
+      if (tid < kH)
+#pragma unroll
+        for (int k = 0; k < MB; ++k)
+          if (k < gs) mgates[k * kH + tid] = wv[k];
     }
 #pragma unroll
     for (int k = 0; k < MB; ++k) {
@@ -230,10 +277,17 @@ __global__ __launch_bounds__(256) void proxy_kernel(const uint8_t* __restrict__ 
     amax = fmaxf(fmaxf(wmax[0], wmax[1]), fmaxf(wmax[2], wmax[3]));
     const float sigma = amax > 0.0f ? amax / 448.0f : 1.0f;
     uint32_t out[8];
+    if (div_rn_ok(sigma)) {  // uniform over the workgroup
+      const float y = 1.0f / sigma;
 #pragma unroll
-    for (int v = 0; v < 8; ++v) {
-      out[v] = encode_e4m3_quad(sum[4 * v] / sigma, sum[4 * v + 1] / sigma, sum[4 * v + 2] / sigma,
-                                sum[4 * v + 3] / sigma);
+      for (int v = 0; v < 8; ++v)
+        out[v] = encode_e4m3_quad(div_rn(sum[4 * v], sigma, y), div_rn(sum[4 * v + 1], sigma, y),
+                                  div_rn(sum[4 * v + 2], sigma, y), div_rn(sum[4 * v + 3], sigma, y));
+    } else {
+#pragma unroll
+      for (int v = 0; v < 8; ++v)
+        out[v] = encode_e4m3_quad(sum[4 * v] / sigma, sum[4 * v + 1] / sigma, sum[4 * v + 2] / sigma,
+                                  sum[4 * v + 3] / sigma);
     }
     uint4* dst = reinterpret_cast<uint4*>(pq + pr * ROW_BYTES + e0);
     dst[0] = uint4{out[0], out[1], out[2], out[3]};
@@ -246,7 +300,7 @@ __global__ __launch_bounds__(256) void proxy_kernel(const uint8_t* __restrict__ 
     if (lo.qlin)  // the staged rows were written before the amax barrier above
       for (int r = wave; r < gs; r += 4)
         lin_row(stage ? reinterpret_cast<const uint8_t*>(mrows + r * (ROW_BYTES / 16)) : q + (r0 + r) * ROW_BYTES,
-                w + (r0 + r) * kH, q_scale[r0 + r], lo.qlin + (r0 + r) * kLinBytes, lo.qlsc + (r0 + r) * kLinLevels,
+                stage ? mgates + r * kH : w + (r0 + r) * kH, q_scale[r0 + r], lo.qlin + (r0 + r) * kLinBytes, lo.qlsc + (r0 + r) * kLinLevels,
                 lane);
     if (lo.plin) {
       uint4* prow = mrows;  // member 0's staged row is no longer read past the barrier
@@ -279,8 +333,9 @@ hipError_t launch_proxy(int dtype, const void* q, const float* q_scale, const fl
   dim3 grid((unsigned)(j1 - j0), (unsigned)st.n);
   // members staged in LDS for their linear terms when one load batch holds a group
   const int stage = dtype == kFp8 && lo.qlin && agg == PIVOT_AGG_MEAN && g > 1 && g <= 8;
-  // dynamic LDS: the staged members, and the proxy's codes (in the first slot)
-  const size_t shmem = std::max(stage ? (size_t)g * kH * kD : 0, dtype == kFp8 && lo.plin ? (size_t)kH * kD : 0);
+  // dynamic LDS: the staged members and their gates, and the proxy's codes (in the first slot)
+  const size_t shmem =
+      std::max(stage ? (size_t)g * (kH * kD + kH * sizeof(float)) : 0, dtype == kFp8 && lo.plin ? (size_t)kH * kD : 0);
   if (dtype == kFp8)
     hipLaunchKernelGGL(proxy_kernel<kFp8>, grid, dim3(256), shmem, stream, (const uint8_t*)q, q_scale, w, g, st, j0,
                        (int)all_groups, agg, (uint8_t*)pq, psc, pw, lo, stage);

@@ -46,6 +46,42 @@ def test_proxy_rows_bit_exact(fmt, g):
         assert np.array_equal(pw[j], ow), j
 
 
+@pytest.mark.parametrize("g", [2, 4])
+def test_proxy_codes_at_ties_and_near_zero(g):
+    """fp8 proxies whose mean / scale lands exactly on E4M3 midpoints (RNE
+    ties), on values of either sign below the smallest subnormal, and on exact
+    zeros.  The members of a group alternate between adjacent codes a and b of
+    one sign, all with the scale 3/16; element 0 is 448 in every member, so the
+    proxy's scale is 3/16 again and every quotient is (a + b) / 2 exactly.
+    Group 1 spans 2^-11 .. 2^-8 of 448 sigma, where the quotient sits near the
+    subnormal and zero boundaries."""
+    rng = np.random.default_rng(11)
+    H, d = 64, 128
+    n_groups = 2
+    q = np.zeros((n_groups * g, H, d), dtype=np.uint8)
+    sc = np.float32(0.1875)
+    for j in range(n_groups):
+        lo = rng.integers(0, 0x7D, size=(H, d)) if j == 0 else rng.integers(0, 8, size=(H, d))
+        sign = (rng.integers(0, 2, size=(H, d)) * 0x80).astype(np.uint8)
+        a = (lo | sign).astype(np.uint8)
+        b = ((lo + 1) | sign).astype(np.uint8)
+        if j == 1:  # opposite signs cancel to zero
+            b[::7] = a[::7] ^ 0x80
+        for u in range(g):
+            q[j * g + u] = a if u % 2 == 0 else b
+            q[j * g + u, 0, 0] = 0x7E  # 448
+    q_scale = np.full(n_groups * g, sc, dtype=np.float32)
+    w = rng.standard_normal((n_groups * g, H)).astype(np.float32)
+    say("proxy ties", g)
+    pq, ps, pw = pv.pivot_proxy_rows(dev(q), dev(q_scale), dev(w), g)
+    pq, ps = host(pq), host(ps)
+    for j in range(n_groups):
+        oq, osc, _ = oracle.proxy("fp8", q[j * g:(j + 1) * g], q_scale[j * g:(j + 1) * g], w[j * g:(j + 1) * g])
+        assert osc == sc, osc
+        assert np.array_equal(pq[j], oq), (j, np.count_nonzero(pq[j] != oq))
+        assert ps[j] == np.float32(osc), j
+
+
 @pytest.mark.parametrize("fmt", ["fp8", "bf16"])
 @pytest.mark.parametrize("n_rows,lim0,step", [(1, 5000, 0), (2, 4999, 1), (3, 700, 7), (5, 33, 2),
                                               (16, 4100, 1), (40, 8300, 3), (64, 0, 130)])
