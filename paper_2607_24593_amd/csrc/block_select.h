@@ -238,37 +238,15 @@ __device__ __forceinline__ void emit_bucket(const Src& src, Bk bucket, int bsel,
   });
 }
 
-template <int THREADS, int NB = 4096, class Src, class Put>
-__device__ bool bucket_select(const Src& src, uint32_t need, uint32_t* hist, uint32_t* lkey, int32_t* lpos,
-                              int32_t* lcount, SelectShared& sh, Put put) {
+// bucket_select's last step: the in_b elements listed in LDS (lkey, lpos)
+// share the bucket holding the need-th element, and rem of them are still
+// wanted.  Each listed element's rank is the number of listed elements
+// ranking above it (key descending, position ascending); those with
+// rank < rem go out through put.  Ends with a workgroup barrier.
+template <int THREADS, class Put>
+__device__ __forceinline__ void rank_listed(uint32_t in_b, uint32_t rem, const uint32_t* lkey, const int32_t* lpos,
+                                            SelectShared& sh, Put put) {
   const int tid = threadIdx.x;
-  uint32_t kmin = ~0u, kmax = 0u;
-  src.visit([&](uint32_t key, int32_t) {
-    kmin = min(kmin, key);
-    kmax = max(kmax, key);
-  });
-  block_pair_reduce<THREADS, true>(kmin, kmax, sh);
-  static_assert(NB % THREADS == 0 || NB < THREADS, "bins per thread");
-  const float fmin = key_float(kmin);
-  const float scale = (float)NB / (key_float(kmax) - fmin);
-  if (kmin == kmax || !(scale > 0.0f && scale < __builtin_inff())) return false;
-  auto bucket = [&](uint32_t key) { return min(NB - 1, (int)((key_float(key) - fmin) * scale)); };
-  for (int k = tid; k < NB; k += THREADS) hist[k] = 0;
-  if (tid == 0) *lcount = 0;
-  __syncthreads();
-  src.visit([&](uint32_t key, int32_t) { atomicAdd(&hist[bucket(key)], 1u); });
-  __syncthreads();
-  find_digit<THREADS, true>(hist, sh, need, NB);
-  const int bsel = (int)sh.digit;
-  const uint32_t rem = need - sh.before, in_b = sh.equal;
-  __syncthreads();
-  if (in_b > (uint32_t)kBucketList) return false;
-  emit_bucket(src, bucket, bsel, sh, put, [&](uint32_t key, int32_t pos) {  // a few elements: a plain LDS atomic
-    const int c = atomicAdd(lcount, 1);
-    lkey[c] = key;
-    lpos[c] = pos;
-  });
-  __syncthreads();
   // rank of each listed member = members ranking above it; G threads share a
   // member (THREADS >= kBucketList >= in_b), each counting over a part of the
   // list with 8 loads issued before the compares, then summed across lanes
@@ -306,6 +284,40 @@ __device__ bool bucket_select(const Src& src, uint32_t need, uint32_t* hist, uin
     wave_append(mine && part == 0 && rank < rem, &sh.emitted, [&](int slot) { put(slot, pos); });
   }
   __syncthreads();
+}
+
+template <int THREADS, int NB = 4096, class Src, class Put>
+__device__ bool bucket_select(const Src& src, uint32_t need, uint32_t* hist, uint32_t* lkey, int32_t* lpos,
+                              int32_t* lcount, SelectShared& sh, Put put) {
+  const int tid = threadIdx.x;
+  uint32_t kmin = ~0u, kmax = 0u;
+  src.visit([&](uint32_t key, int32_t) {
+    kmin = min(kmin, key);
+    kmax = max(kmax, key);
+  });
+  block_pair_reduce<THREADS, true>(kmin, kmax, sh);
+  static_assert(NB % THREADS == 0 || NB < THREADS, "bins per thread");
+  const float fmin = key_float(kmin);
+  const float scale = (float)NB / (key_float(kmax) - fmin);
+  if (kmin == kmax || !(scale > 0.0f && scale < __builtin_inff())) return false;
+  auto bucket = [&](uint32_t key) { return min(NB - 1, (int)((key_float(key) - fmin) * scale)); };
+  for (int k = tid; k < NB; k += THREADS) hist[k] = 0;
+  if (tid == 0) *lcount = 0;
+  __syncthreads();
+  src.visit([&](uint32_t key, int32_t) { atomicAdd(&hist[bucket(key)], 1u); });
+  __syncthreads();
+  find_digit<THREADS, true>(hist, sh, need, NB);
+  const int bsel = (int)sh.digit;
+  const uint32_t rem = need - sh.before, in_b = sh.equal;
+  __syncthreads();
+  if (in_b > (uint32_t)kBucketList) return false;
+  emit_bucket(src, bucket, bsel, sh, put, [&](uint32_t key, int32_t pos) {  // a few elements: a plain LDS atomic
+    const int c = atomicAdd(lcount, 1);
+    lkey[c] = key;
+    lpos[c] = pos;
+  });
+  __syncthreads();
+  rank_listed<THREADS>(in_b, rem, lkey, lpos, sh, put);
   return true;
 }
 

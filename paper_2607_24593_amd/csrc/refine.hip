@@ -666,6 +666,226 @@ __global__ __launch_bounds__(T) __attribute__((amdgpu_waves_per_eu(V <= 16 ? 8 :
   }
 }
 
+// The member select of bf16 score rows of at most 4096 slots, 16 per thread
+// of 256: bucket_select's algorithm (the same NB value buckets over the
+// usable slots' range, so the same decisions), with the scores kept as bf16
+// pairs in registers (widened exactly on use) rather than as order keys.
+// The range, the histogram and the emission form no keys; only the boundary
+// bucket's few members get one.  Unusable slots (past the row, or excluded
+// by the window rule) are masked: their histogram count goes to a sink bin.
+// Each compare's bit mask gives the emission with one LDS atomic per wave.
+// Returns false, having emitted nothing, where bucket_select would (equal
+// values, a boundary bucket longer than kBucketList).  hist: NB + 1 LDS words.
+template <int V, int T, int NB>
+__device__ __forceinline__ bool member_select16(const uint32_t (&sc)[V / 2], const int32_t (&pv)[V], uint32_t vmask,
+                                                bool full, uint32_t m, uint32_t* hist, int32_t* lcount,
+                                                SelectShared& sh, int32_t* __restrict__ orow) {
+  static_assert(V <= 32 && V % 2 == 0 && NB % T == 0 && NB >= 2 * kBucketList, "mask word, bins, list");
+  const int tid = threadIdx.x, lane = tid & 63;
+  auto fv = [&](int v) { return __uint_as_float(v & 1 ? sc[v >> 1] & 0xFFFF0000u : sc[v >> 1] << 16); };
+  auto usable = [&](int v) { return ((vmask >> v) & 1u) != 0u; };
+  if (tid == 0) sh.emitted = 0;  // ordered before any append by the barriers below
+  float lo = __builtin_inff(), hi = -__builtin_inff();
+  if (full) {  // uniform
+#pragma unroll
+    for (int v = 0; v < V; ++v) {
+      lo = fminf(lo, fv(v));
+      hi = fmaxf(hi, fv(v));
+    }
+  } else {
+#pragma unroll
+    for (int v = 0; v < V; ++v) {
+      lo = fminf(lo, usable(v) ? fv(v) : __builtin_inff());
+      hi = fmaxf(hi, usable(v) ? fv(v) : -__builtin_inff());
+    }
+  }
+  uint32_t kmin = float_key(lo), kmax = float_key(hi);
+  block_pair_reduce<T, true>(kmin, kmax, sh);
+  const float fmin = key_float(kmin);
+  const float scale = (float)NB / (key_float(kmax) - fmin);
+  if (kmin == kmax || !(scale > 0.0f && scale < __builtin_inff())) return false;
+  auto bucket = [&](float f, float f0, float s) { return min(NB - 1, (int)((f - f0) * s)); };
+  for (int k = tid; k < NB; k += T) hist[k] = 0;
+  if (tid == 0) *lcount = 0;
+  __syncthreads();
+  if (full) {
+#pragma unroll
+    for (int v = 0; v < V; ++v) atomicAdd(&hist[bucket(fv(v), fmin, scale)], 1u);
+  } else {
+#pragma unroll
+    for (int v = 0; v < V; ++v) atomicAdd(&hist[usable(v) ? bucket(fv(v), fmin, scale) : NB], 1u);
+  }
+  __syncthreads();
+  find_digit<T, true>(hist, sh, m, NB);
+  const int bsel = (int)sh.digit;
+  const uint32_t rem = m - sh.before, in_b = sh.equal;
+  __syncthreads();  // the histogram's words become the boundary list
+  if (in_b > (uint32_t)kBucketList) return false;
+  uint32_t* lkey = hist;
+  int32_t* lpos = reinterpret_cast<int32_t*>(hist + kBucketList);
+  // The buckets are computed again rather than kept from the histogram pass
+  // (sixteen more live registers would cost occupancy); copies of fmin and
+  // scale that the compiler cannot see through keep it from reusing them.
+  const float fmin2 = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(fmin)));
+  const float scale2 = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(scale)));
+  uint32_t tb = 0, lb = 0;  // taken (bucket above bsel) and listed (bucket bsel) slots
+#pragma unroll
+  for (int v = 0; v < V; ++v) {
+    const int bk = bucket(fv(v), fmin2, scale2);
+    tb |= (bk > bsel ? 1u : 0u) << v;
+    lb |= (bk == bsel ? 1u : 0u) << v;
+  }
+  tb &= vmask;
+  lb &= vmask;
+  // one LDS atomic per wave for each of the two appends
+  const uint32_t nt = wave_incl_sum((uint32_t)__popc(tb)), nl = wave_incl_sum((uint32_t)__popc(lb));
+  const uint32_t tt = (uint32_t)__builtin_amdgcn_readlane((int)nt, 63);
+  const uint32_t lt = (uint32_t)__builtin_amdgcn_readlane((int)nl, 63);
+  int tbase = 0, lbase = 0;
+  if (lane == 0) {
+    if (tt) tbase = atomicAdd(&sh.emitted, (int)tt);
+    if (lt) lbase = atomicAdd(lcount, (int)lt);
+  }
+  tbase = __builtin_amdgcn_readfirstlane(tbase);
+  lbase = __builtin_amdgcn_readfirstlane(lbase);
+  const __amdgpu_buffer_rsrc_t orr = buffer_rsrc(orow, m * 4u);  // 32-bit offsets
+#pragma unroll
+  for (int v = 0; v < V; ++v) {
+    const bool t = (tb >> v) & 1u;
+    const uint64_t bal = __ballot(t);
+    if (t) {
+      const int slot = tbase + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
+                                                              __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
+      __builtin_amdgcn_raw_buffer_store_b32((uint32_t)pv[v], orr, 4 * slot, 0, 0);
+    }
+    tbase += (int)__popcll(bal);
+    const bool l = (lb >> v) & 1u;
+    const uint64_t lbal = __ballot(l);
+    if (lbal) {  // uniform over the wave, and rare
+      if (l) {
+        const int slot = lbase + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(lbal >> 32),
+                                                                __builtin_amdgcn_mbcnt_lo((uint32_t)lbal, 0u));
+        lkey[slot] = float_key(fv(v));
+        lpos[slot] = pv[v];
+      }
+      lbase += (int)__popcll(lbal);
+    }
+  }
+  __syncthreads();
+  rank_listed<T>(in_b, rem, lkey, lpos, sh, [&](int slot, int32_t p) { orow[slot] = p; });
+  return true;
+}
+
+// Member selects of bf16 score rows with |C| <= 4096 (the prefill Refine
+// shape): the workgroup mapping, slot rules and early exits of
+// topk_short_kernel, then member_select16, falling back to block_select.
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void topk_member16_kernel(
+    const uint16_t* __restrict__ rsc, const int32_t* __restrict__ cand, int g, SeqTable st, int j0, int nj, int c,
+    SlotRule rule, int m, int32_t* __restrict__ out_idx) {
+  constexpr int V = 16, T = 256, NB = 1024;
+  __shared__ SelectShared sel;
+  __shared__ uint32_t hist[NB + 1];  // the histogram (and a sink bin), then the boundary list
+  __shared__ int32_t lcount, nvalid_sh;
+  int jl, member;
+  member_of((int)blockIdx.x, g, nj, jl, member);
+  jl = __builtin_amdgcn_readfirstlane(jl);  // uniform: scalar registers
+  member = __builtin_amdgcn_readfirstlane(member);
+  const int j = j0 + jl, b = blockIdx.y;
+  if (b >= st.n || j >= seq_groups(st, b, g) || j < st.first_proxy[b]) return;
+  const int gs = min(g, st.n_rows[b] - j * g);
+  if (member >= gs) return;
+  const int tid = threadIdx.x;
+  const int64_t t0 = (int64_t)st.q_pos0[b] + (int64_t)j * g;
+  const int64_t tt = t0 + member;
+  const bool win = rule.window > 0;
+  const int nc = win ? c : (int)min((int64_t)c, t0 + 1);
+  const int64_t grp = (int64_t)st.grp0[b] + j;
+  const uint16_t* srow = uniform_ptr(rsc + (grp * g + member) * (int64_t)c);
+  const int32_t* crow = uniform_ptr(cand + grp * c);
+  int32_t* orow = uniform_ptr(out_idx + ((int64_t)st.row0[b] + (int64_t)j * g + member) * m);
+
+  // quads of scores (8 bytes) and positions (16 bytes) when the rows allow it
+  const bool vec = (c & 3) == 0 && (reinterpret_cast<uintptr_t>(srow) & 7u) == 0 &&
+                   (reinterpret_cast<uintptr_t>(crow) & 15u) == 0;
+  uint32_t sc[V / 2];  // bf16 scores, two per word (the even slot in the low half)
+  int32_t pv[V];       // -1: not usable by this member
+  uint32_t vmask = 0;
+#pragma unroll
+  for (int q4 = 0; q4 < V / 4; ++q4) {
+    const int e0 = 4 * (tid + T * q4);
+    uint32_t s01 = 0, s23 = 0;
+    int32_t p4[4] = {-1, -1, -1, -1};
+    if (vec) {
+      if (e0 < nc) {  // c is a multiple of 4: the quad lies inside the row
+        const uint2 a = *reinterpret_cast<const uint2*>(srow + e0);
+        s01 = a.x;
+        s23 = a.y;
+        const int4 q = *reinterpret_cast<const int4*>(crow + e0);
+        p4[0] = q.x;
+        p4[1] = q.y;
+        p4[2] = q.z;
+        p4[3] = q.w;
+      }
+    } else {
+      uint32_t h[4] = {0, 0, 0, 0};
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (e0 + u < nc) {
+          h[u] = srow[e0 + u];
+          p4[u] = crow[e0 + u];
+        }
+      s01 = h[0] | (h[1] << 16);
+      s23 = h[2] | (h[3] << 16);
+    }
+    sc[2 * q4] = s01;
+    sc[2 * q4 + 1] = s23;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int e = e0 + u;
+      const int32_t p = p4[u];
+      bool ok = e < nc;
+      if (win) ok = ok && p >= 0 && p <= tt && !(e >= rule.wslot && p < tt - rule.window + 1);
+      pv[4 * q4 + u] = ok ? p : -1;
+      vmask |= (ok ? 1u : 0u) << (4 * q4 + u);
+    }
+  }
+  if (!win) {
+    if (nc <= m) {  // every candidate is selected
+      for (int p = tid; p < m; p += T) orow[p] = p < nc ? crow[p] : -1;
+      return;
+    }
+  } else {
+    if (tid == 0) {
+      nvalid_sh = 0;
+      sel.emitted = 0;
+    }
+    __syncthreads();
+    atomicAdd(&nvalid_sh, __popc(vmask));
+    __syncthreads();
+    const int nvalid = nvalid_sh;
+    if (nvalid <= m) {  // every usable slot is selected, then -1 padding
+#pragma unroll
+      for (int v = 0; v < V; ++v)
+        wave_append(pv[v] >= 0, &sel.emitted, [&](int slot) { orow[slot] = pv[v]; });
+      for (int p = nvalid + tid; p < m; p += T) orow[p] = -1;
+      return;
+    }
+    __syncthreads();  // sel.emitted is cleared again below
+  }
+  const bool full = !win && nc == V * T;
+  if (member_select16<V, T, NB>(sc, pv, vmask, full, (uint32_t)m, hist, &lcount, sel, orow)) return;
+  RegSource<V> src;
+#pragma unroll
+  for (int v = 0; v < V; ++v) {
+    src.key[v] = float_key(__uint_as_float(v & 1 ? sc[v >> 1] & 0xFFFF0000u : sc[v >> 1] << 16));
+    src.pos[v] = pv[v];
+  }
+  __syncthreads();
+  if (tid == 0) sel.emitted = 0;
+  __syncthreads();
+  block_select<T, true>(src, (uint32_t)m, sel, [&](int slot, int32_t p) { orow[slot] = p; });
+}
+
 // App. B window union: slot0 + u (u < wg) of every candidate row of the
 // groups [j0, j1) with j >= first_proxy[b] takes position t0 - W + 1 + u, or
 // -1 below 0, past the group's last member, or (dedupe) when it is already
@@ -725,6 +945,9 @@ hipError_t launch_short(const E* rescore, const int32_t* cand, int g, const SeqT
     PIVOT_SHORT(4, 1024);
   else if (few)
     PIVOT_SHORT(8, 1024);
+  else if (c <= 4096 && sizeof(E) == 2)
+    hipLaunchKernelGGL(topk_member16_kernel, sgrid, dim3(256), 0, stream, reinterpret_cast<const uint16_t*>(rescore),
+                       cand, g, st, j0, nj, c, rule, m, out_idx);
   else if (c <= 4096)
     PIVOT_SHORT(16, 256);
   else if (c <= 5120)  // c = 4096 plus a window union
