@@ -776,13 +776,16 @@ __device__ __forceinline__ bool member_select16(const uint32_t (&sc)[V / 2], con
   return true;
 }
 
-// Member selects of bf16 score rows with |C| <= 4096 (the prefill Refine
-// shape): the workgroup mapping, slot rules and early exits of
-// topk_short_kernel, then member_select16, falling back to block_select.
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void topk_member16_kernel(
+// Member selects of bf16 score rows with |C| <= V x T (4096: the prefill
+// Refine shape, 16 per thread of 256; MTP decode, 4 per thread of 1024): the
+// workgroup mapping, slot rules and early exits of topk_short_kernel, then
+// member_select16, falling back to block_select.
+template <int V, int T>
+__global__ __launch_bounds__(T) __attribute__((amdgpu_waves_per_eu(8))) void topk_member16_kernel(
     const uint16_t* __restrict__ rsc, const int32_t* __restrict__ cand, int g, SeqTable st, int j0, int nj, int c,
     SlotRule rule, int m, int32_t* __restrict__ out_idx) {
-  constexpr int V = 16, T = 256, NB = 1024;
+  constexpr int NB = 1024;
+  static_assert(V % 4 == 0, "quads of slots");
   __shared__ SelectShared sel;
   __shared__ uint32_t hist[NB + 1];  // the histogram (and a sink bin), then the boundary list
   __shared__ int32_t lcount, nvalid_sh;
@@ -941,13 +944,16 @@ hipError_t launch_short(const E* rescore, const int32_t* cand, int g, const SeqT
                      m, out_idx)
   if (c <= 1024)
     PIVOT_SHORT(4, 256);
+  else if (few && c <= 4096 && sizeof(E) == 2)
+    hipLaunchKernelGGL((topk_member16_kernel<4, 1024>), sgrid, dim3(1024), 0, stream,
+                       reinterpret_cast<const uint16_t*>(rescore), cand, g, st, j0, nj, c, rule, m, out_idx);
   else if (few && c <= 4096)
     PIVOT_SHORT(4, 1024);
   else if (few)
     PIVOT_SHORT(8, 1024);
   else if (c <= 4096 && sizeof(E) == 2)
-    hipLaunchKernelGGL(topk_member16_kernel, sgrid, dim3(256), 0, stream, reinterpret_cast<const uint16_t*>(rescore),
-                       cand, g, st, j0, nj, c, rule, m, out_idx);
+    hipLaunchKernelGGL((topk_member16_kernel<16, 256>), sgrid, dim3(256), 0, stream,
+                       reinterpret_cast<const uint16_t*>(rescore), cand, g, st, j0, nj, c, rule, m, out_idx);
   else if (c <= 4096)
     PIVOT_SHORT(16, 256);
   else if (c <= 5120)  // c = 4096 plus a window union
