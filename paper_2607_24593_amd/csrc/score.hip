@@ -35,10 +35,14 @@ namespace pivot {
 // loads read zeros, and adding a fragment's lane offset cannot wrap it.
 constexpr uint32_t kDropOffset = 0x80000000u;
 
-// Rows mode stages keys through LDS 4 KiB at a time: 32 fp8 or 16 bf16 keys,
-// each row padded by 16 bytes.
+// Rows mode stages keys through LDS 8 KiB at a time: 64 fp8 or 32 bf16 keys,
+// each row padded by 16 bytes; a thread fetches two 16-byte pieces per stage.
 template <int DT>
-constexpr int kStageKeys = DT == kFp8 ? 32 : 16;
+constexpr int kStageKeys = DT == kFp8 ? 64 : 32;
+template <int DT>
+constexpr int kPassKeys = 256 * 16 / (kD * (DT == kFp8 ? 1 : 2));  // keys of one 16-byte piece per thread
+template <int DT>
+constexpr int kPieces = kStageKeys<DT> / kPassKeys<DT>;
 template <int DT>
 constexpr int kStageSlot = kStageKeys<DT> * (kD * (DT == kFp8 ? 1 : 2) + 16);
 
@@ -59,7 +63,7 @@ __global__ __launch_bounds__(256) void score_kernel(const uint8_t* __restrict__ 
   constexpr int KB = kD * EB;  // bytes per key
   constexpr int RB = KSPLIT ? R : 4 * R;
   // the segment's key scales (fp8); a key index never reaches 4096 (rows
-  // mode: at most 127 stages of 32 keys; keys mode: 2048-key segments plus
+  // mode: at most 64 stages of 64 keys; keys mode: 2048-key segments plus
   // two fragment strides), and 32 spare words keep a stray read inside
   __shared__ float sks[4096 + 32];
   __shared__ __align__(16) uint8_t kst[KSPLIT ? 16 : 3 * kStageSlot<DT>];  // rows mode: staged keys
@@ -210,49 +214,64 @@ __global__ __launch_bounds__(256) void score_kernel(const uint8_t* __restrict__ 
     }
   } else {
     // rows mode: the 4 waves score the same keys, so the workgroup fetches
-    // each 4 KiB stage of keys once (every thread one 16-byte piece, the
+    // each 8 KiB stage of keys once (every thread two 16-byte pieces, the
     // stage one contiguous block) and the waves read their fragments from
     // LDS.  Three LDS slots rotate with one barrier per stage: stage i + 1 is
     // written while stage i is scored, and the slot it overwrites held stage
     // i - 2, which every wave finished before the previous barrier.  Each
-    // thread keeps three stages' loads in flight (registers r0..r2 hold
-    // stages 3 n, 3 n + 1, 3 n + 2).  Key rows sit KB + 16 bytes apart in LDS,
-    // so the 16 rows of a fragment start in 16 different 16-byte bank
-    // groups.  Every wave runs every stage of the workgroup's key range (the
-    // barriers are uniform).
+    // thread has the next stage's loads in flight while a stage is scored
+    // (one register set: more would cost the tile's occupancy of two waves
+    // per SIMD).  Key rows sit KB + 16 bytes apart in LDS, so
+    // the 16 rows of a fragment start in 16 different 16-byte bank groups.
+    // Every wave runs every stage of the workgroup's key range (the barriers
+    // are uniform).
     const int nst = (nseg_keys + kStageKeys<DT> - 1) / kStageKeys<DT>;
     const int my_key = tid / (KB / 16), my_piece = tid % (KB / 16);
     uint8_t* const put_at = kst + my_key * (KB + 16) + 16 * my_piece;
+    struct Pieces {
+      v4i p[kPieces<DT>];
+    };
     // prologue fetches (before the first barrier) read the page table in
     // global memory, later ones the copy staged in LDS
-    auto fetch = [&](int st_i, bool prologue = false) -> v4i {
-      const int e = st_i * kStageKeys<DT> + my_key;
-      uint32_t off;
-      if constexpr (PAGED) {
-        if (e >= nseg_keys) {
-          off = kDropOffset;
-        } else if (prologue) {
-          off = (uint32_t)(km.row(b, seg0 + e) * KB);
+    auto fetch = [&](int st_i, bool prologue = false) -> Pieces {
+      Pieces r;
+#pragma unroll
+      for (int h = 0; h < kPieces<DT>; ++h) {
+        const int e = st_i * kStageKeys<DT> + h * kPassKeys<DT> + my_key;
+        uint32_t off;
+        if constexpr (PAGED) {
+          if (e >= nseg_keys) {
+            off = kDropOffset;
+          } else if (prologue) {
+            off = (uint32_t)(km.row(b, seg0 + e) * KB);
+          } else {
+            const int64_t s = seg0 + e;
+            off = (uint32_t)((((int64_t)spg[(s >> km.shift) - page0] << km.shift) | (s & ((1 << km.shift) - 1))) * KB);
+          }
         } else {
-          const int64_t s = seg0 + e;
-          off = (uint32_t)((((int64_t)spg[(s >> km.shift) - page0] << km.shift) | (s & ((1 << km.shift) - 1))) * KB);
+          off = (uint32_t)e * KB;  // past the segment: zeros (range-checked resource)
         }
-      } else {
-        off = (uint32_t)e * KB;  // past the segment: zeros (range-checked resource)
+        r.p[h] = __builtin_amdgcn_raw_buffer_load_b128(kr, off + 16 * my_piece, 0, 0);
       }
-      return __builtin_amdgcn_raw_buffer_load_b128(kr, off + 16 * my_piece, 0, 0);
+      return r;
     };
-    v4i r0 = fetch(0, true), r1 = fetch(1, true), r2 = fetch(2, true);
+    auto put = [&](const Pieces& r, int slot) {
+#pragma unroll
+      for (int h = 0; h < kPieces<DT>; ++h)
+        *reinterpret_cast<v4i*>(put_at + slot * kStageSlot<DT> + h * kPassKeys<DT> * (KB + 16)) = r.p[h];
+    };
+    Pieces r = fetch(0, true);
     if constexpr (DT == kFp8) {
 #pragma unroll
       for (int u = 0; u < KS_PER; ++u) sks[tid + 256 * u] = ksv[u];  // zeros past the segment
     }
-    *reinterpret_cast<v4i*>(put_at) = r0;
-    r0 = fetch(3, true);
+    put(r, 0);
+    r = fetch(1, true);
     __syncthreads();
-    auto stage = [&](int i, v4i& r, int slot_put, int slot) {
-      *reinterpret_cast<v4i*>(put_at + slot_put * kStageSlot<DT>) = r;  // stage i + 1
-      r = fetch(i + 4);
+    // r holds stage i + 1 on entry; stage s sits in slot s % 3
+    auto stage = [&](int i, int slot_put, int slot) {
+      put(r, slot_put);  // stage i + 1
+      r = fetch(i + 2);
       __syncthreads();
       const int t = i * kStageKeys<DT>;
 #pragma unroll
@@ -269,12 +288,12 @@ __global__ __launch_bounds__(256) void score_kernel(const uint8_t* __restrict__ 
     // own load.
     int i = 0;
     for (; i + 3 <= nst; i += 3) {
-      stage(i, r1, 1, 0);
-      stage(i + 1, r2, 2, 1);
-      stage(i + 2, r0, 0, 2);
+      stage(i, 1, 0);
+      stage(i + 1, 2, 1);
+      stage(i + 2, 0, 2);
     }
-    if (i < nst) stage(i, r1, 1, 0);
-    if (i + 1 < nst) stage(i + 1, r2, 2, 1);
+    if (i < nst) stage(i, 1, 0);
+    if (i + 1 < nst) stage(i + 1, 2, 1);
   }
 }
 
