@@ -132,6 +132,31 @@ class Prefill:
                                      g=g, c=wl.c, out=self.out[sl], ws=self.ws)
 
 
+def run_two_streams(pf, mode, g):
+    """One pass with the chunk calls alternating over two streams, each with
+    its own workspace: the chunks are independent calls (disjoint queries and
+    outputs, read-only keys), so one call's kernels fill the GPU while the
+    other's launch ramps or drains.  Every stream keeps the default priority."""
+    import torch
+    pv, wl = pf.pv, pf.wl
+    if not hasattr(pf, "second"):  # freed with pf
+        pf.second = (torch.cuda.Stream(), torch.empty_like(pf.ws))
+    s1, (s2, ws2) = torch.cuda.current_stream(), pf.second
+    s2.wait_stream(s1)
+    for i, (p0, n) in enumerate(pf.chunks):
+        s, ws = (s1, pf.ws) if i % 2 == 0 else (s2, ws2)
+        sl = slice(p0, p0 + n)
+        args = (pf.q[sl], None if pf.qs is None else pf.qs[sl], pf.w[sl], pf.k[:p0 + n],
+                None if pf.ks is None else pf.ks[:p0 + n], p0, p0 + n, wl.topk)
+        with torch.cuda.stream(s):
+            if mode == "dense":
+                pv.pivot_dense_index(*args, out=pf.out[sl], ws=ws, stream=s)
+            else:
+                pv.pivot_group_index(*args, mode=pv.PIVOT_REUSE if mode == "reuse" else pv.PIVOT_REFINE, g=g,
+                                     c=wl.c, out=pf.out[sl], ws=ws, stream=s)
+    s1.wait_stream(s2)
+
+
 class no_gc:
     """Python's cyclic collector paused around a timed loop: a full collection
     over the interpreter's heap (torch, the workload's arrays) takes tens of ms
@@ -646,6 +671,14 @@ def main():
                                     "speedup_vs_dense": dense_s / s}
         log(f"refine g={g} W=4: {s * 1e3:.2f} ms ({dense_s / s:.2f}x)")
 
+    two = None
+    if not args.no_compare:  # independent chunk calls overlapped on two streams
+        run_two_streams(pf, "refine", g)
+        r2 = timed(lambda: run_two_streams(pf, "refine", g), args.reps)
+        d2 = timed(lambda: run_two_streams(pf, "dense", g), args.reps)
+        two = {"refine_ms_per_pass": r2 * 1e3, "queries_per_s": wl.L / r2, "dense_ms_per_pass": d2 * 1e3,
+               "speedup_vs_dense": d2 / r2, "vs_one_stream": step_s / r2}
+        log(f"two streams: refine {r2 * 1e3:.2f} ms, dense {d2 * 1e3:.2f} ms ({step_s / r2:.3f}x one stream)")
     ic = None if args.no_indexcache else indexcache_bench(pf, g, reps=args.reps)
     bf16 = None if args.no_compare else bf16_score_bench(reps=args.reps)
     if bf16 is not None:
@@ -692,6 +725,7 @@ def main():
         "kernels_note": f"score: HIP events of the {args.steps} timed steps; other kernels: a separate pass of "
                         f"{KB} steps with events around every launch",
         "modes": modes,
+        "two_streams": two,
         "decode": dec,
         "layouts": layouts,
         "indexcache": ic,
