@@ -252,3 +252,19 @@ def test_large_candidate_budget(long20k_fp8, c):
     rng = np.random.default_rng(c)
     groups = sorted({0, n_q // g - 1} | set(int(v) for v in rng.integers(0, n_q // g, 8)))
     check(x, "refine", p0, n_q, 2048, g=g, c=c, groups=groups, label=f"20k refine c{c}")
+
+
+@pytest.mark.parametrize("mode", ["dense", "reuse", "refine"])
+def test_outlier_keys_span_the_score_range(mode):
+    """Two keys with scales 2^40: a row that sees one scores it about 2^40
+    times the others, of either sign, so its scores span ~40 binades and the
+    value buckets of a select crowd nearly every other score into one bucket.
+    The exact fallbacks then decide: in every dense and proxy row, and in the
+    member rows whose candidates hold an outlier.  Checked against the oracle."""
+    x = make_prefill(6000, "fp8", seed=57, threads=8)
+    x.k_scale = x.k_scale.copy()
+    x.k_scale[[123, 2345]] = np.float32(2.0 ** 40)
+    p0, n_q, c, topk = 1500, 4500, 1024, 256
+    g = 1 if mode == "dense" else 4
+    groups = sorted({0, 1, n_q // g - 1} | set(int(v) for v in np.random.default_rng(9).integers(0, n_q // g, 8)))
+    check(x, mode, p0, n_q, topk, g=g, c=0 if mode == "dense" else c, groups=groups, label=f"outlier keys {mode}")
