@@ -268,3 +268,17 @@ def test_outlier_keys_span_the_score_range(mode):
     g = 1 if mode == "dense" else 4
     groups = sorted({0, 1, n_q // g - 1} | set(int(v) for v in np.random.default_rng(9).integers(0, n_q // g, 8)))
     check(x, mode, p0, n_q, topk, g=g, c=0 if mode == "dense" else c, groups=groups, label=f"outlier keys {mode}")
+
+
+@pytest.mark.parametrize("mode,g,topk,c", [
+    ("refine", 16, 64, 512),   # proxies of two member batches; four 4-row re-score blocks per group
+    ("reuse", 16, 64, 512),
+    ("refine", 4, 1, 16),      # top-1 of 16 candidates
+    ("refine", 5, 7, 8),       # c barely above k, groups of five (a 4-row and a 1-row block)
+])
+def test_group_and_selection_extremes(long_fp8, mode, g, topk, c):
+    """Large groups (16 members), top-1, and c one above k, on sampled groups
+    of a later fp8 chunk."""
+    p0, n_q = 4000, 3000
+    groups = _sample_groups(n_q, g, p0, c, np.random.default_rng(g * 100 + topk))
+    check(long_fp8, mode, p0, n_q, topk, g=g, c=c, groups=groups, label=f"{mode} g{g} k{topk} c{c}")
